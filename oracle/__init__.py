@@ -1,0 +1,242 @@
+"""CPU oracle of the canonical-order training step (CANON-v1).
+
+TEST INFRASTRUCTURE.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The product path
+(the GPU library and its binding) never imports it, and it never imports the
+product path; the only shared code is the seeded input generator.
+
+Thin ctypes binding over ``liboracle.so`` (plain C, ``canon_ref.c``).  Arrays
+are numpy; bf16 tensors are uint16 bit patterns.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "canon_ref.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+CFLAGS = ["-O2", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-fno-fast-math", "-march=x86-64-v3",
+          "-std=c11", "-D_GNU_SOURCE"]
+
+
+def build() -> str:
+    subprocess.run(["gcc", *CFLAGS, "-o", _LIB, _SRC, "-lm"], check=True)
+    return _LIB
+
+
+class ModelCfg(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("accum", ctypes.c_int32), ("dp_shard", ctypes.c_int32), ("dp_replicate", ctypes.c_int32)]
+
+
+class AdamWConsts(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in ("lr", "beta1", "one_minus_beta1", "beta2", "one_minus_beta2",
+                                              "inv_bc1", "inv_bc2", "eps", "decay_factor")]
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            raise RuntimeError(f"{_LIB} is not built; run __graft_entry__.build() first")
+        lib = ctypes.CDLL(_LIB)
+        f, i32, i64, vp = ctypes.c_float, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+        sig = {
+            "cref_add": (f, [f, f]), "cref_sub": (f, [f, f]), "cref_mul": (f, [f, f]),
+            "cref_fma": (f, [f, f, f]), "cref_div": (f, [f, f]), "cref_sqrt": (f, [f]),
+            "cref_exp": (f, [f]), "cref_log": (f, [f]), "cref_sigmoid": (f, [f]), "cref_silu": (f, [f]),
+            "cref_bf16": (ctypes.c_uint16, [f]),
+            "cref_prim": (ctypes.c_int, [i32, i64, vp, vp, vp, vp]),
+            "cref_rsum": (f, [vp, i64, i64, i32]),
+            "cref_rdot_bf16": (f, [vp, i64, vp, i64, i64, i32]),
+            "cref_rdot_f32": (f, [vp, i64, vp, i64, i64, i32]),
+            "cref_treefold": (ctypes.c_int, [vp, i64, i64, vp, vp]),
+            "cref_gemm": (ctypes.c_int, [i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64]),
+            "cref_rownorm_fwd": (ctypes.c_int, [i64, i64, vp, vp, f, vp, vp]),
+            "cref_rownorm_bwd": (ctypes.c_int, [i64, i64, vp, vp, vp, vp, vp, vp]),
+            "cref_softmax_causal": (ctypes.c_int, [i64, i64, vp, f, vp]),
+            "cref_xent": (ctypes.c_int, [i64, i64, vp, vp, f, vp, vp, vp]),
+            "cref_grad_accum": (ctypes.c_int, [vp, i64, vp, vp]),
+            "cref_adamw": (ctypes.c_int, [i64, vp, vp, vp, vp, vp, vp, vp]),
+            "cref_block_fwd_bwd": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "cref_step": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "cref_num_threads": (ctypes.c_int, []),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = lib
+    return _lib
+
+
+def lib():
+    return _load()
+
+
+def _p(a: np.ndarray) -> int:
+    assert a.flags.c_contiguous, "oracle arrays must be C-contiguous"
+    return a.ctypes.data
+
+
+def _ptr_array(arrs):
+    return (ctypes.c_void_p * len(arrs))(*[_p(a) for a in arrs])
+
+
+def _check(rc):
+    if rc != 0:
+        raise ValueError(f"oracle call failed with status {rc}")
+
+
+PRIM_OPS = {"add": 0, "sub": 1, "mul": 2, "fma": 3, "div": 4, "sqrt": 5, "exp": 6, "log": 7, "sigmoid": 8,
+            "silu": 9, "bf16": 10}
+
+
+def prim(op: str, a, b=None, c=None) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    b = np.ascontiguousarray(a if b is None else b, dtype=np.float32)
+    c = np.ascontiguousarray(a if c is None else c, dtype=np.float32)
+    out = np.empty_like(a)
+    _check(_load().cref_prim(PRIM_OPS[op], a.size, _p(a), _p(b), _p(c), _p(out)))
+    return out
+
+
+def rsum(t, chunk: int = 32) -> np.float32:
+    t = np.ascontiguousarray(t, dtype=np.float32)
+    return np.float32(_load().cref_rsum(_p(t), t.size, 1, chunk))
+
+
+def rdot_bf16(a, b, chunk: int = 32) -> np.float32:
+    a = np.ascontiguousarray(a, dtype=np.uint16)
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    return np.float32(_load().cref_rdot_bf16(_p(a), 1, _p(b), 1, a.size, chunk))
+
+
+def rdot_f32(a, b, chunk: int = 32) -> np.float32:
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    b = np.ascontiguousarray(b, dtype=np.float32)
+    return np.float32(_load().cref_rdot_f32(_p(a), 1, _p(b), 1, a.size, chunk))
+
+
+def treefold(parts: np.ndarray):
+    parts = np.ascontiguousarray(parts, dtype=np.float32)
+    nparts = parts.shape[0]
+    length = int(np.prod(parts.shape[1:])) if parts.ndim > 1 else 1
+    out = np.empty(parts.shape[1:] if parts.ndim > 1 else (1,), dtype=np.float32)
+    deepest = ctypes.c_int32(0)
+    _check(_load().cref_treefold(_p(parts), nparts, length, _p(out), ctypes.addressof(deepest)))
+    return out, deepest.value
+
+
+def gemm(a: np.ndarray, b: np.ndarray, trans_a: bool = False, trans_b: bool = False) -> np.ndarray:
+    """C = op(A) op(B); a, b uint16 bf16 bit patterns stored row-major; returns fp32 [m, n]."""
+    a = np.ascontiguousarray(a, dtype=np.uint16)
+    b = np.ascontiguousarray(b, dtype=np.uint16)
+    m, k = (a.shape[1], a.shape[0]) if trans_a else a.shape
+    kb, n = (b.shape[1], b.shape[0]) if trans_b else b.shape
+    assert k == kb
+    c = np.empty((m, n), dtype=np.float32)
+    _check(_load().cref_gemm(int(trans_a), int(trans_b), m, n, k, _p(a), a.shape[1], _p(b), b.shape[1], _p(c), n))
+    return c
+
+
+def rownorm_fwd(x: np.ndarray, gain: np.ndarray, eps: float):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    gain = np.ascontiguousarray(gain, dtype=np.uint16)
+    rows, cols = x.shape
+    y = np.empty((rows, cols), dtype=np.uint16)
+    rstd = np.empty(rows, dtype=np.float32)
+    _check(_load().cref_rownorm_fwd(rows, cols, _p(x), _p(gain), eps, _p(y), _p(rstd)))
+    return y, rstd
+
+
+def rownorm_bwd(x, gain, rstd, dy):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    gain = np.ascontiguousarray(gain, dtype=np.uint16)
+    rstd = np.ascontiguousarray(rstd, dtype=np.float32)
+    dy = np.ascontiguousarray(dy, dtype=np.float32)
+    rows, cols = x.shape
+    dx = np.empty((rows, cols), dtype=np.float32)
+    dgain = np.empty(cols, dtype=np.float32)
+    _check(_load().cref_rownorm_bwd(rows, cols, _p(x), _p(gain), _p(rstd), _p(dy), _p(dx), _p(dgain)))
+    return dx, dgain
+
+
+def softmax_causal(raw: np.ndarray, scale: float) -> np.ndarray:
+    raw = np.ascontiguousarray(raw, dtype=np.float32)
+    batch, s, s2 = raw.shape
+    assert s == s2
+    p = np.empty((batch, s, s), dtype=np.uint16)
+    _check(_load().cref_softmax_causal(batch, s, _p(raw), scale, _p(p)))
+    return p
+
+
+def xent(logits: np.ndarray, targets: np.ndarray, inv_tokens: float):
+    logits = np.ascontiguousarray(logits, dtype=np.uint16)
+    targets = np.ascontiguousarray(targets, dtype=np.int32)
+    rows, vocab = logits.shape
+    dl = np.empty((rows, vocab), dtype=np.uint16)
+    rl = np.empty(rows, dtype=np.float32)
+    ml = ctypes.c_float(0)
+    _check(_load().cref_xent(rows, vocab, _p(logits), _p(targets), inv_tokens, _p(dl), _p(rl),
+                             ctypes.addressof(ml)))
+    return dl, rl, np.float32(ml.value)
+
+
+def grad_accum(grads, accum: int, dp_shard: int, dp_replicate: int) -> np.ndarray:
+    grads = [np.ascontiguousarray(g, dtype=np.float32) for g in grads]
+    assert len(grads) == accum * dp_shard * dp_replicate
+    n = grads[0].size
+    out = np.empty(n, dtype=np.float32)
+    plan = Plan(accum, dp_shard, dp_replicate)
+    _check(_load().cref_grad_accum(ctypes.addressof(plan), n, _ptr_array(grads), _p(out)))
+    return out.reshape(grads[0].shape)
+
+
+def adamw(params, m, v, grads, decay_mask, consts: AdamWConsts):
+    """Updates params (uint16), m, v (float32) in place."""
+    sizes = np.array([p.size for p in params], dtype=np.int64)
+    mask = np.ascontiguousarray(np.asarray(decay_mask, dtype=np.uint8))
+    _check(_load().cref_adamw(len(params), _p(sizes), _ptr_array(params), _ptr_array(m), _ptr_array(v),
+                              _ptr_array(grads), _p(mask), ctypes.addressof(consts)))
+
+
+def block_fwd_bwd(cfg: ModelCfg, batch: int, x, dy, w, rope_cos, rope_sin):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    dy = np.ascontiguousarray(dy, dtype=np.float32)
+    w = [np.ascontiguousarray(t, dtype=np.uint16) for t in w]
+    y = np.empty_like(x)
+    dx = np.empty_like(x)
+    dw = [np.empty(t.shape, dtype=np.float32) for t in w]
+    _check(_load().cref_block_fwd_bwd(ctypes.addressof(cfg), batch, _p(x), _p(dy), _ptr_array(w),
+                                      _p(np.ascontiguousarray(rope_cos, dtype=np.float32)),
+                                      _p(np.ascontiguousarray(rope_sin, dtype=np.float32)),
+                                      _p(y), _p(dx), _ptr_array(dw)))
+    return y, dx, dw
+
+
+def step(cfg: ModelCfg, plan: Plan, params, m, v, windows, rope_cos, rope_sin, consts: AdamWConsts,
+         want_grads: bool = False):
+    """Runs one step; updates params, m, v in place; returns (loss, grads or None)."""
+    loss = ctypes.c_float(0)
+    grads = [np.empty(p.shape, dtype=np.float32) for p in params] if want_grads else None
+    windows = np.ascontiguousarray(windows, dtype=np.int32)
+    _check(_load().cref_step(ctypes.addressof(cfg), ctypes.addressof(plan), _ptr_array(params), _ptr_array(m),
+                             _ptr_array(v), _p(windows), _p(np.ascontiguousarray(rope_cos, dtype=np.float32)),
+                             _p(np.ascontiguousarray(rope_sin, dtype=np.float32)), ctypes.addressof(consts),
+                             ctypes.addressof(loss), _ptr_array(grads) if grads is not None else None))
+    return np.float32(loss.value), grads
+
+
+def num_threads() -> int:
+    return int(_load().cref_num_threads())

@@ -1,0 +1,1016 @@
+/*
+ * canon_ref.c - CPU oracle of the canonical-order training step (CANON-v1).
+ *
+ * TEST INFRASTRUCTURE.  This library exists to check the GPU library; only the
+ * tests, the smoke check and the CPU-baseline leg of the benchmark load it.  It
+ * shares no source with the GPU path.
+ *
+ * Every floating-point operation below is spelled out.  Each one follows rule R0
+ * (IEEE-754 binary32, round to nearest even; subnormal inputs read as zero of the
+ * same sign; a result whose rounding to 24 significant bits with unbounded
+ * exponent is below 2^-126 in magnitude becomes zero of the same sign).  This is
+ * the paper's choice to flush subnormals everywhere (Section "Reproducible
+ * Operations", paragraph on subnormals, and its Table of techniques), with the
+ * tininess test that gfx950 applies in flush mode.
+ *
+ * Reductions follow rule R1: the terms of a sum, in the order of their logical
+ * index, are cut into chunks of 32; each chunk is a left-to-right chain started
+ * at +0 (fused multiply-add for bf16 x bf16 products, separate multiply and add
+ * otherwise, the paper's fixed-order and single-convention rules); the chunk
+ * partials are combined by the binary-carry fold of the paper's Algorithm 2
+ * (TreeFold), pushed in ascending chunk order.
+ *
+ * Compiled with -ffp-contract=off and without fast-math, so the compiler neither
+ * fuses nor reorders any of these operations.
+ */
+#include "canon_ref.h"
+
+#include <math.h>
+#include <omp.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define CHUNK 32
+#define TINY 0x1p-126f
+
+/* ======================================================================== */
+/* R0: primitives                                                            */
+/* ======================================================================== */
+
+static inline float f_from_bits(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+static inline uint32_t f_bits(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+
+/* Subnormal input read as zero of the same sign. */
+static inline float daz(float x) { return (x != 0.0f && fabsf(x) < TINY) ? copysignf(0.0f, x) : x; }
+
+/* Round an exactly known real value x (held exactly in a double) to binary32 under R0. */
+static float round_exact_double(double x) {
+  if (x == 0.0 || isinf(x) || isnan(x)) return (float)x;
+  double ax = fabs(x);
+  if (ax < 0x1p-127) return x < 0 ? -0.0f : 0.0f;
+  /* 24-bit rounding with unbounded exponent, moved into the normal float range by an exact scaling */
+  float scaled = (float)(ax * 0x1p64);
+  if (scaled < 0x1p-62f) return x < 0 ? -0.0f : 0.0f;
+  /* not tiny: the ordinary rounding gives the same value */
+  return (float)x;
+}
+
+/* Round the exact value s + e (a double-double with |e| <= ulp(s)/2, s = RN53(s+e)) under R0. */
+static float round_double_double(double s, double e) {
+  double as = fabs(s);
+  if (as < 0x1p-140) return s < 0 ? -0.0f : 0.0f;       /* far below the normal range */
+  double sc = (as < 0x1p-100) ? 0x1p150 : 1.0;          /* exact scaling into the float normal range */
+  double S = s * sc, E = e * sc;
+  float r = (float)S;                                   /* ties-to-even on S alone */
+  double rd = (double)r;
+  if (!isinf(r) && rd != S) {
+    float lo, hi;
+    if (rd < S) { lo = r; hi = nextafterf(r, INFINITY); }
+    else { hi = r; lo = nextafterf(r, -INFINITY); }
+    double mid = ((double)lo + (double)hi) * 0.5;       /* exact */
+    if (S == mid) {                                     /* the tail e decides a tie on S */
+      if (E > 0) r = hi;
+      else if (E < 0) r = lo;
+    }
+  }
+  if (isinf(r)) return r;
+  double ar = fabs((double)r) / sc;
+  if (ar < 0x1p-126) return s < 0 ? -0.0f : 0.0f;
+  return (float)((double)r / sc);
+}
+
+float cref_add(float a, float b) {
+  a = daz(a);
+  b = daz(b);
+  /* both operands are multiples of 2^-149, so a sum below 2^-126 is exact and therefore tiny */
+  float r = a + b;
+  if (r != 0.0f && fabsf(r) < TINY) r = copysignf(0.0f, r);
+  return r;
+}
+
+float cref_sub(float a, float b) { return cref_add(a, -b); }
+
+float cref_mul(float a, float b) {
+  a = daz(a);
+  b = daz(b);
+  return round_exact_double((double)a * (double)b); /* 24 x 24 bits: the double product is exact */
+}
+
+float cref_fma(float a, float b, float c) {
+  a = daz(a);
+  b = daz(b);
+  c = daz(c);
+  float p = a * b;
+  double pd = (double)a * (double)b; /* exact */
+  if ((double)p == pd && (p == 0.0f || fabsf(p) >= TINY)) {
+    /* the product is a normal float (always so for bf16 x bf16 away from underflow): the fused
+       result is the R0 rounding of c + p, which is cref_add */
+    return cref_add(c, p);
+  }
+  double cd = (double)c;
+  double s = pd + cd; /* TwoSum: s + e == pd + cd exactly */
+  double bv = s - pd;
+  double e = (pd - (s - bv)) + (cd - bv);
+  if (s == 0.0 && e == 0.0) return fmaf(a, b, c); /* exact zero: IEEE sign rule */
+  return round_double_double(s, e);
+}
+
+float cref_div(float a, float b) {
+  a = daz(a);
+  b = daz(b);
+  double q = (double)a / (double)b;
+  if (q == 0.0 || isinf(q) || isnan(q)) return (float)q;
+  /* RN24(RN53(x)) == RN24(x) for a quotient of binary32 numbers (53 >= 2*24+2) */
+  double qs = ((double)a * 0x1p100) / (double)b;
+  if (fabsf((float)qs) < 0x1p-26f) return q < 0 ? -0.0f : 0.0f;
+  return (float)q;
+}
+
+float cref_sqrt(float a) {
+  a = daz(a);
+  return sqrtf(a); /* correctly rounded; a square root of a normal float is never tiny */
+}
+
+uint16_t cref_bf16(float x) {
+  uint32_t u = f_bits(daz(x));
+  u = u + 0x7FFFu + ((u >> 16) & 1u); /* round to nearest even on the 16 dropped bits */
+  return (uint16_t)(u >> 16);
+}
+
+static inline float widen(uint16_t h) { return daz(f_from_bits((uint32_t)h << 16)); }
+
+/* ======================================================================== */
+/* R4: canonical functions                                                   */
+/* ======================================================================== */
+
+/* cexp: Cody-Waite reduction by ln 2 split in two parts, degree-7 Taylor polynomial
+   by Horner in separate multiplies and adds, exact scaling by 2^k. */
+static const uint32_t EXP_L2E = 0x3FB8AA3Bu;    /* RN32(1/ln 2) */
+static const uint32_t EXP_LN2_HI = 0x3F317200u; /* ln 2 cut to 15 significant bits */
+static const uint32_t EXP_LN2_LO = 0x35BFBE8Eu; /* RN32(ln 2 - LN2_HI) */
+static const uint32_t EXP_C[8] = {               /* RN32(1/n!) for n = 0..7 */
+    0x3F800000u, 0x3F800000u, 0x3F000000u, 0x3E2AAAABu,
+    0x3D2AAAABu, 0x3C088889u, 0x3AB60B61u, 0x39500D01u};
+
+float cref_exp(float x) {
+  x = daz(x);
+  float t = cref_mul(x, f_from_bits(EXP_L2E));
+  float kf = nearbyintf(t); /* nearest integer, ties to even (default rounding mode); exact */
+  if (kf > 127.0f) return INFINITY;
+  if (kf < -125.0f) return 0.0f;
+  float r = cref_sub(cref_sub(x, cref_mul(kf, f_from_bits(EXP_LN2_HI))), cref_mul(kf, f_from_bits(EXP_LN2_LO)));
+  float p = f_from_bits(EXP_C[7]);
+  for (int i = 6; i >= 0; --i) p = cref_add(cref_mul(p, r), f_from_bits(EXP_C[i]));
+  int k = (int)kf;
+  float scale = f_from_bits((uint32_t)(k + 127) << 23);
+  return cref_mul(p, scale);
+}
+
+/* clog: x = 2^e f with f in (sqrt(1/2), sqrt(2)], s = (f-1)/(f+1), log f = 2 atanh(s) by the odd
+   series up to s^11, then e ln 2 added in two parts. */
+static const uint32_t LOG_SQRT2 = 0x3FB504F3u;            /* RN32(sqrt 2) */
+static const uint32_t LOG_INV[5] = {0x3EAAAAABu, 0x3E4CCCCDu, 0x3E124925u, 0x3DE38E39u,
+                                    0x3DBA2E8Cu}; /* RN32(1/3), 1/5, 1/7, 1/9, 1/11 */
+
+float cref_log(float x) {
+  x = daz(x);
+  if (x == 0.0f) return -INFINITY;
+  if (x < 0.0f || isnan(x)) return NAN;
+  if (isinf(x)) return x;
+  uint32_t u = f_bits(x);
+  int e = (int)((u >> 23) & 0xFFu) - 127;
+  float f = f_from_bits((u & 0x7FFFFFu) | 0x3F800000u);
+  if (f > f_from_bits(LOG_SQRT2)) {
+    f = cref_mul(f, 0.5f);
+    e += 1;
+  }
+  float s = cref_div(cref_sub(f, 1.0f), cref_add(f, 1.0f));
+  float z = cref_mul(s, s);
+  float q = f_from_bits(LOG_INV[4]);
+  for (int i = 3; i >= 0; --i) q = cref_add(cref_mul(q, z), f_from_bits(LOG_INV[i]));
+  q = cref_add(cref_mul(q, z), 1.0f);
+  float lf = cref_mul(cref_add(s, s), q);
+  float ef = (float)e;
+  return cref_add(cref_mul(ef, f_from_bits(EXP_LN2_HI)), cref_add(cref_mul(ef, f_from_bits(EXP_LN2_LO)), lf));
+}
+
+float cref_sigmoid(float x) {
+  x = daz(x);
+  return cref_div(1.0f, cref_add(1.0f, cref_exp(-x)));
+}
+
+float cref_silu(float x) { return cref_mul(x, cref_sigmoid(x)); }
+
+int cref_prim(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out) {
+  if (n < 0 || op < 0 || op > 10) return -1;
+  for (int64_t i = 0; i < n; ++i) {
+    switch (op) {
+      case 0: out[i] = cref_add(a[i], b[i]); break;
+      case 1: out[i] = cref_sub(a[i], b[i]); break;
+      case 2: out[i] = cref_mul(a[i], b[i]); break;
+      case 3: out[i] = cref_fma(a[i], b[i], c[i]); break;
+      case 4: out[i] = cref_div(a[i], b[i]); break;
+      case 5: out[i] = cref_sqrt(a[i]); break;
+      case 6: out[i] = cref_exp(a[i]); break;
+      case 7: out[i] = cref_log(a[i]); break;
+      case 8: out[i] = cref_sigmoid(a[i]); break;
+      case 9: out[i] = cref_silu(a[i]); break;
+      case 10: out[i] = widen(cref_bf16(a[i])); break;
+    }
+  }
+  return 0;
+}
+
+/* ======================================================================== */
+/* R1: canonical reductions, Algorithm 2 (TreeFold)                          */
+/* ======================================================================== */
+
+typedef struct {
+  int n;
+  int level[64];
+  float val[64];
+} sfold;
+
+/* Push: merge with the top entry while it has the same level; the earlier block stays on the left. */
+static void sfold_push(sfold* f, float part) {
+  int level = 0;
+  while (f->n > 0 && f->level[f->n - 1] == level) {
+    part = cref_add(f->val[f->n - 1], part);
+    f->n--;
+    level++;
+  }
+  f->level[f->n] = level;
+  f->val[f->n] = part;
+  f->n++;
+}
+
+/* Result: start from the lowest-level entry (top of the stack), then add the remaining entries in
+   ascending level order. */
+static float sfold_result(const sfold* f) {
+  if (f->n == 0) return 0.0f;
+  float acc = f->val[f->n - 1];
+  for (int i = f->n - 2; i >= 0; --i) acc = cref_add(f->val[i], acc);
+  return acc;
+}
+
+typedef struct {
+  int n;
+  int level[64];
+  float* val[64];
+  int64_t len;
+} vfold;
+
+static void vfold_push(vfold* f, float* part) { /* takes ownership of part */
+  int level = 0;
+  while (f->n > 0 && f->level[f->n - 1] == level) {
+    float* lower = f->val[f->n - 1];
+    for (int64_t j = 0; j < f->len; ++j) part[j] = cref_add(lower[j], part[j]);
+    free(lower);
+    f->n--;
+    level++;
+  }
+  f->level[f->n] = level;
+  f->val[f->n] = part;
+  f->n++;
+}
+
+static void vfold_result(vfold* f, float* out) { /* frees the stack */
+  if (f->n == 0) {
+    for (int64_t j = 0; j < f->len; ++j) out[j] = 0.0f;
+    return;
+  }
+  float* acc = f->val[f->n - 1];
+  for (int i = f->n - 2; i >= 0; --i) {
+    for (int64_t j = 0; j < f->len; ++j) acc[j] = cref_add(f->val[i][j], acc[j]);
+    free(f->val[i]);
+  }
+  memcpy(out, acc, sizeof(float) * (size_t)f->len);
+  free(acc);
+  f->n = 0;
+}
+
+float cref_rsum(const float* t, int64_t n, int64_t stride, int32_t chunk) {
+  sfold f = {0};
+  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
+    int64_t c1 = c0 + chunk < n ? c0 + chunk : n;
+    float s = 0.0f;
+    for (int64_t k = c0; k < c1; ++k) s = cref_add(s, t[k * stride]);
+    sfold_push(&f, s);
+  }
+  return sfold_result(&f);
+}
+
+float cref_rdot_bf16(const uint16_t* a, int64_t sa, const uint16_t* b, int64_t sb, int64_t n, int32_t chunk) {
+  sfold f = {0};
+  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
+    int64_t c1 = c0 + chunk < n ? c0 + chunk : n;
+    float s = 0.0f;
+    for (int64_t k = c0; k < c1; ++k) s = cref_fma(widen(a[k * sa]), widen(b[k * sb]), s);
+    sfold_push(&f, s);
+  }
+  return sfold_result(&f);
+}
+
+float cref_rdot_f32(const float* a, int64_t sa, const float* b, int64_t sb, int64_t n, int32_t chunk) {
+  sfold f = {0};
+  for (int64_t c0 = 0; c0 < n; c0 += chunk) {
+    int64_t c1 = c0 + chunk < n ? c0 + chunk : n;
+    float s = 0.0f;
+    for (int64_t k = c0; k < c1; ++k) s = cref_add(s, cref_mul(a[k * sa], b[k * sb]));
+    sfold_push(&f, s);
+  }
+  return sfold_result(&f);
+}
+
+int cref_treefold(const float* parts, int64_t nparts, int64_t len, float* out, int32_t* max_entries) {
+  if (nparts < 0 || len < 0) return -1;
+  vfold f = {0};
+  f.len = len;
+  int deepest = 0;
+  for (int64_t p = 0; p < nparts; ++p) {
+    if (f.n + 1 > deepest) deepest = f.n + 1;
+    float* part = (float*)malloc(sizeof(float) * (size_t)(len ? len : 1));
+    memcpy(part, parts + p * len, sizeof(float) * (size_t)len);
+    vfold_push(&f, part);
+  }
+  vfold_result(&f, out);
+  if (max_entries) *max_entries = deepest;
+  return 0;
+}
+
+/* ======================================================================== */
+/* R2: GEMM                                                                   */
+/* ======================================================================== */
+
+int cref_gemm(int32_t trans_a, int32_t trans_b, int64_t m, int64_t n, int64_t k, const uint16_t* a, int64_t lda,
+              const uint16_t* b, int64_t ldb, float* c, int64_t ldc) {
+  if (m < 0 || n < 0 || k < 0 || ldc < n) return -1;
+  if (m == 0 || n == 0) return 0;
+  /* B widened once into a dense [k][n] fp32 copy (exact) */
+  float* bw = (float*)malloc(sizeof(float) * (size_t)(k ? k : 1) * (size_t)n);
+  for (int64_t kk = 0; kk < k; ++kk)
+    for (int64_t j = 0; j < n; ++j) bw[kk * n + j] = widen(trans_b ? b[j * ldb + kk] : b[kk * ldb + j]);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t i = 0; i < m; ++i) {
+    vfold f = {0};
+    f.len = n;
+    for (int64_t c0 = 0; c0 < k; c0 += CHUNK) {
+      int64_t c1 = c0 + CHUNK < k ? c0 + CHUNK : k;
+      float* part = (float*)calloc((size_t)n, sizeof(float)); /* chain starts at +0 */
+      for (int64_t kk = c0; kk < c1; ++kk) {
+        float av = widen(trans_a ? a[kk * lda + i] : a[i * lda + kk]);
+        const float* brow = bw + kk * n;
+        for (int64_t j = 0; j < n; ++j) part[j] = cref_fma(av, brow[j], part[j]);
+      }
+      vfold_push(&f, part);
+    }
+    vfold_result(&f, c + i * ldc);
+  }
+  free(bw);
+  return 0;
+}
+
+/* ======================================================================== */
+/* R3: RMSNorm                                                                */
+/* ======================================================================== */
+
+static float inv_of(int64_t d) { return (float)(1.0 / (double)d); } /* RN32(1/d): correctly rounded */
+
+int cref_rownorm_fwd(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps, uint16_t* y,
+                     float* rstd) {
+  if (rows < 0 || cols <= 0) return -1;
+  const float inv_d = inv_of(cols);
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < rows; ++t) {
+    const float* xr = x + t * cols;
+    sfold f = {0};
+    for (int64_t c0 = 0; c0 < cols; c0 += CHUNK) {
+      int64_t c1 = c0 + CHUNK < cols ? c0 + CHUNK : cols;
+      float s = 0.0f;
+      for (int64_t k = c0; k < c1; ++k) s = cref_add(s, cref_mul(xr[k], xr[k]));
+      sfold_push(&f, s);
+    }
+    float ss = sfold_result(&f);
+    float ms = cref_mul(ss, inv_d);
+    float v = cref_add(ms, eps);
+    float r = cref_div(1.0f, cref_sqrt(v));
+    rstd[t] = r;
+    for (int64_t k = 0; k < cols; ++k) y[t * cols + k] = cref_bf16(cref_mul(cref_mul(xr[k], r), widen(gain[k])));
+  }
+  return 0;
+}
+
+int cref_rownorm_bwd(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
+                     const float* dy, float* dx, float* dgain) {
+  if (rows < 0 || cols <= 0) return -1;
+  const float inv_d = inv_of(cols);
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < rows; ++t) {
+    const float* xr = x + t * cols;
+    const float* dyr = dy + t * cols;
+    float r = rstd[t];
+    float* gy = (float*)malloc(sizeof(float) * (size_t)cols);
+    for (int64_t k = 0; k < cols; ++k) gy[k] = cref_mul(dyr[k], widen(gain[k]));
+    float dot = cref_rdot_f32(gy, 1, xr, 1, cols, CHUNK);
+    float q = cref_mul(cref_mul(cref_mul(r, r), r), cref_mul(dot, inv_d));
+    for (int64_t k = 0; k < cols; ++k) dx[t * cols + k] = cref_sub(cref_mul(r, gy[k]), cref_mul(xr[k], q));
+    free(gy);
+  }
+  if (dgain) {
+#pragma omp parallel for schedule(static)
+    for (int64_t k = 0; k < cols; ++k) {
+      sfold f = {0};
+      for (int64_t c0 = 0; c0 < rows; c0 += CHUNK) {
+        int64_t c1 = c0 + CHUNK < rows ? c0 + CHUNK : rows;
+        float s = 0.0f;
+        for (int64_t t = c0; t < c1; ++t) s = cref_add(s, cref_mul(dy[t * cols + k], cref_mul(x[t * cols + k], rstd[t])));
+        sfold_push(&f, s);
+      }
+      dgain[k] = sfold_result(&f);
+    }
+  }
+  return 0;
+}
+
+/* ======================================================================== */
+/* R5: causal softmax, R6: cross-entropy                                      */
+/* ======================================================================== */
+
+int cref_softmax_causal(int64_t batch, int64_t s, const float* raw, float scale, uint16_t* probs) {
+  if (batch < 0 || s < 0) return -1;
+#pragma omp parallel for schedule(dynamic, 4)
+  for (int64_t bi = 0; bi < batch * s; ++bi) {
+    int64_t i = bi % s;
+    const float* row = raw + bi * s;
+    uint16_t* prow = probs + bi * s;
+    float* e = (float*)malloc(sizeof(float) * (size_t)(s ? s : 1));
+    float m = cref_mul(row[0], scale);
+    for (int64_t j = 1; j <= i; ++j) {
+      float sc = cref_mul(row[j], scale);
+      if (sc > m) m = sc;
+    }
+    for (int64_t j = 0; j < s; ++j) e[j] = (j <= i) ? cref_exp(cref_sub(cref_mul(row[j], scale), m)) : 0.0f;
+    float S = cref_rsum(e, s, 1, CHUNK); /* masked keys enter as +0 terms */
+    float r = cref_div(1.0f, S);
+    for (int64_t j = 0; j < s; ++j) prow[j] = (j <= i) ? cref_bf16(cref_mul(e[j], r)) : (uint16_t)0;
+    free(e);
+  }
+  return 0;
+}
+
+int cref_xent(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
+              uint16_t* dlogits, float* row_loss, float* mean_loss) {
+  if (rows < 0 || vocab <= 0) return -1;
+  for (int64_t t = 0; t < rows; ++t)
+    if (targets[t] < 0 || targets[t] >= vocab) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < rows; ++t) {
+    const uint16_t* lr = logits + t * vocab;
+    float* e = (float*)malloc(sizeof(float) * (size_t)vocab);
+    float m = widen(lr[0]);
+    for (int64_t j = 1; j < vocab; ++j) {
+      float l = widen(lr[j]);
+      if (l > m) m = l;
+    }
+    for (int64_t j = 0; j < vocab; ++j) e[j] = cref_exp(cref_sub(widen(lr[j]), m));
+    float S = cref_rsum(e, vocab, 1, CHUNK);
+    float lse = cref_add(m, cref_log(S));
+    int32_t y = targets[t];
+    row_loss[t] = cref_sub(lse, widen(lr[y]));
+    float r = cref_div(1.0f, S);
+    if (dlogits) {
+      for (int64_t j = 0; j < vocab; ++j) {
+        float p = cref_mul(e[j], r);
+        dlogits[t * vocab + j] = cref_bf16(cref_mul(cref_sub(p, j == y ? 1.0f : 0.0f), inv_tokens));
+      }
+    }
+    free(e);
+  }
+  if (mean_loss) *mean_loss = cref_mul(cref_rsum(row_loss, rows, 1, CHUNK), inv_tokens);
+  return 0;
+}
+
+/* ======================================================================== */
+/* R7: gradient plan (Algorithm 1, averages as reciprocal multiplies)        */
+/* ======================================================================== */
+
+typedef struct {
+  cref_plan p;
+  float inv_accum, inv_shard, inv_rep;
+  int64_t n;
+  float* g_r;   /* rank accumulator */
+  float* inner; /* running ascending sum over shards */
+  int have_inner;
+  vfold fold;   /* TreeFold over replicas */
+} plan_state;
+
+static void plan_init(plan_state* s, const cref_plan* p, int64_t n) {
+  memset(s, 0, sizeof(*s));
+  s->p = *p;
+  s->inv_accum = inv_of(p->accum);
+  s->inv_shard = inv_of(p->dp_shard);
+  s->inv_rep = inv_of(p->dp_replicate);
+  s->n = n;
+  s->g_r = (float*)malloc(sizeof(float) * (size_t)(n ? n : 1));
+  s->inner = (float*)malloc(sizeof(float) * (size_t)(n ? n : 1));
+  s->fold.len = n;
+}
+
+static void plan_rank_begin(plan_state* s) {
+  for (int64_t i = 0; i < s->n; ++i) s->g_r[i] = 0.0f;
+}
+
+static void plan_add_microbatch(plan_state* s, const float* grad) {
+  for (int64_t i = 0; i < s->n; ++i) s->g_r[i] = cref_add(s->g_r[i], cref_mul(grad[i], s->inv_accum));
+}
+
+static void plan_rank_end(plan_state* s, int r) {
+  int shard = r % s->p.dp_shard;
+  if (shard == 0) {
+    memcpy(s->inner, s->g_r, sizeof(float) * (size_t)s->n);
+  } else {
+    for (int64_t i = 0; i < s->n; ++i) s->inner[i] = cref_add(s->inner[i], s->g_r[i]);
+  }
+  if (shard == s->p.dp_shard - 1) {
+    float* part = (float*)malloc(sizeof(float) * (size_t)(s->n ? s->n : 1));
+    for (int64_t i = 0; i < s->n; ++i) part[i] = cref_mul(s->inner[i], s->inv_shard);
+    vfold_push(&s->fold, part);
+  }
+}
+
+static void plan_finish(plan_state* s, float* out) {
+  vfold_result(&s->fold, out);
+  for (int64_t i = 0; i < s->n; ++i) out[i] = cref_mul(out[i], s->inv_rep);
+  free(s->g_r);
+  free(s->inner);
+}
+
+static int plan_valid(const cref_plan* p) {
+  return p && p->accum >= 1 && p->dp_shard >= 1 && p->dp_replicate >= 1;
+}
+
+int cref_grad_accum(const cref_plan* plan, int64_t n, const float* const* grads, float* out) {
+  if (!plan_valid(plan) || n < 0) return -1;
+  plan_state s;
+  plan_init(&s, plan, n);
+  int N = plan->dp_shard * plan->dp_replicate;
+  for (int r = 0; r < N; ++r) {
+    plan_rank_begin(&s);
+    for (int k = 0; k < plan->accum; ++k) plan_add_microbatch(&s, grads[r * plan->accum + k]);
+    plan_rank_end(&s, r);
+  }
+  plan_finish(&s, out);
+  return 0;
+}
+
+/* ======================================================================== */
+/* R9: AdamW                                                                  */
+/* ======================================================================== */
+
+static void adamw_tensor(int64_t n, uint16_t* p16, float* m, float* v, const float* g, int decay,
+                         const cref_adamw_consts* k) {
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    float p = widen(p16[i]);
+    if (decay) p = cref_mul(p, k->decay_factor);
+    float gi = g[i];
+    float mi = cref_add(cref_mul(k->beta1, m[i]), cref_mul(k->one_minus_beta1, gi));
+    float vi = cref_add(cref_mul(k->beta2, v[i]), cref_mul(k->one_minus_beta2, cref_mul(gi, gi)));
+    float mh = cref_mul(mi, k->inv_bc1);
+    float vh = cref_mul(vi, k->inv_bc2);
+    float u = cref_div(mh, cref_add(cref_sqrt(vh), k->eps));
+    p = cref_sub(p, cref_mul(k->lr, u));
+    m[i] = mi;
+    v[i] = vi;
+    p16[i] = cref_bf16(p);
+  }
+}
+
+int cref_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m, float* const* v,
+               const float* const* grads, const uint8_t* decay_mask, const cref_adamw_consts* k) {
+  if (n_tensors < 0 || !k) return -1;
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    if (sizes[t] < 0) return -1;
+    adamw_tensor(sizes[t], params[t], m[t], v[t], grads[t], decay_mask[t] != 0, k);
+  }
+  return 0;
+}
+
+/* ======================================================================== */
+/* Elementwise pieces of the decoder                                          */
+/* ======================================================================== */
+
+/* R8: half-split rotation of one head vector v[0..hd) at position s; output bf16. */
+static void rope_fwd(const float* v, int hd, const float* cs, const float* sn, uint16_t* out) {
+  int h = hd / 2;
+  for (int i = 0; i < h; ++i) {
+    float x1 = v[i], x2 = v[i + h];
+    out[i] = cref_bf16(cref_sub(cref_mul(x1, cs[i]), cref_mul(x2, sn[i])));
+    out[i + h] = cref_bf16(cref_add(cref_mul(x2, cs[i]), cref_mul(x1, sn[i])));
+  }
+}
+
+/* transposed rotation of a gradient */
+static void rope_bwd(const float* g, int hd, const float* cs, const float* sn, float* out) {
+  int h = hd / 2;
+  for (int i = 0; i < h; ++i) {
+    float g1 = g[i], g2 = g[i + h];
+    out[i] = cref_add(cref_mul(g1, cs[i]), cref_mul(g2, sn[i]));
+    out[i + h] = cref_sub(cref_mul(g2, cs[i]), cref_mul(g1, sn[i]));
+  }
+}
+
+/* ======================================================================== */
+/* Decoder block                                                              */
+/* ======================================================================== */
+
+typedef struct {
+  int64_t T, B, S, d, H, hd, F;
+  float* x;      /* [T][d] input (residual) */
+  uint16_t* xn;  /* [T][d] */
+  float* rstd1;  /* [T] */
+  uint16_t *q, *k, *v; /* [B][H][S][hd] bf16, q and k after rotation */
+  uint16_t* P;   /* [B][H][S][S] */
+  uint16_t* O;   /* [T][d] */
+  float* h;      /* [T][d] */
+  uint16_t* hn;  /* [T][d] */
+  float* rstd2;  /* [T] */
+  float* gu;     /* [T][2F] */
+  uint16_t* a;   /* [T][F] */
+} block_saved;
+
+static void* xmalloc(size_t n) {
+  void* p = malloc(n ? n : 1);
+  return p;
+}
+
+static void block_saved_alloc(block_saved* s, int64_t B, int64_t S, int64_t d, int64_t H, int64_t F) {
+  s->T = B * S; s->B = B; s->S = S; s->d = d; s->H = H; s->hd = d / H; s->F = F;
+  int64_t T = s->T;
+  s->x = (float*)xmalloc(sizeof(float) * T * d);
+  s->xn = (uint16_t*)xmalloc(2 * T * d);
+  s->rstd1 = (float*)xmalloc(sizeof(float) * T);
+  s->q = (uint16_t*)xmalloc(2 * T * d);
+  s->k = (uint16_t*)xmalloc(2 * T * d);
+  s->v = (uint16_t*)xmalloc(2 * T * d);
+  s->P = (uint16_t*)xmalloc(2 * B * H * S * S);
+  s->O = (uint16_t*)xmalloc(2 * T * d);
+  s->h = (float*)xmalloc(sizeof(float) * T * d);
+  s->hn = (uint16_t*)xmalloc(2 * T * d);
+  s->rstd2 = (float*)xmalloc(sizeof(float) * T);
+  s->gu = (float*)xmalloc(sizeof(float) * T * 2 * F);
+  s->a = (uint16_t*)xmalloc(2 * T * F);
+}
+
+static void block_saved_free(block_saved* s) {
+  free(s->x); free(s->xn); free(s->rstd1); free(s->q); free(s->k); free(s->v); free(s->P); free(s->O);
+  free(s->h); free(s->hn); free(s->rstd2); free(s->gu); free(s->a);
+}
+
+static const uint32_t ATTN_SCALE_128 = 0x3DB504F3u; /* RN32(1/sqrt(128)) */
+
+static float attn_scale(int64_t hd) {
+  if (hd == 128) return f_from_bits(ATTN_SCALE_128);
+  return (float)(1.0 / sqrt((double)hd)); /* RN32(1/sqrt(hd)) for other head sizes used in tests */
+}
+
+/* forward of one block; w = {attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down}; y = block output */
+static void block_fwd(block_saved* s, const float* x, const uint16_t* const* w, const float* rope_cos,
+                      const float* rope_sin, float eps, float* y) {
+  const int64_t T = s->T, B = s->B, S = s->S, d = s->d, H = s->H, hd = s->hd, F = s->F;
+  memcpy(s->x, x, sizeof(float) * T * d);
+  cref_rownorm_fwd(T, d, x, w[0], eps, s->xn, s->rstd1);
+  float* qkv = (float*)xmalloc(sizeof(float) * T * 3 * d);
+  cref_gemm(0, 1, T, 3 * d, d, s->xn, d, w[1], d, qkv, 3 * d);
+  for (int64_t t = 0; t < T; ++t) {
+    int64_t b = t / S, pos = t % S;
+    for (int64_t hh = 0; hh < H; ++hh) {
+      int64_t o = ((b * H + hh) * S + pos) * hd;
+      rope_fwd(qkv + t * 3 * d + hh * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), s->q + o);
+      rope_fwd(qkv + t * 3 * d + d + hh * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), s->k + o);
+      for (int64_t j = 0; j < hd; ++j) s->v[o + j] = cref_bf16(qkv[t * 3 * d + 2 * d + hh * hd + j]);
+    }
+  }
+  free(qkv);
+  float* raw = (float*)xmalloc(sizeof(float) * S * S);
+  float* ob = (float*)xmalloc(sizeof(float) * S * hd);
+  const float c = attn_scale(hd);
+  for (int64_t bh = 0; bh < B * H; ++bh) {
+    int64_t b = bh / H, hh = bh % H;
+    const uint16_t* Q = s->q + bh * S * hd;
+    const uint16_t* K = s->k + bh * S * hd;
+    const uint16_t* V = s->v + bh * S * hd;
+    uint16_t* P = s->P + bh * S * S;
+    cref_gemm(0, 1, S, S, hd, Q, hd, K, hd, raw, S);
+    cref_softmax_causal(1, S, raw, c, P);
+    cref_gemm(0, 0, S, hd, S, P, S, V, hd, ob, hd);
+    for (int64_t pos = 0; pos < S; ++pos)
+      for (int64_t j = 0; j < hd; ++j) s->O[(b * S + pos) * d + hh * hd + j] = cref_bf16(ob[pos * hd + j]);
+  }
+  free(raw);
+  free(ob);
+  float* attn = (float*)xmalloc(sizeof(float) * T * d);
+  cref_gemm(0, 1, T, d, d, s->O, d, w[2], d, attn, d);
+  for (int64_t i = 0; i < T * d; ++i) s->h[i] = cref_add(x[i], attn[i]);
+  free(attn);
+  cref_rownorm_fwd(T, d, s->h, w[3], eps, s->hn, s->rstd2);
+  cref_gemm(0, 1, T, 2 * F, d, s->hn, d, w[4], d, s->gu, 2 * F);
+  for (int64_t t = 0; t < T; ++t)
+    for (int64_t j = 0; j < F; ++j)
+      s->a[t * F + j] = cref_bf16(cref_mul(cref_silu(s->gu[t * 2 * F + j]), s->gu[t * 2 * F + F + j]));
+  float* ffn = (float*)xmalloc(sizeof(float) * T * d);
+  cref_gemm(0, 1, T, d, F, s->a, F, w[5], F, ffn, d);
+  for (int64_t i = 0; i < T * d; ++i) y[i] = cref_add(s->h[i], ffn[i]);
+  free(ffn);
+}
+
+static uint16_t* to_bf16(const float* x, int64_t n) {
+  uint16_t* o = (uint16_t*)xmalloc(2 * n);
+  for (int64_t i = 0; i < n; ++i) o[i] = cref_bf16(x[i]);
+  return o;
+}
+
+/* backward of one block: dy = gradient of the block output; dx = gradient of the block input;
+   dw = the six fp32 weight gradients */
+static void block_bwd(const block_saved* s, const float* dy, const uint16_t* const* w, const float* rope_cos,
+                      const float* rope_sin, float* dx, float* const* dw) {
+  const int64_t T = s->T, B = s->B, S = s->S, d = s->d, H = s->H, hd = s->hd, F = s->F;
+  /* MLP */
+  uint16_t* dyb = to_bf16(dy, T * d);
+  cref_gemm(1, 0, d, F, T, dyb, d, s->a, F, dw[5], F);            /* dW_down = dy^T a */
+  float* da = (float*)xmalloc(sizeof(float) * T * F);
+  cref_gemm(0, 0, T, F, d, dyb, d, w[5], F, da, F);               /* da = dy W_down */
+  free(dyb);
+  uint16_t* dgu = (uint16_t*)xmalloc(2 * T * 2 * F);
+  for (int64_t t = 0; t < T; ++t) {
+    for (int64_t j = 0; j < F; ++j) {
+      float g = s->gu[t * 2 * F + j], u = s->gu[t * 2 * F + F + j], dav = da[t * F + j];
+      float sig = cref_sigmoid(g);
+      float silu = cref_mul(g, sig);
+      float dup = cref_mul(dav, silu);
+      float dsg = cref_mul(sig, cref_add(1.0f, cref_mul(g, cref_sub(1.0f, sig))));
+      float dgate = cref_mul(cref_mul(dav, u), dsg);
+      dgu[t * 2 * F + j] = cref_bf16(dgate);
+      dgu[t * 2 * F + F + j] = cref_bf16(dup);
+    }
+  }
+  free(da);
+  cref_gemm(1, 0, 2 * F, d, T, dgu, 2 * F, s->hn, d, dw[4], d);   /* dW_gate_up = dgu^T hn */
+  float* dhn = (float*)xmalloc(sizeof(float) * T * d);
+  cref_gemm(0, 0, T, d, 2 * F, dgu, 2 * F, w[4], d, dhn, d);      /* dhn = dgu W_gate_up */
+  free(dgu);
+  float* dhnorm = (float*)xmalloc(sizeof(float) * T * d);
+  cref_rownorm_bwd(T, d, s->h, w[3], s->rstd2, dhn, dhnorm, dw[3]);
+  free(dhn);
+  float* dh = (float*)xmalloc(sizeof(float) * T * d);
+  for (int64_t i = 0; i < T * d; ++i) dh[i] = cref_add(dy[i], dhnorm[i]);
+  free(dhnorm);
+  /* attention output projection */
+  uint16_t* dhb = to_bf16(dh, T * d);
+  cref_gemm(1, 0, d, d, T, dhb, d, s->O, d, dw[2], d);            /* dW_o = dh^T O */
+  float* dO = (float*)xmalloc(sizeof(float) * T * d);
+  cref_gemm(0, 0, T, d, d, dhb, d, w[2], d, dO, d);               /* dO = dh W_o */
+  free(dhb);
+  /* attention core, per (batch, head) */
+  const float c = attn_scale(hd);
+  float* dq = (float*)xmalloc(sizeof(float) * T * d);
+  float* dk = (float*)xmalloc(sizeof(float) * T * d);
+  uint16_t* dqkv = (uint16_t*)xmalloc(2 * T * 3 * d);
+  uint16_t* dOb = (uint16_t*)xmalloc(2 * S * hd);
+  uint16_t* Ob = (uint16_t*)xmalloc(2 * S * hd);
+  float* D = (float*)xmalloc(sizeof(float) * S);
+  float* dP = (float*)xmalloc(sizeof(float) * S * S);
+  uint16_t* dS = (uint16_t*)xmalloc(2 * S * S);
+  float* gq = (float*)xmalloc(sizeof(float) * S * hd);
+  float* gk = (float*)xmalloc(sizeof(float) * S * hd);
+  float* gv = (float*)xmalloc(sizeof(float) * S * hd);
+  for (int64_t bh = 0; bh < B * H; ++bh) {
+    int64_t b = bh / H, hh = bh % H;
+    const uint16_t* Q = s->q + bh * S * hd;
+    const uint16_t* K = s->k + bh * S * hd;
+    const uint16_t* V = s->v + bh * S * hd;
+    const uint16_t* P = s->P + bh * S * S;
+    for (int64_t pos = 0; pos < S; ++pos)
+      for (int64_t j = 0; j < hd; ++j) {
+        dOb[pos * hd + j] = cref_bf16(dO[(b * S + pos) * d + hh * hd + j]);
+        Ob[pos * hd + j] = s->O[(b * S + pos) * d + hh * hd + j];
+      }
+    for (int64_t i = 0; i < S; ++i) D[i] = cref_rdot_bf16(dOb + i * hd, 1, Ob + i * hd, 1, hd, CHUNK);
+    cref_gemm(0, 1, S, S, hd, dOb, hd, V, hd, dP, S);             /* dP = dO V^T */
+    for (int64_t i = 0; i < S; ++i)
+      for (int64_t j = 0; j < S; ++j)
+        dS[i * S + j] = (j <= i) ? cref_bf16(cref_mul(cref_mul(widen(P[i * S + j]), cref_sub(dP[i * S + j], D[i])), c))
+                                 : (uint16_t)0;
+    cref_gemm(0, 0, S, hd, S, dS, S, K, hd, gq, hd);              /* dQ = dS K */
+    cref_gemm(1, 0, S, hd, S, dS, S, Q, hd, gk, hd);              /* dK = dS^T Q */
+    cref_gemm(1, 0, S, hd, S, P, S, dOb, hd, gv, hd);             /* dV = P^T dO */
+    for (int64_t pos = 0; pos < S; ++pos) {
+      int64_t t = b * S + pos;
+      rope_bwd(gq + pos * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), dq + t * d + hh * hd);
+      rope_bwd(gk + pos * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), dk + t * d + hh * hd);
+      for (int64_t j = 0; j < hd; ++j) dqkv[t * 3 * d + 2 * d + hh * hd + j] = cref_bf16(gv[pos * hd + j]);
+    }
+  }
+  free(dOb); free(Ob); free(D); free(dP); free(dS); free(gq); free(gk); free(gv); free(dO);
+  for (int64_t t = 0; t < T; ++t)
+    for (int64_t j = 0; j < d; ++j) {
+      dqkv[t * 3 * d + j] = cref_bf16(dq[t * d + j]);
+      dqkv[t * 3 * d + d + j] = cref_bf16(dk[t * d + j]);
+    }
+  free(dq);
+  free(dk);
+  cref_gemm(1, 0, 3 * d, d, T, dqkv, 3 * d, s->xn, d, dw[1], d);  /* dW_qkv = dqkv^T xn */
+  float* dxn = (float*)xmalloc(sizeof(float) * T * d);
+  cref_gemm(0, 0, T, d, 3 * d, dqkv, 3 * d, w[1], d, dxn, d);     /* dxn = dqkv W_qkv */
+  free(dqkv);
+  float* dxnorm = (float*)xmalloc(sizeof(float) * T * d);
+  cref_rownorm_bwd(T, d, s->x, w[0], s->rstd1, dxn, dxnorm, dw[0]);
+  free(dxn);
+  for (int64_t i = 0; i < T * d; ++i) dx[i] = cref_add(dh[i], dxnorm[i]);
+  free(dxnorm);
+  free(dh);
+}
+
+static int cfg_valid(const cref_model_cfg* c) {
+  return c && c->n_layers >= 1 && c->d_model > 0 && c->n_heads > 0 && c->head_dim > 0 &&
+         c->n_heads * c->head_dim == c->d_model && (c->head_dim % 2) == 0 && c->d_ffn > 0 && c->vocab > 0 &&
+         c->seq > 0 && c->micro_seqs > 0;
+}
+
+int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x, const float* dy,
+                       const uint16_t* const* w, const float* rope_cos, const float* rope_sin, float* y, float* dx,
+                       float* const* dw) {
+  if (!cfg_valid(cfg) || batch <= 0) return -1;
+  block_saved s;
+  block_saved_alloc(&s, batch, cfg->seq, cfg->d_model, cfg->n_heads, cfg->d_ffn);
+  block_fwd(&s, x, w, rope_cos, rope_sin, cfg->rms_eps, y);
+  block_bwd(&s, dy, w, rope_cos, rope_sin, dx, dw);
+  block_saved_free(&s);
+  return 0;
+}
+
+/* ======================================================================== */
+/* Full step: forward + backward per microbatch, Algorithm 1, AdamW          */
+/* ======================================================================== */
+
+/* tensor sizes in the declared order */
+static void tensor_sizes(const cref_model_cfg* c, int64_t* sz, uint8_t* decay) {
+  int64_t d = c->d_model, F = c->d_ffn, V = c->vocab;
+  int i = 0;
+  sz[i] = V * d; decay[i++] = 0;                     /* embed */
+  for (int l = 0; l < c->n_layers; ++l) {
+    sz[i] = d; decay[i++] = 0;                       /* attn_norm */
+    sz[i] = 3 * d * d; decay[i++] = 1;               /* w_qkv */
+    sz[i] = d * d; decay[i++] = 1;                   /* w_o */
+    sz[i] = d; decay[i++] = 0;                       /* ffn_norm */
+    sz[i] = 2 * F * d; decay[i++] = 1;               /* w_gate_up */
+    sz[i] = d * F; decay[i++] = 1;                   /* w_down */
+  }
+  sz[i] = d; decay[i++] = 0;                         /* final_norm */
+  sz[i] = V * d; decay[i++] = 1;                     /* head */
+}
+
+/* gradient of the mean loss of one microbatch; grad = flat fp32 buffer in tensor order */
+static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params, const int32_t* tok, int64_t B,
+                                const float* rope_cos, const float* rope_sin, float* grad, const int64_t* off) {
+  const int64_t S = c->seq, d = c->d_model, V = c->vocab, L = c->n_layers;
+  const int64_t T = B * S;
+  int32_t* inp = (int32_t*)xmalloc(sizeof(int32_t) * T);
+  int32_t* lab = (int32_t*)xmalloc(sizeof(int32_t) * T);
+  for (int64_t b = 0; b < B; ++b)
+    for (int64_t s = 0; s < S; ++s) {
+      inp[b * S + s] = tok[b * (S + 1) + s];
+      lab[b * S + s] = tok[b * (S + 1) + s + 1];
+    }
+  /* embedding gather */
+  float* x = (float*)xmalloc(sizeof(float) * T * d);
+  for (int64_t t = 0; t < T; ++t)
+    for (int64_t j = 0; j < d; ++j) x[t * d + j] = widen(params[0][(int64_t)inp[t] * d + j]);
+  block_saved* saved = (block_saved*)xmalloc(sizeof(block_saved) * L);
+  float* y = (float*)xmalloc(sizeof(float) * T * d);
+  for (int64_t l = 0; l < L; ++l) {
+    const uint16_t* w[6];
+    for (int i = 0; i < 6; ++i) w[i] = params[1 + 6 * l + i];
+    block_saved_alloc(&saved[l], B, S, d, c->n_heads, c->d_ffn);
+    block_fwd(&saved[l], x, w, rope_cos, rope_sin, c->rms_eps, y);
+    float* tmp = x; x = y; y = tmp;
+  }
+  /* final norm, head, loss */
+  const int64_t i_fn = 1 + 6 * L, i_head = 2 + 6 * L;
+  uint16_t* xf = (uint16_t*)xmalloc(2 * T * d);
+  float* rstdf = (float*)xmalloc(sizeof(float) * T);
+  cref_rownorm_fwd(T, d, x, params[i_fn], c->rms_eps, xf, rstdf);
+  float* logits_f = (float*)xmalloc(sizeof(float) * T * V);
+  cref_gemm(0, 1, T, V, d, xf, d, params[i_head], d, logits_f, V);
+  uint16_t* logits = to_bf16(logits_f, T * V);
+  free(logits_f);
+  uint16_t* dlogits = (uint16_t*)xmalloc(2 * T * V);
+  float* row_loss = (float*)xmalloc(sizeof(float) * T);
+  float loss = 0.0f;
+  const float invT = inv_of(T);
+  cref_xent(T, V, logits, lab, invT, dlogits, row_loss, &loss);
+  free(logits);
+  free(row_loss);
+  /* backward */
+  cref_gemm(1, 0, V, d, T, dlogits, V, xf, d, grad + off[i_head], d);     /* dHead = dlogits^T xf */
+  float* dxf = (float*)xmalloc(sizeof(float) * T * d);
+  cref_gemm(0, 0, T, d, V, dlogits, V, params[i_head], d, dxf, d);       /* dxf = dlogits Head */
+  free(dlogits);
+  free(xf);
+  float* dx = (float*)xmalloc(sizeof(float) * T * d);
+  cref_rownorm_bwd(T, d, x, params[i_fn], rstdf, dxf, dx, grad + off[i_fn]);
+  free(dxf);
+  free(rstdf);
+  float* dxp = (float*)xmalloc(sizeof(float) * T * d);
+  for (int64_t l = L - 1; l >= 0; --l) {
+    const uint16_t* w[6];
+    float* dw[6];
+    for (int i = 0; i < 6; ++i) {
+      w[i] = params[1 + 6 * l + i];
+      dw[i] = grad + off[1 + 6 * l + i];
+    }
+    block_bwd(&saved[l], dx, w, rope_cos, rope_sin, dxp, dw);
+    block_saved_free(&saved[l]);
+    float* tmp = dx; dx = dxp; dxp = tmp;
+  }
+  free(saved);
+  /* R11: dE[v] = rsum over ascending positions t with inp[t] == v of dx[t] */
+  float* dE = grad + off[0];
+  int64_t* cnt = (int64_t*)calloc((size_t)V + 1, sizeof(int64_t));
+  for (int64_t t = 0; t < T; ++t) cnt[inp[t] + 1]++;
+  for (int64_t v = 0; v < V; ++v) cnt[v + 1] += cnt[v];
+  int64_t* pos = (int64_t*)xmalloc(sizeof(int64_t) * T);
+  int64_t* fill = (int64_t*)xmalloc(sizeof(int64_t) * V);
+  memcpy(fill, cnt, sizeof(int64_t) * V);
+  for (int64_t t = 0; t < T; ++t) pos[fill[inp[t]]++] = t; /* ascending t within each vocab row */
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t v = 0; v < V; ++v) {
+    int64_t n = cnt[v + 1] - cnt[v];
+    for (int64_t j = 0; j < d; ++j) {
+      sfold f = {0};
+      for (int64_t c0 = 0; c0 < n; c0 += CHUNK) {
+        int64_t c1 = c0 + CHUNK < n ? c0 + CHUNK : n;
+        float s = 0.0f;
+        for (int64_t q = c0; q < c1; ++q) s = cref_add(s, dx[pos[cnt[v] + q] * d + j]);
+        sfold_push(&f, s);
+      }
+      dE[v * d + j] = sfold_result(&f);
+    }
+  }
+  free(cnt); free(pos); free(fill);
+  free(dx); free(dxp); free(x); free(y); free(inp); free(lab);
+  return loss;
+}
+
+int cref_step(const cref_model_cfg* c, const cref_plan* plan, uint16_t* const* params, float* const* m,
+              float* const* v, const int32_t* windows, const float* rope_cos, const float* rope_sin,
+              const cref_adamw_consts* k, float* loss_out, float* const* grads_out) {
+  if (!cfg_valid(c) || !plan_valid(plan) || !k) return -1;
+  const int64_t nt = 3 + 6 * (int64_t)c->n_layers;
+  int64_t* sz = (int64_t*)xmalloc(sizeof(int64_t) * nt);
+  uint8_t* decay = (uint8_t*)xmalloc(nt);
+  tensor_sizes(c, sz, decay);
+  int64_t* off = (int64_t*)xmalloc(sizeof(int64_t) * (nt + 1));
+  off[0] = 0;
+  for (int64_t i = 0; i < nt; ++i) off[i + 1] = off[i] + sz[i];
+  const int64_t P = off[nt];
+  const int64_t S1 = c->seq + 1, mb = c->micro_seqs;
+  const int R = plan->dp_shard * plan->dp_replicate;
+  const int64_t M = (int64_t)R * plan->accum * mb;
+  for (int64_t i = 0; i < M * S1; ++i)
+    if (windows[i] < 0 || windows[i] >= c->vocab) { free(sz); free(decay); free(off); return -1; }
+  plan_state gs, ls;
+  plan_init(&gs, plan, P);
+  plan_init(&ls, plan, 1);
+  float* grad = (float*)xmalloc(sizeof(float) * P);
+  int32_t* tok = (int32_t*)xmalloc(sizeof(int32_t) * mb * S1);
+  for (int r = 0; r < R; ++r) {           /* mesh order: r = rep * dp_shard + shard */
+    plan_rank_begin(&gs);
+    plan_rank_begin(&ls);
+    for (int kk = 0; kk < plan->accum; ++kk) {
+      /* R12: rank r owns windows m with m mod R == r, taken in ascending m, micro_seqs per microbatch */
+      for (int64_t sidx = 0; sidx < mb; ++sidx) {
+        int64_t mwin = r + (int64_t)R * (kk * mb + sidx);
+        memcpy(tok + sidx * S1, windows + mwin * S1, sizeof(int32_t) * S1);
+      }
+      float loss = microbatch_fwd_bwd(c, params, tok, mb, rope_cos, rope_sin, grad, off);
+      plan_add_microbatch(&gs, grad);
+      plan_add_microbatch(&ls, &loss);
+    }
+    plan_rank_end(&gs, r);
+    plan_rank_end(&ls, r);
+  }
+  plan_finish(&gs, grad);
+  float loss = 0.0f;
+  plan_finish(&ls, &loss);
+  if (loss_out) *loss_out = loss;
+  if (grads_out)
+    for (int64_t i = 0; i < nt; ++i) memcpy(grads_out[i], grad + off[i], sizeof(float) * sz[i]);
+  const float** gp = (const float**)xmalloc(sizeof(float*) * nt);
+  for (int64_t i = 0; i < nt; ++i) gp[i] = grad + off[i];
+  cref_adamw(nt, sz, params, m, v, gp, decay, k);
+  free(gp); free(grad); free(tok); free(sz); free(decay); free(off);
+  return 0;
+}
+
+int cref_num_threads(void) { return omp_get_max_threads(); }

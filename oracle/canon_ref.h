@@ -1,0 +1,99 @@
+/*
+ * canon_ref.h - CPU oracle of the canonical-order training step (CANON-v1).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the CPU
+ * baseline leg of the benchmark may load this library.  It shares no code with
+ * the GPU library: its own primitives, its own constants, its own header.
+ *
+ * All pointers are host memory owned by the caller.  bf16 tensors are passed as
+ * uint16_t bit patterns.  Functions return 0 on success and a negative value on
+ * invalid arguments.
+ */
+#ifndef CANON_REF_H
+#define CANON_REF_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
+  float rms_eps;
+} cref_model_cfg;
+
+typedef struct {
+  int32_t accum, dp_shard, dp_replicate;
+} cref_plan;
+
+typedef struct {
+  float lr, beta1, one_minus_beta1, beta2, one_minus_beta2, inv_bc1, inv_bc2, eps, decay_factor;
+} cref_adamw_consts;
+
+/* ---- R0 primitives (scalar and vector forms, for the pins) ---- */
+float cref_add(float a, float b);
+float cref_sub(float a, float b);
+float cref_mul(float a, float b);
+float cref_fma(float a, float b, float c);
+float cref_div(float a, float b);
+float cref_sqrt(float a);
+float cref_exp(float x);
+float cref_log(float x);
+float cref_sigmoid(float x);
+float cref_silu(float x);
+uint16_t cref_bf16(float x);
+/* op: 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 exp, 7 log, 8 sigmoid, 9 silu, 10 bf16 round-trip */
+int cref_prim(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out);
+
+/* ---- R1 canonical reductions ---- */
+float cref_rsum(const float* t, int64_t n, int64_t stride, int32_t chunk);
+float cref_rdot_bf16(const uint16_t* a, int64_t sa, const uint16_t* b, int64_t sb, int64_t n, int32_t chunk);
+float cref_rdot_f32(const float* a, int64_t sa, const float* b, int64_t sb, int64_t n, int32_t chunk);
+/* Alg. 2 over nparts vectors of length len (parts[p*len ...]); *max_entries gets the deepest stack
+   size seen, counting the incoming partial. */
+int cref_treefold(const float* parts, int64_t nparts, int64_t len, float* out, int32_t* max_entries);
+
+/* ---- R2 GEMM: C[i,j] = rsum_k A(i,k) B(k,j), bf16 operands, fp32 result ---- */
+int cref_gemm(int32_t trans_a, int32_t trans_b, int64_t m, int64_t n, int64_t k, const uint16_t* a, int64_t lda,
+              const uint16_t* b, int64_t ldb, float* c, int64_t ldc);
+
+/* ---- R3 RMSNorm ---- */
+int cref_rownorm_fwd(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps, uint16_t* y,
+                     float* rstd);
+int cref_rownorm_bwd(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
+                     const float* dy, float* dx, float* dgain);
+
+/* ---- R5 causal softmax of raw scores (scale applied inside), R6 cross-entropy ---- */
+int cref_softmax_causal(int64_t batch, int64_t s, const float* raw, float scale, uint16_t* probs);
+int cref_xent(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
+              uint16_t* dlogits, float* row_loss, float* mean_loss);
+
+/* ---- R7 gradient plan (Alg. 1 + Alg. 2) ---- */
+int cref_grad_accum(const cref_plan* plan, int64_t n, const float* const* grads, float* out);
+
+/* ---- R9 AdamW ---- */
+int cref_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m, float* const* v,
+               const float* const* grads, const uint8_t* decay_mask, const cref_adamw_consts* k);
+
+/* ---- one decoder block, forward + backward ----
+   x, dy: fp32 [batch*seq, d]; w: the six block tensors in order attn_norm, w_qkv, w_o, ffn_norm,
+   w_gate_up, w_down; y: block output; dx: input gradient; dw: six fp32 gradient buffers. */
+int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x, const float* dy,
+                       const uint16_t* const* w, const float* rope_cos, const float* rope_sin, float* y, float* dx,
+                       float* const* dw);
+
+/* ---- full step: Alg. 1 over virtual ranks, then AdamW ----
+   params/m/v: n_tensors = 3 + 6*n_layers tensors in declared order (embed, per layer: attn_norm, w_qkv,
+   w_o, ffn_norm, w_gate_up, w_down; final_norm, head).  windows: [M][seq+1] int32 with
+   M = dp_shard*dp_replicate*accum*micro_seqs.  grads_out (optional, may be NULL): per-tensor fp32
+   buffers receiving the reduced gradient g. */
+int cref_step(const cref_model_cfg* cfg, const cref_plan* plan, uint16_t* const* params, float* const* m,
+              float* const* v, const int32_t* windows, const float* rope_cos, const float* rope_sin,
+              const cref_adamw_consts* k, float* loss_out, float* const* grads_out);
+
+int cref_num_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
