@@ -1,0 +1,177 @@
+/*
+ * canon.h - C ABI of libcanon: one replayed training step in canonical order, on MI355X (gfx950).
+ *
+ * The method is the paper's auditable replay:
+ *   - every floating-point reduction follows one fixed order on all hardware (section "Reproducible
+ *     Operations": fixed reduction order, one fused-multiply-add convention, subnormals flushed);
+ *   - the gradients of the data-parallel ranks are combined by Algorithm 1 (audit replay of one step),
+ *     with Algorithm 2 (binary-carry tree fold) across replicas, the ascending-shard reduce-scatter order
+ *     and averages taken as reciprocal multiplies (appendix "Deterministic Gradient Reduction");
+ *   - AdamW is widened to fp32 and rounded to bf16 once (training recipe, optimizer-state precision).
+ * The order itself (rules R0-R12, "CANON-v1") is stated with each entry point below.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE memory owned by the caller.  bf16 tensors are uint16_t bit patterns.
+ *     Arrays of tensor pointers (e.g. the parameter list) are HOST arrays of device pointers, read during
+ *     the call.  Structs are passed by host pointer and read during the call.
+ *   - The library allocates no device memory.  Scratch space comes from a caller-owned workspace whose
+ *     size is given by the matching *_workspace_bytes function.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).  Work is enqueued on it and
+ *     the call returns after validation and launch; device faults surface at the caller's next
+ *     synchronisation.
+ *   - Invalid arguments return CANON_EINVAL and enqueue nothing.  Valid requests outside what this
+ *     version implements return CANON_EUNSUPPORTED.  A failed launch returns CANON_EDEVICE.
+ *   - Calls on different streams may run concurrently; calls that share output buffers must be ordered
+ *     by the caller.
+ */
+#ifndef CANON_H
+#define CANON_H
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CANON_OK = 0,
+  CANON_EINVAL = -1,
+  CANON_EUNSUPPORTED = -2,
+  CANON_EDEVICE = -3,
+  CANON_EWORKSPACE = -4
+} canon_status;
+
+/* The declared order.  Version 1 requires: version = 1, chunk = 32, tree = CANON_TREE_BINARY_CARRY,
+   ftz = 1.  Anything else returns CANON_EUNSUPPORTED. */
+enum { CANON_TREE_BINARY_CARRY = 0 };
+typedef struct {
+  int32_t version; /* 1 */
+  int32_t chunk;   /* chain length: 32 */
+  int32_t tree;    /* CANON_TREE_BINARY_CARRY (Algorithm 2 over chunk partials) */
+  int32_t ftz;     /* 1: subnormal inputs read as signed zero; tiny results (after rounding) flushed */
+} canon_order;
+
+/* Algorithm 1's mesh: N = dp_shard * dp_replicate virtual ranks, rank r = rep * dp_shard + shard,
+   each accumulating `accum` microbatches. */
+typedef struct {
+  int32_t accum, dp_shard, dp_replicate;
+} canon_dp_plan;
+
+/* Llama-style decoder: pre-norm RMSNorm blocks, causal multi-head attention with half-split RoPE,
+   SwiGLU MLP (gate and up as one fused weight), untied embedding and head, no biases (the paper's
+   architecture section, with the variants the paper adds beyond a plain block left out). */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
+  float rms_eps; /* fp32 value, e.g. RN32(1e-5) */
+} canon_model_cfg;
+
+/* AdamW constants, each evaluated in double and rounded once to fp32 by the caller (R9). */
+typedef struct {
+  float lr, beta1, one_minus_beta1, beta2, one_minus_beta2, inv_bc1, inv_bc2, eps, decay_factor;
+} canon_adamw_consts;
+
+/* ------------------------------------------------------------------------------------------------ */
+/* GEMM (R1, R2).  C[i,j] = sum over k of A(i,k) B(k,j), bf16 operands, fp32 result.  The k terms are
+   cut into chunks of 32, each a left-to-right fma chain from +0 in ascending k, and the chunk partials
+   are combined by Algorithm 2 (binary carry, leftover blocks smallest first).  A(i,k) = a[i*lda + k]
+   (trans_a = 0) or a[k*lda + i] (trans_a = 1); B(k,j) = b[k*ldb + j] (trans_b = 0) or b[j*ldb + k]
+   (trans_b = 1); C row-major with leading dimension ldc >= n.  k = 0 writes +0; m = 0 or n = 0 is a
+   no-op.  Operands must not alias C. */
+canon_status canon_gemm(const canon_order* order, int32_t trans_a, int32_t trans_b, int64_t m, int64_t n,
+                        int64_t k, const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, float* c,
+                        int64_t ldc, void* stream);
+
+/* Strided batched form: matrix z of the batch uses a + z*stride_a, b + z*stride_b, c + z*stride_c
+   (strides in elements). */
+canon_status canon_gemm_strided_batched(const canon_order* order, int32_t trans_a, int32_t trans_b, int64_t m,
+                                        int64_t n, int64_t k, const uint16_t* a, int64_t lda, int64_t stride_a,
+                                        const uint16_t* b, int64_t ldb, int64_t stride_b, float* c, int64_t ldc,
+                                        int64_t stride_c, int64_t batch, void* stream);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* RMSNorm rows (R3; the architecture section's pre-norm RMSNorm without bias), x fp32 [rows, cols].
+   dir = CANON_FWD: y (bf16 [rows, cols]) = bf16(RN(RN(x*r)*g)) with r = CRdiv(1, CRsqrt(RN(ms + eps))),
+       ms = RN(R1(x*x) * RN(1/cols)); rstd (fp32 [rows]) = r.  dy, dx, dgain unused (may be NULL).
+   dir = CANON_BWD: inputs x, gain, rstd (from the forward), dy (fp32 [rows, cols]); outputs dx (fp32
+       [rows, cols]) and, if dgain != NULL, dgain (fp32 [cols]) = R1 over rows of RN(dy*RN(x*r)). */
+enum { CANON_FWD = 0, CANON_BWD = 1 };
+canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, int64_t cols, const float* x,
+                           const uint16_t* gain, float eps, uint16_t* y, float* rstd, const float* dy, float* dx,
+                           float* dgain, void* stream);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* Row softmax / cross-entropy (R5, R6; the audit section names the sums inside softmax among the
+   reductions that need a definite order).
+   mode = CANON_SOFTMAX_CAUSAL: x = fp32 raw scores [rows, cols] forming rows/cols stacked square
+       matrices; row r is query i = r mod cols.  score = RN(x*scale); keys j <= i only; out =
+       probabilities bf16 [rows, cols], +0 for masked keys.  targets, row_loss, mean_loss unused.
+   mode = CANON_XENT: x = bf16 logits [rows, cols = vocab]; targets int32 [rows] in [0, cols);
+       out = dlogits bf16 [rows, cols] = bf16(RN(RN(p - onehot) * inv_tokens)); row_loss fp32 [rows];
+       mean_loss (fp32 scalar, device) = RN(R1(row_loss) * inv_tokens).  Targets are checked on the
+       device; an out-of-range target makes the kernel write NaN to mean_loss. */
+enum { CANON_SOFTMAX_CAUSAL = 0, CANON_XENT = 1 };
+canon_status canon_softmax_xent(const canon_order* order, int32_t mode, int64_t rows, int64_t cols, const void* x,
+                                float scale, const int32_t* targets, float inv_tokens, uint16_t* out,
+                                float* row_loss, float* mean_loss, void* stream);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* Gradient plan (R7 = Algorithm 1 with Algorithm 2 over replicas, averages by reciprocal multiply).
+   grads: HOST array of N*accum device pointers (N = dp_shard*dp_replicate), rank-major, microbatch-
+   minor (grads[r*accum + k]); each points to n fp32 values.  out: n fp32 values.  This version fuses
+   up to 64 buffers in one pass (CANON_EUNSUPPORTED beyond). */
+canon_status canon_grad_accum(const canon_order* order, const canon_dp_plan* plan, int64_t n,
+                              const float* const* grads, float* out, void* stream);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* AdamW (R9): per tensor t of n_tensors (HOST arrays of device pointers and host sizes), widen the bf16
+   parameter, apply decoupled decay if decay_mask[t] (host) != 0, update fp32 m and v, bias-correct by
+   reciprocal multiply, divide by RN(CRsqrt(vh) + eps), round the parameter to bf16 once.  In place. */
+canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m,
+                         float* const* v, const float* const* grads, const uint8_t* decay_mask,
+                         const canon_adamw_consts* consts, void* stream);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* One decoder block, forward then backward, for `batch` sequences of cfg->seq tokens (T = batch*seq).
+   x, dy: fp32 [T, d_model] (block input, gradient of the block output).  w: HOST array of the six bf16
+   block tensors in the order attn_norm [d], w_qkv [3d, d], w_o [d, d], ffn_norm [d], w_gate_up [2F, d]
+   (gate rows first), w_down [d, F].  rope_cos/rope_sin: fp32 [seq, head_dim/2].  Outputs: y (block
+   output), dx (input gradient), dw: HOST array of six fp32 gradient buffers shaped like w. */
+canon_status canon_block_fwd_bwd(const canon_order* order, const canon_model_cfg* cfg, int32_t batch,
+                                 const float* x, const float* dy, const uint16_t* const* w, const float* rope_cos,
+                                 const float* rope_sin, float* y, float* dx, float* const* dw, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+size_t canon_block_workspace_bytes(const canon_model_cfg* cfg, int32_t batch);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* One training step (Algorithm 1 on one device).  For each virtual rank r in mesh order and each of its
+   `accum` microbatches (R12: rank r owns windows m with m mod N == r, micro_seqs consecutive ones per
+   microbatch), run forward and backward of the whole model, then reduce the gradients and the
+   microbatch losses through the plan and apply AdamW (R9).
+   params, m, v: HOST arrays of n = 3 + 6*n_layers device pointers in the declared order: embed [V, d];
+   per layer attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down; final_norm [d]; head [V, d].  params
+   (bf16), m and v (fp32) are updated in place.  windows: device int32 [M, seq+1], M = N*accum*
+   micro_seqs, each token in [0, vocab) (checked on the device: an out-of-range token makes the loss
+   NaN and leaves the parameters unchanged).  loss_out: device fp32 scalar.  grads_out: NULL, or a HOST
+   array of n device fp32 buffers that receive the reduced gradient.  step_t is informational (the
+   bias corrections come in consts). */
+canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, const canon_dp_plan* plan,
+                        uint16_t* const* params, float* const* m, float* const* v, int32_t step_t,
+                        const int32_t* windows, const float* rope_cos, const float* rope_sin,
+                        const canon_adamw_consts* consts, void* workspace, size_t workspace_bytes,
+                        float* loss_out, float* const* grads_out, void* stream);
+size_t canon_step_workspace_bytes(const canon_model_cfg* cfg, const canon_dp_plan* plan);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
+   the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,
+   10 bf16 round trip.  a, b, c, out: device fp32 [n] (b, c may be NULL when unused). */
+canon_status canon_devmath(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
+                           void* stream);
+
+const char* canon_status_str(canon_status s);
+int32_t canon_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

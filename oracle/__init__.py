@@ -181,16 +181,16 @@ def softmax_causal(raw: np.ndarray, scale: float) -> np.ndarray:
     return p
 
 
-def xent(logits: np.ndarray, targets: np.ndarray, inv_tokens: float):
+def xent(logits: np.ndarray, targets: np.ndarray, inv_tokens: float, want_dlogits: bool = True):
     logits = np.ascontiguousarray(logits, dtype=np.uint16)
     targets = np.ascontiguousarray(targets, dtype=np.int32)
     rows, vocab = logits.shape
-    dl = np.empty((rows, vocab), dtype=np.uint16)
+    dl = np.empty((rows, vocab) if want_dlogits else (1,), dtype=np.uint16)
     rl = np.empty(rows, dtype=np.float32)
     ml = ctypes.c_float(0)
-    _check(_load().cref_xent(rows, vocab, _p(logits), _p(targets), inv_tokens, _p(dl), _p(rl),
-                             ctypes.addressof(ml)))
-    return dl, rl, np.float32(ml.value)
+    _check(_load().cref_xent(rows, vocab, _p(logits), _p(targets), inv_tokens, _p(dl) if want_dlogits else None,
+                             _p(rl), ctypes.addressof(ml)))
+    return (dl if want_dlogits else None), rl, np.float32(ml.value)
 
 
 def grad_accum(grads, accum: int, dp_shard: int, dp_replicate: int) -> np.ndarray:

@@ -1,0 +1,183 @@
+"""ctypes binding of libcanon (include/canon.h): argument marshalling only.
+
+Every computation runs in the HIP library; this module passes device pointers, sizes and the current
+HIP stream, and raises on a non-OK status.  There is no fallback: if the library is not built, loading
+fails with an error.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libcanon.so")
+
+OK, EINVAL, EUNSUPPORTED, EDEVICE, EWORKSPACE = 0, -1, -2, -3, -4
+FWD, BWD = 0, 1
+SOFTMAX_CAUSAL, XENT = 0, 1
+
+
+class CanonError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {_lib().canon_status_str(status).decode()} ({status})")
+
+
+class Order(ctypes.Structure):
+    _fields_ = [("version", ctypes.c_int32), ("chunk", ctypes.c_int32), ("tree", ctypes.c_int32),
+                ("ftz", ctypes.c_int32)]
+
+
+class DPPlan(ctypes.Structure):
+    _fields_ = [("accum", ctypes.c_int32), ("dp_shard", ctypes.c_int32), ("dp_replicate", ctypes.c_int32)]
+
+
+class ModelCfg(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float)]
+
+
+class AdamWConsts(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in ("lr", "beta1", "one_minus_beta1", "beta2", "one_minus_beta2",
+                                              "inv_bc1", "inv_bc2", "eps", "decay_factor")]
+
+
+ORDER_V1 = Order(1, 32, 0, 1)
+_L = None
+
+
+def _lib():
+    global _L
+    if _L is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+        sigs = {
+            "canon_gemm": (i32, [vp, i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]),
+            "canon_gemm_strided_batched": (i32, [vp, i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64,
+                                                 i64, i64, vp]),
+            "canon_rownorm": (i32, [vp, i32, i64, i64, vp, vp, f32, vp, vp, vp, vp, vp, vp]),
+            "canon_softmax_xent": (i32, [vp, i32, i64, i64, vp, f32, vp, f32, vp, vp, vp, vp]),
+            "canon_grad_accum": (i32, [vp, vp, i64, vp, vp, vp]),
+            "canon_adamw": (i32, [i64, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "canon_block_fwd_bwd": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+            "canon_block_workspace_bytes": (sz, [vp, i32]),
+            "canon_step": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp, vp, vp]),
+            "canon_step_workspace_bytes": (sz, [vp, vp]),
+            "canon_devmath": (i32, [i32, i64, vp, vp, vp, vp, vp]),
+            "canon_status_str": (ctypes.c_char_p, [i32]),
+            "canon_version": (i32, []),
+        }
+        for name, (res, args) in sigs.items():
+            fn = getattr(lib, name)
+            fn.restype, fn.argtypes = res, args
+        _L = lib
+    return _L
+
+
+def lib():
+    return _lib()
+
+
+def _check(st: int, where: str):
+    if st != OK:
+        raise CanonError(st, where)
+
+
+def _ptr(t) -> int:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    assert t.is_cuda and t.is_contiguous(), "device tensors must be contiguous CUDA/HIP tensors"
+    return t.data_ptr()
+
+
+def _ptrs(ts):
+    return (ctypes.c_void_p * len(ts))(*[_ptr(t) for t in ts])
+
+
+def _stream(stream=None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+# ---- entry points (same names as the C ABI, without the prefix) -------------------------------------
+
+def gemm(m, n, k, a, lda, b, ldb, c, ldc, trans_a=0, trans_b=0, order=ORDER_V1, stream=None):
+    _check(_lib().canon_gemm(ctypes.byref(order), int(trans_a), int(trans_b), m, n, k, _ptr(a), lda, _ptr(b), ldb,
+                             _ptr(c), ldc, _stream(stream)), "canon_gemm")
+
+
+def gemm_strided_batched(m, n, k, a, lda, stride_a, b, ldb, stride_b, c, ldc, stride_c, batch, trans_a=0, trans_b=0,
+                         order=ORDER_V1, stream=None):
+    _check(_lib().canon_gemm_strided_batched(ctypes.byref(order), int(trans_a), int(trans_b), m, n, k, _ptr(a), lda,
+                                             stride_a, _ptr(b), ldb, stride_b, _ptr(c), ldc, stride_c, batch,
+                                             _stream(stream)), "canon_gemm_strided_batched")
+
+
+def rownorm(direction, rows, cols, x, gain, eps, y=None, rstd=None, dy=None, dx=None, dgain=None, order=ORDER_V1,
+            stream=None):
+    _check(_lib().canon_rownorm(ctypes.byref(order), direction, rows, cols, _ptr(x), _ptr(gain), eps, _ptr(y),
+                                _ptr(rstd), _ptr(dy), _ptr(dx), _ptr(dgain), _stream(stream)), "canon_rownorm")
+
+
+def softmax_xent(mode, rows, cols, x, out, scale=1.0, targets=None, inv_tokens=1.0, row_loss=None, mean_loss=None,
+                 order=ORDER_V1, stream=None):
+    _check(_lib().canon_softmax_xent(ctypes.byref(order), mode, rows, cols, _ptr(x), scale, _ptr(targets),
+                                     inv_tokens, _ptr(out), _ptr(row_loss), _ptr(mean_loss), _stream(stream)),
+           "canon_softmax_xent")
+
+
+def grad_accum(plan: DPPlan, n, grads, out, order=ORDER_V1, stream=None):
+    _check(_lib().canon_grad_accum(ctypes.byref(order), ctypes.byref(plan), n, _ptrs(grads), _ptr(out),
+                                   _stream(stream)), "canon_grad_accum")
+
+
+def adamw(params, m, v, grads, decay_mask, consts: AdamWConsts, stream=None):
+    n = len(params)
+    sizes = (ctypes.c_int64 * n)(*[p.numel() for p in params])
+    mask = (ctypes.c_uint8 * n)(*[int(x) for x in decay_mask])
+    _check(_lib().canon_adamw(n, sizes, _ptrs(params), _ptrs(m), _ptrs(v), _ptrs(grads), mask, ctypes.byref(consts),
+                              _stream(stream)), "canon_adamw")
+
+
+def block_workspace_bytes(cfg: ModelCfg, batch: int) -> int:
+    return int(_lib().canon_block_workspace_bytes(ctypes.byref(cfg), batch))
+
+
+def block_fwd_bwd(cfg: ModelCfg, batch, x, dy, w, rope_cos, rope_sin, y, dx, dw, workspace, order=ORDER_V1,
+                  stream=None):
+    _check(_lib().canon_block_fwd_bwd(ctypes.byref(order), ctypes.byref(cfg), batch, _ptr(x), _ptr(dy), _ptrs(w),
+                                      _ptr(rope_cos), _ptr(rope_sin), _ptr(y), _ptr(dx), _ptrs(dw), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)),
+           "canon_block_fwd_bwd")
+
+
+def step_workspace_bytes(cfg: ModelCfg, plan: DPPlan) -> int:
+    return int(_lib().canon_step_workspace_bytes(ctypes.byref(cfg), ctypes.byref(plan)))
+
+
+def step(cfg: ModelCfg, plan: DPPlan, params, m, v, windows, rope_cos, rope_sin, consts: AdamWConsts, workspace,
+         loss_out, grads_out=None, step_t=1, order=ORDER_V1, stream=None):
+    _check(_lib().canon_step(ctypes.byref(order), ctypes.byref(cfg), ctypes.byref(plan), _ptrs(params), _ptrs(m),
+                             _ptrs(v), step_t, _ptr(windows), _ptr(rope_cos), _ptr(rope_sin), ctypes.byref(consts),
+                             _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(loss_out),
+                             _ptrs(grads_out) if grads_out is not None else None, _stream(stream)), "canon_step")
+
+
+DEVMATH_OPS = {"add": 0, "sub": 1, "mul": 2, "fma": 3, "div": 4, "sqrt": 5, "exp": 6, "log": 7, "sigmoid": 8,
+               "silu": 9, "bf16": 10}
+
+
+def devmath(op: str, n, a, b=None, c=None, out=None, stream=None):
+    _check(_lib().canon_devmath(DEVMATH_OPS[op], n, _ptr(a), _ptr(b), _ptr(c), _ptr(out), _stream(stream)),
+           "canon_devmath")
+
+
+def version() -> int:
+    return int(_lib().canon_version())

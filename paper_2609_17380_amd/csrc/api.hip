@@ -1,0 +1,622 @@
+// api.hip - the C ABI of libcanon: argument validation, workspace layout and the host-side orchestration
+// of the decoder block and of the replayed step (Algorithm 1 over virtual ranks, then AdamW).
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <string.h>
+
+#include <vector>
+
+#include "canon.h"
+#include "canon_internal.h"
+
+using namespace canon;
+
+namespace {
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+canon_status check_order(const canon_order* o) {
+  if (!o) return CANON_EINVAL;
+  if (o->version != 1 || o->chunk != 32 || o->tree != CANON_TREE_BINARY_CARRY || o->ftz != 1)
+    return CANON_EUNSUPPORTED;
+  return CANON_OK;
+}
+
+canon_status dev(hipError_t e) { return e == hipSuccess ? CANON_OK : CANON_EDEVICE; }
+
+#define TRY(expr)                                  \
+  do {                                             \
+    hipError_t _e = (expr);                        \
+    if (_e != hipSuccess) return CANON_EDEVICE;    \
+  } while (0)
+
+GemmArgs mk(int ta, int tb, int64_t m, int64_t n, int64_t k, const uint16_t* a, int64_t lda, const uint16_t* b,
+            int64_t ldb, void* c, int64_t ldc, int out_bf16 = 0) {
+  GemmArgs g;
+  memset(&g, 0, sizeof(g));
+  g.a = a; g.b = b; g.c = c;
+  g.m = m; g.n = n; g.k = k; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
+  g.nb2 = 1; g.batch = 1;
+  g.trans_a = ta; g.trans_b = tb; g.out_bf16 = out_bf16;
+  g.kmode = KMODE_FULL; g.tri_lower = 0;
+  return g;
+}
+
+// K limit of the register fold (chunk count must stay below 2^levels)
+bool gemm_k_supported(int64_t k) { return ((k + 31) / 32) < (int64_t(1) << gemm_max_levels()); }
+
+// Bump allocator over the caller's workspace (base == nullptr: size query only).
+struct Carver {
+  char* base;
+  size_t off = 0;
+  explicit Carver(void* b) : base((char*)b) {}
+  template <class T>
+  T* take(int64_t n) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? (T*)(base + off) : nullptr;
+    off += sizeof(T) * (size_t)(n > 0 ? n : 1);
+    return p;
+  }
+};
+
+struct Dims {
+  int64_t B, S, T, d, H, hd, F, V;
+  float eps, scale;
+};
+
+float attn_scale(int64_t hd) {
+  if (hd == 128) {
+    uint32_t u = 0x3DB504F3u;  // RN32(1/sqrt(128))
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+  }
+  return (float)(1.0 / sqrt((double)hd));
+}
+
+Dims dims_of(const canon_model_cfg* c, int64_t B) {
+  Dims D;
+  D.B = B; D.S = c->seq; D.T = B * c->seq; D.d = c->d_model; D.H = c->n_heads; D.hd = c->head_dim;
+  D.F = c->d_ffn; D.V = c->vocab; D.eps = c->rms_eps; D.scale = attn_scale(c->head_dim);
+  return D;
+}
+
+bool cfg_ok(const canon_model_cfg* c) {
+  return c && c->n_layers >= 1 && c->d_model > 0 && c->n_heads > 0 && c->head_dim > 0 && (c->head_dim % 2) == 0 &&
+         (int64_t)c->n_heads * c->head_dim == c->d_model && c->d_ffn > 0 && c->vocab > 0 && c->seq > 0 &&
+         c->micro_seqs > 0 && gemm_k_supported(c->vocab) && gemm_k_supported((int64_t)c->seq * c->micro_seqs) &&
+         gemm_k_supported(2 * (int64_t)c->d_ffn) && gemm_k_supported(3 * (int64_t)c->d_model);
+}
+
+// activations a block saves for its backward pass
+struct LayerSave {
+  uint16_t *xn, *q, *k, *v, *P, *O, *hn, *a;
+  float *rstd1, *h, *rstd2, *gu;
+};
+
+void carve_save(Carver& cv, const Dims& D, LayerSave& s) {
+  const int64_t T = D.T, d = D.d;
+  s.xn = cv.take<uint16_t>(T * d);
+  s.rstd1 = cv.take<float>(T);
+  s.q = cv.take<uint16_t>(T * d);
+  s.k = cv.take<uint16_t>(T * d);
+  s.v = cv.take<uint16_t>(T * d);
+  s.P = cv.take<uint16_t>(D.B * D.H * D.S * D.S);
+  s.O = cv.take<uint16_t>(T * d);
+  s.h = cv.take<float>(T * d);
+  s.hn = cv.take<uint16_t>(T * d);
+  s.rstd2 = cv.take<float>(T);
+  s.gu = cv.take<float>(T * 2 * D.F);
+  s.a = cv.take<uint16_t>(T * D.F);
+}
+
+// transient buffers shared by all layers
+struct Scratch {
+  float *qkv, *scores, *tmp_d, *da, *dtmp, *dtmp2, *dh, *dq, *dk, *Dv;
+  uint16_t *dy_b, *dgu, *dO, *dS, *dqkv;
+};
+
+void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
+  const int64_t T = D.T, d = D.d;
+  s.qkv = cv.take<float>(T * 3 * d);
+  s.scores = cv.take<float>(D.B * D.H * D.S * D.S);
+  s.tmp_d = cv.take<float>(T * d);
+  s.da = cv.take<float>(T * D.F);
+  s.dtmp = cv.take<float>(T * d);
+  s.dtmp2 = cv.take<float>(T * d);
+  s.dh = cv.take<float>(T * d);
+  s.dq = cv.take<float>(T * d);
+  s.dk = cv.take<float>(T * d);
+  s.Dv = cv.take<float>(D.B * D.H * D.S);
+  s.dy_b = cv.take<uint16_t>(T * d);
+  s.dgu = cv.take<uint16_t>(T * 2 * D.F);
+  s.dO = cv.take<uint16_t>(T * d);
+  s.dS = cv.take<uint16_t>(D.B * D.H * D.S * D.S);
+  s.dqkv = cv.take<uint16_t>(T * 3 * d);
+}
+
+hipError_t gemm(const GemmArgs& g, hipStream_t s) { return gemm_launch(g, s); }
+
+// per-head batched GEMM over (b, h): A/B/C offsets b*s?1 + h*s?2
+GemmArgs batched(GemmArgs g, const Dims& D, int64_t sa1, int64_t sa2, int64_t sb1, int64_t sb2, int64_t sc1,
+                 int64_t sc2) {
+  g.batch = D.B * D.H; g.nb2 = D.H;
+  g.sa1 = sa1; g.sa2 = sa2; g.sb1 = sb1; g.sb2 = sb2; g.sc1 = sc1; g.sc2 = sc2;
+  return g;
+}
+
+// Forward of one block: x (input, kept by the caller) -> y; activations saved in sv.
+canon_status block_forward(const Dims& D, const uint16_t* const* w, const float* cosT, const float* sinT,
+                           const float* x, LayerSave& sv, Scratch& sc, float* y, hipStream_t s) {
+  const int64_t T = D.T, d = D.d, S = D.S, H = D.H, hd = D.hd, F = D.F;
+  TRY(rownorm_fwd_launch(T, d, x, w[0], D.eps, sv.xn, sv.rstd1, s));
+  TRY(gemm(mk(0, 1, T, 3 * d, d, sv.xn, d, w[1], d, sc.qkv, 3 * d), s));
+  TRY(rope_qkv_launch(D.B, S, H, hd, sc.qkv, cosT, sinT, sv.q, sv.k, sv.v, s));
+  {  // raw scores Q K^T, lower-triangle tiles only
+    GemmArgs g = batched(mk(0, 1, S, S, hd, sv.q, hd, sv.k, hd, sc.scores, S), D, H * S * hd, S * hd, H * S * hd,
+                         S * hd, H * S * S, S * S);
+    g.tri_lower = 1;
+    TRY(gemm(g, s));
+  }
+  TRY(softmax_causal_launch(D.B * H * S, S, sc.scores, D.scale, sv.P, s));
+  {  // O = P V (keys beyond the tile's last query are masked chunks), bf16 into [T, d]
+    GemmArgs g = batched(mk(0, 0, S, hd, S, sv.P, S, sv.v, hd, sv.O, d, 1), D, H * S * S, S * S, H * S * hd, S * hd,
+                         S * d, hd);
+    g.kmode = KMODE_TRAIL;
+    TRY(gemm(g, s));
+  }
+  TRY(gemm(mk(0, 1, T, d, d, sv.O, d, w[2], d, sc.tmp_d, d), s));
+  TRY(add_f32_launch(T * d, x, sc.tmp_d, sv.h, s));
+  TRY(rownorm_fwd_launch(T, d, sv.h, w[3], D.eps, sv.hn, sv.rstd2, s));
+  TRY(gemm(mk(0, 1, T, 2 * F, d, sv.hn, d, w[4], d, sv.gu, 2 * F), s));
+  TRY(swiglu_fwd_launch(T, F, sv.gu, sv.a, s));
+  TRY(gemm(mk(0, 1, T, d, F, sv.a, F, w[5], F, sc.tmp_d, d), s));
+  TRY(add_f32_launch(T * d, sv.h, sc.tmp_d, y, s));
+  return CANON_OK;
+}
+
+// Backward of one block: dy (gradient of the block output) -> dx; weight gradients into dw[0..5].
+canon_status block_backward(const Dims& D, const uint16_t* const* w, const float* cosT, const float* sinT,
+                            const float* x, const LayerSave& sv, Scratch& sc, const float* dy, float* dx,
+                            float* const* dw, hipStream_t s) {
+  const int64_t T = D.T, d = D.d, S = D.S, H = D.H, hd = D.hd, F = D.F;
+  TRY(cast_bf16_launch(T * d, dy, sc.dy_b, s));
+  TRY(gemm(mk(1, 0, d, F, T, sc.dy_b, d, sv.a, F, dw[5], F), s));        // dW_down = dy^T a
+  TRY(gemm(mk(0, 0, T, F, d, sc.dy_b, d, w[5], F, sc.da, F), s));        // da = dy W_down
+  TRY(swiglu_bwd_launch(T, F, sv.gu, sc.da, sc.dgu, s));
+  TRY(gemm(mk(1, 0, 2 * F, d, T, sc.dgu, 2 * F, sv.hn, d, dw[4], d), s)); // dW_gate_up = dgu^T hn
+  TRY(gemm(mk(0, 0, T, d, 2 * F, sc.dgu, 2 * F, w[4], d, sc.dtmp, d), s)); // dhn = dgu W_gate_up
+  TRY(rownorm_bwd_launch(T, d, sv.h, w[3], sv.rstd2, sc.dtmp, sc.dtmp2, dw[3], s));
+  TRY(add_f32_launch(T * d, dy, sc.dtmp2, sc.dh, s));                     // dh = dy + norm path
+  TRY(cast_bf16_launch(T * d, sc.dh, sc.dy_b, s));
+  TRY(gemm(mk(1, 0, d, d, T, sc.dy_b, d, sv.O, d, dw[2], d), s));        // dW_o = dh^T O
+  TRY(gemm(mk(0, 0, T, d, d, sc.dy_b, d, w[2], d, sc.dO, d, 1), s));     // dO = dh W_o (bf16)
+  TRY(attn_rowdot_launch(D.B, H, S, hd, sc.dO, sv.O, d, sc.Dv, s));      // D = rowsum(dO * O)
+  {  // dP = dO V^T, lower-triangle tiles
+    GemmArgs g = batched(mk(0, 1, S, S, hd, sc.dO, d, sv.v, hd, sc.scores, S), D, S * d, hd, H * S * hd, S * hd,
+                         H * S * S, S * S);
+    g.tri_lower = 1;
+    TRY(gemm(g, s));
+  }
+  TRY(attn_dS_launch(D.B * H, S, sv.P, sc.scores, sc.Dv, D.scale, sc.dS, s));
+  {  // dQ = dS K (over keys)
+    GemmArgs g = batched(mk(0, 0, S, hd, S, sc.dS, S, sv.k, hd, sc.dq, d), D, H * S * S, S * S, H * S * hd, S * hd,
+                         S * d, hd);
+    g.kmode = KMODE_TRAIL;
+    TRY(gemm(g, s));
+  }
+  {  // dK = dS^T Q (over queries)
+    GemmArgs g = batched(mk(1, 0, S, hd, S, sc.dS, S, sv.q, hd, sc.dk, d), D, H * S * S, S * S, H * S * hd, S * hd,
+                         S * d, hd);
+    g.kmode = KMODE_LEAD;
+    TRY(gemm(g, s));
+  }
+  {  // dV = P^T dO (over queries), bf16 into dqkv columns [2d, 3d)
+    GemmArgs g = batched(mk(1, 0, S, hd, S, sv.P, S, sc.dO, d, sc.dqkv + 2 * d, 3 * d, 1), D, H * S * S, S * S, S * d,
+                         hd, S * 3 * d, hd);
+    g.kmode = KMODE_LEAD;
+    TRY(gemm(g, s));
+  }
+  TRY(rope_bwd_launch(D.B, S, H, hd, sc.dq, sc.dk, cosT, sinT, sc.dqkv, s));
+  TRY(gemm(mk(1, 0, 3 * d, d, T, sc.dqkv, 3 * d, sv.xn, d, dw[1], d), s)); // dW_qkv = dqkv^T xn
+  TRY(gemm(mk(0, 0, T, d, 3 * d, sc.dqkv, 3 * d, w[1], d, sc.dtmp, d), s)); // dxn = dqkv W_qkv
+  TRY(rownorm_bwd_launch(T, d, x, w[0], sv.rstd1, sc.dtmp, sc.dtmp2, dw[0], s));
+  TRY(add_f32_launch(T * d, sc.dh, sc.dtmp2, dx, s));
+  return CANON_OK;
+}
+
+// ---- step layout ---------------------------------------------------------------------------------
+int bit_length(int64_t x) {
+  int b = 0;
+  while ((int64_t(1) << b) <= x) ++b;
+  return b;
+}
+
+void tensor_sizes(const canon_model_cfg* c, std::vector<int64_t>& sz, std::vector<uint8_t>& decay) {
+  const int64_t d = c->d_model, F = c->d_ffn, V = c->vocab;
+  sz.clear(); decay.clear();
+  sz.push_back(V * d); decay.push_back(0);
+  for (int l = 0; l < c->n_layers; ++l) {
+    int64_t s6[6] = {d, 3 * d * d, d * d, d, 2 * F * d, d * F};
+    uint8_t d6[6] = {0, 1, 1, 0, 1, 1};
+    for (int i = 0; i < 6; ++i) { sz.push_back(s6[i]); decay.push_back(d6[i]); }
+  }
+  sz.push_back(d); decay.push_back(0);
+  sz.push_back(V * d); decay.push_back(1);
+}
+
+struct StepLayout {
+  std::vector<LayerSave> saves;
+  std::vector<float*> xs;  // residual stream: xs[0] = embedding output, xs[l+1] = block l output
+  Scratch sc;
+  uint16_t *xf, *logits, *dlogits;
+  float *rstdf, *row_loss, *dxf, *dxA, *dxB;
+  int32_t *win, *lab, *bad;
+  void* embed_scratch;
+  float* grad;            // one microbatch's gradient, all tensors
+  float* g_r;             // rank accumulator (accum > 1)
+  std::vector<float*> pool;  // inner + fold stack buffers
+  float* loss_mb;         // [1]
+  float* loss_gr;         // [1]
+  std::vector<float*> loss_pool;
+};
+
+void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, int64_t P, StepLayout& L) {
+  Dims D = dims_of(c, c->micro_seqs);
+  L.saves.resize(c->n_layers);
+  for (auto& s : L.saves) carve_save(cv, D, s);
+  L.xs.resize(c->n_layers + 1);
+  for (auto& x : L.xs) x = cv.take<float>(D.T * D.d);
+  carve_scratch(cv, D, L.sc);
+  L.xf = cv.take<uint16_t>(D.T * D.d);
+  L.rstdf = cv.take<float>(D.T);
+  L.logits = cv.take<uint16_t>(D.T * D.V);
+  L.dlogits = cv.take<uint16_t>(D.T * D.V);
+  L.row_loss = cv.take<float>(D.T);
+  L.dxf = cv.take<float>(D.T * D.d);
+  L.dxA = cv.take<float>(D.T * D.d);
+  L.dxB = cv.take<float>(D.T * D.d);
+  L.win = cv.take<int32_t>((int64_t)c->micro_seqs * (c->seq + 1));
+  L.lab = cv.take<int32_t>(D.T);
+  L.bad = cv.take<int32_t>(1);
+  L.embed_scratch = cv.take<char>((int64_t)embed_bwd_scratch_bytes(D.T));
+  L.grad = cv.take<float>(P);
+  L.g_r = p->accum > 1 ? cv.take<float>(P) : nullptr;
+  const int nbuf = bit_length(p->dp_replicate) + 1;
+  L.pool.resize(nbuf);
+  for (auto& b : L.pool) b = cv.take<float>(P);
+  L.loss_mb = cv.take<float>(1);
+  L.loss_gr = cv.take<float>(1);
+  L.loss_pool.resize(nbuf);
+  for (auto& b : L.loss_pool) b = cv.take<float>(1);
+}
+
+// Algorithm 1 driven from the host over device buffers of n floats (the gradient, or the loss with n = 1).
+struct PlanRun {
+  int64_t n;
+  canon_dp_plan p;
+  float inv_accum, inv_shard, inv_rep;
+  float* g_r;                   // nullptr when accum == 1 (the microbatch buffer is reused in place)
+  std::vector<float*> free_bufs;
+  std::vector<std::pair<int, float*>> stack;  // (level, buffer) of Algorithm 2
+  float* inner = nullptr;
+
+  PlanRun(int64_t n_, const canon_dp_plan& p_, float* gr, const std::vector<float*>& pool) : n(n_), p(p_), g_r(gr) {
+    inv_accum = (float)(1.0 / p.accum);
+    inv_shard = (float)(1.0 / p.dp_shard);
+    inv_rep = (float)(1.0 / p.dp_replicate);
+    free_bufs = pool;
+  }
+  float* take() {
+    float* b = free_bufs.back();
+    free_bufs.pop_back();
+    return b;
+  }
+  // microbatch k of rank r produced `grad` (may be overwritten when accum == 1)
+  hipError_t microbatch(int r, int k, float* grad, hipStream_t s) {
+    float* gr = g_r ? g_r : grad;
+    hipError_t e = plan_accum_launch(n, grad, inv_accum, g_r ? (k == 0) : 1, gr, s);
+    if (e != hipSuccess || k != p.accum - 1) return e;
+    const int shard = r % p.dp_shard;
+    if (shard == 0) inner = take();
+    e = plan_shard_launch(n, gr, shard == 0, inner, s);
+    if (e != hipSuccess || shard != p.dp_shard - 1) return e;
+    e = plan_scale_launch(n, inner, inv_shard, inner, s);
+    int level = 0;
+    float* part = inner;
+    while (e == hipSuccess && !stack.empty() && stack.back().first == level) {
+      float* lower = stack.back().second;
+      e = plan_merge_launch(n, lower, part, s);  // part = lower + part
+      free_bufs.push_back(lower);
+      stack.pop_back();
+      ++level;
+    }
+    stack.push_back({level, part});
+    inner = nullptr;
+    return e;
+  }
+  // Result of Algorithm 2 times 1/dp_replicate; returns the buffer holding g
+  float* finish(hipStream_t s, hipError_t* err) {
+    float* acc = stack.back().second;
+    hipError_t e = hipSuccess;
+    for (int i = (int)stack.size() - 2; i >= 0 && e == hipSuccess; --i) e = plan_merge_launch(n, stack[i].second, acc, s);
+    if (e == hipSuccess) e = plan_scale_launch(n, acc, inv_rep, acc, s);
+    *err = e;
+    return acc;
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+const char* canon_status_str(canon_status s) {
+  switch (s) {
+    case CANON_OK: return "ok";
+    case CANON_EINVAL: return "invalid argument";
+    case CANON_EUNSUPPORTED: return "unsupported by this version";
+    case CANON_EDEVICE: return "device error";
+    case CANON_EWORKSPACE: return "workspace too small";
+  }
+  return "unknown status";
+}
+
+int32_t canon_version(void) { return 1; }
+
+canon_status canon_gemm_strided_batched(const canon_order* order, int32_t trans_a, int32_t trans_b, int64_t m,
+                                        int64_t n, int64_t k, const uint16_t* a, int64_t lda, int64_t stride_a,
+                                        const uint16_t* b, int64_t ldb, int64_t stride_b, float* c, int64_t ldc,
+                                        int64_t stride_c, int64_t batch, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (m < 0 || n < 0 || k < 0 || batch < 0) return CANON_EINVAL;
+  if (m == 0 || n == 0 || batch == 0) return CANON_OK;
+  if (!c || (k > 0 && (!a || !b))) return CANON_EINVAL;
+  if (lda < (trans_a ? m : k) || ldb < (trans_b ? k : n) || ldc < n || lda < 1 || ldb < 1) return CANON_EINVAL;
+  if (batch > 65535) return CANON_EUNSUPPORTED;
+  if (!gemm_k_supported(k)) return CANON_EUNSUPPORTED;
+  const int64_t tiles = ((m + 63) / 64) * ((n + 127) / 128);
+  if (tiles > 0x7FFFFFFF) return CANON_EUNSUPPORTED;
+  GemmArgs g = mk(trans_a ? 1 : 0, trans_b ? 1 : 0, m, n, k, a, lda, b, ldb, c, ldc);
+  g.batch = batch; g.nb2 = 1; g.sa1 = stride_a; g.sb1 = stride_b; g.sc1 = stride_c;
+  return dev(gemm_launch(g, as_stream(stream)));
+}
+
+canon_status canon_gemm(const canon_order* order, int32_t trans_a, int32_t trans_b, int64_t m, int64_t n, int64_t k,
+                        const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, float* c, int64_t ldc,
+                        void* stream) {
+  return canon_gemm_strided_batched(order, trans_a, trans_b, m, n, k, a, lda, 0, b, ldb, 0, c, ldc, 0, 1, stream);
+}
+
+canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, int64_t cols, const float* x,
+                           const uint16_t* gain, float eps, uint16_t* y, float* rstd, const float* dy, float* dx,
+                           float* dgain, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (rows < 0 || cols < 1) return CANON_EINVAL;
+  if (cols > (int64_t(1) << 26) || rows > (int64_t(1) << 21)) return CANON_EUNSUPPORTED;
+  hipStream_t s = as_stream(stream);
+  if (dir == CANON_FWD) {
+    if (rows > 0 && (!x || !gain || !y || !rstd)) return CANON_EINVAL;
+    return dev(rownorm_fwd_launch(rows, cols, x, gain, eps, y, rstd, s));
+  }
+  if (dir == CANON_BWD) {
+    if (rows > 0 && (!x || !gain || !rstd || !dy || !dx)) return CANON_EINVAL;
+    return dev(rownorm_bwd_launch(rows, cols, x, gain, rstd, dy, dx, dgain, s));
+  }
+  return CANON_EINVAL;
+}
+
+canon_status canon_softmax_xent(const canon_order* order, int32_t mode, int64_t rows, int64_t cols, const void* x,
+                                float scale, const int32_t* targets, float inv_tokens, uint16_t* out,
+                                float* row_loss, float* mean_loss, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (rows < 0 || cols < 1) return CANON_EINVAL;
+  if (cols > (int64_t(1) << 26) || rows > (int64_t(1) << 31)) return CANON_EUNSUPPORTED;
+  hipStream_t s = as_stream(stream);
+  if (mode == CANON_SOFTMAX_CAUSAL) {
+    if (rows % cols != 0) return CANON_EINVAL;
+    if (rows > 0 && (!x || !out)) return CANON_EINVAL;
+    return dev(softmax_causal_launch(rows, cols, (const float*)x, scale, out, s));
+  }
+  if (mode == CANON_XENT) {
+    if (rows > 0 && (!x || !targets || !out || !row_loss)) return CANON_EINVAL;
+    if (rows > (int64_t(1) << 22)) return CANON_EUNSUPPORTED;
+    return dev(xent_launch(rows, cols, (const uint16_t*)x, targets, inv_tokens, out, row_loss, mean_loss, s));
+  }
+  return CANON_EINVAL;
+}
+
+canon_status canon_grad_accum(const canon_order* order, const canon_dp_plan* plan, int64_t n,
+                              const float* const* grads, float* out, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (!plan || plan->accum < 1 || plan->dp_shard < 1 || plan->dp_replicate < 1 || n < 0) return CANON_EINVAL;
+  const int64_t nb = (int64_t)plan->accum * plan->dp_shard * plan->dp_replicate;
+  if (nb > kMaxFusedBuffers) return CANON_EUNSUPPORTED;
+  if (n == 0) return CANON_OK;
+  if (!grads || !out) return CANON_EINVAL;
+  PlanPtrs pp;
+  memset(&pp, 0, sizeof(pp));
+  for (int64_t i = 0; i < nb; ++i) {
+    if (!grads[i]) return CANON_EINVAL;
+    pp.p[i] = grads[i];
+  }
+  return dev(grad_accum_fused_launch(plan->accum, plan->dp_shard, plan->dp_replicate, n, pp, out, as_stream(stream)));
+}
+
+canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m,
+                         float* const* v, const float* const* grads, const uint8_t* decay_mask,
+                         const canon_adamw_consts* consts, void* stream) {
+  if (n_tensors < 0 || !consts) return CANON_EINVAL;
+  if (n_tensors > 0 && (!sizes || !params || !m || !v || !grads || !decay_mask)) return CANON_EINVAL;
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    if (sizes[t] < 0) return CANON_EINVAL;
+    if (sizes[t] > 0 && (!params[t] || !m[t] || !v[t] || !grads[t])) return CANON_EINVAL;
+  }
+  const float c9[9] = {consts->lr, consts->beta1, consts->one_minus_beta1, consts->beta2, consts->one_minus_beta2,
+                       consts->inv_bc1, consts->inv_bc2, consts->eps, consts->decay_factor};
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    hipError_t e = adamw_launch(sizes[t], params[t], m[t], v[t], grads[t], decay_mask[t] != 0, c9, nullptr,
+                                as_stream(stream));
+    if (e != hipSuccess) return CANON_EDEVICE;
+  }
+  return CANON_OK;
+}
+
+canon_status canon_devmath(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
+                           void* stream) {
+  if (op < 0 || op > 10 || n < 0) return CANON_EINVAL;
+  if (n == 0) return CANON_OK;
+  if (!a || !out) return CANON_EINVAL;
+  if ((op <= 4 && !b) || (op == 3 && !c)) return CANON_EINVAL;
+  return dev(devmath_launch(op, n, a, b, c, out, as_stream(stream)));
+}
+
+size_t canon_block_workspace_bytes(const canon_model_cfg* cfg, int32_t batch) {
+  if (!cfg_ok(cfg) || batch < 1) return 0;
+  Dims D = dims_of(cfg, batch);
+  Carver cv(nullptr);
+  LayerSave sv;
+  Scratch sc;
+  carve_save(cv, D, sv);
+  carve_scratch(cv, D, sc);
+  return cv.off + 256;
+}
+
+canon_status canon_block_fwd_bwd(const canon_order* order, const canon_model_cfg* cfg, int32_t batch, const float* x,
+                                 const float* dy, const uint16_t* const* w, const float* rope_cos,
+                                 const float* rope_sin, float* y, float* dx, float* const* dw, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (!cfg_ok(cfg) || batch < 1 || !x || !dy || !w || !rope_cos || !rope_sin || !y || !dx || !dw)
+    return CANON_EINVAL;
+  for (int i = 0; i < 6; ++i)
+    if (!w[i] || !dw[i]) return CANON_EINVAL;
+  if ((int64_t)batch * cfg->n_heads > 65535) return CANON_EUNSUPPORTED;
+  const size_t need = canon_block_workspace_bytes(cfg, batch);
+  if (!workspace || workspace_bytes < need) return CANON_EWORKSPACE;
+  Dims D = dims_of(cfg, batch);
+  Carver cv(workspace);
+  LayerSave sv;
+  Scratch sc;
+  carve_save(cv, D, sv);
+  carve_scratch(cv, D, sc);
+  hipStream_t s = as_stream(stream);
+  st = block_forward(D, w, rope_cos, rope_sin, x, sv, sc, y, s);
+  if (st != CANON_OK) return st;
+  return block_backward(D, w, rope_cos, rope_sin, x, sv, sc, dy, dx, dw, s);
+}
+
+size_t canon_step_workspace_bytes(const canon_model_cfg* cfg, const canon_dp_plan* plan) {
+  if (!cfg_ok(cfg) || !plan || plan->accum < 1 || plan->dp_shard < 1 || plan->dp_replicate < 1) return 0;
+  std::vector<int64_t> sz;
+  std::vector<uint8_t> decay;
+  tensor_sizes(cfg, sz, decay);
+  int64_t P = 0;
+  for (int64_t v : sz) P += v;
+  Carver cv(nullptr);
+  StepLayout L;
+  carve_step(cv, cfg, plan, P, L);
+  return cv.off + 256;
+}
+
+canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, const canon_dp_plan* plan,
+                        uint16_t* const* params, float* const* m, float* const* v, int32_t step_t,
+                        const int32_t* windows, const float* rope_cos, const float* rope_sin,
+                        const canon_adamw_consts* consts, void* workspace, size_t workspace_bytes, float* loss_out,
+                        float* const* grads_out, void* stream) {
+  (void)step_t;
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (!cfg_ok(cfg) || !plan || plan->accum < 1 || plan->dp_shard < 1 || plan->dp_replicate < 1) return CANON_EINVAL;
+  if (!params || !m || !v || !windows || !rope_cos || !rope_sin || !consts || !loss_out) return CANON_EINVAL;
+  std::vector<int64_t> sz;
+  std::vector<uint8_t> decay;
+  tensor_sizes(cfg, sz, decay);
+  const int64_t nt = (int64_t)sz.size();
+  for (int64_t t = 0; t < nt; ++t)
+    if (!params[t] || !m[t] || !v[t] || (grads_out && !grads_out[t])) return CANON_EINVAL;
+  if ((int64_t)cfg->micro_seqs * cfg->n_heads > 65535) return CANON_EUNSUPPORTED;
+  std::vector<int64_t> off(nt + 1, 0);
+  for (int64_t t = 0; t < nt; ++t) off[t + 1] = off[t] + sz[t];
+  const int64_t P = off[nt];
+  const size_t need = canon_step_workspace_bytes(cfg, plan);
+  if (!workspace || workspace_bytes < need) return CANON_EWORKSPACE;
+
+  hipStream_t s = as_stream(stream);
+  Carver cv(workspace);
+  StepLayout L;
+  carve_step(cv, cfg, plan, P, L);
+  const Dims D = dims_of(cfg, cfg->micro_seqs);
+  const int R = plan->dp_shard * plan->dp_replicate;
+  const int64_t S1 = cfg->seq + 1, mb = cfg->micro_seqs;
+  const int64_t M = (int64_t)R * plan->accum * mb;
+  const float invT = (float)(1.0 / (double)D.T);
+
+  TRY(hipMemsetAsync(L.bad, 0, sizeof(int32_t), s));
+  TRY(token_check_launch(M * S1, windows, cfg->vocab, L.bad, s));
+
+  PlanRun gplan(P, *plan, L.g_r, L.pool);
+  PlanRun lplan(1, *plan, plan->accum > 1 ? L.loss_gr : nullptr, L.loss_pool);
+  const int nl = cfg->n_layers;
+  for (int r = 0; r < R; ++r) {
+    for (int k = 0; k < plan->accum; ++k) {
+      // R12: windows r + R*(k*mb + s), s < mb
+      for (int64_t si = 0; si < mb; ++si) {
+        const int64_t mw = r + (int64_t)R * (k * mb + si);
+        TRY(hipMemcpyAsync(L.win + si * S1, windows + mw * S1, sizeof(int32_t) * S1, hipMemcpyDeviceToDevice, s));
+      }
+      TRY(embed_gather_launch(mb, D.S, D.d, L.win, S1, params[0], D.V, L.xs[0], s));
+      TRY(labels_launch(mb, D.S, L.win, S1, L.lab, s));
+      for (int l = 0; l < nl; ++l) {
+        const uint16_t* w[6];
+        for (int i = 0; i < 6; ++i) w[i] = params[1 + 6 * l + i];
+        st = block_forward(D, w, rope_cos, rope_sin, L.xs[l], L.saves[l], L.sc, L.xs[l + 1], s);
+        if (st != CANON_OK) return st;
+      }
+      const int64_t i_fn = 1 + 6 * nl, i_head = 2 + 6 * nl;
+      TRY(rownorm_fwd_launch(D.T, D.d, L.xs[nl], params[i_fn], D.eps, L.xf, L.rstdf, s));
+      TRY(gemm(mk(0, 1, D.T, D.V, D.d, L.xf, D.d, params[i_head], D.d, L.logits, D.V, 1), s));
+      TRY(xent_launch(D.T, D.V, L.logits, L.lab, invT, L.dlogits, L.row_loss, L.loss_mb, s));
+      TRY(gemm(mk(1, 0, D.V, D.d, D.T, L.dlogits, D.V, L.xf, D.d, L.grad + off[i_head], D.d), s));
+      TRY(gemm(mk(0, 0, D.T, D.d, D.V, L.dlogits, D.V, params[i_head], D.d, L.dxf, D.d), s));
+      TRY(rownorm_bwd_launch(D.T, D.d, L.xs[nl], params[i_fn], L.rstdf, L.dxf, L.dxA, L.grad + off[i_fn], s));
+      float* dcur = L.dxA;
+      float* dnext = L.dxB;
+      for (int l = nl - 1; l >= 0; --l) {
+        const uint16_t* w[6];
+        float* dw[6];
+        for (int i = 0; i < 6; ++i) {
+          w[i] = params[1 + 6 * l + i];
+          dw[i] = L.grad + off[1 + 6 * l + i];
+        }
+        st = block_backward(D, w, rope_cos, rope_sin, L.xs[l], L.saves[l], L.sc, dcur, dnext, dw, s);
+        if (st != CANON_OK) return st;
+        float* t = dcur; dcur = dnext; dnext = t;
+      }
+      TRY(embed_bwd_launch(mb, D.S, D.d, L.win, S1, D.V, dcur, L.grad + off[0], L.embed_scratch, s));
+      TRY(gplan.microbatch(r, k, L.grad, s));
+      TRY(lplan.microbatch(r, k, L.loss_mb, s));
+    }
+  }
+  hipError_t e = hipSuccess;
+  float* g = gplan.finish(s, &e);
+  TRY(e);
+  float* lossv = lplan.finish(s, &e);
+  TRY(e);
+  TRY(hipMemcpyAsync(loss_out, lossv, sizeof(float), hipMemcpyDeviceToDevice, s));
+  TRY(set_nan_if_launch(L.bad, loss_out, s));
+  if (grads_out)
+    for (int64_t t = 0; t < nt; ++t)
+      TRY(hipMemcpyAsync(grads_out[t], g + off[t], sizeof(float) * sz[t], hipMemcpyDeviceToDevice, s));
+  const float c9[9] = {consts->lr, consts->beta1, consts->one_minus_beta1, consts->beta2, consts->one_minus_beta2,
+                       consts->inv_bc1, consts->inv_bc2, consts->eps, consts->decay_factor};
+  for (int64_t t = 0; t < nt; ++t)
+    TRY(adamw_launch(sz[t], params[t], m[t], v[t], g + off[t], decay[t], c9, L.bad, s));
+  return CANON_OK;
+}
+
+}  // extern "C"

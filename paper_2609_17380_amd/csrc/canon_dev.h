@@ -1,0 +1,129 @@
+// canon_dev.h - device-side numerics of CANON-v1 for gfx950.
+//
+// R0 (binary32, round to nearest even, subnormals flushed) is what gfx950 computes natively in flush mode:
+// this library is built with -fgpu-flush-denormals-to-zero, so every VALU and MFMA operation reads
+// subnormal inputs as signed zero and flushes a result whose rounding to 24 bits with unbounded exponent
+// is below 2^-126 (IEEE tininess after rounding).  Division and square root are the compiler's correctly
+// rounded sequences (-fhip-fp32-correctly-rounded-divide-sqrt).  -ffp-contract=off keeps every multiply
+// and add a separate rounding unless written as __builtin_fmaf.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace canon {
+
+constexpr int kChunk = 32;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  // exact widening; a subnormal bf16 is read as zero of its sign (R0 input rule)
+  uint32_t u = (uint32_t)h << 16;
+  if ((u & 0x7F800000u) == 0u) u &= 0x80000000u;
+  return __uint_as_float(u);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  // a subnormal input reads as zero of its sign; then round to nearest even on the 16 dropped bits
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0u) u &= 0x80000000u;
+  u = u + 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+// ---- cexp: Cody-Waite reduction by ln 2 (two parts), degree-7 Taylor polynomial (Horner, separate
+// multiply and add), exact scaling by 2^k.  Constants are the binary32 roundings of their definitions.
+constexpr float kLog2e = 0x1.715476p+0f;        // RN32(1/ln 2)              0x3FB8AA3B
+constexpr float kLn2Hi = 0x1.62e4p-1f;          // ln 2 cut to 15 bits       0x3F317200
+constexpr float kLn2Lo = 0x1.7f7d1cp-20f;       // RN32(ln 2 - kLn2Hi)       0x35BFBE8E
+constexpr float kInvFact2 = 0x1p-1f;            // 1/2!
+constexpr float kInvFact3 = 0x1.555556p-3f;     // RN32(1/3!)                0x3E2AAAAB
+constexpr float kInvFact4 = 0x1.555556p-5f;     // RN32(1/4!)                0x3D2AAAAB
+constexpr float kInvFact5 = 0x1.111112p-7f;     // RN32(1/5!)                0x3C088889
+constexpr float kInvFact6 = 0x1.6c16c2p-10f;    // RN32(1/6!)                0x3AB60B61
+constexpr float kInvFact7 = 0x1.a01a02p-13f;    // RN32(1/7!)                0x39500D01
+
+__device__ __forceinline__ float cexp(float x) {
+  float t = x * kLog2e;
+  float kf = __builtin_rintf(t);  // nearest integer, ties to even
+  if (kf > 127.0f) return __builtin_inff();
+  if (kf < -125.0f) return 0.0f;
+  float hi = kf * kLn2Hi;
+  float lo = kf * kLn2Lo;
+  float r = x - hi;
+  r = r - lo;
+  float p = kInvFact7;
+  p = p * r; p = p + kInvFact6;
+  p = p * r; p = p + kInvFact5;
+  p = p * r; p = p + kInvFact4;
+  p = p * r; p = p + kInvFact3;
+  p = p * r; p = p + kInvFact2;
+  p = p * r; p = p + 1.0f;
+  p = p * r; p = p + 1.0f;
+  int k = (int)kf;
+  float scale = __uint_as_float((uint32_t)(k + 127) << 23);
+  return p * scale;
+}
+
+// ---- clog: x = 2^e f, f in (sqrt(1/2), sqrt(2)]; s = (f-1)/(f+1); log f = 2 atanh(s) by the odd series
+// through s^11; result = e*ln2 (two parts) + log f.
+constexpr float kSqrt2 = 0x1.6a09e6p+0f;        // RN32(sqrt 2)              0x3FB504F3
+constexpr float kInv3 = 0x1.555556p-2f;         // RN32(1/3)                 0x3EAAAAAB
+constexpr float kInv5 = 0x1.99999ap-3f;         // RN32(1/5)                 0x3E4CCCCD
+constexpr float kInv7 = 0x1.24924ap-3f;         // RN32(1/7)                 0x3E124925
+constexpr float kInv9 = 0x1.c71c72p-4f;         // RN32(1/9)                 0x3DE38E39
+constexpr float kInv11 = 0x1.745d18p-4f;        // RN32(1/11)                0x3DBA2E8C
+
+__device__ __forceinline__ float clog(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u & 0x7F800000u) == 0u) return -__builtin_inff();  // zero or subnormal (read as zero)
+  if (u & 0x80000000u) return __builtin_nanf("");
+  if ((u & 0x7F800000u) == 0x7F800000u) return x;
+  int e = (int)((u >> 23) & 0xFFu) - 127;
+  float f = __uint_as_float((u & 0x7FFFFFu) | 0x3F800000u);
+  if (f > kSqrt2) {
+    f = f * 0.5f;
+    e += 1;
+  }
+  float num = f - 1.0f;
+  float den = f + 1.0f;
+  float s = num / den;
+  float z = s * s;
+  float q = kInv11;
+  q = q * z; q = q + kInv9;
+  q = q * z; q = q + kInv7;
+  q = q * z; q = q + kInv5;
+  q = q * z; q = q + kInv3;
+  q = q * z; q = q + 1.0f;
+  float s2 = s + s;
+  float lf = s2 * q;
+  float ef = (float)e;
+  float a = ef * kLn2Lo;
+  a = a + lf;
+  float b = ef * kLn2Hi;
+  return b + a;
+}
+
+__device__ __forceinline__ float csigmoid(float x) {
+  float e = cexp(-x);
+  float den = 1.0f + e;
+  return 1.0f / den;
+}
+
+__device__ __forceinline__ float csilu(float x) { return x * csigmoid(x); }
+
+// ---- R1 helpers ---------------------------------------------------------------------------------
+// Algorithm 2 over nparts chunk partials held one per lane of a wavefront (lane = chunk index, lanes
+// >= nparts ignored): level by level, a node adds its right neighbour's subtree only when that subtree
+// holds at least one real chunk, otherwise it passes through unchanged.  This is the zero-padded perfect
+// tree without adding any padding, i.e. the binary-carry fold with leftover blocks combined smallest
+// first.  Returns the total in lane 0.
+__device__ __forceinline__ float wave_fold(float p, int nparts) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1) {
+    float other = __shfl_down(p, s, 64);
+    if ((lane & (2 * s - 1)) == 0 && lane + s < nparts) p = p + other;
+  }
+  return p;
+}
+
+}  // namespace canon

@@ -1,0 +1,78 @@
+// canon_internal.h - argument structs and kernel launchers shared by the library's sources.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace canon {
+
+enum { KMODE_FULL = 0, KMODE_TRAIL = 1, KMODE_LEAD = 2 };
+
+// One (possibly batched) GEMM.  Matrix z of the batch is (z1, z2) = (z / nb2, z % nb2), with operand
+// offsets z1*s?1 + z2*s?2 (elements).
+struct GemmArgs {
+  const uint16_t* a;
+  const uint16_t* b;
+  void* c;
+  int64_t m, n, k, lda, ldb, ldc;
+  int64_t sa1, sa2, sb1, sb2, sc1, sc2;
+  int64_t nb2, batch;
+  int32_t trans_a, trans_b, out_bf16, kmode, tri_lower;
+};
+
+hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);
+int gemm_max_levels();
+
+// rows.hip
+hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps,
+                              uint16_t* y, float* rstd, hipStream_t s);
+hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
+                              const float* dy, float* dx, float* dgain, hipStream_t s);
+hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, uint16_t* probs,
+                                 hipStream_t s);
+hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets,
+                       float inv_tokens, uint16_t* dlogits, float* row_loss, float* mean_loss, hipStream_t s);
+hipError_t attn_rowdot_launch(int64_t B, int64_t H, int64_t S, int64_t hd, const uint16_t* dO, const uint16_t* O,
+                              int64_t ld, float* D, hipStream_t s);
+hipError_t attn_dS_launch(int64_t BH, int64_t S, const uint16_t* P, const float* dP, const float* D, float scale,
+                          uint16_t* dS, hipStream_t s);
+
+// elementwise.hip
+hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* qkv, const float* cosT,
+                           const float* sinT, uint16_t* q, uint16_t* k, uint16_t* v, hipStream_t s);
+hipError_t rope_bwd_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* dq, const float* dk,
+                           const float* cosT, const float* sinT, uint16_t* dqkv, hipStream_t s);
+hipError_t swiglu_fwd_launch(int64_t T, int64_t F, const float* gu, uint16_t* a, hipStream_t s);
+hipError_t swiglu_bwd_launch(int64_t T, int64_t F, const float* gu, const float* da, uint16_t* dgu, hipStream_t s);
+hipError_t add_f32_launch(int64_t n, const float* a, const float* b, float* out, hipStream_t s);
+hipError_t cast_bf16_launch(int64_t n, const float* x, uint16_t* y, hipStream_t s);
+hipError_t widen_bf16_launch(int64_t n, const uint16_t* x, float* y, hipStream_t s);
+hipError_t token_check_launch(int64_t n, const int32_t* tok, int32_t bound, int32_t* bad_flag, hipStream_t s);
+hipError_t embed_gather_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld,
+                               const uint16_t* E, int64_t V, float* x, hipStream_t s);
+hipError_t labels_launch(int64_t B, int64_t S, const int32_t* win, int64_t win_ld, int32_t* lab, hipStream_t s);
+size_t embed_bwd_scratch_bytes(int64_t T);
+hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld, int64_t V,
+                            const float* dx, float* dE, void* scratch, hipStream_t s);
+hipError_t devmath_launch(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
+                          hipStream_t s);
+
+// optim.hip
+constexpr int kMaxFusedBuffers = 64;
+struct PlanPtrs {
+  const float* p[kMaxFusedBuffers];
+};
+hipError_t grad_accum_fused_launch(int accum, int dp_shard, int dp_replicate, int64_t n, const PlanPtrs& ptrs,
+                                   float* out, hipStream_t s);
+// out = (first ? +0 : out) + RN(grad * inv)        (Algorithm 1, microbatch accumulation)
+hipError_t plan_accum_launch(int64_t n, const float* grad, float inv, int first, float* out, hipStream_t s);
+// out = first ? a : RN(out + a)                      (ascending shard sum)
+hipError_t plan_shard_launch(int64_t n, const float* a, int first, float* out, hipStream_t s);
+// out = RN(lower + out)                              (fold merge, lower block on the left)
+hipError_t plan_merge_launch(int64_t n, const float* lower, float* out, hipStream_t s);
+// out = RN(x * inv) (in place allowed)
+hipError_t plan_scale_launch(int64_t n, const float* x, float inv, float* out, hipStream_t s);
+hipError_t adamw_launch(int64_t n, uint16_t* p, float* m, float* v, const float* g, int decay, const float* consts9,
+                        const int32_t* skip_flag, hipStream_t s);
+hipError_t set_nan_if_launch(const int32_t* flag, float* x, hipStream_t s);
+
+}  // namespace canon

@@ -1,0 +1,311 @@
+// elementwise.hip - RoPE (R8), SwiGLU (R4), residual adds and casts (R10), embedding gather and the
+// ordered embedding backward (R11), and a device-math probe for the primitives.
+#include <hip/hip_runtime.h>
+
+#include "canon_dev.h"
+#include "canon_internal.h"
+
+namespace canon {
+
+static inline unsigned blocks_for(int64_t n) { return (unsigned)((n + 255) / 256); }
+
+// qkv fp32 [B*S, 3d] -> q, k (rotated) and v as bf16 [B, H, S, hd].
+__global__ void rope_qkv_kernel(int64_t B, int64_t S, int64_t H, int64_t hd, const float* __restrict__ qkv,
+                                const float* __restrict__ cosT, const float* __restrict__ sinT,
+                                uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v) {
+  const int64_t hh = hd / 2;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= B * S * H * hh) return;
+  const int64_t i = idx % hh, h = (idx / hh) % H, t = idx / (hh * H);
+  const int64_t b = t / S, s = t % S;
+  const int64_t d = H * hd;
+  const float c = cosT[s * hh + i], sn = sinT[s * hh + i];
+  const float* row = qkv + t * 3 * d + h * hd;
+  const int64_t o = ((b * H + h) * S + s) * hd;
+  {
+    float x1 = row[i], x2 = row[i + hh];
+    float a = x1 * c, bq = x2 * sn;
+    float e = x2 * c, f = x1 * sn;
+    q[o + i] = f32_to_bf16(a - bq);
+    q[o + i + hh] = f32_to_bf16(e + f);
+  }
+  {
+    float x1 = row[d + i], x2 = row[d + i + hh];
+    float a = x1 * c, bq = x2 * sn;
+    float e = x2 * c, f = x1 * sn;
+    k[o + i] = f32_to_bf16(a - bq);
+    k[o + i + hh] = f32_to_bf16(e + f);
+  }
+  v[o + i] = f32_to_bf16(row[2 * d + i]);
+  v[o + i + hh] = f32_to_bf16(row[2 * d + i + hh]);
+}
+
+hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* qkv, const float* cosT,
+                           const float* sinT, uint16_t* q, uint16_t* k, uint16_t* v, hipStream_t s) {
+  const int64_t n = B * S * H * (hd / 2);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_qkv_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, hd, qkv, cosT, sinT, q, k, v);
+  return hipGetLastError();
+}
+
+// transposed rotation of the q and k gradients ([B*S, d] fp32) into dqkv bf16 [B*S, 3d] columns [0, 2d).
+__global__ void rope_bwd_kernel(int64_t B, int64_t S, int64_t H, int64_t hd, const float* __restrict__ dq,
+                                const float* __restrict__ dk, const float* __restrict__ cosT,
+                                const float* __restrict__ sinT, uint16_t* __restrict__ dqkv) {
+  const int64_t hh = hd / 2;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= B * S * H * hh) return;
+  const int64_t i = idx % hh, h = (idx / hh) % H, t = idx / (hh * H);
+  const int64_t s = t % S;
+  const int64_t d = H * hd;
+  const float c = cosT[s * hh + i], sn = sinT[s * hh + i];
+  const float* src[2] = {dq, dk};
+#pragma unroll
+  for (int w = 0; w < 2; ++w) {
+    const float* g = src[w] + t * d + h * hd;
+    float g1 = g[i], g2 = g[i + hh];
+    float a = g1 * c, b = g2 * sn;
+    float e = g2 * c, f = g1 * sn;
+    dqkv[t * 3 * d + w * d + h * hd + i] = f32_to_bf16(a + b);
+    dqkv[t * 3 * d + w * d + h * hd + i + hh] = f32_to_bf16(e - f);
+  }
+}
+
+hipError_t rope_bwd_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* dq, const float* dk,
+                           const float* cosT, const float* sinT, uint16_t* dqkv, hipStream_t s) {
+  const int64_t n = B * S * H * (hd / 2);
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(rope_bwd_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, hd, dq, dk, cosT, sinT, dqkv);
+  return hipGetLastError();
+}
+
+// a = bf16(RN(silu(gate) * up)); gu = [T, 2F] with gate columns first.
+__global__ void swiglu_fwd_kernel(int64_t T, int64_t F, const float* __restrict__ gu, uint16_t* __restrict__ a) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= T * F) return;
+  const int64_t t = idx / F, j = idx % F;
+  float g = gu[t * 2 * F + j], u = gu[t * 2 * F + F + j];
+  float sl = csilu(g);
+  a[idx] = f32_to_bf16(sl * u);
+}
+
+__global__ void swiglu_bwd_kernel(int64_t T, int64_t F, const float* __restrict__ gu, const float* __restrict__ da,
+                                  uint16_t* __restrict__ dgu) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= T * F) return;
+  const int64_t t = idx / F, j = idx % F;
+  float g = gu[t * 2 * F + j], u = gu[t * 2 * F + F + j], dav = da[idx];
+  float sig = csigmoid(g);
+  float sl = g * sig;
+  float dup = dav * sl;
+  float oms = 1.0f - sig;
+  float gs = g * oms;
+  float ops = 1.0f + gs;
+  float dsg = sig * ops;
+  float du = dav * u;
+  float dgate = du * dsg;
+  dgu[t * 2 * F + j] = f32_to_bf16(dgate);
+  dgu[t * 2 * F + F + j] = f32_to_bf16(dup);
+}
+
+hipError_t swiglu_fwd_launch(int64_t T, int64_t F, const float* gu, uint16_t* a, hipStream_t s) {
+  if (T * F == 0) return hipSuccess;
+  hipLaunchKernelGGL(swiglu_fwd_kernel, dim3(blocks_for(T * F)), dim3(256), 0, s, T, F, gu, a);
+  return hipGetLastError();
+}
+
+hipError_t swiglu_bwd_launch(int64_t T, int64_t F, const float* gu, const float* da, uint16_t* dgu, hipStream_t s) {
+  if (T * F == 0) return hipSuccess;
+  hipLaunchKernelGGL(swiglu_bwd_kernel, dim3(blocks_for(T * F)), dim3(256), 0, s, T, F, gu, da, dgu);
+  return hipGetLastError();
+}
+
+__global__ void add_f32_kernel(int64_t n, const float* __restrict__ a, const float* __restrict__ b, float* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) out[i] = a[i] + b[i];
+}
+
+__global__ void cast_bf16_kernel(int64_t n, const float* __restrict__ x, uint16_t* __restrict__ y) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] = f32_to_bf16(x[i]);
+}
+
+__global__ void widen_bf16_kernel(int64_t n, const uint16_t* __restrict__ x, float* __restrict__ y) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) y[i] = bf16_to_f32(x[i]);
+}
+
+hipError_t add_f32_launch(int64_t n, const float* a, const float* b, float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(add_f32_kernel, dim3(blocks_for(n)), dim3(256), 0, s, n, a, b, out);
+  return hipGetLastError();
+}
+
+hipError_t cast_bf16_launch(int64_t n, const float* x, uint16_t* y, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(cast_bf16_kernel, dim3(blocks_for(n)), dim3(256), 0, s, n, x, y);
+  return hipGetLastError();
+}
+
+hipError_t widen_bf16_launch(int64_t n, const uint16_t* x, float* y, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(widen_bf16_kernel, dim3(blocks_for(n)), dim3(256), 0, s, n, x, y);
+  return hipGetLastError();
+}
+
+__global__ void token_check_kernel(int64_t n, const int32_t* __restrict__ tok, int32_t bound, int32_t* flag) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n && (tok[i] < 0 || tok[i] >= bound)) atomicOr(flag, 1);
+}
+
+hipError_t token_check_launch(int64_t n, const int32_t* tok, int32_t bound, int32_t* flag, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(token_check_kernel, dim3(blocks_for(n)), dim3(256), 0, s, n, tok, bound, flag);
+  return hipGetLastError();
+}
+
+// x[b*S + s, :] = widen(E[win[b, s], :]); an out-of-range token gives a zero row (the step reports it).
+__global__ void embed_gather_kernel(int64_t B, int64_t S, int64_t d, const int32_t* __restrict__ win, int64_t win_ld,
+                                    const uint16_t* __restrict__ E, int64_t V, float* __restrict__ x) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= B * S * d) return;
+  const int64_t k = idx % d, t = idx / d, b = t / S, s = t % S;
+  const int32_t tok = win[b * win_ld + s];
+  x[idx] = (tok >= 0 && tok < V) ? bf16_to_f32(E[(int64_t)tok * d + k]) : 0.0f;
+}
+
+hipError_t embed_gather_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld, const uint16_t* E,
+                               int64_t V, float* x, hipStream_t s) {
+  const int64_t n = B * S * d;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(embed_gather_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, d, win, win_ld, E, V, x);
+  return hipGetLastError();
+}
+
+__global__ void labels_kernel(int64_t B, int64_t S, const int32_t* __restrict__ win, int64_t win_ld,
+                              int32_t* __restrict__ lab) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= B * S) return;
+  const int64_t b = idx / S, s = idx % S;
+  lab[idx] = win[b * win_ld + s + 1];
+}
+
+hipError_t labels_launch(int64_t B, int64_t S, const int32_t* win, int64_t win_ld, int32_t* lab, hipStream_t s) {
+  if (B * S == 0) return hipSuccess;
+  hipLaunchKernelGGL(labels_kernel, dim3(blocks_for(B * S)), dim3(256), 0, s, B, S, win, win_ld, lab);
+  return hipGetLastError();
+}
+
+// ---- embedding backward (R11) --------------------------------------------------------------------
+// A stable counting sort of the positions by token: position t goes to slot
+//   #{t' : tok[t'] < tok[t]} + #{t' < t : tok[t'] == tok[t]},
+// so each token's positions sit together in ascending t.  Then one workgroup per token segment reduces
+// dx over the segment's positions in that order (chunks of 32, binary-carry fold), per column.
+__device__ __forceinline__ int32_t tok_at(const int32_t* win, int64_t win_ld, int64_t S, int64_t t) {
+  return win[(t / S) * win_ld + (t % S)];
+}
+
+__global__ void embed_sort_kernel(int64_t T, int64_t S, const int32_t* __restrict__ win, int64_t win_ld,
+                                  int32_t* __restrict__ perm) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= T) return;
+  const int32_t v = tok_at(win, win_ld, S, t);
+  int64_t before = 0, rank = 0;
+  for (int64_t u = 0; u < T; ++u) {
+    int32_t w = tok_at(win, win_ld, S, u);
+    before += (w < v);
+    rank += (w == v && u < t);
+  }
+  perm[before + rank] = (int32_t)t;
+}
+
+__global__ void fill_zero_kernel(int64_t n, float* __restrict__ x) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) x[i] = 0.0f;
+}
+
+__global__ __launch_bounds__(256) void embed_segment_kernel(int64_t T, int64_t S, int64_t d,
+                                                            const int32_t* __restrict__ win, int64_t win_ld,
+                                                            int64_t V, const int32_t* __restrict__ perm,
+                                                            const float* __restrict__ dx, float* __restrict__ dE) {
+  const int64_t p = blockIdx.x;
+  const int32_t v = tok_at(win, win_ld, S, perm[p]);
+  if (p > 0 && tok_at(win, win_ld, S, perm[p - 1]) == v) return;  // not the first slot of its segment
+  if (v < 0 || v >= V) return;
+  int64_t n = 1;
+  while (p + n < T && tok_at(win, win_ld, S, perm[p + n]) == v) ++n;
+  for (int64_t k = threadIdx.x; k < d; k += 256) {
+    float st[16];
+    int64_t count = 0;
+    for (int64_t c0 = 0; c0 < n; c0 += kChunk) {
+      float s = 0.0f;
+      const int64_t c1 = c0 + kChunk < n ? c0 + kChunk : n;
+      for (int64_t q = c0; q < c1; ++q) s = s + dx[(int64_t)perm[p + q] * d + k];
+      // binary-carry push
+#pragma unroll
+      for (int L = 0; L < 16; ++L) {
+        if ((count >> L) & 1) {
+          s = st[L] + s;
+        } else {
+          st[L] = s;
+          break;
+        }
+      }
+      ++count;
+    }
+    float r = 0.0f;
+    bool have = false;
+#pragma unroll
+    for (int L = 0; L < 16; ++L) {
+      if ((count >> L) & 1) {
+        if (!have) { r = st[L]; have = true; }
+        else r = st[L] + r;
+      }
+    }
+    dE[(int64_t)v * d + k] = r;
+  }
+}
+
+size_t embed_bwd_scratch_bytes(int64_t T) { return sizeof(int32_t) * (size_t)(T > 0 ? T : 1); }
+
+hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld, int64_t V,
+                            const float* dx, float* dE, void* scratch, hipStream_t s) {
+  const int64_t T = B * S;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks_for(V * d)), dim3(256), 0, s, V * d, dE);
+  if (T == 0) return hipGetLastError();
+  int32_t* perm = (int32_t*)scratch;
+  hipLaunchKernelGGL(embed_sort_kernel, dim3(blocks_for(T)), dim3(256), 0, s, T, S, win, win_ld, perm);
+  hipLaunchKernelGGL(embed_segment_kernel, dim3((unsigned)T), dim3(256), 0, s, T, S, d, win, win_ld, V, perm, dx, dE);
+  return hipGetLastError();
+}
+
+// ---- device evaluation of the primitives -----------------------------------------------------------
+__global__ void devmath_kernel(int32_t op, int64_t n, const float* __restrict__ a, const float* __restrict__ b,
+                               const float* __restrict__ c, float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float x = a[i], r = 0.0f;
+  switch (op) {
+    case 0: r = x + b[i]; break;
+    case 1: r = x - b[i]; break;
+    case 2: r = x * b[i]; break;
+    case 3: r = __builtin_fmaf(x, b[i], c[i]); break;
+    case 4: r = x / b[i]; break;
+    case 5: r = __builtin_sqrtf(x); break;
+    case 6: r = cexp(x); break;
+    case 7: r = clog(x); break;
+    case 8: r = csigmoid(x); break;
+    case 9: r = csilu(x); break;
+    case 10: r = bf16_to_f32(f32_to_bf16(x)); break;
+  }
+  out[i] = r;
+}
+
+hipError_t devmath_launch(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
+                          hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(devmath_kernel, dim3(blocks_for(n)), dim3(256), 0, s, op, n, a, b, c, out);
+  return hipGetLastError();
+}
+
+}  // namespace canon

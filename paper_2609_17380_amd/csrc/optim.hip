@@ -1,0 +1,166 @@
+// optim.hip - the gradient plan (R7: Algorithm 1 with Algorithm 2 over replicas) and AdamW (R9).
+// All of these are streaming, HBM-bound kernels: one element per thread, no cross-element arithmetic, so
+// the order of every per-element operation is fixed by the code and independent of the launch shape.
+#include <hip/hip_runtime.h>
+
+#include "canon_dev.h"
+#include "canon_internal.h"
+
+namespace canon {
+
+static inline unsigned grid_for(int64_t n) {
+  int64_t b = (n + 255) / 256;
+  return (unsigned)(b < 65536 * 16 ? b : 65536 * 16);  // grid-stride beyond this
+}
+
+// One pass over N*accum buffers: per element, Algorithm 1 in registers with a binary-carry stack over the
+// replica partials.
+__global__ __launch_bounds__(256) void grad_accum_fused_kernel(int accum, int dp_shard, int dp_replicate, int64_t n,
+                                                               PlanPtrs ptrs, float inv_accum, float inv_shard,
+                                                               float inv_rep, float* __restrict__ out) {
+  const int N = dp_shard * dp_replicate;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    float stack[8];
+    int pushed = 0;
+    float inner = 0.0f;
+    for (int r = 0; r < N; ++r) {
+      float g = 0.0f;
+      for (int k = 0; k < accum; ++k) {
+        float t = ptrs.p[r * accum + k][i] * inv_accum;
+        g = g + t;
+      }
+      const int shard = r % dp_shard;
+      inner = (shard == 0) ? g : inner + g;
+      if (shard == dp_shard - 1) {
+        float part = inner * inv_shard;
+#pragma unroll
+        for (int L = 0; L < 8; ++L) {
+          if ((pushed >> L) & 1) {
+            part = stack[L] + part;
+          } else {
+            stack[L] = part;
+            break;
+          }
+        }
+        ++pushed;
+      }
+    }
+    float res = 0.0f;
+    bool have = false;
+#pragma unroll
+    for (int L = 0; L < 8; ++L) {
+      if ((pushed >> L) & 1) {
+        if (!have) { res = stack[L]; have = true; }
+        else res = stack[L] + res;
+      }
+    }
+    out[i] = res * inv_rep;
+  }
+}
+
+hipError_t grad_accum_fused_launch(int accum, int dp_shard, int dp_replicate, int64_t n, const PlanPtrs& ptrs,
+                                   float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const float inv_accum = (float)(1.0 / accum), inv_shard = (float)(1.0 / dp_shard),
+              inv_rep = (float)(1.0 / dp_replicate);  // RN32 of each reciprocal
+  hipLaunchKernelGGL(grad_accum_fused_kernel, dim3(grid_for(n)), dim3(256), 0, s, accum, dp_shard, dp_replicate, n,
+                     ptrs, inv_accum, inv_shard, inv_rep, out);
+  return hipGetLastError();
+}
+
+__global__ void plan_accum_kernel(int64_t n, const float* __restrict__ grad, float inv, int first, float* out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    float t = grad[i] * inv;
+    float base = first ? 0.0f : out[i];
+    out[i] = base + t;
+  }
+}
+
+__global__ void plan_shard_kernel(int64_t n, const float* __restrict__ a, int first, float* out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    out[i] = first ? a[i] : out[i] + a[i];
+}
+
+__global__ void plan_merge_kernel(int64_t n, const float* __restrict__ lower, float* out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    out[i] = lower[i] + out[i];
+}
+
+__global__ void plan_scale_kernel(int64_t n, const float* x, float inv, float* out) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+    out[i] = x[i] * inv;
+}
+
+hipError_t plan_accum_launch(int64_t n, const float* grad, float inv, int first, float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(plan_accum_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, grad, inv, first, out);
+  return hipGetLastError();
+}
+
+hipError_t plan_shard_launch(int64_t n, const float* a, int first, float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(plan_shard_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, a, first, out);
+  return hipGetLastError();
+}
+
+hipError_t plan_merge_launch(int64_t n, const float* lower, float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(plan_merge_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, lower, out);
+  return hipGetLastError();
+}
+
+hipError_t plan_scale_launch(int64_t n, const float* x, float inv, float* out, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(plan_scale_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, x, inv, out);
+  return hipGetLastError();
+}
+
+struct AdamWK {
+  float lr, beta1, omb1, beta2, omb2, inv_bc1, inv_bc2, eps, decay_factor;
+};
+
+__global__ __launch_bounds__(256) void adamw_kernel(int64_t n, uint16_t* __restrict__ p16, float* __restrict__ m,
+                                                    float* __restrict__ v, const float* __restrict__ g, int decay,
+                                                    AdamWK k, const int32_t* __restrict__ skip) {
+  if (skip && *skip) return;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    float p = bf16_to_f32(p16[i]);
+    if (decay) p = p * k.decay_factor;
+    const float gi = g[i];
+    float m1 = k.beta1 * m[i];
+    float m2 = k.omb1 * gi;
+    float mi = m1 + m2;
+    float gg = gi * gi;
+    float v1 = k.beta2 * v[i];
+    float v2 = k.omb2 * gg;
+    float vi = v1 + v2;
+    float mh = mi * k.inv_bc1;
+    float vh = vi * k.inv_bc2;
+    float den = __builtin_sqrtf(vh) + k.eps;
+    float u = mh / den;
+    float step = k.lr * u;
+    p = p - step;
+    m[i] = mi;
+    v[i] = vi;
+    p16[i] = f32_to_bf16(p);
+  }
+}
+
+hipError_t adamw_launch(int64_t n, uint16_t* p, float* m, float* v, const float* g, int decay, const float* c9,
+                        const int32_t* skip_flag, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  AdamWK k{c9[0], c9[1], c9[2], c9[3], c9[4], c9[5], c9[6], c9[7], c9[8]};
+  hipLaunchKernelGGL(adamw_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, p, m, v, g, decay, k, skip_flag);
+  return hipGetLastError();
+}
+
+__global__ void set_nan_if_kernel(const int32_t* flag, float* x) {
+  if (*flag) x[0] = __builtin_nanf("");
+}
+
+hipError_t set_nan_if_launch(const int32_t* flag, float* x, hipStream_t s) {
+  hipLaunchKernelGGL(set_nan_if_kernel, dim3(1), dim3(1), 0, s, flag, x);
+  return hipGetLastError();
+}
+
+}  // namespace canon

@@ -14,6 +14,7 @@ from fractions import Fraction as F
 import numpy as np
 import pytest
 
+import adversarial as ADV
 import exact_r0 as X
 import oracle
 
@@ -25,51 +26,14 @@ def f32_from_bits(u):
 
 
 def random_floats(n, exp_lo=0, exp_hi=254):
-    sign = RNG.integers(0, 2, n, dtype=np.uint32) << 31
-    ex = RNG.integers(exp_lo, exp_hi + 1, n, dtype=np.uint32) << 23
-    man = RNG.integers(0, 1 << 23, n, dtype=np.uint32)
-    return f32_from_bits(sign | ex | man)
+    return ADV.random_floats(RNG, n, exp_lo, exp_hi)
 
 
 def bits(x):
     return np.asarray(x, dtype=np.float32).view(np.uint32)
 
 
-def adversarial_pairs():
-    """(a, b, c) triples hitting ties, cancellation, the 2^-126 band, signed zeros and subnormals."""
-    a, b, c = [], [], []
-    n = 3000
-    # wide-range random values, including subnormal inputs
-    a += list(random_floats(n, 0, 254)); b += list(random_floats(n, 0, 254)); c += list(random_floats(n, 0, 254))
-    # moderate exponents where sums interact
-    a += list(random_floats(n, 100, 150)); b += list(random_floats(n, 100, 150)); c += list(random_floats(n, 100, 150))
-    # exact ties for add: b = odd multiple of half an ulp of a
-    base = random_floats(n, 110, 140)
-    ulp = np.spacing(np.abs(base)).astype(np.float64)
-    tie = (ulp / 2 * (2 * RNG.integers(0, 4, n) + 1) * RNG.choice([-1, 1], n)).astype(np.float32)
-    a += list(base); b += list(tie); c += list(tie)
-    # products and fused results landing next to 2^-126
-    T = 2.0 ** -126
-    ua = (0.5 + RNG.random(n) * 0.5).astype(np.float32)
-    ub = ((T / ua.astype(np.float64)) * (1 + (RNG.random(n) - 0.5) * 2.0 ** -21)).astype(np.float32)
-    ub = np.maximum(ub, np.float32(T)) * RNG.choice([-1, 1], n).astype(np.float32)
-    a += list(ua); b += list(ub); c += [np.float32(0.0)] * n
-    a2 = (1.0 + RNG.integers(1, 2 ** 23, n) * 2.0 ** -23).astype(np.float32)
-    cc = np.full(n, 2.0 ** -124, np.float32) * RNG.choice([-1, 1], n).astype(np.float32)
-    b2 = ((-(2.0 ** -124 - T * (1 + (RNG.random(n) - 0.5) * 2.0 ** -20) * np.sign(cc)) / a2.astype(np.float64))
-          ).astype(np.float32)
-    a += list(a2); b += list(b2); c += list(cc)
-    # cancellation in add: b close to -a
-    a += list(base); b += list((-base * (1 + RNG.integers(-3, 4, n) * 2.0 ** -23)).astype(np.float32)); c += list(base)
-    # signed zeros
-    for za in (0.0, -0.0, 1.5, -1.5, 2.0 ** -130, -(2.0 ** -130)):
-        for zb in (0.0, -0.0, 3.0, -3.0):
-            for zc in (0.0, -0.0, -4.5):
-                a.append(np.float32(za)); b.append(np.float32(zb)); c.append(np.float32(zc))
-    return (np.array(a, np.float32), np.array(b, np.float32), np.array(c, np.float32))
-
-
-A, B, C = adversarial_pairs()
+A, B, C = ADV.triples()
 
 
 @pytest.mark.parametrize("op", ["add", "sub", "mul", "fma", "div"])
