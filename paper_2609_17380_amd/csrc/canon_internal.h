@@ -17,6 +17,7 @@ struct GemmArgs {
   int64_t sa1, sa2, sb1, sb2, sc1, sc2;
   int64_t nb2, batch;
   int32_t trans_a, trans_b, out_bf16, kmode, tri_lower;
+  int32_t vec;  // set by the launcher: 16-byte operand loads allowed
 };
 
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);

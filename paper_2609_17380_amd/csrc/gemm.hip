@@ -13,9 +13,15 @@
 //
 // Tiling: a workgroup of 4 waves computes a 64 x 128 tile of C; wave (wr, wc) owns rows 32*wr..+32 and
 // columns 64*wc..+64 as the instruction's two 32x32 blocks (block 0: columns +0..31, block 1: +32..63).
-// Per chunk the 64x32 A tile and 32x128 B tile are staged through LDS as fp32 (widened once, k-major so
-// that a lane reads one float per k), double buffered, with the next chunk's global loads issued before
-// the current chunk's MFMA chain.  The binary-carry stack lives in registers (MAXL levels of 32 floats).
+// Two workgroups share a CU (two waves per SIMD) so one hides the other's LDS and barrier waits.
+// Per chunk the 64x32 A tile and 32x128 B tile are staged through LDS as fp32, widened once and double
+// buffered, with the next chunk's 16-byte global loads in flight during the current chunk's MFMA chain.
+// An operand whose source is k-contiguous is stored as rows [row][k] (one 16-byte LDS read gives a lane
+// four k values); one whose source is row-contiguous is stored k-major [k][row] (one 4-byte read per k),
+// so neither layout needs a transposing scatter.
+// Fold: inside an aligned group of four chunks the two lowest levels of Algorithm 2 are fixed and merged
+// in place; the group partial is pushed at level 2.  Levels 2 and 3 stay in registers; levels 4 and up,
+// touched once per 16 chunks, live in per-lane private memory.
 //
 // Causal modes (attention): KMODE_TRAIL skips key chunks that are masked for every row of the tile and
 // KMODE_LEAD skips query chunks below the tile; the skipped chunks' partials are exactly +0 in the
@@ -28,105 +34,279 @@
 namespace canon {
 
 typedef float v32f __attribute__((ext_vector_type(32)));
+typedef float v4f __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 64, BN = 128, KC = 32;
-constexpr int APAD = 4, BPAD = 4;
+constexpr int LDK = KC + 4;               // row-layout stride (floats): [row][k]
+constexpr int LDMA = BM + 4, LDMB = BN + 4;  // k-major stride (floats): [k][row]
+constexpr int A_FLOATS = (BM * LDK > KC * LDMA) ? BM * LDK : KC * LDMA;
+constexpr int B_FLOATS = (BN * LDK > KC * LDMB) ? BN * LDK : KC * LDMB;
 
-template <bool TA, bool TB>
-__device__ __forceinline__ void load_tiles(const GemmArgs& g, const uint16_t* A, const uint16_t* B, int64_t row0,
-                                           int64_t col0, int64_t k0, uint16_t (&ra)[8], uint16_t (&rb)[16]) {
-  const int t = threadIdx.x;
-  // A: 64 rows x 32 k, 8 consecutive elements per thread
-  {
-    int64_t r, kk;
-    if (!TA) { r = t >> 2; kk = (t & 3) * 8; }
-    else { kk = t >> 3; r = (t & 7) * 8; }
+// Raw bf16 data of one chunk for one thread: 8 A elements and 16 B elements, as 16-byte vectors.
+struct Raw {
+  uint4 a, b0, b1;
+};
+
+// bf16 pair packed in a 32-bit word -> two floats.  No explicit input flush: in flush mode the matrix
+// core reads a subnormal operand as zero of its sign (measured on gfx950), which is the R0 input rule.
+__device__ __forceinline__ void widen8(const uint4& u, float (&f)[8]) {
+  f[0] = __uint_as_float(u.x << 16); f[1] = __uint_as_float(u.x & 0xFFFF0000u);
+  f[2] = __uint_as_float(u.y << 16); f[3] = __uint_as_float(u.y & 0xFFFF0000u);
+  f[4] = __uint_as_float(u.z << 16); f[5] = __uint_as_float(u.z & 0xFFFF0000u);
+  f[6] = __uint_as_float(u.w << 16); f[7] = __uint_as_float(u.w & 0xFFFF0000u);
+}
+
+__device__ __forceinline__ uint4 pack8(const uint16_t (&h)[8]) {
+  uint4 u;
+  u.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+  u.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+  u.z = (uint32_t)h[4] | ((uint32_t)h[5] << 16);
+  u.w = (uint32_t)h[6] | ((uint32_t)h[7] << 16);
+  return u;
+}
+
+// 8 consecutive elements of which only the first `valid` exist: zero fill beyond.
+template <bool FAST>
+__device__ __forceinline__ uint4 load8(const uint16_t* p, int64_t valid, bool vec) {
+  if (FAST) return *reinterpret_cast<const uint4*>(p);
+  if (vec && valid >= 8) return *reinterpret_cast<const uint4*>(p);
+  uint16_t h[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      int64_t ri = row0 + r + (TA ? e : 0), ki = k0 + kk + (TA ? 0 : e);
-      ra[e] = (ri < g.m && ki < g.k) ? (TA ? A[ki * g.lda + ri] : A[ri * g.lda + ki]) : (uint16_t)0;
-    }
+  for (int e = 0; e < 8; ++e) h[e] = (e < valid) ? p[e] : (uint16_t)0;
+  return pack8(h);
+}
+
+// Global -> registers for the chunk starting at k0.  Per operand, a thread takes 8 consecutive elements
+// along the source's contiguous dimension: (row, 8 k) for a k-contiguous source, (k, 8 rows) otherwise.
+// FAST: the whole chunk is in range and 16-byte aligned (no checks).
+template <bool TA, bool TB, bool FAST>
+__device__ __forceinline__ Raw load_chunk(const GemmArgs& g, const uint16_t* A, const uint16_t* B, int64_t row0,
+                                          int64_t col0, int64_t k0, bool vec) {
+  const int t = threadIdx.x;
+  Raw r;
+  if (!TA) {
+    const int64_t row = row0 + (t >> 2), k = k0 + (t & 3) * 8;
+    r.a = load8<FAST>(A + row * g.lda + k, (row < g.m) ? (g.k - k) : 0, vec);
+  } else {
+    const int64_t k = k0 + (t >> 3), row = row0 + (t & 7) * 8;
+    r.a = load8<FAST>(A + k * g.lda + row, (k < g.k) ? (g.m - row) : 0, vec);
   }
-  // B: 32 k x 128 cols, two groups of 8 per thread
 #pragma unroll
   for (int it = 0; it < 2; ++it) {
-    int idx = t + 256 * it;
-    int64_t c, kk;
-    if (!TB) { kk = idx >> 4; c = (idx & 15) * 8; }
-    else { c = idx >> 2; kk = (idx & 3) * 8; }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      int64_t ci = col0 + c + (TB ? 0 : e), ki = k0 + kk + (TB ? e : 0);
-      rb[it * 8 + e] = (ci < g.n && ki < g.k) ? (TB ? B[ci * g.ldb + ki] : B[ki * g.ldb + ci]) : (uint16_t)0;
+    const int idx = t + 256 * it;
+    uint4 v;
+    if (TB) {
+      const int64_t col = col0 + (idx >> 2), k = k0 + (idx & 3) * 8;
+      v = load8<FAST>(B + col * g.ldb + k, (col < g.n) ? (g.k - k) : 0, vec);
+    } else {
+      const int64_t k = k0 + (idx >> 4), col = col0 + (idx & 15) * 8;
+      v = load8<FAST>(B + k * g.ldb + col, (k < g.k) ? (g.n - col) : 0, vec);
     }
+    if (it == 0) r.b0 = v; else r.b1 = v;
+  }
+  return r;
+}
+
+__device__ __forceinline__ void st8(float* d, const float (&f)[8]) {
+  *reinterpret_cast<v4f*>(d) = v4f{f[0], f[1], f[2], f[3]};
+  *reinterpret_cast<v4f*>(d + 4) = v4f{f[4], f[5], f[6], f[7]};
+}
+
+// Registers -> LDS: rows [row][k] for k-contiguous sources, k-major [k][row] otherwise; both are
+// 8 contiguous floats per thread.
+template <bool TA, bool TB>
+__device__ __forceinline__ void store_chunk(float* As, float* Bs, const Raw& r) {
+  const int t = threadIdx.x;
+  float f[8];
+  widen8(r.a, f);
+  if (!TA) st8(As + (t >> 2) * LDK + (t & 3) * 8, f);
+  else st8(As + (t >> 3) * LDMA + (t & 7) * 8, f);
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const int idx = t + 256 * it;
+    widen8(it == 0 ? r.b0 : r.b1, f);
+    if (TB) st8(Bs + (idx >> 2) * LDK + (idx & 3) * 8, f);
+    else st8(Bs + (idx >> 4) * LDMB + (idx & 15) * 8, f);
   }
 }
 
-template <bool TA, bool TB>
-__device__ __forceinline__ void store_tiles(float (*As)[BM + APAD], float (*Bs)[BN + BPAD], const uint16_t (&ra)[8],
-                                            const uint16_t (&rb)[16]) {
-  const int t = threadIdx.x;
-  {
-    int r, kk;
-    if (!TA) { r = t >> 2; kk = (t & 3) * 8; }
-    else { kk = t >> 3; r = (t & 7) * 8; }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      if (!TA) As[kk + e][r] = bf16_to_f32(ra[e]);
-      else As[kk][r + e] = bf16_to_f32(ra[e]);
-    }
-  }
-#pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    int idx = t + 256 * it;
-    int c, kk;
-    if (!TB) { kk = idx >> 4; c = (idx & 15) * 8; }
-    else { c = idx >> 2; kk = (idx & 3) * 8; }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      if (!TB) Bs[kk][c + e] = bf16_to_f32(rb[it * 8 + e]);
-      else Bs[kk + e][c] = bf16_to_f32(rb[it * 8 + e]);
-    }
-  }
+// four consecutive k values (4*g4 .. 4*g4+3) of this lane's row / column
+template <bool KMAJOR, int LDM>
+__device__ __forceinline__ v4f fetch4(const float* base, int idx, int g4) {
+  if (!KMAJOR) return *reinterpret_cast<const v4f*>(base + idx * LDK + 4 * g4);
+  const float* p = base + (4 * g4) * LDM + idx;
+  return v4f{p[0], p[LDM], p[2 * LDM], p[3 * LDM]};
 }
 
-// Binary-carry stack of Algorithm 2 with MAXL levels, each level a register set of its own (a recursive
-// member chain, so no level is ever addressed dynamically).  push(p, c) pushes the partial of chunk c
-// (c = number of partials pushed before it): at each level whose bit of c is set the stored block is
-// merged, earlier block on the left, and the carry moves up.  The caller keeps the chunk count below
-// 2^MAXL so a carry never leaves the top level.
-template <int L>
-struct FoldStack {
-  v32f s;
-  FoldStack<L - 1> up;
-  __device__ __forceinline__ void clear(const v32f& z) { s = z; up.clear(z); }
+// One full chunk's chain: 32 dependent rank-1 updates from +0, operand reads one group ahead.
+#ifndef CHAIN_VARIANT
+#define CHAIN_VARIANT 0
+#endif
+template <bool TA, bool TB>
+__device__ __forceinline__ v32f chain_full(const float* As, const float* Bs, int ai, int bi) {
+  v32f acc;
+#pragma unroll
+  for (int v = 0; v < 32; ++v) acc[v] = 0.0f;
+#if CHAIN_VARIANT == 2
+  v4f a4[KC / 4], b4[KC / 4];
+#pragma unroll
+  for (int g4 = 0; g4 < KC / 4; ++g4) {
+    a4[g4] = fetch4<TA, LDMA>(As, ai, g4);
+    b4[g4] = fetch4<!TB, LDMB>(Bs, bi, g4);
+  }
+#pragma unroll
+  for (int g4 = 0; g4 < KC / 4; ++g4)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x1f32(a4[g4][j], b4[g4][j], acc, 0, 0, 0);
+#elif CHAIN_VARIANT == 1
+  v4f a0 = fetch4<TA, LDMA>(As, ai, 0), b0 = fetch4<!TB, LDMB>(Bs, bi, 0);
+  v4f a1 = fetch4<TA, LDMA>(As, ai, 1), b1 = fetch4<!TB, LDMB>(Bs, bi, 1);
+#pragma unroll
+  for (int g4 = 0; g4 < KC / 4; ++g4) {
+    v4f a2 = a1, b2 = b1;
+    if (g4 + 2 < KC / 4) {
+      a2 = fetch4<TA, LDMA>(As, ai, g4 + 2);
+      b2 = fetch4<!TB, LDMB>(Bs, bi, g4 + 2);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x1f32(a0[j], b0[j], acc, 0, 0, 0);
+    a0 = a1; b0 = b1; a1 = a2; b1 = b2;
+  }
+#else
+  v4f a4 = fetch4<TA, LDMA>(As, ai, 0), b4 = fetch4<!TB, LDMB>(Bs, bi, 0);
+#pragma unroll
+  for (int g4 = 0; g4 < KC / 4; ++g4) {
+    v4f an = a4, bn = b4;
+    if (g4 + 1 < KC / 4) {
+      an = fetch4<TA, LDMA>(As, ai, g4 + 1);
+      bn = fetch4<!TB, LDMB>(Bs, bi, g4 + 1);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x1f32(a4[j], b4[j], acc, 0, 0, 0);
+    a4 = an;
+    b4 = bn;
+  }
+#endif
+  return acc;
+}
+
+// A ragged last chunk: only its kleft < 32 real terms enter the chain.
+template <bool TA, bool TB>
+__device__ __forceinline__ v32f chain_part(const float* As, const float* Bs, int ai, int bi, int kleft) {
+  v32f acc;
+#pragma unroll
+  for (int v = 0; v < 32; ++v) acc[v] = 0.0f;
+  for (int kk = 0; kk < kleft; ++kk) {
+    float av = TA ? As[kk * LDMA + ai] : As[ai * LDK + kk];
+    float bv = TB ? Bs[bi * LDK + kk] : Bs[kk * LDMB + bi];
+    acc = __builtin_amdgcn_mfma_f32_32x32x1f32(av, bv, acc, 0, 0, 0);
+  }
+  return acc;
+}
+
+// Fold levels kept in private memory (levels >= the register levels); rarely touched.
+template <int N>
+struct FoldMem {
+  float s[N > 0 ? N : 1][32];
+  // levels whose bit is set in c0 hold +0 (skipped leading blocks); the others are written before read
+  __device__ __forceinline__ void clear(int64_t c0) {
+    for (int L = 0; L < N; ++L, c0 >>= 1)
+      if (c0 & 1)
+        for (int v = 0; v < 32; ++v) s[L][v] = 0.0f;
+  }
   __device__ __forceinline__ void push(v32f p, int64_t c) {
-    if (c & 1) up.push(s + p, c >> 1);
+    int L = 0;
+    while (c & 1) {
+      v32f lower;
+#pragma unroll
+      for (int v = 0; v < 32; ++v) lower[v] = s[L][v];
+      p = lower + p;
+      c >>= 1;
+      ++L;
+    }
+#pragma unroll
+    for (int v = 0; v < 32; ++v) s[L][v] = p[v];
+  }
+  __device__ __forceinline__ void result(v32f& r, bool& have, int64_t n) const {
+    for (int L = 0; L < N; ++L, n >>= 1) {
+      if (n & 1) {
+        v32f x;
+#pragma unroll
+        for (int v = 0; v < 32; ++v) x[v] = s[L][v];
+        if (!have) { r = x; have = true; }
+        else r = x + r;
+      }
+    }
+  }
+};
+
+// Binary-carry stack of Algorithm 2: R register levels, then the private-memory levels (a separate object,
+// so that the dynamically indexed memory levels never force the register levels out of registers).
+// push(p, c, mem) pushes the partial with index c at this level: at each level whose bit of c is set the
+// stored block is merged (earlier block on the left) and the carry moves up.  The caller keeps the chunk
+// count below 2^MAXL.
+template <int R>
+struct FoldRegs {
+  v32f s;
+  FoldRegs<R - 1> up;
+  // the stack after c0 pushes of +0: +0 at the set bits of c0
+  template <class M>
+  __device__ __forceinline__ void clear(const v32f& z, int64_t c0, M& mem) {
+    s = z;
+    up.clear(z, c0 >> 1, mem);
+  }
+  template <class M>
+  __device__ __forceinline__ void push(v32f p, int64_t c, M& mem) {
+    if (c & 1) up.push(s + p, c >> 1, mem);
     else s = p;
   }
   // Result: lowest occupied level first, then the others in ascending level order
-  __device__ __forceinline__ void result(v32f& r, bool& have, int64_t n) const {
+  template <class M>
+  __device__ __forceinline__ void result(v32f& r, bool& have, int64_t n, const M& mem) const {
     if (n & 1) {
       if (!have) { r = s; have = true; }
       else r = s + r;
     }
-    up.result(r, have, n >> 1);
+    up.result(r, have, n >> 1, mem);
   }
 };
 template <>
-struct FoldStack<0> {
-  __device__ __forceinline__ void clear(const v32f&) {}
-  __device__ __forceinline__ void push(v32f, int64_t) {}
-  __device__ __forceinline__ void result(v32f&, bool&, int64_t) const {}
+struct FoldRegs<0> {
+  template <class M>
+  __device__ __forceinline__ void clear(const v32f&, int64_t c0, M& mem) { mem.clear(c0); }
+  template <class M>
+  __device__ __forceinline__ void push(v32f p, int64_t c, M& mem) { mem.push(p, c); }
+  template <class M>
+  __device__ __forceinline__ void result(v32f& r, bool& have, int64_t n, const M& mem) const {
+    mem.result(r, have, n);
+  }
 };
 
 template <int MAXL, bool TA, bool TB>
-__global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g) {
-  __shared__ float As[2][KC][BM + APAD];
-  __shared__ float Bs[2][KC][BN + BPAD];
+__global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) float As[2][A_FLOATS];
+  __shared__ __attribute__((aligned(16))) float Bs[2][B_FLOATS];
+  // the stack holds levels >= 2 (levels 0 and 1 live inside the group code): register levels (three for
+  // the row/row layout, two for layouts with k-major staging, which need more address registers), the
+  // rest in private memory
+  constexpr int RLMAX = (!TA && TB) ? 3 : 2;
+  constexpr int RL = (MAXL - 2) < RLMAX ? (MAXL - 2) : RLMAX;
+  constexpr int NMEM = MAXL - 2 - RL;
 
+  // tile order: consecutive workgroups go to different XCDs, so first give each XCD a contiguous run of
+  // tiles; then walk that run in groups of GM tile rows (column of GM tiles, then the next column), so the
+  // workgroups resident on one XCD share a few A and B tiles in its L2
+  constexpr int64_t GM = 8;
   const int64_t tiles_n = (g.n + BN - 1) / BN;
-  const int64_t tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int64_t tiles_m = (g.m + BM - 1) / BM;
+  const int64_t tiles = tiles_m * tiles_n;
+  int64_t tile = blockIdx.x;
+  if ((tiles & 7) == 0) tile = (blockIdx.x & 7) * (tiles >> 3) + (blockIdx.x >> 3);
+  const int64_t group = tile / (GM * tiles_n);
+  const int64_t first_m = group * GM;
+  const int64_t gsize = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
+  const int64_t within = tile - group * GM * tiles_n;
+  const int64_t tm = first_m + within % gsize, tn = within / gsize;
   const int64_t row0 = tm * BM, col0 = tn * BN;
   if (g.tri_lower && col0 > row0 + BM - 1) return;  // output tile entirely above the diagonal
 
@@ -134,12 +314,17 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g) {
   const int64_t z1 = z / g.nb2, z2 = z % g.nb2;
   const uint16_t* A = g.a + z1 * g.sa1 + z2 * g.sa2;
   const uint16_t* B = g.b + z1 * g.sb1 + z2 * g.sb2;
+  const bool vec = g.vec != 0;
+  const bool tile_in = vec && row0 + BM <= g.m && col0 + BN <= g.n;
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
   const int wr = w >> 1, wc = w & 1;
+  const int ai = wr * 32 + (lane & 31);  // this lane's A row within the tile
+  const int bi = wc * 64 + lane;         // this lane's B column within the tile
 
   const int64_t nc = (g.k + KC - 1) / KC;
+  const int64_t kfull = g.k / KC;  // chunks with all 32 terms
   int64_t c_begin = 0, c_end = nc;
   if (g.kmode == KMODE_TRAIL) {
     int64_t last_row = row0 + BM < g.m ? row0 + BM : g.m;  // rows of this tile are < last_row
@@ -153,44 +338,92 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g) {
   v32f zero;
 #pragma unroll
   for (int v = 0; v < 32; ++v) zero[v] = 0.0f;
-  // leading skipped chunks: the stack after pushing c_begin partials of +0 holds +0 at its set bits
-  FoldStack<MAXL> S;
-  S.clear(zero);
+  // Level-2 stack (one entry per aligned group of four chunks).  Groups entirely before c_begin are
+  // skipped chunks: pushing them as +0 partials leaves +0 at the set bits of their count, i.e. clear().
+  FoldRegs<RL> S;
+  FoldMem<NMEM> Smem;
+  S.clear(zero, c_begin >> 2, Smem);
 
-  uint16_t ra[8], rb[16];
   int buf = 0;
-  if (c_begin < c_end) {
-    load_tiles<TA, TB>(g, A, B, row0, col0, c_begin * KC, ra, rb);
-    store_tiles<TA, TB>(As[0], Bs[0], ra, rb);
-  }
+  if (c_begin < c_end)
+    store_chunk<TA, TB>(As[0], Bs[0], load_chunk<TA, TB, false>(g, A, B, row0, col0, c_begin * KC, vec));
   __syncthreads();
 
-  const int arow = wr * 32 + (lane & 31);
-  const int bcol = wc * 64 + lane;
-  for (int64_t c = c_begin; c < c_end; ++c) {
+  // generic pipelined chunk (checked loads, ragged chunk allowed); chunks run in ascending order from
+  // c_begin, so chunk c + 1 is the next one to run
+  auto run_chunk = [&](int64_t c) -> v32f {
     const bool more = c + 1 < c_end;
-    if (more) load_tiles<TA, TB>(g, A, B, row0, col0, (c + 1) * KC, ra, rb);
-    v32f acc = zero;
+    Raw nxt;
+    if (more) nxt = load_chunk<TA, TB, false>(g, A, B, row0, col0, (c + 1) * KC, vec);
+    __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
     const int64_t kleft = g.k - c * KC;
-    if (kleft >= KC) {
-#pragma unroll
-      for (int kk = 0; kk < KC; ++kk)
-        acc = __builtin_amdgcn_mfma_f32_32x32x1f32(As[buf][kk][arow], Bs[buf][kk][bcol], acc, 0, 0, 0);
-    } else {
-      for (int kk = 0; kk < (int)kleft; ++kk)
-        acc = __builtin_amdgcn_mfma_f32_32x32x1f32(As[buf][kk][arow], Bs[buf][kk][bcol], acc, 0, 0, 0);
-    }
-    S.push(acc, c);
-    if (more) store_tiles<TA, TB>(As[buf ^ 1], Bs[buf ^ 1], ra, rb);
+    v32f acc = (kleft >= KC) ? chain_full<TA, TB>(As[buf], Bs[buf], ai, bi)
+                             : chain_part<TA, TB>(As[buf], Bs[buf], ai, bi, (int)kleft);
+    if (more) store_chunk<TA, TB>(As[buf ^ 1], Bs[buf ^ 1], nxt);
     __syncthreads();
     buf ^= 1;
+    return acc;
+  };
+  // fast chunk: this and the next chunk full and in range (unchecked 16-byte loads)
+  auto run_fast = [&](int64_t c) -> v32f {
+    Raw nxt = load_chunk<TA, TB, true>(g, A, B, row0, col0, (c + 1) * KC, vec);
+    __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
+    v32f acc = chain_full<TA, TB>(As[buf], Bs[buf], ai, bi);
+    __builtin_amdgcn_sched_barrier(0);
+    store_chunk<TA, TB>(As[buf ^ 1], Bs[buf ^ 1], nxt);
+    __syncthreads();
+    buf ^= 1;
+    return acc;
+  };
+  // a chunk of the group: real chunks run, skipped ones (outside [c_begin, c_end)) are +0 partials
+  auto part = [&](int64_t c) -> v32f { return (c >= c_begin && c < c_end) ? run_chunk(c) : zero; };
+
+  // Groups of four chunks.  A complete group's partial ((p0 + p1) + (p2 + p3)) is exactly the level-2
+  // entry that four pushes would build; it is pushed at level 2 with the group index.  The last group may
+  // be partial (nc not a multiple of 4): its r chunks form the lowest entries of the final stack
+  // (r = 1: p0; 2: p0 + p1; 3: levels 1 and 0 hold p0 + p1 and p2) and start the Result.
+  const int64_t ng_full = nc >> 2;
+  int64_t gj = c_begin >> 2;
+  for (; gj < ng_full; ++gj) {
+    const int64_t c = gj * 4;
+    if (c >= c_end) break;  // the rest are skipped chunks
+    v32f q;
+    if (tile_in && c >= c_begin && c + 5 <= c_end && c + 5 <= kfull) {
+      v32f p0 = run_fast(c);
+      v32f p1 = run_fast(c + 1);
+      v32f s01 = p0 + p1;
+      v32f p2 = run_fast(c + 2);
+      v32f p3 = run_fast(c + 3);
+      q = s01 + (p2 + p3);
+    } else {
+      v32f p0 = part(c);
+      v32f p1 = part(c + 1);
+      v32f s01 = p0 + p1;
+      v32f p2 = part(c + 2);
+      v32f p3 = part(c + 3);
+      q = s01 + (p2 + p3);
+    }
+    S.push(q, gj, Smem);
   }
-  // trailing skipped chunks: push +0 partials (their merges turn a -0 partial into +0, as the chain does)
-  for (int64_t c = c_end; c < nc; ++c) S.push(zero, c);
+  // complete groups made only of skipped trailing chunks: their partial is +0
+  for (; gj < ng_full; ++gj) S.push(zero + zero, gj, Smem);
 
   v32f r = zero;
   bool have = false;
-  S.result(r, have, nc);
+  const int rem = (int)(nc & 3);
+  if (rem) {
+    const int64_t c = ng_full * 4;
+    v32f p0 = part(c);
+    if (rem == 1) {
+      r = p0;
+    } else {
+      v32f p1 = part(c + 1);
+      r = p0 + p1;
+      if (rem == 3) r = r + part(c + 2);
+    }
+    have = true;
+  }
+  S.result(r, have, ng_full, Smem);
 
   // store: register v, lane l -> block v/16, row (v%4) + 4*(l/32) + 8*((v%16)/4), column l%32
   const int64_t crow0 = row0 + wr * 32, ccol0 = col0 + wc * 64;
@@ -222,8 +455,14 @@ static hipError_t launch_maxl(const GemmArgs& g, dim3 grid, hipStream_t s) {
 
 int gemm_max_levels() { return 12; }
 
-hipError_t gemm_launch(const GemmArgs& g, hipStream_t s) {
-  if (g.m == 0 || g.n == 0 || g.batch == 0) return hipSuccess;
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
+  if (gin.m == 0 || gin.n == 0 || gin.batch == 0) return hipSuccess;
+  GemmArgs g = gin;
+  // 16-byte vector loads need every row start and batch offset on a 16-byte boundary
+  g.vec = aligned16(g.a) && aligned16(g.b) && g.lda % 8 == 0 && g.ldb % 8 == 0 && g.sa1 % 8 == 0 &&
+          g.sa2 % 8 == 0 && g.sb1 % 8 == 0 && g.sb2 % 8 == 0;
   const int64_t nc = (g.k + KC - 1) / KC;
   int bits = 0;
   while ((int64_t(1) << bits) <= nc) ++bits;  // nc < 2^bits: a push never runs past the top level
