@@ -43,6 +43,20 @@ def step_flops(L=L, d=D, H=H, hd=HD, F=F, V=V, S=S, mb=MB, ranks=8):
     return per_mb * ranks
 
 
+def gemm_traffic_from_profile():
+    """HBM bytes per launch of the dominant GEMM from the committed counter summary, or None when the GEMM
+    source has changed since the counters were taken."""
+    import hashlib
+    prof = os.path.join(ROOT, "profiles", "gemm_8192x16384x2048_launch_and_traffic.md")
+    src = os.path.join(ROOT, "paper_2609_17380_amd", "csrc", "gemm.hip")
+    if not os.path.exists(prof):
+        return None
+    fields = dict(l.split(":", 1) for l in open(prof) if l.startswith(("traffic_bytes_per_launch:", "gemm_source_sha256:")))
+    if fields.get("gemm_source_sha256", "").strip() != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -132,7 +146,7 @@ def main():
     torch.cuda.synchronize()
     blas_ms = e0.elapsed_time(e1) / args.gemm_reps
     blas_tf = gemm_flop / (blas_ms * 1e-3) / 1e12
-    traffic = None
+    traffic = gemm_traffic_from_profile()
     roofline = {"bound": "mfma", "achieved": round(gemm_tf, 2), "peak": PEAK_FP32_MFMA, "unit": "TFLOP/s",
                 "frac": round(gemm_tf / PEAK_FP32_MFMA, 4), "traffic": traffic,
                 "kernel": f"gemm_mfma_kernel {gm}x{gn}x{gk} (fp32 rank-1 MFMA chains)",

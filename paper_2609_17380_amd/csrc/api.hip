@@ -84,7 +84,8 @@ Dims dims_of(const canon_model_cfg* c, int64_t B) {
 bool cfg_ok(const canon_model_cfg* c) {
   return c && c->n_layers >= 1 && c->d_model > 0 && c->n_heads > 0 && c->head_dim > 0 && (c->head_dim % 2) == 0 &&
          (int64_t)c->n_heads * c->head_dim == c->d_model && c->d_ffn > 0 && c->vocab > 0 && c->seq > 0 &&
-         c->micro_seqs > 0 && gemm_k_supported(c->vocab) && gemm_k_supported((int64_t)c->seq * c->micro_seqs) &&
+         c->micro_seqs > 0 && c->vocab <= 131072 && c->d_model <= 32768 && c->seq <= 32768 &&
+         gemm_k_supported(c->vocab) && gemm_k_supported((int64_t)c->seq * c->micro_seqs) &&
          gemm_k_supported(2 * (int64_t)c->d_ffn) && gemm_k_supported(3 * (int64_t)c->d_model);
 }
 
@@ -394,7 +395,7 @@ canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, 
   canon_status st = check_order(order);
   if (st != CANON_OK) return st;
   if (rows < 0 || cols < 1) return CANON_EINVAL;
-  if (cols > (int64_t(1) << 26) || rows > (int64_t(1) << 21)) return CANON_EUNSUPPORTED;
+  if (cols > 32768 || rows > (int64_t(1) << 26)) return CANON_EUNSUPPORTED;  // row kernels stage <= 1024 chunks
   hipStream_t s = as_stream(stream);
   if (dir == CANON_FWD) {
     if (rows > 0 && (!x || !gain || !y || !rstd)) return CANON_EINVAL;
@@ -413,16 +414,17 @@ canon_status canon_softmax_xent(const canon_order* order, int32_t mode, int64_t 
   canon_status st = check_order(order);
   if (st != CANON_OK) return st;
   if (rows < 0 || cols < 1) return CANON_EINVAL;
-  if (cols > (int64_t(1) << 26) || rows > (int64_t(1) << 31)) return CANON_EUNSUPPORTED;
+  if (rows > (int64_t(1) << 31)) return CANON_EUNSUPPORTED;
   hipStream_t s = as_stream(stream);
   if (mode == CANON_SOFTMAX_CAUSAL) {
+    if (cols > 32768) return CANON_EUNSUPPORTED;  // one wavefront stages at most 1024 chunks
     if (rows % cols != 0) return CANON_EINVAL;
     if (rows > 0 && (!x || !out)) return CANON_EINVAL;
     return dev(softmax_causal_launch(rows, cols, (const float*)x, scale, out, s));
   }
   if (mode == CANON_XENT) {
     if (rows > 0 && (!x || !targets || !out || !row_loss)) return CANON_EINVAL;
-    if (rows > (int64_t(1) << 22)) return CANON_EUNSUPPORTED;
+    if (rows > (int64_t(1) << 31) || cols > 131072) return CANON_EUNSUPPORTED;  // at most 4096 chunks per row
     return dev(xent_launch(rows, cols, (const uint16_t*)x, targets, inv_tokens, out, row_loss, mean_loss, s));
   }
   return CANON_EINVAL;

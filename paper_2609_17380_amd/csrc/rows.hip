@@ -82,37 +82,72 @@ __device__ __forceinline__ float wave_max(float m) {
 }
 
 // ------------------------------------------------------------------------------------------------
-// RMSNorm forward: one wavefront per row.
-__global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
-                                                          const uint16_t* __restrict__ gain, float eps, float inv_d,
-                                                          uint16_t* __restrict__ y, float* __restrict__ rstd) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+// Coalesced row reduction for one wavefront.  A segment of 64 chunks (2048 terms) is read coalesced (lane l
+// takes terms 64q + l), staged in LDS as padded rows [chunk][33], and lane c then runs chunk c's chain
+// sequentially from LDS; the chunk partials of all segments collect in `parts` and are folded by lane
+// blocks + wave_fold (Algorithm 2).  term(j) evaluates the j-th term of the row.
+struct WaveStage {
+  float t[64][33];
+};
+
+// Stage one segment (terms seg0 .. seg0 + 2047 of a row of n terms) and write its chunk partials to parts.
+template <class Term>
+__device__ __forceinline__ void wave_segment_chunks(int64_t seg0, int64_t n, WaveStage& st, float* parts, Term term) {
   const int lane = threadIdx.x & 63;
-  if (row >= rows) return;
-  const float* xr = x + row * cols;
-  const int64_t nc = (cols + kChunk - 1) / kChunk;
+  const int64_t nc = (n + kChunk - 1) / kChunk;
+#pragma unroll 4
+  for (int q = 0; q < 32; ++q) {
+    const int local = 64 * q + lane;
+    const int64_t j = seg0 + local;
+    st.t[local >> 5][local & 31] = (j < n) ? term(j) : 0.0f;
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  const int64_t c = seg0 / kChunk + lane;
+  if (c < nc) {
+    const int64_t k1 = n - c * kChunk < kChunk ? n - c * kChunk : kChunk;
+    float s = 0.0f;
+    for (int i = 0; i < (int)k1; ++i) s = s + st.t[lane][i];
+    parts[c] = s;
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+}
+
+template <class Term>
+__device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* parts, Term term) {
+  const int lane = threadIdx.x & 63;
+  const int64_t nc = (n + kChunk - 1) / kChunk;
+  for (int64_t seg0 = 0; seg0 < n; seg0 += 64 * kChunk) wave_segment_chunks(seg0, n, st, parts, term);
   const int64_t G = block_chunks(nc, 64);
   const int64_t c0 = lane * G, c1 = (c0 + G < nc) ? c0 + G : nc;
   LocalFold f;
-  for (int64_t c = c0; c < c1; ++c) {
-    float s = 0.0f;
-    const int64_t k1 = (c + 1) * kChunk < cols ? (c + 1) * kChunk : cols;
-    for (int64_t k = c * kChunk; k < k1; ++k) {
-      float v = xr[k];
-      float sq = v * v;
-      s = s + sq;
-    }
-    f.push(s);
-  }
-  float p = f.result();
-  float ss = wave_fold(p, (int)((nc + G - 1) / G));
-  ss = __shfl(ss, 0, 64);
+  for (int64_t c = c0; c < c1; ++c) f.push(parts[c]);
+  float tot = wave_fold(f.result(), (int)((nc + G - 1) / G));
+  return __shfl(tot, 0, 64);
+}
+
+constexpr int kMaxRowChunks = 64 * 16;  // rows up to 32768 terms in the wave kernels
+
+// RMSNorm forward: one wavefront per row, 4 rows per workgroup.
+__global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
+                                                          const uint16_t* __restrict__ gain, float eps, float inv_d,
+                                                          uint16_t* __restrict__ y, float* __restrict__ rstd) {
+  __shared__ WaveStage st[4];
+  __shared__ float parts[4][kMaxRowChunks];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= rows) return;
+  const float* xr = x + row * cols;
+  float ss = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
+    float v = xr[j];
+    return v * v;
+  });
   float ms = ss * inv_d;
   float var = ms + eps;
   float r = 1.0f / __builtin_sqrtf(var);
   if (lane == 0) rstd[row] = r;
-  const int64_t e0 = c0 * kChunk, e1 = (c1 * kChunk < cols) ? c1 * kChunk : cols;
-  for (int64_t k = e0; k < e1; ++k) {
+  for (int64_t k = lane; k < cols; k += 64) {
     float xv = xr[k] * r;
     float yv = xv * bf16_to_f32(gain[k]);
     y[row * cols + k] = f32_to_bf16(yv);
@@ -125,35 +160,23 @@ __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t 
                                                           const float* __restrict__ rstd,
                                                           const float* __restrict__ dy, float inv_d,
                                                           float* __restrict__ dx) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+  __shared__ WaveStage st[4];
+  __shared__ float parts[4][kMaxRowChunks];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;
   const float* xr = x + row * cols;
   const float* dyr = dy + row * cols;
-  const int64_t nc = (cols + kChunk - 1) / kChunk;
-  const int64_t G = block_chunks(nc, 64);
-  const int64_t c0 = lane * G, c1 = (c0 + G < nc) ? c0 + G : nc;
-  LocalFold f;
-  for (int64_t c = c0; c < c1; ++c) {
-    float s = 0.0f;
-    const int64_t k1 = (c + 1) * kChunk < cols ? (c + 1) * kChunk : cols;
-    for (int64_t k = c * kChunk; k < k1; ++k) {
-      float gy = dyr[k] * bf16_to_f32(gain[k]);
-      float pr = gy * xr[k];
-      s = s + pr;
-    }
-    f.push(s);
-  }
-  float p = f.result();
-  float dot = wave_fold(p, (int)((nc + G - 1) / G));
-  dot = __shfl(dot, 0, 64);
+  float dot = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
+    float gy = dyr[j] * bf16_to_f32(gain[j]);
+    return gy * xr[j];
+  });
   const float r = rstd[row];
   float r2 = r * r;
   float r3 = r2 * r;
   float dd = dot * inv_d;
   float q = r3 * dd;
-  const int64_t e0 = c0 * kChunk, e1 = (c1 * kChunk < cols) ? c1 * kChunk : cols;
-  for (int64_t k = e0; k < e1; ++k) {
+  for (int64_t k = lane; k < cols; k += 64) {
     float gy = dyr[k] * bf16_to_f32(gain[k]);
     float a = r * gy;
     float b = xr[k] * q;
@@ -161,17 +184,19 @@ __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t 
   }
 }
 
-// dgain[k] = R1 over rows t of RN(dy[t,k] * RN(x[t,k] * rstd[t])).  64 columns per workgroup; the four
-// wavefronts take four aligned power-of-two groups of row chunks.
-__global__ __launch_bounds__(256) void rownorm_dgain_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
-                                                            const float* __restrict__ rstd,
-                                                            const float* __restrict__ dy,
-                                                            float* __restrict__ dgain) {
-  __shared__ float part[4][64];
+// dgain[k] = R1 over rows t of RN(dy[t,k] * RN(x[t,k] * rstd[t])).  A workgroup of 16 wavefronts takes 64
+// columns (lane = column, so row reads are coalesced); wavefront q folds the aligned power-of-two group of
+// row chunks [q*G, q*G + G), then the 16 group results are folded with the pass-through rule.
+constexpr int kDgainGroups = 16;
+__global__ __launch_bounds__(1024) void rownorm_dgain_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
+                                                             const float* __restrict__ rstd,
+                                                             const float* __restrict__ dy,
+                                                             float* __restrict__ dgain) {
+  __shared__ float part[kDgainGroups][64];
   const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
   const int64_t col = (int64_t)blockIdx.x * 64 + lane;
   const int64_t nc = (rows + kChunk - 1) / kChunk;
-  const int64_t G = block_chunks(nc, 4);
+  const int64_t G = block_chunks(nc, kDgainGroups);
   const int64_t c0 = grp * G, c1 = (c0 + G < nc) ? c0 + G : nc;
   LocalFold f;
   if (col < cols) {
@@ -189,12 +214,16 @@ __global__ __launch_bounds__(256) void rownorm_dgain_kernel(int64_t rows, int64_
   part[grp][lane] = f.result();
   __syncthreads();
   if (grp == 0 && col < cols) {
-    float a = part[0][lane];
-    if (G < nc) a = a + part[1][lane];
-    float b = part[2][lane];
-    if (3 * G < nc) b = b + part[3][lane];
-    if (2 * G < nc) a = a + b;
-    dgain[col] = a;
+    // fold the group results: level by level, a node adds its right neighbour when that subtree is real
+    float v[kDgainGroups];
+#pragma unroll
+    for (int q = 0; q < kDgainGroups; ++q) v[q] = part[q][lane];
+#pragma unroll
+    for (int sdist = 1; sdist < kDgainGroups; sdist <<= 1)
+#pragma unroll
+      for (int q = 0; q + sdist < kDgainGroups; q += 2 * sdist)
+        if ((q + sdist) * G < nc) v[q] = v[q] + v[q + sdist];
+    dgain[col] = v[0];
   }
 }
 
@@ -217,46 +246,36 @@ hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const 
   hipLaunchKernelGGL(rownorm_bwd_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, rows, cols, x, gain, rstd,
                      dy, inv_d, dx);
   if (dgain)
-    hipLaunchKernelGGL(rownorm_dgain_kernel, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s, rows, cols, x, rstd,
-                       dy, dgain);
+    hipLaunchKernelGGL(rownorm_dgain_kernel, dim3((unsigned)((cols + 63) / 64)), dim3(1024), 0, s, rows, cols, x,
+                       rstd, dy, dgain);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------------------------
-// Causal softmax of raw scores: row r is query i = r mod cols; one wavefront per row.
+// Causal softmax of raw scores: row r is query i = r mod cols; one wavefront per row, coalesced.
 __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64_t cols, const float* __restrict__ raw,
                                                              float scale, uint16_t* __restrict__ probs) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+  __shared__ WaveStage st[4];
+  __shared__ float parts[4][kMaxRowChunks];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;
   const int64_t i = row % cols;
   const float* rr = raw + row * cols;
-  const int64_t nc = (cols + kChunk - 1) / kChunk;
-  const int64_t G = block_chunks(nc, 64);
-  const int64_t c0 = lane * G, c1 = (c0 + G < nc) ? c0 + G : nc;
-  const int64_t e0 = c0 * kChunk, e1 = (c1 * kChunk < cols) ? c1 * kChunk : cols;
   float m = -__builtin_inff();
-  for (int64_t j = e0; j < e1 && j <= i; ++j) m = fmaxf(m, rr[j] * scale);
+  for (int64_t j = lane; j <= i; j += 64) m = fmaxf(m, rr[j] * scale);
   m = wave_max(m);
-  LocalFold f;
-  for (int64_t c = c0; c < c1; ++c) {
-    float s = 0.0f;
-    const int64_t k1 = (c + 1) * kChunk < cols ? (c + 1) * kChunk : cols;
-    for (int64_t j = c * kChunk; j < k1; ++j) {
-      float e = 0.0f;
-      if (j <= i) {
-        float sc = rr[j] * scale;
-        e = cexp(sc - m);
-      }
-      s = s + e;
+  // masked keys enter the chain as +0 terms
+  const float S = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
+    float e = 0.0f;
+    if (j <= i) {
+      float sc = rr[j] * scale;
+      e = cexp(sc - m);
     }
-    f.push(s);
-  }
-  float p = f.result();
-  float S = wave_fold(p, (int)((nc + G - 1) / G));
-  S = __shfl(S, 0, 64);
+    return e;
+  });
   const float rcp = 1.0f / S;
-  for (int64_t j = e0; j < e1; ++j) {
+  for (int64_t j = lane; j < cols; j += 64) {
     uint16_t o = 0;
     if (j <= i) {
       float sc = rr[j] * scale;
@@ -276,33 +295,32 @@ hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, f
 }
 
 // ------------------------------------------------------------------------------------------------
-// Cross-entropy: one 256-thread workgroup per row.
+// Cross-entropy: one 256-thread workgroup per row.  The four wavefronts take the row's 2048-term segments
+// round-robin and write the chunk partials; the partials are then folded across the workgroup.
+constexpr int kMaxXentChunks = 4096;  // vocabularies up to 131072
 __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, const uint16_t* __restrict__ logits,
                                                    const int32_t* __restrict__ targets, float inv_tokens,
                                                    uint16_t* __restrict__ dlogits, float* __restrict__ row_loss) {
+  __shared__ WaveStage st[4];
+  __shared__ float parts[kMaxXentChunks];
   __shared__ float red[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = blockIdx.x;
   const uint16_t* lr = logits + row * vocab;
+  float m = -__builtin_inff();
+  for (int64_t j = threadIdx.x; j < vocab; j += 256) m = fmaxf(m, bf16_to_f32(lr[j]));
+  m = wave_max(m);
+  if (lane == 0) red[w] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  for (int64_t seg0 = (int64_t)w * 64 * kChunk; seg0 < vocab; seg0 += 4 * 64 * kChunk)
+    wave_segment_chunks(seg0, vocab, st[w], parts, [&](int64_t j) { return cexp(bf16_to_f32(lr[j]) - m); });
+  __syncthreads();
   const int64_t nc = (vocab + kChunk - 1) / kChunk;
   const int64_t G = block_chunks(nc, 256);
   const int64_t c0 = threadIdx.x * G, c1 = (c0 + G < nc) ? c0 + G : nc;
-  const int64_t e0 = c0 * kChunk, e1 = (c1 * kChunk < vocab) ? c1 * kChunk : vocab;
-  float m = -__builtin_inff();
-  for (int64_t j = e0; j < e1; ++j) m = fmaxf(m, bf16_to_f32(lr[j]));
-  m = wave_max(m);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
-  __syncthreads();
-  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   LocalFold f;
-  for (int64_t c = c0; c < c1; ++c) {
-    float s = 0.0f;
-    const int64_t k1 = (c + 1) * kChunk < vocab ? (c + 1) * kChunk : vocab;
-    for (int64_t j = c * kChunk; j < k1; ++j) {
-      float e = cexp(bf16_to_f32(lr[j]) - m);
-      s = s + e;
-    }
-    f.push(s);
-  }
+  for (int64_t c = c0; c < c1; ++c) f.push(parts[c]);
   const float S = block_fold(f.result(), (nc + G - 1) / G);
   const int32_t y = targets[row];
   const bool valid = y >= 0 && y < vocab;
@@ -312,7 +330,7 @@ __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, 
   }
   const float rcp = 1.0f / S;
   if (dlogits) {
-    for (int64_t j = e0; j < e1; ++j) {
+    for (int64_t j = threadIdx.x; j < vocab; j += 256) {
       float e = cexp(bf16_to_f32(lr[j]) - m);
       float p = e * rcp;
       float q = p - (j == y ? 1.0f : 0.0f);
