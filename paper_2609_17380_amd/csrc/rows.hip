@@ -114,11 +114,16 @@ __device__ __forceinline__ void wave_segment_chunks(int64_t seg0, int64_t n, Wav
   __builtin_amdgcn_wave_barrier();
 }
 
+// nz: terms at index >= nz are known to be +0 (masked); chunks made only of them have partial +0 and are not
+// staged.
 template <class Term>
-__device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* parts, Term term) {
+__device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* parts, Term term, int64_t nz) {
   const int lane = threadIdx.x & 63;
   const int64_t nc = (n + kChunk - 1) / kChunk;
-  for (int64_t seg0 = 0; seg0 < n; seg0 += 64 * kChunk) wave_segment_chunks(seg0, n, st, parts, term);
+  for (int64_t seg0 = 0; seg0 < n && seg0 < nz; seg0 += 64 * kChunk) wave_segment_chunks(seg0, n, st, parts, term);
+  for (int64_t c = (nz + kChunk - 1) / kChunk + lane; c < nc; c += 64) parts[c] = 0.0f;
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
   const int64_t G = block_chunks(nc, 64);
   const int64_t c0 = lane * G, c1 = (c0 + G < nc) ? c0 + G : nc;
   LocalFold f;
@@ -142,7 +147,7 @@ __global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t 
   float ss = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
     float v = xr[j];
     return v * v;
-  });
+  }, cols);
   float ms = ss * inv_d;
   float var = ms + eps;
   float r = 1.0f / __builtin_sqrtf(var);
@@ -170,7 +175,7 @@ __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t 
   float dot = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
     float gy = dyr[j] * bf16_to_f32(gain[j]);
     return gy * xr[j];
-  });
+  }, cols);
   const float r = rstd[row];
   float r2 = r * r;
   float r3 = r2 * r;
@@ -273,7 +278,7 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
       e = cexp(sc - m);
     }
     return e;
-  });
+  }, i + 1);
   const float rcp = 1.0f / S;
   for (int64_t j = lane; j < cols; j += 64) {
     uint16_t o = 0;
