@@ -57,6 +57,133 @@ def gemm_traffic_from_profile():
     return int(fields["traffic_bytes_per_launch"])
 
 
+# GEMM shapes of the 1B decoder over one microbatch of 8192 tokens: (name, m, n, k, A stored [k, m], B stored [n, k])
+GEMM_SWEEP = [("qkv", 8192, 6144, 2048, 0, 1), ("out", 8192, 2048, 2048, 0, 1), ("gate_up", 8192, 16384, 2048, 0, 1),
+              ("down", 8192, 2048, 8192, 0, 1), ("head", 8192, 50304, 2048, 0, 1),
+              ("wgrad_qkv", 6144, 2048, 8192, 1, 0), ("wgrad_out", 2048, 2048, 8192, 1, 0),
+              ("wgrad_gate_up", 16384, 2048, 8192, 1, 0), ("wgrad_down", 2048, 8192, 8192, 1, 0),
+              ("wgrad_head", 50304, 2048, 8192, 1, 0),
+              ("dgrad_qkv", 8192, 2048, 6144, 0, 0), ("dgrad_gate_up", 8192, 2048, 16384, 0, 0),
+              ("dgrad_down", 8192, 8192, 2048, 0, 0), ("dgrad_head", 8192, 2048, 50304, 0, 0)]
+
+
+def _timed(torch, stream, fn, reps, warm=1):
+    for _ in range(warm):
+        fn()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(reps):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def _hbm(ms, nbytes):
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "ms": round(ms, 4), "bytes": int(nbytes), "achieved": round(gbs, 1), "unit": "GB/s",
+            "peak": PEAK_HBM, "frac": round(gbs / PEAK_HBM, 4)}
+
+
+def kernel_table(C, I, torch, np, stream, dev):
+    """Each entry point at the shapes of the single-kernel workloads: the GEMM sweep over the 1B shapes, RMSNorm
+    over a microbatch, causal softmax at 16 heads x 2048 x 2048, cross-entropy 8192 x 50304, the ordered sum of 8
+    gradient buffers of 1.2e9 fp32, AdamW over 1.2e9 parameters, and one decoder block forward + backward.
+    Inputs are seeded N(0, sigma) draws made on the device (the values do not change the work); bytes are the
+    algorithmic minimum each kernel must move."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+
+    def randn(shape, std=1.0, dtype=torch.float32):
+        return (torch.randn(shape, generator=g, device=dev, dtype=torch.float32) * std).to(dtype)
+
+    out = {}
+    print("bench: kernel table", file=sys.stderr, flush=True)
+    for name, m, n, k, ta, tb in GEMM_SWEEP:
+        a = randn((k, m) if ta else (m, k), dtype=torch.bfloat16)
+        b = randn((n, k) if tb else (k, n), dtype=torch.bfloat16)
+        c = torch.empty((m, n), dtype=torch.float32, device=dev)
+        lda, ldb = a.shape[1], b.shape[1]
+        ms = _timed(torch, stream, lambda: C.gemm(m, n, k, a, lda, b, ldb, c, n, ta, tb, stream=stream), 3)
+        tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+        out[f"gemm_{name}_{m}x{n}x{k}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tf, 2),
+                                           "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
+                                           "frac": round(tf / PEAK_FP32_MFMA, 4),
+                                           "pct_bf16_peak": round(100 * tf / PEAK_BF16_MFMA, 3)}
+        del a, b, c
+
+    T, d = MB * S, D
+    x = randn((T, d))
+    gain = torch.full((d,), 0x3F80, dtype=torch.int16, device=dev)
+    y = torch.empty((T, d), dtype=torch.int16, device=dev)
+    rstd = torch.empty(T, dtype=torch.float32, device=dev)
+    ms = _timed(torch, stream, lambda: C.rownorm(C.FWD, T, d, x, gain, 1e-5, y=y, rstd=rstd, stream=stream), 20)
+    out[f"rownorm_fwd_{T}x{d}"] = _hbm(ms, T * d * (4 + 2) + T * 4 + d * 2)
+    dy, dx = randn((T, d)), torch.empty((T, d), dtype=torch.float32, device=dev)
+    dgain = torch.empty(d, dtype=torch.float32, device=dev)
+    ms = _timed(torch, stream, lambda: C.rownorm(C.BWD, T, d, x, gain, 1e-5, rstd=rstd, dy=dy, dx=dx, dgain=dgain,
+                                                stream=stream), 20)
+    out[f"rownorm_bwd_{T}x{d}"] = _hbm(ms, T * d * 12 + T * 4 + d * 6)
+    del x, y, rstd, dy, dx, dgain
+
+    bh = 16
+    raw = randn((bh, S, S))
+    probs = torch.empty((bh, S, S), dtype=torch.int16, device=dev)
+    scale = float(np.float32(1 / np.sqrt(128)))
+    ms = _timed(torch, stream, lambda: C.softmax_xent(C.SOFTMAX_CAUSAL, bh * S, S, raw, probs, scale=scale,
+                                                     stream=stream), 10)
+    out[f"softmax_causal_{bh}x{S}x{S}"] = _hbm(ms, bh * (S * (S + 1) // 2) * 4 + bh * S * S * 2)
+    del raw, probs
+
+    logits = randn((T, V), std=2.0, dtype=torch.bfloat16)
+    tgt = torch.randint(0, V, (T,), generator=g, device=dev, dtype=torch.int32)
+    dl = torch.empty((T, V), dtype=torch.bfloat16, device=dev)
+    rl = torch.empty(T, dtype=torch.float32, device=dev)
+    ml = torch.empty(1, dtype=torch.float32, device=dev)
+    ms = _timed(torch, stream, lambda: C.softmax_xent(C.XENT, T, V, logits, dl, targets=tgt, inv_tokens=1.0 / T,
+                                                     row_loss=rl, mean_loss=ml, stream=stream), 10)
+    out[f"xent_{T}x{V}"] = _hbm(ms, T * V * 4 + T * 8)
+    del logits, tgt, dl, rl, ml
+
+    n = 1_200_000_000
+    grads = [randn((n,), std=1e-3) for _ in range(8)]
+    gsum = torch.empty(n, dtype=torch.float32, device=dev)
+    ms = _timed(torch, stream, lambda: C.grad_accum(C.DPPlan(1, 8, 1), n, grads, gsum, stream=stream), 3)
+    out["grad_accum_8x1.2e9"] = _hbm(ms, 9 * n * 4)
+    del grads
+    torch.cuda.empty_cache()
+    p = randn((n,), std=0.02, dtype=torch.bfloat16)
+    m1 = torch.zeros(n, dtype=torch.float32, device=dev)
+    v1 = torch.zeros(n, dtype=torch.float32, device=dev)
+    consts = C.AdamWConsts(*I.adamw_constants())
+    ms = _timed(torch, stream, lambda: C.adamw([p], [m1], [v1], [gsum], [1], consts, stream=stream), 3)
+    out["adamw_1.2e9"] = _hbm(ms, n * 24)
+    del p, m1, v1, gsum
+    torch.cuda.empty_cache()
+
+    cfg = C.ModelCfg(1, D, H, HD, F, V, S, 1, np.float32(1e-5))
+    xb, dyb = randn((S, D)), randn((S, D)).to(torch.bfloat16).float()
+    w = [torch.full((D,), 0x3F80, dtype=torch.int16, device=dev), randn((3 * D, D), 0.02, torch.bfloat16),
+         randn((D, D), 0.02, torch.bfloat16), torch.full((D,), 0x3F80, dtype=torch.int16, device=dev),
+         randn((2 * F, D), 0.02, torch.bfloat16), randn((D, F), 0.02, torch.bfloat16)]
+    dw = [torch.empty(t.shape, dtype=torch.float32, device=dev) for t in w]
+    cos, sin = I.rope_tables(S, HD)
+    cos, sin = torch.from_numpy(cos).to(dev), torch.from_numpy(sin).to(dev)
+    yb, dxb = torch.empty_like(xb), torch.empty_like(xb)
+    wsb = torch.empty(C.block_workspace_bytes(cfg, 1), dtype=torch.uint8, device=dev)
+    ms = _timed(torch, stream, lambda: C.block_fwd_bwd(cfg, 1, xb, dyb, w, cos, sin, yb, dxb, dw, wsb,
+                                                      stream=stream), 3)
+    fl = step_flops(L=1, mb=1, ranks=1) - 3 * 2 * S * D * V  # one block, no head
+    out[f"block_fwd_bwd_seq{S}"] = {"bound": "mfma", "ms": round(ms, 3), "achieved": round(fl / (ms * 1e-3) / 1e12, 2),
+                                    "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
+                                    "frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA, 4)}
+    for k_, v_ in out.items():
+        print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({100 * v_['frac']:.1f}%)",
+              file=sys.stderr, flush=True)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -64,6 +191,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gemm-reps", type=int, default=10)
+    ap.add_argument("--no-kernel-table", action="store_true")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -152,6 +280,10 @@ def main():
                 "kernel": f"gemm_mfma_kernel {gm}x{gn}x{gk} (fp32 rank-1 MFMA chains)",
                 "avg_launch_ms": round(gemm_ms, 4), "pct_bf16_peak": round(100 * gemm_tf / PEAK_BF16_MFMA, 3)}
 
+    del ws
+    torch.cuda.empty_cache()
+    kernels = {} if args.no_kernel_table else kernel_table(C, I, torch, np, stream, dev)
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -183,7 +315,7 @@ def main():
             R * PLAN[0] * MB * S / (ms * 1e-3), 1),
         "gemm_tflops": round(gemm_tf, 2), "gemm_pct_bf16_peak": round(100 * gemm_tf / PEAK_BF16_MFMA, 3),
         "gemm_unconstrained_library_tflops": round(blas_tf, 2),
-        "roofline": roofline, "cpu_baseline": cpu, "loss": float(loss.item()),
+        "roofline": roofline, "cpu_baseline": cpu, "loss": float(loss.item()), "kernels": kernels,
     }
     print(json.dumps(out), flush=True)
 

@@ -57,3 +57,32 @@ def chunk_partials(terms, chunk=32):
 
 def canonical_sum(terms, chunk=32):
     return padded_tree(chunk_partials(terms, chunk))
+
+
+def canonical_dot_r0(a, b, chunk=32):
+    """The canonical dot product of two float sequences in exact rational arithmetic with the R0 rounding
+    model (DAZ inputs, one round to nearest even per fma, flush of tiny results): fma chains of `chunk` terms
+    from +0, then the zero-padded tree with absent padding.  Valid over the whole float range."""
+    import exact_r0 as R
+    n = len(a)
+    parts = []
+    for c0 in range(0, n, chunk):
+        s = np.float32(0.0)
+        for x, y in zip(a[c0:c0 + chunk], b[c0:c0 + chunk]):
+            s = R.fma(x, y, s)
+        parts.append(s)
+    if not parts:
+        return np.float32(0.0)
+    size = 1
+    while size < len(parts):
+        size *= 2
+
+    def rec(lo, sz):
+        if sz == 1:
+            return parts[lo]
+        half = sz // 2
+        if lo + half >= len(parts):
+            return rec(lo, half)
+        return R.add(rec(lo, half), rec(lo + half, half))
+
+    return rec(0, size)

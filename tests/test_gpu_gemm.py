@@ -109,3 +109,19 @@ def test_full_size_sampled(name, m, n, k, ta, tb):
     got = np.array([c[i, j] for i, j in idx], np.float32)
     want = np.array([oracle.rdot_bf16(a[:, i] if ta else a[i], b[j] if tb else b[:, j]) for i, j in idx], np.float32)
     assert_bits(got, want, name)
+
+
+@pytest.mark.parametrize("kind", ["wide", "tiny", "ties", "cancel", "huge"])
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+@pytest.mark.parametrize("m,n,k", [(130, 260, 192), (70, 130, 167)])
+def test_adversarial_operands(kind, ta, tb, m, n, k):
+    # the matrix-core chains against the oracle where rounding decides: subnormal products and partial sums
+    # (flush), bf16 subnormal operands (read as zero), round-half-even ties, exact cancellation with signed
+    # zeros, overflow to infinity; vector-load tiles and ragged tiles
+    import adversarial as ADV
+    print(f"gemm adversarial {kind} {m}x{n}x{k} ta={ta} tb={tb}", flush=True)
+    a, b = ADV.gemm_operands(kind, m, n, k, seed=11)
+    a_st = np.ascontiguousarray(a.T) if ta else a
+    b_st = np.ascontiguousarray(b.T) if tb else b
+    assert_bits(gpu_gemm(a_st, b_st, ta, tb, m, n, k), oracle.gemm(a_st, b_st, bool(ta), bool(tb)),
+                f"{kind} {m}x{n}x{k}")

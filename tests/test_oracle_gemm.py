@@ -84,3 +84,29 @@ def test_cfg1_error_bound_and_negative_control():
                 s = np.float32(s + np.float32(af[i, kk] * bf[kk, j]))
             differ += bits(s) != bits(c[i, j])
     assert differ > 0
+
+
+@pytest.mark.parametrize("kind", ["wide", "tiny", "ties", "cancel"])
+def test_adversarial_operands_match_exact_model(kind):
+    # every output of a 6x7x70 product (three chunks, a ragged one) against the exact-rational R0 model of the
+    # canonical dot product: subnormal products and partials, ties, cancellation and signed zeros
+    import adversarial as ADV
+    a, b = ADV.gemm_operands(kind, 6, 7, 70)
+    c = oracle.gemm(a, b)
+    af, bf = widen(a), widen(b)
+    for i in range(6):
+        for j in range(7):
+            want = CF.canonical_dot_r0([float(x) for x in af[i]], [float(y) for y in bf[:, j]])
+            assert bits(c[i, j]) == bits(want), (kind, i, j, c[i, j], want)
+
+
+def test_adversarial_closed_forms():
+    import adversarial as ADV
+    # cancel: every product meets its negation next in the chain, so every partial and every output is +0
+    a, b = ADV.gemm_operands("cancel", 9, 11, 2 * 32 * 3)
+    assert np.all(bits(oracle.gemm(a, b)) == 0)
+    # huge: same-signed products of at least 2^124 overflow inside the first chunk: +-inf by the column's sign
+    a, b = ADV.gemm_operands("huge", 5, 8, 70)
+    c = oracle.gemm(a, b)
+    sign = np.where(b[0] >> 15, -1.0, 1.0).astype(np.float32)
+    assert np.array_equal(bits(c), bits(np.broadcast_to(sign * np.float32(np.inf), c.shape)))
