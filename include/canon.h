@@ -93,7 +93,9 @@ canon_status canon_gemm_strided_batched(const canon_order* order, int32_t trans_
    dir = CANON_FWD: y (bf16 [rows, cols]) = bf16(RN(RN(x*r)*g)) with r = CRdiv(1, CRsqrt(RN(ms + eps))),
        ms = RN(R1(x*x) * RN(1/cols)); rstd (fp32 [rows]) = r.  dy, dx, dgain unused (may be NULL).
    dir = CANON_BWD: inputs x, gain, rstd (from the forward), dy (fp32 [rows, cols]); outputs dx (fp32
-       [rows, cols]) and, if dgain != NULL, dgain (fp32 [cols]) = R1 over rows of RN(dy*RN(x*r)). */
+       [rows, cols]) and, if dgain != NULL, dgain (fp32 [cols]) = R1 over rows of RN(dy*RN(x*r)).
+       dx also serves as scratch for the dgain chunk partials before it receives its values, so dx must not
+       overlap x, dy, rstd, gain or dgain (CANON_EINVAL otherwise). */
 enum { CANON_FWD = 0, CANON_BWD = 1 };
 canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, int64_t cols, const float* x,
                            const uint16_t* gain, float eps, uint16_t* y, float* rstd, const float* dy, float* dx,

@@ -403,6 +403,18 @@ canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, 
   }
   if (dir == CANON_BWD) {
     if (rows > 0 && (!x || !gain || !rstd || !dy || !dx)) return CANON_EINVAL;
+    if (rows > 0) {  // dx is written before x, dy, rstd, gain are last read: no overlap allowed
+      const char* d0 = (const char*)dx;
+      const char* d1 = d0 + sizeof(float) * rows * cols;
+      auto apart = [&](const void* p, size_t bytes) {
+        const char* q = (const char*)p;
+        return !p || q + bytes <= d0 || q >= d1;
+      };
+      if (!apart(x, sizeof(float) * rows * cols) || !apart(dy, sizeof(float) * rows * cols) ||
+          !apart(rstd, sizeof(float) * rows) || !apart(gain, sizeof(uint16_t) * cols) ||
+          !apart(dgain, sizeof(float) * cols))
+        return CANON_EINVAL;
+    }
     return dev(rownorm_bwd_launch(rows, cols, x, gain, rstd, dy, dx, dgain, s));
   }
   return CANON_EINVAL;

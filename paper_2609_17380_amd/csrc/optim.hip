@@ -13,8 +13,101 @@ static inline unsigned grid_for(int64_t n) {
   return (unsigned)(b < 65536 * 16 ? b : 65536 * 16);  // grid-stride beyond this
 }
 
-// One pass over N*accum buffers: per element, Algorithm 1 in registers with a binary-carry stack over the
-// replica partials.
+// Algorithm 1 for one element with its buffers' values in v[0..NB): rank r's microbatches are v[r*accum ..
+// r*accum + accum), ranks in mesh order (shard index fastest).  Each microbatch gradient is scaled by
+// RN(1/accum) and summed from +0; ranks of one replica are summed in ascending shard order and scaled by
+// RN(1/dp_shard); the replica partials go through Algorithm 2's binary-carry stack (earlier block on the
+// left, Result from the lowest level up) and the total is scaled by RN(1/dp_replicate).  The loop over the
+// buffers is unrolled with constant indices, so v stays in registers; the branches depend only on the plan.
+template <int NB>
+__device__ __forceinline__ float plan_element(const float (&v)[NB], int accum, int dp_shard, float inv_accum,
+                                              float inv_shard, float inv_rep) {
+  float stack[8];
+  int pushed = 0;
+  float g = 0.0f, inner = 0.0f;
+  int k = 0, shard = 0;
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    g = ((k == 0) ? 0.0f : g) + v[b] * inv_accum;
+    if (++k == accum) {
+      k = 0;
+      inner = (shard == 0) ? g : inner + g;
+      if (++shard == dp_shard) {
+        shard = 0;
+        float part = inner * inv_shard;
+#pragma unroll
+        for (int L = 0; L < 8; ++L) {
+          if ((pushed >> L) & 1) {
+            part = stack[L] + part;
+          } else {
+            stack[L] = part;
+            break;
+          }
+        }
+        ++pushed;
+      }
+    }
+  }
+  float res = 0.0f;
+  bool have = false;
+#pragma unroll
+  for (int L = 0; L < 8; ++L) {
+    if ((pushed >> L) & 1) {
+      if (!have) {
+        res = stack[L];
+        have = true;
+      } else {
+        res = stack[L] + res;
+      }
+    }
+  }
+  return res * inv_rep;
+}
+
+// NB buffers known at compile time: four elements per thread with 16-byte streaming loads, all NB loads
+// issued before the arithmetic; the n % 4 tail is done by the first threads of the grid.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int NB>
+__global__ __launch_bounds__(256) void grad_accum_vec_kernel(int accum, int dp_shard, int64_t n, PlanPtrs ptrs,
+                                                             float inv_accum, float inv_shard, float inv_rep,
+                                                             float* __restrict__ out) {
+  const int64_t n4 = n >> 2;
+  const int64_t stride = (int64_t)gridDim.x * 256;
+  const int64_t tid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  for (int64_t i = tid; i < n4; i += stride) {
+    f32x4 q[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) q[b] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(ptrs.p[b]) + i);
+    f32x4 r;
+    {
+      float v[NB];
+#pragma unroll
+      for (int b = 0; b < NB; ++b) v[b] = q[b].x;
+      r.x = plan_element<NB>(v, accum, dp_shard, inv_accum, inv_shard, inv_rep);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) v[b] = q[b].y;
+      r.y = plan_element<NB>(v, accum, dp_shard, inv_accum, inv_shard, inv_rep);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) v[b] = q[b].z;
+      r.z = plan_element<NB>(v, accum, dp_shard, inv_accum, inv_shard, inv_rep);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) v[b] = q[b].w;
+      r.w = plan_element<NB>(v, accum, dp_shard, inv_accum, inv_shard, inv_rep);
+    }
+    __builtin_nontemporal_store(r, reinterpret_cast<f32x4*>(out) + i);
+  }
+  const int64_t t = n4 * 4 + tid;
+  if (t < n) {
+    float v[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) v[b] = ptrs.p[b][t];
+    out[t] = plan_element<NB>(v, accum, dp_shard, inv_accum, inv_shard, inv_rep);
+  }
+}
+
+// Any plan up to kMaxFusedBuffers buffers, one element per thread (the same walk as plan_element, with the
+// buffers read as the walk reaches them).
 __global__ __launch_bounds__(256) void grad_accum_fused_kernel(int accum, int dp_shard, int dp_replicate, int64_t n,
                                                                PlanPtrs ptrs, float inv_accum, float inv_shard,
                                                                float inv_rep, float* __restrict__ out) {
@@ -25,10 +118,7 @@ __global__ __launch_bounds__(256) void grad_accum_fused_kernel(int accum, int dp
     float inner = 0.0f;
     for (int r = 0; r < N; ++r) {
       float g = 0.0f;
-      for (int k = 0; k < accum; ++k) {
-        float t = ptrs.p[r * accum + k][i] * inv_accum;
-        g = g + t;
-      }
+      for (int k = 0; k < accum; ++k) g = g + ptrs.p[r * accum + k][i] * inv_accum;
       const int shard = r % dp_shard;
       inner = (shard == 0) ? g : inner + g;
       if (shard == dp_shard - 1) {
@@ -50,8 +140,12 @@ __global__ __launch_bounds__(256) void grad_accum_fused_kernel(int accum, int dp
 #pragma unroll
     for (int L = 0; L < 8; ++L) {
       if ((pushed >> L) & 1) {
-        if (!have) { res = stack[L]; have = true; }
-        else res = stack[L] + res;
+        if (!have) {
+          res = stack[L];
+          have = true;
+        } else {
+          res = stack[L] + res;
+        }
       }
     }
     out[i] = res * inv_rep;
@@ -63,6 +157,25 @@ hipError_t grad_accum_fused_launch(int accum, int dp_shard, int dp_replicate, in
   if (n == 0) return hipSuccess;
   const float inv_accum = (float)(1.0 / accum), inv_shard = (float)(1.0 / dp_shard),
               inv_rep = (float)(1.0 / dp_replicate);  // RN32 of each reciprocal
+  const int nb = accum * dp_shard * dp_replicate;
+  bool aligned = ((uintptr_t)out & 15) == 0;
+  for (int b = 0; b < nb; ++b) aligned = aligned && ((uintptr_t)ptrs.p[b] & 15) == 0;
+  if (aligned && nb <= 16) {
+    int64_t blocks = ((n >> 2) + 255) / 256;
+    if (blocks < 1) blocks = 1;
+    const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);  // grid-stride: 32 waves per CU
+#define CANON_GA(NBV)                                                                                         \
+  case NBV:                                                                                                   \
+    hipLaunchKernelGGL(grad_accum_vec_kernel<NBV>, dim3(grid), dim3(256), 0, s, accum, dp_shard, n, ptrs,      \
+                       inv_accum, inv_shard, inv_rep, out);                                                   \
+    return hipGetLastError();
+    switch (nb) {
+      CANON_GA(1) CANON_GA(2) CANON_GA(3) CANON_GA(4) CANON_GA(5) CANON_GA(6) CANON_GA(7) CANON_GA(8)
+      CANON_GA(9) CANON_GA(10) CANON_GA(11) CANON_GA(12) CANON_GA(13) CANON_GA(14) CANON_GA(15) CANON_GA(16)
+      default: break;
+    }
+#undef CANON_GA
+  }
   hipLaunchKernelGGL(grad_accum_fused_kernel, dim3(grid_for(n)), dim3(256), 0, s, accum, dp_shard, dp_replicate, n,
                      ptrs, inv_accum, inv_shard, inv_rep, out);
   return hipGetLastError();

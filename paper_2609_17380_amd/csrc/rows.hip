@@ -12,14 +12,15 @@
 
 namespace canon {
 
-constexpr int kLocalLevels = 16;  // a lane block of up to 2^15 chunks
-
-struct LocalFold {
-  float s[kLocalLevels];
+// Binary-carry fold of a lane's consecutive chunk partials (Algorithm 2 on one lane): up to 2^LEVELS - 1
+// pushes.
+template <int LEVELS>
+struct LocalFoldN {
+  float s[LEVELS];
   int64_t count = 0;
   __device__ void push(float p) {
 #pragma unroll
-    for (int L = 0; L < kLocalLevels; ++L) {
+    for (int L = 0; L < LEVELS; ++L) {
       if ((count >> L) & 1) {
         p = s[L] + p;
       } else {
@@ -33,15 +34,20 @@ struct LocalFold {
     float r = 0.0f;
     bool have = false;
 #pragma unroll
-    for (int L = 0; L < kLocalLevels; ++L) {
+    for (int L = 0; L < LEVELS; ++L) {
       if ((count >> L) & 1) {
-        if (!have) { r = s[L]; have = true; }
-        else r = s[L] + r;
+        if (!have) {
+          r = s[L];
+          have = true;
+        } else {
+          r = s[L] + r;
+        }
       }
     }
     return r;
   }
 };
+using LocalFold = LocalFoldN<16>;  // a lane block of up to 2^16 - 1 chunks
 
 // chunks per lane so that `lanes` lanes cover nc chunks with aligned power-of-two blocks
 __device__ __forceinline__ int64_t block_chunks(int64_t nc, int lanes) {
@@ -81,25 +87,91 @@ __device__ __forceinline__ float wave_max(float m) {
   return m;
 }
 
+// ---- W-wide loads and stores (W = 1, 4 or 8 consecutive elements; the caller guarantees alignment) ----
+template <int W>
+__device__ __forceinline__ void ldf(const float* p, float (&f)[W]) {
+  if constexpr (W == 1) {
+    f[0] = p[0];
+  } else {
+#pragma unroll
+    for (int i = 0; i < W; i += 4) {
+      const float4 v = *reinterpret_cast<const float4*>(p + i);
+      f[i] = v.x; f[i + 1] = v.y; f[i + 2] = v.z; f[i + 3] = v.w;
+    }
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void ldb(const uint16_t* p, float (&f)[W]) {
+  if constexpr (W == 1) {
+    f[0] = bf16_to_f32(p[0]);
+  } else if constexpr (W == 4) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    f[0] = bf16_to_f32((uint16_t)(u.x & 0xFFFFu)); f[1] = bf16_to_f32((uint16_t)(u.x >> 16));
+    f[2] = bf16_to_f32((uint16_t)(u.y & 0xFFFFu)); f[3] = bf16_to_f32((uint16_t)(u.y >> 16));
+  } else {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[2 * i] = bf16_to_f32((uint16_t)(w4[i] & 0xFFFFu));
+      f[2 * i + 1] = bf16_to_f32((uint16_t)(w4[i] >> 16));
+    }
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void stb(uint16_t* p, const uint16_t (&h)[W]) {
+  if constexpr (W == 1) {
+    p[0] = h[0];
+  } else if constexpr (W == 4) {
+    *reinterpret_cast<uint2*>(p) = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16),
+                                              (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+  } else {
+    *reinterpret_cast<uint4*>(p) =
+        make_uint4((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16),
+                   (uint32_t)h[4] | ((uint32_t)h[5] << 16), (uint32_t)h[6] | ((uint32_t)h[7] << 16));
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void stf(float* p, const float (&f)[W]) {
+  if constexpr (W == 1) {
+    p[0] = f[0];
+  } else {
+#pragma unroll
+    for (int i = 0; i < W; i += 4) *reinterpret_cast<float4*>(p + i) = make_float4(f[i], f[i + 1], f[i + 2], f[i + 3]);
+  }
+}
+
 // ------------------------------------------------------------------------------------------------
 // Coalesced row reduction for one wavefront.  A segment of 64 chunks (2048 terms) is read coalesced (lane l
-// takes terms 64q + l), staged in LDS as padded rows [chunk][33], and lane c then runs chunk c's chain
-// sequentially from LDS; the chunk partials of all segments collect in `parts` and are folded by lane
-// blocks + wave_fold (Algorithm 2).  term(j) evaluates the j-th term of the row.
+// takes terms 64W q + W l .. + W-1), staged in LDS as padded rows [chunk][33], and lane c then runs chunk
+// c's chain sequentially from LDS; the chunk partials of all segments collect in `parts` and are folded by
+// lane blocks + wave_fold (Algorithm 2).  term(j, f) evaluates terms j .. j+W-1 of the row into f (for
+// W > 1 the row length is a multiple of W, so a vector is either wholly inside the row or wholly past it).
 struct WaveStage {
   float t[64][33];
 };
 
-// Stage one segment (terms seg0 .. seg0 + 2047 of a row of n terms) and write its chunk partials to parts.
-template <class Term>
+template <int W, class Term>
 __device__ __forceinline__ void wave_segment_chunks(int64_t seg0, int64_t n, WaveStage& st, float* parts, Term term) {
   const int lane = threadIdx.x & 63;
   const int64_t nc = (n + kChunk - 1) / kChunk;
-#pragma unroll 4
-  for (int q = 0; q < 32; ++q) {
-    const int local = 64 * q + lane;
+#pragma unroll 2
+  for (int q = 0; q < 64 * kChunk / (64 * W); ++q) {
+    const int local = 64 * W * q + W * lane;
     const int64_t j = seg0 + local;
-    st.t[local >> 5][local & 31] = (j < n) ? term(j) : 0.0f;
+    float f[W];
+    if (j < n) {
+      term(j, f);
+    } else {
+#pragma unroll
+      for (int i = 0; i < W; ++i) f[i] = 0.0f;
+    }
+    float* dst = &st.t[local >> 5][local & 31];
+#pragma unroll
+    for (int i = 0; i < W; ++i) dst[i] = f[i];
   }
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
@@ -116,11 +188,11 @@ __device__ __forceinline__ void wave_segment_chunks(int64_t seg0, int64_t n, Wav
 
 // nz: terms at index >= nz are known to be +0 (masked); chunks made only of them have partial +0 and are not
 // staged.
-template <class Term>
+template <int W, class Term>
 __device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* parts, Term term, int64_t nz) {
   const int lane = threadIdx.x & 63;
   const int64_t nc = (n + kChunk - 1) / kChunk;
-  for (int64_t seg0 = 0; seg0 < n && seg0 < nz; seg0 += 64 * kChunk) wave_segment_chunks(seg0, n, st, parts, term);
+  for (int64_t seg0 = 0; seg0 < n && seg0 < nz; seg0 += 64 * kChunk) wave_segment_chunks<W>(seg0, n, st, parts, term);
   for (int64_t c = (nz + kChunk - 1) / kChunk + lane; c < nc; c += 64) parts[c] = 0.0f;
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
@@ -134,95 +206,141 @@ __device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* 
 
 constexpr int kMaxRowChunks = 64 * 16;  // rows up to 32768 terms in the wave kernels
 
+// The wave kernels take 4 rows per workgroup, with parts[] as dynamic LDS of 4 x (chunks per row) floats.
+static inline size_t wave_kernel_lds(int64_t cols) { return sizeof(float) * 4 * (size_t)((cols + kChunk - 1) / kChunk); }
+
 // RMSNorm forward: one wavefront per row, 4 rows per workgroup.
+template <int W>
 __global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
                                                           const uint16_t* __restrict__ gain, float eps, float inv_d,
                                                           uint16_t* __restrict__ y, float* __restrict__ rstd) {
   __shared__ WaveStage st[4];
-  __shared__ float parts[4][kMaxRowChunks];
+  extern __shared__ float dyn[];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;
+  const int64_t nc = (cols + kChunk - 1) / kChunk;
   const float* xr = x + row * cols;
-  float ss = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
-    float v = xr[j];
-    return v * v;
+  float ss = wave_row_rsum<W>(cols, st[w], dyn + w * nc, [&](int64_t j, float (&f)[W]) {
+    ldf<W>(xr + j, f);
+#pragma unroll
+    for (int i = 0; i < W; ++i) f[i] = f[i] * f[i];
   }, cols);
   float ms = ss * inv_d;
   float var = ms + eps;
   float r = 1.0f / __builtin_sqrtf(var);
   if (lane == 0) rstd[row] = r;
-  for (int64_t k = lane; k < cols; k += 64) {
-    float xv = xr[k] * r;
-    float yv = xv * bf16_to_f32(gain[k]);
-    y[row * cols + k] = f32_to_bf16(yv);
+  for (int64_t k = (int64_t)lane * W; k < cols; k += 64 * W) {
+    float xv[W], gv[W];
+    uint16_t h[W];
+    ldf<W>(xr + k, xv);
+    ldb<W>(gain + k, gv);
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+      float xn = xv[i] * r;
+      h[i] = f32_to_bf16(xn * gv[i]);
+    }
+    stb<W>(y + row * cols + k, h);
   }
 }
 
 // RMSNorm backward (dx): one wavefront per row.
+template <int W>
 __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
                                                           const uint16_t* __restrict__ gain,
                                                           const float* __restrict__ rstd,
                                                           const float* __restrict__ dy, float inv_d,
                                                           float* __restrict__ dx) {
   __shared__ WaveStage st[4];
-  __shared__ float parts[4][kMaxRowChunks];
+  extern __shared__ float dyn[];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;
+  const int64_t nc = (cols + kChunk - 1) / kChunk;
   const float* xr = x + row * cols;
   const float* dyr = dy + row * cols;
-  float dot = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
-    float gy = dyr[j] * bf16_to_f32(gain[j]);
-    return gy * xr[j];
+  float dot = wave_row_rsum<W>(cols, st[w], dyn + w * nc, [&](int64_t j, float (&f)[W]) {
+    float dv[W], gv[W], xv[W];
+    ldf<W>(dyr + j, dv);
+    ldb<W>(gain + j, gv);
+    ldf<W>(xr + j, xv);
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+      float gy = dv[i] * gv[i];
+      f[i] = gy * xv[i];
+    }
   }, cols);
   const float r = rstd[row];
   float r2 = r * r;
   float r3 = r2 * r;
   float dd = dot * inv_d;
   float q = r3 * dd;
-  for (int64_t k = lane; k < cols; k += 64) {
-    float gy = dyr[k] * bf16_to_f32(gain[k]);
-    float a = r * gy;
-    float b = xr[k] * q;
-    dx[row * cols + k] = a - b;
+  for (int64_t k = (int64_t)lane * W; k < cols; k += 64 * W) {
+    float dv[W], gv[W], xv[W], o[W];
+    ldf<W>(dyr + k, dv);
+    ldb<W>(gain + k, gv);
+    ldf<W>(xr + k, xv);
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+      float gy = dv[i] * gv[i];
+      float a = r * gy;
+      float b = xv[i] * q;
+      o[i] = a - b;
+    }
+    stf<W>(dx + row * cols + k, o);
   }
 }
 
-// dgain[k] = R1 over rows t of RN(dy[t,k] * RN(x[t,k] * rstd[t])).  A workgroup of 16 wavefronts takes 64
-// columns (lane = column, so row reads are coalesced); wavefront q folds the aligned power-of-two group of
-// row chunks [q*G, q*G + G), then the 16 group results are folded with the pass-through rule.
+// dgain[k] = R1 over rows t of RN(dy[t,k] * RN(x[t,k] * rstd[t])), in two launches.  First every (chunk of
+// 32 rows, column) chain, one per thread (lane = column, so row reads are coalesced), into part[c][k];
+// then per column Algorithm 2 over its chunk partials in ascending order: a workgroup of 16 wavefronts
+// takes 64 columns, wavefront q folds the aligned power-of-two group of chunks [q*G, q*G + G), and the 16
+// group results are folded with the pass-through rule.
+__global__ __launch_bounds__(256) void rownorm_dgain_part_kernel(int64_t rows, int64_t cols,
+                                                                 const float* __restrict__ x,
+                                                                 const float* __restrict__ rstd,
+                                                                 const float* __restrict__ dy,
+                                                                 float* __restrict__ part) {
+  const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t c = blockIdx.y;
+  if (col >= cols) return;
+  const int64_t t0 = c * kChunk, t1 = (t0 + kChunk < rows) ? t0 + kChunk : rows;
+  float s = 0.0f;
+  for (int64_t t = t0; t < t1; ++t) {
+    float xh = x[t * cols + col] * rstd[t];
+    float pr = dy[t * cols + col] * xh;
+    s = s + pr;
+  }
+  part[c * cols + col] = s;
+}
+
 constexpr int kDgainGroups = 16;
-__global__ __launch_bounds__(1024) void rownorm_dgain_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
-                                                             const float* __restrict__ rstd,
-                                                             const float* __restrict__ dy,
-                                                             float* __restrict__ dgain) {
-  __shared__ float part[kDgainGroups][64];
+__global__ __launch_bounds__(1024) void rownorm_dgain_fold_kernel(int64_t rows, int64_t cols,
+                                                                  const float* __restrict__ part,
+                                                                  float* __restrict__ dgain) {
+  __shared__ float gres[kDgainGroups][64];
   const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
   const int64_t col = (int64_t)blockIdx.x * 64 + lane;
   const int64_t nc = (rows + kChunk - 1) / kChunk;
   const int64_t G = block_chunks(nc, kDgainGroups);
   const int64_t c0 = grp * G, c1 = (c0 + G < nc) ? c0 + G : nc;
-  LocalFold f;
+  LocalFoldN<22> f;
   if (col < cols) {
-    for (int64_t c = c0; c < c1; ++c) {
-      float s = 0.0f;
-      const int64_t t1 = (c + 1) * kChunk < rows ? (c + 1) * kChunk : rows;
-      for (int64_t t = c * kChunk; t < t1; ++t) {
-        float xh = x[t * cols + col] * rstd[t];
-        float pr = dy[t * cols + col] * xh;
-        s = s + pr;
-      }
-      f.push(s);
+    int64_t c = c0;
+    for (; c + 4 <= c1; c += 4) {
+      const float p0 = part[c * cols + col], p1 = part[(c + 1) * cols + col];
+      const float p2 = part[(c + 2) * cols + col], p3 = part[(c + 3) * cols + col];
+      f.push(p0); f.push(p1); f.push(p2); f.push(p3);
     }
+    for (; c < c1; ++c) f.push(part[c * cols + col]);
   }
-  part[grp][lane] = f.result();
+  gres[grp][lane] = f.result();
   __syncthreads();
   if (grp == 0 && col < cols) {
     // fold the group results: level by level, a node adds its right neighbour when that subtree is real
     float v[kDgainGroups];
 #pragma unroll
-    for (int q = 0; q < kDgainGroups; ++q) v[q] = part[q][lane];
+    for (int q = 0; q < kDgainGroups; ++q) v[q] = gres[q][lane];
 #pragma unroll
     for (int sdist = 1; sdist < kDgainGroups; sdist <<= 1)
 #pragma unroll
@@ -232,15 +350,23 @@ __global__ __launch_bounds__(1024) void rownorm_dgain_kernel(int64_t rows, int64
   }
 }
 
+static inline bool al(const void* p, unsigned a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
 hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps, uint16_t* y,
                               float* rstd, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const float inv_d = (float)(1.0 / (double)cols);  // RN32(1/cols), correctly rounded
-  hipLaunchKernelGGL(rownorm_fwd_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, rows, cols, x, gain, eps,
-                     inv_d, y, rstd);
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  const size_t lds = wave_kernel_lds(cols);
+  if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(y, 8))
+    hipLaunchKernelGGL(rownorm_fwd_kernel<4>, grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y, rstd);
+  else
+    hipLaunchKernelGGL(rownorm_fwd_kernel<1>, grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y, rstd);
   return hipGetLastError();
 }
 
+// dx doubles as the scratch of the dgain chunk partials (ceil(rows/32) x cols floats <= rows x cols), so
+// the dgain launches run before the dx kernel overwrites it.
 hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
                               const float* dy, float* dx, float* dgain, hipStream_t s) {
   if (rows == 0) {
@@ -248,78 +374,126 @@ hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const 
     return hipSuccess;
   }
   const float inv_d = (float)(1.0 / (double)cols);
-  hipLaunchKernelGGL(rownorm_bwd_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, rows, cols, x, gain, rstd,
-                     dy, inv_d, dx);
-  if (dgain)
-    hipLaunchKernelGGL(rownorm_dgain_kernel, dim3((unsigned)((cols + 63) / 64)), dim3(1024), 0, s, rows, cols, x,
-                       rstd, dy, dgain);
+  if (dgain) {
+    const int64_t nc = (rows + kChunk - 1) / kChunk;
+    hipLaunchKernelGGL(rownorm_dgain_part_kernel, dim3((unsigned)((cols + 255) / 256), (unsigned)nc), dim3(256), 0,
+                       s, rows, cols, x, rstd, dy, dx);
+    hipLaunchKernelGGL(rownorm_dgain_fold_kernel, dim3((unsigned)((cols + 63) / 64)), dim3(1024), 0, s, rows, cols,
+                       dx, dgain);
+  }
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  const size_t lds = wave_kernel_lds(cols);
+  if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(dy, 16) && al(dx, 16))
+    hipLaunchKernelGGL(rownorm_bwd_kernel<4>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
+  else
+    hipLaunchKernelGGL(rownorm_bwd_kernel<1>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------------------------
 // Causal softmax of raw scores: row r is query i = r mod cols; one wavefront per row, coalesced.
+template <int W>
 __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64_t cols, const float* __restrict__ raw,
                                                              float scale, uint16_t* __restrict__ probs) {
   __shared__ WaveStage st[4];
-  __shared__ float parts[4][kMaxRowChunks];
+  extern __shared__ float dyn[];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;
+  const int64_t nc = (cols + kChunk - 1) / kChunk;
   const int64_t i = row % cols;
   const float* rr = raw + row * cols;
   float m = -__builtin_inff();
-  for (int64_t j = lane; j <= i; j += 64) m = fmaxf(m, rr[j] * scale);
+  for (int64_t j = (int64_t)lane * W; j <= i; j += 64 * W) {
+    float v[W];
+    ldf<W>(rr + j, v);
+#pragma unroll
+    for (int t = 0; t < W; ++t)
+      if (j + t <= i) m = fmaxf(m, v[t] * scale);
+  }
   m = wave_max(m);
   // masked keys enter the chain as +0 terms
-  const float S = wave_row_rsum(cols, st[w], parts[w], [&](int64_t j) {
-    float e = 0.0f;
-    if (j <= i) {
-      float sc = rr[j] * scale;
-      e = cexp(sc - m);
+  const float S = wave_row_rsum<W>(cols, st[w], dyn + w * nc, [&](int64_t j, float (&f)[W]) {
+    float v[W];
+    ldf<W>(rr + j, v);
+#pragma unroll
+    for (int t = 0; t < W; ++t) {
+      float e = 0.0f;
+      if (j + t <= i) {
+        float sc = v[t] * scale;
+        e = cexp(sc - m);
+      }
+      f[t] = e;
     }
-    return e;
   }, i + 1);
   const float rcp = 1.0f / S;
-  for (int64_t j = lane; j < cols; j += 64) {
-    uint16_t o = 0;
+  for (int64_t j = (int64_t)lane * W; j < cols; j += 64 * W) {
+    uint16_t o[W];
     if (j <= i) {
-      float sc = rr[j] * scale;
-      float e = cexp(sc - m);
-      o = f32_to_bf16(e * rcp);
+      float v[W];
+      ldf<W>(rr + j, v);
+#pragma unroll
+      for (int t = 0; t < W; ++t) {
+        o[t] = 0;
+        if (j + t <= i) {
+          float sc = v[t] * scale;
+          float e = cexp(sc - m);
+          o[t] = f32_to_bf16(e * rcp);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int t = 0; t < W; ++t) o[t] = 0;
     }
-    probs[row * cols + j] = o;
+    stb<W>(probs + row * cols + j, o);
   }
 }
 
 hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, uint16_t* probs,
                                  hipStream_t s) {
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(softmax_causal_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, s, rows, cols, raw, scale,
-                     probs);
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  const size_t lds = wave_kernel_lds(cols);
+  if (cols % 4 == 0 && al(raw, 16) && al(probs, 8))
+    hipLaunchKernelGGL(softmax_causal_kernel<4>, grid, dim3(256), lds, s, rows, cols, raw, scale, probs);
+  else
+    hipLaunchKernelGGL(softmax_causal_kernel<1>, grid, dim3(256), lds, s, rows, cols, raw, scale, probs);
   return hipGetLastError();
 }
 
 // ------------------------------------------------------------------------------------------------
 // Cross-entropy: one 256-thread workgroup per row.  The four wavefronts take the row's 2048-term segments
-// round-robin and write the chunk partials; the partials are then folded across the workgroup.
-constexpr int kMaxXentChunks = 4096;  // vocabularies up to 131072
+// round-robin and write the chunk partials; the partials are then folded across the workgroup.  With W = 8
+// (vocab a multiple of 8, 16-byte aligned logits and dlogits) every logit load and dlogit store moves 8 bf16
+// values per lane.  parts[] is dynamic LDS sized to the row's chunk count.
+
+template <int W>
 __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, const uint16_t* __restrict__ logits,
                                                    const int32_t* __restrict__ targets, float inv_tokens,
                                                    uint16_t* __restrict__ dlogits, float* __restrict__ row_loss) {
   __shared__ WaveStage st[4];
-  __shared__ float parts[kMaxXentChunks];
+  extern __shared__ float parts[];
   __shared__ float red[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = blockIdx.x;
   const uint16_t* lr = logits + row * vocab;
   float m = -__builtin_inff();
-  for (int64_t j = threadIdx.x; j < vocab; j += 256) m = fmaxf(m, bf16_to_f32(lr[j]));
+  for (int64_t j = (int64_t)threadIdx.x * W; j < vocab; j += 256 * W) {
+    float f[W];
+    ldb<W>(lr + j, f);
+#pragma unroll
+    for (int i = 0; i < W; ++i) m = fmaxf(m, f[i]);
+  }
   m = wave_max(m);
   if (lane == 0) red[w] = m;
   __syncthreads();
   m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
   for (int64_t seg0 = (int64_t)w * 64 * kChunk; seg0 < vocab; seg0 += 4 * 64 * kChunk)
-    wave_segment_chunks(seg0, vocab, st[w], parts, [&](int64_t j) { return cexp(bf16_to_f32(lr[j]) - m); });
+    wave_segment_chunks<W>(seg0, vocab, st[w], parts, [&](int64_t j, float (&f)[W]) {
+      ldb<W>(lr + j, f);
+#pragma unroll
+      for (int i = 0; i < W; ++i) f[i] = cexp(f[i] - m);
+    });
   __syncthreads();
   const int64_t nc = (vocab + kChunk - 1) / kChunk;
   const int64_t G = block_chunks(nc, 256);
@@ -335,11 +509,18 @@ __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, 
   }
   const float rcp = 1.0f / S;
   if (dlogits) {
-    for (int64_t j = threadIdx.x; j < vocab; j += 256) {
-      float e = cexp(bf16_to_f32(lr[j]) - m);
-      float p = e * rcp;
-      float q = p - (j == y ? 1.0f : 0.0f);
-      dlogits[row * vocab + j] = f32_to_bf16(q * inv_tokens);
+    for (int64_t j = (int64_t)threadIdx.x * W; j < vocab; j += 256 * W) {
+      float fv[W];
+      uint16_t h[W];
+      ldb<W>(lr + j, fv);
+#pragma unroll
+      for (int i = 0; i < W; ++i) {
+        float e = cexp(fv[i] - m);
+        float pr = e * rcp;
+        float q = pr - ((j + i) == y ? 1.0f : 0.0f);
+        h[i] = f32_to_bf16(q * inv_tokens);
+      }
+      stb<W>(dlogits + row * vocab + j, h);
     }
   }
 }
@@ -363,9 +544,15 @@ __global__ __launch_bounds__(256) void mean_loss_kernel(int64_t rows, const floa
 
 hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
                        uint16_t* dlogits, float* row_loss, float* mean_loss, hipStream_t s) {
-  if (rows > 0)
-    hipLaunchKernelGGL(xent_kernel, dim3((unsigned)rows), dim3(256), 0, s, rows, vocab, logits, targets, inv_tokens,
-                       dlogits, row_loss);
+  if (rows > 0) {
+    const size_t lds = sizeof(float) * (size_t)((vocab + kChunk - 1) / kChunk);
+    if (vocab % 8 == 0 && al(logits, 16) && al(dlogits, 16))
+      hipLaunchKernelGGL(xent_kernel<8>, dim3((unsigned)rows), dim3(256), lds, s, rows, vocab, logits, targets,
+                         inv_tokens, dlogits, row_loss);
+    else
+      hipLaunchKernelGGL(xent_kernel<1>, dim3((unsigned)rows), dim3(256), lds, s, rows, vocab, logits, targets,
+                         inv_tokens, dlogits, row_loss);
+  }
   if (mean_loss)
     hipLaunchKernelGGL(mean_loss_kernel, dim3(1), dim3(256), 0, s, rows, row_loss, inv_tokens, mean_loss);
   return hipGetLastError();

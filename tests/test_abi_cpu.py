@@ -39,3 +39,27 @@ def test_oracle_and_library_share_no_source():
     orc = open(os.path.join(ROOT, "oracle", "canon_ref.c")).read()
     assert "canon_dev.h" not in orc and "canon.h" not in orc.replace("canon_ref.h", "")
     assert "canon_ref" not in lib_src
+
+
+def test_host_validation_rejects_before_any_launch():
+    # argument checks run on the host and return before anything is enqueued, so they need no GPU; the
+    # pointers below are never dereferenced
+    import ctypes
+    import paper_2609_17380_amd.canon as C
+    lib = C.lib()
+    order = ctypes.byref(C.ORDER_V1)
+    base = 1 << 32
+    rows, cols = 64, 128
+    n = rows * cols * 4
+    x, dy, dx, rstd, gain, dg = base, base + n, base + 2 * n, base + 3 * n, base + 3 * n + 4096, base + 3 * n + 8192
+    # dx overlapping dy, x, rstd or dgain is rejected (dx holds scratch before its values)
+    for bad_dx in (dy + 4, x, rstd - 8, dg - 16):
+        assert lib.canon_rownorm(order, C.BWD, rows, cols, x, gain, 1e-5, None, rstd, dy, bad_dx, dg, None) == C.EINVAL
+    # a wrong order descriptor and a bad direction
+    bad = C.Order(1, 31, 0, 1)
+    assert lib.canon_rownorm(ctypes.byref(bad), C.FWD, rows, cols, x, gain, 1e-5, dx, rstd, None, None, None,
+                             None) != C.OK
+    assert lib.canon_rownorm(order, 7, rows, cols, x, gain, 1e-5, dx, rstd, None, None, None, None) == C.EINVAL
+    # GEMM with negative sizes, softmax with rows not a multiple of cols
+    assert lib.canon_gemm(order, 0, 0, -1, 4, 4, x, 4, dy, 4, dx, 4, None) == C.EINVAL
+    assert lib.canon_softmax_xent(order, C.SOFTMAX_CAUSAL, 10, 4, x, 1.0, None, 1.0, dx, None, None, None) == C.EINVAL

@@ -13,7 +13,8 @@ from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, hos
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("rows,cols", [(5, 96), (64, 2048), (33, 2048 + 96), (8192, 2048)])
+@pytest.mark.parametrize("rows,cols", [(5, 96), (64, 2048), (33, 2048 + 96), (8192, 2048), (7, 1001),
+                                       (1541, 64)])
 def test_rownorm_fwd_bwd(rows, cols):
     print(f"rownorm {rows}x{cols}", flush=True)
     x = (I.normal_f32((rows, cols), 0, 3) * 2).astype(np.float32)
@@ -36,7 +37,7 @@ def test_rownorm_fwd_bwd(rows, cols):
     assert_bits(host_f32(dgn), dg_o, "dgain")
 
 
-@pytest.mark.parametrize("bh,s", [(3, 200), (2, 64), (4, 2048)])
+@pytest.mark.parametrize("bh,s", [(3, 200), (2, 64), (4, 2048), (2, 70), (1, 33)])
 def test_softmax_causal(bh, s):
     print(f"softmax {bh}x{s}x{s}", flush=True)
     raw = I.normal_f32((bh, s, s), 0, I.TENSOR_IDS["scores"]) * np.float32(8)
@@ -48,7 +49,7 @@ def test_softmax_causal(bh, s):
     assert_bits(host_u16(p), want, "probs")
 
 
-@pytest.mark.parametrize("rows,vocab", [(7, 1000), (16, 50304), (3, 33)])
+@pytest.mark.parametrize("rows,vocab", [(7, 1000), (16, 50304), (3, 33), (4, 1004)])
 def test_xent(rows, vocab):
     print(f"xent {rows}x{vocab}", flush=True)
     logits = I.normal_bf16((rows, vocab), 0, I.TENSOR_IDS["logits"], std=2.0)
@@ -89,14 +90,22 @@ def test_xent_full_size_sampled_rows():
     assert_bits(host_f32(ml), np.array([ml_all], np.float32), "mean_loss")
 
 
-@pytest.mark.parametrize("plan", [(1, 8, 1), (1, 1, 8), (2, 4, 1), (1, 2, 3), (3, 2, 3), (1, 1, 7)])
-def test_grad_accum(plan):
+@pytest.mark.parametrize("plan", [(1, 8, 1), (1, 1, 8), (2, 4, 1), (1, 2, 3), (3, 2, 3), (1, 1, 7), (1, 16, 1),
+                                  (2, 2, 4), (1, 32, 2), (1, 1, 1)])
+@pytest.mark.parametrize("n,offset", [(100003, 0), (4099, 1), (3, 0), (1, 0)])
+def test_grad_accum(plan, n, offset):
+    # up to 16 buffers with 16-byte aligned pointers take the vector kernel (n % 4 tail included); more
+    # buffers, or a pointer off 16-byte alignment (offset 1), take the one-element-per-thread kernel
     accum, shard, rep = plan
-    n = 100003
+    print(f"grad_accum plan {plan} n={n} offset={offset}", flush=True)
     grads = [I.normal_f32((n,), 0, I.TENSOR_IDS["grads"] + i, std=1e-3) for i in range(accum * shard * rep)]
     want = oracle.grad_accum(grads, accum, shard, rep)
-    out = torch.empty(n, dtype=torch.float32, device=DEV)
-    dg = [dev_f32(g) for g in grads]
+    out = torch.empty(n + offset, dtype=torch.float32, device=DEV)[offset:]
+    dg = []
+    for g in grads:
+        t = torch.empty(n + offset, dtype=torch.float32, device=DEV)
+        t[offset:] = dev_f32(g)
+        dg.append(t[offset:])
     C.grad_accum(C.DPPlan(accum, shard, rep), n, dg, out)
     torch.cuda.synchronize()
     assert_bits(host_f32(out), want, f"plan {plan}")
