@@ -163,7 +163,7 @@ hipError_t grad_accum_fused_launch(int accum, int dp_shard, int dp_replicate, in
   if (aligned && nb <= 16) {
     int64_t blocks = ((n >> 2) + 255) / 256;
     if (blocks < 1) blocks = 1;
-    const unsigned grid = (unsigned)(blocks < 8192 ? blocks : 8192);  // grid-stride: 32 waves per CU
+    const unsigned grid = (unsigned)(blocks < (1 << 20) ? blocks : (1 << 20));  // grid-stride beyond 2^20 groups
 #define CANON_GA(NBV)                                                                                         \
   case NBV:                                                                                                   \
     hipLaunchKernelGGL(grad_accum_vec_kernel<NBV>, dim3(grid), dim3(256), 0, s, accum, dp_shard, n, ptrs,      \

@@ -111,7 +111,9 @@ def test_grad_accum(plan, n, offset):
     assert_bits(host_f32(out), want, f"plan {plan}")
 
 
-def test_adamw():
+@pytest.mark.parametrize("offset", [0, 1])
+def test_adamw(offset):
+    # offset 1 puts every pointer off 16-byte alignment
     sizes = [1000, 37, 4096]
     k = I.adamw_constants()
     ps = [I.normal_bf16((s,), 1, 40 + i, std=0.02) for i, s in enumerate(sizes)]
@@ -121,8 +123,15 @@ def test_adamw():
     mask = [1, 0, 1]
     po, mo, vo = [p.copy() for p in ps], [m.copy() for m in ms], [v.copy() for v in vs]
     oracle.adamw(po, mo, vo, gs, mask, oracle.AdamWConsts(*k))
-    pg, mg, vg = [dev_bf16(p) for p in ps], [dev_f32(m) for m in ms], [dev_f32(v) for v in vs]
-    C.adamw(pg, mg, vg, [dev_f32(g) for g in gs], mask, C.AdamWConsts(*k))
+    def shifted(t):
+        if not offset:
+            return t
+        u = torch.empty(t.numel() + offset, dtype=t.dtype, device=DEV)
+        u[offset:] = t
+        return u[offset:]
+
+    pg, mg, vg = [shifted(dev_bf16(p)) for p in ps], [shifted(dev_f32(m)) for m in ms], [shifted(dev_f32(v)) for v in vs]
+    C.adamw(pg, mg, vg, [shifted(dev_f32(g)) for g in gs], mask, C.AdamWConsts(*k))
     torch.cuda.synchronize()
     for i in range(3):
         assert_bits(host_u16(pg[i]), po[i], f"p{i}")
