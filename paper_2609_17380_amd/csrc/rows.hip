@@ -120,6 +120,15 @@ __device__ __forceinline__ void ldb(const uint16_t* p, float (&f)[W]) {
   }
 }
 
+__device__ __forceinline__ void ldb8_regs(const uint4& u, float (&f)[8]) {
+  const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = bf16_to_f32((uint16_t)(w4[i] & 0xFFFFu));
+    f[2 * i + 1] = bf16_to_f32((uint16_t)(w4[i] >> 16));
+  }
+}
+
 template <int W>
 __device__ __forceinline__ void stb(uint16_t* p, const uint16_t (&h)[W]) {
   if constexpr (W == 1) {
@@ -209,6 +218,37 @@ constexpr int kMaxRowChunks = 64 * 16;  // rows up to 32768 terms in the wave ke
 // The wave kernels take 4 rows per workgroup, with parts[] as dynamic LDS of 4 x (chunks per row) floats.
 static inline size_t wave_kernel_lds(int64_t cols) { return sizeof(float) * 4 * (size_t)((cols + kChunk - 1) / kChunk); }
 
+// Register-resident rows (cols <= 2048, a multiple of 4, aligned): lane l holds terms 4l + 256q .. +3 of
+// its row for q < 8, read from memory once.  The chunk chains still run one per lane over a padded LDS
+// transpose of the row (the same staging layout as wave_segment_chunks), then fold across the wavefront.
+constexpr int kRegQ = 8;  // float4 vectors per lane: 64 x 4 x 8 = 2048 terms
+constexpr int64_t kRegCols = 64 * 4 * kRegQ;
+
+// Chain of every chunk of one staged row (nc <= 64 chunks, n terms) and the fold: returns the row sum.
+__device__ __forceinline__ float reg_row_sum(WaveStage& st, const float (&e)[kRegQ][4], int64_t n) {
+  const int lane = threadIdx.x & 63;
+  const int nc = (int)((n + kChunk - 1) / kChunk);
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int local = 256 * q + 4 * lane;
+    if (local < n) {
+      float* dst = &st.t[local >> 5][local & 31];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) dst[t] = e[q][t];
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  float p = 0.0f;
+  if (lane < nc) {
+    const int k1 = (int)(n - (int64_t)lane * kChunk < kChunk ? n - (int64_t)lane * kChunk : kChunk);
+    for (int i = 0; i < k1; ++i) p = p + st.t[lane][i];
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  return __shfl(wave_fold(p, nc), 0, 64);
+}
+
 // RMSNorm forward: one wavefront per row, 4 rows per workgroup.
 template <int W>
 __global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
@@ -291,6 +331,100 @@ __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t 
   }
 }
 
+// RMSNorm forward and backward with register-resident rows (same arithmetic as the kernels above).
+__global__ __launch_bounds__(256) void rownorm_fwd_reg_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
+                                                              const uint16_t* __restrict__ gain, float eps,
+                                                              float inv_d, uint16_t* __restrict__ y,
+                                                              float* __restrict__ rstd) {
+  __shared__ WaveStage st[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= rows) return;
+  const float* xr = x + row * cols;
+  float xv[kRegQ][4], sq[kRegQ][4];
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int64_t j = 256 * q + 4 * lane;
+    float v[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (j < cols) ldf<4>(xr + j, v);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      xv[q][t] = v[t];
+      sq[q][t] = v[t] * v[t];
+    }
+  }
+  const float ss = reg_row_sum(st[w], sq, cols);
+  float ms = ss * inv_d;
+  float var = ms + eps;
+  float r = 1.0f / __builtin_sqrtf(var);
+  if (lane == 0) rstd[row] = r;
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int64_t j = 256 * q + 4 * lane;
+    if (j < cols) {
+      float gv[4];
+      uint16_t h[4];
+      ldb<4>(gain + j, gv);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float xn = xv[q][t] * r;
+        h[t] = f32_to_bf16(xn * gv[t]);
+      }
+      stb<4>(y + row * cols + j, h);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void rownorm_bwd_reg_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
+                                                              const uint16_t* __restrict__ gain,
+                                                              const float* __restrict__ rstd,
+                                                              const float* __restrict__ dy, float inv_d,
+                                                              float* __restrict__ dx) {
+  __shared__ WaveStage st[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= rows) return;
+  const float* xr = x + row * cols;
+  const float* dyr = dy + row * cols;
+  float xv[kRegQ][4], gy[kRegQ][4], tm[kRegQ][4];
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int64_t j = 256 * q + 4 * lane;
+    float dv[4] = {0.0f, 0.0f, 0.0f, 0.0f}, gv[4] = {0.0f, 0.0f, 0.0f, 0.0f}, xx[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (j < cols) {
+      ldf<4>(dyr + j, dv);
+      ldb<4>(gain + j, gv);
+      ldf<4>(xr + j, xx);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      xv[q][t] = xx[t];
+      gy[q][t] = dv[t] * gv[t];
+      tm[q][t] = gy[q][t] * xx[t];
+    }
+  }
+  const float dot = reg_row_sum(st[w], tm, cols);
+  const float r = rstd[row];
+  float r2 = r * r;
+  float r3 = r2 * r;
+  float dd = dot * inv_d;
+  float qq = r3 * dd;
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int64_t j = 256 * q + 4 * lane;
+    if (j < cols) {
+      float o[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float a = r * gy[q][t];
+        float b = xv[q][t] * qq;
+        o[t] = a - b;
+      }
+      stf<4>(dx + row * cols + j, o);
+    }
+  }
+}
+
 // dgain[k] = R1 over rows t of RN(dy[t,k] * RN(x[t,k] * rstd[t])), in two launches.  First every (chunk of
 // 32 rows, column) chain, one per thread (lane = column, so row reads are coalesced), into part[c][k];
 // then per column Algorithm 2 over its chunk partials in ascending order: a workgroup of 16 wavefronts
@@ -358,7 +492,9 @@ hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const 
   const float inv_d = (float)(1.0 / (double)cols);  // RN32(1/cols), correctly rounded
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
-  if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(y, 8))
+  if (cols % 4 == 0 && cols <= kRegCols && al(x, 16) && al(gain, 8) && al(y, 8))
+    hipLaunchKernelGGL(rownorm_fwd_reg_kernel, grid, dim3(256), 0, s, rows, cols, x, gain, eps, inv_d, y, rstd);
+  else if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(y, 8))
     hipLaunchKernelGGL(rownorm_fwd_kernel<4>, grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y, rstd);
   else
     hipLaunchKernelGGL(rownorm_fwd_kernel<1>, grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y, rstd);
@@ -383,7 +519,9 @@ hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const 
   }
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
-  if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(dy, 16) && al(dx, 16))
+  if (cols % 4 == 0 && cols <= kRegCols && al(x, 16) && al(gain, 8) && al(dy, 16) && al(dx, 16))
+    hipLaunchKernelGGL(rownorm_bwd_reg_kernel, grid, dim3(256), 0, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
+  else if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(dy, 16) && al(dx, 16))
     hipLaunchKernelGGL(rownorm_bwd_kernel<4>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
   else
     hipLaunchKernelGGL(rownorm_bwd_kernel<1>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
@@ -449,12 +587,67 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
   }
 }
 
+__global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, int64_t cols,
+                                                                 const float* __restrict__ raw, float scale,
+                                                                 uint16_t* __restrict__ probs) {
+  __shared__ WaveStage st[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= rows) return;
+  const int64_t i = row % cols;
+  const float* rr = raw + row * cols;
+  float e[kRegQ][4];
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int64_t j = 256 * q + 4 * lane;
+    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (j < cols && j <= i) v = *reinterpret_cast<const float4*>(rr + j);
+    e[q][0] = v.x; e[q][1] = v.y; e[q][2] = v.z; e[q][3] = v.w;
+  }
+  float m = -__builtin_inff();
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int64_t j = 256 * q + 4 * lane + t;
+      if (j < cols && j <= i) m = fmaxf(m, e[q][t] * scale);
+    }
+  m = wave_max(m);
+  // masked keys enter the chain as +0 terms
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int64_t j = 256 * q + 4 * lane + t;
+      float x = 0.0f;
+      if (j < cols && j <= i) {
+        float sc = e[q][t] * scale;
+        x = cexp(sc - m);
+      }
+      e[q][t] = x;
+    }
+  const float S = reg_row_sum(st[w], e, cols);
+  const float rcp = 1.0f / S;
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int64_t j = 256 * q + 4 * lane;
+    if (j < cols) {
+      uint16_t o[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) o[t] = (j + t <= i) ? f32_to_bf16(e[q][t] * rcp) : (uint16_t)0;
+      stb<4>(probs + row * cols + j, o);
+    }
+  }
+}
+
 hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, uint16_t* probs,
                                  hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
-  if (cols % 4 == 0 && al(raw, 16) && al(probs, 8))
+  if (cols % 4 == 0 && cols <= kRegCols && al(raw, 16) && al(probs, 8))
+    hipLaunchKernelGGL(softmax_causal_reg_kernel, grid, dim3(256), 0, s, rows, cols, raw, scale, probs);
+  else if (cols % 4 == 0 && al(raw, 16) && al(probs, 8))
     hipLaunchKernelGGL(softmax_causal_kernel<4>, grid, dim3(256), lds, s, rows, cols, raw, scale, probs);
   else
     hipLaunchKernelGGL(softmax_causal_kernel<1>, grid, dim3(256), lds, s, rows, cols, raw, scale, probs);
@@ -525,6 +718,108 @@ __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, 
   }
 }
 
+// Cross-entropy with the row's bf16 logits held in registers (vocab <= 51200, a multiple of 8, aligned):
+// thread t holds elements 8 (t + 256 q) .. +7 for q < kXentQ, read once.  Segment s of 2048 terms is
+// exactly vector q = s of every thread, so the workgroup stages four segments at a time (one per
+// wavefront buffer, thread t writing chunk t/4 at offset 8 (t % 4)), then wavefront w runs the chains of
+// segment buffer w.
+constexpr int kXentQ = 25;
+constexpr int64_t kXentRegVocab = 256 * 8 * kXentQ;
+
+__global__ __launch_bounds__(256) void xent_reg_kernel(int64_t rows, int64_t vocab,
+                                                       const uint16_t* __restrict__ logits,
+                                                       const int32_t* __restrict__ targets, float inv_tokens,
+                                                       uint16_t* __restrict__ dlogits, float* __restrict__ row_loss) {
+  __shared__ WaveStage st[4];
+  extern __shared__ float parts[];
+  __shared__ float red[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63, t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  const uint16_t* lr = logits + row * vocab;
+  const int64_t n8 = vocab >> 3;
+  uint4 raw[kXentQ];
+#pragma unroll
+  for (int q = 0; q < kXentQ; ++q) {
+    const int64_t j8 = t + 256 * q;
+    raw[q] = (j8 < n8) ? reinterpret_cast<const uint4*>(lr)[j8] : make_uint4(0u, 0u, 0u, 0u);
+  }
+  float m = -__builtin_inff();
+#pragma unroll
+  for (int q = 0; q < kXentQ; ++q) {
+    if (t + 256 * q < n8) {
+      float f[8];
+      ldb8_regs(raw[q], f);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) m = fmaxf(m, f[i]);
+    }
+  }
+  m = wave_max(m);
+  if (lane == 0) red[w] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  const int64_t nc = (vocab + kChunk - 1) / kChunk;
+  const int nseg = (int)((vocab + 2047) / 2048);
+#pragma unroll
+  for (int s0 = 0; s0 < kXentQ; s0 += 4) {
+    if (s0 < nseg) {
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int sg = s0 + b;
+        if (sg < kXentQ && sg < nseg && t + 256 * sg < n8) {
+          float f[8];
+          ldb8_regs(raw[sg], f);
+          float* dst = &st[b].t[t >> 2][8 * (t & 3)];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) dst[i] = cexp(f[i] - m);
+        }
+      }
+      __syncthreads();
+      const int sg = s0 + w;
+      if (sg < nseg) {
+        const int64_t c = (int64_t)sg * 64 + lane;
+        if (c < nc) {
+          const int64_t k1 = vocab - c * kChunk < kChunk ? vocab - c * kChunk : kChunk;
+          float sacc = 0.0f;
+          for (int i = 0; i < (int)k1; ++i) sacc = sacc + st[w].t[lane][i];
+          parts[c] = sacc;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const int64_t G = block_chunks(nc, 256);
+  const int64_t c0 = threadIdx.x * G, c1 = (c0 + G < nc) ? c0 + G : nc;
+  LocalFold f;
+  for (int64_t c = c0; c < c1; ++c) f.push(parts[c]);
+  const float S = block_fold(f.result(), (nc + G - 1) / G);
+  const int32_t y = targets[row];
+  const bool valid = y >= 0 && y < vocab;
+  if (threadIdx.x == 0) {
+    float lse = m + clog(S);
+    row_loss[row] = valid ? lse - bf16_to_f32(lr[y]) : __builtin_nanf("");
+  }
+  const float rcp = 1.0f / S;
+  if (dlogits) {
+#pragma unroll
+    for (int q = 0; q < kXentQ; ++q) {
+      const int64_t j8 = t + 256 * q;
+      if (j8 < n8) {
+        float fv[8];
+        uint16_t h[8];
+        ldb8_regs(raw[q], fv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          float e = cexp(fv[i] - m);
+          float pr = e * rcp;
+          float qd = pr - ((j8 * 8 + i) == y ? 1.0f : 0.0f);
+          h[i] = f32_to_bf16(qd * inv_tokens);
+        }
+        stb<8>(dlogits + row * vocab + j8 * 8, h);
+      }
+    }
+  }
+}
+
 // mean_loss = RN(R1(row_loss) * inv_tokens): one workgroup.
 __global__ __launch_bounds__(256) void mean_loss_kernel(int64_t rows, const float* __restrict__ row_loss,
                                                         float inv_tokens, float* __restrict__ out) {
@@ -546,7 +841,10 @@ hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, cons
                        uint16_t* dlogits, float* row_loss, float* mean_loss, hipStream_t s) {
   if (rows > 0) {
     const size_t lds = sizeof(float) * (size_t)((vocab + kChunk - 1) / kChunk);
-    if (vocab % 8 == 0 && al(logits, 16) && al(dlogits, 16))
+    if (vocab % 8 == 0 && vocab <= kXentRegVocab && al(logits, 16) && al(dlogits, 16))
+      hipLaunchKernelGGL(xent_reg_kernel, dim3((unsigned)rows), dim3(256), lds, s, rows, vocab, logits, targets,
+                         inv_tokens, dlogits, row_loss);
+    else if (vocab % 8 == 0 && al(logits, 16) && al(dlogits, 16))
       hipLaunchKernelGGL(xent_kernel<8>, dim3((unsigned)rows), dim3(256), lds, s, rows, vocab, logits, targets,
                          inv_tokens, dlogits, row_loss);
     else

@@ -37,7 +37,7 @@ def test_rownorm_fwd_bwd(rows, cols):
     assert_bits(host_f32(dgn), dg_o, "dgain")
 
 
-@pytest.mark.parametrize("bh,s", [(3, 200), (2, 64), (4, 2048), (2, 70), (1, 33)])
+@pytest.mark.parametrize("bh,s", [(3, 200), (2, 64), (4, 2048), (2, 70), (1, 33), (1, 2304)])
 def test_softmax_causal(bh, s):
     print(f"softmax {bh}x{s}x{s}", flush=True)
     raw = I.normal_f32((bh, s, s), 0, I.TENSOR_IDS["scores"]) * np.float32(8)
@@ -49,7 +49,7 @@ def test_softmax_causal(bh, s):
     assert_bits(host_u16(p), want, "probs")
 
 
-@pytest.mark.parametrize("rows,vocab", [(7, 1000), (16, 50304), (3, 33), (4, 1004)])
+@pytest.mark.parametrize("rows,vocab", [(7, 1000), (16, 50304), (3, 33), (4, 1004), (2, 51208)])
 def test_xent(rows, vocab):
     print(f"xent {rows}x{vocab}", flush=True)
     logits = I.normal_bf16((rows, vocab), 0, I.TENSOR_IDS["logits"], std=2.0)
