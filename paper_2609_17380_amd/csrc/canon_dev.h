@@ -42,10 +42,10 @@ constexpr float kInvFact6 = 0x1.6c16c2p-10f;    // RN32(1/6!)                0x3
 constexpr float kInvFact7 = 0x1.a01a02p-13f;    // RN32(1/7!)                0x39500D01
 
 __device__ __forceinline__ float cexp(float x) {
+  // written without branches (the range checks select the result), so unrolled loops of cexp stay
+  // straight-line code; the arithmetic is the same sequence of roundings either way
   float t = x * kLog2e;
   float kf = __builtin_rintf(t);  // nearest integer, ties to even
-  if (kf > 127.0f) return __builtin_inff();
-  if (kf < -125.0f) return 0.0f;
   float hi = kf * kLn2Hi;
   float lo = kf * kLn2Lo;
   float r = x - hi;
@@ -58,9 +58,13 @@ __device__ __forceinline__ float cexp(float x) {
   p = p * r; p = p + kInvFact2;
   p = p * r; p = p + 1.0f;
   p = p * r; p = p + 1.0f;
-  int k = (int)kf;
+  const float kc = fminf(fmaxf(kf, -126.0f), 127.0f);  // k itself whenever the result is not selected away
+  const int k = (int)kc;
   float scale = __uint_as_float((uint32_t)(k + 127) << 23);
-  return p * scale;
+  float res = p * scale;
+  res = (kf < -125.0f) ? 0.0f : res;
+  res = (kf > 127.0f) ? __builtin_inff() : res;
+  return res;
 }
 
 // ---- clog: x = 2^e f, f in (sqrt(1/2), sqrt(2)]; s = (f-1)/(f+1); log f = 2 atanh(s) by the odd series
