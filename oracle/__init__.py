@@ -71,6 +71,9 @@ def _load():
             "cref_adamw": (ctypes.c_int, [i64, vp, vp, vp, vp, vp, vp, vp]),
             "cref_block_fwd_bwd": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
             "cref_step": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "cref_quant_scales": (ctypes.c_int, [i64, i64, vp, vp]),
+            "cref_quantize": (ctypes.c_int, [i64, i64, i32, vp, vp, i32, vp]),
+            "cref_gemm_i8": (ctypes.c_int, [i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, f, vp]),
             "cref_num_threads": (ctypes.c_int, []),
         }
         for name, (res, args) in sig.items():
@@ -236,6 +239,38 @@ def step(cfg: ModelCfg, plan: Plan, params, m, v, windows, rope_cos, rope_sin, c
                              _p(np.ascontiguousarray(rope_sin, dtype=np.float32)), ctypes.addressof(consts),
                              ctypes.addressof(loss), _ptr_array(grads) if grads is not None else None))
     return np.float32(loss.value), grads
+
+
+def quant_scales(w: np.ndarray) -> np.ndarray:
+    """R13 per-row LSQ step of a bf16 [rows, cols] matrix (uint16 bit patterns)."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    out = np.empty(w.shape[0], dtype=np.float32)
+    _check(_load().cref_quant_scales(w.shape[0], w.shape[1], _p(w), _p(out)))
+    return out
+
+
+def quantize(x: np.ndarray, scale, per_row: bool) -> np.ndarray:
+    """R13 quantisation of an fp32 (float32 array) or bf16 (uint16 array) [rows, cols] tensor to int8."""
+    x = np.ascontiguousarray(x)
+    dtype = 0 if x.dtype == np.float32 else 1
+    assert x.dtype in (np.float32, np.uint16)
+    s = np.ascontiguousarray(np.atleast_1d(np.asarray(scale, dtype=np.float32)))
+    q = np.empty(x.shape, dtype=np.int8)
+    _check(_load().cref_quantize(x.shape[0], x.shape[1], dtype, _p(x), _p(s), int(per_row), _p(q)))
+    return q
+
+
+def gemm_i8(a: np.ndarray, b: np.ndarray, sa: float, sb: np.ndarray):
+    """R13 int8 GEMM: a [m, k], b [n, k] int8 -> (exact int32 acc [m, n], dequantised fp32 y [m, n])."""
+    a = np.ascontiguousarray(a, dtype=np.int8)
+    b = np.ascontiguousarray(b, dtype=np.int8)
+    m, k = a.shape
+    n = b.shape[0]
+    sb = np.ascontiguousarray(sb, dtype=np.float32)
+    acc = np.empty((m, n), dtype=np.int32)
+    y = np.empty((m, n), dtype=np.float32)
+    _check(_load().cref_gemm_i8(m, n, k, _p(a), k, _p(b), k, _p(acc), _p(y), n, np.float32(sa), _p(sb)))
+    return acc, y
 
 
 def num_threads() -> int:

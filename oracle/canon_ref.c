@@ -1013,4 +1013,73 @@ int cref_step(const cref_model_cfg* c, const cref_plan* plan, uint16_t* const* p
   return 0;
 }
 
+/* ======================================================================== */
+/* R13: int8 quantised linear (forward)                                      */
+/* ======================================================================== */
+/* The paper trains every attention and feed-forward projection with 8-bit weights and activations:
+   per-output-channel weight step sizes re-pinned at each step to the LSQ initialisation value
+   2 mean(|w|) / sqrt(q_max) (architecture section, int8 bullet; appendix on the quantisation-level
+   collapse), a per-tensor activation step, exact int32 accumulation, then dequantisation.  The division
+   by sqrt(q_max) is a multiply by the binary32 rounding of 1/sqrt(127). */
+static const uint32_t INV_SQRT_QMAX = 0x3DB5BB09u; /* RN32(1/sqrt(127)) */
+
+int cref_quant_scales(int64_t rows, int64_t cols, const uint16_t* w, float* scale) {
+  if (rows < 0 || cols < 1 || (rows > 0 && (!w || !scale))) return -1;
+  const float inv_k = inv_of(cols);
+  const float c = f_from_bits(INV_SQRT_QMAX);
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) {
+    float* t = (float*)malloc(sizeof(float) * (size_t)cols);
+    for (int64_t k = 0; k < cols; ++k) t[k] = fabsf(widen(w[r * cols + k]));
+    const float a = cref_rsum(t, cols, 1, CHUNK);
+    const float mean = cref_mul(a, inv_k);
+    const float two = cref_mul(2.0f, mean);
+    scale[r] = cref_mul(two, c);
+    free(t);
+  }
+  return 0;
+}
+
+static int8_t quant1(float x, float s) {
+  s = daz(s);
+  if (!(s > 0.0f)) return 0;
+  const float t = cref_div(x, s);
+  if (isnan(t)) return 0;
+  double r = rint((double)t); /* nearest integer, ties to even (default rounding mode) */
+  if (r > 127.0) r = 127.0;
+  if (r < -128.0) r = -128.0;
+  return (int8_t)r;
+}
+
+int cref_quantize(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale, int32_t per_row,
+                  int8_t* q) {
+  if (rows < 0 || cols < 0 || (dtype != 0 && dtype != 1)) return -1;
+  if (rows * cols > 0 && (!x || !scale || !q)) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < rows; ++r) {
+    const float s = scale[per_row ? r : 0];
+    for (int64_t k = 0; k < cols; ++k) {
+      const int64_t i = r * cols + k;
+      const float v = dtype == 0 ? ((const float*)x)[i] : widen(((const uint16_t*)x)[i]);
+      q[i] = quant1(v, s);
+    }
+  }
+  return 0;
+}
+
+int cref_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int64_t lda, const int8_t* b, int64_t ldb,
+                 int32_t* acc, float* y, int64_t ldc, float sa, const float* sb) {
+  if (m < 0 || n < 0 || k < 0 || k > 65536 || lda < k || ldb < k || ldc < n) return -1;
+  if (y && !sb) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < m; ++i)
+    for (int64_t j = 0; j < n; ++j) {
+      int64_t s = 0; /* exact */
+      for (int64_t kk = 0; kk < k; ++kk) s += (int64_t)a[i * lda + kk] * (int64_t)b[j * ldb + kk];
+      if (acc) acc[i * ldc + j] = (int32_t)s;
+      if (y) y[i * ldc + j] = cref_mul(cref_mul((float)s, sa), sb[j]); /* (float) of an int: round to nearest even */
+    }
+  return 0;
+}
+
 int cref_num_threads(void) { return omp_get_max_threads(); }

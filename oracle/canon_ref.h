@@ -91,6 +91,20 @@ int cref_step(const cref_model_cfg* cfg, const cref_plan* plan, uint16_t* const*
               float* const* v, const int32_t* windows, const float* rope_cos, const float* rope_sin,
               const cref_adamw_consts* k, float* loss_out, float* const* grads_out);
 
+/* ---- R13 int8 quantised linear, forward (the W8A8 training path) ----
+   quant_scales: per-row LSQ step of a bf16 matrix [rows][cols] re-pinned from the weights:
+     s[r] = RN(RN(2 * RN(R1(|w[r,:]|) * RN(1/cols))) * RN(1/sqrt(127))).
+   quantize: q = clamp(rne(RN(x / s)), -128, 127) for x fp32 (dtype 0) or bf16 (dtype 1), with one step
+     per row (per_row = 1) or one for the whole tensor (per_row = 0); a step that is not > 0 after the
+     input flush quantises to 0, and so does a NaN quotient.
+   gemm_i8: acc[i][j] = sum_k a[i][k] * b[j][k] exactly (int8 operands, a [m][k], b [n][k]); acc (int32,
+     optional) and y[i][j] = RN(RN(RN32(acc) * sa) * sb[j]) (fp32, optional), ldc for both.  k <= 65536. */
+int cref_quant_scales(int64_t rows, int64_t cols, const uint16_t* w, float* scale);
+int cref_quantize(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale, int32_t per_row,
+                  int8_t* q);
+int cref_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int64_t lda, const int8_t* b, int64_t ldb,
+                 int32_t* acc, float* y, int64_t ldc, float sa, const float* sb);
+
 int cref_num_threads(void);
 
 #ifdef __cplusplus
