@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s
+PEAK_INT8_MFMA = 5000.0  # TOP/s, MI355X dense int8 matrix
 
 L, D, H, HD, F, V, S, MB = 16, 2048, 16, 128, 8192, 50304, 2048, 4
 PLAN = (1, 8, 1)
@@ -112,6 +113,30 @@ def kernel_table(C, I, torch, np, stream, dev):
                                            "frac": round(tf / PEAK_FP32_MFMA, 4),
                                            "pct_bf16_peak": round(100 * tf / PEAK_BF16_MFMA, 3)}
         del a, b, c
+
+    # the int8 quantised linear (the paper's W8A8 path): exact int8 GEMM with dequantisation at the
+    # projection shapes of the 1B decoder, and the quantisers
+    for name, m, n, k in [("qkv", 8192, 6144, 2048), ("gate_up", 8192, 16384, 2048), ("down", 8192, 2048, 8192),
+                          ("out", 8192, 2048, 2048)]:
+        qa = torch.randint(-128, 128, (m, k), generator=g, device=dev, dtype=torch.int8)
+        qb = torch.randint(-128, 128, (n, k), generator=g, device=dev, dtype=torch.int8)
+        sa = torch.full((1,), 0.01, device=dev)
+        sb = torch.full((n,), 0.001, device=dev)
+        yq = torch.empty((m, n), dtype=torch.float32, device=dev)
+        ms = _timed(torch, stream, lambda: C.gemm_i8(m, n, k, qa, k, qb, k, y=yq, sa=sa, sb=sb, stream=stream), 5)
+        tops = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+        out[f"gemm_i8_{name}_{m}x{n}x{k}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tops, 1),
+                                              "unit": "TOP/s", "peak": PEAK_INT8_MFMA,
+                                              "frac": round(tops / PEAK_INT8_MFMA, 4)}
+        del qa, qb, yq
+    wq = randn((16384, 2048), 0.02, torch.bfloat16)
+    swq = torch.empty(16384, dtype=torch.float32, device=dev)
+    ms = _timed(torch, stream, lambda: C.quant_scales(16384, 2048, wq, swq, stream=stream), 10)
+    out["quant_scales_16384x2048"] = _hbm(ms, 16384 * 2048 * 2 + 16384 * 4)
+    qq = torch.empty((16384, 2048), dtype=torch.int8, device=dev)
+    ms = _timed(torch, stream, lambda: C.quantize(16384, 2048, wq, swq, True, qq, stream=stream), 10)
+    out["quantize_16384x2048_bf16"] = _hbm(ms, 16384 * 2048 * 3 + 16384 * 4)
+    del wq, swq, qq
 
     T, d = MB * S, D
     x = randn((T, d))

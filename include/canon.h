@@ -164,6 +164,32 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
 size_t canon_step_workspace_bytes(const canon_model_cfg* cfg, const canon_dp_plan* plan);
 
 /* ------------------------------------------------------------------------------------------------ */
+/* ------------------------------------------------------------------------------------------------ */
+/* int8 quantised linear, forward (the paper's W8A8 training path: the architecture section's int8
+   quantisation-aware training bullet, the training-details paragraph on int8 computation, and the
+   appendix that replaces the learned weight step by its re-pinned LSQ initialisation value).
+
+   canon_quant_scales: per-row step of a bf16 weight matrix w [rows, cols] (one row per output channel):
+     scale[r] = RN(RN(2 * RN(R1(|w[r,:]|) * RN(1/cols))) * RN(1/sqrt(127))), R1 over the row in column
+     order.  scale: device fp32 [rows].  cols in [1, 32768].
+   canon_quantize: q = clamp(rne(RN(x / s)), -128, 127) element by element for x [rows, cols] fp32
+     (in_dtype CANON_F32) or bf16 (CANON_BF16); s = scale[r] for row r when per_row, else scale[0]
+     (e.g. a per-tensor activation step).  A step that is not > 0 once flushed, or a NaN quotient, gives
+     0.  scale, x, q: device memory; q int8 [rows, cols].
+   canon_gemm_i8: acc[i][j] = sum_k a[i][k] * b[j][k] exactly, a int8 [m, k] (leading dim lda), b int8
+     [n, k] (ldb; one output column per row, as weights [out][in]); writes acc (int32, may be NULL) and
+     y[i][j] = RN(RN(RN32(acc) * sa[0]) * sb[j]) (fp32, may be NULL; sa device scalar, sb device [n]),
+     both with leading dim ldc.  k in [0, 65536] keeps |acc| < 2^31.  The integer sum is exact in any
+     order, so this kernel runs on the int8 matrix instructions without an order constraint. */
+enum { CANON_F32 = 0, CANON_BF16 = 1 };
+canon_status canon_quant_scales(const canon_order* order, int64_t rows, int64_t cols, const uint16_t* w,
+                                float* scale, void* stream);
+canon_status canon_quantize(int64_t rows, int64_t cols, int32_t in_dtype, const void* x, const float* scale,
+                            int32_t per_row, int8_t* q, void* stream);
+canon_status canon_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int64_t lda, const int8_t* b,
+                           int64_t ldb, int32_t* acc, float* y, int64_t ldc, const float* sa, const float* sb,
+                           void* stream);
+
 /* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
    the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,
    10 bf16 round trip.  a, b, c, out: device fp32 [n] (b, c may be NULL when unused). */

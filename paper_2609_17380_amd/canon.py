@@ -69,6 +69,9 @@ def _lib():
             "canon_step": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp, vp, vp]),
             "canon_step_workspace_bytes": (sz, [vp, vp]),
             "canon_devmath": (i32, [i32, i64, vp, vp, vp, vp, vp]),
+            "canon_quant_scales": (i32, [vp, i64, i64, vp, vp, vp]),
+            "canon_quantize": (i32, [i64, i64, i32, vp, vp, i32, vp, vp]),
+            "canon_gemm_i8": (i32, [i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, vp, vp, vp]),
             "canon_status_str": (ctypes.c_char_p, [i32]),
             "canon_version": (i32, []),
         }
@@ -172,6 +175,25 @@ def step(cfg: ModelCfg, plan: DPPlan, params, m, v, windows, rope_cos, rope_sin,
 
 DEVMATH_OPS = {"add": 0, "sub": 1, "mul": 2, "fma": 3, "div": 4, "sqrt": 5, "exp": 6, "log": 7, "sigmoid": 8,
                "silu": 9, "bf16": 10}
+
+
+F32, BF16 = 0, 1
+
+
+def quant_scales(rows, cols, w, scale, order=ORDER_V1, stream=None):
+    _check(_lib().canon_quant_scales(ctypes.byref(order), rows, cols, _ptr(w), _ptr(scale), _stream(stream)),
+           "canon_quant_scales")
+
+
+def quantize(rows, cols, x, scale, per_row, q, stream=None):
+    dtype = F32 if x.dtype == torch.float32 else BF16
+    _check(_lib().canon_quantize(rows, cols, dtype, _ptr(x), _ptr(scale), int(per_row), _ptr(q), _stream(stream)),
+           "canon_quantize")
+
+
+def gemm_i8(m, n, k, a, lda, b, ldb, acc=None, y=None, ldc=None, sa=None, sb=None, stream=None):
+    _check(_lib().canon_gemm_i8(m, n, k, _ptr(a), lda, _ptr(b), ldb, _ptr(acc), _ptr(y), n if ldc is None else ldc,
+                                _ptr(sa), _ptr(sb), _stream(stream)), "canon_gemm_i8")
 
 
 def devmath(op: str, n, a, b=None, c=None, out=None, stream=None):

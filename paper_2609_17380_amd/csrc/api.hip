@@ -460,6 +460,35 @@ canon_status canon_grad_accum(const canon_order* order, const canon_dp_plan* pla
   return dev(grad_accum_fused_launch(plan->accum, plan->dp_shard, plan->dp_replicate, n, pp, out, as_stream(stream)));
 }
 
+canon_status canon_quant_scales(const canon_order* order, int64_t rows, int64_t cols, const uint16_t* w,
+                                float* scale, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (rows < 0 || cols < 1) return CANON_EINVAL;
+  if (cols > 32768 || rows > (int64_t(1) << 31)) return CANON_EUNSUPPORTED;  // one wavefront stages the row
+  if (rows > 0 && (!w || !scale)) return CANON_EINVAL;
+  return dev(quant_scales_launch(rows, cols, w, scale, as_stream(stream)));
+}
+
+canon_status canon_quantize(int64_t rows, int64_t cols, int32_t in_dtype, const void* x, const float* scale,
+                            int32_t per_row, int8_t* q, void* stream) {
+  if (rows < 0 || cols < 0 || (in_dtype != CANON_F32 && in_dtype != CANON_BF16)) return CANON_EINVAL;
+  if (rows * cols > 0 && (!x || !scale || !q)) return CANON_EINVAL;
+  return dev(quantize_launch(rows, cols, in_dtype, x, scale, per_row != 0, q, as_stream(stream)));
+}
+
+canon_status canon_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int64_t lda, const int8_t* b,
+                           int64_t ldb, int32_t* acc, float* y, int64_t ldc, const float* sa, const float* sb,
+                           void* stream) {
+  if (m < 0 || n < 0 || k < 0 || lda < k || ldb < k || ldc < n) return CANON_EINVAL;
+  if (k > 65536) return CANON_EUNSUPPORTED;
+  if (m > 0 && n > 0 && ((k > 0 && (!a || !b)) || (!acc && !y) || (y && (!sa || !sb)))) return CANON_EINVAL;
+  GemmI8Args g{};
+  g.a = a; g.b = b; g.acc = acc; g.y = y; g.sa = sa; g.sb = sb;
+  g.m = m; g.n = n; g.k = k; g.lda = lda; g.ldb = ldb; g.ldc = ldc;
+  return dev(gemm_i8_launch(g, as_stream(stream)));
+}
+
 canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m,
                          float* const* v, const float* const* grads, const uint8_t* decay_mask,
                          const canon_adamw_consts* consts, void* stream) {

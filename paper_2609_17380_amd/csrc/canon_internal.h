@@ -21,6 +21,19 @@ struct GemmArgs {
 };
 
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);
+
+// gemm_i8.hip: exact int8 GEMM (a [m][k], b [n][k]) with optional int32 and dequantised fp32 outputs
+struct GemmI8Args {
+  const int8_t* a;
+  const int8_t* b;
+  int32_t* acc;     // may be null
+  float* y;         // may be null
+  const float* sa;  // device scalar (needed when y is set)
+  const float* sb;  // device [n] (needed when y is set)
+  int64_t m, n, k, lda, ldb, ldc;
+  int32_t vec;      // set by the launcher
+};
+hipError_t gemm_i8_launch(const GemmI8Args& g, hipStream_t s);
 int gemm_max_levels();
 
 // rows.hip
@@ -32,6 +45,7 @@ hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, f
                                  hipStream_t s);
 hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets,
                        float inv_tokens, uint16_t* dlogits, float* row_loss, float* mean_loss, hipStream_t s);
+hipError_t quant_scales_launch(int64_t rows, int64_t cols, const uint16_t* w, float* scale, hipStream_t s);
 hipError_t attn_rowdot_launch(int64_t B, int64_t H, int64_t S, int64_t hd, const uint16_t* dO, const uint16_t* O,
                               int64_t ld, float* D, hipStream_t s);
 hipError_t attn_dS_launch(int64_t BH, int64_t S, const uint16_t* P, const float* dP, const float* D, float scale,
@@ -54,6 +68,8 @@ hipError_t labels_launch(int64_t B, int64_t S, const int32_t* win, int64_t win_l
 size_t embed_bwd_scratch_bytes(int64_t T);
 hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld, int64_t V,
                             const float* dx, float* dE, void* scratch, hipStream_t s);
+hipError_t quantize_launch(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale,
+                           int32_t per_row, int8_t* q, hipStream_t s);
 hipError_t devmath_launch(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
                           hipStream_t s);
 

@@ -279,6 +279,43 @@ hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win,
   return hipGetLastError();
 }
 
+// Quantiser of the int8 quantised linear: q = clamp(rne(RN(x / s)), -128, 127), x fp32 (dtype 0) or bf16
+// (dtype 1), one step per row or for the whole tensor.  A step that is not > 0 once flushed, or a NaN
+// quotient, gives 0.
+template <int DT>
+__global__ void quantize_kernel(int64_t rows, int64_t cols, const void* __restrict__ x,
+                                const float* __restrict__ scale, int32_t per_row, int8_t* __restrict__ q) {
+  const int64_t n = rows * cols;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+    uint32_t sb = __float_as_uint(scale[per_row ? i / cols : 0]);
+    if ((sb & 0x7F800000u) == 0u) sb &= 0x80000000u;  // a subnormal step reads as zero
+    const float sv = __uint_as_float(sb);
+    const float v = DT == 0 ? static_cast<const float*>(x)[i] : bf16_to_f32(static_cast<const uint16_t*>(x)[i]);
+    int8_t out = 0;
+    if (sv > 0.0f) {
+      const float t = v / sv;
+      if (t == t) {
+        const float r = __builtin_rintf(t);
+        out = (int8_t)(int)fminf(fmaxf(r, -128.0f), 127.0f);
+      }
+    }
+    q[i] = out;
+  }
+}
+
+hipError_t quantize_launch(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale,
+                           int32_t per_row, int8_t* q, hipStream_t s) {
+  const int64_t n = rows * cols;
+  if (n == 0) return hipSuccess;
+  int64_t b = (n + 255) / 256;
+  const unsigned grid = (unsigned)(b < (1 << 20) ? b : (1 << 20));
+  if (dtype == 0)
+    hipLaunchKernelGGL(quantize_kernel<0>, dim3(grid), dim3(256), 0, s, rows, cols, x, scale, per_row, q);
+  else
+    hipLaunchKernelGGL(quantize_kernel<1>, dim3(grid), dim3(256), 0, s, rows, cols, x, scale, per_row, q);
+  return hipGetLastError();
+}
+
 // ---- device evaluation of the primitives -----------------------------------------------------------
 __global__ void devmath_kernel(int32_t op, int64_t n, const float* __restrict__ a, const float* __restrict__ b,
                                const float* __restrict__ c, float* __restrict__ out) {

@@ -529,6 +529,43 @@ hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const 
 }
 
 // ------------------------------------------------------------------------------------------------
+// LSQ step re-pin of the int8 quantised linear: per row r of a bf16 matrix,
+// s[r] = RN(RN(2 * RN(R1(|w[r,:]|) * RN(1/cols))) * RN32(1/sqrt(127))).  One wavefront per row.
+constexpr uint32_t kInvSqrtQmaxBits = 0x3DB5BB09u;  // RN32(1/sqrt(127))
+
+template <int W>
+__global__ __launch_bounds__(256) void quant_scales_kernel(int64_t rows, int64_t cols, const uint16_t* __restrict__ w,
+                                                           float inv_k, float* __restrict__ scale) {
+  __shared__ WaveStage st[4];
+  extern __shared__ float dyn[];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wv;
+  if (row >= rows) return;
+  const int64_t nc = (cols + kChunk - 1) / kChunk;
+  const uint16_t* wr = w + row * cols;
+  const float a = wave_row_rsum<W>(cols, st[wv], dyn + wv * nc, [&](int64_t j, float (&f)[W]) {
+    ldb<W>(wr + j, f);
+#pragma unroll
+    for (int i = 0; i < W; ++i) f[i] = __builtin_fabsf(f[i]);
+  }, cols);
+  const float mean = a * inv_k;
+  const float two = 2.0f * mean;
+  if (lane == 0) scale[row] = two * __uint_as_float(kInvSqrtQmaxBits);
+}
+
+hipError_t quant_scales_launch(int64_t rows, int64_t cols, const uint16_t* w, float* scale, hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  const float inv_k = (float)(1.0 / (double)cols);  // RN32(1/cols)
+  const dim3 grid((unsigned)((rows + 3) / 4));
+  const size_t lds = wave_kernel_lds(cols);
+  if (cols % 4 == 0 && al(w, 8))
+    hipLaunchKernelGGL(quant_scales_kernel<4>, grid, dim3(256), lds, s, rows, cols, w, inv_k, scale);
+  else
+    hipLaunchKernelGGL(quant_scales_kernel<1>, grid, dim3(256), lds, s, rows, cols, w, inv_k, scale);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------------------------
 // Causal softmax of raw scores: row r is query i = r mod cols; one wavefront per row, coalesced.
 template <int W>
 __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64_t cols, const float* __restrict__ raw,

@@ -1,0 +1,123 @@
+"""The int8 quantised linear on the GPU against the oracle: LSQ step re-pin (bit-exact fp32), quantiser
+(byte-exact), exact int8 GEMM (bit-exact int32) and its dequantisation (bit-exact fp32), at small
+shapes with ragged tiles and at the 1B decoder's shapes on sampled rows."""
+import numpy as np
+import pytest
+import torch
+
+import adversarial as ADV
+import oracle
+import paper_2609_17380_amd.canon as C
+import paper_2609_17380_amd.inputs as I
+from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, host_f32
+
+pytestmark = pytest.mark.gpu
+RNG = np.random.default_rng(8)
+
+
+def dev_i8(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int8)).to(DEV)
+
+
+@pytest.mark.parametrize("rows,cols", [(5, 2048), (130, 97), (3, 1), (64, 8192), (2, 32768)])
+def test_quant_scales(rows, cols):
+    print(f"quant_scales {rows}x{cols}", flush=True)
+    w = I.normal_bf16((rows, cols), 0, I.TENSOR_IDS["gemm_b"], std=0.02)
+    w[0, : min(cols, 7)] = np.array([0x0001, 0x8003, 0x7F7F, 0xFF7F, 0x0000, 0x8000, 0x3F80], np.uint16)[: min(cols, 7)]
+    want = oracle.quant_scales(w)
+    got = torch.empty(rows, dtype=torch.float32, device=DEV)
+    C.quant_scales(rows, cols, dev_bf16(w), got)
+    torch.cuda.synchronize()
+    assert_bits(host_f32(got), want, "scale")
+
+
+def special_values(shape):
+    x = (RNG.standard_normal(shape) * 3).astype(np.float32)
+    flat = x.reshape(-1)
+    sp = np.array([0.5, 1.5, -2.5, 127.5, -128.5, 1e30, -1e30, np.inf, -np.inf, np.nan, -0.0, 1e-40],
+                  np.float32)
+    flat[: sp.size] = sp
+    return x
+
+
+@pytest.mark.parametrize("per_row", [True, False])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_quantize(per_row, dtype):
+    rows, cols = 37, 301
+    x = special_values((rows, cols))
+    s = (np.abs(RNG.standard_normal(rows)) * 0.1 + 0.01).astype(np.float32)
+    s[1], s[2], s[3], s[4] = 0.0, -1.0, np.nan, 1e-40  # steps that quantise to 0
+    if not per_row:
+        s = s[:1]
+    if dtype == "bf16":
+        xh = (x.view(np.uint32) >> 16).astype(np.uint16)
+        want, xd = oracle.quantize(xh, s, per_row), dev_bf16(xh)
+    else:
+        want, xd = oracle.quantize(x, s, per_row), dev_f32(x)
+    q = torch.empty((rows, cols), dtype=torch.int8, device=DEV)
+    C.quantize(rows, cols, xd, dev_f32(s), per_row, q)
+    torch.cuda.synchronize()
+    got = q.cpu().numpy()
+    assert np.array_equal(got, want), np.argwhere(got != want)[:5]
+
+
+def gemm_case(m, n, k, a_off=0, seed=0, extreme=False):
+    rng = np.random.default_rng(seed)
+    if extreme:
+        a = np.full((m, k), -128, np.int8)
+        b = np.full((n, k), -128, np.int8)
+        b[1::2] = 127
+    else:
+        a = rng.integers(-128, 128, (m, k)).astype(np.int8)
+        b = rng.integers(-128, 128, (n, k)).astype(np.int8)
+    sa = np.float32(0.0173)
+    sb = (np.abs(rng.standard_normal(n)) * 0.01).astype(np.float32)
+    acc_o, y_o = oracle.gemm_i8(a, b, sa, sb)
+    ad = torch.empty(m * k + a_off, dtype=torch.int8, device=DEV)
+    ad[a_off:] = dev_i8(a).reshape(-1)
+    acc = torch.full((m, n), -1, dtype=torch.int32, device=DEV)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+    C.gemm_i8(m, n, k, ad[a_off:], k, dev_i8(b), k, acc=acc, y=y, sa=dev_f32(np.array([sa])), sb=dev_f32(sb))
+    torch.cuda.synchronize()
+    assert np.array_equal(acc.cpu().numpy(), acc_o)
+    assert_bits(host_f32(y), y_o, "y")
+
+
+@pytest.mark.parametrize("m,n,k", [(130, 260, 192), (128, 128, 64), (1, 1, 1), (200, 3, 1000), (64, 300, 48),
+                                   (129, 129, 4096), (7, 5, 0)])
+def test_gemm_i8(m, n, k):
+    print(f"gemm_i8 {m}x{n}x{k}", flush=True)
+    gemm_case(m, n, k)
+
+
+def test_gemm_i8_misaligned_and_extreme():
+    gemm_case(70, 90, 160, a_off=3)           # operand off 16-byte alignment: byte loads
+    gemm_case(64, 64, 65536, extreme=True)    # |acc| up to 2^30
+
+
+def test_quantised_linear_1b_shapes_sampled():
+    # the gate/up projection of the 1B decoder over one microbatch: scales of the weights, quantised weights
+    # and activations, int8 GEMM and dequantisation; sampled activation rows through the oracle
+    T, K, N = 8192, 2048, 16384
+    w = I.normal_bf16((N, K), 0, I.TENSOR_IDS["gemm_b"], std=0.02)
+    x = I.normal_f32((T, K), 0, I.TENSOR_IDS["gemm_a"])
+    sx = np.array([0.0625], np.float32)  # per-tensor activation step
+    wd, xd, sxd = dev_bf16(w), dev_f32(x), dev_f32(sx)
+    sw = torch.empty(N, dtype=torch.float32, device=DEV)
+    C.quant_scales(N, K, wd, sw)
+    qw = torch.empty((N, K), dtype=torch.int8, device=DEV)
+    qx = torch.empty((T, K), dtype=torch.int8, device=DEV)
+    C.quantize(N, K, wd, sw, True, qw)
+    C.quantize(T, K, xd, sxd, False, qx)
+    y = torch.empty((T, N), dtype=torch.float32, device=DEV)
+    C.gemm_i8(T, N, K, qx, K, qw, K, y=y, sa=sxd, sb=sw)
+    torch.cuda.synchronize()
+    sw_o = oracle.quant_scales(w)
+    assert_bits(host_f32(sw), sw_o, "weight steps")
+    qw_o = oracle.quantize(w, sw_o, True)
+    assert np.array_equal(qw.cpu().numpy(), qw_o)
+    rows = np.concatenate([np.arange(0, 64), RNG.choice(T, 64, replace=False)])
+    qx_o = oracle.quantize(x[rows], sx, False)
+    assert np.array_equal(qx.cpu().numpy()[rows], qx_o)
+    _, y_o = oracle.gemm_i8(qx_o, qw_o, sx[0], sw_o)
+    assert_bits(host_f32(y)[rows], y_o, "y rows")
