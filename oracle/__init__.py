@@ -74,6 +74,8 @@ def _load():
             "cref_quant_scales": (ctypes.c_int, [i64, i64, vp, vp]),
             "cref_quantize": (ctypes.c_int, [i64, i64, i32, vp, vp, i32, vp]),
             "cref_gemm_i8": (ctypes.c_int, [i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, f, vp]),
+            "cref_fwht256": (ctypes.c_int, [i64, vp]),
+            "cref_qlinear_bwd": (ctypes.c_int, [i64, i64, i64, vp, vp, f, vp, vp, vp, vp]),
             "cref_num_threads": (ctypes.c_int, []),
         }
         for name, (res, args) in sig.items():
@@ -271,6 +273,29 @@ def gemm_i8(a: np.ndarray, b: np.ndarray, sa: float, sb: np.ndarray):
     y = np.empty((m, n), dtype=np.float32)
     _check(_load().cref_gemm_i8(m, n, k, _p(a), k, _p(b), k, _p(acc), _p(y), n, np.float32(sa), _p(sb)))
     return acc, y
+
+
+def fwht256(v: np.ndarray) -> np.ndarray:
+    """R14 block Walsh-Hadamard rotation (blocks of 256 along the flattened array), returned as a copy."""
+    out = np.array(v, dtype=np.float32, copy=True, order="C")
+    _check(_load().cref_fwht256(out.size, _p(out)))
+    return out
+
+
+def qlinear_bwd(dy: np.ndarray, qx: np.ndarray, sx: float, qw: np.ndarray, sw: np.ndarray, want_dx=True,
+                want_dw=True):
+    """R14 int8 backward: (dx [T, K], dw [N, K]) from dy [T, N] and the forward's codes and steps."""
+    dy = np.ascontiguousarray(dy, dtype=np.float32)
+    qx = np.ascontiguousarray(qx, dtype=np.int8)
+    qw = np.ascontiguousarray(qw, dtype=np.int8)
+    sw = np.ascontiguousarray(sw, dtype=np.float32)
+    T, N = dy.shape
+    K = qx.shape[1]
+    dx = np.empty((T, K), np.float32) if want_dx else None
+    dw = np.empty((N, K), np.float32) if want_dw else None
+    _check(_load().cref_qlinear_bwd(T, N, K, _p(dy), _p(qx), np.float32(sx), _p(qw), _p(sw),
+                                    _p(dx) if dx is not None else None, _p(dw) if dw is not None else None))
+    return dx, dw
 
 
 def num_threads() -> int:

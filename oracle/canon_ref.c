@@ -1082,4 +1082,89 @@ int cref_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int64_t lda, 
   return 0;
 }
 
+/* ======================================================================== */
+/* R14: int8 quantised linear, backward                                      */
+/* ======================================================================== */
+/* The paper's backward for the int8 linear layers passes the gradient through both quantisers unchanged
+   (straight-through estimator) and runs the two gradient GEMMs in int8 after rotating the operands along
+   the contraction dimension by a Walsh-Hadamard transform (training-details paragraph on int8
+   computation).  Here: blocks of 256, the Sylvester matrix scaled by 1/16, evaluated as the fast transform
+   with strides 1, 2, ..., 128; per-tensor absmax steps for the rotated operands. */
+static const uint32_t INV_127 = 0x3C010204u; /* RN32(1/127) */
+
+static void fwht_block(float* v) {
+  for (int h = 1; h < 256; h <<= 1)
+    for (int i = 0; i < 256; ++i)
+      if (!(i & h)) {
+        const float a = v[i], b = v[i + h];
+        v[i] = cref_add(a, b);
+        v[i + h] = cref_sub(a, b);
+      }
+  for (int i = 0; i < 256; ++i) v[i] = cref_mul(v[i], 0.0625f);
+}
+
+int cref_fwht256(int64_t n, float* v) {
+  if (n < 0 || n % 256) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t b = 0; b < n / 256; ++b) fwht_block(v + b * 256);
+  return 0;
+}
+
+/* per-tensor step of a rotated operand: RN(amax * RN(1/127)); amax orders |x| by bit pattern, so a NaN is
+   above every number and gives a NaN step (which quantises everything to 0) */
+static float absmax_step(const float* x, int64_t n) {
+  uint32_t m = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const uint32_t u = f_bits(daz(x[i])) & 0x7FFFFFFFu;
+    if (u > m) m = u;
+  }
+  return cref_mul(f_from_bits(m), f_from_bits(INV_127));
+}
+
+/* rotated-and-quantised operand [rows][L] from src viewed as [rows][L] (row stride L) */
+static void rot_quant(float* buf, int64_t rows, int64_t L, int8_t* q, float* step) {
+  cref_fwht256(rows * L, buf);
+  *step = absmax_step(buf, rows * L);
+  cref_quantize(rows, L, 0, buf, step, 0, q);
+}
+
+int cref_qlinear_bwd(int64_t T, int64_t N, int64_t K, const float* dy, const int8_t* qx, float sx, const int8_t* qw,
+                     const float* sw, float* dx, float* dw) {
+  if (T < 1 || N < 1 || K < 1 || (dx && N % 256) || (dw && T % 256) || !dy || !qx || !qw || !sw) return -1;
+  if (dx) { /* dx[t][k] = sum_n dy[t][n] W^[n][k]: contraction over N */
+    float* g = (float*)xmalloc(sizeof(float) * (size_t)(T * N));
+    memcpy(g, dy, sizeof(float) * (size_t)(T * N));
+    float* wt = (float*)xmalloc(sizeof(float) * (size_t)(K * N)); /* W^ transposed: [K][N] */
+    for (int64_t n = 0; n < N; ++n)
+      for (int64_t k = 0; k < K; ++k) wt[k * N + n] = cref_mul(sw[n], (float)qw[n * K + k]);
+    int8_t* qg = (int8_t*)xmalloc((size_t)(T * N));
+    int8_t* qwt = (int8_t*)xmalloc((size_t)(K * N));
+    float sg, swt;
+    rot_quant(g, T, N, qg, &sg);
+    rot_quant(wt, K, N, qwt, &swt);
+    float* sb = (float*)xmalloc(sizeof(float) * (size_t)K);
+    for (int64_t k = 0; k < K; ++k) sb[k] = swt;
+    cref_gemm_i8(T, K, N, qg, N, qwt, N, NULL, dx, K, sg, sb);
+    free(g); free(wt); free(qg); free(qwt); free(sb);
+  }
+  if (dw) { /* dw[n][k] = sum_t dy[t][n] X^[t][k]: contraction over T */
+    float* gt = (float*)xmalloc(sizeof(float) * (size_t)(N * T)); /* dy transposed: [N][T] */
+    for (int64_t t = 0; t < T; ++t)
+      for (int64_t n = 0; n < N; ++n) gt[n * T + t] = dy[t * N + n];
+    float* xt = (float*)xmalloc(sizeof(float) * (size_t)(K * T)); /* X^ transposed: [K][T] */
+    for (int64_t t = 0; t < T; ++t)
+      for (int64_t k = 0; k < K; ++k) xt[k * T + t] = cref_mul(sx, (float)qx[t * K + k]);
+    int8_t* qgt = (int8_t*)xmalloc((size_t)(N * T));
+    int8_t* qxt = (int8_t*)xmalloc((size_t)(K * T));
+    float sgt, sxt;
+    rot_quant(gt, N, T, qgt, &sgt);
+    rot_quant(xt, K, T, qxt, &sxt);
+    float* sb = (float*)xmalloc(sizeof(float) * (size_t)K);
+    for (int64_t k = 0; k < K; ++k) sb[k] = sxt;
+    cref_gemm_i8(N, K, T, qgt, T, qxt, T, NULL, dw, K, sgt, sb);
+    free(gt); free(xt); free(qgt); free(qxt); free(sb);
+  }
+  return 0;
+}
+
 int cref_num_threads(void) { return omp_get_max_threads(); }

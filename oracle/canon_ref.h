@@ -105,6 +105,18 @@ int cref_quantize(int64_t rows, int64_t cols, int32_t dtype, const void* x, cons
 int cref_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int64_t lda, const int8_t* b, int64_t ldb,
                  int32_t* acc, float* y, int64_t ldc, float sa, const float* sb);
 
+/* ---- R14 int8 quantised linear, backward (straight-through estimator, Walsh-Hadamard rotated) ----
+   fwht256: v (n values, n a multiple of 256) rotated in place block by block: per block of 256,
+     butterflies (a, b) -> (RN(a + b), RN(a - b)) over strides 1, 2, ..., 128, then RN(x * 1/16).
+   qlinear_bwd: given dy fp32 [T][N], the forward's int8 codes qx [T][K] (step sx) and qw [N][K] (steps
+     sw[N]), computes dx = dy . W^ and dw = dy^T . X^ (W^ = RN(sw[n] qw), X^ = RN(sx qx)) as int8 GEMMs:
+     each operand is rotated along the contraction dimension (N for dx, T for dw; a multiple of 256 when that output is asked for),
+     quantised with the per-tensor step RN(amax * RN(1/127)) (amax: the largest |value|, NaN above all),
+     multiplied exactly, and dequantised as RN(RN(RN32(acc) * s_left) * s_right).  dx or dw may be NULL. */
+int cref_fwht256(int64_t n, float* v);
+int cref_qlinear_bwd(int64_t T, int64_t N, int64_t K, const float* dy, const int8_t* qx, float sx, const int8_t* qw,
+                     const float* sw, float* dx, float* dw);
+
 int cref_num_threads(void);
 
 #ifdef __cplusplus

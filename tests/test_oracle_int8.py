@@ -107,3 +107,83 @@ def test_gemm_i8_extreme_range():
     a = np.full((1, k), -128, np.int8)
     acc, y = oracle.gemm_i8(a, a, np.float32(1.0), np.ones(1, np.float32))
     assert acc[0, 0] == 2 ** 30 and y[0, 0] == np.float32(2.0 ** 30)
+
+
+def sylvester(n):
+    h = np.array([[1]], np.int64)
+    while h.shape[0] < n:
+        h = np.block([[h, h], [h, -h]])
+    return h
+
+
+def test_fwht_matches_the_hadamard_matrix_on_integers():
+    # integer inputs keep every butterfly exact, so the transform must equal H_256 v / 16 exactly
+    H = sylvester(256)
+    v = RNG.integers(-1000, 1001, (3, 256)).astype(np.float32)
+    want = (v.astype(np.float64) @ H.T) / 16.0
+    got = oracle.fwht256(v)
+    assert np.array_equal(got.astype(np.float64), want)
+    assert np.array_equal(oracle.fwht256(got), v)  # the scaled transform is an involution in the exact regime
+
+
+def rot(x):
+    return oracle.fwht256(x)
+
+
+def one_hot_blocks(rows, L, rng, sign=True):
+    # 127 at one position per block of 256 (random sign): rotating such a row gives values +-127/16
+    v = np.zeros((rows, L), np.float32)
+    for r in range(rows):
+        for b in range(L // 256):
+            v[r, b * 256 + rng.integers(0, 256)] = 127.0 * (rng.choice([-1, 1]) if sign else 1)
+    return v
+
+
+def test_qlinear_bwd_exact_regime_dx():
+    # dy and W^ built so that both rotated operands are integers in [-127, 127] with 127 present: every step
+    # is 1, quantisation is exact, and dx must be the exact product rounded once
+    rng = np.random.default_rng(5)
+    T, N, K = 256, 512, 48
+    U = rng.integers(-127, 128, (T, N)).astype(np.float32)
+    U[0, 0] = 127
+    dy = rot(U)                                   # rot(dy) = U exactly
+    V = one_hot_blocks(K, N, rng)                 # rows k of W^ transposed, rotated
+    wt = rot(V)                                   # W^T: values +-127/16
+    qw = np.rint(wt.T * 16).astype(np.int8)       # W^ = qw / 16 exactly
+    sw = np.full(N, 1 / 16, np.float32)
+    qx = np.zeros((T, K), np.int8)
+    dx, _ = oracle.qlinear_bwd(dy, qx, 1.0, qw, sw, want_dw=False)
+    exact = U.astype(np.int64) @ V.astype(np.int64).T
+    assert np.array_equal(bits(dx), bits(exact.astype(np.float32)))
+
+
+def test_qlinear_bwd_exact_regime_dw():
+    rng = np.random.default_rng(6)
+    T, N, K = 512, 64, 40
+    G = rng.integers(-127, 128, (N, T)).astype(np.float32)
+    G[0, 0] = -127
+    dy = rot(G).T.copy()                          # rot along T of dy^T rows = G
+    V2 = one_hot_blocks(K, T, rng)
+    xt = rot(V2)                                  # X^ transposed: +-127/16
+    qx = np.rint(xt.T * 16).astype(np.int8)       # X^ = qx / 16 exactly
+    qw = np.zeros((N, K), np.int8)
+    _, dw = oracle.qlinear_bwd(dy, qx, 1 / 16, qw, np.ones(N, np.float32), want_dx=False)
+    exact = G.astype(np.int64) @ V2.astype(np.int64).T
+    assert np.array_equal(bits(dw), bits(exact.astype(np.float32)))
+
+
+def test_qlinear_bwd_error_against_float64():
+    # general inputs: the int8 gradients approximate the float64 products of the dequantised operands
+    rng = np.random.default_rng(7)
+    T, N, K = 512, 512, 64
+    dy = (rng.standard_normal((T, N)) * 1e-3).astype(np.float32)
+    dy[3, 7] = 0.05  # an outlier, which the rotation spreads
+    qx = rng.integers(-128, 128, (T, K)).astype(np.int8)
+    qw = rng.integers(-128, 128, (N, K)).astype(np.int8)
+    sx, sw = np.float32(0.02), (np.abs(rng.standard_normal(N)) * 0.001 + 1e-4).astype(np.float32)
+    dx, dw = oracle.qlinear_bwd(dy, qx, sx, qw, sw)
+    W = sw[:, None].astype(np.float64) * qw
+    X = float(sx) * qx.astype(np.float64)
+    for got, want in ((dx, dy.astype(np.float64) @ W), (dw, dy.astype(np.float64).T @ X)):
+        rel = np.linalg.norm(got - want) / np.linalg.norm(want)
+        assert rel < 0.05, rel
