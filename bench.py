@@ -129,6 +129,23 @@ def kernel_table(C, I, torch, np, stream, dev):
                                               "unit": "TOP/s", "peak": PEAK_INT8_MFMA,
                                               "frac": round(tops / PEAK_INT8_MFMA, 4)}
         del qa, qb, yq
+    # int8 backward of the gate/up projection: rotated straight-through dx and dW (2 GEMMs of 2*T*N*K each)
+    Tq, Nq, Kq = 8192, 16384, 2048
+    dyq = randn((Tq, Nq), 1e-3)
+    qxq = torch.randint(-128, 128, (Tq, Kq), generator=g, device=dev, dtype=torch.int8)
+    qwq = torch.randint(-128, 128, (Nq, Kq), generator=g, device=dev, dtype=torch.int8)
+    sxq = torch.full((1,), 0.02, device=dev)
+    swq = torch.full((Nq,), 0.001, device=dev)
+    dxq = torch.empty((Tq, Kq), device=dev)
+    dwq = torch.empty((Nq, Kq), device=dev)
+    wsq = torch.empty(C.qlinear_bwd_workspace_bytes(Tq, Nq, Kq), dtype=torch.uint8, device=dev)
+    ms = _timed(torch, stream, lambda: C.qlinear_bwd(Tq, Nq, Kq, dyq, qxq, sxq, qwq, swq, dxq, dwq, wsq,
+                                                    stream=stream), 3)
+    tops = 2 * 2.0 * Tq * Nq * Kq / (ms * 1e-3) / 1e12
+    out[f"qlinear_bwd_gate_up_{Tq}x{Nq}x{Kq}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tops, 1),
+                                                 "unit": "TOP/s", "peak": PEAK_INT8_MFMA,
+                                                 "frac": round(tops / PEAK_INT8_MFMA, 4)}
+    del dyq, qxq, qwq, dxq, dwq, wsq
     wq = randn((16384, 2048), 0.02, torch.bfloat16)
     swq = torch.empty(16384, dtype=torch.float32, device=dev)
     ms = _timed(torch, stream, lambda: C.quant_scales(16384, 2048, wq, swq, stream=stream), 10)

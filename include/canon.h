@@ -190,6 +190,22 @@ canon_status canon_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int
                            int64_t ldb, int32_t* acc, float* y, int64_t ldc, const float* sa, const float* sb,
                            void* stream);
 
+/* Backward of the int8 quantised linear (the same training-details paragraph: straight-through
+   estimator, both gradient GEMMs in int8 after a Walsh-Hadamard rotation along the contraction
+   dimension).  Inputs: dy fp32 [T, N]; the forward's codes qx int8 [T, K] with the device scalar step sx
+   and qw int8 [N, K] with the device steps sw [N].  Outputs (either may be NULL): dx fp32 [T, K] =
+   dy . W^ and dw fp32 [N, K] = dy^T . X^, where W^ = RN(sw[n] * qw), X^ = RN(sx * qx).  Each operand is
+   rotated along the contraction dimension (N for dx, T for dw; a multiple of 256 when that output is
+   asked for) in blocks of 256 by the Sylvester matrix scaled by 1/16 (fast transform, strides 1..128),
+   quantised with the per-tensor step RN(amax * RN(1/127)) (amax: the largest |value| by bit pattern),
+   multiplied exactly on the int8 matrix cores and dequantised as RN(RN(RN32(acc) * s_left) * s_right).
+   workspace: device memory of canon_qlinear_bwd_workspace_bytes(T, N, K) bytes (rotated operands and
+   their codes); T*N and K*max(N, T) at most 2^34. */
+canon_status canon_qlinear_bwd(const canon_order* order, int64_t T, int64_t N, int64_t K, const float* dy,
+                               const int8_t* qx, const float* sx, const int8_t* qw, const float* sw, float* dx,
+                               float* dw, void* workspace, size_t workspace_bytes, void* stream);
+size_t canon_qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K);
+
 /* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
    the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,
    10 bf16 round trip.  a, b, c, out: device fp32 [n] (b, c may be NULL when unused). */

@@ -72,6 +72,8 @@ def _lib():
             "canon_quant_scales": (i32, [vp, i64, i64, vp, vp, vp]),
             "canon_quantize": (i32, [i64, i64, i32, vp, vp, i32, vp, vp]),
             "canon_gemm_i8": (i32, [i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, vp, vp, vp]),
+            "canon_qlinear_bwd": (i32, [vp, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+            "canon_qlinear_bwd_workspace_bytes": (sz, [i64, i64, i64]),
             "canon_status_str": (ctypes.c_char_p, [i32]),
             "canon_version": (i32, []),
         }
@@ -194,6 +196,16 @@ def quantize(rows, cols, x, scale, per_row, q, stream=None):
 def gemm_i8(m, n, k, a, lda, b, ldb, acc=None, y=None, ldc=None, sa=None, sb=None, stream=None):
     _check(_lib().canon_gemm_i8(m, n, k, _ptr(a), lda, _ptr(b), ldb, _ptr(acc), _ptr(y), n if ldc is None else ldc,
                                 _ptr(sa), _ptr(sb), _stream(stream)), "canon_gemm_i8")
+
+
+def qlinear_bwd_workspace_bytes(T, N, K) -> int:
+    return int(_lib().canon_qlinear_bwd_workspace_bytes(T, N, K))
+
+
+def qlinear_bwd(T, N, K, dy, qx, sx, qw, sw, dx, dw, workspace, order=ORDER_V1, stream=None):
+    _check(_lib().canon_qlinear_bwd(ctypes.byref(order), T, N, K, _ptr(dy), _ptr(qx), _ptr(sx), _ptr(qw), _ptr(sw),
+                                    _ptr(dx), _ptr(dw), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                    _stream(stream)), "canon_qlinear_bwd")
 
 
 def devmath(op: str, n, a, b=None, c=None, out=None, stream=None):

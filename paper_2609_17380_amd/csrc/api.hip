@@ -489,6 +489,26 @@ canon_status canon_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int
   return dev(gemm_i8_launch(g, as_stream(stream)));
 }
 
+canon_status canon_qlinear_bwd(const canon_order* order, int64_t T, int64_t N, int64_t K, const float* dy,
+                               const int8_t* qx, const float* sx, const int8_t* qw, const float* sw, float* dx,
+                               float* dw, void* workspace, size_t workspace_bytes, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (T < 1 || N < 1 || K < 1 || (!dx && !dw)) return CANON_EINVAL;
+  if ((dx && N % 256) || (dw && T % 256)) return CANON_EUNSUPPORTED;  // whole rotation blocks
+  if ((dx && N > 65536) || (dw && T > 65536)) return CANON_EUNSUPPORTED;  // the int8 GEMM's k bound
+  if (T * N > (int64_t(1) << 34) || K * (N > T ? N : T) > (int64_t(1) << 34)) return CANON_EUNSUPPORTED;
+  if (!dy || !qx || !sx || !qw || !sw || !workspace) return CANON_EINVAL;
+  if (workspace_bytes < qlinear_bwd_workspace_bytes(T, N, K)) return CANON_EWORKSPACE;
+  if (((uintptr_t)dy & 15) || ((uintptr_t)workspace & 255)) return CANON_EINVAL;
+  return dev(qlinear_bwd_launch(T, N, K, dy, qx, sx, qw, sw, dx, dw, workspace, as_stream(stream)));
+}
+
+size_t canon_qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K) {
+  if (T < 1 || N < 1 || K < 1) return 0;
+  return qlinear_bwd_workspace_bytes(T, N, K);
+}
+
 canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m,
                          float* const* v, const float* const* grads, const uint8_t* decay_mask,
                          const canon_adamw_consts* consts, void* stream) {

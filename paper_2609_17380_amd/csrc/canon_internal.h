@@ -31,9 +31,15 @@ struct GemmI8Args {
   const float* sa;  // device scalar (needed when y is set)
   const float* sb;  // device [n] (needed when y is set)
   int64_t m, n, k, lda, ldb, ldc;
-  int32_t vec;      // set by the launcher
+  int32_t sb_scalar;  // 1: sb[0] for every column
+  int32_t vec;        // set by the launcher
 };
 hipError_t gemm_i8_launch(const GemmI8Args& g, hipStream_t s);
+
+// qlinear.hip: int8 backward (rotated straight-through gradients)
+size_t qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K);
+hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const float* dy, const int8_t* qx, const float* sx,
+                              const int8_t* qw, const float* sw, float* dx, float* dw, void* ws, hipStream_t s);
 int gemm_max_levels();
 
 // rows.hip

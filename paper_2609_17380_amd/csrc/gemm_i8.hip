@@ -7,9 +7,10 @@
 // reordered and spread over matrix instructions freely.  The dequantised output is
 // y[i][j] = RN(RN(RN32(acc) * sa) * sb[j]).
 //
-// Tiling: a workgroup of 4 wavefronts owns a 128 x 128 output tile, each wavefront a 64 x 64 block made of
-// 2 x 2 v_mfma_i32_32x32x32_i8 blocks.  Stages of 64 k bytes are staged through LDS (rows padded to 80
-// bytes, which makes the 16-byte operand reads of 32 consecutive rows conflict-free), double buffered.
+// Tiling: a workgroup of 4 wavefronts owns a 128 x 64 WN output tile, each wavefront a 64 x 32 WN block made
+// of 2 x WN v_mfma_i32_32x32x32_i8 blocks (WN = 2: 128 x 128 tiles, measured best at the 1B shapes).  Stages
+// of KS = 128 k bytes are staged through LDS (rows padded by 16 bytes, which keeps the 16-byte operand reads
+// of 32 consecutive rows free of bank conflicts), double buffered.
 // Each lane of a 32x32x32 instruction supplies 16 consecutive k bytes of one row of A and of B; the two
 // half-wavefronts cover k 0..15 and 16..31 of the instruction's 32.
 #include <hip/hip_runtime.h>
@@ -21,11 +22,19 @@ namespace canon {
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int QBM = 128, QBN = 128, QKS = 64;
-constexpr int QLD = QKS + 16;
+constexpr int QBM = 128;
 
+template <int WN, int KS>
+struct I8Cfg {
+  static constexpr int BN = 64 * WN;          // workgroup tile columns
+  static constexpr int LD = KS + 16;          // padded LDS row (bytes)
+  static constexpr int AV = QBM * KS / 16 / 256;  // 16-byte vectors of A per thread per stage
+  static constexpr int BV = BN * KS / 16 / 256;   // ... of B
+};
+
+template <int WN, int KS>
 struct I8Raw {
-  uint4 a[2], b[2];
+  uint4 a[I8Cfg<WN, KS>::AV], b[I8Cfg<WN, KS>::BV];
 };
 
 // 16 consecutive bytes of which the first `valid` exist (zero fill beyond)
@@ -38,40 +47,56 @@ __device__ __forceinline__ uint4 ld16(const int8_t* p, int64_t valid, bool vec) 
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-template <bool FAST>
-__device__ __forceinline__ I8Raw load_stage(const GemmI8Args& g, int64_t row0, int64_t col0, int64_t k0) {
+// Global -> registers for the stage starting at k0: vector idx = t + 256 it covers row idx / (KS/16),
+// 16-byte segment idx % (KS/16) of the row's KS bytes.
+template <int WN, int KS, bool FAST>
+__device__ __forceinline__ I8Raw<WN, KS> load_stage(const GemmI8Args& g, int64_t row0, int64_t col0, int64_t k0) {
+  using Cf = I8Cfg<WN, KS>;
+  constexpr int SEG = KS / 16;
   const int t = threadIdx.x;
-  I8Raw r;
+  I8Raw<WN, KS> r;
 #pragma unroll
-  for (int it = 0; it < 2; ++it) {
+  for (int it = 0; it < Cf::AV; ++it) {
     const int idx = t + 256 * it;
-    const int rr = idx >> 2;
-    const int64_t k = k0 + 16 * (idx & 3);
-    const int64_t row = row0 + rr, col = col0 + rr;
+    const int64_t k = k0 + 16 * (idx % SEG), row = row0 + idx / SEG;
     r.a[it] = ld16<FAST>(g.a + row * g.lda + k, (row < g.m) ? g.k - k : 0, g.vec);
+  }
+#pragma unroll
+  for (int it = 0; it < Cf::BV; ++it) {
+    const int idx = t + 256 * it;
+    const int64_t k = k0 + 16 * (idx % SEG), col = col0 + idx / SEG;
     r.b[it] = ld16<FAST>(g.b + col * g.ldb + k, (col < g.n) ? g.k - k : 0, g.vec);
   }
   return r;
 }
 
-__device__ __forceinline__ void store_stage(int8_t* As, int8_t* Bs, const I8Raw& r) {
+template <int WN, int KS>
+__device__ __forceinline__ void store_stage(int8_t* As, int8_t* Bs, const I8Raw<WN, KS>& r) {
+  using Cf = I8Cfg<WN, KS>;
+  constexpr int SEG = KS / 16;
   const int t = threadIdx.x;
 #pragma unroll
-  for (int it = 0; it < 2; ++it) {
+  for (int it = 0; it < Cf::AV; ++it) {
     const int idx = t + 256 * it;
-    const int off = (idx >> 2) * QLD + 16 * (idx & 3);
-    *reinterpret_cast<uint4*>(As + off) = r.a[it];
-    *reinterpret_cast<uint4*>(Bs + off) = r.b[it];
+    *reinterpret_cast<uint4*>(As + (idx / SEG) * Cf::LD + 16 * (idx % SEG)) = r.a[it];
+  }
+#pragma unroll
+  for (int it = 0; it < Cf::BV; ++it) {
+    const int idx = t + 256 * it;
+    *reinterpret_cast<uint4*>(Bs + (idx / SEG) * Cf::LD + 16 * (idx % SEG)) = r.b[it];
   }
 }
 
+template <int WN, int KS>
 __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
-  __shared__ __attribute__((aligned(16))) int8_t As[2][QBM * QLD];
-  __shared__ __attribute__((aligned(16))) int8_t Bs[2][QBN * QLD];
+  using Cf = I8Cfg<WN, KS>;
+  constexpr int BN = Cf::BN, LD = Cf::LD;
+  __shared__ __attribute__((aligned(16))) int8_t As[2][QBM * LD];
+  __shared__ __attribute__((aligned(16))) int8_t Bs[2][BN * LD];
 
   // tile order: a contiguous run of tiles per XCD, walked in groups of 8 tile rows
   constexpr int64_t GM = 8;
-  const int64_t tiles_n = (g.n + QBN - 1) / QBN;
+  const int64_t tiles_n = (g.n + BN - 1) / BN;
   const int64_t tiles_m = (g.m + QBM - 1) / QBM;
   const int64_t tiles = tiles_m * tiles_n;
   int64_t tile = blockIdx.x;
@@ -80,50 +105,53 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
   const int64_t first_m = group * GM;
   const int64_t gsize = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
   const int64_t within = tile - group * GM * tiles_n;
-  const int64_t row0 = (first_m + within % gsize) * QBM, col0 = (within / gsize) * QBN;
-  const bool tile_in = g.vec && row0 + QBM <= g.m && col0 + QBN <= g.n;
+  const int64_t row0 = (first_m + within % gsize) * QBM, col0 = (within / gsize) * BN;
+  const bool tile_in = g.vec && row0 + QBM <= g.m && col0 + BN <= g.n;
 
+  // wavefront (wr, wc) owns rows [64 wr, 64 wr + 64) and columns [32 WN wc, 32 WN (wc + 1)) of the tile
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int wr = w >> 1, wc = w & 1;
-  const int ar = 64 * wr + (lane & 31), bc = 64 * wc + (lane & 31);
+  const int ar = 64 * wr + (lane & 31), bc = 32 * WN * wc + (lane & 31);
   const int kh = 16 * (lane >> 5);
 
-  i32x16 acc[2][2];
+  i32x16 acc[2][WN];
 #pragma unroll
   for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int v2 = 0; v2 < 2; ++v2)
+    for (int v2 = 0; v2 < WN; ++v2)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[h][v2][v] = 0;
 
-  const int64_t ns = (g.k + QKS - 1) / QKS;
+  const int64_t ns = (g.k + KS - 1) / KS;
   int buf = 0;
-  if (ns > 0) store_stage(As[0], Bs[0], load_stage<false>(g, row0, col0, 0));
+  if (ns > 0) store_stage<WN, KS>(As[0], Bs[0], load_stage<WN, KS, false>(g, row0, col0, 0));
   __syncthreads();
   for (int64_t s = 0; s < ns; ++s) {
     const bool more = s + 1 < ns;
-    I8Raw nxt;
+    I8Raw<WN, KS> nxt;
     if (more) {
-      if (tile_in && (s + 2) * QKS <= g.k) nxt = load_stage<true>(g, row0, col0, (s + 1) * QKS);
-      else nxt = load_stage<false>(g, row0, col0, (s + 1) * QKS);
+      if (tile_in && (s + 2) * KS <= g.k) nxt = load_stage<WN, KS, true>(g, row0, col0, (s + 1) * KS);
+      else nxt = load_stage<WN, KS, false>(g, row0, col0, (s + 1) * KS);
     }
     __builtin_amdgcn_sched_barrier(0);
     const int8_t* as = As[buf];
     const int8_t* bs = Bs[buf];
 #pragma unroll
-    for (int ks = 0; ks < QKS / 32; ++ks) {
+    for (int ks = 0; ks < KS / 32; ++ks) {
       const int kk = 32 * ks + kh;
-      const i32x4 a0 = *reinterpret_cast<const i32x4*>(as + ar * QLD + kk);
-      const i32x4 a1 = *reinterpret_cast<const i32x4*>(as + (ar + 32) * QLD + kk);
-      const i32x4 b0 = *reinterpret_cast<const i32x4*>(bs + bc * QLD + kk);
-      const i32x4 b1 = *reinterpret_cast<const i32x4*>(bs + (bc + 32) * QLD + kk);
-      acc[0][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a0, b0, acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a0, b1, acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a1, b0, acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a1, b1, acc[1][1], 0, 0, 0);
+      i32x4 a[2], b[WN];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) a[h] = *reinterpret_cast<const i32x4*>(as + (ar + 32 * h) * LD + kk);
+#pragma unroll
+      for (int v2 = 0; v2 < WN; ++v2) b[v2] = *reinterpret_cast<const i32x4*>(bs + (bc + 32 * v2) * LD + kk);
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int v2 = 0; v2 < WN; ++v2)
+          acc[h][v2] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[h], b[v2], acc[h][v2], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (more) store_stage(As[buf ^ 1], Bs[buf ^ 1], nxt);
+    if (more) store_stage<WN, KS>(As[buf ^ 1], Bs[buf ^ 1], nxt);
     __syncthreads();
     buf ^= 1;
   }
@@ -133,29 +161,32 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
 #pragma unroll
   for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int v2 = 0; v2 < 2; ++v2)
+    for (int v2 = 0; v2 < WN; ++v2)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int64_t i = row0 + 64 * wr + 32 * h + (v & 3) + 4 * (lane >> 5) + 8 * (v >> 2);
-        const int64_t j = col0 + 64 * wc + 32 * v2 + (lane & 31);
+        const int64_t j = col0 + 32 * WN * wc + 32 * v2 + (lane & 31);
         if (i < g.m && j < g.n) {
           const int32_t a = acc[h][v2][v];
           if (g.acc) g.acc[i * g.ldc + j] = a;
           if (g.y) {
             const float af = (float)a;  // round to nearest even
             const float t = af * sa;
-            g.y[i * g.ldc + j] = t * g.sb[j];
+            g.y[i * g.ldc + j] = t * g.sb[g.sb_scalar ? 0 : j];
           }
         }
       }
 }
 
+constexpr int I8_WN = 2, I8_KS = 128;
+
 hipError_t gemm_i8_launch(const GemmI8Args& gin, hipStream_t s) {
   if (gin.m == 0 || gin.n == 0) return hipSuccess;
   GemmI8Args g = gin;
   g.vec = ((uintptr_t)g.a & 15) == 0 && ((uintptr_t)g.b & 15) == 0 && g.lda % 16 == 0 && g.ldb % 16 == 0;
-  const int64_t tiles = ((g.m + QBM - 1) / QBM) * ((g.n + QBN - 1) / QBN);
-  hipLaunchKernelGGL(gemm_i8_kernel, dim3((unsigned)tiles), dim3(256), 0, s, g);
+  constexpr int BN = I8Cfg<I8_WN, I8_KS>::BN;
+  const int64_t tiles = ((g.m + QBM - 1) / QBM) * ((g.n + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_i8_kernel<I8_WN, I8_KS>), dim3((unsigned)tiles), dim3(256), 0, s, g);
   return hipGetLastError();
 }
 

@@ -121,3 +121,37 @@ def test_quantised_linear_1b_shapes_sampled():
     assert np.array_equal(qx.cpu().numpy()[rows], qx_o)
     _, y_o = oracle.gemm_i8(qx_o, qw_o, sx[0], sw_o)
     assert_bits(host_f32(y)[rows], y_o, "y rows")
+
+
+def qlinear_bwd_case(T, N, K, seed, want_dx=True, want_dw=True, outlier=True):
+    rng = np.random.default_rng(seed)
+    dy = (rng.standard_normal((T, N)) * 1e-3).astype(np.float32)
+    if outlier:
+        dy[1, 3] = 0.08
+    dy[0, :4] = np.array([1e-40, -0.0, 0.0, 3e-39], np.float32)  # subnormal and signed-zero inputs
+    qx = rng.integers(-128, 128, (T, K)).astype(np.int8)
+    qw = rng.integers(-128, 128, (N, K)).astype(np.int8)
+    sx = np.array([0.021], np.float32)
+    sw = (np.abs(rng.standard_normal(N)) * 0.001 + 1e-4).astype(np.float32)
+    dx_o, dw_o = oracle.qlinear_bwd(dy, qx, sx[0], qw, sw, want_dx=want_dx, want_dw=want_dw)
+    ws = torch.empty(C.qlinear_bwd_workspace_bytes(T, N, K), dtype=torch.uint8, device=DEV)
+    dx = torch.full((T, K), float("nan"), device=DEV) if want_dx else None
+    dw = torch.full((N, K), float("nan"), device=DEV) if want_dw else None
+    C.qlinear_bwd(T, N, K, dev_f32(dy), dev_i8(qx), dev_f32(sx), dev_i8(qw), dev_f32(sw), dx, dw, ws)
+    torch.cuda.synchronize()
+    if want_dx:
+        assert_bits(host_f32(dx), dx_o, "dx")
+    if want_dw:
+        assert_bits(host_f32(dw), dw_o, "dw")
+
+
+@pytest.mark.parametrize("T,N,K", [(256, 256, 64), (512, 768, 72), (256, 512, 1), (768, 256, 130)])
+def test_qlinear_bwd(T, N, K):
+    print(f"qlinear_bwd {T}x{N}x{K}", flush=True)
+    qlinear_bwd_case(T, N, K, seed=T + N + K)
+
+
+def test_qlinear_bwd_one_output_and_mid_size():
+    qlinear_bwd_case(256, 96, 40, seed=1, want_dx=False)   # dW only: N need not be a multiple of 256
+    qlinear_bwd_case(80, 512, 40, seed=2, want_dw=False)   # dx only: T need not be a multiple of 256
+    qlinear_bwd_case(2048, 2048, 512, seed=3)              # several tiles per operand, full rotation blocks
