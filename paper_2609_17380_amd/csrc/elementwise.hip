@@ -282,31 +282,61 @@ hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win,
 // Quantiser of the int8 quantised linear: q = clamp(rne(RN(x / s)), -128, 127), x fp32 (dtype 0) or bf16
 // (dtype 1), one step per row or for the whole tensor.  A step that is not > 0 once flushed, or a NaN
 // quotient, gives 0.
+__device__ __forceinline__ int8_t quant1(float v, float sv) {
+  int8_t out = 0;
+  if (sv > 0.0f) {
+    const float t = v / sv;
+    if (t == t) {
+      const float r = __builtin_rintf(t);
+      out = (int8_t)(int)fminf(fmaxf(r, -128.0f), 127.0f);
+    }
+  }
+  return out;
+}
+
+__device__ __forceinline__ float step_daz(float s) {
+  uint32_t sb = __float_as_uint(s);
+  if ((sb & 0x7F800000u) == 0u) sb &= 0x80000000u;  // a subnormal step reads as zero
+  return __uint_as_float(sb);
+}
+
 template <int DT>
 __global__ void quantize_kernel(int64_t rows, int64_t cols, const void* __restrict__ x,
                                 const float* __restrict__ scale, int32_t per_row, int8_t* __restrict__ q) {
   const int64_t n = rows * cols;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
-    uint32_t sb = __float_as_uint(scale[per_row ? i / cols : 0]);
-    if ((sb & 0x7F800000u) == 0u) sb &= 0x80000000u;  // a subnormal step reads as zero
-    const float sv = __uint_as_float(sb);
+    const float sv = step_daz(scale[per_row ? i / cols : 0]);
     const float v = DT == 0 ? static_cast<const float*>(x)[i] : bf16_to_f32(static_cast<const uint16_t*>(x)[i]);
-    int8_t out = 0;
-    if (sv > 0.0f) {
-      const float t = v / sv;
-      if (t == t) {
-        const float r = __builtin_rintf(t);
-        out = (int8_t)(int)fminf(fmaxf(r, -128.0f), 127.0f);
-      }
-    }
-    q[i] = out;
+    q[i] = quant1(v, sv);
   }
+}
+
+// one step for the whole tensor, fp32 input, 16-byte aligned x and 4-byte aligned q: 4 values per thread
+__global__ void quantize_tensor4_kernel(int64_t n, const float* __restrict__ x, const float* __restrict__ scale,
+                                        int8_t* __restrict__ q) {
+  const float sv = step_daz(scale[0]);
+  const int64_t n4 = n >> 2;
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+    const float4 v = reinterpret_cast<const float4*>(x)[i];
+    const uint32_t b0 = (uint8_t)quant1(v.x, sv), b1 = (uint8_t)quant1(v.y, sv), b2 = (uint8_t)quant1(v.z, sv),
+                   b3 = (uint8_t)quant1(v.w, sv);
+    reinterpret_cast<uint32_t*>(q)[i] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+  }
+  const int64_t t = n4 * 4 + (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t < n) q[t] = quant1(x[t], sv);
 }
 
 hipError_t quantize_launch(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale,
                            int32_t per_row, int8_t* q, hipStream_t s) {
   const int64_t n = rows * cols;
   if (n == 0) return hipSuccess;
+  if (dtype == 0 && !per_row && ((uintptr_t)x & 15) == 0 && ((uintptr_t)q & 3) == 0) {
+    int64_t b = ((n >> 2) + 255) / 256;
+    if (b < 1) b = 1;
+    const unsigned grid = (unsigned)(b < (1 << 20) ? b : (1 << 20));
+    hipLaunchKernelGGL(quantize_tensor4_kernel, dim3(grid), dim3(256), 0, s, n, (const float*)x, scale, q);
+    return hipGetLastError();
+  }
   int64_t b = (n + 255) / 256;
   const unsigned grid = (unsigned)(b < (1 << 20) ? b : (1 << 20));
   if (dtype == 0)

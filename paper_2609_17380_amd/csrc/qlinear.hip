@@ -41,15 +41,15 @@ __global__ __launch_bounds__(256) void transpose_kernel(int64_t R, int64_t C, co
 }
 
 // dst = blockwise rotation of src (n values, blocks of 256; in place allowed), and amax = max over the
-// bit patterns of |result| (atomic max of non-negative patterns: order-free).  One wavefront per block,
-// lane l holding values 4l .. 4l+3; butterflies of strides 1 and 2 inside the lane, the others across
-// lanes by xor shuffles.
+// bit patterns of |result| (an atomic max of non-negative patterns, which is order-free).  Each wavefront
+// rotates blocks in a grid-stride loop, lane l holding values 4l .. 4l+3: butterflies of strides 1 and 2
+// inside the lane, the others across lanes by xor shuffles.  One atomic per workgroup.
 __global__ __launch_bounds__(256) void fwht_kernel(int64_t n, const float* __restrict__ src, float* dst,
                                                    uint32_t* __restrict__ amax) {
-  const int lane = threadIdx.x & 63;
-  const int64_t blk = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  __shared__ uint32_t wmax[4];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   uint32_t m = 0;
-  if (blk * 256 < n) {
+  for (int64_t blk = (int64_t)blockIdx.x * 4 + wv; blk * 256 < n; blk += (int64_t)gridDim.x * 4) {
     const float4 x = reinterpret_cast<const float4*>(src + blk * 256)[lane];
     float v[4] = {x.x, x.y, x.z, x.w};
     {  // stride 1: pairs (0,1), (2,3); stride 2: pairs (0,2), (1,3)
@@ -85,7 +85,13 @@ __global__ __launch_bounds__(256) void fwht_kernel(int64_t n, const float* __res
     const uint32_t o = __shfl_xor(m, s, 64);
     m = o > m ? o : m;
   }
-  if (lane == 0 && m) atomicMax(amax, m);
+  if (lane == 0) wmax[wv] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = wmax[0];
+    for (int i = 1; i < 4; ++i) t = wmax[i] > t ? wmax[i] : t;
+    if (t) atomicMax(amax, t);
+  }
 }
 
 __global__ void qlin_zero_kernel(uint32_t* amax, int n) {
@@ -100,7 +106,8 @@ __global__ void qlin_step_kernel(const uint32_t* __restrict__ amax, float* __res
 static hipError_t fwht_launch(int64_t n, const float* src, float* dst, uint32_t* amax, hipStream_t s) {
   const int64_t blocks = n / 256;
   if (blocks == 0) return hipSuccess;
-  hipLaunchKernelGGL(fwht_kernel, dim3((unsigned)((blocks + 3) / 4)), dim3(256), 0, s, n, src, dst, amax);
+  const int64_t wgs = (blocks + 3) / 4;
+  hipLaunchKernelGGL(fwht_kernel, dim3((unsigned)(wgs < 4096 ? wgs : 4096)), dim3(256), 0, s, n, src, dst, amax);
   return hipGetLastError();
 }
 
