@@ -193,13 +193,15 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
   TRY(gemm(mk(1, 0, d, d, T, sc.dy_b, d, sv.O, d, dw[2], d), s));        // dW_o = dh^T O
   TRY(gemm(mk(0, 0, T, d, d, sc.dy_b, d, w[2], d, sc.dO, d, 1), s));     // dO = dh W_o (bf16)
   TRY(attn_rowdot_launch(D.B, H, S, hd, sc.dO, sv.O, d, sc.Dv, s));      // D = rowsum(dO * O)
-  {  // dP = dO V^T, lower-triangle tiles
-    GemmArgs g = batched(mk(0, 1, S, S, hd, sc.dO, d, sv.v, hd, sc.scores, S), D, S * d, hd, H * S * hd, S * hd,
+  {  // dP = dO V^T on the lower-triangle tiles, turned into dS = P * (dP - D) * c in the epilogue (bf16)
+    GemmArgs g = batched(mk(0, 1, S, S, hd, sc.dO, d, sv.v, hd, sc.dS, S), D, S * d, hd, H * S * hd, S * hd,
                          H * S * S, S * S);
     g.tri_lower = 1;
+    g.epi = EPI_DS;
+    g.ds_p = sv.P; g.ds_d = sc.Dv; g.ds_scale = D.scale;
+    g.ds_ldp = S; g.ds_sp1 = H * S * S; g.ds_sp2 = S * S; g.ds_sd1 = H * S; g.ds_sd2 = S;
     TRY(gemm(g, s));
   }
-  TRY(attn_dS_launch(D.B * H, S, sv.P, sc.scores, sc.Dv, D.scale, sc.dS, s));
   {  // dQ = dS K (over keys)
     GemmArgs g = batched(mk(0, 0, S, hd, S, sc.dS, S, sv.k, hd, sc.dq, d), D, H * S * S, S * S, H * S * hd, S * hd,
                          S * d, hd);

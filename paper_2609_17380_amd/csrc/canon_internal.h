@@ -18,7 +18,17 @@ struct GemmArgs {
   int64_t nb2, batch;
   int32_t trans_a, trans_b, out_bf16, kmode, tri_lower;
   int32_t vec;  // set by the launcher: 16-byte operand loads allowed
+  // EPI_DS epilogue (attention backward, R5): the finished value d = dP[i][j] of a square per-head matrix
+  // becomes dS[i][j] = bf16(RN(RN(P[i][j] * RN(d - D[i])) * ds_scale)) for j <= i, 0 above the diagonal,
+  // written as bf16 into C.  P: bf16 with leading dim ds_ldp and batch offsets ds_sp1/ds_sp2; D: fp32
+  // per row with batch offsets ds_sd1/ds_sd2.
+  int32_t epi;
+  const uint16_t* ds_p;
+  const float* ds_d;
+  float ds_scale;
+  int64_t ds_ldp, ds_sp1, ds_sp2, ds_sd1, ds_sd2;
 };
+enum { EPI_NONE = 0, EPI_DS = 1 };
 
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);
 
@@ -54,8 +64,6 @@ hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, cons
 hipError_t quant_scales_launch(int64_t rows, int64_t cols, const uint16_t* w, float* scale, hipStream_t s);
 hipError_t attn_rowdot_launch(int64_t B, int64_t H, int64_t S, int64_t hd, const uint16_t* dO, const uint16_t* O,
                               int64_t ld, float* D, hipStream_t s);
-hipError_t attn_dS_launch(int64_t BH, int64_t S, const uint16_t* P, const float* dP, const float* D, float scale,
-                          uint16_t* dS, hipStream_t s);
 
 // elementwise.hip
 hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* qkv, const float* cosT,

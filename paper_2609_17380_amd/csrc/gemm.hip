@@ -306,7 +306,14 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   const int64_t first_m = group * GM;
   const int64_t gsize = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
   const int64_t within = tile - group * GM * tiles_n;
-  const int64_t tm = first_m + within % gsize, tn = within / gsize;
+  int64_t tm = first_m + within % gsize, tn = within / gsize;
+  if (g.kmode != KMODE_FULL) {
+    // causally skipping GEMMs: tile cost grows with the row tile (TRAIL) or shrinks with it (LEAD); launch the
+    // longest tiles first so the short ones fill the tail
+    tm = blockIdx.x / tiles_n;
+    tn = blockIdx.x % tiles_n;
+    if (g.kmode == KMODE_TRAIL) tm = tiles_m - 1 - tm;
+  }
   const int64_t row0 = tm * BM, col0 = tn * BN;
   if (g.tri_lower && col0 > row0 + BM - 1) return;  // output tile entirely above the diagonal
 
@@ -427,6 +434,27 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
 
   // store: register v, lane l -> block v/16, row (v%4) + 4*(l/32) + 8*((v%16)/4), column l%32
   const int64_t crow0 = row0 + wr * 32, ccol0 = col0 + wc * 64;
+  if (g.epi == EPI_DS) {
+    uint16_t* C = (uint16_t*)g.c + z1 * g.sc1 + z2 * g.sc2;
+    const uint16_t* P = g.ds_p + z1 * g.ds_sp1 + z2 * g.ds_sp2;
+    const float* Dv = g.ds_d + z1 * g.ds_sd1 + z2 * g.ds_sd2;
+#pragma unroll
+    for (int v = 0; v < 32; ++v) {
+      const int vv = v & 15, blk = v >> 4;
+      const int64_t i = crow0 + (vv & 3) + 4 * (lane >> 5) + 8 * (vv >> 2);
+      const int64_t j = ccol0 + blk * 32 + (lane & 31);
+      if (i < g.m && j < g.n) {
+        uint16_t o = 0;
+        if (j <= i) {
+          const float t = r[v] - Dv[i];
+          const float u = bf16_to_f32(P[i * g.ds_ldp + j]) * t;
+          o = f32_to_bf16(u * g.ds_scale);
+        }
+        C[i * g.ldc + j] = o;
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int v = 0; v < 32; ++v) {
     const int vv = v & 15, blk = v >> 4;

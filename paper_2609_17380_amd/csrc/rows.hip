@@ -923,29 +923,4 @@ hipError_t attn_rowdot_launch(int64_t B, int64_t H, int64_t S, int64_t hd, const
   return hipGetLastError();
 }
 
-// dS = bf16(RN(RN(P * RN(dP - D)) * scale)) for j <= i, +0 for masked keys.
-__global__ __launch_bounds__(256) void attn_dS_kernel(int64_t BH, int64_t S, const uint16_t* __restrict__ P,
-                                                      const float* __restrict__ dP, const float* __restrict__ D,
-                                                      float scale, uint16_t* __restrict__ dS) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = BH * S * S;
-  if (idx >= total) return;
-  const int64_t j = idx % S, row = idx / S, i = row % S;
-  uint16_t o = 0;
-  if (j <= i) {
-    float t = dP[idx] - D[row];
-    float u = bf16_to_f32(P[idx]) * t;
-    o = f32_to_bf16(u * scale);
-  }
-  dS[idx] = o;
-}
-
-hipError_t attn_dS_launch(int64_t BH, int64_t S, const uint16_t* P, const float* dP, const float* D, float scale,
-                          uint16_t* dS, hipStream_t s) {
-  const int64_t n = BH * S * S;
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_dS_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, BH, S, P, dP, D, scale, dS);
-  return hipGetLastError();
-}
-
 }  // namespace canon
