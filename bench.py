@@ -325,6 +325,17 @@ def main():
     del ws
     torch.cuda.empty_cache()
     kernels = {} if args.no_kernel_table else kernel_table(C, I, torch, np, stream, dev)
+    if not args.no_kernel_table:
+        # the canonical state hash of the post-step state (parameters, both moments): 1,279,854,592 x 10 bytes
+        state = pg + mg + vg
+        hws = torch.empty(C.state_hash_workspace_bytes(state), dtype=torch.uint8, device=dev)
+        hd = torch.empty(32, dtype=torch.uint8, device=dev)
+        hms = _timed(torch, stream, lambda: C.state_hash(state, hd, hws, stream=stream), 3)
+        hbytes = sum(t.numel() * t.element_size() for t in state)
+        kernels["state_hash_params_m_v"] = _hbm(hms, hbytes)
+        print(f"bench:   state_hash_params_m_v: {hms:.3f} ms, {kernels['state_hash_params_m_v']['achieved']} GB/s",
+              file=sys.stderr, flush=True)
+        del hws
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -206,6 +206,22 @@ canon_status canon_qlinear_bwd(const canon_order* order, int64_t T, int64_t N, i
                                float* dw, void* workspace, size_t workspace_bytes, void* stream);
 size_t canon_qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K);
 
+/* ------------------------------------------------------------------------------------------------ */
+/* Canonical state hash H1 (the paper's per-step state hash, moved onto the device as the paper proposes;
+   the paper leaves the function open, so H1 is this library's definition): SHA-256 (FIPS 180-4) over a
+   fixed tree.  A tensor of n bytes is cut into nb = ceil(n/64) blocks of 64 bytes and W = max(1,
+   ceil(nb/1024)) leaves, leaf l holding blocks l, l+W, l+2W, ... in order; leaf digest = SHA-256 of its
+   bytes; leaf digests fold pairwise level by level as SHA-256(left || right), an odd last node passing up
+   unchanged; tensor digest = SHA-256(0x02 || index (8 bytes LE) || n (8 bytes LE) || root); state digest =
+   SHA-256(0x03 || tensor digests in order).
+   ptrs, nbytes: HOST arrays of n_tensors device pointers and byte counts (any tensors: parameters, moments,
+   gradients, batches).  digest: device, 32 bytes.  workspace: device memory of
+   canon_state_hash_workspace_bytes(n_tensors, nbytes) bytes, 256-byte aligned.  The call stages a small
+   table from host memory into the workspace (copied before it returns) and enqueues three kernels. */
+canon_status canon_state_hash(int64_t n_tensors, const void* const* ptrs, const int64_t* nbytes, uint8_t* digest,
+                              void* workspace, size_t workspace_bytes, void* stream);
+size_t canon_state_hash_workspace_bytes(int64_t n_tensors, const int64_t* nbytes);
+
 /* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
    the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,
    10 bf16 round trip.  a, b, c, out: device fp32 [n] (b, c may be NULL when unused). */

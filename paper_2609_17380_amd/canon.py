@@ -74,6 +74,8 @@ def _lib():
             "canon_gemm_i8": (i32, [i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, vp, vp, vp]),
             "canon_qlinear_bwd": (i32, [vp, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
             "canon_qlinear_bwd_workspace_bytes": (sz, [i64, i64, i64]),
+            "canon_state_hash": (i32, [i64, vp, vp, vp, vp, sz, vp]),
+            "canon_state_hash_workspace_bytes": (sz, [i64, vp]),
             "canon_status_str": (ctypes.c_char_p, [i32]),
             "canon_version": (i32, []),
         }
@@ -206,6 +208,21 @@ def qlinear_bwd(T, N, K, dy, qx, sx, qw, sw, dx, dw, workspace, order=ORDER_V1, 
     _check(_lib().canon_qlinear_bwd(ctypes.byref(order), T, N, K, _ptr(dy), _ptr(qx), _ptr(sx), _ptr(qw), _ptr(sw),
                                     _ptr(dx), _ptr(dw), _ptr(workspace), workspace.numel() * workspace.element_size(),
                                     _stream(stream)), "canon_qlinear_bwd")
+
+
+def _nbytes(tensors):
+    return (ctypes.c_int64 * len(tensors))(*[t.numel() * t.element_size() for t in tensors])
+
+
+def state_hash_workspace_bytes(tensors) -> int:
+    return int(_lib().canon_state_hash_workspace_bytes(len(tensors), _nbytes(tensors)))
+
+
+def state_hash(tensors, digest, workspace, stream=None):
+    """Canonical state hash H1 of the tensors (declared order) into digest (device uint8 [32])."""
+    _check(_lib().canon_state_hash(len(tensors), _ptrs(tensors), _nbytes(tensors), _ptr(digest), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(), _stream(stream)),
+           "canon_state_hash")
 
 
 def devmath(op: str, n, a, b=None, c=None, out=None, stream=None):

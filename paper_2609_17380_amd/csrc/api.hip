@@ -511,6 +511,81 @@ size_t canon_qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K) {
   return qlinear_bwd_workspace_bytes(T, N, K);
 }
 
+namespace {
+struct HashPlan {
+  int64_t total_leaves = 0, n_wg = 0;
+  size_t off_tens = 0, off_wgt = 0, off_wgf = 0, off_la = 0, off_lb = 0, off_td = 0, bytes = 0;
+};
+
+HashPlan hash_plan(int64_t n, const int64_t* nbytes) {
+  HashPlan hp;
+  for (int64_t t = 0; t < n; ++t) {
+    const int64_t w = hash_leaf_count(nbytes[t]);
+    hp.total_leaves += w;
+    hp.n_wg += (w + 255) / 256;
+  }
+  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  size_t o = 0;
+  hp.off_tens = o; o += up(sizeof(HashTensor) * (size_t)n);
+  hp.off_wgt = o; o += up(sizeof(int32_t) * (size_t)hp.n_wg);
+  hp.off_wgf = o; o += up(sizeof(int64_t) * (size_t)hp.n_wg);
+  hp.off_la = o; o += up(32 * (size_t)hp.total_leaves);
+  hp.off_lb = o; o += up(32 * (size_t)hp.total_leaves);
+  hp.off_td = o; o += up(32 * (size_t)n);
+  hp.bytes = o;
+  return hp;
+}
+}  // namespace
+
+size_t canon_state_hash_workspace_bytes(int64_t n_tensors, const int64_t* nbytes) {
+  if (n_tensors < 0 || (n_tensors > 0 && !nbytes)) return 0;
+  for (int64_t t = 0; t < n_tensors; ++t)
+    if (nbytes[t] < 0) return 0;
+  return hash_plan(n_tensors, nbytes).bytes;
+}
+
+canon_status canon_state_hash(int64_t n_tensors, const void* const* ptrs, const int64_t* nbytes, uint8_t* digest,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  if (n_tensors < 0 || !digest || !workspace || (n_tensors > 0 && (!ptrs || !nbytes))) return CANON_EINVAL;
+  if (n_tensors > (int64_t(1) << 24)) return CANON_EUNSUPPORTED;
+  for (int64_t t = 0; t < n_tensors; ++t)
+    if (nbytes[t] < 0 || (nbytes[t] > 0 && !ptrs[t])) return CANON_EINVAL;
+  if ((uintptr_t)workspace & 255) return CANON_EINVAL;
+  const HashPlan hp = hash_plan(n_tensors, nbytes);
+  if (workspace_bytes < hp.bytes) return CANON_EWORKSPACE;
+  if (hp.n_wg > INT32_MAX) return CANON_EUNSUPPORTED;
+  // host tables: per tensor, and per workgroup (tensor, first leaf)
+  std::vector<char> host(hp.off_la);
+  HashTensor* tens = (HashTensor*)(host.data() + hp.off_tens);
+  int32_t* wgt = (int32_t*)(host.data() + hp.off_wgt);
+  int64_t* wgf = (int64_t*)(host.data() + hp.off_wgf);
+  int64_t leaf = 0, wg = 0;
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    const int64_t w = hash_leaf_count(nbytes[t]);
+    tens[t].ptr = ptrs[t];
+    tens[t].nbytes = nbytes[t];
+    tens[t].leaves = w;
+    tens[t].leaf_offset = leaf;
+    tens[t].aligned = (((uintptr_t)ptrs[t]) & 15) == 0;
+    for (int64_t f = 0; f < w; f += 256) {
+      wgt[wg] = (int32_t)t;
+      wgf[wg] = f;
+      ++wg;
+    }
+    leaf += w;
+  }
+  hipStream_t s = as_stream(stream);
+  char* ws = (char*)workspace;
+  if (hp.off_la > 0) {
+    hipError_t e = hipMemcpyAsync(ws, host.data(), hp.off_la, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return CANON_EDEVICE;
+  }
+  return dev(hash_launch(n_tensors, (const HashTensor*)(ws + hp.off_tens), hp.n_wg,
+                         (const int32_t*)(ws + hp.off_wgt), (const int64_t*)(ws + hp.off_wgf),
+                         (uint32_t*)(ws + hp.off_la), (uint32_t*)(ws + hp.off_lb), (uint32_t*)(ws + hp.off_td),
+                         digest, s));
+}
+
 canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m,
                          float* const* v, const float* const* grads, const uint8_t* decay_mask,
                          const canon_adamw_consts* consts, void* stream) {

@@ -46,6 +46,17 @@ struct GemmI8Args {
 };
 hipError_t gemm_i8_launch(const GemmI8Args& g, hipStream_t s);
 
+// hash.hip: canonical state hash
+struct HashTensor {
+  const void* ptr;
+  int64_t nbytes, leaves, leaf_offset;
+  int32_t aligned;  // 16-byte aligned base: vector loads
+};
+int64_t hash_leaf_count(int64_t nbytes);
+hipError_t hash_launch(int64_t n_tensors, const HashTensor* tens_dev, int64_t n_wg, const int32_t* wg_tensor,
+                       const int64_t* wg_first, uint32_t* leaf_a, uint32_t* leaf_b, uint32_t* tensor_digests,
+                       uint8_t* out, hipStream_t s);
+
 // qlinear.hip: int8 backward (rotated straight-through gradients)
 size_t qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K);
 hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const float* dy, const int8_t* qx, const float* sx,

@@ -63,3 +63,24 @@ def test_host_validation_rejects_before_any_launch():
     # GEMM with negative sizes, softmax with rows not a multiple of cols
     assert lib.canon_gemm(order, 0, 0, -1, 4, 4, x, 4, dy, 4, dx, 4, None) == C.EINVAL
     assert lib.canon_softmax_xent(order, C.SOFTMAX_CAUSAL, 10, 4, x, 1.0, None, 1.0, dx, None, None, None) == C.EINVAL
+
+
+def test_sha256_constants_in_the_device_source():
+    # the round constants and initial state are the first 32 fraction bits of the cube roots of the first 64
+    # primes and of the square roots of the first 8 (FIPS 180-4); integer roots keep this exact
+    import re
+    src = open(os.path.join(ROOT, "paper_2609_17380_amd", "csrc", "hash.hip")).read()
+    k = [int(x, 16) for x in re.findall(r"0x([0-9a-f]{8})u", src[src.index("kSha256K"):src.index("kSha256H0")])]
+    h0 = [int(x, 16) for x in re.findall(r"0x([0-9a-f]{8})u", src[src.index("kSha256H0"):src.index("rotr")])]
+    primes = [p for p in range(2, 400) if all(p % q for q in range(2, int(p ** 0.5) + 1))][:64]
+
+    def iroot(n, r):
+        x = int(round(n ** (1.0 / r)))
+        while x ** r > n:
+            x -= 1
+        while (x + 1) ** r <= n:
+            x += 1
+        return x
+
+    assert k == [iroot(p << 96, 3) & 0xFFFFFFFF for p in primes]
+    assert h0 == [iroot(p << 64, 2) & 0xFFFFFFFF for p in primes[:8]]
