@@ -45,6 +45,11 @@ class AdamWConsts(ctypes.Structure):
                                               "inv_bc1", "inv_bc2", "eps", "decay_factor")]
 
 
+class ClipCfg(ctypes.Structure):
+    """R15 clip settings: clip threshold, spike threshold, updates skipped per spike (0: no spike rule)."""
+    _fields_ = [("max_norm", ctypes.c_float), ("spike_norm", ctypes.c_float), ("skip_steps", ctypes.c_int32)]
+
+
 def _load():
     global _lib
     if _lib is None:
@@ -70,7 +75,10 @@ def _load():
             "cref_grad_accum": (ctypes.c_int, [vp, i64, vp, vp]),
             "cref_adamw": (ctypes.c_int, [i64, vp, vp, vp, vp, vp, vp, vp]),
             "cref_block_fwd_bwd": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
-            "cref_step": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "cref_step": (ctypes.c_int, [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "cref_global_norm": (f, [i64, vp, vp]),
+            "cref_clip_decide": (ctypes.c_int, [f, vp, vp, vp, vp]),
+            "cref_clip_apply": (ctypes.c_int, [i64, vp, vp, f]),
             "cref_quant_scales": (ctypes.c_int, [i64, i64, vp, vp]),
             "cref_quantize": (ctypes.c_int, [i64, i64, i32, vp, vp, i32, vp]),
             "cref_gemm_i8": (ctypes.c_int, [i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, f, vp]),
@@ -231,16 +239,50 @@ def block_fwd_bwd(cfg: ModelCfg, batch: int, x, dy, w, rope_cos, rope_sin):
 
 
 def step(cfg: ModelCfg, plan: Plan, params, m, v, windows, rope_cos, rope_sin, consts: AdamWConsts,
-         want_grads: bool = False):
-    """Runs one step; updates params, m, v in place; returns (loss, grads or None)."""
+         want_grads: bool = False, clip: ClipCfg | None = None, skip_state: int = 0):
+    """Runs one step; updates params, m, v in place; returns (loss, grads or None).
+
+    With ``clip`` (R15) it returns (loss, grads, info) where info holds the pre-clip ``norm``, the spike
+    counter ``skip_state`` after the step and ``skipped``."""
     loss = ctypes.c_float(0)
+    norm = ctypes.c_float(0)
+    state = ctypes.c_int32(skip_state)
+    skipped = ctypes.c_int32(0)
     grads = [np.empty(p.shape, dtype=np.float32) for p in params] if want_grads else None
     windows = np.ascontiguousarray(windows, dtype=np.int32)
     _check(_load().cref_step(ctypes.addressof(cfg), ctypes.addressof(plan), _ptr_array(params), _ptr_array(m),
                              _ptr_array(v), _p(windows), _p(np.ascontiguousarray(rope_cos, dtype=np.float32)),
                              _p(np.ascontiguousarray(rope_sin, dtype=np.float32)), ctypes.addressof(consts),
-                             ctypes.addressof(loss), _ptr_array(grads) if grads is not None else None))
-    return np.float32(loss.value), grads
+                             ctypes.addressof(clip) if clip is not None else None,
+                             ctypes.addressof(loss), _ptr_array(grads) if grads is not None else None,
+                             ctypes.addressof(norm), ctypes.addressof(state), ctypes.addressof(skipped)))
+    if clip is None:
+        return np.float32(loss.value), grads
+    return np.float32(loss.value), grads, {"norm": np.float32(norm.value), "skip_state": state.value,
+                                           "skipped": skipped.value}
+
+
+def global_norm(grads) -> np.float32:
+    """R15 pre-clip global norm of a list of fp32 tensors taken end to end in list order."""
+    grads = [np.ascontiguousarray(g, dtype=np.float32) for g in grads]
+    sizes = np.array([g.size for g in grads], dtype=np.int64)
+    return np.float32(_load().cref_global_norm(len(grads), _p(sizes), _ptr_array(grads)))
+
+
+def clip_decide(norm, clip: ClipCfg, skip_state: int = 0):
+    """R15 decision for one step: returns (coef, skip_state after the step, skipped)."""
+    coef = ctypes.c_float(0)
+    state = ctypes.c_int32(skip_state)
+    skipped = ctypes.c_int32(0)
+    _check(_load().cref_clip_decide(float(np.float32(norm)), ctypes.addressof(clip), ctypes.addressof(state),
+                                    ctypes.addressof(coef), ctypes.addressof(skipped)))
+    return np.float32(coef.value), state.value, skipped.value
+
+
+def clip_apply(grads, coef) -> None:
+    """R15: g <- RN(g * coef) in place (float32 arrays) when coef < 1."""
+    sizes = np.array([g.size for g in grads], dtype=np.int64)
+    _check(_load().cref_clip_apply(len(grads), _p(sizes), _ptr_array(grads), float(np.float32(coef))))
 
 
 def quant_scales(w: np.ndarray) -> np.ndarray:

@@ -597,6 +597,60 @@ int cref_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params,
 }
 
 /* ======================================================================== */
+/* R15: global gradient norm, clip and spike skip                             */
+/* ======================================================================== */
+
+/* The global l2 norm of the gradient (training-setup paragraph on the optimizer: clipping to a global
+   norm of 1.0).  The gradient tensors, laid end to end in the declared tensor order, form one vector;
+   its sum of squares is an R1 reduction over that vector's index (terms RN(g*g), chunks of 32 that may
+   run across a tensor boundary, chunk partials folded by Algorithm 2), and the norm is its correctly
+   rounded square root. */
+float cref_global_norm(int64_t n_tensors, const int64_t* sizes, const float* const* grads) {
+  sfold f = {0};
+  float s = 0.0f;
+  int in_chunk = 0;
+  for (int64_t t = 0; t < n_tensors; ++t)
+    for (int64_t i = 0; i < sizes[t]; ++i) {
+      const float g = grads[t][i];
+      s = cref_add(s, cref_mul(g, g));
+      if (++in_chunk == CHUNK) {
+        sfold_push(&f, s);
+        s = 0.0f;
+        in_chunk = 0;
+      }
+    }
+  if (in_chunk) sfold_push(&f, s);
+  return cref_sqrt(sfold_result(&f));
+}
+
+/* Clip coefficient and spike decision for one step (the optimizer paragraph's clip at 1.0; the section
+   on gradient behaviour: a pre-clip norm above 5 skips five optimizer steps).
+   coef = CRdiv(max_norm, RN(norm + RN32(1e-6))); the gradient is scaled by coef when coef < 1.
+   A spike is a norm that is not <= spike_norm (NaN included); it sets the counter of updates still to
+   skip to skip_steps, so that the spiking step and the skip_steps - 1 after it apply no update; a spike
+   inside that window starts it again.  skip_steps = 0 turns the spike rule off. */
+int cref_clip_decide(float norm, const cref_clip_cfg* k, int32_t* skip_state, float* coef, int32_t* skipped) {
+  if (!k || !(k->max_norm > 0.0f) || k->skip_steps < 0 || (k->skip_steps > 0 && !skip_state)) return -1;
+  *coef = cref_div(k->max_norm, cref_add(norm, 1e-6f));
+  int32_t left = skip_state ? *skip_state : 0;
+  if (k->skip_steps > 0 && !(norm <= k->spike_norm)) left = k->skip_steps;
+  const int32_t skip = left > 0;
+  if (skip) left -= 1;
+  if (skip_state) *skip_state = left;
+  *skipped = skip;
+  return 0;
+}
+
+/* g <- RN(g * coef) for every element when coef < 1; otherwise the gradient is left as it is. */
+int cref_clip_apply(int64_t n_tensors, const int64_t* sizes, float* const* grads, float coef) {
+  if (n_tensors < 0) return -1;
+  if (!(coef < 1.0f)) return 0;
+  for (int64_t t = 0; t < n_tensors; ++t)
+    for (int64_t i = 0; i < sizes[t]; ++i) grads[t][i] = cref_mul(grads[t][i], coef);
+  return 0;
+}
+
+/* ======================================================================== */
 /* Elementwise pieces of the decoder                                          */
 /* ======================================================================== */
 
@@ -964,8 +1018,11 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
 
 int cref_step(const cref_model_cfg* c, const cref_plan* plan, uint16_t* const* params, float* const* m,
               float* const* v, const int32_t* windows, const float* rope_cos, const float* rope_sin,
-              const cref_adamw_consts* k, float* loss_out, float* const* grads_out) {
+              const cref_adamw_consts* k, const cref_clip_cfg* clip, float* loss_out, float* const* grads_out,
+              float* norm_out, int32_t* skip_state, int32_t* skipped_out) {
   if (!cfg_valid(c) || !plan_valid(plan) || !k) return -1;
+  if (clip && (!(clip->max_norm > 0.0f) || clip->skip_steps < 0 || (clip->skip_steps > 0 && !skip_state)))
+    return -1;
   const int64_t nt = 3 + 6 * (int64_t)c->n_layers;
   int64_t* sz = (int64_t*)xmalloc(sizeof(int64_t) * nt);
   uint8_t* decay = (uint8_t*)xmalloc(nt);
@@ -1006,9 +1063,19 @@ int cref_step(const cref_model_cfg* c, const cref_plan* plan, uint16_t* const* p
   if (loss_out) *loss_out = loss;
   if (grads_out)
     for (int64_t i = 0; i < nt; ++i) memcpy(grads_out[i], grad + off[i], sizeof(float) * sz[i]);
-  const float** gp = (const float**)xmalloc(sizeof(float*) * nt);
+  float** gp = (float**)xmalloc(sizeof(float*) * nt);
   for (int64_t i = 0; i < nt; ++i) gp[i] = grad + off[i];
-  cref_adamw(nt, sz, params, m, v, gp, decay, k);
+  int32_t skipped = 0;
+  if (clip) {
+    /* R15: pre-clip norm of the reduced gradient, then the clip and the spike rule */
+    const float norm = cref_global_norm(nt, sz, (const float* const*)gp);
+    float coef;
+    cref_clip_decide(norm, clip, skip_state, &coef, &skipped);
+    cref_clip_apply(nt, sz, gp, coef);
+    if (norm_out) *norm_out = norm;
+  }
+  if (skipped_out) *skipped_out = skipped;
+  if (!skipped) cref_adamw(nt, sz, params, m, v, (const float* const*)gp, decay, k);
   free(gp); free(grad); free(tok); free(sz); free(decay); free(off);
   return 0;
 }

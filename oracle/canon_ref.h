@@ -30,6 +30,13 @@ typedef struct {
   float lr, beta1, one_minus_beta1, beta2, one_minus_beta2, inv_bc1, inv_bc2, eps, decay_factor;
 } cref_adamw_consts;
 
+/* R15 clip settings: max_norm > 0 (the clip threshold), spike_norm (a pre-clip norm not <= it is a
+   spike), skip_steps >= 0 (updates skipped per spike, the spiking step included; 0: no spike rule). */
+typedef struct {
+  float max_norm, spike_norm;
+  int32_t skip_steps;
+} cref_clip_cfg;
+
 /* ---- R0 primitives (scalar and vector forms, for the pins) ---- */
 float cref_add(float a, float b);
 float cref_sub(float a, float b);
@@ -75,6 +82,16 @@ int cref_grad_accum(const cref_plan* plan, int64_t n, const float* const* grads,
 int cref_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m, float* const* v,
                const float* const* grads, const uint8_t* decay_mask, const cref_adamw_consts* k);
 
+/* ---- R15 global gradient norm, clip, spike skip ----
+   global_norm: CRsqrt of the R1 sum of RN(g*g) over the tensors laid end to end in the given order.
+   clip_decide: coef = CRdiv(max_norm, RN(norm + RN32(1e-6))); a norm that is not <= spike_norm sets
+     *skip_state (updates still to skip) to skip_steps; *skipped = (*skip_state > 0), and a skipped step
+     takes one off the counter.  skip_state may be NULL when skip_steps = 0.
+   clip_apply: g <- RN(g * coef) in place when coef < 1. */
+float cref_global_norm(int64_t n_tensors, const int64_t* sizes, const float* const* grads);
+int cref_clip_decide(float norm, const cref_clip_cfg* k, int32_t* skip_state, float* coef, int32_t* skipped);
+int cref_clip_apply(int64_t n_tensors, const int64_t* sizes, float* const* grads, float coef);
+
 /* ---- one decoder block, forward + backward ----
    x, dy: fp32 [batch*seq, d]; w: the six block tensors in order attn_norm, w_qkv, w_o, ffn_norm,
    w_gate_up, w_down; y: block output; dx: input gradient; dw: six fp32 gradient buffers. */
@@ -86,10 +103,13 @@ int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x,
    params/m/v: n_tensors = 3 + 6*n_layers tensors in declared order (embed, per layer: attn_norm, w_qkv,
    w_o, ffn_norm, w_gate_up, w_down; final_norm, head).  windows: [M][seq+1] int32 with
    M = dp_shard*dp_replicate*accum*micro_seqs.  grads_out (optional, may be NULL): per-tensor fp32
-   buffers receiving the reduced gradient g. */
+   buffers receiving the reduced gradient g (before any clip).  clip (optional): R15 between the
+   plan and AdamW; norm_out gets the pre-clip norm, skip_state is the spike counter (in/out), and
+   skipped_out (optional) is set to 1 when the update was skipped. */
 int cref_step(const cref_model_cfg* cfg, const cref_plan* plan, uint16_t* const* params, float* const* m,
               float* const* v, const int32_t* windows, const float* rope_cos, const float* rope_sin,
-              const cref_adamw_consts* k, float* loss_out, float* const* grads_out);
+              const cref_adamw_consts* k, const cref_clip_cfg* clip, float* loss_out, float* const* grads_out,
+              float* norm_out, int32_t* skip_state, int32_t* skipped_out);
 
 /* ---- R13 int8 quantised linear, forward (the W8A8 training path) ----
    quant_scales: per-row LSQ step of a bf16 matrix [rows][cols] re-pinned from the weights:
