@@ -133,6 +133,40 @@ canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* cons
                          const canon_adamw_consts* consts, void* stream);
 
 /* ------------------------------------------------------------------------------------------------ */
+/* Global-norm clip and spike skip (R15; the optimizer paragraph of the training setup clips gradients to a
+   global l2 norm of 1.0, and the section on gradient behaviour skips five optimizer steps when the
+   pre-clip norm exceeds 5).
+   The gradient tensors laid end to end in the given order form one vector g; its pre-clip norm is
+   CRsqrt(Q), Q the R1 sum over g's flat index of RN(g_i * g_i) (chunks of 32 run across tensor
+   boundaries).  coef = CRdiv(max_norm, RN(norm + RN32(1e-6))); when coef < 1 every element becomes
+   RN(g_i * coef), otherwise g is left untouched.  A norm that is not <= spike_norm (NaN included) is a
+   spike: it sets *skip_state to skip_steps.  The step applies no update when *skip_state > 0 after that,
+   and such a step takes one off *skip_state; so one spike skips the spiking step and the skip_steps - 1
+   after it, and a spike inside that window starts it again.
+   Settings and outputs (all pointers device memory, written in stream order):
+     max_norm > 0 (+inf: no clip); spike_norm; skip_steps >= 0 (0: no spike rule, skip_state unused);
+     norm_out: fp32 scalar, the pre-clip norm, or NULL; skip_state: int32 counter, read and written,
+     required when skip_steps > 0 (start it at 0); skipped_out: int32, 1 when this step applies no update,
+     or NULL.  Invalid settings: CANON_EINVAL. */
+typedef struct {
+  float max_norm;
+  float spike_norm;
+  int32_t skip_steps;
+  float* norm_out;
+  int32_t* skip_state;
+  int32_t* skipped_out;
+} canon_clip;
+
+/* Norm, spike decision and clip of n_tensors fp32 device buffers (grads[t] of sizes[t] elements, sizes[t]
+   >= 0; the clip writes them in place).  The caller skips its optimizer update when *skipped_out is 1.
+   workspace: device memory of canon_clip_grad_norm_workspace_bytes(n_tensors, sizes) bytes, 256-byte
+   aligned; it holds the tensor table and the block sums.  Up to 2^40 elements in total. */
+canon_status canon_clip_grad_norm(const canon_order* order, int64_t n_tensors, const int64_t* sizes,
+                                  float* const* grads, const canon_clip* clip, void* workspace,
+                                  size_t workspace_bytes, void* stream);
+size_t canon_clip_grad_norm_workspace_bytes(int64_t n_tensors, const int64_t* sizes);
+
+/* ------------------------------------------------------------------------------------------------ */
 /* One decoder block, forward then backward, for `batch` sequences of cfg->seq tokens (T = batch*seq).
    x, dy: fp32 [T, d_model] (block input, gradient of the block output).  w: HOST array of the six bf16
    block tensors in the order attn_norm [d], w_qkv [3d, d], w_o [d, d], ffn_norm [d], w_gate_up [2F, d]
@@ -154,13 +188,17 @@ size_t canon_block_workspace_bytes(const canon_model_cfg* cfg, int32_t batch);
    (bf16), m and v (fp32) are updated in place.  windows: device int32 [M, seq+1], M = N*accum*
    micro_seqs, each token in [0, vocab) (checked on the device: an out-of-range token makes the loss
    NaN and leaves the parameters unchanged).  loss_out: device fp32 scalar.  grads_out: NULL, or a HOST
-   array of n device fp32 buffers that receive the reduced gradient.  step_t is informational (the
-   bias corrections come in consts). */
+   array of n device fp32 buffers that receive the reduced gradient (before any clip).  clip: NULL, or the
+   R15 settings (canon_clip above) applied to the reduced gradient of all n tensors in the declared order
+   between the plan and AdamW; a skipped step leaves params, m and v unchanged.  An out-of-range token
+   also makes *norm_out NaN and sets *skipped_out, and leaves *skip_state unchanged.  step_t is
+   informational (the bias corrections come in consts; a caller that skips an update does not advance
+   them). */
 canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, const canon_dp_plan* plan,
                         uint16_t* const* params, float* const* m, float* const* v, int32_t step_t,
                         const int32_t* windows, const float* rope_cos, const float* rope_sin,
-                        const canon_adamw_consts* consts, void* workspace, size_t workspace_bytes,
-                        float* loss_out, float* const* grads_out, void* stream);
+                        const canon_adamw_consts* consts, const canon_clip* clip, void* workspace,
+                        size_t workspace_bytes, float* loss_out, float* const* grads_out, void* stream);
 size_t canon_step_workspace_bytes(const canon_model_cfg* cfg, const canon_dp_plan* plan);
 
 /* ------------------------------------------------------------------------------------------------ */

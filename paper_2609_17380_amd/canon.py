@@ -45,6 +45,16 @@ class AdamWConsts(ctypes.Structure):
                                               "inv_bc1", "inv_bc2", "eps", "decay_factor")]
 
 
+class Clip(ctypes.Structure):
+    """R15 settings and device outputs (pointers are device addresses, 0 for none)."""
+    _fields_ = [("max_norm", ctypes.c_float), ("spike_norm", ctypes.c_float), ("skip_steps", ctypes.c_int32),
+                ("norm_out", ctypes.c_void_p), ("skip_state", ctypes.c_void_p), ("skipped_out", ctypes.c_void_p)]
+
+
+def make_clip(max_norm, spike_norm, skip_steps, norm_out=None, skip_state=None, skipped_out=None) -> Clip:
+    return Clip(max_norm, spike_norm, skip_steps, _ptr(norm_out), _ptr(skip_state), _ptr(skipped_out))
+
+
 ORDER_V1 = Order(1, 32, 0, 1)
 _L = None
 
@@ -66,7 +76,9 @@ def _lib():
             "canon_adamw": (i32, [i64, vp, vp, vp, vp, vp, vp, vp, vp]),
             "canon_block_fwd_bwd": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
             "canon_block_workspace_bytes": (sz, [vp, i32]),
-            "canon_step": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, sz, vp, vp, vp]),
+            "canon_step": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp]),
+            "canon_clip_grad_norm": (i32, [vp, i64, vp, vp, vp, vp, sz, vp]),
+            "canon_clip_grad_norm_workspace_bytes": (sz, [i64, vp]),
             "canon_step_workspace_bytes": (sz, [vp, vp]),
             "canon_devmath": (i32, [i32, i64, vp, vp, vp, vp, vp]),
             "canon_quant_scales": (i32, [vp, i64, i64, vp, vp, vp]),
@@ -170,11 +182,28 @@ def step_workspace_bytes(cfg: ModelCfg, plan: DPPlan) -> int:
 
 
 def step(cfg: ModelCfg, plan: DPPlan, params, m, v, windows, rope_cos, rope_sin, consts: AdamWConsts, workspace,
-         loss_out, grads_out=None, step_t=1, order=ORDER_V1, stream=None):
+         loss_out, grads_out=None, step_t=1, order=ORDER_V1, stream=None, clip: Clip | None = None):
     _check(_lib().canon_step(ctypes.byref(order), ctypes.byref(cfg), ctypes.byref(plan), _ptrs(params), _ptrs(m),
                              _ptrs(v), step_t, _ptr(windows), _ptr(rope_cos), _ptr(rope_sin), ctypes.byref(consts),
+                             ctypes.byref(clip) if clip is not None else None,
                              _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(loss_out),
                              _ptrs(grads_out) if grads_out is not None else None, _stream(stream)), "canon_step")
+
+
+def _sizes(tensors):
+    return (ctypes.c_int64 * len(tensors))(*[t.numel() for t in tensors])
+
+
+def clip_grad_norm_workspace_bytes(grads) -> int:
+    return int(_lib().canon_clip_grad_norm_workspace_bytes(len(grads), _sizes(grads)))
+
+
+def clip_grad_norm(grads, clip: Clip, workspace, order=ORDER_V1, stream=None):
+    """R15 norm, spike decision and in-place clip of fp32 device tensors taken end to end in list order."""
+    _check(_lib().canon_clip_grad_norm(ctypes.byref(order), len(grads), _sizes(grads), _ptrs(grads),
+                                       ctypes.byref(clip), _ptr(workspace),
+                                       workspace.numel() * workspace.element_size(), _stream(stream)),
+           "canon_clip_grad_norm")
 
 
 DEVMATH_OPS = {"add": 0, "sub": 1, "mul": 2, "fma": 3, "div": 4, "sqrt": 5, "exp": 6, "log": 7, "sigmoid": 8,

@@ -262,6 +262,9 @@ struct StepLayout {
   float* loss_mb;         // [1]
   float* loss_gr;         // [1]
   std::vector<float*> loss_pool;
+  float* norm_part;       // R15 block sums
+  float* clip_coef;       // [1]
+  int32_t* skip;          // [1]: no update this step (bad token or spike window)
 };
 
 void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, int64_t P, StepLayout& L) {
@@ -292,6 +295,9 @@ void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, in
   L.loss_gr = cv.take<float>(1);
   L.loss_pool.resize(nbuf);
   for (auto& b : L.loss_pool) b = cv.take<float>(1);
+  L.norm_part = cv.take<float>(gnorm_blocks(P));
+  L.clip_coef = cv.take<float>(1);
+  L.skip = cv.take<int32_t>(1);
 }
 
 // Algorithm 1 driven from the host over device buffers of n floats (the gradient, or the loss with n = 1).
@@ -599,9 +605,75 @@ canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* cons
                        consts->inv_bc1, consts->inv_bc2, consts->eps, consts->decay_factor};
   for (int64_t t = 0; t < n_tensors; ++t) {
     hipError_t e = adamw_launch(sizes[t], params[t], m[t], v[t], grads[t], decay_mask[t] != 0, c9, nullptr,
-                                as_stream(stream));
+                                nullptr, as_stream(stream));
     if (e != hipSuccess) return CANON_EDEVICE;
   }
+  return CANON_OK;
+}
+
+size_t canon_clip_grad_norm_workspace_bytes(int64_t n_tensors, const int64_t* sizes) {
+  if (n_tensors < 0 || (n_tensors > 0 && !sizes)) return 0;
+  int64_t n = 0;
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    if (sizes[t] < 0) return 0;
+    n += sizes[t];
+  }
+  Carver cv(nullptr);
+  cv.take<const float*>(n_tensors);
+  cv.take<int64_t>(n_tensors + 1);
+  cv.take<float>(gnorm_blocks(n));
+  cv.take<float>(1);
+  return cv.off + 256;
+}
+
+canon_status canon_clip_grad_norm(const canon_order* order, int64_t n_tensors, const int64_t* sizes,
+                                  float* const* grads, const canon_clip* clip, void* workspace,
+                                  size_t workspace_bytes, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (n_tensors < 0 || !clip || (n_tensors > 0 && (!sizes || !grads))) return CANON_EINVAL;
+  if (!(clip->max_norm > 0.0f) || clip->skip_steps < 0 || (clip->skip_steps > 0 && !clip->skip_state))
+    return CANON_EINVAL;
+  if (n_tensors > INT32_MAX - 1) return CANON_EUNSUPPORTED;
+  int64_t n = 0;
+  bool vec4 = true;
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    if (sizes[t] < 0 || (sizes[t] > 0 && !grads[t])) return CANON_EINVAL;
+    n += sizes[t];
+    if (sizes[t] % 4 != 0 || ((uintptr_t)grads[t] & 15)) vec4 = false;
+  }
+  if (n > (int64_t(1) << 40)) return CANON_EUNSUPPORTED;
+  const size_t need = canon_clip_grad_norm_workspace_bytes(n_tensors, sizes);
+  if (!workspace || workspace_bytes < need) return CANON_EWORKSPACE;
+  hipStream_t s = as_stream(stream);
+  Carver cv(workspace);
+  const float** ptr_d = cv.take<const float*>(n_tensors);
+  int64_t* start_d = cv.take<int64_t>(n_tensors + 1);
+  float* part = cv.take<float>(gnorm_blocks(n));
+  float* coef = cv.take<float>(1);
+  NormSrc src{};
+  src.nt = (int32_t)n_tensors;
+  if (n_tensors == 1) {
+    src.one = grads[0];
+  } else if (n_tensors > 1) {
+    std::vector<const float*> hp(grads, grads + n_tensors);
+    std::vector<int64_t> hs(n_tensors + 1, 0);
+    for (int64_t t = 0; t < n_tensors; ++t) hs[t + 1] = hs[t] + sizes[t];
+    TRY(hipMemcpyAsync(ptr_d, hp.data(), sizeof(float*) * n_tensors, hipMemcpyHostToDevice, s));
+    TRY(hipMemcpyAsync(start_d, hs.data(), sizeof(int64_t) * (n_tensors + 1), hipMemcpyHostToDevice, s));
+    src.ptr = ptr_d;
+    src.start = start_d;
+  }
+  ClipDecision d{};
+  d.max_norm = clip->max_norm;
+  d.spike_norm = clip->spike_norm;
+  d.skip_steps = clip->skip_steps;
+  d.norm_out = clip->norm_out;
+  d.coef_out = coef;
+  d.skip_state = clip->skip_state;
+  d.skipped_out = clip->skipped_out;
+  TRY(gnorm_launch(src, n, vec4 ? 1 : 0, part, d, s));
+  for (int64_t t = 0; t < n_tensors; ++t) TRY(clip_scale_launch(sizes[t], grads[t], coef, s));
   return CANON_OK;
 }
 
@@ -666,13 +738,15 @@ size_t canon_step_workspace_bytes(const canon_model_cfg* cfg, const canon_dp_pla
 canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, const canon_dp_plan* plan,
                         uint16_t* const* params, float* const* m, float* const* v, int32_t step_t,
                         const int32_t* windows, const float* rope_cos, const float* rope_sin,
-                        const canon_adamw_consts* consts, void* workspace, size_t workspace_bytes, float* loss_out,
-                        float* const* grads_out, void* stream) {
+                        const canon_adamw_consts* consts, const canon_clip* clip, void* workspace,
+                        size_t workspace_bytes, float* loss_out, float* const* grads_out, void* stream) {
   (void)step_t;
   canon_status st = check_order(order);
   if (st != CANON_OK) return st;
   if (!cfg_ok(cfg) || !plan || plan->accum < 1 || plan->dp_shard < 1 || plan->dp_replicate < 1) return CANON_EINVAL;
   if (!params || !m || !v || !windows || !rope_cos || !rope_sin || !consts || !loss_out) return CANON_EINVAL;
+  if (clip && (!(clip->max_norm > 0.0f) || clip->skip_steps < 0 || (clip->skip_steps > 0 && !clip->skip_state)))
+    return CANON_EINVAL;
   std::vector<int64_t> sz;
   std::vector<uint8_t> decay;
   tensor_sizes(cfg, sz, decay);
@@ -754,8 +828,30 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
       TRY(hipMemcpyAsync(grads_out[t], g + off[t], sizeof(float) * sz[t], hipMemcpyDeviceToDevice, s));
   const float c9[9] = {consts->lr, consts->beta1, consts->one_minus_beta1, consts->beta2, consts->one_minus_beta2,
                        consts->inv_bc1, consts->inv_bc2, consts->eps, consts->decay_factor};
+  const float* gscale = nullptr;
+  const int32_t* skip = L.bad;
+  if (clip) {
+    // R15 on the reduced gradient (one flat buffer in declared order): pre-clip norm, clip coefficient and
+    // spike counter; the clip itself is applied inside AdamW
+    NormSrc src{};
+    src.one = g;
+    src.nt = 1;
+    ClipDecision d{};
+    d.max_norm = clip->max_norm;
+    d.spike_norm = clip->spike_norm;
+    d.skip_steps = clip->skip_steps;
+    d.bad = L.bad;
+    d.norm_out = clip->norm_out;
+    d.coef_out = L.clip_coef;
+    d.skip_state = clip->skip_state;
+    d.skip_flag = L.skip;
+    d.skipped_out = clip->skipped_out;
+    TRY(gnorm_launch(src, P, (P % 4 == 0 && ((uintptr_t)g & 15) == 0) ? 1 : 0, L.norm_part, d, s));
+    gscale = L.clip_coef;
+    skip = L.skip;
+  }
   for (int64_t t = 0; t < nt; ++t)
-    TRY(adamw_launch(sz[t], params[t], m[t], v[t], g + off[t], decay[t], c9, L.bad, s));
+    TRY(adamw_launch(sz[t], params[t], m[t], v[t], g + off[t], decay[t], c9, gscale, skip, s));
   return CANON_OK;
 }
 

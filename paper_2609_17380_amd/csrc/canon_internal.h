@@ -63,6 +63,28 @@ hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const float* dy, 
                               const int8_t* qw, const float* sw, float* dx, float* dw, void* ws, hipStream_t s);
 int gemm_max_levels();
 
+// norm.hip: global gradient norm, clip coefficient, spike decision (R15)
+struct NormSrc {
+  const float* one;          // the whole vector in one buffer, or null
+  const float* const* ptr;   // device [nt]: tensor bases (when one is null)
+  const int64_t* start;      // device [nt + 1]: flat index of each tensor's first element; start[nt] = n
+  int32_t nt;
+};
+struct ClipDecision {
+  float max_norm, spike_norm;
+  int32_t skip_steps;
+  const int32_t* bad;    // may be null: a set flag marks the gradient invalid
+  float* norm_out;       // may be null
+  float* coef_out;       // device scalar, required
+  int32_t* skip_state;   // may be null when skip_steps = 0
+  int32_t* skip_flag;    // may be null: 1 when no update is to be applied
+  int32_t* skipped_out;  // may be null
+};
+int64_t gnorm_blocks(int64_t n);  // block partials the launch needs
+hipError_t gnorm_launch(const NormSrc& src, int64_t n, int vec4, float* part, const ClipDecision& d, hipStream_t s);
+// g <- RN(g * *coef) when *coef < 1
+hipError_t clip_scale_launch(int64_t n, float* g, const float* coef, hipStream_t s);
+
 // rows.hip
 hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps,
                               uint16_t* y, float* rstd, hipStream_t s);
@@ -113,8 +135,9 @@ hipError_t plan_shard_launch(int64_t n, const float* a, int first, float* out, h
 hipError_t plan_merge_launch(int64_t n, const float* lower, float* out, hipStream_t s);
 // out = RN(x * inv) (in place allowed)
 hipError_t plan_scale_launch(int64_t n, const float* x, float inv, float* out, hipStream_t s);
+// gscale (may be null): the gradient is taken as RN(g * *gscale) when *gscale < 1 (the R15 clip)
 hipError_t adamw_launch(int64_t n, uint16_t* p, float* m, float* v, const float* g, int decay, const float* consts9,
-                        const int32_t* skip_flag, hipStream_t s);
+                        const float* gscale, const int32_t* skip_flag, hipStream_t s);
 hipError_t set_nan_if_launch(const int32_t* flag, float* x, hipStream_t s);
 
 }  // namespace canon

@@ -234,12 +234,16 @@ struct AdamWK {
 
 __global__ __launch_bounds__(256) void adamw_kernel(int64_t n, uint16_t* __restrict__ p16, float* __restrict__ m,
                                                     float* __restrict__ v, const float* __restrict__ g, int decay,
-                                                    AdamWK k, const int32_t* __restrict__ skip) {
+                                                    AdamWK k, const float* __restrict__ gscale,
+                                                    const int32_t* __restrict__ skip) {
   if (skip && *skip) return;
+  const float c = gscale ? *gscale : 1.0f;
+  const bool clip = c < 1.0f;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
     float p = bf16_to_f32(p16[i]);
     if (decay) p = p * k.decay_factor;
-    const float gi = g[i];
+    float gi = g[i];
+    if (clip) gi = gi * c;
     float m1 = k.beta1 * m[i];
     float m2 = k.omb1 * gi;
     float mi = m1 + m2;
@@ -260,10 +264,10 @@ __global__ __launch_bounds__(256) void adamw_kernel(int64_t n, uint16_t* __restr
 }
 
 hipError_t adamw_launch(int64_t n, uint16_t* p, float* m, float* v, const float* g, int decay, const float* c9,
-                        const int32_t* skip_flag, hipStream_t s) {
+                        const float* gscale, const int32_t* skip_flag, hipStream_t s) {
   if (n == 0) return hipSuccess;
   AdamWK k{c9[0], c9[1], c9[2], c9[3], c9[4], c9[5], c9[6], c9[7], c9[8]};
-  hipLaunchKernelGGL(adamw_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, p, m, v, g, decay, k, skip_flag);
+  hipLaunchKernelGGL(adamw_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, p, m, v, g, decay, k, gscale, skip_flag);
   return hipGetLastError();
 }
 

@@ -12,75 +12,6 @@
 
 namespace canon {
 
-// Binary-carry fold of a lane's consecutive chunk partials (Algorithm 2 on one lane): up to 2^LEVELS - 1
-// pushes.
-template <int LEVELS>
-struct LocalFoldN {
-  float s[LEVELS];
-  int64_t count = 0;
-  __device__ void push(float p) {
-#pragma unroll
-    for (int L = 0; L < LEVELS; ++L) {
-      if ((count >> L) & 1) {
-        p = s[L] + p;
-      } else {
-        s[L] = p;
-        break;
-      }
-    }
-    ++count;
-  }
-  __device__ float result() const {
-    float r = 0.0f;
-    bool have = false;
-#pragma unroll
-    for (int L = 0; L < LEVELS; ++L) {
-      if ((count >> L) & 1) {
-        if (!have) {
-          r = s[L];
-          have = true;
-        } else {
-          r = s[L] + r;
-        }
-      }
-    }
-    return r;
-  }
-};
-using LocalFold = LocalFoldN<16>;  // a lane block of up to 2^16 - 1 chunks
-
-// chunks per lane so that `lanes` lanes cover nc chunks with aligned power-of-two blocks
-__device__ __forceinline__ int64_t block_chunks(int64_t nc, int lanes) {
-  int64_t G = 1;
-  while (G * lanes < nc) G <<= 1;
-  return G;
-}
-
-// Fold of per-thread partials across a 256-thread workgroup; thread t holds part t (valid for t < nparts).
-// Returns the total to every thread.
-__device__ float block_fold(float p, int64_t nparts) {
-  __shared__ float wsum[4];
-  __shared__ float total;
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  int64_t nl = nparts - 64 * w;
-  nl = nl < 0 ? 0 : (nl > 64 ? 64 : nl);
-  float r = wave_fold(p, (int)nl);
-  if (lane == 0) wsum[w] = r;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float a = wsum[0];
-    if (64 < nparts) a = a + wsum[1];
-    float b = wsum[2];
-    if (192 < nparts) b = b + wsum[3];
-    if (128 < nparts) a = a + b;
-    total = a;
-  }
-  __syncthreads();
-  float t = total;
-  __syncthreads();
-  return t;
-}
-
 __device__ __forceinline__ float wave_max(float m) {
 #pragma unroll
   for (int s = 32; s >= 1; s >>= 1) m = fmaxf(m, __shfl_xor(m, s, 64));
