@@ -90,7 +90,8 @@ def _hbm(ms, nbytes):
 def kernel_table(C, I, torch, np, stream, dev):
     """Each entry point at the shapes of the single-kernel workloads: the GEMM sweep over the 1B shapes, RMSNorm
     over a microbatch, causal softmax at 16 heads x 2048 x 2048, cross-entropy 8192 x 50304, the ordered sum of 8
-    gradient buffers of 1.2e9 fp32, AdamW over 1.2e9 parameters, and one decoder block forward + backward.
+    gradient buffers of 1.2e9 fp32, AdamW over 1.2e9 parameters, the global gradient norm (and clip) over the
+    1B gradient, and one decoder block forward + backward.
     Inputs are seeded N(0, sigma) draws made on the device (the values do not change the work); bytes are the
     algorithmic minimum each kernel must move."""
     g = torch.Generator(device=dev)
@@ -201,7 +202,20 @@ def kernel_table(C, I, torch, np, stream, dev):
     consts = C.AdamWConsts(*I.adamw_constants())
     ms = _timed(torch, stream, lambda: C.adamw([p], [m1], [v1], [gsum], [1], consts, stream=stream), 3)
     out["adamw_1.2e9"] = _hbm(ms, n * 24)
-    del p, m1, v1, gsum
+    del p, m1, v1
+    # R15 over the whole 1B gradient in one flat buffer (the step's launch): the norm alone (clip not
+    # engaged: 4 bytes read per element), then norm + in-place clip (engaged: 12 bytes per element)
+    P = sum(int(np.prod(sh)) for _, sh, _, _ in I.model_param_shapes(L, D, F, V))
+    gflat = randn((P,), std=1e-3)
+    nrm = torch.empty(1, dtype=torch.float32, device=dev)
+    cws = torch.empty(C.clip_grad_norm_workspace_bytes([gflat]), dtype=torch.uint8, device=dev)
+    off = C.make_clip(float(np.float32(1e30)), float("inf"), 0, nrm)
+    ms = _timed(torch, stream, lambda: C.clip_grad_norm([gflat], off, cws, stream=stream), 5)
+    out[f"global_norm_{P}"] = _hbm(ms, 4 * P)
+    on = C.make_clip(1e-30, float("inf"), 0, nrm)  # coef < 1 every call: the clip pass runs each time
+    ms = _timed(torch, stream, lambda: C.clip_grad_norm([gflat], on, cws, stream=stream), 3)
+    out[f"global_norm_and_clip_{P}"] = _hbm(ms, 12 * P)
+    del gflat, gsum, cws
     torch.cuda.empty_cache()
 
     cfg = C.ModelCfg(1, D, H, HD, F, V, S, 1, np.float32(1e-5))
@@ -266,17 +280,22 @@ def main():
     consts = C.AdamWConsts(*I.adamw_constants())
     ws = torch.empty(C.step_workspace_bytes(cfg, plan), dtype=torch.uint8, device=dev)
     loss = torch.zeros(1, dtype=torch.float32, device=dev)
+    # the paper's clip to a global norm of 1.0 (R15) runs in every step; the spike rule is off here, since a
+    # skipped update would leave work out of the timed step
+    gnorm = torch.zeros(1, dtype=torch.float32, device=dev)
+    clip = C.make_clip(1.0, float("inf"), 0, gnorm)
     torch.cuda.synchronize()
     print(f"bench: inputs ready in {time.time() - t0:.1f}s; workspace {ws.numel() / 1e9:.1f} GB",
           file=sys.stderr, flush=True)
 
     def one_step():
-        C.step(cfg, plan, pg, mg, vg, windows, cos, sin, consts, ws, loss, stream=stream)
+        C.step(cfg, plan, pg, mg, vg, windows, cos, sin, consts, ws, loss, stream=stream, clip=clip)
 
     for i in range(args.warmup):
         one_step()
         torch.cuda.synchronize()
-        print(f"bench: warmup step {i} loss {loss.item():.5f}", file=sys.stderr, flush=True)
+        print(f"bench: warmup step {i} loss {loss.item():.5f} pre-clip grad norm {gnorm.item():.5f}",
+              file=sys.stderr, flush=True)
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     ev0.record(stream)
@@ -363,12 +382,14 @@ def main():
         "config": {"workload": "1B-shaped canonical step replay (16 layers, d 2048, 16x128 heads, FFN 8192, "
                                "vocab 50304, seq 2048; 8 ranks x 4 sequences by Algorithm 1; AdamW)",
                    "global_batch": R * PLAN[0] * MB, "seq_len": S, "parallelism": "dp8 emulated on 1 GPU",
-                   "plan": {"accum": PLAN[0], "dp_shard": PLAN[1], "dp_replicate": PLAN[2]}},
+                   "plan": {"accum": PLAN[0], "dp_shard": PLAN[1], "dp_replicate": PLAN[2]},
+                   "clip": {"max_norm": 1.0, "spike_rule": "off (a skipped update would drop work)"}},
         "step_replay_seconds": round(ms / 1000, 3), "step_flops": flops, "tokens_per_s": round(
             R * PLAN[0] * MB * S / (ms * 1e-3), 1),
         "gemm_tflops": round(gemm_tf, 2), "gemm_pct_bf16_peak": round(100 * gemm_tf / PEAK_BF16_MFMA, 3),
         "gemm_unconstrained_library_tflops": round(blas_tf, 2),
-        "roofline": roofline, "cpu_baseline": cpu, "loss": float(loss.item()), "kernels": kernels,
+        "roofline": roofline, "cpu_baseline": cpu, "loss": float(loss.item()),
+        "grad_norm_preclip": float(gnorm.item()), "kernels": kernels,
     }
     print(json.dumps(out), flush=True)
 

@@ -18,7 +18,10 @@ namespace canon {
 
 namespace {
 
-constexpr int kNormBlockChunks = 1024;               // 4 wavefronts x 4 segments x 64 chunks
+constexpr int kWaveSegs = 4;                         // segments of 64 chunks per wavefront
+constexpr int kWaveChunks = 64 * kWaveSegs;          // 256 chunks per wavefront
+constexpr int kNormBlockChunks = 4 * kWaveChunks;    // 4 wavefronts: 1024 chunks (32768 terms) per workgroup
+constexpr int kFinalWaves = 16;                      // wavefronts of the block-sum fold
 constexpr int kSegTerms = 64 * kChunk;               // 2048 terms per segment
 constexpr float kClipEps = 1e-6f;                    // RN32(1e-6), added to the norm before the division
 
@@ -70,22 +73,25 @@ __global__ __launch_bounds__(256) void gnorm_block_kernel(int64_t n, NormSrc src
   __shared__ float wsum[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t nc = (n + kChunk - 1) / kChunk;
-  const int64_t cw = (int64_t)blockIdx.x * kNormBlockChunks + (int64_t)w * 256;  // wave's first chunk
+  const int64_t cw = (int64_t)blockIdx.x * kNormBlockChunks + (int64_t)w * kWaveChunks;  // wave's first chunk
   int cur = 0;
   if (MULTI) cur = find_tensor(src, cw * kChunk + W * lane < n ? cw * kChunk + W * lane : n - 1);
-  float seg[4];
+  // the wave's segments are consecutive complete subtrees of 64 chunks: a binary-carry fold over the real
+  // ones gives the wave's subtree with the pass-through rule
+  LocalFoldN<8> wf;
   float nxt[Q][W];
 #pragma unroll
   for (int q = 0; q < Q; ++q) load_terms<W, MULTI>(src, n, cw * kChunk + 64 * W * q + W * lane, cur, nxt[q]);
 #pragma unroll
-  for (int sg = 0; sg < 4; ++sg) {
+  for (int sg = 0; sg < kWaveSegs; ++sg) {
     const int64_t c0 = cw + 64 * sg;
+    if (c0 >= nc) break;
     float f[Q][W];
 #pragma unroll
     for (int q = 0; q < Q; ++q)
 #pragma unroll
       for (int i = 0; i < W; ++i) f[q][i] = nxt[q][i];
-    if (sg < 3) {
+    if (sg + 1 < kWaveSegs) {
 #pragma unroll
       for (int q = 0; q < Q; ++q)
         load_terms<W, MULTI>(src, n, (c0 + 64) * kChunk + 64 * W * q + W * lane, cur, nxt[q]);
@@ -106,30 +112,22 @@ __global__ __launch_bounds__(256) void gnorm_block_kernel(int64_t n, NormSrc src
       for (int i = 0; i < k1; ++i) p = p + st[w].t[lane][i];
     }
     const int64_t real = nc - c0;
-    seg[sg] = wave_fold(p, real < 0 ? 0 : (real > 64 ? 64 : (int)real));
+    const float seg = wave_fold(p, real > 64 ? 64 : (int)real);
+    if (lane == 0) wf.push(seg);
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_wave_barrier();
   }
-  // segments 0..3 of the wave, then waves 0..3 of the workgroup: pairs of complete subtrees, with the
-  // right one passed over when it holds no real chunk
-  if (lane == 0) {
-    float a = seg[0];
-    if (cw + 64 < nc) a = a + seg[1];
-    if (cw + 128 < nc) {
-      float b = seg[2];
-      if (cw + 192 < nc) b = b + seg[3];
-      a = a + b;
-    }
-    wsum[w] = a;
-  }
+  if (lane == 0) wsum[w] = wf.result();
   __syncthreads();
+  // the workgroup's four waves: pairs of complete subtrees, the right one passed over when it holds no real
+  // chunk
   if (threadIdx.x == 0) {
     const int64_t cb = (int64_t)blockIdx.x * kNormBlockChunks;
     float a = wsum[0];
-    if (cb + 256 < nc) a = a + wsum[1];
-    if (cb + 512 < nc) {
+    if (cb + kWaveChunks < nc) a = a + wsum[1];
+    if (cb + 2 * kWaveChunks < nc) {
       float b = wsum[2];
-      if (cb + 768 < nc) b = b + wsum[3];
+      if (cb + 3 * kWaveChunks < nc) b = b + wsum[3];
       a = a + b;
     }
     part[blockIdx.x] = a;
@@ -139,17 +137,48 @@ __global__ __launch_bounds__(256) void gnorm_block_kernel(int64_t n, NormSrc src
 // Fold of the block sums, square root, clip coefficient, spike counter.  bad (may be null): a set flag
 // means the gradient is not valid (an out-of-range token): the norm is NaN, no update is applied and the
 // spike counter is left alone.
-__global__ __launch_bounds__(256) void gnorm_final_kernel(int64_t nb, const float* __restrict__ part, float max_norm,
-                                                          float spike_norm, int32_t skip_steps,
-                                                          const int32_t* __restrict__ bad, float* norm_out,
-                                                          float* coef_out, int32_t* skip_state, int32_t* skip_flag,
-                                                          int32_t* skipped_out) {
-  const int64_t G = block_chunks(nb, 256);
-  const int64_t b0 = (int64_t)threadIdx.x * G, b1 = (b0 + G < nb) ? b0 + G : nb;
-  LocalFoldN<20> f;
-  for (int64_t b = b0; b < b1; ++b) f.push(part[b]);
-  const float q = block_fold(f.result(), (nb + G - 1) / G);
+__global__ __launch_bounds__(64 * kFinalWaves) void gnorm_final_kernel(
+    int64_t nb, const float* __restrict__ part, float max_norm, float spike_norm, int32_t skip_steps,
+    const int32_t* __restrict__ bad, float* norm_out, float* coef_out, int32_t* skip_state, int32_t* skip_flag,
+    int32_t* skipped_out) {
+  // wave w folds the aligned range [w R, (w + 1) R) of block sums, R a power of two >= 64: 64 consecutive
+  // sums per read (coalesced) folded across the lanes, those 64-subtrees pushed into a binary-carry fold;
+  // then the waves' subtrees are folded level by level with the pass-through rule
+  __shared__ float wsum[kFinalWaves];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  int64_t R = 64;
+  while (kFinalWaves * R < nb) R <<= 1;
+  LocalFoldN<24> wf;
+  const int64_t r0 = (int64_t)w * R, r1 = (r0 + R < nb) ? r0 + R : nb;
+  constexpr int kBatch = 16;
+  for (int64_t b = r0; b < r1; b += 64 * kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const int64_t j = b + 64 * i + lane;
+      v[i] = j < r1 ? part[j] : 0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < kBatch; ++i) {
+      const int64_t s0 = b + 64 * i;
+      if (s0 < r1) {
+        const float t = wave_fold(v[i], (int)(r1 - s0 < 64 ? r1 - s0 : 64));
+        if (lane == 0) wf.push(t);
+      }
+    }
+  }
+  if (lane == 0) wsum[w] = wf.result();
+  __syncthreads();
   if (threadIdx.x != 0) return;
+  float v[kFinalWaves];
+#pragma unroll
+  for (int q = 0; q < kFinalWaves; ++q) v[q] = wsum[q];
+#pragma unroll
+  for (int d = 1; d < kFinalWaves; d <<= 1)
+#pragma unroll
+    for (int q = 0; q + d < kFinalWaves; q += 2 * d)
+      if ((q + d) * R < nb) v[q] = v[q] + v[q + d];
+  const float q = v[0];
   float norm = __builtin_sqrtf(q);
   float coef;
   int32_t skip;
@@ -215,7 +244,7 @@ hipError_t gnorm_launch(const NormSrc& src, int64_t n, int vec4, float* part, co
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(gnorm_final_kernel, dim3(1), dim3(256), 0, s, nb, part, d.max_norm, d.spike_norm, d.skip_steps,
+  hipLaunchKernelGGL(gnorm_final_kernel, dim3(1), dim3(64 * kFinalWaves), 0, s, nb, part, d.max_norm, d.spike_norm, d.skip_steps,
                      d.bad, d.norm_out, d.coef_out, d.skip_state, d.skip_flag, d.skipped_out);
   return hipGetLastError();
 }
