@@ -33,7 +33,9 @@ def build() -> str:
 class ModelCfg(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
-                ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float)]
+                ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("n_kv_heads", ctypes.c_int32), ("qk_norm", ctypes.c_int32), ("embed_norm", ctypes.c_int32),
+                ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float)]
 
 
 class Plan(ctypes.Structure):
@@ -71,7 +73,10 @@ def _load():
             "cref_rownorm_fwd": (ctypes.c_int, [i64, i64, vp, vp, f, vp, vp]),
             "cref_rownorm_bwd": (ctypes.c_int, [i64, i64, vp, vp, vp, vp, vp, vp]),
             "cref_softmax_causal": (ctypes.c_int, [i64, i64, vp, f, vp]),
+            "cref_softmax_window": (ctypes.c_int, [i64, i64, vp, f, i64, vp]),
             "cref_xent": (ctypes.c_int, [i64, i64, vp, vp, f, vp, vp, vp]),
+            "cref_xent_z": (ctypes.c_int, [i64, i64, vp, vp, f, f, vp, vp, vp]),
+            "cref_rownorm_fwd_f32": (ctypes.c_int, [i64, i64, vp, vp, f, vp, vp]),
             "cref_grad_accum": (ctypes.c_int, [vp, i64, vp, vp]),
             "cref_adamw": (ctypes.c_int, [i64, vp, vp, vp, vp, vp, vp, vp]),
             "cref_block_fwd_bwd": (ctypes.c_int, [vp, i32, vp, vp, vp, vp, vp, vp, vp, vp]),
@@ -173,6 +178,17 @@ def rownorm_fwd(x: np.ndarray, gain: np.ndarray, eps: float):
     return y, rstd
 
 
+def rownorm_fwd_f32(x: np.ndarray, gain: np.ndarray, eps: float):
+    """R3 forward with an fp32 output (the embedding norm of R16)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    gain = np.ascontiguousarray(gain, dtype=np.uint16)
+    rows, cols = x.shape
+    y = np.empty((rows, cols), dtype=np.float32)
+    rstd = np.empty(rows, dtype=np.float32)
+    _check(_load().cref_rownorm_fwd_f32(rows, cols, _p(x), _p(gain), eps, _p(y), _p(rstd)))
+    return y, rstd
+
+
 def rownorm_bwd(x, gain, rstd, dy):
     x = np.ascontiguousarray(x, dtype=np.float32)
     gain = np.ascontiguousarray(gain, dtype=np.uint16)
@@ -185,24 +201,34 @@ def rownorm_bwd(x, gain, rstd, dy):
     return dx, dgain
 
 
-def softmax_causal(raw: np.ndarray, scale: float) -> np.ndarray:
+def softmax_causal(raw: np.ndarray, scale: float, window: int = 0) -> np.ndarray:
+    """R5; with window > 0 (R16), query i sees keys i - window < j <= i."""
     raw = np.ascontiguousarray(raw, dtype=np.float32)
     batch, s, s2 = raw.shape
     assert s == s2
     p = np.empty((batch, s, s), dtype=np.uint16)
-    _check(_load().cref_softmax_causal(batch, s, _p(raw), scale, _p(p)))
+    if window:
+        _check(_load().cref_softmax_window(batch, s, _p(raw), scale, window, _p(p)))
+    else:
+        _check(_load().cref_softmax_causal(batch, s, _p(raw), scale, _p(p)))
     return p
 
 
-def xent(logits: np.ndarray, targets: np.ndarray, inv_tokens: float, want_dlogits: bool = True):
+def xent(logits: np.ndarray, targets: np.ndarray, inv_tokens: float, want_dlogits: bool = True,
+         z_loss: float = 0.0):
+    """R6; with z_loss > 0, R16's z-loss in the same pass."""
     logits = np.ascontiguousarray(logits, dtype=np.uint16)
     targets = np.ascontiguousarray(targets, dtype=np.int32)
     rows, vocab = logits.shape
     dl = np.empty((rows, vocab) if want_dlogits else (1,), dtype=np.uint16)
     rl = np.empty(rows, dtype=np.float32)
     ml = ctypes.c_float(0)
-    _check(_load().cref_xent(rows, vocab, _p(logits), _p(targets), inv_tokens, _p(dl) if want_dlogits else None,
-                             _p(rl), ctypes.addressof(ml)))
+    if z_loss:
+        _check(_load().cref_xent_z(rows, vocab, _p(logits), _p(targets), inv_tokens, z_loss,
+                                   _p(dl) if want_dlogits else None, _p(rl), ctypes.addressof(ml)))
+    else:
+        _check(_load().cref_xent(rows, vocab, _p(logits), _p(targets), inv_tokens,
+                                 _p(dl) if want_dlogits else None, _p(rl), ctypes.addressof(ml)))
     return (dl if want_dlogits else None), rl, np.float32(ml.value)
 
 

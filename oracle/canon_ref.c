@@ -400,6 +400,22 @@ int cref_rownorm_fwd(int64_t rows, int64_t cols, const float* x, const uint16_t*
   return 0;
 }
 
+/* R3 forward with the output kept in fp32 (the embedding norm of R16, whose output is the residual stream) */
+int cref_rownorm_fwd_f32(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps, float* y,
+                         float* rstd) {
+  if (rows < 0 || cols <= 0) return -1;
+  const float inv_d = inv_of(cols);
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < rows; ++t) {
+    const float* xr = x + t * cols;
+    float ss = cref_rdot_f32(xr, 1, xr, 1, cols, CHUNK);
+    float r = cref_div(1.0f, cref_sqrt(cref_add(cref_mul(ss, inv_d), eps)));
+    rstd[t] = r;
+    for (int64_t k = 0; k < cols; ++k) y[t * cols + k] = cref_mul(cref_mul(xr[k], r), widen(gain[k]));
+  }
+  return 0;
+}
+
 int cref_rownorm_bwd(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
                      const float* dy, float* dx, float* dgain) {
   if (rows < 0 || cols <= 0) return -1;
@@ -436,33 +452,44 @@ int cref_rownorm_bwd(int64_t rows, int64_t cols, const float* x, const uint16_t*
 /* R5: causal softmax, R6: cross-entropy                                      */
 /* ======================================================================== */
 
-int cref_softmax_causal(int64_t batch, int64_t s, const float* raw, float scale, uint16_t* probs) {
-  if (batch < 0 || s < 0) return -1;
+/* R5 with the hybrid attention window of R16: query i sees keys j with i - window < j <= i (window 0:
+   every j <= i).  Keys outside enter the row sum as +0 terms at their own positions. */
+int cref_softmax_window(int64_t batch, int64_t s, const float* raw, float scale, int64_t window, uint16_t* probs) {
+  if (batch < 0 || s < 0 || window < 0) return -1;
 #pragma omp parallel for schedule(dynamic, 4)
   for (int64_t bi = 0; bi < batch * s; ++bi) {
     int64_t i = bi % s;
+    int64_t j0 = (window > 0 && i - window + 1 > 0) ? i - window + 1 : 0; /* first key seen */
     const float* row = raw + bi * s;
     uint16_t* prow = probs + bi * s;
     float* e = (float*)malloc(sizeof(float) * (size_t)(s ? s : 1));
-    float m = cref_mul(row[0], scale);
-    for (int64_t j = 1; j <= i; ++j) {
+    float m = cref_mul(row[j0], scale);
+    for (int64_t j = j0 + 1; j <= i; ++j) {
       float sc = cref_mul(row[j], scale);
       if (sc > m) m = sc;
     }
-    for (int64_t j = 0; j < s; ++j) e[j] = (j <= i) ? cref_exp(cref_sub(cref_mul(row[j], scale), m)) : 0.0f;
+    for (int64_t j = 0; j < s; ++j) e[j] = (j >= j0 && j <= i) ? cref_exp(cref_sub(cref_mul(row[j], scale), m)) : 0.0f;
     float S = cref_rsum(e, s, 1, CHUNK); /* masked keys enter as +0 terms */
     float r = cref_div(1.0f, S);
-    for (int64_t j = 0; j < s; ++j) prow[j] = (j <= i) ? cref_bf16(cref_mul(e[j], r)) : (uint16_t)0;
+    for (int64_t j = 0; j < s; ++j) prow[j] = (j >= j0 && j <= i) ? cref_bf16(cref_mul(e[j], r)) : (uint16_t)0;
     free(e);
   }
   return 0;
 }
 
-int cref_xent(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
-              uint16_t* dlogits, float* row_loss, float* mean_loss) {
-  if (rows < 0 || vocab <= 0) return -1;
+int cref_softmax_causal(int64_t batch, int64_t s, const float* raw, float scale, uint16_t* probs) {
+  return cref_softmax_window(batch, s, raw, scale, 0, probs);
+}
+
+/* R6 with the z-loss of R16 (the architecture section: weight 1e-4, in the same pass as the cross-entropy).
+   z = lse, the row's log-partition; row loss RN(CE + RN(z_loss * RN(z * z))); each probability is scaled
+   by RN(1 + RN(RN(2 z_loss) * z)) before the target is subtracted.  z_loss = 0 is the plain R6. */
+int cref_xent_z(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
+                float z_loss, uint16_t* dlogits, float* row_loss, float* mean_loss) {
+  if (rows < 0 || vocab <= 0 || !(z_loss >= 0.0f)) return -1;
   for (int64_t t = 0; t < rows; ++t)
     if (targets[t] < 0 || targets[t] >= vocab) return -1;
+  const float z2 = cref_mul(2.0f, z_loss);
 #pragma omp parallel for schedule(static)
   for (int64_t t = 0; t < rows; ++t) {
     const uint16_t* lr = logits + t * vocab;
@@ -476,11 +503,18 @@ int cref_xent(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t
     float S = cref_rsum(e, vocab, 1, CHUNK);
     float lse = cref_add(m, cref_log(S));
     int32_t y = targets[t];
-    row_loss[t] = cref_sub(lse, widen(lr[y]));
+    float ce = cref_sub(lse, widen(lr[y]));
+    float pscale = 1.0f;
+    if (z_loss != 0.0f) {
+      ce = cref_add(ce, cref_mul(z_loss, cref_mul(lse, lse)));
+      pscale = cref_add(1.0f, cref_mul(z2, lse));
+    }
+    row_loss[t] = ce;
     float r = cref_div(1.0f, S);
     if (dlogits) {
       for (int64_t j = 0; j < vocab; ++j) {
         float p = cref_mul(e[j], r);
+        if (z_loss != 0.0f) p = cref_mul(p, pscale);
         dlogits[t * vocab + j] = cref_bf16(cref_mul(cref_sub(p, j == y ? 1.0f : 0.0f), inv_tokens));
       }
     }
@@ -488,6 +522,11 @@ int cref_xent(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t
   }
   if (mean_loss) *mean_loss = cref_mul(cref_rsum(row_loss, rows, 1, CHUNK), inv_tokens);
   return 0;
+}
+
+int cref_xent(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
+              uint16_t* dlogits, float* row_loss, float* mean_loss) {
+  return cref_xent_z(rows, vocab, logits, targets, inv_tokens, 0.0f, dlogits, row_loss, mean_loss);
 }
 
 /* ======================================================================== */
@@ -679,11 +718,16 @@ static void rope_bwd(const float* g, int hd, const float* cs, const float* sn, f
 /* ======================================================================== */
 
 typedef struct {
-  int64_t T, B, S, d, H, hd, F;
+  int64_t T, B, S, d, H, Hkv, hd, F, N; /* N = (H + 2 Hkv) hd: width of the fused q, k, v projection */
+  int64_t window;                        /* 0: full causal; W: query i sees keys i - W + 1 .. i */
+  int qk_norm;
+  float eps;
   float* x;      /* [T][d] input (residual) */
   uint16_t* xn;  /* [T][d] */
   float* rstd1;  /* [T] */
-  uint16_t *q, *k, *v; /* [B][H][S][hd] bf16, q and k after rotation */
+  float* qkv;    /* [T][N] projection output (kept for the QK-norm backward) */
+  float* rq;     /* [T][H + Hkv]: QK-norm r of each q and k head row */
+  uint16_t *q, *k, *v; /* q [B][H][S][hd], k and v [B][Hkv][S][hd] bf16, q and k after rotation */
   uint16_t* P;   /* [B][H][S][S] */
   uint16_t* O;   /* [T][d] */
   float* h;      /* [T][d] */
@@ -698,16 +742,22 @@ static void* xmalloc(size_t n) {
   return p;
 }
 
-static void block_saved_alloc(block_saved* s, int64_t B, int64_t S, int64_t d, int64_t H, int64_t F) {
-  s->T = B * S; s->B = B; s->S = S; s->d = d; s->H = H; s->hd = d / H; s->F = F;
-  int64_t T = s->T;
+static int64_t kv_heads(const cref_model_cfg* c) { return c->n_kv_heads > 0 ? c->n_kv_heads : c->n_heads; }
+
+static void block_saved_alloc(block_saved* s, const cref_model_cfg* c, int64_t B, int64_t window) {
+  s->B = B; s->S = c->seq; s->T = B * c->seq; s->d = c->d_model; s->H = c->n_heads; s->Hkv = kv_heads(c);
+  s->hd = c->head_dim; s->F = c->d_ffn; s->N = (s->H + 2 * s->Hkv) * s->hd;
+  s->window = window; s->qk_norm = c->qk_norm; s->eps = c->rms_eps;
+  const int64_t T = s->T, d = s->d, S = s->S, F = s->F, kvw = s->Hkv * s->hd;
   s->x = (float*)xmalloc(sizeof(float) * T * d);
   s->xn = (uint16_t*)xmalloc(2 * T * d);
   s->rstd1 = (float*)xmalloc(sizeof(float) * T);
+  s->qkv = (float*)xmalloc(sizeof(float) * T * s->N);
+  s->rq = (float*)xmalloc(sizeof(float) * T * (s->H + s->Hkv));
   s->q = (uint16_t*)xmalloc(2 * T * d);
-  s->k = (uint16_t*)xmalloc(2 * T * d);
-  s->v = (uint16_t*)xmalloc(2 * T * d);
-  s->P = (uint16_t*)xmalloc(2 * B * H * S * S);
+  s->k = (uint16_t*)xmalloc(2 * T * kvw);
+  s->v = (uint16_t*)xmalloc(2 * T * kvw);
+  s->P = (uint16_t*)xmalloc(2 * B * s->H * S * S);
   s->O = (uint16_t*)xmalloc(2 * T * d);
   s->h = (float*)xmalloc(sizeof(float) * T * d);
   s->hn = (uint16_t*)xmalloc(2 * T * d);
@@ -717,8 +767,8 @@ static void block_saved_alloc(block_saved* s, int64_t B, int64_t S, int64_t d, i
 }
 
 static void block_saved_free(block_saved* s) {
-  free(s->x); free(s->xn); free(s->rstd1); free(s->q); free(s->k); free(s->v); free(s->P); free(s->O);
-  free(s->h); free(s->hn); free(s->rstd2); free(s->gu); free(s->a);
+  free(s->x); free(s->xn); free(s->rstd1); free(s->qkv); free(s->rq); free(s->q); free(s->k); free(s->v);
+  free(s->P); free(s->O); free(s->h); free(s->hn); free(s->rstd2); free(s->gu); free(s->a);
 }
 
 static const uint32_t ATTN_SCALE_128 = 0x3DB504F3u; /* RN32(1/sqrt(128)) */
@@ -728,35 +778,68 @@ static float attn_scale(int64_t hd) {
   return (float)(1.0 / sqrt((double)hd)); /* RN32(1/sqrt(hd)) for other head sizes used in tests */
 }
 
-/* forward of one block; w = {attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down}; y = block output */
+/* R16 gain-free QK-norm of one head row (the architecture section: RMSNorm per head before RoPE, no
+   gain): r as in R3, the normalised row kept in fp32 for the rotation. */
+static float headnorm_r(const float* x, int64_t n, float eps) {
+  const float ss = cref_rdot_f32(x, 1, x, 1, n, CHUNK);
+  const float ms = cref_mul(ss, inv_of(n));
+  return cref_div(1.0f, cref_sqrt(cref_add(ms, eps)));
+}
+
+/* R3's input gradient with the gain left out: gy is the gradient of the normalised row. */
+static void headnorm_bwd(const float* x, float r, const float* gy, int64_t n, float* dx) {
+  const float dot = cref_rdot_f32(gy, 1, x, 1, n, CHUNK);
+  const float q = cref_mul(cref_mul(cref_mul(r, r), r), cref_mul(dot, inv_of(n)));
+  for (int64_t k = 0; k < n; ++k) dx[k] = cref_sub(cref_mul(r, gy[k]), cref_mul(x[k], q));
+}
+
+/* q or k head row at projection column col0 of token t: optional QK-norm, then the rotation, bf16 out */
+static void head_in(block_saved* s, int64_t t, int64_t col0, int64_t ridx, const float* rope_cos,
+                    const float* rope_sin, uint16_t* out) {
+  const int64_t hd = s->hd, pos = t % s->S;
+  const float* x = s->qkv + t * s->N + col0;
+  float* xn = (float*)xmalloc(sizeof(float) * hd);
+  if (s->qk_norm) {
+    const float r = headnorm_r(x, hd, s->eps);
+    s->rq[t * (s->H + s->Hkv) + ridx] = r;
+    for (int64_t j = 0; j < hd; ++j) xn[j] = cref_mul(x[j], r);
+  } else {
+    memcpy(xn, x, sizeof(float) * hd);
+  }
+  rope_fwd(xn, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), out);
+  free(xn);
+}
+
+/* forward of one block; w = {attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down}; y = block output.
+   w_qkv rows: H query heads, then Hkv key heads, then Hkv value heads (hd rows each).  Query head h reads
+   key/value head h / (H / Hkv). */
 static void block_fwd(block_saved* s, const float* x, const uint16_t* const* w, const float* rope_cos,
-                      const float* rope_sin, float eps, float* y) {
-  const int64_t T = s->T, B = s->B, S = s->S, d = s->d, H = s->H, hd = s->hd, F = s->F;
+                      const float* rope_sin, float* y) {
+  const int64_t T = s->T, B = s->B, S = s->S, d = s->d, H = s->H, Hkv = s->Hkv, hd = s->hd, F = s->F, N = s->N;
+  const int64_t G = H / Hkv;
   memcpy(s->x, x, sizeof(float) * T * d);
-  cref_rownorm_fwd(T, d, x, w[0], eps, s->xn, s->rstd1);
-  float* qkv = (float*)xmalloc(sizeof(float) * T * 3 * d);
-  cref_gemm(0, 1, T, 3 * d, d, s->xn, d, w[1], d, qkv, 3 * d);
+  cref_rownorm_fwd(T, d, x, w[0], s->eps, s->xn, s->rstd1);
+  cref_gemm(0, 1, T, N, d, s->xn, d, w[1], d, s->qkv, N);
   for (int64_t t = 0; t < T; ++t) {
-    int64_t b = t / S, pos = t % S;
-    for (int64_t hh = 0; hh < H; ++hh) {
-      int64_t o = ((b * H + hh) * S + pos) * hd;
-      rope_fwd(qkv + t * 3 * d + hh * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), s->q + o);
-      rope_fwd(qkv + t * 3 * d + d + hh * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), s->k + o);
-      for (int64_t j = 0; j < hd; ++j) s->v[o + j] = cref_bf16(qkv[t * 3 * d + 2 * d + hh * hd + j]);
+    const int64_t b = t / S, pos = t % S;
+    for (int64_t hh = 0; hh < H; ++hh) head_in(s, t, hh * hd, hh, rope_cos, rope_sin, s->q + ((b * H + hh) * S + pos) * hd);
+    for (int64_t g = 0; g < Hkv; ++g) {
+      const int64_t o = ((b * Hkv + g) * S + pos) * hd;
+      head_in(s, t, (H + g) * hd, H + g, rope_cos, rope_sin, s->k + o);
+      for (int64_t j = 0; j < hd; ++j) s->v[o + j] = cref_bf16(s->qkv[t * N + (H + Hkv + g) * hd + j]);
     }
   }
-  free(qkv);
   float* raw = (float*)xmalloc(sizeof(float) * S * S);
   float* ob = (float*)xmalloc(sizeof(float) * S * hd);
   const float c = attn_scale(hd);
   for (int64_t bh = 0; bh < B * H; ++bh) {
-    int64_t b = bh / H, hh = bh % H;
+    int64_t b = bh / H, hh = bh % H, g = hh / G;
     const uint16_t* Q = s->q + bh * S * hd;
-    const uint16_t* K = s->k + bh * S * hd;
-    const uint16_t* V = s->v + bh * S * hd;
+    const uint16_t* K = s->k + (b * Hkv + g) * S * hd;
+    const uint16_t* V = s->v + (b * Hkv + g) * S * hd;
     uint16_t* P = s->P + bh * S * S;
     cref_gemm(0, 1, S, S, hd, Q, hd, K, hd, raw, S);
-    cref_softmax_causal(1, S, raw, c, P);
+    cref_softmax_window(1, S, raw, c, s->window, P);
     cref_gemm(0, 0, S, hd, S, P, S, V, hd, ob, hd);
     for (int64_t pos = 0; pos < S; ++pos)
       for (int64_t j = 0; j < hd; ++j) s->O[(b * S + pos) * d + hh * hd + j] = cref_bf16(ob[pos * hd + j]);
@@ -767,7 +850,7 @@ static void block_fwd(block_saved* s, const float* x, const uint16_t* const* w, 
   cref_gemm(0, 1, T, d, d, s->O, d, w[2], d, attn, d);
   for (int64_t i = 0; i < T * d; ++i) s->h[i] = cref_add(x[i], attn[i]);
   free(attn);
-  cref_rownorm_fwd(T, d, s->h, w[3], eps, s->hn, s->rstd2);
+  cref_rownorm_fwd(T, d, s->h, w[3], s->eps, s->hn, s->rstd2);
   cref_gemm(0, 1, T, 2 * F, d, s->hn, d, w[4], d, s->gu, 2 * F);
   for (int64_t t = 0; t < T; ++t)
     for (int64_t j = 0; j < F; ++j)
@@ -784,11 +867,31 @@ static uint16_t* to_bf16(const float* x, int64_t n) {
   return o;
 }
 
+/* gradient of a rotated (and, with QK-norm, normalised) head row back to the projection output, bf16 */
+static void head_out(const block_saved* s, int64_t t, int64_t col0, int64_t ridx, const float* g,
+                     const float* rope_cos, const float* rope_sin, uint16_t* dqkv) {
+  const int64_t hd = s->hd, pos = t % s->S;
+  float* gn = (float*)xmalloc(sizeof(float) * hd);
+  rope_bwd(g, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), gn);
+  if (s->qk_norm) {
+    float* gx = (float*)xmalloc(sizeof(float) * hd);
+    headnorm_bwd(s->qkv + t * s->N + col0, s->rq[t * (s->H + s->Hkv) + ridx], gn, hd, gx);
+    for (int64_t j = 0; j < hd; ++j) dqkv[t * s->N + col0 + j] = cref_bf16(gx[j]);
+    free(gx);
+  } else {
+    for (int64_t j = 0; j < hd; ++j) dqkv[t * s->N + col0 + j] = cref_bf16(gn[j]);
+  }
+  free(gn);
+}
+
 /* backward of one block: dy = gradient of the block output; dx = gradient of the block input;
-   dw = the six fp32 weight gradients */
+   dw = the six fp32 weight gradients.  With grouped heads, the gradient of a shared key (value) head is
+   one contraction over every (query head of its group, query) pair, heads in ascending order and queries
+   ascending within each (R16). */
 static void block_bwd(const block_saved* s, const float* dy, const uint16_t* const* w, const float* rope_cos,
                       const float* rope_sin, float* dx, float* const* dw) {
-  const int64_t T = s->T, B = s->B, S = s->S, d = s->d, H = s->H, hd = s->hd, F = s->F;
+  const int64_t T = s->T, B = s->B, S = s->S, d = s->d, H = s->H, Hkv = s->Hkv, hd = s->hd, F = s->F, N = s->N;
+  const int64_t G = H / Hkv, W = s->window;
   /* MLP */
   uint16_t* dyb = to_bf16(dy, T * d);
   cref_gemm(1, 0, d, F, T, dyb, d, s->a, F, dw[5], F);            /* dW_down = dy^T a */
@@ -825,57 +928,60 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
   float* dO = (float*)xmalloc(sizeof(float) * T * d);
   cref_gemm(0, 0, T, d, d, dhb, d, w[2], d, dO, d);               /* dO = dh W_o */
   free(dhb);
-  /* attention core, per (batch, head) */
+  /* attention core, per (batch, key/value head group) */
   const float c = attn_scale(hd);
-  float* dq = (float*)xmalloc(sizeof(float) * T * d);
-  float* dk = (float*)xmalloc(sizeof(float) * T * d);
-  uint16_t* dqkv = (uint16_t*)xmalloc(2 * T * 3 * d);
-  uint16_t* dOb = (uint16_t*)xmalloc(2 * S * hd);
+  uint16_t* dqkv = (uint16_t*)xmalloc(2 * T * N);
+  uint16_t* dOs = (uint16_t*)xmalloc(2 * G * S * hd);  /* the group's dO, head after head */
+  uint16_t* Qs = (uint16_t*)xmalloc(2 * G * S * hd);   /* the group's Q, head after head */
+  uint16_t* Ps = (uint16_t*)xmalloc(2 * G * S * S);    /* the group's P, head after head */
+  uint16_t* dSs = (uint16_t*)xmalloc(2 * G * S * S);   /* the group's dS, head after head */
   uint16_t* Ob = (uint16_t*)xmalloc(2 * S * hd);
   float* D = (float*)xmalloc(sizeof(float) * S);
   float* dP = (float*)xmalloc(sizeof(float) * S * S);
-  uint16_t* dS = (uint16_t*)xmalloc(2 * S * S);
   float* gq = (float*)xmalloc(sizeof(float) * S * hd);
   float* gk = (float*)xmalloc(sizeof(float) * S * hd);
   float* gv = (float*)xmalloc(sizeof(float) * S * hd);
-  for (int64_t bh = 0; bh < B * H; ++bh) {
-    int64_t b = bh / H, hh = bh % H;
-    const uint16_t* Q = s->q + bh * S * hd;
-    const uint16_t* K = s->k + bh * S * hd;
-    const uint16_t* V = s->v + bh * S * hd;
-    const uint16_t* P = s->P + bh * S * S;
-    for (int64_t pos = 0; pos < S; ++pos)
-      for (int64_t j = 0; j < hd; ++j) {
-        dOb[pos * hd + j] = cref_bf16(dO[(b * S + pos) * d + hh * hd + j]);
-        Ob[pos * hd + j] = s->O[(b * S + pos) * d + hh * hd + j];
-      }
-    for (int64_t i = 0; i < S; ++i) D[i] = cref_rdot_bf16(dOb + i * hd, 1, Ob + i * hd, 1, hd, CHUNK);
-    cref_gemm(0, 1, S, S, hd, dOb, hd, V, hd, dP, S);             /* dP = dO V^T */
-    for (int64_t i = 0; i < S; ++i)
-      for (int64_t j = 0; j < S; ++j)
-        dS[i * S + j] = (j <= i) ? cref_bf16(cref_mul(cref_mul(widen(P[i * S + j]), cref_sub(dP[i * S + j], D[i])), c))
+  for (int64_t b = 0; b < B; ++b) {
+    for (int64_t g = 0; g < Hkv; ++g) {
+      const uint16_t* K = s->k + (b * Hkv + g) * S * hd;
+      const uint16_t* V = s->v + (b * Hkv + g) * S * hd;
+      for (int64_t e = 0; e < G; ++e) {
+        const int64_t hh = g * G + e, bh = b * H + hh;
+        uint16_t* dOb = dOs + e * S * hd;
+        uint16_t* dS = dSs + e * S * S;
+        memcpy(Qs + e * S * hd, s->q + bh * S * hd, 2 * S * hd);
+        memcpy(Ps + e * S * S, s->P + bh * S * S, 2 * S * S);
+        const uint16_t* P = s->P + bh * S * S;
+        for (int64_t pos = 0; pos < S; ++pos)
+          for (int64_t j = 0; j < hd; ++j) {
+            dOb[pos * hd + j] = cref_bf16(dO[(b * S + pos) * d + hh * hd + j]);
+            Ob[pos * hd + j] = s->O[(b * S + pos) * d + hh * hd + j];
+          }
+        for (int64_t i = 0; i < S; ++i) D[i] = cref_rdot_bf16(dOb + i * hd, 1, Ob + i * hd, 1, hd, CHUNK);
+        cref_gemm(0, 1, S, S, hd, dOb, hd, V, hd, dP, S);           /* dP = dO V^T */
+        for (int64_t i = 0; i < S; ++i)
+          for (int64_t j = 0; j < S; ++j) {
+            const int seen = j <= i && (W == 0 || j > i - W);
+            dS[i * S + j] = seen ? cref_bf16(cref_mul(cref_mul(widen(P[i * S + j]), cref_sub(dP[i * S + j], D[i])), c))
                                  : (uint16_t)0;
-    cref_gemm(0, 0, S, hd, S, dS, S, K, hd, gq, hd);              /* dQ = dS K */
-    cref_gemm(1, 0, S, hd, S, dS, S, Q, hd, gk, hd);              /* dK = dS^T Q */
-    cref_gemm(1, 0, S, hd, S, P, S, dOb, hd, gv, hd);             /* dV = P^T dO */
-    for (int64_t pos = 0; pos < S; ++pos) {
-      int64_t t = b * S + pos;
-      rope_bwd(gq + pos * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), dq + t * d + hh * hd);
-      rope_bwd(gk + pos * hd, (int)hd, rope_cos + pos * (hd / 2), rope_sin + pos * (hd / 2), dk + t * d + hh * hd);
-      for (int64_t j = 0; j < hd; ++j) dqkv[t * 3 * d + 2 * d + hh * hd + j] = cref_bf16(gv[pos * hd + j]);
+          }
+        cref_gemm(0, 0, S, hd, S, dS, S, K, hd, gq, hd);            /* dQ = dS K */
+        for (int64_t pos = 0; pos < S; ++pos)
+          head_out(s, b * S + pos, hh * hd, hh, gq + pos * hd, rope_cos, rope_sin, dqkv);
+      }
+      cref_gemm(1, 0, S, hd, G * S, dSs, S, Qs, hd, gk, hd);       /* dK = sum over the group of dS^T Q */
+      cref_gemm(1, 0, S, hd, G * S, Ps, S, dOs, hd, gv, hd);       /* dV = sum over the group of P^T dO */
+      for (int64_t pos = 0; pos < S; ++pos) {
+        const int64_t t = b * S + pos;
+        head_out(s, t, (H + g) * hd, H + g, gk + pos * hd, rope_cos, rope_sin, dqkv);
+        for (int64_t j = 0; j < hd; ++j) dqkv[t * N + (H + Hkv + g) * hd + j] = cref_bf16(gv[pos * hd + j]);
+      }
     }
   }
-  free(dOb); free(Ob); free(D); free(dP); free(dS); free(gq); free(gk); free(gv); free(dO);
-  for (int64_t t = 0; t < T; ++t)
-    for (int64_t j = 0; j < d; ++j) {
-      dqkv[t * 3 * d + j] = cref_bf16(dq[t * d + j]);
-      dqkv[t * 3 * d + d + j] = cref_bf16(dk[t * d + j]);
-    }
-  free(dq);
-  free(dk);
-  cref_gemm(1, 0, 3 * d, d, T, dqkv, 3 * d, s->xn, d, dw[1], d);  /* dW_qkv = dqkv^T xn */
+  free(dOs); free(Qs); free(Ps); free(dSs); free(Ob); free(D); free(dP); free(gq); free(gk); free(gv); free(dO);
+  cref_gemm(1, 0, N, d, T, dqkv, N, s->xn, d, dw[1], d);          /* dW_qkv = dqkv^T xn */
   float* dxn = (float*)xmalloc(sizeof(float) * T * d);
-  cref_gemm(0, 0, T, d, 3 * d, dqkv, 3 * d, w[1], d, dxn, d);     /* dxn = dqkv W_qkv */
+  cref_gemm(0, 0, T, d, N, dqkv, N, w[1], d, dxn, d);             /* dxn = dqkv W_qkv */
   free(dqkv);
   float* dxnorm = (float*)xmalloc(sizeof(float) * T * d);
   cref_rownorm_bwd(T, d, s->x, w[0], s->rstd1, dxn, dxnorm, dw[0]);
@@ -886,9 +992,23 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
 }
 
 static int cfg_valid(const cref_model_cfg* c) {
-  return c && c->n_layers >= 1 && c->d_model > 0 && c->n_heads > 0 && c->head_dim > 0 &&
-         c->n_heads * c->head_dim == c->d_model && (c->head_dim % 2) == 0 && c->d_ffn > 0 && c->vocab > 0 &&
-         c->seq > 0 && c->micro_seqs > 0;
+  if (!c || c->n_layers < 1 || c->d_model <= 0 || c->n_heads <= 0 || c->head_dim <= 0 ||
+      c->n_heads * c->head_dim != c->d_model || (c->head_dim % 2) != 0 || c->d_ffn <= 0 || c->vocab <= 0 ||
+      c->seq <= 0 || c->micro_seqs <= 0)
+    return 0;
+  if (c->n_kv_heads < 0 || (c->n_kv_heads > 0 && c->n_heads % c->n_kv_heads != 0)) return 0;
+  if ((c->qk_norm != 0 && c->qk_norm != 1) || (c->embed_norm != 0 && c->embed_norm != 1)) return 0;
+  if (c->swa_window < 0 || c->swa_full_every < 0) return 0;
+  if (!(c->z_loss >= 0.0f) || isinf(c->z_loss)) return 0;
+  return 1;
+}
+
+/* R16 hybrid attention: layer l (0-based) of L is windowed unless it is one of every swa_full_every-th
+   layers (l + 1 a multiple of it) or the last layer. */
+static int64_t layer_window(const cref_model_cfg* c, int64_t l) {
+  if (c->swa_window == 0) return 0;
+  if ((c->swa_full_every > 0 && (l + 1) % c->swa_full_every == 0) || l == c->n_layers - 1) return 0;
+  return c->swa_window;
 }
 
 int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x, const float* dy,
@@ -896,8 +1016,8 @@ int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x,
                        float* const* dw) {
   if (!cfg_valid(cfg) || batch <= 0) return -1;
   block_saved s;
-  block_saved_alloc(&s, batch, cfg->seq, cfg->d_model, cfg->n_heads, cfg->d_ffn);
-  block_fwd(&s, x, w, rope_cos, rope_sin, cfg->rms_eps, y);
+  block_saved_alloc(&s, cfg, batch, cfg->swa_window);
+  block_fwd(&s, x, w, rope_cos, rope_sin, y);
   block_bwd(&s, dy, w, rope_cos, rope_sin, dx, dw);
   block_saved_free(&s);
   return 0;
@@ -907,14 +1027,20 @@ int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x,
 /* Full step: forward + backward per microbatch, Algorithm 1, AdamW          */
 /* ======================================================================== */
 
-/* tensor sizes in the declared order */
+static int64_t n_tensors_of(const cref_model_cfg* c) { return 3 + 6 * (int64_t)c->n_layers + (c->embed_norm ? 1 : 0); }
+static int64_t layer0_of(const cref_model_cfg* c) { return 1 + (c->embed_norm ? 1 : 0); } /* first layer tensor */
+
+/* tensor sizes in the declared order: embed, [embed_norm], per layer attn_norm, w_qkv, w_o, ffn_norm,
+   w_gate_up, w_down, then final_norm, head */
 static void tensor_sizes(const cref_model_cfg* c, int64_t* sz, uint8_t* decay) {
   int64_t d = c->d_model, F = c->d_ffn, V = c->vocab;
+  int64_t N = (c->n_heads + 2 * kv_heads(c)) * (int64_t)c->head_dim;
   int i = 0;
   sz[i] = V * d; decay[i++] = 0;                     /* embed */
+  if (c->embed_norm) { sz[i] = d; decay[i++] = 0; }  /* embed_norm gain */
   for (int l = 0; l < c->n_layers; ++l) {
     sz[i] = d; decay[i++] = 0;                       /* attn_norm */
-    sz[i] = 3 * d * d; decay[i++] = 1;               /* w_qkv */
+    sz[i] = N * d; decay[i++] = 1;                   /* w_qkv */
     sz[i] = d * d; decay[i++] = 1;                   /* w_o */
     sz[i] = d; decay[i++] = 0;                       /* ffn_norm */
     sz[i] = 2 * F * d; decay[i++] = 1;               /* w_gate_up */
@@ -936,21 +1062,30 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
       inp[b * S + s] = tok[b * (S + 1) + s];
       lab[b * S + s] = tok[b * (S + 1) + s + 1];
     }
-  /* embedding gather */
+  /* embedding gather, then (R16) the embedding norm, whose fp32 output enters the first block */
+  const int64_t l0 = layer0_of(c);
   float* x = (float*)xmalloc(sizeof(float) * T * d);
   for (int64_t t = 0; t < T; ++t)
     for (int64_t j = 0; j < d; ++j) x[t * d + j] = widen(params[0][(int64_t)inp[t] * d + j]);
+  float* x_emb = NULL;   /* the gathered rows, kept for the embedding norm's backward */
+  float* rstd_emb = NULL;
+  if (c->embed_norm) {
+    x_emb = x;
+    rstd_emb = (float*)xmalloc(sizeof(float) * T);
+    x = (float*)xmalloc(sizeof(float) * T * d);
+    cref_rownorm_fwd_f32(T, d, x_emb, params[1], c->rms_eps, x, rstd_emb);
+  }
   block_saved* saved = (block_saved*)xmalloc(sizeof(block_saved) * L);
   float* y = (float*)xmalloc(sizeof(float) * T * d);
   for (int64_t l = 0; l < L; ++l) {
     const uint16_t* w[6];
-    for (int i = 0; i < 6; ++i) w[i] = params[1 + 6 * l + i];
-    block_saved_alloc(&saved[l], B, S, d, c->n_heads, c->d_ffn);
-    block_fwd(&saved[l], x, w, rope_cos, rope_sin, c->rms_eps, y);
+    for (int i = 0; i < 6; ++i) w[i] = params[l0 + 6 * l + i];
+    block_saved_alloc(&saved[l], c, B, layer_window(c, l));
+    block_fwd(&saved[l], x, w, rope_cos, rope_sin, y);
     float* tmp = x; x = y; y = tmp;
   }
   /* final norm, head, loss */
-  const int64_t i_fn = 1 + 6 * L, i_head = 2 + 6 * L;
+  const int64_t i_fn = l0 + 6 * L, i_head = i_fn + 1;
   uint16_t* xf = (uint16_t*)xmalloc(2 * T * d);
   float* rstdf = (float*)xmalloc(sizeof(float) * T);
   cref_rownorm_fwd(T, d, x, params[i_fn], c->rms_eps, xf, rstdf);
@@ -962,7 +1097,7 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
   float* row_loss = (float*)xmalloc(sizeof(float) * T);
   float loss = 0.0f;
   const float invT = inv_of(T);
-  cref_xent(T, V, logits, lab, invT, dlogits, row_loss, &loss);
+  cref_xent_z(T, V, logits, lab, invT, c->z_loss, dlogits, row_loss, &loss);
   free(logits);
   free(row_loss);
   /* backward */
@@ -980,14 +1115,21 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
     const uint16_t* w[6];
     float* dw[6];
     for (int i = 0; i < 6; ++i) {
-      w[i] = params[1 + 6 * l + i];
-      dw[i] = grad + off[1 + 6 * l + i];
+      w[i] = params[l0 + 6 * l + i];
+      dw[i] = grad + off[l0 + 6 * l + i];
     }
     block_bwd(&saved[l], dx, w, rope_cos, rope_sin, dxp, dw);
     block_saved_free(&saved[l]);
     float* tmp = dx; dx = dxp; dxp = tmp;
   }
   free(saved);
+  if (c->embed_norm) {
+    /* the embedding norm's backward: dx (gradient of its output) -> gradient of the gathered rows */
+    cref_rownorm_bwd(T, d, x_emb, params[1], rstd_emb, dx, dxp, grad + off[1]);
+    float* tmp = dx; dx = dxp; dxp = tmp;
+    free(x_emb);
+    free(rstd_emb);
+  }
   /* R11: dE[v] = rsum over ascending positions t with inp[t] == v of dx[t] */
   float* dE = grad + off[0];
   int64_t* cnt = (int64_t*)calloc((size_t)V + 1, sizeof(int64_t));
@@ -1023,7 +1165,7 @@ int cref_step(const cref_model_cfg* c, const cref_plan* plan, uint16_t* const* p
   if (!cfg_valid(c) || !plan_valid(plan) || !k) return -1;
   if (clip && (!(clip->max_norm > 0.0f) || clip->skip_steps < 0 || (clip->skip_steps > 0 && !skip_state)))
     return -1;
-  const int64_t nt = 3 + 6 * (int64_t)c->n_layers;
+  const int64_t nt = n_tensors_of(c);
   int64_t* sz = (int64_t*)xmalloc(sizeof(int64_t) * nt);
   uint8_t* decay = (uint8_t*)xmalloc(nt);
   tensor_sizes(c, sz, decay);

@@ -17,9 +17,14 @@
 extern "C" {
 #endif
 
+/* Model shape and the R16 variants (all zero: the plain block).  n_kv_heads: 0 (= n_heads) or a divisor
+   of n_heads; qk_norm, embed_norm: 0 or 1; swa_window: 0 (full causal) or the window of the windowed
+   layers, which are all but every swa_full_every-th and the last; z_loss: weight, 0 for none. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
   float rms_eps;
+  int32_t n_kv_heads, qk_norm, embed_norm, swa_window, swa_full_every;
+  float z_loss;
 } cref_model_cfg;
 
 typedef struct {
@@ -69,11 +74,19 @@ int cref_rownorm_fwd(int64_t rows, int64_t cols, const float* x, const uint16_t*
                      float* rstd);
 int cref_rownorm_bwd(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
                      const float* dy, float* dx, float* dgain);
+/* R3 forward with the output kept in fp32: y = RN(RN(x * r) * g) */
+int cref_rownorm_fwd_f32(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps, float* y,
+                         float* rstd);
 
-/* ---- R5 causal softmax of raw scores (scale applied inside), R6 cross-entropy ---- */
+/* ---- R5 causal softmax of raw scores (scale applied inside), R6 cross-entropy ----
+   softmax_window: query i sees keys i - window < j <= i (window 0: all j <= i).
+   xent_z: R6 plus the z-loss of weight z_loss (0: plain R6). */
 int cref_softmax_causal(int64_t batch, int64_t s, const float* raw, float scale, uint16_t* probs);
+int cref_softmax_window(int64_t batch, int64_t s, const float* raw, float scale, int64_t window, uint16_t* probs);
 int cref_xent(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
               uint16_t* dlogits, float* row_loss, float* mean_loss);
+int cref_xent_z(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
+                float z_loss, uint16_t* dlogits, float* row_loss, float* mean_loss);
 
 /* ---- R7 gradient plan (Alg. 1 + Alg. 2) ---- */
 int cref_grad_accum(const cref_plan* plan, int64_t n, const float* const* grads, float* out);
@@ -93,15 +106,16 @@ int cref_clip_decide(float norm, const cref_clip_cfg* k, int32_t* skip_state, fl
 int cref_clip_apply(int64_t n_tensors, const int64_t* sizes, float* const* grads, float coef);
 
 /* ---- one decoder block, forward + backward ----
-   x, dy: fp32 [batch*seq, d]; w: the six block tensors in order attn_norm, w_qkv, w_o, ffn_norm,
-   w_gate_up, w_down; y: block output; dx: input gradient; dw: six fp32 gradient buffers. */
+   x, dy: fp32 [batch*seq, d]; w: the six block tensors in order attn_norm, w_qkv ([(H + 2 Hkv) hd, d]:
+   query heads, key heads, value heads), w_o, ffn_norm, w_gate_up, w_down; y: block output; dx: input
+   gradient; dw: six fp32 gradient buffers.  The block's attention window is cfg->swa_window. */
 int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x, const float* dy,
                        const uint16_t* const* w, const float* rope_cos, const float* rope_sin, float* y, float* dx,
                        float* const* dw);
 
 /* ---- full step: Alg. 1 over virtual ranks, then AdamW ----
-   params/m/v: n_tensors = 3 + 6*n_layers tensors in declared order (embed, per layer: attn_norm, w_qkv,
-   w_o, ffn_norm, w_gate_up, w_down; final_norm, head).  windows: [M][seq+1] int32 with
+   params/m/v: n_tensors = 3 + 6*n_layers (+1 with embed_norm) tensors in declared order (embed,
+   [embed_norm], per layer: attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down; final_norm, head).  windows: [M][seq+1] int32 with
    M = dp_shard*dp_replicate*accum*micro_seqs.  grads_out (optional, may be NULL): per-tensor fp32
    buffers receiving the reduced gradient g (before any clip).  clip (optional): R15 between the
    plan and AdamW; norm_out gets the pre-clip norm, skip_state is the spike counter (in/out), and

@@ -28,7 +28,7 @@ TENSOR_IDS = {
     "grads": 8,            # + rank index
     "adam_p": 40, "adam_g": 41,
     "windows": 50,
-    "embed": 100, "head": 101, "final_norm": 102,
+    "embed": 100, "head": 101, "final_norm": 102, "embed_norm": 103,
     "attn_norm": 200, "w_qkv": 201, "w_o": 202, "ffn_norm": 203, "w_gate_up": 204, "w_down": 205,
 }
 LAYER_STRIDE = 16
@@ -125,23 +125,30 @@ def adamw_constants(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8, wd=0.1, t=1):
     return tuple(float(np.float32(v)) for v in vals)
 
 
-def model_param_shapes(n_layers, d_model, d_ffn, vocab):
-    """Parameter tensors in the declared order, with (name, shape, init std, weight-decay flag)."""
+def model_param_shapes(n_layers, d_model, d_ffn, vocab, kv_dim=None, embed_norm=False):
+    """Parameter tensors in the declared order, with (name, shape, init std, weight-decay flag).
+    kv_dim: width of the key (and of the value) projection, n_kv_heads * head_dim (default d_model);
+    embed_norm: a gain tensor after the embedding."""
+    kv = d_model if kv_dim is None else kv_dim
     out = [("embed", (vocab, d_model), 0.02, 0)]
+    if embed_norm:
+        out.append(("embed_norm", (d_model,), None, 0))
     for l in range(n_layers):
-        out += [(f"l{l}.attn_norm", (d_model,), None, 0), (f"l{l}.w_qkv", (3 * d_model, d_model), 0.02, 1),
+        out += [(f"l{l}.attn_norm", (d_model,), None, 0), (f"l{l}.w_qkv", (d_model + 2 * kv, d_model), 0.02, 1),
                 (f"l{l}.w_o", (d_model, d_model), 0.02, 1), (f"l{l}.ffn_norm", (d_model,), None, 0),
                 (f"l{l}.w_gate_up", (2 * d_ffn, d_model), 0.02, 1), (f"l{l}.w_down", (d_model, d_ffn), 0.02, 1)]
     out += [("final_norm", (d_model,), None, 0), ("head", (vocab, d_model), 0.02, 1)]
     return out
 
 
-def model_params(n_layers, d_model, d_ffn, vocab, seed=0, std=0.02, out=None):
+def model_params(n_layers, d_model, d_ffn, vocab, seed=0, std=0.02, out=None, kv_dim=None, embed_norm=False):
     """bf16 parameters: N(0, std) for matrices, 1.0 for norm gains.  ``out`` may hold preallocated
     uint16 buffers (e.g. pinned host tensors) to fill instead of new numpy arrays."""
     res = []
-    base = {"embed": TENSOR_IDS["embed"], "head": TENSOR_IDS["head"], "final_norm": TENSOR_IDS["final_norm"]}
-    for idx, (name, shape, s, _) in enumerate(model_param_shapes(n_layers, d_model, d_ffn, vocab)):
+    base = {"embed": TENSOR_IDS["embed"], "head": TENSOR_IDS["head"], "final_norm": TENSOR_IDS["final_norm"],
+            "embed_norm": TENSOR_IDS["embed_norm"]}
+    for idx, (name, shape, s, _) in enumerate(model_param_shapes(n_layers, d_model, d_ffn, vocab, kv_dim,
+                                                                 embed_norm)):
         buf = None if out is None else out[idx]
         if s is None:
             arr = np.full(shape, 0x3F80, dtype=np.uint16) if buf is None else buf

@@ -62,22 +62,40 @@ def rope(x, cos, sin):
     return torch.cat([x1 * cos - x2 * sin, x2 * cos + x1 * sin], dim=-1)
 
 
-def block(x, w, B, S, H, hd, F, eps, cos, sin, scale):
-    """w: dict of float64 tensors attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down."""
-    d = H * hd
+def headnorm(x, eps):
+    """Gain-free RMSNorm of each head row (last dimension)."""
+    return x * torch.rsqrt((x * x).mean(dim=-1, keepdim=True) + eps)
+
+
+def block(x, w, B, S, H, hd, F, eps, cos, sin, scale, Hkv=None, qk_norm=False, window=0):
+    """w: dict of float64 tensors attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down.  Hkv: key/value heads
+    (query head h reads head h // (H // Hkv)); qk_norm: gain-free per-head RMSNorm of q and k before the
+    rotation; window: query i sees keys i - window < j <= i (0: all j <= i)."""
+    Hkv = H if Hkv is None else Hkv
+    d, kvw = H * hd, Hkv * hd
     xn = rmsnorm(x, w["attn_norm"], eps)
-    qkv = linear(xn, w["w_qkv"])                                     # [T, 3d]
-    q, k, v = qkv[:, :d], qkv[:, d:2 * d], qkv[:, 2 * d:]
+    qkv = linear(xn, w["w_qkv"])                                     # [T, d + 2 kvw]
+    q, k, v = qkv[:, :d], qkv[:, d:d + kvw], qkv[:, d + kvw:]
 
-    def heads(t):
-        return t.reshape(B, S, H, hd).permute(0, 2, 1, 3)            # [B, H, S, hd]
+    def heads(t, n):
+        return t.reshape(B, S, n, hd).permute(0, 2, 1, 3)            # [B, n, S, hd]
 
-    qh = rf(rope(heads(q), cos, sin))
-    kh = rf(rope(heads(k), cos, sin))
-    vh = rf(heads(v))
+    qh, kh = heads(q, H), heads(k, Hkv)
+    if qk_norm:
+        qh, kh = headnorm(qh, eps), headnorm(kh, eps)
+    qh = rf(rope(qh, cos, sin))
+    kh = rf(rope(kh, cos, sin))
+    vh = rf(heads(v, Hkv))
+    G = H // Hkv
+    kh = kh.repeat_interleave(G, dim=1)                              # [B, H, S, hd]
+    vh = vh.repeat_interleave(G, dim=1)
     raw = rb(qh @ kh.transpose(-1, -2))                              # [B, H, S, S]
     sc = raw * scale
-    mask = torch.tril(torch.ones(S, S, dtype=torch.bool))
+    i = torch.arange(S).unsqueeze(1)
+    j = torch.arange(S).unsqueeze(0)
+    mask = j <= i
+    if window:
+        mask = mask & (j > i - window)
     sc = sc.masked_fill(~mask, float("-inf"))
     p = rf(torch.softmax(sc, dim=-1))
     o = rb(p @ vh)                                                   # [B, H, S, hd]
@@ -90,17 +108,34 @@ def block(x, w, B, S, H, hd, F, eps, cos, sin, scale):
     return h + linear(a, w["w_down"])
 
 
+def layer_window(cfg, l):
+    win = cfg.get("swa_window", 0)
+    every = cfg.get("swa_full_every", 0)
+    if not win or (every and (l + 1) % every == 0) or l == cfg["L"] - 1:
+        return 0
+    return win
+
+
 def model_loss(params, tok, cfg, cos, sin, scale):
-    """params: list of float64 leaf tensors in declared order; tok: int64 [B, S+1]."""
+    """params: list of float64 leaf tensors in declared order; tok: int64 [B, S+1].  cfg may name the
+    variants Hkv, qk_norm, embed_norm, swa_window, swa_full_every, z_loss."""
     B, S1 = tok.shape
     S = S1 - 1
     d, H, hd, F, L = cfg["d"], cfg["H"], cfg["hd"], cfg["F"], cfg["L"]
+    en = 1 if cfg.get("embed_norm") else 0
     inp, lab = tok[:, :S].reshape(-1), tok[:, 1:].reshape(-1)
     x = params[0][inp]
+    if en:
+        x = rmsnorm(x, params[1], cfg["eps"])
     names = ["attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down"]
     for l in range(L):
-        w = {n: params[1 + 6 * l + i] for i, n in enumerate(names)}
-        x = block(x, w, B, S, H, hd, F, cfg["eps"], cos, sin, scale)
-    xf = rmsnorm(x, params[1 + 6 * L], cfg["eps"])
-    logits = rf(linear(xf, params[2 + 6 * L]))
-    return torch.nn.functional.cross_entropy(logits, lab, reduction="mean")
+        w = {n: params[1 + en + 6 * l + i] for i, n in enumerate(names)}
+        x = block(x, w, B, S, H, hd, F, cfg["eps"], cos, sin, scale, cfg.get("Hkv"), cfg.get("qk_norm", False),
+                  layer_window(cfg, l))
+    xf = rmsnorm(x, params[1 + en + 6 * L], cfg["eps"])
+    logits = rf(linear(xf, params[2 + en + 6 * L]))
+    loss = torch.nn.functional.cross_entropy(logits, lab, reduction="mean")
+    zw = cfg.get("z_loss", 0.0)
+    if zw:
+        loss = loss + zw * (torch.logsumexp(logits, dim=-1) ** 2).mean()
+    return loss
