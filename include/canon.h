@@ -57,12 +57,27 @@ typedef struct {
   int32_t accum, dp_shard, dp_replicate;
 } canon_dp_plan;
 
-/* Llama-style decoder: pre-norm RMSNorm blocks, causal multi-head attention with half-split RoPE,
-   SwiGLU MLP (gate and up as one fused weight), untied embedding and head, no biases (the paper's
-   architecture section, with the variants the paper adds beyond a plain block left out). */
+/* Llama-style decoder: pre-norm RMSNorm blocks, causal attention with half-split RoPE, SwiGLU MLP (gate
+   and up as one fused weight), untied embedding and head, no biases (the paper's architecture section).
+   The paper's further variants (R16, same section) are switched on by the fields after rms_eps; all zero
+   gives the plain block:
+     n_kv_heads:     0 (= n_heads) or a divisor of n_heads; query head h reads key/value head
+                     h / (n_heads / n_kv_heads).  w_qkv is [(n_heads + 2 n_kv_heads) head_dim, d_model]:
+                     query heads, then key heads, then value heads.  The gradient of a shared key (value)
+                     head is one contraction over its group's query heads (ascending) and their queries.
+     qk_norm:        1: gain-free RMSNorm (eps = rms_eps) of every q and k head row before the rotation,
+                     its output kept fp32 into the rotation.
+     embed_norm:     1: an RMSNorm with its own gain (tensor "embed_norm", after embed in the declared
+                     order) on the gathered embedding rows, fp32 output into the first block.
+     swa_window:     0: every layer full causal; W > 0: query i sees keys i - W < j <= i in every layer
+                     except every swa_full_every-th (l + 1 a multiple of it, 0 = none) and the last.
+     z_loss:         weight of the z-loss (0: none): row loss RN(CE + RN(z * RN(lse^2))), probabilities
+                     scaled by RN(1 + RN(RN(2 z) * lse)) in the logit gradient. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
   float rms_eps; /* fp32 value, e.g. RN32(1e-5) */
+  int32_t n_kv_heads, qk_norm, embed_norm, swa_window, swa_full_every;
+  float z_loss;
 } canon_model_cfg;
 
 /* AdamW constants, each evaluated in double and rounded once to fp32 by the caller (R9). */
@@ -95,26 +110,33 @@ canon_status canon_gemm_strided_batched(const canon_order* order, int32_t trans_
    dir = CANON_BWD: inputs x, gain, rstd (from the forward), dy (fp32 [rows, cols]); outputs dx (fp32
        [rows, cols]) and, if dgain != NULL, dgain (fp32 [cols]) = R1 over rows of RN(dy*RN(x*r)).
        dx also serves as scratch for the dgain chunk partials before it receives its values, so dx must not
-       overlap x, dy, rstd, gain or dgain (CANON_EINVAL otherwise). */
-enum { CANON_FWD = 0, CANON_BWD = 1 };
+       overlap x, dy, rstd, gain or dgain (CANON_EINVAL otherwise).
+   dir = CANON_FWD_F32: as CANON_FWD with y fp32 [rows, cols] = RN(RN(x*r)*g) (no bf16 rounding; the
+       embedding norm of R16). */
+enum { CANON_FWD = 0, CANON_BWD = 1, CANON_FWD_F32 = 2 };
 canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, int64_t cols, const float* x,
-                           const uint16_t* gain, float eps, uint16_t* y, float* rstd, const float* dy, float* dx,
+                           const uint16_t* gain, float eps, void* y, float* rstd, const float* dy, float* dx,
                            float* dgain, void* stream);
 
 /* ------------------------------------------------------------------------------------------------ */
 /* Row softmax / cross-entropy (R5, R6; the audit section names the sums inside softmax among the
    reductions that need a definite order).
    mode = CANON_SOFTMAX_CAUSAL: x = fp32 raw scores [rows, cols] forming rows/cols stacked square
-       matrices; row r is query i = r mod cols.  score = RN(x*scale); keys j <= i only; out =
-       probabilities bf16 [rows, cols], +0 for masked keys.  targets, row_loss, mean_loss unused.
+       matrices; row r is query i = r mod cols.  score = RN(x*scale); keys j <= i only, and with
+       window > 0 only keys j > i - window (R16's sliding window); the row sum still runs over every key
+       position, masked ones as +0 terms.  out = probabilities bf16 [rows, cols], +0 for masked keys.
+       targets, inv_tokens, z_loss, row_loss, mean_loss unused.
    mode = CANON_XENT: x = bf16 logits [rows, cols = vocab]; targets int32 [rows] in [0, cols);
-       out = dlogits bf16 [rows, cols] = bf16(RN(RN(p - onehot) * inv_tokens)); row_loss fp32 [rows];
-       mean_loss (fp32 scalar, device) = RN(R1(row_loss) * inv_tokens).  Targets are checked on the
-       device; an out-of-range target makes the kernel write NaN to mean_loss. */
+       out = dlogits bf16 [rows, cols] = bf16(RN(RN(p' - onehot) * inv_tokens)) with p' = p, or with
+       z_loss > 0 p' = RN(p * RN(1 + RN(RN(2 z_loss) * lse))); row_loss fp32 [rows] = RN(lse - x[target]),
+       plus RN(z_loss * RN(lse * lse)) with the z-loss; mean_loss (fp32 scalar, device) =
+       RN(R1(row_loss) * inv_tokens).  Targets are checked on the device; an out-of-range target makes
+       its row loss, and so mean_loss, NaN.  window unused.
+   window >= 0, z_loss >= 0 and finite (CANON_EINVAL otherwise). */
 enum { CANON_SOFTMAX_CAUSAL = 0, CANON_XENT = 1 };
 canon_status canon_softmax_xent(const canon_order* order, int32_t mode, int64_t rows, int64_t cols, const void* x,
-                                float scale, const int32_t* targets, float inv_tokens, uint16_t* out,
-                                float* row_loss, float* mean_loss, void* stream);
+                                float scale, int64_t window, const int32_t* targets, float inv_tokens, float z_loss,
+                                uint16_t* out, float* row_loss, float* mean_loss, void* stream);
 
 /* ------------------------------------------------------------------------------------------------ */
 /* Gradient plan (R7 = Algorithm 1 with Algorithm 2 over replicas, averages by reciprocal multiply).
@@ -169,8 +191,9 @@ size_t canon_clip_grad_norm_workspace_bytes(int64_t n_tensors, const int64_t* si
 /* ------------------------------------------------------------------------------------------------ */
 /* One decoder block, forward then backward, for `batch` sequences of cfg->seq tokens (T = batch*seq).
    x, dy: fp32 [T, d_model] (block input, gradient of the block output).  w: HOST array of the six bf16
-   block tensors in the order attn_norm [d], w_qkv [3d, d], w_o [d, d], ffn_norm [d], w_gate_up [2F, d]
-   (gate rows first), w_down [d, F].  rope_cos/rope_sin: fp32 [seq, head_dim/2].  Outputs: y (block
+   block tensors in the order attn_norm [d], w_qkv [(n_heads + 2 n_kv_heads) head_dim, d], w_o [d, d],
+   ffn_norm [d], w_gate_up [2F, d] (gate rows first), w_down [d, F].  The block's attention window is
+   cfg->swa_window (the step applies the per-layer rule); embed_norm and z_loss do not apply to a block.  rope_cos/rope_sin: fp32 [seq, head_dim/2].  Outputs: y (block
    output), dx (input gradient), dw: HOST array of six fp32 gradient buffers shaped like w. */
 canon_status canon_block_fwd_bwd(const canon_order* order, const canon_model_cfg* cfg, int32_t batch,
                                  const float* x, const float* dy, const uint16_t* const* w, const float* rope_cos,
@@ -183,8 +206,9 @@ size_t canon_block_workspace_bytes(const canon_model_cfg* cfg, int32_t batch);
    `accum` microbatches (R12: rank r owns windows m with m mod N == r, micro_seqs consecutive ones per
    microbatch), run forward and backward of the whole model, then reduce the gradients and the
    microbatch losses through the plan and apply AdamW (R9).
-   params, m, v: HOST arrays of n = 3 + 6*n_layers device pointers in the declared order: embed [V, d];
-   per layer attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down; final_norm [d]; head [V, d].  params
+   params, m, v: HOST arrays of n = 3 + 6*n_layers (+1 with embed_norm) device pointers in the declared
+   order: embed [V, d]; [embed_norm [d]]; per layer attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down;
+   final_norm [d]; head [V, d].  params
    (bf16), m and v (fp32) are updated in place.  windows: device int32 [M, seq+1], M = N*accum*
    micro_seqs, each token in [0, vocab) (checked on the device: an out-of-range token makes the loss
    NaN and leaves the parameters unchanged).  loss_out: device fp32 scalar.  grads_out: NULL, or a HOST

@@ -15,7 +15,7 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libcanon.so")
 
 OK, EINVAL, EUNSUPPORTED, EDEVICE, EWORKSPACE = 0, -1, -2, -3, -4
-FWD, BWD = 0, 1
+FWD, BWD, FWD_F32 = 0, 1, 2
 SOFTMAX_CAUSAL, XENT = 0, 1
 
 
@@ -37,7 +37,9 @@ class DPPlan(ctypes.Structure):
 class ModelCfg(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
-                ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float)]
+                ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("n_kv_heads", ctypes.c_int32), ("qk_norm", ctypes.c_int32), ("embed_norm", ctypes.c_int32),
+                ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float)]
 
 
 class AdamWConsts(ctypes.Structure):
@@ -71,7 +73,7 @@ def _lib():
             "canon_gemm_strided_batched": (i32, [vp, i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64,
                                                  i64, i64, vp]),
             "canon_rownorm": (i32, [vp, i32, i64, i64, vp, vp, f32, vp, vp, vp, vp, vp, vp]),
-            "canon_softmax_xent": (i32, [vp, i32, i64, i64, vp, f32, vp, f32, vp, vp, vp, vp]),
+            "canon_softmax_xent": (i32, [vp, i32, i64, i64, vp, f32, i64, vp, f32, f32, vp, vp, vp, vp]),
             "canon_grad_accum": (i32, [vp, vp, i64, vp, vp, vp]),
             "canon_adamw": (i32, [i64, vp, vp, vp, vp, vp, vp, vp, vp]),
             "canon_block_fwd_bwd": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
@@ -146,10 +148,10 @@ def rownorm(direction, rows, cols, x, gain, eps, y=None, rstd=None, dy=None, dx=
 
 
 def softmax_xent(mode, rows, cols, x, out, scale=1.0, targets=None, inv_tokens=1.0, row_loss=None, mean_loss=None,
-                 order=ORDER_V1, stream=None):
-    _check(_lib().canon_softmax_xent(ctypes.byref(order), mode, rows, cols, _ptr(x), scale, _ptr(targets),
-                                     inv_tokens, _ptr(out), _ptr(row_loss), _ptr(mean_loss), _stream(stream)),
-           "canon_softmax_xent")
+                 order=ORDER_V1, stream=None, window=0, z_loss=0.0):
+    _check(_lib().canon_softmax_xent(ctypes.byref(order), mode, rows, cols, _ptr(x), scale, window, _ptr(targets),
+                                     inv_tokens, z_loss, _ptr(out), _ptr(row_loss), _ptr(mean_loss),
+                                     _stream(stream)), "canon_softmax_xent")
 
 
 def grad_accum(plan: DPPlan, n, grads, out, order=ORDER_V1, stream=None):

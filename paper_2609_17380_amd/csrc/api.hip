@@ -61,7 +61,10 @@ struct Carver {
 
 struct Dims {
   int64_t B, S, T, d, H, hd, F, V;
-  float eps, scale;
+  int64_t Hkv, G, kvw, N;  // key/value heads, query heads per group, key width Hkv*hd, fused projection width
+  int64_t window;          // this block's attention window (0: full causal)
+  int qk_norm;
+  float eps, scale, z_loss;
 };
 
 float attn_scale(int64_t hd) {
@@ -74,25 +77,43 @@ float attn_scale(int64_t hd) {
   return (float)(1.0 / sqrt((double)hd));
 }
 
+int64_t kv_heads(const canon_model_cfg* c) { return c->n_kv_heads > 0 ? c->n_kv_heads : c->n_heads; }
+
+// the attention window of layer l: the hybrid rule keeps every swa_full_every-th layer and the last full
+int64_t layer_window(const canon_model_cfg* c, int64_t l) {
+  if (c->swa_window == 0) return 0;
+  if ((c->swa_full_every > 0 && (l + 1) % c->swa_full_every == 0) || l == c->n_layers - 1) return 0;
+  return c->swa_window;
+}
+
 Dims dims_of(const canon_model_cfg* c, int64_t B) {
   Dims D;
   D.B = B; D.S = c->seq; D.T = B * c->seq; D.d = c->d_model; D.H = c->n_heads; D.hd = c->head_dim;
   D.F = c->d_ffn; D.V = c->vocab; D.eps = c->rms_eps; D.scale = attn_scale(c->head_dim);
+  D.Hkv = kv_heads(c); D.G = D.H / D.Hkv; D.kvw = D.Hkv * D.hd; D.N = D.d + 2 * D.kvw;
+  D.window = c->swa_window; D.qk_norm = c->qk_norm; D.z_loss = c->z_loss;
   return D;
 }
 
 bool cfg_ok(const canon_model_cfg* c) {
-  return c && c->n_layers >= 1 && c->d_model > 0 && c->n_heads > 0 && c->head_dim > 0 && (c->head_dim % 2) == 0 &&
-         (int64_t)c->n_heads * c->head_dim == c->d_model && c->d_ffn > 0 && c->vocab > 0 && c->seq > 0 &&
-         c->micro_seqs > 0 && c->vocab <= 131072 && c->d_model <= 32768 && c->seq <= 32768 &&
-         gemm_k_supported(c->vocab) && gemm_k_supported((int64_t)c->seq * c->micro_seqs) &&
-         gemm_k_supported(2 * (int64_t)c->d_ffn) && gemm_k_supported(3 * (int64_t)c->d_model);
+  if (!(c && c->n_layers >= 1 && c->d_model > 0 && c->n_heads > 0 && c->head_dim > 0 && (c->head_dim % 2) == 0 &&
+        (int64_t)c->n_heads * c->head_dim == c->d_model && c->d_ffn > 0 && c->vocab > 0 && c->seq > 0 &&
+        c->micro_seqs > 0 && c->vocab <= 131072 && c->d_model <= 32768 && c->seq <= 32768))
+    return false;
+  if (c->n_kv_heads < 0 || (c->n_kv_heads > 0 && c->n_heads % c->n_kv_heads != 0)) return false;
+  if ((c->qk_norm != 0 && c->qk_norm != 1) || (c->embed_norm != 0 && c->embed_norm != 1)) return false;
+  if (c->swa_window < 0 || c->swa_full_every < 0 || !(c->z_loss >= 0.0f) || isinf(c->z_loss)) return false;
+  const int64_t G = c->n_heads / kv_heads(c);
+  return gemm_k_supported(c->vocab) && gemm_k_supported((int64_t)c->seq * c->micro_seqs) &&
+         gemm_k_supported(2 * (int64_t)c->d_ffn) && gemm_k_supported(c->d_model + 2 * kv_heads(c) * c->head_dim) &&
+         gemm_k_supported(G * (int64_t)c->seq);
 }
 
 // activations a block saves for its backward pass
 struct LayerSave {
   uint16_t *xn, *q, *k, *v, *P, *O, *hn, *a;
   float *rstd1, *h, *rstd2, *gu;
+  float *qkv, *rq;  // QK-norm only: the projection output and the r of each q and k head row
 };
 
 void carve_save(Carver& cv, const Dims& D, LayerSave& s) {
@@ -100,8 +121,10 @@ void carve_save(Carver& cv, const Dims& D, LayerSave& s) {
   s.xn = cv.take<uint16_t>(T * d);
   s.rstd1 = cv.take<float>(T);
   s.q = cv.take<uint16_t>(T * d);
-  s.k = cv.take<uint16_t>(T * d);
-  s.v = cv.take<uint16_t>(T * d);
+  s.k = cv.take<uint16_t>(T * D.kvw);
+  s.v = cv.take<uint16_t>(T * D.kvw);
+  s.qkv = D.qk_norm ? cv.take<float>(T * D.N) : nullptr;
+  s.rq = D.qk_norm ? cv.take<float>(T * (D.H + D.Hkv)) : nullptr;
   s.P = cv.take<uint16_t>(D.B * D.H * D.S * D.S);
   s.O = cv.take<uint16_t>(T * d);
   s.h = cv.take<float>(T * d);
@@ -114,12 +137,12 @@ void carve_save(Carver& cv, const Dims& D, LayerSave& s) {
 // transient buffers shared by all layers
 struct Scratch {
   float *qkv, *scores, *tmp_d, *da, *dtmp, *dtmp2, *dh, *dq, *dk, *Dv;
-  uint16_t *dy_b, *dgu, *dO, *dS, *dqkv;
+  uint16_t *dy_b, *dgu, *dO, *dS, *dqkv, *dOh;
 };
 
 void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
   const int64_t T = D.T, d = D.d;
-  s.qkv = cv.take<float>(T * 3 * d);
+  s.qkv = cv.take<float>(T * D.N);
   s.scores = cv.take<float>(D.B * D.H * D.S * D.S);
   s.tmp_d = cv.take<float>(T * d);
   s.da = cv.take<float>(T * D.F);
@@ -127,13 +150,14 @@ void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
   s.dtmp2 = cv.take<float>(T * d);
   s.dh = cv.take<float>(T * d);
   s.dq = cv.take<float>(T * d);
-  s.dk = cv.take<float>(T * d);
+  s.dk = cv.take<float>(T * D.kvw);
   s.Dv = cv.take<float>(D.B * D.H * D.S);
   s.dy_b = cv.take<uint16_t>(T * d);
   s.dgu = cv.take<uint16_t>(T * 2 * D.F);
   s.dO = cv.take<uint16_t>(T * d);
   s.dS = cv.take<uint16_t>(D.B * D.H * D.S * D.S);
-  s.dqkv = cv.take<uint16_t>(T * 3 * d);
+  s.dqkv = cv.take<uint16_t>(T * D.N);
+  s.dOh = D.G > 1 ? cv.take<uint16_t>(T * d) : nullptr;
 }
 
 hipError_t gemm(const GemmArgs& g, hipStream_t s) { return gemm_launch(g, s); }
@@ -146,24 +170,28 @@ GemmArgs batched(GemmArgs g, const Dims& D, int64_t sa1, int64_t sa2, int64_t sb
   return g;
 }
 
-// Forward of one block: x (input, kept by the caller) -> y; activations saved in sv.
+// Forward of one block: x (input, kept by the caller) -> y; activations saved in sv.  Query head h reads
+// key/value head h / G (the GEMMs' b_group); with QK-norm the projection output is kept for the backward.
 canon_status block_forward(const Dims& D, const uint16_t* const* w, const float* cosT, const float* sinT,
                            const float* x, LayerSave& sv, Scratch& sc, float* y, hipStream_t s) {
-  const int64_t T = D.T, d = D.d, S = D.S, H = D.H, hd = D.hd, F = D.F;
+  const int64_t T = D.T, d = D.d, S = D.S, H = D.H, Hkv = D.Hkv, hd = D.hd, F = D.F, N = D.N;
+  float* qkv = D.qk_norm ? sv.qkv : sc.qkv;
   TRY(rownorm_fwd_launch(T, d, x, w[0], D.eps, sv.xn, sv.rstd1, s));
-  TRY(gemm(mk(0, 1, T, 3 * d, d, sv.xn, d, w[1], d, sc.qkv, 3 * d), s));
-  TRY(rope_qkv_launch(D.B, S, H, hd, sc.qkv, cosT, sinT, sv.q, sv.k, sv.v, s));
+  TRY(gemm(mk(0, 1, T, N, d, sv.xn, d, w[1], d, qkv, N), s));
+  TRY(rope_qkv_launch(D.B, S, H, Hkv, hd, qkv, cosT, sinT, D.qk_norm, D.eps, sv.q, sv.k, sv.v, sv.rq, s));
   {  // raw scores Q K^T, lower-triangle tiles only
-    GemmArgs g = batched(mk(0, 1, S, S, hd, sv.q, hd, sv.k, hd, sc.scores, S), D, H * S * hd, S * hd, H * S * hd,
-                         S * hd, H * S * S, S * S);
+    GemmArgs g = batched(mk(0, 1, S, S, hd, sv.q, hd, sv.k, hd, sc.scores, S), D, H * S * hd, S * hd,
+                         Hkv * S * hd, S * hd, H * S * S, S * S);
     g.tri_lower = 1;
+    g.b_group = (int32_t)D.G;
     TRY(gemm(g, s));
   }
-  TRY(softmax_causal_launch(D.B * H * S, S, sc.scores, D.scale, sv.P, s));
+  TRY(softmax_causal_launch(D.B * H * S, S, sc.scores, D.scale, D.window, sv.P, s));
   {  // O = P V (keys beyond the tile's last query are masked chunks), bf16 into [T, d]
-    GemmArgs g = batched(mk(0, 0, S, hd, S, sv.P, S, sv.v, hd, sv.O, d, 1), D, H * S * S, S * S, H * S * hd, S * hd,
-                         S * d, hd);
+    GemmArgs g = batched(mk(0, 0, S, hd, S, sv.P, S, sv.v, hd, sv.O, d, 1), D, H * S * S, S * S, Hkv * S * hd,
+                         S * hd, S * d, hd);
     g.kmode = KMODE_TRAIL;
+    g.b_group = (int32_t)D.G;
     TRY(gemm(g, s));
   }
   TRY(gemm(mk(0, 1, T, d, d, sv.O, d, w[2], d, sc.tmp_d, d), s));
@@ -176,11 +204,14 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
   return CANON_OK;
 }
 
-// Backward of one block: dy (gradient of the block output) -> dx; weight gradients into dw[0..5].
+// Backward of one block: dy (gradient of the block output) -> dx; weight gradients into dw[0..5].  The
+// gradient of a shared key (value) head is one contraction over its group's query heads and their queries,
+// heads in order: the group's dS (P) and Q (dO) rows are contiguous head after head, one GEMM with K = G*S.
 canon_status block_backward(const Dims& D, const uint16_t* const* w, const float* cosT, const float* sinT,
                             const float* x, const LayerSave& sv, Scratch& sc, const float* dy, float* dx,
                             float* const* dw, hipStream_t s) {
-  const int64_t T = D.T, d = D.d, S = D.S, H = D.H, hd = D.hd, F = D.F;
+  const int64_t T = D.T, d = D.d, S = D.S, H = D.H, Hkv = D.Hkv, G = D.G, hd = D.hd, F = D.F, N = D.N;
+  const int64_t kvw = D.kvw;
   TRY(cast_bf16_launch(T * d, dy, sc.dy_b, s));
   TRY(gemm(mk(1, 0, d, F, T, sc.dy_b, d, sv.a, F, dw[5], F), s));        // dW_down = dy^T a
   TRY(gemm(mk(0, 0, T, F, d, sc.dy_b, d, w[5], F, sc.da, F), s));        // da = dy W_down
@@ -193,36 +224,47 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
   TRY(gemm(mk(1, 0, d, d, T, sc.dy_b, d, sv.O, d, dw[2], d), s));        // dW_o = dh^T O
   TRY(gemm(mk(0, 0, T, d, d, sc.dy_b, d, w[2], d, sc.dO, d, 1), s));     // dO = dh W_o (bf16)
   TRY(attn_rowdot_launch(D.B, H, S, hd, sc.dO, sv.O, d, sc.Dv, s));      // D = rowsum(dO * O)
-  {  // dP = dO V^T on the lower-triangle tiles, turned into dS = P * (dP - D) * c in the epilogue (bf16)
-    GemmArgs g = batched(mk(0, 1, S, S, hd, sc.dO, d, sv.v, hd, sc.dS, S), D, S * d, hd, H * S * hd, S * hd,
+  {  // dP = dO V^T, turned into dS = P * (dP - D) * c in the epilogue (bf16).  One head per key/value head:
+     // the lower-triangle tiles only, since the dK and dQ GEMMs never read above the diagonal tiles.  Grouped
+     // heads: every tile (+0 above the diagonal), since dK then reads each head's dS whole.
+    GemmArgs g = batched(mk(0, 1, S, S, hd, sc.dO, d, sv.v, hd, sc.dS, S), D, S * d, hd, Hkv * S * hd, S * hd,
                          H * S * S, S * S);
-    g.tri_lower = 1;
+    g.tri_lower = G == 1 ? 1 : 0;
+    g.b_group = (int32_t)G;
     g.epi = EPI_DS;
-    g.ds_p = sv.P; g.ds_d = sc.Dv; g.ds_scale = D.scale;
+    g.ds_p = sv.P; g.ds_d = sc.Dv; g.ds_scale = D.scale; g.ds_window = D.window;
     g.ds_ldp = S; g.ds_sp1 = H * S * S; g.ds_sp2 = S * S; g.ds_sd1 = H * S; g.ds_sd2 = S;
     TRY(gemm(g, s));
   }
   {  // dQ = dS K (over keys)
-    GemmArgs g = batched(mk(0, 0, S, hd, S, sc.dS, S, sv.k, hd, sc.dq, d), D, H * S * S, S * S, H * S * hd, S * hd,
-                         S * d, hd);
+    GemmArgs g = batched(mk(0, 0, S, hd, S, sc.dS, S, sv.k, hd, sc.dq, d), D, H * S * S, S * S, Hkv * S * hd,
+                         S * hd, S * d, hd);
     g.kmode = KMODE_TRAIL;
+    g.b_group = (int32_t)G;
     TRY(gemm(g, s));
   }
-  {  // dK = dS^T Q (over queries)
-    GemmArgs g = batched(mk(1, 0, S, hd, S, sc.dS, S, sv.q, hd, sc.dk, d), D, H * S * S, S * S, H * S * hd, S * hd,
-                         S * d, hd);
-    g.kmode = KMODE_LEAD;
-    TRY(gemm(g, s));
+  // per (batch, key/value head): the group's G heads stacked along the contraction
+  auto grouped = [&](GemmArgs g, int64_t sa1, int64_t sa2, int64_t sb1, int64_t sb2, int64_t sc1, int64_t sc2) {
+    g.batch = D.B * Hkv; g.nb2 = Hkv;
+    g.sa1 = sa1; g.sa2 = sa2; g.sb1 = sb1; g.sb2 = sb2; g.sc1 = sc1; g.sc2 = sc2;
+    g.kmode = G == 1 ? KMODE_LEAD : KMODE_FULL;  // one head: queries before the key are zero chunks
+    return g;
+  };
+  // dK = sum over the group of dS^T Q (over the group's queries)
+  TRY(gemm(grouped(mk(1, 0, S, hd, G * S, sc.dS, S, sv.q, hd, sc.dk, kvw), H * S * S, G * S * S, H * S * hd,
+                   G * S * hd, S * kvw, hd), s));
+  // dV = sum over the group of P^T dO, bf16 into the value columns of dqkv
+  const uint16_t* dO_heads = sc.dO;
+  int64_t dO_s1 = S * d, dO_s2 = hd, dO_ld = d;
+  if (G > 1) {  // the group's dO rows must be contiguous: head-major copy
+    TRY(heads_major_launch(D.B, S, H, hd, sc.dO, sc.dOh, s));
+    dO_heads = sc.dOh; dO_s1 = H * S * hd; dO_s2 = G * S * hd; dO_ld = hd;
   }
-  {  // dV = P^T dO (over queries), bf16 into dqkv columns [2d, 3d)
-    GemmArgs g = batched(mk(1, 0, S, hd, S, sv.P, S, sc.dO, d, sc.dqkv + 2 * d, 3 * d, 1), D, H * S * S, S * S, S * d,
-                         hd, S * 3 * d, hd);
-    g.kmode = KMODE_LEAD;
-    TRY(gemm(g, s));
-  }
-  TRY(rope_bwd_launch(D.B, S, H, hd, sc.dq, sc.dk, cosT, sinT, sc.dqkv, s));
-  TRY(gemm(mk(1, 0, 3 * d, d, T, sc.dqkv, 3 * d, sv.xn, d, dw[1], d), s)); // dW_qkv = dqkv^T xn
-  TRY(gemm(mk(0, 0, T, d, 3 * d, sc.dqkv, 3 * d, w[1], d, sc.dtmp, d), s)); // dxn = dqkv W_qkv
+  TRY(gemm(grouped(mk(1, 0, S, hd, G * S, sv.P, S, dO_heads, dO_ld, sc.dqkv + d + kvw, N, 1), H * S * S, G * S * S,
+                   dO_s1, dO_s2, S * N, hd), s));
+  TRY(rope_bwd_launch(D.B, S, H, Hkv, hd, sc.dq, sc.dk, cosT, sinT, D.qk_norm, sv.qkv, sv.rq, sc.dqkv, s));
+  TRY(gemm(mk(1, 0, N, d, T, sc.dqkv, N, sv.xn, d, dw[1], d), s));       // dW_qkv = dqkv^T xn
+  TRY(gemm(mk(0, 0, T, d, N, sc.dqkv, N, w[1], d, sc.dtmp, d), s));      // dxn = dqkv W_qkv
   TRY(rownorm_bwd_launch(T, d, x, w[0], sv.rstd1, sc.dtmp, sc.dtmp2, dw[0], s));
   TRY(add_f32_launch(T * d, sc.dh, sc.dtmp2, dx, s));
   return CANON_OK;
@@ -235,12 +277,16 @@ int bit_length(int64_t x) {
   return b;
 }
 
+// tensors in the declared order: embed, [embed_norm], per layer attn_norm, w_qkv, w_o, ffn_norm, w_gate_up,
+// w_down, then final_norm, head
 void tensor_sizes(const canon_model_cfg* c, std::vector<int64_t>& sz, std::vector<uint8_t>& decay) {
   const int64_t d = c->d_model, F = c->d_ffn, V = c->vocab;
+  const int64_t N = d + 2 * kv_heads(c) * c->head_dim;
   sz.clear(); decay.clear();
   sz.push_back(V * d); decay.push_back(0);
+  if (c->embed_norm) { sz.push_back(d); decay.push_back(0); }
   for (int l = 0; l < c->n_layers; ++l) {
-    int64_t s6[6] = {d, 3 * d * d, d * d, d, 2 * F * d, d * F};
+    int64_t s6[6] = {d, N * d, d * d, d, 2 * F * d, d * F};
     uint8_t d6[6] = {0, 1, 1, 0, 1, 1};
     for (int i = 0; i < 6; ++i) { sz.push_back(s6[i]); decay.push_back(d6[i]); }
   }
@@ -265,6 +311,8 @@ struct StepLayout {
   float* norm_part;       // R15 block sums
   float* clip_coef;       // [1]
   int32_t* skip;          // [1]: no update this step (bad token or spike window)
+  float* x_emb;           // embedding norm: the gathered rows [T][d]
+  float* rstd_emb;        // embedding norm: r per row [T]
 };
 
 void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, int64_t P, StepLayout& L) {
@@ -298,6 +346,8 @@ void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, in
   L.norm_part = cv.take<float>(gnorm_blocks(P));
   L.clip_coef = cv.take<float>(1);
   L.skip = cv.take<int32_t>(1);
+  L.x_emb = c->embed_norm ? cv.take<float>(D.T * D.d) : nullptr;
+  L.rstd_emb = c->embed_norm ? cv.take<float>(D.T) : nullptr;
 }
 
 // Algorithm 1 driven from the host over device buffers of n floats (the gradient, or the loss with n = 1).
@@ -398,16 +448,17 @@ canon_status canon_gemm(const canon_order* order, int32_t trans_a, int32_t trans
 }
 
 canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, int64_t cols, const float* x,
-                           const uint16_t* gain, float eps, uint16_t* y, float* rstd, const float* dy, float* dx,
+                           const uint16_t* gain, float eps, void* y, float* rstd, const float* dy, float* dx,
                            float* dgain, void* stream) {
   canon_status st = check_order(order);
   if (st != CANON_OK) return st;
   if (rows < 0 || cols < 1) return CANON_EINVAL;
   if (cols > 32768 || rows > (int64_t(1) << 26)) return CANON_EUNSUPPORTED;  // row kernels stage <= 1024 chunks
   hipStream_t s = as_stream(stream);
-  if (dir == CANON_FWD) {
+  if (dir == CANON_FWD || dir == CANON_FWD_F32) {
     if (rows > 0 && (!x || !gain || !y || !rstd)) return CANON_EINVAL;
-    return dev(rownorm_fwd_launch(rows, cols, x, gain, eps, y, rstd, s));
+    if (dir == CANON_FWD_F32) return dev(rownorm_fwd_f32_launch(rows, cols, x, gain, eps, (float*)y, rstd, s));
+    return dev(rownorm_fwd_launch(rows, cols, x, gain, eps, (uint16_t*)y, rstd, s));
   }
   if (dir == CANON_BWD) {
     if (rows > 0 && (!x || !gain || !rstd || !dy || !dx)) return CANON_EINVAL;
@@ -429,23 +480,24 @@ canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, 
 }
 
 canon_status canon_softmax_xent(const canon_order* order, int32_t mode, int64_t rows, int64_t cols, const void* x,
-                                float scale, const int32_t* targets, float inv_tokens, uint16_t* out,
-                                float* row_loss, float* mean_loss, void* stream) {
+                                float scale, int64_t window, const int32_t* targets, float inv_tokens, float z_loss,
+                                uint16_t* out, float* row_loss, float* mean_loss, void* stream) {
   canon_status st = check_order(order);
   if (st != CANON_OK) return st;
-  if (rows < 0 || cols < 1) return CANON_EINVAL;
+  if (rows < 0 || cols < 1 || window < 0 || !(z_loss >= 0.0f) || isinf(z_loss)) return CANON_EINVAL;
   if (rows > (int64_t(1) << 31)) return CANON_EUNSUPPORTED;
   hipStream_t s = as_stream(stream);
   if (mode == CANON_SOFTMAX_CAUSAL) {
     if (cols > 32768) return CANON_EUNSUPPORTED;  // one wavefront stages at most 1024 chunks
     if (rows % cols != 0) return CANON_EINVAL;
     if (rows > 0 && (!x || !out)) return CANON_EINVAL;
-    return dev(softmax_causal_launch(rows, cols, (const float*)x, scale, out, s));
+    return dev(softmax_causal_launch(rows, cols, (const float*)x, scale, window, out, s));
   }
   if (mode == CANON_XENT) {
     if (rows > 0 && (!x || !targets || !out || !row_loss)) return CANON_EINVAL;
     if (rows > (int64_t(1) << 31) || cols > 131072) return CANON_EUNSUPPORTED;  // at most 4096 chunks per row
-    return dev(xent_launch(rows, cols, (const uint16_t*)x, targets, inv_tokens, out, row_loss, mean_loss, s));
+    return dev(xent_launch(rows, cols, (const uint16_t*)x, targets, inv_tokens, z_loss, out, row_loss, mean_loss,
+                           s));
   }
   return CANON_EINVAL;
 }
@@ -776,6 +828,7 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
   PlanRun gplan(P, *plan, L.g_r, L.pool);
   PlanRun lplan(1, *plan, plan->accum > 1 ? L.loss_gr : nullptr, L.loss_pool);
   const int nl = cfg->n_layers;
+  const int64_t l0 = cfg->embed_norm ? 2 : 1;  // first layer tensor
   for (int r = 0; r < R; ++r) {
     for (int k = 0; k < plan->accum; ++k) {
       // R12: windows r + R*(k*mb + s), s < mb
@@ -783,18 +836,25 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
         const int64_t mw = r + (int64_t)R * (k * mb + si);
         TRY(hipMemcpyAsync(L.win + si * S1, windows + mw * S1, sizeof(int32_t) * S1, hipMemcpyDeviceToDevice, s));
       }
-      TRY(embed_gather_launch(mb, D.S, D.d, L.win, S1, params[0], D.V, L.xs[0], s));
+      if (cfg->embed_norm) {  // the embedding norm's fp32 output is the first block's input
+        TRY(embed_gather_launch(mb, D.S, D.d, L.win, S1, params[0], D.V, L.x_emb, s));
+        TRY(rownorm_fwd_f32_launch(D.T, D.d, L.x_emb, params[1], D.eps, L.xs[0], L.rstd_emb, s));
+      } else {
+        TRY(embed_gather_launch(mb, D.S, D.d, L.win, S1, params[0], D.V, L.xs[0], s));
+      }
       TRY(labels_launch(mb, D.S, L.win, S1, L.lab, s));
       for (int l = 0; l < nl; ++l) {
         const uint16_t* w[6];
-        for (int i = 0; i < 6; ++i) w[i] = params[1 + 6 * l + i];
-        st = block_forward(D, w, rope_cos, rope_sin, L.xs[l], L.saves[l], L.sc, L.xs[l + 1], s);
+        for (int i = 0; i < 6; ++i) w[i] = params[l0 + 6 * l + i];
+        Dims Dl = D;
+        Dl.window = layer_window(cfg, l);
+        st = block_forward(Dl, w, rope_cos, rope_sin, L.xs[l], L.saves[l], L.sc, L.xs[l + 1], s);
         if (st != CANON_OK) return st;
       }
-      const int64_t i_fn = 1 + 6 * nl, i_head = 2 + 6 * nl;
+      const int64_t i_fn = l0 + 6 * nl, i_head = i_fn + 1;
       TRY(rownorm_fwd_launch(D.T, D.d, L.xs[nl], params[i_fn], D.eps, L.xf, L.rstdf, s));
       TRY(gemm(mk(0, 1, D.T, D.V, D.d, L.xf, D.d, params[i_head], D.d, L.logits, D.V, 1), s));
-      TRY(xent_launch(D.T, D.V, L.logits, L.lab, invT, L.dlogits, L.row_loss, L.loss_mb, s));
+      TRY(xent_launch(D.T, D.V, L.logits, L.lab, invT, D.z_loss, L.dlogits, L.row_loss, L.loss_mb, s));
       TRY(gemm(mk(1, 0, D.V, D.d, D.T, L.dlogits, D.V, L.xf, D.d, L.grad + off[i_head], D.d), s));
       TRY(gemm(mk(0, 0, D.T, D.d, D.V, L.dlogits, D.V, params[i_head], D.d, L.dxf, D.d), s));
       TRY(rownorm_bwd_launch(D.T, D.d, L.xs[nl], params[i_fn], L.rstdf, L.dxf, L.dxA, L.grad + off[i_fn], s));
@@ -804,11 +864,17 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
         const uint16_t* w[6];
         float* dw[6];
         for (int i = 0; i < 6; ++i) {
-          w[i] = params[1 + 6 * l + i];
-          dw[i] = L.grad + off[1 + 6 * l + i];
+          w[i] = params[l0 + 6 * l + i];
+          dw[i] = L.grad + off[l0 + 6 * l + i];
         }
-        st = block_backward(D, w, rope_cos, rope_sin, L.xs[l], L.saves[l], L.sc, dcur, dnext, dw, s);
+        Dims Dl = D;
+        Dl.window = layer_window(cfg, l);
+        st = block_backward(Dl, w, rope_cos, rope_sin, L.xs[l], L.saves[l], L.sc, dcur, dnext, dw, s);
         if (st != CANON_OK) return st;
+        float* t = dcur; dcur = dnext; dnext = t;
+      }
+      if (cfg->embed_norm) {  // back through the embedding norm to the gathered rows
+        TRY(rownorm_bwd_launch(D.T, D.d, L.x_emb, params[1], L.rstd_emb, dcur, dnext, L.grad + off[1], s));
         float* t = dcur; dcur = dnext; dnext = t;
       }
       TRY(embed_bwd_launch(mb, D.S, D.d, L.win, S1, D.V, dcur, L.grad + off[0], L.embed_scratch, s));

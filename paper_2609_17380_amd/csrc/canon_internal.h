@@ -17,16 +17,18 @@ struct GemmArgs {
   int64_t sa1, sa2, sb1, sb2, sc1, sc2;
   int64_t nb2, batch;
   int32_t trans_a, trans_b, out_bf16, kmode, tri_lower;
-  int32_t vec;  // set by the launcher: 16-byte operand loads allowed
+  int32_t vec;      // set by the launcher: 16-byte operand loads allowed
+  int32_t b_group;  // > 1: B's inner batch offset is (z2 / b_group) * sb2 (grouped key/value heads)
   // EPI_DS epilogue (attention backward, R5): the finished value d = dP[i][j] of a square per-head matrix
-  // becomes dS[i][j] = bf16(RN(RN(P[i][j] * RN(d - D[i])) * ds_scale)) for j <= i, 0 above the diagonal,
-  // written as bf16 into C.  P: bf16 with leading dim ds_ldp and batch offsets ds_sp1/ds_sp2; D: fp32
+  // becomes dS[i][j] = bf16(RN(RN(P[i][j] * RN(d - D[i])) * ds_scale)) for j <= i (and j > i - ds_window
+  // when ds_window > 0), +0 elsewhere, written as bf16 into C.  P: bf16 with leading dim ds_ldp and batch offsets ds_sp1/ds_sp2; D: fp32
   // per row with batch offsets ds_sd1/ds_sd2.
   int32_t epi;
   const uint16_t* ds_p;
   const float* ds_d;
   float ds_scale;
   int64_t ds_ldp, ds_sp1, ds_sp2, ds_sd1, ds_sd2;
+  int64_t ds_window;
 };
 enum { EPI_NONE = 0, EPI_DS = 1 };
 
@@ -88,21 +90,35 @@ hipError_t clip_scale_launch(int64_t n, float* g, const float* coef, hipStream_t
 // rows.hip
 hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps,
                               uint16_t* y, float* rstd, hipStream_t s);
+// the same with y kept fp32 (the embedding norm)
+hipError_t rownorm_fwd_f32_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps,
+                                  float* y, float* rstd, hipStream_t s);
 hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
                               const float* dy, float* dx, float* dgain, hipStream_t s);
-hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, uint16_t* probs,
-                                 hipStream_t s);
+// window > 0: query i sees keys i - window < j <= i
+hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, int64_t window,
+                                 uint16_t* probs, hipStream_t s);
 hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets,
-                       float inv_tokens, uint16_t* dlogits, float* row_loss, float* mean_loss, hipStream_t s);
+                       float inv_tokens, float z_loss, uint16_t* dlogits, float* row_loss, float* mean_loss,
+                       hipStream_t s);
 hipError_t quant_scales_launch(int64_t rows, int64_t cols, const uint16_t* w, float* scale, hipStream_t s);
 hipError_t attn_rowdot_launch(int64_t B, int64_t H, int64_t S, int64_t hd, const uint16_t* dO, const uint16_t* O,
                               int64_t ld, float* D, hipStream_t s);
 
 // elementwise.hip
-hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* qkv, const float* cosT,
-                           const float* sinT, uint16_t* q, uint16_t* k, uint16_t* v, hipStream_t s);
-hipError_t rope_bwd_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* dq, const float* dk,
-                           const float* cosT, const float* sinT, uint16_t* dqkv, hipStream_t s);
+// qkv [T][(H + 2 Hkv) hd] -> q [B][H][S][hd], k and v [B][Hkv][S][hd] (bf16); with qk_norm, the gain-free
+// per-head RMSNorm first, its r per head row into rq [T][H + Hkv]
+hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd, const float* qkv,
+                           const float* cosT, const float* sinT, int qk_norm, float eps, uint16_t* q, uint16_t* k,
+                           uint16_t* v, float* rq, hipStream_t s);
+// dq [T][H hd], dk [T][Hkv hd] -> the q and k columns of dqkv [T][(H + 2 Hkv) hd] (bf16); with qk_norm also
+// the norm's backward (qkv: the forward's projection output, rq its r)
+hipError_t rope_bwd_launch(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd, const float* dq, const float* dk,
+                           const float* cosT, const float* sinT, int qk_norm, const float* qkv, const float* rq,
+                           uint16_t* dqkv, hipStream_t s);
+// [T][H hd] bf16 -> [B][H][S][hd]
+hipError_t heads_major_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const uint16_t* src, uint16_t* dst,
+                              hipStream_t s);
 hipError_t swiglu_fwd_launch(int64_t T, int64_t F, const float* gu, uint16_t* a, hipStream_t s);
 hipError_t swiglu_bwd_launch(int64_t T, int64_t F, const float* gu, const float* da, uint16_t* dgu, hipStream_t s);
 hipError_t add_f32_launch(int64_t n, const float* a, const float* b, float* out, hipStream_t s);

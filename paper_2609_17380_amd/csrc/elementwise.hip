@@ -9,73 +9,201 @@ namespace canon {
 
 static inline unsigned blocks_for(int64_t n) { return (unsigned)((n + 255) / 256); }
 
-// qkv fp32 [B*S, 3d] -> q, k (rotated) and v as bf16 [B, H, S, hd].
-__global__ void rope_qkv_kernel(int64_t B, int64_t S, int64_t H, int64_t hd, const float* __restrict__ qkv,
-                                const float* __restrict__ cosT, const float* __restrict__ sinT,
-                                uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v) {
-  const int64_t hh = hd / 2;
+// The fused projection qkv [T][N], N = (H + 2 Hkv) hd, holds H query heads, then Hkv key heads, then Hkv
+// value heads.  Head slot u < H + Hkv names query head u (u < H) or key head u - H; both are rotated at
+// their position and stored bf16 head-major (q [B][H][S][hd], k and v [B][Hkv][S][hd]); the key slots also
+// copy their value head.
+__global__ void rope_qkv_kernel(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd,
+                                const float* __restrict__ qkv, const float* __restrict__ cosT,
+                                const float* __restrict__ sinT, uint16_t* __restrict__ q, uint16_t* __restrict__ k,
+                                uint16_t* __restrict__ v) {
+  const int64_t hh = hd / 2, U = H + Hkv, N = (H + 2 * Hkv) * hd;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= B * S * H * hh) return;
-  const int64_t i = idx % hh, h = (idx / hh) % H, t = idx / (hh * H);
+  if (idx >= B * S * U * hh) return;
+  const int64_t i = idx % hh, u = (idx / hh) % U, t = idx / (hh * U);
   const int64_t b = t / S, s = t % S;
-  const int64_t d = H * hd;
   const float c = cosT[s * hh + i], sn = sinT[s * hh + i];
-  const float* row = qkv + t * 3 * d + h * hd;
-  const int64_t o = ((b * H + h) * S + s) * hd;
-  {
-    float x1 = row[i], x2 = row[i + hh];
-    float a = x1 * c, bq = x2 * sn;
-    float e = x2 * c, f = x1 * sn;
-    q[o + i] = f32_to_bf16(a - bq);
-    q[o + i + hh] = f32_to_bf16(e + f);
+  const float* row = qkv + t * N + u * hd;
+  uint16_t* out = u < H ? q + ((b * H + u) * S + s) * hd : k + ((b * Hkv + (u - H)) * S + s) * hd;
+  float x1 = row[i], x2 = row[i + hh];
+  float a = x1 * c, bq = x2 * sn;
+  float e = x2 * c, f = x1 * sn;
+  out[i] = f32_to_bf16(a - bq);
+  out[i + hh] = f32_to_bf16(e + f);
+  if (u >= H) {
+    const float* vr = row + Hkv * hd;
+    uint16_t* vo = v + ((b * Hkv + (u - H)) * S + s) * hd;
+    vo[i] = f32_to_bf16(vr[i]);
+    vo[i + hh] = f32_to_bf16(vr[i + hh]);
   }
-  {
-    float x1 = row[d + i], x2 = row[d + i + hh];
-    float a = x1 * c, bq = x2 * sn;
-    float e = x2 * c, f = x1 * sn;
-    k[o + i] = f32_to_bf16(a - bq);
-    k[o + i + hh] = f32_to_bf16(e + f);
-  }
-  v[o + i] = f32_to_bf16(row[2 * d + i]);
-  v[o + i + hh] = f32_to_bf16(row[2 * d + i + hh]);
 }
 
-hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* qkv, const float* cosT,
-                           const float* sinT, uint16_t* q, uint16_t* k, uint16_t* v, hipStream_t s) {
-  const int64_t n = B * S * H * (hd / 2);
+// The same with the gain-free QK-norm before the rotation: one thread per head row.  r = 1 / sqrt(RN(ms +
+// eps)) with ms = RN(R1(x^2) * RN(1/hd)) (chains of 32, Algorithm 2), saved per row in rq [T][H + Hkv];
+// the normalised row RN(x * r) stays fp32 into the rotation.
+__global__ void rope_qkv_norm_kernel(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd,
+                                     const float* __restrict__ qkv, const float* __restrict__ cosT,
+                                     const float* __restrict__ sinT, float eps, float inv_hd,
+                                     uint16_t* __restrict__ q, uint16_t* __restrict__ k, uint16_t* __restrict__ v,
+                                     float* __restrict__ rq) {
+  const int64_t hh = hd / 2, U = H + Hkv, N = (H + 2 * Hkv) * hd;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= B * S * U) return;
+  const int64_t u = idx % U, t = idx / U;
+  const int64_t b = t / S, s = t % S;
+  const float* row = qkv + t * N + u * hd;
+  LocalFoldN<8> fold;
+  for (int64_t c0 = 0; c0 < hd; c0 += kChunk) {
+    const int64_t c1 = c0 + kChunk < hd ? c0 + kChunk : hd;
+    float acc = 0.0f;
+    for (int64_t j = c0; j < c1; ++j) {
+      const float xj = row[j];
+      acc = acc + xj * xj;
+    }
+    fold.push(acc);
+  }
+  const float ms = fold.result() * inv_hd;
+  const float var = ms + eps;
+  const float r = 1.0f / __builtin_sqrtf(var);
+  rq[idx] = r;
+  uint16_t* out = u < H ? q + ((b * H + u) * S + s) * hd : k + ((b * Hkv + (u - H)) * S + s) * hd;
+  for (int64_t i = 0; i < hh; ++i) {
+    const float c = cosT[s * hh + i], sn = sinT[s * hh + i];
+    const float x1 = row[i] * r, x2 = row[i + hh] * r;
+    float a = x1 * c, bq = x2 * sn;
+    float e = x2 * c, f = x1 * sn;
+    out[i] = f32_to_bf16(a - bq);
+    out[i + hh] = f32_to_bf16(e + f);
+  }
+  if (u >= H) {
+    const float* vr = row + Hkv * hd;
+    uint16_t* vo = v + ((b * Hkv + (u - H)) * S + s) * hd;
+    for (int64_t j = 0; j < hd; ++j) vo[j] = f32_to_bf16(vr[j]);
+  }
+}
+
+hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd, const float* qkv,
+                           const float* cosT, const float* sinT, int qk_norm, float eps, uint16_t* q, uint16_t* k,
+                           uint16_t* v, float* rq, hipStream_t s) {
+  if (qk_norm) {
+    const int64_t n = B * S * (H + Hkv);
+    if (n == 0) return hipSuccess;
+    const float inv_hd = (float)(1.0 / (double)hd);  // RN32(1/hd)
+    hipLaunchKernelGGL(rope_qkv_norm_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, Hkv, hd, qkv, cosT, sinT,
+                       eps, inv_hd, q, k, v, rq);
+    return hipGetLastError();
+  }
+  const int64_t n = B * S * (H + Hkv) * (hd / 2);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_qkv_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, hd, qkv, cosT, sinT, q, k, v);
+  hipLaunchKernelGGL(rope_qkv_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, Hkv, hd, qkv, cosT, sinT, q, k,
+                     v);
   return hipGetLastError();
 }
 
-// transposed rotation of the q and k gradients ([B*S, d] fp32) into dqkv bf16 [B*S, 3d] columns [0, 2d).
-__global__ void rope_bwd_kernel(int64_t B, int64_t S, int64_t H, int64_t hd, const float* __restrict__ dq,
-                                const float* __restrict__ dk, const float* __restrict__ cosT,
-                                const float* __restrict__ sinT, uint16_t* __restrict__ dqkv) {
-  const int64_t hh = hd / 2;
+// Transposed rotation of the q and k gradients (dq [T][H hd], dk [T][Hkv hd], fp32) into the q and k columns
+// of dqkv (bf16 [T][N]).
+__global__ void rope_bwd_kernel(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd,
+                                const float* __restrict__ dq, const float* __restrict__ dk,
+                                const float* __restrict__ cosT, const float* __restrict__ sinT,
+                                uint16_t* __restrict__ dqkv) {
+  const int64_t hh = hd / 2, U = H + Hkv, N = (H + 2 * Hkv) * hd;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= B * S * H * hh) return;
-  const int64_t i = idx % hh, h = (idx / hh) % H, t = idx / (hh * H);
+  if (idx >= B * S * U * hh) return;
+  const int64_t i = idx % hh, u = (idx / hh) % U, t = idx / (hh * U);
   const int64_t s = t % S;
-  const int64_t d = H * hd;
   const float c = cosT[s * hh + i], sn = sinT[s * hh + i];
-  const float* src[2] = {dq, dk};
-#pragma unroll
-  for (int w = 0; w < 2; ++w) {
-    const float* g = src[w] + t * d + h * hd;
-    float g1 = g[i], g2 = g[i + hh];
-    float a = g1 * c, b = g2 * sn;
-    float e = g2 * c, f = g1 * sn;
-    dqkv[t * 3 * d + w * d + h * hd + i] = f32_to_bf16(a + b);
-    dqkv[t * 3 * d + w * d + h * hd + i + hh] = f32_to_bf16(e - f);
+  const float* g = u < H ? dq + t * H * hd + u * hd : dk + t * Hkv * hd + (u - H) * hd;
+  float g1 = g[i], g2 = g[i + hh];
+  float a = g1 * c, b = g2 * sn;
+  float e = g2 * c, f = g1 * sn;
+  dqkv[t * N + u * hd + i] = f32_to_bf16(a + b);
+  dqkv[t * N + u * hd + i + hh] = f32_to_bf16(e - f);
+}
+
+// element j of the transposed rotation of head row g at position s
+__device__ __forceinline__ float rope_bwd_elem(const float* g, const float* cs, const float* sn, int64_t hh,
+                                               int64_t j) {
+  if (j < hh) {
+    const float a = g[j] * cs[j], b = g[j + hh] * sn[j];
+    return a + b;
+  }
+  const int64_t i = j - hh;
+  const float e = g[j] * cs[i], f = g[i] * sn[i];
+  return e - f;
+}
+
+// With QK-norm: the transposed rotation, then R3's input gradient without a gain (dot = R1(gy * x), q =
+// RN(RN(RN(r r) r) RN(dot / hd)), dx = RN(RN(r gy) - RN(x q))), one thread per head row.
+__global__ void rope_bwd_norm_kernel(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd,
+                                     const float* __restrict__ dq, const float* __restrict__ dk,
+                                     const float* __restrict__ qkv, const float* __restrict__ rq,
+                                     const float* __restrict__ cosT, const float* __restrict__ sinT, float inv_hd,
+                                     uint16_t* __restrict__ dqkv) {
+  const int64_t hh = hd / 2, U = H + Hkv, N = (H + 2 * Hkv) * hd;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= B * S * U) return;
+  const int64_t u = idx % U, t = idx / U, s = t % S;
+  const float* g = u < H ? dq + t * H * hd + u * hd : dk + t * Hkv * hd + (u - H) * hd;
+  const float* x = qkv + t * N + u * hd;
+  const float* cs = cosT + s * hh;
+  const float* sn = sinT + s * hh;
+  const float r = rq[idx];
+  LocalFoldN<8> fold;
+  for (int64_t c0 = 0; c0 < hd; c0 += kChunk) {
+    const int64_t c1 = c0 + kChunk < hd ? c0 + kChunk : hd;
+    float acc = 0.0f;
+    for (int64_t j = c0; j < c1; ++j) {
+      const float p = rope_bwd_elem(g, cs, sn, hh, j) * x[j];
+      acc = acc + p;
+    }
+    fold.push(acc);
+  }
+  const float dot = fold.result();
+  const float r2 = r * r;
+  const float r3 = r2 * r;
+  const float dm = dot * inv_hd;
+  const float qc = r3 * dm;
+  for (int64_t j = 0; j < hd; ++j) {
+    const float gy = rope_bwd_elem(g, cs, sn, hh, j);
+    const float a = r * gy, b = x[j] * qc;
+    dqkv[t * N + u * hd + j] = f32_to_bf16(a - b);
   }
 }
 
-hipError_t rope_bwd_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const float* dq, const float* dk,
-                           const float* cosT, const float* sinT, uint16_t* dqkv, hipStream_t s) {
-  const int64_t n = B * S * H * (hd / 2);
+hipError_t rope_bwd_launch(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd, const float* dq, const float* dk,
+                           const float* cosT, const float* sinT, int qk_norm, const float* qkv, const float* rq,
+                           uint16_t* dqkv, hipStream_t s) {
+  if (qk_norm) {
+    const int64_t n = B * S * (H + Hkv);
+    if (n == 0) return hipSuccess;
+    const float inv_hd = (float)(1.0 / (double)hd);
+    hipLaunchKernelGGL(rope_bwd_norm_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, Hkv, hd, dq, dk, qkv, rq,
+                       cosT, sinT, inv_hd, dqkv);
+    return hipGetLastError();
+  }
+  const int64_t n = B * S * (H + Hkv) * (hd / 2);
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(rope_bwd_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, hd, dq, dk, cosT, sinT, dqkv);
+  hipLaunchKernelGGL(rope_bwd_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, Hkv, hd, dq, dk, cosT, sinT,
+                     dqkv);
+  return hipGetLastError();
+}
+
+// dO [T][H hd] (token-major) -> head-major [B][H][S][hd], bf16: the grouped heads' value gradient reads a
+// group's dO as one stacked operand
+__global__ void heads_major_kernel(int64_t B, int64_t S, int64_t H, int64_t hd, const uint16_t* __restrict__ src,
+                                   uint16_t* __restrict__ dst) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= B * S * H * hd) return;
+  const int64_t j = idx % hd, h = (idx / hd) % H, t = idx / (hd * H);
+  const int64_t b = t / S, s = t % S;
+  dst[((b * H + h) * S + s) * hd + j] = src[idx];
+}
+
+hipError_t heads_major_launch(int64_t B, int64_t S, int64_t H, int64_t hd, const uint16_t* src, uint16_t* dst,
+                              hipStream_t s) {
+  const int64_t n = B * S * H * hd;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(heads_major_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, hd, src, dst);
   return hipGetLastError();
 }
 

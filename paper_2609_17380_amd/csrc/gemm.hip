@@ -320,7 +320,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   const int64_t z = blockIdx.z;
   const int64_t z1 = z / g.nb2, z2 = z % g.nb2;
   const uint16_t* A = g.a + z1 * g.sa1 + z2 * g.sa2;
-  const uint16_t* B = g.b + z1 * g.sb1 + z2 * g.sb2;
+  const uint16_t* B = g.b + z1 * g.sb1 + (g.b_group > 1 ? z2 / g.b_group : z2) * g.sb2;
   const bool vec = g.vec != 0;
   const bool tile_in = vec && row0 + BM <= g.m && col0 + BN <= g.n;
 
@@ -445,7 +445,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
       const int64_t j = ccol0 + blk * 32 + (lane & 31);
       if (i < g.m && j < g.n) {
         uint16_t o = 0;
-        if (j <= i) {
+        if (j <= i && (g.ds_window == 0 || j > i - g.ds_window)) {
           const float t = r[v] - Dv[i];
           const float u = bf16_to_f32(P[i * g.ds_ldp + j]) * t;
           o = f32_to_bf16(u * g.ds_scale);

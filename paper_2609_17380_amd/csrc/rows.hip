@@ -181,10 +181,10 @@ __device__ __forceinline__ float reg_row_sum(WaveStage& st, const float (&e)[kRe
 }
 
 // RMSNorm forward: one wavefront per row, 4 rows per workgroup.
-template <int W>
+template <int W, bool F32>
 __global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
                                                           const uint16_t* __restrict__ gain, float eps, float inv_d,
-                                                          uint16_t* __restrict__ y, float* __restrict__ rstd) {
+                                                          void* __restrict__ y, float* __restrict__ rstd) {
   __shared__ WaveStage st[4];
   extern __shared__ float dyn[];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -206,12 +206,15 @@ __global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t 
     uint16_t h[W];
     ldf<W>(xr + k, xv);
     ldb<W>(gain + k, gv);
+    float o[W];
 #pragma unroll
     for (int i = 0; i < W; ++i) {
       float xn = xv[i] * r;
-      h[i] = f32_to_bf16(xn * gv[i]);
+      o[i] = xn * gv[i];
+      h[i] = f32_to_bf16(o[i]);
     }
-    stb<W>(y + row * cols + k, h);
+    if (F32) stf<W>((float*)y + row * cols + k, o);
+    else stb<W>((uint16_t*)y + row * cols + k, h);
   }
 }
 
@@ -263,9 +266,10 @@ __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t 
 }
 
 // RMSNorm forward and backward with register-resident rows (same arithmetic as the kernels above).
+template <bool F32>
 __global__ __launch_bounds__(256) void rownorm_fwd_reg_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
                                                               const uint16_t* __restrict__ gain, float eps,
-                                                              float inv_d, uint16_t* __restrict__ y,
+                                                              float inv_d, void* __restrict__ y,
                                                               float* __restrict__ rstd) {
   __shared__ WaveStage st[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -293,15 +297,17 @@ __global__ __launch_bounds__(256) void rownorm_fwd_reg_kernel(int64_t rows, int6
   for (int q = 0; q < kRegQ; ++q) {
     const int64_t j = 256 * q + 4 * lane;
     if (j < cols) {
-      float gv[4];
+      float gv[4], o[4];
       uint16_t h[4];
       ldb<4>(gain + j, gv);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         float xn = xv[q][t] * r;
-        h[t] = f32_to_bf16(xn * gv[t]);
+        o[t] = xn * gv[t];
+        h[t] = f32_to_bf16(o[t]);
       }
-      stb<4>(y + row * cols + j, h);
+      if (F32) stf<4>((float*)y + row * cols + j, o);
+      else stb<4>((uint16_t*)y + row * cols + j, h);
     }
   }
 }
@@ -417,19 +423,33 @@ __global__ __launch_bounds__(1024) void rownorm_dgain_fold_kernel(int64_t rows, 
 
 static inline bool al(const void* p, unsigned a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
-hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps, uint16_t* y,
-                              float* rstd, hipStream_t s) {
+template <bool F32>
+static hipError_t rownorm_fwd_any(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps,
+                                  void* y, float* rstd, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const float inv_d = (float)(1.0 / (double)cols);  // RN32(1/cols), correctly rounded
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
-  if (cols % 4 == 0 && cols <= kRegCols && al(x, 16) && al(gain, 8) && al(y, 8))
-    hipLaunchKernelGGL(rownorm_fwd_reg_kernel, grid, dim3(256), 0, s, rows, cols, x, gain, eps, inv_d, y, rstd);
-  else if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(y, 8))
-    hipLaunchKernelGGL(rownorm_fwd_kernel<4>, grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y, rstd);
+  const unsigned ya = F32 ? 16 : 8;
+  if (cols % 4 == 0 && cols <= kRegCols && al(x, 16) && al(gain, 8) && al(y, ya))
+    hipLaunchKernelGGL(rownorm_fwd_reg_kernel<F32>, grid, dim3(256), 0, s, rows, cols, x, gain, eps, inv_d, y, rstd);
+  else if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(y, ya))
+    hipLaunchKernelGGL((rownorm_fwd_kernel<4, F32>), grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y,
+                       rstd);
   else
-    hipLaunchKernelGGL(rownorm_fwd_kernel<1>, grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y, rstd);
+    hipLaunchKernelGGL((rownorm_fwd_kernel<1, F32>), grid, dim3(256), lds, s, rows, cols, x, gain, eps, inv_d, y,
+                       rstd);
   return hipGetLastError();
+}
+
+hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps, uint16_t* y,
+                              float* rstd, hipStream_t s) {
+  return rownorm_fwd_any<false>(rows, cols, x, gain, eps, y, rstd, s);
+}
+
+hipError_t rownorm_fwd_f32_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps,
+                                  float* y, float* rstd, hipStream_t s) {
+  return rownorm_fwd_any<true>(rows, cols, x, gain, eps, y, rstd, s);
 }
 
 // dx doubles as the scratch of the dgain chunk partials (ceil(rows/32) x cols floats <= rows x cols), so
@@ -497,10 +517,12 @@ hipError_t quant_scales_launch(int64_t rows, int64_t cols, const uint16_t* w, fl
 }
 
 // ------------------------------------------------------------------------------------------------
-// Causal softmax of raw scores: row r is query i = r mod cols; one wavefront per row, coalesced.
+// Causal softmax of raw scores: row r is query i = r mod cols; one wavefront per row, coalesced.  With
+// window > 0 query i sees keys j0 = max(0, i - window + 1) .. i (the hybrid attention's windowed layers).
 template <int W>
 __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64_t cols, const float* __restrict__ raw,
-                                                             float scale, uint16_t* __restrict__ probs) {
+                                                             float scale, int64_t window,
+                                                             uint16_t* __restrict__ probs) {
   __shared__ WaveStage st[4];
   extern __shared__ float dyn[];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -508,6 +530,7 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
   if (row >= rows) return;
   const int64_t nc = (cols + kChunk - 1) / kChunk;
   const int64_t i = row % cols;
+  const int64_t j0 = (window > 0 && i - window + 1 > 0) ? i - window + 1 : 0;
   const float* rr = raw + row * cols;
   float m = -__builtin_inff();
   for (int64_t j = (int64_t)lane * W; j <= i; j += 64 * W) {
@@ -515,7 +538,7 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
     ldf<W>(rr + j, v);
 #pragma unroll
     for (int t = 0; t < W; ++t)
-      if (j + t <= i) m = fmaxf(m, v[t] * scale);
+      if ((j + t <= i && j + t >= j0)) m = fmaxf(m, v[t] * scale);
   }
   m = wave_max(m);
   // masked keys enter the chain as +0 terms
@@ -525,7 +548,7 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
 #pragma unroll
     for (int t = 0; t < W; ++t) {
       float e = 0.0f;
-      if (j + t <= i) {
+      if ((j + t <= i && j + t >= j0)) {
         float sc = v[t] * scale;
         e = cexp(sc - m);
       }
@@ -541,7 +564,7 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
 #pragma unroll
       for (int t = 0; t < W; ++t) {
         o[t] = 0;
-        if (j + t <= i) {
+        if ((j + t <= i && j + t >= j0)) {
           float sc = v[t] * scale;
           float e = cexp(sc - m);
           o[t] = f32_to_bf16(e * rcp);
@@ -557,12 +580,13 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
 
 __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, int64_t cols,
                                                                  const float* __restrict__ raw, float scale,
-                                                                 uint16_t* __restrict__ probs) {
+                                                                 int64_t window, uint16_t* __restrict__ probs) {
   __shared__ WaveStage st[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
   if (row >= rows) return;
   const int64_t i = row % cols;
+  const int64_t j0 = (window > 0 && i - window + 1 > 0) ? i - window + 1 : 0;
   const float* rr = raw + row * cols;
   float e[kRegQ][4];
 #pragma unroll
@@ -578,7 +602,7 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
       const int64_t j = 256 * q + 4 * lane + t;
-      if (j < cols && j <= i) m = fmaxf(m, e[q][t] * scale);
+      if (j < cols && j <= i && j >= j0) m = fmaxf(m, e[q][t] * scale);
     }
   m = wave_max(m);
   // masked keys enter the chain as +0 terms
@@ -588,7 +612,7 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
     for (int t = 0; t < 4; ++t) {
       const int64_t j = 256 * q + 4 * lane + t;
       float x = 0.0f;
-      if (j < cols && j <= i) {
+      if (j < cols && j <= i && j >= j0) {
         float sc = e[q][t] * scale;
         x = cexp(sc - m);
       }
@@ -602,23 +626,23 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
     if (j < cols) {
       uint16_t o[4];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) o[t] = (j + t <= i) ? f32_to_bf16(e[q][t] * rcp) : (uint16_t)0;
+      for (int t = 0; t < 4; ++t) o[t] = ((j + t <= i && j + t >= j0)) ? f32_to_bf16(e[q][t] * rcp) : (uint16_t)0;
       stb<4>(probs + row * cols + j, o);
     }
   }
 }
 
-hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, uint16_t* probs,
-                                 hipStream_t s) {
+hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, int64_t window,
+                                 uint16_t* probs, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
   if (cols % 4 == 0 && cols <= kRegCols && al(raw, 16) && al(probs, 8))
-    hipLaunchKernelGGL(softmax_causal_reg_kernel, grid, dim3(256), 0, s, rows, cols, raw, scale, probs);
+    hipLaunchKernelGGL(softmax_causal_reg_kernel, grid, dim3(256), 0, s, rows, cols, raw, scale, window, probs);
   else if (cols % 4 == 0 && al(raw, 16) && al(probs, 8))
-    hipLaunchKernelGGL(softmax_causal_kernel<4>, grid, dim3(256), lds, s, rows, cols, raw, scale, probs);
+    hipLaunchKernelGGL(softmax_causal_kernel<4>, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs);
   else
-    hipLaunchKernelGGL(softmax_causal_kernel<1>, grid, dim3(256), lds, s, rows, cols, raw, scale, probs);
+    hipLaunchKernelGGL(softmax_causal_kernel<1>, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs);
   return hipGetLastError();
 }
 
@@ -631,7 +655,8 @@ hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, f
 template <int W>
 __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, const uint16_t* __restrict__ logits,
                                                    const int32_t* __restrict__ targets, float inv_tokens,
-                                                   uint16_t* __restrict__ dlogits, float* __restrict__ row_loss) {
+                                                   float z_loss, float z2, uint16_t* __restrict__ dlogits,
+                                                   float* __restrict__ row_loss) {
   __shared__ WaveStage st[4];
   extern __shared__ float parts[];
   __shared__ float red[4];
@@ -664,9 +689,20 @@ __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, 
   const float S = block_fold(f.result(), (nc + G - 1) / G);
   const int32_t y = targets[row];
   const bool valid = y >= 0 && y < vocab;
+  // z-loss (weight z_loss, z2 = RN(2 z_loss)): the row loss gains RN(z_loss * RN(lse^2)) and every
+  // probability is scaled by RN(1 + RN(z2 * lse)) before the target is subtracted
+  const float lse = m + clog(S);
+  const bool zl = z_loss != 0.0f;
+  const float zt = z2 * lse;
+  const float pscale = 1.0f + zt;
   if (threadIdx.x == 0) {
-    float lse = m + clog(S);
-    row_loss[row] = valid ? lse - bf16_to_f32(lr[y]) : __builtin_nanf("");
+    float ce = lse - bf16_to_f32(lr[valid ? y : 0]);
+    if (zl) {
+      const float l2 = lse * lse;
+      const float zterm = z_loss * l2;
+      ce = ce + zterm;
+    }
+    row_loss[row] = valid ? ce : __builtin_nanf("");
   }
   const float rcp = 1.0f / S;
   if (dlogits) {
@@ -678,6 +714,7 @@ __global__ __launch_bounds__(256) void xent_kernel(int64_t rows, int64_t vocab, 
       for (int i = 0; i < W; ++i) {
         float e = cexp(fv[i] - m);
         float pr = e * rcp;
+        if (zl) pr = pr * pscale;
         float q = pr - ((j + i) == y ? 1.0f : 0.0f);
         h[i] = f32_to_bf16(q * inv_tokens);
       }
@@ -697,7 +734,8 @@ constexpr int64_t kXentRegVocab = 256 * 8 * kXentQ;
 __global__ __launch_bounds__(256) void xent_reg_kernel(int64_t rows, int64_t vocab,
                                                        const uint16_t* __restrict__ logits,
                                                        const int32_t* __restrict__ targets, float inv_tokens,
-                                                       uint16_t* __restrict__ dlogits, float* __restrict__ row_loss) {
+                                                       float z_loss, float z2, uint16_t* __restrict__ dlogits,
+                                                       float* __restrict__ row_loss) {
   __shared__ WaveStage st[4];
   extern __shared__ float parts[];
   __shared__ float red[4];
@@ -762,9 +800,20 @@ __global__ __launch_bounds__(256) void xent_reg_kernel(int64_t rows, int64_t voc
   const float S = block_fold(f.result(), (nc + G - 1) / G);
   const int32_t y = targets[row];
   const bool valid = y >= 0 && y < vocab;
+  // z-loss (weight z_loss, z2 = RN(2 z_loss)): the row loss gains RN(z_loss * RN(lse^2)) and every
+  // probability is scaled by RN(1 + RN(z2 * lse)) before the target is subtracted
+  const float lse = m + clog(S);
+  const bool zl = z_loss != 0.0f;
+  const float zt = z2 * lse;
+  const float pscale = 1.0f + zt;
   if (threadIdx.x == 0) {
-    float lse = m + clog(S);
-    row_loss[row] = valid ? lse - bf16_to_f32(lr[y]) : __builtin_nanf("");
+    float ce = lse - bf16_to_f32(lr[valid ? y : 0]);
+    if (zl) {
+      const float l2 = lse * lse;
+      const float zterm = z_loss * l2;
+      ce = ce + zterm;
+    }
+    row_loss[row] = valid ? ce : __builtin_nanf("");
   }
   const float rcp = 1.0f / S;
   if (dlogits) {
@@ -779,6 +828,7 @@ __global__ __launch_bounds__(256) void xent_reg_kernel(int64_t rows, int64_t voc
         for (int i = 0; i < 8; ++i) {
           float e = cexp(fv[i] - m);
           float pr = e * rcp;
+          if (zl) pr = pr * pscale;
           float qd = pr - ((j8 * 8 + i) == y ? 1.0f : 0.0f);
           h[i] = f32_to_bf16(qd * inv_tokens);
         }
@@ -806,18 +856,19 @@ __global__ __launch_bounds__(256) void mean_loss_kernel(int64_t rows, const floa
 }
 
 hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets, float inv_tokens,
-                       uint16_t* dlogits, float* row_loss, float* mean_loss, hipStream_t s) {
+                       float z_loss, uint16_t* dlogits, float* row_loss, float* mean_loss, hipStream_t s) {
   if (rows > 0) {
     const size_t lds = sizeof(float) * (size_t)((vocab + kChunk - 1) / kChunk);
+    const float z2 = 2.0f * z_loss;  // exact
     if (vocab % 8 == 0 && vocab <= kXentRegVocab && al(logits, 16) && al(dlogits, 16))
       hipLaunchKernelGGL(xent_reg_kernel, dim3((unsigned)rows), dim3(256), lds, s, rows, vocab, logits, targets,
-                         inv_tokens, dlogits, row_loss);
+                         inv_tokens, z_loss, z2, dlogits, row_loss);
     else if (vocab % 8 == 0 && al(logits, 16) && al(dlogits, 16))
       hipLaunchKernelGGL(xent_kernel<8>, dim3((unsigned)rows), dim3(256), lds, s, rows, vocab, logits, targets,
-                         inv_tokens, dlogits, row_loss);
+                         inv_tokens, z_loss, z2, dlogits, row_loss);
     else
       hipLaunchKernelGGL(xent_kernel<1>, dim3((unsigned)rows), dim3(256), lds, s, rows, vocab, logits, targets,
-                         inv_tokens, dlogits, row_loss);
+                         inv_tokens, z_loss, z2, dlogits, row_loss);
   }
   if (mean_loss)
     hipLaunchKernelGGL(mean_loss_kernel, dim3(1), dim3(256), 0, s, rows, row_loss, inv_tokens, mean_loss);

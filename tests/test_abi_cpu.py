@@ -62,7 +62,18 @@ def test_host_validation_rejects_before_any_launch():
     assert lib.canon_rownorm(order, 7, rows, cols, x, gain, 1e-5, dx, rstd, None, None, None, None) == C.EINVAL
     # GEMM with negative sizes, softmax with rows not a multiple of cols
     assert lib.canon_gemm(order, 0, 0, -1, 4, 4, x, 4, dy, 4, dx, 4, None) == C.EINVAL
-    assert lib.canon_softmax_xent(order, C.SOFTMAX_CAUSAL, 10, 4, x, 1.0, None, 1.0, dx, None, None, None) == C.EINVAL
+    assert lib.canon_softmax_xent(order, C.SOFTMAX_CAUSAL, 10, 4, x, 1.0, 0, None, 1.0, 0.0, dx, None, None,
+                                  None) == C.EINVAL
+    # a negative window or z-loss weight
+    assert lib.canon_softmax_xent(order, C.SOFTMAX_CAUSAL, 8, 4, x, 1.0, -1, None, 1.0, 0.0, dx, None, None,
+                                  None) == C.EINVAL
+    assert lib.canon_softmax_xent(order, C.XENT, 8, 4, x, 1.0, 0, x, 1.0, -1.0, dx, dy, None, None) == C.EINVAL
+    # model configs: kv heads that do not divide the query heads, a bad flag, a negative window
+    for fields in ({"n_kv_heads": 3}, {"qk_norm": 2}, {"swa_window": -1}, {"z_loss": -1.0}):
+        cfg = C.ModelCfg(1, 64, 4, 16, 96, 97, 48, 1, 1e-5)
+        for k_, v_ in fields.items():
+            setattr(cfg, k_, v_)
+        assert lib.canon_block_workspace_bytes(ctypes.byref(cfg), 1) == 0, fields
 
 
 def test_sha256_constants_in_the_device_source():
