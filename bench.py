@@ -32,6 +32,27 @@ PLAN = (1, 8, 1)
 METRIC = "canonical-order GEMM TFLOP/s (% of bf16 peak), bit-exact; 1B step replay secs"
 
 
+def attn_pairs(S, window):
+    """(query, key) pairs a head computes over in one sequence: causal, or the sliding window."""
+    if not window or window >= S:
+        return S * (S + 1) // 2
+    return window * (window + 1) // 2 + (S - window) * window
+
+
+def step_flops_open1b(L, d, H, Hkv, hd, F, V, S, mb, window, full_every, ranks=1):
+    """Algorithmic FLOP of one step of the paper's own architecture (grouped heads, hybrid windows): every
+    forward and backward GEMM, attention over visible (query, key) pairs only."""
+    T = mb * S
+    N = d + 2 * Hkv * hd
+    fwd_layer = 2 * T * (d * N + d * d + d * 2 * F + F * d)
+    total = 0
+    for l in range(L):
+        full = (full_every and (l + 1) % full_every == 0) or l == L - 1
+        pairs = attn_pairs(S, 0 if full else window)
+        total += 3 * fwd_layer + mb * H * pairs * 12 * hd  # QK^T, PV forward; dP, dQ, dK, dV backward
+    return ranks * (total + 3 * 2 * T * d * V)
+
+
 def step_flops(L=L, d=D, H=H, hd=HD, F=F, V=V, S=S, mb=MB, ranks=8):
     """Algorithmic FLOPs of one step: every GEMM of forward and backward (2 per multiply-add), attention
     counted over the unmasked (causal) entries only."""
@@ -234,10 +255,54 @@ def kernel_table(C, I, torch, np, stream, dev):
     out[f"block_fwd_bwd_seq{S}"] = {"bound": "mfma", "ms": round(ms, 3), "achieved": round(fl / (ms * 1e-3) / 1e12, 2),
                                     "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
                                     "frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA, 4)}
+    del xb, dyb, w, dw, yb, dxb, wsb
+    torch.cuda.empty_cache()
+    out.update(open1b_step(C, I, torch, np, stream, dev))
     for k_, v_ in out.items():
         print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({100 * v_['frac']:.1f}%)",
               file=sys.stderr, flush=True)
     return out
+
+
+# The paper's own 1B architecture (its hyperparameter table): 24 layers, d 2048, 16 query / 4 key-value heads
+# of 128, FFN 5632, vocab 128256, sequence 4096, sliding window 512 with every 5th and the last layer full,
+# gain-free QK-norm, embedding norm, z-loss 1e-4; 4 sequences per microbatch.
+O1B = dict(L=24, d=2048, H=16, Hkv=4, hd=128, F=5632, V=128256, S=4096, mb=4, window=512, full_every=5)
+
+
+def open1b_step(C, I, torch, np, stream, dev):
+    """One step of the paper's architecture with every variant on (one rank, one microbatch of 4 x 4096 tokens,
+    the clip at 1.0), timed after one warmup step."""
+    o = O1B
+    print("bench: open-1B step (all variants)", file=sys.stderr, flush=True)
+    cfg = C.ModelCfg(o["L"], o["d"], o["H"], o["hd"], o["F"], o["V"], o["S"], o["mb"], np.float32(1e-5), o["Hkv"],
+                     1, 1, o["window"], o["full_every"], np.float32(1e-4))
+    plan = C.DPPlan(1, 1, 1)
+    params = I.model_params(o["L"], o["d"], o["F"], o["V"], seed=0, std=0.02, kv_dim=o["Hkv"] * o["hd"],
+                            embed_norm=True)
+    pg = [torch.from_numpy(p.view(np.int16)).to(dev) for p in params]
+    del params
+    mg = [torch.zeros(p.shape, dtype=torch.float32, device=dev) for p in pg]
+    vg = [torch.zeros(p.shape, dtype=torch.float32, device=dev) for p in pg]
+    windows = torch.from_numpy(I.uniform_int((o["mb"], o["S"] + 1), 0, I.TENSOR_IDS["windows"], o["V"])).to(dev)
+    cos, sin = I.rope_tables(o["S"], o["hd"])
+    cos, sin = torch.from_numpy(cos).to(dev), torch.from_numpy(sin).to(dev)
+    consts = C.AdamWConsts(*I.adamw_constants())
+    ws = torch.empty(C.step_workspace_bytes(cfg, plan), dtype=torch.uint8, device=dev)
+    loss = torch.zeros(1, dtype=torch.float32, device=dev)
+    gnorm = torch.zeros(1, dtype=torch.float32, device=dev)
+    clip = C.make_clip(1.0, float("inf"), 0, gnorm)
+    ms = _timed(torch, stream, lambda: C.step(cfg, plan, pg, mg, vg, windows, cos, sin, consts, ws, loss,
+                                              stream=stream, clip=clip), 1)
+    fl = step_flops_open1b(o["L"], o["d"], o["H"], o["Hkv"], o["hd"], o["F"], o["V"], o["S"], o["mb"], o["window"],
+                           o["full_every"])
+    tf = fl / (ms * 1e-3) / 1e12
+    res = {"bound": "mfma", "ms": round(ms, 2), "achieved": round(tf, 2), "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
+           "frac": round(tf / PEAK_FP32_MFMA, 4), "flops": fl, "tokens_per_s": round(o["mb"] * o["S"] / (ms * 1e-3), 1),
+           "loss": float(loss.item()), "grad_norm_preclip": float(gnorm.item())}
+    del ws, pg, mg, vg
+    torch.cuda.empty_cache()
+    return {"step_open1b_4x4096_all_variants": res}
 
 
 def main():
@@ -248,6 +313,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gemm-reps", type=int, default=10)
     ap.add_argument("--no-kernel-table", action="store_true")
+    ap.add_argument("--open1b-only", action="store_true",
+                    help="time only the paper-architecture step (all variants) and print its entry")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -264,6 +331,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
+    if args.open1b_only:
+        print(json.dumps(open1b_step(C, I, torch, np, stream, dev)), flush=True)
+        return
     print("bench: generating inputs", file=sys.stderr, flush=True)
     t0 = time.time()
     params = I.model_params(L, D, F, V, seed=0, std=0.02)

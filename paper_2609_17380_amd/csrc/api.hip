@@ -183,6 +183,7 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
     GemmArgs g = batched(mk(0, 1, S, S, hd, sv.q, hd, sv.k, hd, sc.scores, S), D, H * S * hd, S * hd,
                          Hkv * S * hd, S * hd, H * S * S, S * S);
     g.tri_lower = 1;
+    g.kwin = D.window;  // tiles left of the window band are not computed (the softmax reads none of them)
     g.b_group = (int32_t)D.G;
     TRY(gemm(g, s));
   }
@@ -191,6 +192,7 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
     GemmArgs g = batched(mk(0, 0, S, hd, S, sv.P, S, sv.v, hd, sv.O, d, 1), D, H * S * S, S * S, Hkv * S * hd,
                          S * hd, S * d, hd);
     g.kmode = KMODE_TRAIL;
+    g.kwin = D.window;
     g.b_group = (int32_t)D.G;
     TRY(gemm(g, s));
   }
@@ -224,12 +226,15 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
   TRY(gemm(mk(1, 0, d, d, T, sc.dy_b, d, sv.O, d, dw[2], d), s));        // dW_o = dh^T O
   TRY(gemm(mk(0, 0, T, d, d, sc.dy_b, d, w[2], d, sc.dO, d, 1), s));     // dO = dh W_o (bf16)
   TRY(attn_rowdot_launch(D.B, H, S, hd, sc.dO, sv.O, d, sc.Dv, s));      // D = rowsum(dO * O)
-  {  // dP = dO V^T, turned into dS = P * (dP - D) * c in the epilogue (bf16).  One head per key/value head:
-     // the lower-triangle tiles only, since the dK and dQ GEMMs never read above the diagonal tiles.  Grouped
-     // heads: every tile (+0 above the diagonal), since dK then reads each head's dS whole.
+  {  // dP = dO V^T, turned into dS = P * (dP - D) * c in the epilogue (bf16).  Tiles with no visible entry are
+     // not computed: those left of the window band get their +0 written (the windowed dQ and dK ranges may
+     // read them); those above the diagonal stay unwritten with one head per key/value head (the dQ and dK
+     // ranges never reach them), and get their +0 with grouped heads (dK then reads each head's dS whole).
     GemmArgs g = batched(mk(0, 1, S, S, hd, sc.dO, d, sv.v, hd, sc.dS, S), D, S * d, hd, Hkv * S * hd, S * hd,
                          H * S * S, S * S);
-    g.tri_lower = G == 1 ? 1 : 0;
+    g.tri_lower = 1;
+    g.kwin = D.window;
+    g.zero_dead = G > 1 ? 1 : 0;
     g.b_group = (int32_t)G;
     g.epi = EPI_DS;
     g.ds_p = sv.P; g.ds_d = sc.Dv; g.ds_scale = D.scale; g.ds_window = D.window;
@@ -240,6 +245,7 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
     GemmArgs g = batched(mk(0, 0, S, hd, S, sc.dS, S, sv.k, hd, sc.dq, d), D, H * S * S, S * S, Hkv * S * hd,
                          S * hd, S * d, hd);
     g.kmode = KMODE_TRAIL;
+    g.kwin = D.window;
     g.b_group = (int32_t)G;
     TRY(gemm(g, s));
   }
@@ -247,7 +253,12 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
   auto grouped = [&](GemmArgs g, int64_t sa1, int64_t sa2, int64_t sb1, int64_t sb2, int64_t sc1, int64_t sc2) {
     g.batch = D.B * Hkv; g.nb2 = Hkv;
     g.sa1 = sa1; g.sa2 = sa2; g.sb1 = sb1; g.sb2 = sb2; g.sc1 = sc1; g.sc2 = sc2;
-    g.kmode = G == 1 ? KMODE_LEAD : KMODE_FULL;  // one head: queries before the key are zero chunks
+    // in each head's segment of the contraction, queries before the key tile (and after its window) are
+    // zero chunks; segments need S to be a multiple of 128 (whole groups of four chunks)
+    const bool seg = G == 1 || S % 128 == 0;
+    g.kmode = seg ? KMODE_LEAD : KMODE_FULL;
+    if (seg) g.kwin = D.window;
+    if (G > 1 && seg) g.kseg = S;
     return g;
   };
   // dK = sum over the group of dS^T Q (over the group's queries)

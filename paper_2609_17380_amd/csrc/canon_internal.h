@@ -19,6 +19,10 @@ struct GemmArgs {
   int32_t trans_a, trans_b, out_bf16, kmode, tri_lower;
   int32_t vec;      // set by the launcher: 16-byte operand loads allowed
   int32_t b_group;  // > 1: B's inner batch offset is (z2 / b_group) * sb2 (grouped key/value heads)
+  int64_t kwin;     // > 0: sliding attention window for the KMODE ranges and the tri_lower band
+  int32_t zero_dead;  // EPI_DS with tri_lower: write the +0 of the tiles above the diagonal too
+  int64_t kseg;       // > 0 (a multiple of 128 dividing k): the KMODE ranges repeat in every K segment of kseg
+                      // (grouped heads stacked along K); 0: one segment
   // EPI_DS epilogue (attention backward, R5): the finished value d = dP[i][j] of a square per-head matrix
   // becomes dS[i][j] = bf16(RN(RN(P[i][j] * RN(d - D[i])) * ds_scale)) for j <= i (and j > i - ds_window
   // when ds_window > 0), +0 elsewhere, written as bf16 into C.  P: bf16 with leading dim ds_ldp and batch offsets ds_sp1/ds_sp2; D: fp32

@@ -82,6 +82,219 @@ __global__ void rope_qkv_norm_kernel(int64_t B, int64_t S, int64_t H, int64_t Hk
   }
 }
 
+// Wavefront-per-segment QK-norm (head size HD = 64, 128 or 256).  A segment is up to 2048 consecutive floats
+// of one token's q part (H heads) or k part (Hkv heads): whole heads, read coalesced, lane l holding
+// elements 256 q + 4 l .. +3.  Squares (or, backward, the products gy * x) are staged transposed in LDS so
+// that lane c runs chunk c's chain; the HD / 32 chunks of a head fold by shuffles (a complete subtree), and
+// the rotation's partner element i +- HD/2 sits in lane l ^ (HD / 8).
+struct QkStage {
+  float t[64][33];
+};
+
+__device__ __forceinline__ void qk_item(int64_t item, int64_t nsq, int64_t nsk, int64_t& t, int& part, int64_t& seg) {
+  const int64_t per = nsq + nsk;
+  t = item / per;
+  const int64_t r = item % per;
+  part = r < nsq ? 0 : 1;
+  seg = part == 0 ? r : r - nsq;
+}
+
+// chains of the staged segment (len floats) and the per-head fold: lane h * (HD / 32) returns head h's sum
+template <int HD>
+__device__ __forceinline__ float qk_head_sums(QkStage& st, int64_t len) {
+  constexpr int CPH = HD / 32;
+  const int lane = threadIdx.x & 63;
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  float p = 0.0f;
+  if (lane < len / kChunk) {
+    for (int i = 0; i < kChunk; ++i) p = p + st.t[lane][i];
+  }
+#pragma unroll
+  for (int sft = 1; sft < CPH; sft <<= 1) {
+    const float o = __shfl_down(p, sft, 64);
+    if ((lane & (2 * sft - 1)) == 0) p = p + o;
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  return p;
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void rope_qkv_norm_wave_kernel(int64_t B, int64_t S, int64_t H, int64_t Hkv,
+                                                                 const float* __restrict__ qkv,
+                                                                 const float* __restrict__ cosT,
+                                                                 const float* __restrict__ sinT, float eps,
+                                                                 float inv_hd, uint16_t* __restrict__ q,
+                                                                 uint16_t* __restrict__ k, uint16_t* __restrict__ v,
+                                                                 float* __restrict__ rq) {
+  constexpr int CPH = HD / 32, HH = HD / 2;
+  __shared__ QkStage stage[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t N = (H + 2 * Hkv) * HD;
+  const int64_t nsq = (H * HD + 2047) / 2048, nsk = (Hkv * HD + 2047) / 2048;
+  const int64_t item = (int64_t)blockIdx.x * 4 + w;
+  if (item >= B * S * (nsq + nsk)) return;
+  int64_t t, seg;
+  int part;
+  qk_item(item, nsq, nsk, t, part, seg);
+  const int64_t b = t / S, s = t % S;
+  const int64_t nh = part == 0 ? H : Hkv;
+  const int64_t len = (nh * HD - seg * 2048) < 2048 ? nh * HD - seg * 2048 : 2048;
+  const int64_t head0 = seg * (2048 / HD);
+  const float* src = qkv + t * N + (part == 0 ? 0 : H * HD) + seg * 2048;
+  float x[8][4];
+#pragma unroll
+  for (int qq = 0; qq < 8; ++qq) {
+    const int64_t e = 256 * qq + 4 * lane;
+    float4 f4 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (e < len) f4 = *reinterpret_cast<const float4*>(src + e);
+    x[qq][0] = f4.x; x[qq][1] = f4.y; x[qq][2] = f4.z; x[qq][3] = f4.w;
+    if (e < len) {
+      float* dst = &stage[w].t[e >> 5][e & 31];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) dst[kk] = x[qq][kk] * x[qq][kk];
+    }
+  }
+  const float ss = qk_head_sums<HD>(stage[w], len);
+  float r = 0.0f;
+  if ((lane % CPH) == 0 && lane < len / kChunk) {
+    const float ms = ss * inv_hd;
+    const float var = ms + eps;
+    r = 1.0f / __builtin_sqrtf(var);
+    rq[t * (H + Hkv) + (part == 0 ? 0 : H) + head0 + lane / CPH] = r;
+  }
+  uint16_t* outb = part == 0 ? q : k;
+#pragma unroll
+  for (int qq = 0; qq < 8; ++qq) {
+    const int64_t e = 256 * qq + 4 * lane;
+    const int hl = (int)((256 * qq + 4 * lane) / HD);
+    const float rr = __shfl(r, (hl * CPH) & 63, 64);
+    float xn[4], xp[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) xn[kk] = x[qq][kk] * rr;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) xp[kk] = __shfl_xor(xn[kk], HD / 8, 64);
+    if (e < len) {
+      const int i0 = (int)((256 * qq + 4 * lane) % HD);
+      uint16_t o[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int i = i0 + kk, ih = i % HH;
+        const float c = cosT[s * HH + ih], sn = sinT[s * HH + ih];
+        const float a = xn[kk] * c, bb = xp[kk] * sn;
+        o[kk] = f32_to_bf16(i < HH ? a - bb : a + bb);
+      }
+      uint16_t* dst = outb + ((b * nh + head0 + hl) * S + s) * HD + i0;
+      *reinterpret_cast<uint2*>(dst) = make_uint2((uint32_t)o[0] | ((uint32_t)o[1] << 16),
+                                                  (uint32_t)o[2] | ((uint32_t)o[3] << 16));
+    }
+  }
+  if (part == 1) {  // the value heads of this segment
+    const float* vs = qkv + t * N + (H + Hkv) * HD + seg * 2048;
+#pragma unroll
+    for (int qq = 0; qq < 8; ++qq) {
+      const int64_t e = 256 * qq + 4 * lane;
+      if (e < len) {
+        const float4 f4 = *reinterpret_cast<const float4*>(vs + e);
+        const int hl = (int)(e / HD), i0 = (int)(e % HD);
+        uint16_t* dst = v + ((b * Hkv + head0 + hl) * S + s) * HD + i0;
+        *reinterpret_cast<uint2*>(dst) =
+            make_uint2((uint32_t)f32_to_bf16(f4.x) | ((uint32_t)f32_to_bf16(f4.y) << 16),
+                       (uint32_t)f32_to_bf16(f4.z) | ((uint32_t)f32_to_bf16(f4.w) << 16));
+      }
+    }
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(256) void rope_bwd_norm_wave_kernel(int64_t B, int64_t S, int64_t H, int64_t Hkv,
+                                                                 const float* __restrict__ dq,
+                                                                 const float* __restrict__ dk,
+                                                                 const float* __restrict__ qkv,
+                                                                 const float* __restrict__ rq,
+                                                                 const float* __restrict__ cosT,
+                                                                 const float* __restrict__ sinT, float inv_hd,
+                                                                 uint16_t* __restrict__ dqkv) {
+  constexpr int CPH = HD / 32, HH = HD / 2;
+  __shared__ QkStage stage[4];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t N = (H + 2 * Hkv) * HD;
+  const int64_t nsq = (H * HD + 2047) / 2048, nsk = (Hkv * HD + 2047) / 2048;
+  const int64_t item = (int64_t)blockIdx.x * 4 + w;
+  if (item >= B * S * (nsq + nsk)) return;
+  int64_t t, seg;
+  int part;
+  qk_item(item, nsq, nsk, t, part, seg);
+  const int64_t s = t % S;
+  const int64_t nh = part == 0 ? H : Hkv;
+  const int64_t len = (nh * HD - seg * 2048) < 2048 ? nh * HD - seg * 2048 : 2048;
+  const int64_t head0 = seg * (2048 / HD);
+  const float* gsrc = part == 0 ? dq + t * H * HD + seg * 2048 : dk + t * Hkv * HD + seg * 2048;
+  const int64_t col0 = (part == 0 ? 0 : H * HD) + seg * 2048;
+  const float* xsrc = qkv + t * N + col0;
+  float gy[8][4], x[8][4];
+#pragma unroll
+  for (int qq = 0; qq < 8; ++qq) {
+    const int64_t e = 256 * qq + 4 * lane;
+    float4 g4 = make_float4(0.0f, 0.0f, 0.0f, 0.0f), x4 = g4;
+    if (e < len) {
+      g4 = *reinterpret_cast<const float4*>(gsrc + e);
+      x4 = *reinterpret_cast<const float4*>(xsrc + e);
+    }
+    const float g[4] = {g4.x, g4.y, g4.z, g4.w};
+    x[qq][0] = x4.x; x[qq][1] = x4.y; x[qq][2] = x4.z; x[qq][3] = x4.w;
+    float gp[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) gp[kk] = __shfl_xor(g[kk], HD / 8, 64);
+    const int i0 = (int)((256 * qq + 4 * lane) % HD);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int i = i0 + kk, ih = i % HH;
+      const float c = (e < len) ? cosT[s * HH + ih] : 0.0f, sn = (e < len) ? sinT[s * HH + ih] : 0.0f;
+      const float a = g[kk] * c, bb = gp[kk] * sn;
+      gy[qq][kk] = i < HH ? a + bb : a - bb;
+    }
+    if (e < len) {
+      float* dst = &stage[w].t[e >> 5][e & 31];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) dst[kk] = gy[qq][kk] * x[qq][kk];
+    }
+  }
+  const float dot = qk_head_sums<HD>(stage[w], len);
+  float r = 0.0f, qc = 0.0f;
+  if ((lane % CPH) == 0 && lane < len / kChunk) {
+    r = rq[t * (H + Hkv) + (part == 0 ? 0 : H) + head0 + lane / CPH];
+    const float r2 = r * r;
+    const float r3 = r2 * r;
+    const float dm = dot * inv_hd;
+    qc = r3 * dm;
+  }
+#pragma unroll
+  for (int qq = 0; qq < 8; ++qq) {
+    const int64_t e = 256 * qq + 4 * lane;
+    const int hl = (int)((256 * qq + 4 * lane) / HD);
+    const float rr = __shfl(r, (hl * CPH) & 63, 64);
+    const float qh = __shfl(qc, (hl * CPH) & 63, 64);
+    if (e < len) {
+      uint16_t o[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const float a = rr * gy[qq][kk], bb = x[qq][kk] * qh;
+        o[kk] = f32_to_bf16(a - bb);
+      }
+      uint16_t* dst = dqkv + t * N + col0 + e;
+      *reinterpret_cast<uint2*>(dst) = make_uint2((uint32_t)o[0] | ((uint32_t)o[1] << 16),
+                                                  (uint32_t)o[2] | ((uint32_t)o[3] << 16));
+    }
+  }
+}
+
+static bool qk_wave_ok(int64_t H, int64_t Hkv, int64_t hd, const void* a, const void* b) {
+  return (hd == 64 || hd == 128 || hd == 256) && ((uintptr_t)a & 15) == 0 && ((uintptr_t)b & 7) == 0 && H > 0 &&
+         Hkv > 0;
+}
+
 hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t hd, const float* qkv,
                            const float* cosT, const float* sinT, int qk_norm, float eps, uint16_t* q, uint16_t* k,
                            uint16_t* v, float* rq, hipStream_t s) {
@@ -89,6 +302,20 @@ hipError_t rope_qkv_launch(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t
     const int64_t n = B * S * (H + Hkv);
     if (n == 0) return hipSuccess;
     const float inv_hd = (float)(1.0 / (double)hd);  // RN32(1/hd)
+    if (qk_wave_ok(H, Hkv, hd, qkv, q) && ((uintptr_t)k & 7) == 0 && ((uintptr_t)v & 7) == 0) {
+      const int64_t items = B * S * ((H * hd + 2047) / 2048 + (Hkv * hd + 2047) / 2048);
+      const dim3 grid((unsigned)((items + 3) / 4));
+      if (hd == 64)
+        hipLaunchKernelGGL(rope_qkv_norm_wave_kernel<64>, grid, dim3(256), 0, s, B, S, H, Hkv, qkv, cosT, sinT, eps,
+                           inv_hd, q, k, v, rq);
+      else if (hd == 128)
+        hipLaunchKernelGGL(rope_qkv_norm_wave_kernel<128>, grid, dim3(256), 0, s, B, S, H, Hkv, qkv, cosT, sinT, eps,
+                           inv_hd, q, k, v, rq);
+      else
+        hipLaunchKernelGGL(rope_qkv_norm_wave_kernel<256>, grid, dim3(256), 0, s, B, S, H, Hkv, qkv, cosT, sinT, eps,
+                           inv_hd, q, k, v, rq);
+      return hipGetLastError();
+    }
     hipLaunchKernelGGL(rope_qkv_norm_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, Hkv, hd, qkv, cosT, sinT,
                        eps, inv_hd, q, k, v, rq);
     return hipGetLastError();
@@ -177,6 +404,20 @@ hipError_t rope_bwd_launch(int64_t B, int64_t S, int64_t H, int64_t Hkv, int64_t
     const int64_t n = B * S * (H + Hkv);
     if (n == 0) return hipSuccess;
     const float inv_hd = (float)(1.0 / (double)hd);
+    if (qk_wave_ok(H, Hkv, hd, qkv, dqkv) && ((uintptr_t)dq & 15) == 0 && ((uintptr_t)dk & 15) == 0) {
+      const int64_t items = B * S * ((H * hd + 2047) / 2048 + (Hkv * hd + 2047) / 2048);
+      const dim3 grid((unsigned)((items + 3) / 4));
+      if (hd == 64)
+        hipLaunchKernelGGL(rope_bwd_norm_wave_kernel<64>, grid, dim3(256), 0, s, B, S, H, Hkv, dq, dk, qkv, rq, cosT,
+                           sinT, inv_hd, dqkv);
+      else if (hd == 128)
+        hipLaunchKernelGGL(rope_bwd_norm_wave_kernel<128>, grid, dim3(256), 0, s, B, S, H, Hkv, dq, dk, qkv, rq, cosT,
+                           sinT, inv_hd, dqkv);
+      else
+        hipLaunchKernelGGL(rope_bwd_norm_wave_kernel<256>, grid, dim3(256), 0, s, B, S, H, Hkv, dq, dk, qkv, rq, cosT,
+                           sinT, inv_hd, dqkv);
+      return hipGetLastError();
+    }
     hipLaunchKernelGGL(rope_bwd_norm_kernel, dim3(blocks_for(n)), dim3(256), 0, s, B, S, H, Hkv, hd, dq, dk, qkv, rq,
                        cosT, sinT, inv_hd, dqkv);
     return hipGetLastError();

@@ -25,7 +25,11 @@
 //
 // Causal modes (attention): KMODE_TRAIL skips key chunks that are masked for every row of the tile and
 // KMODE_LEAD skips query chunks below the tile; the skipped chunks' partials are exactly +0 in the
-// canonical chain and are still folded (pushed as +0), so the result equals the full-range chain.
+// canonical chain and are still folded (pushed as +0), so the result equals the full-range chain.  With a
+// sliding window kwin, TRAIL also skips the key chunks before the window of the tile's first query and
+// LEAD the query chunks after the window of the tile's last key.  Output tiles with no visible entry
+// (tri_lower: above the diagonal, or left of the window band) are not computed: the dS epilogue writes
+// their +0 (band tiles always, diagonal tiles when zero_dead), other outputs leave them unwritten.
 #include <hip/hip_runtime.h>
 
 #include "canon_dev.h"
@@ -315,7 +319,10 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     if (g.kmode == KMODE_TRAIL) tm = tiles_m - 1 - tm;
   }
   const int64_t row0 = tm * BM, col0 = tn * BN;
-  if (g.tri_lower && col0 > row0 + BM - 1) return;  // output tile entirely above the diagonal
+  const bool upper_dead = g.tri_lower && col0 > row0 + BM - 1;                           // above the diagonal
+  const bool band_dead = g.tri_lower && g.kwin > 0 && col0 + BN - 1 <= row0 - g.kwin;   // left of the window
+  if ((upper_dead && !(g.zero_dead && g.epi == EPI_DS)) || (band_dead && g.epi != EPI_DS)) return;
+  const bool dead = upper_dead || band_dead;  // the epilogue writes this tile's +0
 
   const int64_t z = blockIdx.z;
   const int64_t z1 = z / g.nb2, z2 = z % g.nb2;
@@ -332,36 +339,52 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
 
   const int64_t nc = (g.k + KC - 1) / KC;
   const int64_t kfull = g.k / KC;  // chunks with all 32 terms
-  int64_t c_begin = 0, c_end = nc;
+  // The real chunks: in each K segment of spc chunks (one segment unless kseg is set), the local chunks
+  // [lb, le); every other chunk is a +0 partial.
+  const int64_t spc = g.kseg > 0 ? g.kseg / KC : nc;
+  const int64_t nseg = g.kseg > 0 ? nc / spc : 1;
+  const int64_t ncs = g.kseg > 0 ? spc : nc;
+  int64_t lb = 0, le = ncs;
+  const int64_t last_row = row0 + BM < g.m ? row0 + BM : g.m;  // rows of this tile are < last_row
   if (g.kmode == KMODE_TRAIL) {
-    int64_t last_row = row0 + BM < g.m ? row0 + BM : g.m;  // rows of this tile are < last_row
     int64_t ce = (last_row + KC - 1) / KC;
-    c_end = ce < nc ? ce : nc;
+    le = ce < ncs ? ce : ncs;
+    if (g.kwin > 0 && row0 - g.kwin + 1 > 0) {  // keys before the first query's window
+      const int64_t cb = (row0 - g.kwin + 1) / KC;
+      lb = cb < le ? cb : le;
+    }
   } else if (g.kmode == KMODE_LEAD) {
     int64_t cb = row0 / KC;
-    c_begin = cb < nc ? cb : nc;
+    lb = cb < ncs ? cb : ncs;
+    if (g.kwin > 0) {  // queries after the last key's window: the last visible query is last_row - 2 + kwin
+      const int64_t ce = (last_row - 2 + g.kwin) / KC + 1;
+      le = ce < ncs ? ce : ncs;
+      if (le < lb) le = lb;
+    }
   }
+  if (dead) lb = le = 0;
 
   v32f zero;
 #pragma unroll
   for (int v = 0; v < 32; ++v) zero[v] = 0.0f;
-  // Level-2 stack (one entry per aligned group of four chunks).  Groups entirely before c_begin are
-  // skipped chunks: pushing them as +0 partials leaves +0 at the set bits of their count, i.e. clear().
+  // Level-2 stack (one entry per aligned group of four chunks).  Groups entirely before lb (in the first
+  // segment) are skipped chunks: pushing them as +0 partials leaves +0 at the set bits of their count,
+  // i.e. clear().
   FoldRegs<RL> S;
   FoldMem<NMEM> Smem;
-  S.clear(zero, c_begin >> 2, Smem);
+  S.clear(zero, lb >> 2, Smem);
 
   int buf = 0;
-  if (c_begin < c_end)
-    store_chunk<TA, TB>(As[0], Bs[0], load_chunk<TA, TB, false>(g, A, B, row0, col0, c_begin * KC, vec));
+  if (lb < le)
+    store_chunk<TA, TB>(As[0], Bs[0], load_chunk<TA, TB, false>(g, A, B, row0, col0, lb * KC, vec));
   __syncthreads();
 
-  // generic pipelined chunk (checked loads, ragged chunk allowed); chunks run in ascending order from
-  // c_begin, so chunk c + 1 is the next one to run
-  auto run_chunk = [&](int64_t c) -> v32f {
-    const bool more = c + 1 < c_end;
+  // generic pipelined chunk (checked loads, ragged chunk allowed): real chunks run in ascending order;
+  // nextc is the next real chunk (its loads go ahead of this chunk's chain), or -1
+  auto run_chunk = [&](int64_t c, int64_t nextc) -> v32f {
+    const bool more = nextc >= 0;
     Raw nxt;
-    if (more) nxt = load_chunk<TA, TB, false>(g, A, B, row0, col0, (c + 1) * KC, vec);
+    if (more) nxt = load_chunk<TA, TB, false>(g, A, B, row0, col0, nextc * KC, vec);
     __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
     const int64_t kleft = g.k - c * KC;
     v32f acc = (kleft >= KC) ? chain_full<TA, TB>(As[buf], Bs[buf], ai, bi)
@@ -371,7 +394,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     buf ^= 1;
     return acc;
   };
-  // fast chunk: this and the next chunk full and in range (unchecked 16-byte loads)
+  // fast chunk: this and the next chunk full and real (unchecked 16-byte loads)
   auto run_fast = [&](int64_t c) -> v32f {
     Raw nxt = load_chunk<TA, TB, true>(g, A, B, row0, col0, (c + 1) * KC, vec);
     __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
@@ -382,20 +405,33 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     buf ^= 1;
     return acc;
   };
-  // a chunk of the group: real chunks run, skipped ones (outside [c_begin, c_end)) are +0 partials
-  auto part = [&](int64_t c) -> v32f { return (c >= c_begin && c < c_end) ? run_chunk(c) : zero; };
+  // the next real chunk after real chunk c of the segment starting at chunk base
+  auto next_real = [&](int64_t c, int64_t base) -> int64_t {
+    if (c + 1 - base < le) return c + 1;
+    return (base + spc < nc && lb < le) ? base + spc + lb : -1;
+  };
+  // a chunk of a group in the segment at base: real chunks run, skipped ones are +0 partials
+  auto part = [&](int64_t c, int64_t base) -> v32f {
+    return (c - base >= lb && c - base < le) ? run_chunk(c, next_real(c, base)) : zero;
+  };
 
   // Groups of four chunks.  A complete group's partial ((p0 + p1) + (p2 + p3)) is exactly the level-2
   // entry that four pushes would build; it is pushed at level 2 with the group index.  The last group may
-  // be partial (nc not a multiple of 4): its r chunks form the lowest entries of the final stack
-  // (r = 1: p0; 2: p0 + p1; 3: levels 1 and 0 hold p0 + p1 and p2) and start the Result.
+  // be partial (nc not a multiple of 4, one segment only): its r chunks form the lowest entries of the
+  // final stack (r = 1: p0; 2: p0 + p1; 3: levels 1 and 0 hold p0 + p1 and p2) and start the Result.
+  // With segments, spc is a multiple of 4, so a group never spans two.
   const int64_t ng_full = nc >> 2;
-  int64_t gj = c_begin >> 2;
+  const int64_t gps = nseg > 1 ? spc >> 2 : ng_full + 1;  // groups per segment
+  int64_t gj = lb >> 2;
   for (; gj < ng_full; ++gj) {
-    const int64_t c = gj * 4;
-    if (c >= c_end) break;  // the rest are skipped chunks
+    const int64_t sgi = nseg > 1 ? gj / gps : 0;
+    const int64_t base = sgi * spc;
+    const int64_t c = gj * 4, cl = c - base;
+    if (nseg == 1 && cl >= le) break;  // the rest are skipped chunks
     v32f q;
-    if (tile_in && c >= c_begin && c + 5 <= c_end && c + 5 <= kfull) {
+    if (cl + 4 <= lb || cl >= le) {
+      q = zero + zero;  // a group of skipped chunks
+    } else if (tile_in && cl >= lb && cl + 5 <= le && c + 5 <= kfull) {
       v32f p0 = run_fast(c);
       v32f p1 = run_fast(c + 1);
       v32f s01 = p0 + p1;
@@ -403,11 +439,11 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
       v32f p3 = run_fast(c + 3);
       q = s01 + (p2 + p3);
     } else {
-      v32f p0 = part(c);
-      v32f p1 = part(c + 1);
+      v32f p0 = part(c, base);
+      v32f p1 = part(c + 1, base);
       v32f s01 = p0 + p1;
-      v32f p2 = part(c + 2);
-      v32f p3 = part(c + 3);
+      v32f p2 = part(c + 2, base);
+      v32f p3 = part(c + 3, base);
       q = s01 + (p2 + p3);
     }
     S.push(q, gj, Smem);
@@ -420,13 +456,13 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   const int rem = (int)(nc & 3);
   if (rem) {
     const int64_t c = ng_full * 4;
-    v32f p0 = part(c);
+    v32f p0 = part(c, 0);
     if (rem == 1) {
       r = p0;
     } else {
-      v32f p1 = part(c + 1);
+      v32f p1 = part(c + 1, 0);
       r = p0 + p1;
-      if (rem == 3) r = r + part(c + 2);
+      if (rem == 3) r = r + part(c + 2, 0);
     }
     have = true;
   }

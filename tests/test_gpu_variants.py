@@ -71,9 +71,13 @@ def cfgs(L, d, H, F, V, S, mb, Hkv=0, qk=0, en=0, win=0, every=0, z=0.0):
     return oracle.ModelCfg(*args), C.ModelCfg(*args)
 
 
+# S a multiple of 128 takes the grouped dK/dV GEMMs with per-head skip ranges; other S the full contraction
 @pytest.mark.parametrize("d,H,Hkv,qk,win,F,S,batch", [(256, 4, 2, 0, 0, 384, 96, 2), (256, 4, 1, 1, 0, 320, 130, 1),
                                                      (256, 4, 4, 1, 40, 384, 96, 2), (256, 2, 1, 1, 33, 256, 130, 1),
-                                                     (512, 4, 2, 1, 64, 384, 160, 1), (256, 4, 2, 1, 17, 384, 96, 2)])
+                                                     (512, 4, 2, 1, 64, 384, 160, 1), (256, 4, 2, 1, 17, 384, 96, 2),
+                                                     (256, 4, 2, 1, 0, 384, 256, 1), (256, 4, 1, 0, 100, 256, 384, 1),
+                                                     (512, 8, 2, 1, 64, 384, 256, 2), (256, 4, 1, 1, 1, 256, 128, 1),
+                                                     (256, 4, 2, 0, 300, 256, 256, 1)])
 def test_block_variants_bit_exact(d, H, Hkv, qk, win, F, S, batch):
     print(f"block d={d} H={H} Hkv={Hkv} qk={qk} win={win} F={F} S={S} B={batch}", flush=True)
     hd = d // H
@@ -138,11 +142,14 @@ def run_step(L, d, H, F, V, S, mb, plan, variant, seed=0, clip=None):
     (dict(Hkv=2), (1, 1, 2)),
     (dict(win=17, every=3, z=1e-4), (1, 2, 1)),
     (dict(en=1), (1, 1, 1)),
+    (dict(Hkv=2, qk=1, en=1, win=48, every=2, z=1e-4, S=128), (1, 2, 1)),
 ])
 def test_step_variants_bit_exact(variant, plan):
     print(f"step variant {variant} plan {plan}", flush=True)
     clip = (1.0, 5.0, 5) if variant.get("qk") else None
-    res, (po, mo, vo), (lg, gg, pg, mg, vg, ng) = run_step(3, 256, 4, 256, 300, 64, 2, plan, variant, clip=clip)
+    variant = dict(variant)
+    S = variant.pop("S", 64)
+    res, (po, mo, vo), (lg, gg, pg, mg, vg, ng) = run_step(3, 256, 4, 256, 300, S, 2, plan, variant, clip=clip)
     loss_o, g_o = res[0], res[1]
     assert_bits(lg, np.array([loss_o], np.float32), "loss")
     if clip:
