@@ -35,7 +35,8 @@ class ModelCfg(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("n_kv_heads", ctypes.c_int32), ("qk_norm", ctypes.c_int32), ("embed_norm", ctypes.c_int32),
-                ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float)]
+                ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float),
+                ("pv_int8", ctypes.c_int32), ("dq_fixed_bits", ctypes.c_int32)]
 
 
 class Plan(ctypes.Structure):
@@ -89,6 +90,10 @@ def _load():
             "cref_gemm_i8": (ctypes.c_int, [i64, i64, i64, vp, i64, vp, i64, vp, vp, i64, f, vp]),
             "cref_fwht256": (ctypes.c_int, [i64, vp]),
             "cref_qlinear_bwd": (ctypes.c_int, [i64, i64, i64, vp, vp, f, vp, vp, vp, vp]),
+            "cref_attn_pv_i8": (ctypes.c_int, [i64, i64, vp, vp, vp]),
+            "cref_attn_dq_fixed": (ctypes.c_int, [i64, i64, i64, i32, vp, vp, vp]),
+            "cref_fx_product": (ctypes.c_uint64, [ctypes.c_uint16, ctypes.c_uint16, i32]),
+            "cref_fx_to_f32": (f, [ctypes.c_uint64, i32]),
             "cref_num_threads": (ctypes.c_int, []),
         }
         for name, (res, args) in sig.items():
@@ -364,6 +369,38 @@ def qlinear_bwd(dy: np.ndarray, qx: np.ndarray, sx: float, qw: np.ndarray, sw: n
     _check(_load().cref_qlinear_bwd(T, N, K, _p(dy), _p(qx), np.float32(sx), _p(qw), _p(sw),
                                     _p(dx) if dx is not None else None, _p(dw) if dw is not None else None))
     return dx, dw
+
+
+def attn_pv_i8(P: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """R17 int8 P.V of one head: P bf16 [S, S] (uint16), V bf16 [S, hd] -> O fp32 [S, hd]."""
+    P = np.ascontiguousarray(P, dtype=np.uint16)
+    V = np.ascontiguousarray(V, dtype=np.uint16)
+    S, hd = V.shape
+    assert P.shape == (S, S)
+    O = np.empty((S, hd), np.float32)
+    _check(_load().cref_attn_pv_i8(S, hd, _p(P), _p(V), _p(O)))
+    return O
+
+
+def attn_dq_fixed(dS: np.ndarray, K: np.ndarray, frac_bits: int, window: int = 0) -> np.ndarray:
+    """R18 fixed-point dQ of one head: dS bf16 [S, S], K bf16 [S, hd] -> dQ fp32 [S, hd] (causal, window)."""
+    dS = np.ascontiguousarray(dS, dtype=np.uint16)
+    K = np.ascontiguousarray(K, dtype=np.uint16)
+    S, hd = K.shape
+    assert dS.shape == (S, S)
+    dQ = np.empty((S, hd), np.float32)
+    _check(_load().cref_attn_dq_fixed(S, hd, window, frac_bits, _p(dS), _p(K), _p(dQ)))
+    return dQ
+
+
+def fx_product(a: int, b: int, frac_bits: int) -> int:
+    """R18 fixed-point value (as an unsigned 64-bit pattern) of the product of two bf16 bit patterns."""
+    return int(_load().cref_fx_product(a, b, frac_bits))
+
+
+def fx_to_f32(total: int, frac_bits: int) -> np.float32:
+    """R18 rounding of a wrapped 64-bit sum (unsigned pattern) times 2^-F to binary32."""
+    return np.float32(_load().cref_fx_to_f32(total % (1 << 64), frac_bits))
 
 
 def num_threads() -> int:

@@ -721,6 +721,7 @@ typedef struct {
   int64_t T, B, S, d, H, Hkv, hd, F, N; /* N = (H + 2 Hkv) hd: width of the fused q, k, v projection */
   int64_t window;                        /* 0: full causal; W: query i sees keys i - W + 1 .. i */
   int qk_norm;
+  int pv_int8, dq_bits;                  /* R17 P.V, R18 dQ (0: off) */
   float eps;
   float* x;      /* [T][d] input (residual) */
   uint16_t* xn;  /* [T][d] */
@@ -748,6 +749,7 @@ static void block_saved_alloc(block_saved* s, const cref_model_cfg* c, int64_t B
   s->B = B; s->S = c->seq; s->T = B * c->seq; s->d = c->d_model; s->H = c->n_heads; s->Hkv = kv_heads(c);
   s->hd = c->head_dim; s->F = c->d_ffn; s->N = (s->H + 2 * s->Hkv) * s->hd;
   s->window = window; s->qk_norm = c->qk_norm; s->eps = c->rms_eps;
+  s->pv_int8 = c->pv_int8; s->dq_bits = c->dq_fixed_bits;
   const int64_t T = s->T, d = s->d, S = s->S, F = s->F, kvw = s->Hkv * s->hd;
   s->x = (float*)xmalloc(sizeof(float) * T * d);
   s->xn = (uint16_t*)xmalloc(2 * T * d);
@@ -840,7 +842,8 @@ static void block_fwd(block_saved* s, const float* x, const uint16_t* const* w, 
     uint16_t* P = s->P + bh * S * S;
     cref_gemm(0, 1, S, S, hd, Q, hd, K, hd, raw, S);
     cref_softmax_window(1, S, raw, c, s->window, P);
-    cref_gemm(0, 0, S, hd, S, P, S, V, hd, ob, hd);
+    if (s->pv_int8) cref_attn_pv_i8(S, hd, P, V, ob);          /* R17 */
+    else cref_gemm(0, 0, S, hd, S, P, S, V, hd, ob, hd);
     for (int64_t pos = 0; pos < S; ++pos)
       for (int64_t j = 0; j < hd; ++j) s->O[(b * S + pos) * d + hh * hd + j] = cref_bf16(ob[pos * hd + j]);
   }
@@ -965,7 +968,8 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
             dS[i * S + j] = seen ? cref_bf16(cref_mul(cref_mul(widen(P[i * S + j]), cref_sub(dP[i * S + j], D[i])), c))
                                  : (uint16_t)0;
           }
-        cref_gemm(0, 0, S, hd, S, dS, S, K, hd, gq, hd);            /* dQ = dS K */
+        if (s->dq_bits) cref_attn_dq_fixed(S, hd, W, s->dq_bits, dS, K, gq); /* dQ = dS K by R18 */
+        else cref_gemm(0, 0, S, hd, S, dS, S, K, hd, gq, hd);       /* dQ = dS K */
         for (int64_t pos = 0; pos < S; ++pos)
           head_out(s, b * S + pos, hh * hd, hh, gq + pos * hd, rope_cos, rope_sin, dqkv);
       }
@@ -1000,6 +1004,7 @@ static int cfg_valid(const cref_model_cfg* c) {
   if ((c->qk_norm != 0 && c->qk_norm != 1) || (c->embed_norm != 0 && c->embed_norm != 1)) return 0;
   if (c->swa_window < 0 || c->swa_full_every < 0) return 0;
   if (!(c->z_loss >= 0.0f) || isinf(c->z_loss)) return 0;
+  if ((c->pv_int8 != 0 && c->pv_int8 != 1) || c->dq_fixed_bits < 0 || c->dq_fixed_bits > 62) return 0;
   return 1;
 }
 
@@ -1372,6 +1377,115 @@ int cref_qlinear_bwd(int64_t T, int64_t N, int64_t K, const float* dy, const int
     for (int64_t k = 0; k < K; ++k) sb[k] = sxt;
     cref_gemm_i8(N, K, T, qgt, T, qxt, T, NULL, dw, K, sgt, sb);
     free(gt); free(xt); free(qgt); free(qxt); free(sb);
+  }
+  return 0;
+}
+
+/* ======================================================================== */
+/* R17: int8 P.V inside the attention forward                                */
+/* ======================================================================== */
+/* The paper's flash-attention forward quantises the attention weights and the values to int8 per block and
+   multiplies them on the integer matrix cores, while the scores and the softmax stay in higher precision
+   (training-details paragraph on int8 computation; architecture section, int8 bullet).  Here a block of P
+   is 64 queries x 64 keys and a block of V is 64 keys x head_dim.  Each block's step is its absmax times
+   RN(1/127) (the rule of R14's rotated operands), the codes come from R13's quantiser, the product of a P
+   block and a V block is an exact integer sum, dequantised as RN(RN(RN32(acc) * sP) * sV) (left operand's
+   step first, as in R13), and the per-block results are summed by R1 over the key blocks in ascending
+   order. */
+#define PV_BLOCK 64
+
+/* step of a bf16 block [rows][cols] with row stride ld: RN(amax * RN(1/127)), amax by bit pattern */
+static float block_absmax_step(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld) {
+  uint32_t m = 0;
+  for (int64_t r = 0; r < rows; ++r)
+    for (int64_t c = 0; c < cols; ++c) {
+      const uint32_t u = f_bits(widen(x[r * ld + c])) & 0x7FFFFFFFu;
+      if (u > m) m = u;
+    }
+  return cref_mul(f_from_bits(m), f_from_bits(INV_127));
+}
+
+int cref_attn_pv_i8(int64_t S, int64_t hd, const uint16_t* P, const uint16_t* V, float* O) {
+  if (S < 1 || hd < 1 || !P || !V || !O) return -1;
+  const int64_t nb = (S + PV_BLOCK - 1) / PV_BLOCK;
+  float* sv = (float*)xmalloc(sizeof(float) * (size_t)nb);
+  int8_t* qv = (int8_t*)xmalloc((size_t)(S * hd));
+  for (int64_t kb = 0; kb < nb; ++kb) {
+    const int64_t k0 = kb * PV_BLOCK, nk = (S - k0) < PV_BLOCK ? (S - k0) : PV_BLOCK;
+    sv[kb] = block_absmax_step(V + k0 * hd, nk, hd, hd);
+    for (int64_t j = k0; j < k0 + nk; ++j)
+      for (int64_t c = 0; c < hd; ++c) qv[j * hd + c] = quant1(widen(V[j * hd + c]), sv[kb]);
+  }
+#pragma omp parallel for schedule(static)
+  for (int64_t qb = 0; qb < nb; ++qb) {
+    const int64_t i0 = qb * PV_BLOCK, ni = (S - i0) < PV_BLOCK ? (S - i0) : PV_BLOCK;
+    float* sp = (float*)xmalloc(sizeof(float) * (size_t)nb);
+    int8_t* qp = (int8_t*)xmalloc((size_t)(ni * S)); /* the query block's codes, [ni][S] */
+    float* terms = (float*)xmalloc(sizeof(float) * (size_t)nb);
+    for (int64_t kb = 0; kb < nb; ++kb) {
+      const int64_t k0 = kb * PV_BLOCK, nk = (S - k0) < PV_BLOCK ? (S - k0) : PV_BLOCK;
+      sp[kb] = block_absmax_step(P + i0 * S + k0, ni, nk, S);
+      for (int64_t i = 0; i < ni; ++i)
+        for (int64_t j = k0; j < k0 + nk; ++j) qp[i * S + j] = quant1(widen(P[(i0 + i) * S + j]), sp[kb]);
+    }
+    for (int64_t i = 0; i < ni; ++i)
+      for (int64_t c = 0; c < hd; ++c) {
+        for (int64_t kb = 0; kb < nb; ++kb) {
+          const int64_t k0 = kb * PV_BLOCK, k1 = (S - k0) < PV_BLOCK ? S : k0 + PV_BLOCK;
+          int64_t acc = 0; /* exact: |acc| <= 64 * 128 * 128 */
+          for (int64_t j = k0; j < k1; ++j) acc += (int64_t)qp[i * S + j] * (int64_t)qv[j * hd + c];
+          terms[kb] = cref_mul(cref_mul((float)acc, sp[kb]), sv[kb]);
+        }
+        O[(i0 + i) * hd + c] = cref_rsum(terms, nb, 1, CHUNK);
+      }
+    free(sp); free(qp); free(terms);
+  }
+  free(sv); free(qv);
+  return 0;
+}
+
+/* ======================================================================== */
+/* R18: dQ accumulated in 64-bit fixed point                                 */
+/* ======================================================================== */
+/* The paper's deterministic flash backward accumulates the query gradient in 64-bit fixed point, which
+   makes the sum independent of the order in which keys are visited (training-details paragraph on int8
+   computation).  Here each product dS * K (exact: two bf16 significands) is scaled by 2^F and rounded to
+   the nearest integer, ties to even; products and their sum are taken modulo 2^64 (two's complement), so
+   every order of the keys gives the same 64 bits.  The sum times 2^-F is rounded once to binary32 under
+   R0.  This implementation works in 80-bit long double, whose 64-bit significand holds every product
+   times 2^F and every int64 exactly. */
+uint64_t cref_fx_product(uint16_t a, uint16_t b, int32_t frac_bits) {
+  const double p = (double)widen(a) * (double)widen(b); /* exact: 8 x 8 significant bits */
+  if (p == 0.0) return 0;
+  const long double x = ldexpl((long double)p, frac_bits);
+  const long double r = nearbyintl(x); /* default rounding mode: ties to even */
+  long double m = fabsl(r);
+  const long double two64 = ldexpl(1.0L, 64);
+  if (m >= two64) m = fmodl(m, two64); /* exact */
+  const uint64_t u = (uint64_t)m;
+  return r < 0 ? (uint64_t)0 - u : u;
+}
+
+float cref_fx_to_f32(uint64_t sum, int32_t frac_bits) {
+  const int64_t s = (int64_t)sum;
+  if (s == 0) return 0.0f;
+  const float r = (float)(long double)s; /* one rounding to 24 significant bits, ties to even */
+  /* r * 2^-F is exact unless it lies below 2^-126, where R0 gives a zero of its sign */
+  if (fabsl(ldexpl((long double)r, -frac_bits)) < ldexpl(1.0L, -126)) return copysignf(0.0f, r);
+  return ldexpf(r, -frac_bits);
+}
+
+int cref_attn_dq_fixed(int64_t S, int64_t hd, int64_t window, int32_t frac_bits, const uint16_t* dS,
+                       const uint16_t* K, float* dQ) {
+  if (S < 1 || hd < 1 || window < 0 || frac_bits < 1 || frac_bits > 62 || !dS || !K || !dQ) return -1;
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < S; ++i) {
+    const int64_t j0 = (window > 0 && i - window + 1 > 0) ? i - window + 1 : 0;
+    for (int64_t c = 0; c < hd; ++c) {
+      uint64_t sum = 0;
+      for (int64_t j = j0; j <= i; ++j) sum += cref_fx_product(dS[i * S + j], K[j * hd + c], frac_bits);
+      dQ[i * hd + c] = cref_fx_to_f32(sum, frac_bits);
+    }
   }
   return 0;
 }

@@ -19,12 +19,15 @@ extern "C" {
 
 /* Model shape and the R16 variants (all zero: the plain block).  n_kv_heads: 0 (= n_heads) or a divisor
    of n_heads; qk_norm, embed_norm: 0 or 1; swa_window: 0 (full causal) or the window of the windowed
-   layers, which are all but every swa_full_every-th and the last; z_loss: weight, 0 for none. */
+   layers, which are all but every swa_full_every-th and the last; z_loss: weight, 0 for none.
+   pv_int8: 0 or 1, the attention forward's P.V by R17; dq_fixed_bits: 0 (dQ by R2) or F in [1, 62], the
+   attention backward's dQ by R18 with F fractional bits. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
   float rms_eps;
   int32_t n_kv_heads, qk_norm, embed_norm, swa_window, swa_full_every;
   float z_loss;
+  int32_t pv_int8, dq_fixed_bits;
 } cref_model_cfg;
 
 typedef struct {
@@ -150,6 +153,24 @@ int cref_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int64_t lda, 
 int cref_fwht256(int64_t n, float* v);
 int cref_qlinear_bwd(int64_t T, int64_t N, int64_t K, const float* dy, const int8_t* qx, float sx, const int8_t* qw,
                      const float* sw, float* dx, float* dw);
+
+/* ---- R17 int8 P.V inside the attention forward, one head ----
+   P: bf16 [S][S] attention weights (masked entries +0), V: bf16 [S][hd]; O: fp32 [S][hd].  Blocks of 64
+   queries x 64 keys of P and 64 keys x hd of V each get the step RN(amax * RN(1/127)) (amax by bit
+   pattern); codes by R13's quantiser; each block product is an exact integer sum dequantised as
+   RN(RN(RN32(acc) * sP) * sV); O = R1 over key blocks ascending. */
+int cref_attn_pv_i8(int64_t S, int64_t hd, const uint16_t* P, const uint16_t* V, float* O);
+
+/* ---- R18 dQ in 64-bit fixed point, one head ----
+   dQ[i][c] = RN(sum_j fx(dS[i][j] * K[j][c]) * 2^-F) over the keys j the query sees (j <= i, and
+   j > i - window when window > 0); fx(p) = the nearest integer to p * 2^F (ties to even), reduced modulo
+   2^64; the sum wraps modulo 2^64 (two's complement), so its value does not depend on the order of the
+   keys; the final rounding follows R0 (flush below 2^-126).  dS, K: bf16 [S][S], [S][hd]; dQ fp32. */
+int cref_attn_dq_fixed(int64_t S, int64_t hd, int64_t window, int32_t frac_bits, const uint16_t* dS,
+                       const uint16_t* K, float* dQ);
+/* fx of one product, and the conversion of a wrapped sum back to fp32 (exported for the pins) */
+uint64_t cref_fx_product(uint16_t a, uint16_t b, int32_t frac_bits);
+float cref_fx_to_f32(uint64_t sum, int32_t frac_bits);
 
 int cref_num_threads(void);
 
