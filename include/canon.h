@@ -72,12 +72,19 @@ typedef struct {
      swa_window:     0: every layer full causal; W > 0: query i sees keys i - W < j <= i in every layer
                      except every swa_full_every-th (l + 1 a multiple of it, 0 = none) and the last.
      z_loss:         weight of the z-loss (0: none): row loss RN(CE + RN(z * RN(lse^2))), probabilities
-                     scaled by RN(1 + RN(RN(2 z) * lse)) in the logit gradient. */
+                     scaled by RN(1 + RN(RN(2 z) * lse)) in the logit gradient.
+   The attention kernels of the paper's int8 path (training-details paragraph on int8 computation):
+     pv_int8:        1: the forward P.V in int8 per block (R17, canon_attn_pv_i8 below); head_dim a multiple of
+                     32 up to 256 and seq <= 8192, else CANON_EUNSUPPORTED.  The backward stays the bf16 one
+                     (straight-through).
+     dq_fixed_bits:  0: dQ by the canonical GEMM; F in [1, 62]: dQ accumulated in 64-bit fixed point with F
+                     fractional bits (R18, canon_attn_dq_fixed below); head_dim in {16, 32, 64, 128}. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
   float rms_eps; /* fp32 value, e.g. RN32(1e-5) */
   int32_t n_kv_heads, qk_norm, embed_norm, swa_window, swa_full_every;
   float z_loss;
+  int32_t pv_int8, dq_fixed_bits;
 } canon_model_cfg;
 
 /* AdamW constants, each evaluated in double and rounded once to fp32 by the caller (R9). */
@@ -283,6 +290,34 @@ size_t canon_qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K);
 canon_status canon_state_hash(int64_t n_tensors, const void* const* ptrs, const int64_t* nbytes, uint8_t* digest,
                               void* workspace, size_t workspace_bytes, void* stream);
 size_t canon_state_hash_workspace_bytes(int64_t n_tensors, const int64_t* nbytes);
+
+/* ------------------------------------------------------------------------------------------------ */
+/* Attention kernels of the paper's int8 path (training-details paragraph on int8 computation: the flash
+   forward's P.V quantised to int8 per block on the integer matrix cores; the flash backward accumulating
+   the query gradient in 64-bit fixed point).  Layouts as inside the decoder block: P and dS bf16
+   [batch][n_heads][seq][seq] (row = query); V and K bf16 [batch][n_kv_heads][seq][head_dim]; O and dQ
+   [batch][seq][n_heads * head_dim], head h at columns h * head_dim.  Query head h reads key/value head
+   h / (n_heads / n_kv_heads).  Query i sees keys j <= i, and j > i - window when window > 0; entries of P
+   and dS outside that set are not read (taken as +0).
+
+   canon_attn_pv_i8 (R17): blocks of 64 queries x 64 keys of P and 64 keys x head_dim of V each get the step
+     RN(amax * RN(1/127)) (amax by bit pattern), codes clamp(rne(RN(x / step)), -128, 127); a P block times a
+     V block is an exact int32 sum, dequantised as RN(RN(RN32(acc) * sP) * sV); O is the R1 sum of these
+     terms over key blocks in ascending order.  Writes O as fp32 (o_f32) and/or bf16 (o_bf16), either may
+     be NULL.  head_dim a multiple of 32 up to 256; seq <= 8192.  workspace: device memory of
+     canon_attn_pv_i8_workspace_bytes(batch, n_kv_heads, seq, head_dim) bytes, 256-byte aligned (the V codes
+     and steps).
+   canon_attn_dq_fixed (R18): dQ[i][c] = the sum over visible keys j of fx(dS[i][j] * K[j][c]), where fx(p)
+     is the integer nearest to p * 2^frac_bits (ties to even), summed modulo 2^64 (the result is the same
+     for every order of the keys), then times 2^-frac_bits rounded once to fp32 under R0.  frac_bits in
+     [1, 62]; head_dim in {16, 32, 64, 128}. */
+size_t canon_attn_pv_i8_workspace_bytes(int64_t batch, int64_t n_kv_heads, int64_t seq, int64_t head_dim);
+canon_status canon_attn_pv_i8(int64_t batch, int64_t n_heads, int64_t n_kv_heads, int64_t seq, int64_t head_dim,
+                              int64_t window, const uint16_t* P, const uint16_t* V, float* o_f32, uint16_t* o_bf16,
+                              void* workspace, size_t workspace_bytes, void* stream);
+canon_status canon_attn_dq_fixed(int64_t batch, int64_t n_heads, int64_t n_kv_heads, int64_t seq, int64_t head_dim,
+                                 int64_t window, int32_t frac_bits, const uint16_t* dS, const uint16_t* K, float* dQ,
+                                 void* stream);
 
 /* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
    the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,

@@ -39,7 +39,8 @@ class ModelCfg(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
                 ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("n_kv_heads", ctypes.c_int32), ("qk_norm", ctypes.c_int32), ("embed_norm", ctypes.c_int32),
-                ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float)]
+                ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float),
+                ("pv_int8", ctypes.c_int32), ("dq_fixed_bits", ctypes.c_int32)]
 
 
 class AdamWConsts(ctypes.Structure):
@@ -90,6 +91,9 @@ def _lib():
             "canon_qlinear_bwd_workspace_bytes": (sz, [i64, i64, i64]),
             "canon_state_hash": (i32, [i64, vp, vp, vp, vp, sz, vp]),
             "canon_state_hash_workspace_bytes": (sz, [i64, vp]),
+            "canon_attn_pv_i8": (i32, [i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, sz, vp]),
+            "canon_attn_pv_i8_workspace_bytes": (sz, [i64, i64, i64, i64]),
+            "canon_attn_dq_fixed": (i32, [i64, i64, i64, i64, i64, i64, i32, vp, vp, vp, vp]),
             "canon_status_str": (ctypes.c_char_p, [i32]),
             "canon_version": (i32, []),
         }
@@ -165,6 +169,22 @@ def adamw(params, m, v, grads, decay_mask, consts: AdamWConsts, stream=None):
     mask = (ctypes.c_uint8 * n)(*[int(x) for x in decay_mask])
     _check(_lib().canon_adamw(n, sizes, _ptrs(params), _ptrs(m), _ptrs(v), _ptrs(grads), mask, ctypes.byref(consts),
                               _stream(stream)), "canon_adamw")
+
+
+def attn_pv_i8_workspace_bytes(batch, n_kv_heads, seq, head_dim) -> int:
+    return int(_lib().canon_attn_pv_i8_workspace_bytes(batch, n_kv_heads, seq, head_dim))
+
+
+def attn_pv_i8(batch, n_heads, n_kv_heads, seq, head_dim, window, P, V, workspace, o_f32=None, o_bf16=None,
+               stream=None):
+    _check(_lib().canon_attn_pv_i8(batch, n_heads, n_kv_heads, seq, head_dim, window, _ptr(P), _ptr(V), _ptr(o_f32),
+                                   _ptr(o_bf16), _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                   _stream(stream)), "canon_attn_pv_i8")
+
+
+def attn_dq_fixed(batch, n_heads, n_kv_heads, seq, head_dim, window, frac_bits, dS, K, dQ, stream=None):
+    _check(_lib().canon_attn_dq_fixed(batch, n_heads, n_kv_heads, seq, head_dim, window, frac_bits, _ptr(dS), _ptr(K),
+                                      _ptr(dQ), _stream(stream)), "canon_attn_dq_fixed")
 
 
 def block_workspace_bytes(cfg: ModelCfg, batch: int) -> int:

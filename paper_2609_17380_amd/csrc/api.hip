@@ -64,6 +64,7 @@ struct Dims {
   int64_t Hkv, G, kvw, N;  // key/value heads, query heads per group, key width Hkv*hd, fused projection width
   int64_t window;          // this block's attention window (0: full causal)
   int qk_norm;
+  int pv_int8, dq_bits;    // R17 int8 P.V; R18 fixed-point dQ with dq_bits fractional bits (0: off)
   float eps, scale, z_loss;
 };
 
@@ -92,6 +93,7 @@ Dims dims_of(const canon_model_cfg* c, int64_t B) {
   D.F = c->d_ffn; D.V = c->vocab; D.eps = c->rms_eps; D.scale = attn_scale(c->head_dim);
   D.Hkv = kv_heads(c); D.G = D.H / D.Hkv; D.kvw = D.Hkv * D.hd; D.N = D.d + 2 * D.kvw;
   D.window = c->swa_window; D.qk_norm = c->qk_norm; D.z_loss = c->z_loss;
+  D.pv_int8 = c->pv_int8; D.dq_bits = c->dq_fixed_bits;
   return D;
 }
 
@@ -103,10 +105,19 @@ bool cfg_ok(const canon_model_cfg* c) {
   if (c->n_kv_heads < 0 || (c->n_kv_heads > 0 && c->n_heads % c->n_kv_heads != 0)) return false;
   if ((c->qk_norm != 0 && c->qk_norm != 1) || (c->embed_norm != 0 && c->embed_norm != 1)) return false;
   if (c->swa_window < 0 || c->swa_full_every < 0 || !(c->z_loss >= 0.0f) || isinf(c->z_loss)) return false;
+  if ((c->pv_int8 != 0 && c->pv_int8 != 1) || c->dq_fixed_bits < 0 || c->dq_fixed_bits > 62) return false;
   const int64_t G = c->n_heads / kv_heads(c);
   return gemm_k_supported(c->vocab) && gemm_k_supported((int64_t)c->seq * c->micro_seqs) &&
          gemm_k_supported(2 * (int64_t)c->d_ffn) && gemm_k_supported(c->d_model + 2 * kv_heads(c) * c->head_dim) &&
          gemm_k_supported(G * (int64_t)c->seq);
+}
+
+// shapes the R17 and R18 kernels are built for
+bool attn_variants_supported(const canon_model_cfg* c) {
+  if (c->pv_int8 && (c->head_dim % 32 != 0 || c->head_dim > 256 || c->seq > 8192)) return false;
+  if (c->dq_fixed_bits && c->head_dim != 16 && c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
+    return false;
+  return true;
 }
 
 // activations a block saves for its backward pass
@@ -138,6 +149,8 @@ void carve_save(Carver& cv, const Dims& D, LayerSave& s) {
 struct Scratch {
   float *qkv, *scores, *tmp_d, *da, *dtmp, *dtmp2, *dh, *dq, *dk, *Dv;
   uint16_t *dy_b, *dgu, *dO, *dS, *dqkv, *dOh;
+  int8_t* qvt;  // R17: V codes, transposed per key block
+  float* sv;    // R17: V block steps
 };
 
 void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
@@ -158,6 +171,9 @@ void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
   s.dS = cv.take<uint16_t>(D.B * D.H * D.S * D.S);
   s.dqkv = cv.take<uint16_t>(T * D.N);
   s.dOh = D.G > 1 ? cv.take<uint16_t>(T * d) : nullptr;
+  const int64_t nb = attn_pv_blocks(D.S);
+  s.qvt = D.pv_int8 ? cv.take<int8_t>(D.B * D.Hkv * D.hd * nb * 64) : nullptr;
+  s.sv = D.pv_int8 ? cv.take<float>(D.B * D.Hkv * nb) : nullptr;
 }
 
 hipError_t gemm(const GemmArgs& g, hipStream_t s) { return gemm_launch(g, s); }
@@ -188,7 +204,9 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
     TRY(gemm(g, s));
   }
   TRY(softmax_causal_launch(D.B * H * S, S, sc.scores, D.scale, D.window, sv.P, s));
-  {  // O = P V (keys beyond the tile's last query are masked chunks), bf16 into [T, d]
+  if (D.pv_int8) {  // R17: O = P V on the int8 matrix cores, per block of 64 queries x 64 keys
+    TRY(attn_pv_i8_launch(D.B, H, Hkv, S, hd, D.window, sv.P, sv.v, nullptr, sv.O, d, sc.qvt, sc.sv, s));
+  } else {  // O = P V (keys beyond the tile's last query are masked chunks), bf16 into [T, d]
     GemmArgs g = batched(mk(0, 0, S, hd, S, sv.P, S, sv.v, hd, sv.O, d, 1), D, H * S * S, S * S, Hkv * S * hd,
                          S * hd, S * d, hd);
     g.kmode = KMODE_TRAIL;
@@ -241,7 +259,9 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
     g.ds_ldp = S; g.ds_sp1 = H * S * S; g.ds_sp2 = S * S; g.ds_sd1 = H * S; g.ds_sd2 = S;
     TRY(gemm(g, s));
   }
-  {  // dQ = dS K (over keys)
+  if (D.dq_bits) {  // R18: dQ = dS K accumulated in 64-bit fixed point
+    TRY(attn_dq_fixed_launch(D.B, H, Hkv, S, hd, D.window, D.dq_bits, sc.dS, sv.k, sc.dq, d, s));
+  } else {  // dQ = dS K (over keys)
     GemmArgs g = batched(mk(0, 0, S, hd, S, sc.dS, S, sv.k, hd, sc.dq, d), D, H * S * S, S * S, Hkv * S * hd,
                          S * hd, S * d, hd);
     g.kmode = KMODE_TRAIL;
@@ -740,6 +760,47 @@ canon_status canon_clip_grad_norm(const canon_order* order, int64_t n_tensors, c
   return CANON_OK;
 }
 
+size_t canon_attn_pv_i8_workspace_bytes(int64_t batch, int64_t n_kv_heads, int64_t seq, int64_t head_dim) {
+  if (batch < 1 || n_kv_heads < 1 || seq < 1 || head_dim < 1) return 0;
+  const int64_t nb = attn_pv_blocks(seq);
+  Carver cv(nullptr);
+  cv.take<int8_t>(batch * n_kv_heads * head_dim * nb * 64);
+  cv.take<float>(batch * n_kv_heads * nb);
+  return cv.off + 256;
+}
+
+canon_status canon_attn_pv_i8(int64_t batch, int64_t n_heads, int64_t n_kv_heads, int64_t seq, int64_t head_dim,
+                              int64_t window, const uint16_t* P, const uint16_t* V, float* o_f32, uint16_t* o_bf16,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  if (batch < 0 || n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads != 0 || seq < 1 || head_dim < 1 ||
+      window < 0)
+    return CANON_EINVAL;
+  if (head_dim % 32 != 0 || head_dim > 256 || seq > 8192 || batch * n_heads > 65535) return CANON_EUNSUPPORTED;
+  if (batch == 0) return CANON_OK;
+  if (!P || !V || (!o_f32 && !o_bf16) || !workspace || ((uintptr_t)workspace & 255)) return CANON_EINVAL;
+  if (workspace_bytes < canon_attn_pv_i8_workspace_bytes(batch, n_kv_heads, seq, head_dim)) return CANON_EWORKSPACE;
+  const int64_t nb = attn_pv_blocks(seq);
+  Carver cv(workspace);
+  int8_t* qvt = cv.take<int8_t>(batch * n_kv_heads * head_dim * nb * 64);
+  float* sv = cv.take<float>(batch * n_kv_heads * nb);
+  return dev(attn_pv_i8_launch(batch, n_heads, n_kv_heads, seq, head_dim, window, P, V, o_f32, o_bf16,
+                               n_heads * head_dim, qvt, sv, as_stream(stream)));
+}
+
+canon_status canon_attn_dq_fixed(int64_t batch, int64_t n_heads, int64_t n_kv_heads, int64_t seq, int64_t head_dim,
+                                 int64_t window, int32_t frac_bits, const uint16_t* dS, const uint16_t* K, float* dQ,
+                                 void* stream) {
+  if (batch < 0 || n_heads < 1 || n_kv_heads < 1 || n_heads % n_kv_heads != 0 || seq < 1 || head_dim < 1 ||
+      window < 0 || frac_bits < 1 || frac_bits > 62)
+    return CANON_EINVAL;
+  if ((head_dim != 16 && head_dim != 32 && head_dim != 64 && head_dim != 128) || batch * n_heads > 65535)
+    return CANON_EUNSUPPORTED;
+  if (batch == 0) return CANON_OK;
+  if (!dS || !K || !dQ) return CANON_EINVAL;
+  return dev(attn_dq_fixed_launch(batch, n_heads, n_kv_heads, seq, head_dim, window, frac_bits, dS, K, dQ,
+                                  n_heads * head_dim, as_stream(stream)));
+}
+
 canon_status canon_devmath(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
                            void* stream) {
   if (op < 0 || op > 10 || n < 0) return CANON_EINVAL;
@@ -768,6 +829,7 @@ canon_status canon_block_fwd_bwd(const canon_order* order, const canon_model_cfg
   if (st != CANON_OK) return st;
   if (!cfg_ok(cfg) || batch < 1 || !x || !dy || !w || !rope_cos || !rope_sin || !y || !dx || !dw)
     return CANON_EINVAL;
+  if (!attn_variants_supported(cfg)) return CANON_EUNSUPPORTED;
   for (int i = 0; i < 6; ++i)
     if (!w[i] || !dw[i]) return CANON_EINVAL;
   if ((int64_t)batch * cfg->n_heads > 65535) return CANON_EUNSUPPORTED;
@@ -808,6 +870,7 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
   if (st != CANON_OK) return st;
   if (!cfg_ok(cfg) || !plan || plan->accum < 1 || plan->dp_shard < 1 || plan->dp_replicate < 1) return CANON_EINVAL;
   if (!params || !m || !v || !windows || !rope_cos || !rope_sin || !consts || !loss_out) return CANON_EINVAL;
+  if (!attn_variants_supported(cfg)) return CANON_EUNSUPPORTED;
   if (clip && (!(clip->max_norm > 0.0f) || clip->skip_steps < 0 || (clip->skip_steps > 0 && !clip->skip_state)))
     return CANON_EINVAL;
   std::vector<int64_t> sz;

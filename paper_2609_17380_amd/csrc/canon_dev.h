@@ -114,6 +114,27 @@ __device__ __forceinline__ float csigmoid(float x) {
 
 __device__ __forceinline__ float csilu(float x) { return x * csigmoid(x); }
 
+// Quantiser of the int8 quantised linear: q = clamp(rne(RN(x / s)), -128, 127), x fp32 (dtype 0) or bf16
+// (dtype 1), one step per row or for the whole tensor.  A step that is not > 0 once flushed, or a NaN
+// quotient, gives 0.
+__device__ __forceinline__ int8_t quant1(float v, float sv) {
+  int8_t out = 0;
+  if (sv > 0.0f) {
+    const float t = v / sv;
+    if (t == t) {
+      const float r = __builtin_rintf(t);
+      out = (int8_t)(int)fminf(fmaxf(r, -128.0f), 127.0f);
+    }
+  }
+  return out;
+}
+
+__device__ __forceinline__ float step_daz(float s) {
+  uint32_t sb = __float_as_uint(s);
+  if ((sb & 0x7F800000u) == 0u) sb &= 0x80000000u;  // a subnormal step reads as zero
+  return __uint_as_float(sb);
+}
+
 // ---- R1 helpers ---------------------------------------------------------------------------------
 // Algorithm 2 over nparts chunk partials held one per lane of a wavefront (lane = chunk index, lanes
 // >= nparts ignored): level by level, a node adds its right neighbour's subtree only when that subtree

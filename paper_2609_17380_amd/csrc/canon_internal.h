@@ -158,6 +158,15 @@ hipError_t plan_scale_launch(int64_t n, const float* x, float inv, float* out, h
 // gscale (may be null): the gradient is taken as RN(g * *gscale) when *gscale < 1 (the R15 clip)
 hipError_t adamw_launch(int64_t n, uint16_t* p, float* m, float* v, const float* g, int decay, const float* consts9,
                         const float* gscale, const int32_t* skip_flag, hipStream_t s);
+// R17 int8 P.V per block (attn_i8.hip): qvt int8 [B][Hkv][hd][64 nb] and sv fp32 [B][Hkv][nb] are scratch,
+// nb = attn_pv_blocks(S); hd a multiple of 32 up to 256, S up to 8192.  R18 fixed-point dQ: hd in
+// {16, 32, 64, 128}, F in [1, 62].
+int64_t attn_pv_blocks(int64_t S);
+hipError_t attn_pv_i8_launch(int64_t B, int64_t H, int64_t Hkv, int64_t S, int64_t hd, int64_t window,
+                             const uint16_t* P, const uint16_t* V, float* of, uint16_t* ob, int64_t ldo, int8_t* qvt,
+                             float* sv, hipStream_t s);
+hipError_t attn_dq_fixed_launch(int64_t B, int64_t H, int64_t Hkv, int64_t S, int64_t hd, int64_t window, int F,
+                                const uint16_t* dS, const uint16_t* K, float* dQ, int64_t ldq, hipStream_t s);
 hipError_t set_nan_if_launch(const int32_t* flag, float* x, hipStream_t s);
 
 }  // namespace canon

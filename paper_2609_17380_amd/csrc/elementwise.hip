@@ -648,27 +648,6 @@ hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win,
   return hipGetLastError();
 }
 
-// Quantiser of the int8 quantised linear: q = clamp(rne(RN(x / s)), -128, 127), x fp32 (dtype 0) or bf16
-// (dtype 1), one step per row or for the whole tensor.  A step that is not > 0 once flushed, or a NaN
-// quotient, gives 0.
-__device__ __forceinline__ int8_t quant1(float v, float sv) {
-  int8_t out = 0;
-  if (sv > 0.0f) {
-    const float t = v / sv;
-    if (t == t) {
-      const float r = __builtin_rintf(t);
-      out = (int8_t)(int)fminf(fmaxf(r, -128.0f), 127.0f);
-    }
-  }
-  return out;
-}
-
-__device__ __forceinline__ float step_daz(float s) {
-  uint32_t sb = __float_as_uint(s);
-  if ((sb & 0x7F800000u) == 0u) sb &= 0x80000000u;  // a subnormal step reads as zero
-  return __uint_as_float(sb);
-}
-
 template <int DT>
 __global__ void quantize_kernel(int64_t rows, int64_t cols, const void* __restrict__ x,
                                 const float* __restrict__ scale, int32_t per_row, int8_t* __restrict__ q) {
