@@ -26,6 +26,7 @@ PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s
 PEAK_INT8_MFMA = 5000.0  # TOP/s, MI355X dense int8 matrix
+PEAK_VALU_OPS = 39.3     # T lane-operations/s: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (fp32 or fp64 FMA issue rate)
 
 L, D, H, HD, F, V, S, MB = 16, 2048, 16, 128, 8192, 50304, 2048, 4
 PLAN = (1, 8, 1)
@@ -257,10 +258,46 @@ def kernel_table(C, I, torch, np, stream, dev):
                                     "frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA, 4)}
     del xb, dyb, w, dw, yb, dxb, wsb
     torch.cuda.empty_cache()
+    out.update(int8_attention(C, torch, stream, dev, randn))
     out.update(open1b_step(C, I, torch, np, stream, dev))
+    out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
     for k_, v_ in out.items():
         print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({100 * v_['frac']:.1f}%)",
               file=sys.stderr, flush=True)
+    return out
+
+
+def int8_attention(C, torch, stream, dev, randn):
+    """The int8 path's attention kernels at the paper's shape (4 sequences x 16 heads (4 key/value heads) x 4096
+    tokens, head_dim 128), full causal and 512-token window: P.V in int8 per block (bound by reading P once:
+    2 bytes per visible entry, plus V and O) and dQ in 64-bit fixed point (bound by the VALU: one binary64 fma
+    and a 64-bit add, 3 lane-operations, per product)."""
+    o = O1B
+    B, Hh, Hkv, Ss, hd = o["mb"], o["H"], o["Hkv"], o["S"], o["hd"]
+    out = {}
+    P = randn((B, Hh, Ss, Ss), 1e-3, torch.bfloat16).abs()
+    Vt = randn((B, Hkv, Ss, hd), 1.0, torch.bfloat16)
+    ob = torch.empty((B, Ss, Hh * hd), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(C.attn_pv_i8_workspace_bytes(B, Hkv, Ss, hd), dtype=torch.uint8, device=dev)
+    dQ = torch.empty((B, Ss, Hh * hd), dtype=torch.float32, device=dev)
+    for window in (0, o["window"]):
+        pairs = attn_pairs(Ss, window)
+        ms = _timed(torch, stream, lambda: C.attn_pv_i8(B, Hh, Hkv, Ss, hd, window, P, Vt, ws, o_bf16=ob,
+                                                       stream=stream), 3)
+        nbytes = 2 * B * Hh * pairs + 2 * B * Hkv * Ss * hd + 2 * B * Ss * Hh * hd
+        e = _hbm(ms, nbytes)
+        e["int8_tops"] = round(2.0 * B * Hh * pairs * hd / (ms * 1e-3) / 1e12, 1)
+        out[f"attn_pv_i8_{B}x{Hh}x{Ss}x{hd}_w{window}"] = e
+        ms = _timed(torch, stream, lambda: C.attn_dq_fixed(B, Hh, Hkv, Ss, hd, window, 40, P, Vt, dQ,
+                                                          stream=stream), 3)
+        prods = B * Hh * pairs * hd
+        ops = 3.0 * prods / (ms * 1e-3) / 1e12
+        out[f"attn_dq_fixed_{B}x{Hh}x{Ss}x{hd}_w{window}"] = {
+            "bound": "alu", "ms": round(ms, 4), "achieved": round(ops, 2), "unit": "T lane-op/s",
+            "peak": PEAK_VALU_OPS, "frac": round(ops / PEAK_VALU_OPS, 4),
+            "products_per_s": round(prods / (ms * 1e-3), 1)}
+    del P, Vt, ob, ws, dQ
+    torch.cuda.empty_cache()
     return out
 
 
@@ -270,13 +307,14 @@ def kernel_table(C, I, torch, np, stream, dev):
 O1B = dict(L=24, d=2048, H=16, Hkv=4, hd=128, F=5632, V=128256, S=4096, mb=4, window=512, full_every=5)
 
 
-def open1b_step(C, I, torch, np, stream, dev):
+def open1b_step(C, I, torch, np, stream, dev, int8_attn=False):
     """One step of the paper's architecture with every variant on (one rank, one microbatch of 4 x 4096 tokens,
-    the clip at 1.0), timed after one warmup step."""
+    the clip at 1.0), timed after one warmup step.  int8_attn: also the int8 path's attention kernels (P.V in
+    int8 per block, dQ in 64-bit fixed point with 40 fractional bits)."""
     o = O1B
-    print("bench: open-1B step (all variants)", file=sys.stderr, flush=True)
+    print(f"bench: open-1B step (all variants{', int8 attention' if int8_attn else ''})", file=sys.stderr, flush=True)
     cfg = C.ModelCfg(o["L"], o["d"], o["H"], o["hd"], o["F"], o["V"], o["S"], o["mb"], np.float32(1e-5), o["Hkv"],
-                     1, 1, o["window"], o["full_every"], np.float32(1e-4))
+                     1, 1, o["window"], o["full_every"], np.float32(1e-4), int(int8_attn), 40 if int8_attn else 0)
     plan = C.DPPlan(1, 1, 1)
     params = I.model_params(o["L"], o["d"], o["F"], o["V"], seed=0, std=0.02, kv_dim=o["Hkv"] * o["hd"],
                             embed_norm=True)
@@ -302,7 +340,7 @@ def open1b_step(C, I, torch, np, stream, dev):
            "loss": float(loss.item()), "grad_norm_preclip": float(gnorm.item())}
     del ws, pg, mg, vg
     torch.cuda.empty_cache()
-    return {"step_open1b_4x4096_all_variants": res}
+    return {"step_open1b_4x4096_all_variants" + ("_int8_attention" if int8_attn else ""): res}
 
 
 def main():
@@ -314,7 +352,8 @@ def main():
     ap.add_argument("--gemm-reps", type=int, default=10)
     ap.add_argument("--no-kernel-table", action="store_true")
     ap.add_argument("--open1b-only", action="store_true",
-                    help="time only the paper-architecture step (all variants) and print its entry")
+                    help="time only the paper-architecture step (all variants; without and with the int8 "
+                         "attention kernels) and print its entries")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -332,7 +371,9 @@ def main():
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
     if args.open1b_only:
-        print(json.dumps(open1b_step(C, I, torch, np, stream, dev)), flush=True)
+        res = open1b_step(C, I, torch, np, stream, dev)
+        res.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
+        print(json.dumps(res), flush=True)
         return
     print("bench: generating inputs", file=sys.stderr, flush=True)
     t0 = time.time()

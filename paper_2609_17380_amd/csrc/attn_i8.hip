@@ -14,7 +14,7 @@
 // shifts: for |p 2^F| < 2^51, fma(dS 2^F, K, 1.5 2^52) in binary64 is 1.5 2^52 + rne(p 2^F) exactly (the
 // product of two 8-bit significands is exact, and numbers in [2^52, 2^53) are the integers), so the bit
 // pattern of that double is a constant plus fx(p); the constants are taken off once at the end.  A key tile
-// whose largest |dS| 2^F |K| is not below 2^51 takes an exact path that decomposes the product instead.
+// whose largest |dS| 2^F |K| is not below 2^51 takes a longer exact form for its products (fx_any).
 #include <hip/hip_runtime.h>
 
 #include "canon_dev.h"
@@ -26,7 +26,7 @@ namespace {
 
 constexpr int PVB = 64;                      // R17 block: queries and keys
 constexpr uint32_t kInv127Bits = 0x3C010204u;  // RN32(1/127)
-constexpr int DQK = 32;                      // R18 keys per staged tile
+constexpr int DQK = 16;                      // R18 keys per staged tile
 constexpr double kMagic = 0x1.8p52;          // 1.5 * 2^52
 constexpr uint64_t kMagicBits = 0x4338000000000000ull;
 
@@ -37,6 +37,18 @@ typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 __device__ __forceinline__ uint32_t bf16_mag(uint16_t h) {
   const uint32_t m = h & 0x7FFFu;
   return (m & 0x7F80u) ? m : 0u;
+}
+
+// R13's quantiser clamp(rne(RN(v / s)), -128, 127) for a step s > 0 (finite, normal) and |v| <= 128 s, from
+// t = RN(v * rs) with rs = RN(1 / s): |t - v/s| <= |v/s| (2^-23 + 2^-48) < 2^-16 and |RN(v/s) - v/s| <= 2^-17, so
+// when t is farther than 2^-15 from every half-integer, no rounding boundary separates t from RN(v / s) and
+// both round to the same integer.  Closer than that, the correctly rounded quotient decides.
+__device__ __forceinline__ int8_t quant_recip(float v, float s, float rs) {
+  const float t = v * rs;
+  const float n = __builtin_rintf(t);
+  const float d = fabsf(t - n);  // exact (Sterbenz), at most 1/2
+  if (0.5f - d > 0x1p-15f) return (int8_t)(int)fminf(fmaxf(n, -128.0f), 127.0f);
+  return quant1(v, s);
 }
 
 __device__ __forceinline__ uint32_t wave_umax(uint32_t v) {
@@ -92,13 +104,19 @@ struct PvArgs {
 };
 
 // One workgroup per (sequence, head, query block of 64).  Wavefront w owns rows 32 (w & 1) .. + 31 of the
-// block and the 32-column blocks (w >> 1), (w >> 1) + 2, ... of the head dimension (NCB of them).
+// block and the 32-column blocks (w >> 1), (w >> 1) + 2, ... of the head dimension (NCB of them).  Per key
+// block: the P tile (already in registers) is masked and its absmax reduced (shuffles, then four wavefront
+// maxima through LDS); the codes of P and of V go to LDS, while later key blocks' P tiles and V codes load
+// into registers and the matrix instructions and the dequantising chain run.  LDS tiles and the maxima
+// are double buffered, so each key block takes two barriers; the operands of the next three key blocks are
+// in flight in registers.
 template <int NCB>
 __global__ __launch_bounds__(256) void attn_pv_i8_kernel(PvArgs a) {
   constexpr int LD = PVB + 16;  // padded LDS row (bytes)
-  __shared__ __attribute__((aligned(16))) int8_t As[PVB * LD];
-  __shared__ __attribute__((aligned(16))) int8_t Bs[64 * NCB * LD];
-  __shared__ uint32_t red[4];
+  constexpr int NVQ = NCB;      // 16-byte V-code vectors per thread (hd * 4 vectors of a block / 256 threads)
+  __shared__ __attribute__((aligned(16))) int8_t As[2][PVB * LD];
+  __shared__ __attribute__((aligned(16))) int8_t Bs[2][64 * NCB * LD];
+  __shared__ uint32_t red[2][4];
   const int64_t S = a.S, W = a.window, hd = a.hd, nb = a.Sp / PVB;
   const int64_t qb = nb - 1 - (int64_t)blockIdx.x;  // longest rows first
   const int64_t bh = blockIdx.y, b = bh / a.H, h = bh % a.H, g = h / (a.H / a.Hkv);
@@ -115,115 +133,190 @@ __global__ __launch_bounds__(256) void attn_pv_i8_kernel(PvArgs a) {
   const int pr = threadIdx.x >> 2, pc = 16 * (threadIdx.x & 3);
   const int64_t pi = i0 + pr;
 
+  // 16 bf16 values as 8 words (element e in the low or high half of word e / 2)
+  auto load_p = [&](int64_t kb, uint32_t (&pw)[8]) __attribute__((always_inline)) {
+    const int64_t k0 = kb * PVB;
+    if (a.vec && pi < S && k0 + pc + 16 <= S) {
+      const uint4 u0 = *reinterpret_cast<const uint4*>(Ph + pi * S + k0 + pc);
+      const uint4 u1 = *reinterpret_cast<const uint4*>(Ph + pi * S + k0 + pc + 8);
+      pw[0] = u0.x; pw[1] = u0.y; pw[2] = u0.z; pw[3] = u0.w;
+      pw[4] = u1.x; pw[5] = u1.y; pw[6] = u1.z; pw[7] = u1.w;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t j = k0 + pc + 2 * e;
+        const uint32_t lo = (pi < S && j < S) ? Ph[pi * S + j] : 0u;
+        const uint32_t hi = (pi < S && j + 1 < S) ? Ph[pi * S + j + 1] : 0u;
+        pw[e] = lo | (hi << 16);
+      }
+    }
+  };
+  auto load_v = [&](int64_t kb, uint32_t (&vq)[4 * NVQ]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < NVQ; ++q) {
+      const int64_t v = threadIdx.x + 256 * q;
+      if (v < hd * 4) {
+        const uint4 u = *reinterpret_cast<const uint4*>(qv + (v >> 2) * a.Sp + kb * PVB + 16 * (v & 3));
+        vq[4 * q] = u.x; vq[4 * q + 1] = u.y; vq[4 * q + 2] = u.z; vq[4 * q + 3] = u.w;
+      }
+    }
+  };
+
   float ch[NCB][16], pend[NCB][16], lvl1[NCB][16];
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
     for (int v = 0; v < 16; ++v) { ch[cb][v] = 0.0f; pend[cb][v] = 0.0f; lvl1[cb][v] = 0.0f; }
-
-  const int64_t c_hi = kb_hi / 32;
-  for (int64_t c = 0; c <= c_hi; ++c) {
+  // chain c of the R1 sum over key blocks is finished: Algorithm 2 over at most four chain partials (uniform
+  // branches with whole-array loops, so the arrays stay in registers)
+  auto finish_chain = [&](int64_t c) __attribute__((always_inline)) {
+    if ((c & 1) == 0) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) pend[cb][v] = ch[cb][v];
+    } else if (c == 1) {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) lvl1[cb][v] = pend[cb][v] + ch[cb][v];
+    } else {
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) lvl1[cb][v] = lvl1[cb][v] + (pend[cb][v] + ch[cb][v]);
+    }
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
       for (int v = 0; v < 16; ++v) ch[cb][v] = 0.0f;
-    const int64_t kb_a = (32 * c > kb_lo) ? 32 * c : kb_lo;
-    const int64_t kb_b = (32 * c + 32 < kb_hi + 1) ? 32 * c + 32 : kb_hi + 1;
-    for (int64_t kb = kb_a; kb < kb_b; ++kb) {
-      const int64_t k0 = kb * PVB;
-      uint16_t pv[16];
-      if (a.vec && pi < S && k0 + pc + 16 <= S) {
-        const uint4 u0 = *reinterpret_cast<const uint4*>(Ph + pi * S + k0 + pc);
-        const uint4 u1 = *reinterpret_cast<const uint4*>(Ph + pi * S + k0 + pc + 8);
-        const uint32_t wv[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) { pv[2 * e] = (uint16_t)(wv[e] & 0xFFFFu); pv[2 * e + 1] = (uint16_t)(wv[e] >> 16); }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int64_t j = k0 + pc + e;
-          pv[e] = (pi < S && j < S) ? Ph[pi * S + j] : (uint16_t)0;
-        }
-      }
-      uint32_t m = 0;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int64_t j = k0 + pc + e;
-        const bool seen = pi < S && j <= pi && (W == 0 || j > pi - W);
-        if (!seen) pv[e] = 0;
-        m = max(m, bf16_mag(pv[e]));
-      }
-      m = block_umax(m, red);
-      const float sp = __uint_as_float(m << 16) * __uint_as_float(kInv127Bits);
-      const float spd = step_daz(sp);
-      uint32_t word[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        uint32_t x = 0;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x |= (uint32_t)(uint8_t)quant1(bf16_to_f32(pv[4 * q + e]), spd) << (8 * e);
-        word[q] = x;
-      }
-      *reinterpret_cast<uint4*>(As + pr * LD + pc) = make_uint4(word[0], word[1], word[2], word[3]);
-      for (int64_t v = threadIdx.x; v < hd * 4; v += 256) {
-        const int64_t col = v >> 2, seg = 16 * (v & 3);
-        *reinterpret_cast<uint4*>(Bs + col * LD + seg) = *reinterpret_cast<const uint4*>(qv + col * a.Sp + k0 + seg);
-      }
-      __syncthreads();
-      const float svk = svh[kb];
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        const int colb = cw + 2 * cb;
-        if (32 * colb < hd) {
-          i32x16 acc;
-#pragma unroll
-          for (int v = 0; v < 16; ++v) acc[v] = 0;
-#pragma unroll
-          for (int ks = 0; ks < 2; ++ks) {
-            const int kk = 32 * ks + 16 * (lane >> 5);
-            const i32x4 av = *reinterpret_cast<const i32x4*>(As + (32 * rh + (lane & 31)) * LD + kk);
-            const i32x4 bv = *reinterpret_cast<const i32x4*>(Bs + (32 * colb + (lane & 31)) * LD + kk);
-            acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(av, bv, acc, 0, 0, 0);
-          }
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const float t = (float)acc[v] * sp;  // RN32 of the integer, then the two dequantising roundings
-            const float y = t * svk;
-            ch[cb][v] = ch[cb][v] + y;
-          }
-        }
-      }
-      __syncthreads();
+  };
+
+  // chains wholly before the first visible block hold +0: with pend = lvl1 = +0 the fold state is already
+  // what finishing them would leave
+  int64_t cur_c = kb_lo / 32;
+  // one key block: its operands (pws, vqs, svs) were loaded three blocks earlier; once staged, the same
+  // registers receive the operands of block kb + 3
+  auto step = [&](int64_t kb, int buf, uint32_t (&pws)[8], uint32_t (&vqs)[4 * NVQ], float& svs)
+                  __attribute__((always_inline)) {
+    if ((kb & 31) == 0 && kb != kb_lo) {  // the previous block closed chain cur_c
+      finish_chain(cur_c);
+      ++cur_c;
     }
-    // chain c is finished: Algorithm 2 over at most four chain partials
+    const int64_t k0 = kb * PVB;
+    uint32_t pwv[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pwv[e] = pws[e];
+    uint32_t m = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t j = k0 + pc + e;
+      const bool seen = pi < S && j <= pi && (W == 0 || j > pi - W);
+      const uint32_t keep = seen ? (0xFFFFu << (16 * (e & 1))) : 0u;
+      pwv[e >> 1] &= keep | (0xFFFFu << (16 * ((e & 1) ^ 1)));
+      m = max(m, bf16_mag((uint16_t)(pwv[e >> 1] >> (16 * (e & 1)))));
+    }
+    m = wave_umax(m);
+    if (lane == 0) red[buf][w] = m;
+    __syncthreads();
+    m = max(max(red[buf][0], red[buf][1]), max(red[buf][2], red[buf][3]));
+    const float sp = __uint_as_float(m << 16) * __uint_as_float(kInv127Bits);
+    const float spd = step_daz(sp);
+    // every |p| <= amax, so |p / sp| < 128 whenever the step is a positive finite number (normal after the flush)
+    const bool recip = spd > 0.0f && spd < __builtin_inff();
+    const float rsp = recip ? 1.0f / spd : 0.0f;
+    uint32_t word0 = 0, word1 = 0, word2 = 0, word3 = 0;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const float pf = bf16_to_f32((uint16_t)(pwv[e >> 1] >> (16 * (e & 1))));
+      const int8_t c = recip ? quant_recip(pf, spd, rsp) : quant1(pf, spd);
+      const uint32_t bits = (uint32_t)(uint8_t)c << (8 * (e & 3));
+      if (e < 4) word0 |= bits;
+      else if (e < 8) word1 |= bits;
+      else if (e < 12) word2 |= bits;
+      else word3 |= bits;
+    }
+    *reinterpret_cast<uint4*>(As[buf] + pr * LD + pc) = make_uint4(word0, word1, word2, word3);
+#pragma unroll
+    for (int q = 0; q < NVQ; ++q) {
+      const int64_t v = threadIdx.x + 256 * q;
+      if (v < hd * 4)
+        *reinterpret_cast<uint4*>(Bs[buf] + (v >> 2) * LD + 16 * (v & 3)) =
+            make_uint4(vqs[4 * q], vqs[4 * q + 1], vqs[4 * q + 2], vqs[4 * q + 3]);
+    }
+    const float svk = svs;
+    if (kb + 3 <= kb_hi) {
+      load_p(kb + 3, pws);
+      load_v(kb + 3, vqs);
+      svs = svh[kb + 3];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      const int colb = cw + 2 * cb;
+      if (32 * colb < hd) {
+        i32x16 acc;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[v] = 0;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          const int kk = 32 * ks + 16 * (lane >> 5);
+          const i32x4 av = *reinterpret_cast<const i32x4*>(As[buf] + (32 * rh + (lane & 31)) * LD + kk);
+          const i32x4 bv = *reinterpret_cast<const i32x4*>(Bs[buf] + (32 * colb + (lane & 31)) * LD + kk);
+          acc = __builtin_amdgcn_mfma_i32_32x32x32_i8(av, bv, acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const float t = (float)acc[v] * sp;  // RN32 of the integer, then the two dequantising roundings
+          const float y = t * svk;
+          ch[cb][v] = ch[cb][v] + y;
+        }
+      }
+    }
+  };
+
+  uint32_t pa[8], pb[8], pcx[8];
+  uint32_t va[4 * NVQ], vb[4 * NVQ], vc[4 * NVQ];
+  float sa = 0.0f, sb = 0.0f, sc = 0.0f;
+  load_p(kb_lo, pa); load_v(kb_lo, va); sa = svh[kb_lo];
+  if (kb_lo + 1 <= kb_hi) { load_p(kb_lo + 1, pb); load_v(kb_lo + 1, vb); sb = svh[kb_lo + 1]; }
+  if (kb_lo + 2 <= kb_hi) { load_p(kb_lo + 2, pcx); load_v(kb_lo + 2, vc); sc = svh[kb_lo + 2]; }
+  for (int64_t kb = kb_lo; kb <= kb_hi; kb += 3) {
+    step(kb, 0, pa, va, sa);
+    if (kb + 1 <= kb_hi) step(kb + 1, 1, pb, vb, sb);
+    if (kb + 2 <= kb_hi) step(kb + 2, 0, pcx, vc, sc);
+  }
+  finish_chain(cur_c);
+  const int64_t nc = cur_c + 1;  // chains after the last seen block hold +0 and change nothing
+  // the fold's result: one chain, pend; two or four, lvl1; three, lvl1 + pend (into ch)
+  if (nc == 1) {
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        if ((c & 1) == 0) {
-          pend[cb][v] = ch[cb][v];
-        } else {
-          const float pair = pend[cb][v] + ch[cb][v];
-          lvl1[cb][v] = (c == 1) ? pair : lvl1[cb][v] + pair;
-        }
-      }
+      for (int v = 0; v < 16; ++v) ch[cb][v] = pend[cb][v];
+  } else if (nc == 3) {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) ch[cb][v] = lvl1[cb][v] + pend[cb][v];
+  } else {
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) ch[cb][v] = lvl1[cb][v];
   }
-  const int64_t nc = c_hi + 1;  // chains after the last seen block hold +0 and change nothing
 #pragma unroll
   for (int cb = 0; cb < NCB; ++cb) {
     const int colb = cw + 2 * cb;
     if (32 * colb >= hd) continue;
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
-      float r = pend[cb][v];
-      if (nc == 2 || nc == 4) r = lvl1[cb][v];
-      else if (nc == 3) r = lvl1[cb][v] + pend[cb][v];
       const int64_t i = i0 + 32 * rh + (v & 3) + 4 * (lane >> 5) + 8 * (v >> 2);
       const int64_t col = 32 * colb + (lane & 31);
       if (i < S) {
         const int64_t o = (b * S + i) * a.ldo + h * hd + col;
-        if (a.of) a.of[o] = r;
-        if (a.ob) a.ob[o] = f32_to_bf16(r);
+        if (a.of) a.of[o] = ch[cb][v];
+        if (a.ob) a.ob[o] = f32_to_bf16(ch[cb][v]);
       }
     }
   }
@@ -231,23 +324,19 @@ __global__ __launch_bounds__(256) void attn_pv_i8_kernel(PvArgs a) {
 
 // ---- R18 ----------------------------------------------------------------------------------------------
 
-// fx of an exact binary64 product x of two 8-bit significands (any magnitude): nearest integer, ties to
-// even, modulo 2^64
-__device__ __noinline__ uint64_t fx_exact(double x) {
-  if (x == 0.0) return 0;
+// fx of an exact binary64 product x of two 8-bit significands, any magnitude, without branches.  Below 2^51
+// the magic-number rounding applies.  Otherwise x = m 2^e with m < 2^16 and e >= 35 is an integer divisible
+// by 2^35, and fx(x) = x modulo 2^64: |x| minus its multiple of 2^64 is exact (a multiple of 2^35 below
+// 2^64), and is hi 2^32 with hi < 2^32 an exact unsigned conversion; the sign is applied modulo 2^64.
+__device__ __forceinline__ uint64_t fx_any(double x) {
   const double ax = fabs(x);
-  uint64_t u;
-  if (ax < 0x1p52) {
-    u = (uint64_t)rint(ax);  // rounds half to even; below 2^52, so the conversion is exact
-  } else {
-    // an integer: significand M (53 bits) times 2^(E - 52); modulo 2^64 the bits shifted past 63 vanish
-    const uint64_t bitsx = __double_as_longlong(ax);
-    const int64_t E = (int64_t)((bitsx >> 52) & 0x7FF) - 1023;
-    const uint64_t M = (bitsx & 0xFFFFFFFFFFFFFull) | (1ull << 52);
-    const int64_t sh = E - 52;
-    u = sh >= 64 ? 0ull : (M << sh);
-  }
-  return x < 0.0 ? (uint64_t)0 - u : u;
+  const uint64_t small = (uint64_t)__double_as_longlong(__builtin_fma(x, 1.0, kMagic)) - kMagicBits;
+  const double q = trunc(ax * 0x1p-64);
+  const double r = __builtin_fma(-q, 0x1p64, ax);
+  const uint32_t hi = (uint32_t)(r * 0x1p-32);
+  uint64_t big = (uint64_t)hi << 32;
+  big = x < 0.0 ? (uint64_t)0 - big : big;
+  return ax < 0x1p51 ? small : big;
 }
 
 // RN32 of (wrapped sum as int64) * 2^-F under R0: one rounding to 24 bits, then a flush below 2^-126
@@ -279,99 +368,179 @@ struct DqArgs {
   float* dQ;           // [B][S][ldq], head h at columns h hd ..
   int64_t S, H, Hkv, hd, window, ldq;
   int F;
-  int vec;  // 16-byte loads of dS rows allowed
+  int vec;  // 16-byte loads of dS and K rows allowed
 };
 
-// One workgroup per (sequence, head, query block of 64); thread t accumulates rows 4 (t / 16) .. + 3 and
-// columns C (t % 16) .. + C - 1 (hd = 16 C) in 64-bit integers.
-template <int C>
-__global__ __launch_bounds__(256) void attn_dq_fixed_kernel(DqArgs a) {
+constexpr int DQB = 128;  // R18 query rows per workgroup
+
+// The key tiles of one query block, summed into acc.  EXACT = false: the magic-number form (fast); a tile
+// whose bound |dS| 2^F |K| reaches 2^51 makes the call return true, and the caller runs the tiles again with
+// EXACT = true (fx_any for every product).  Key tiles of 16: the staged tile is converted to binary64 in
+// LDS (dS times 2^F, masked entries 0) while the next tile's bf16 values are loaded into registers; two
+// barriers per tile.
+template <int C, bool EXACT>
+__device__ __forceinline__ bool dq_tiles(const DqArgs& a, double (*ds_t)[DQB], double (*k_t)[16 * C],
+                                         uint32_t (*red)[2][4], uint64_t (&acc)[8][C], uint64_t& n_fast) {
   constexpr int HD = 16 * C;
-  __shared__ __attribute__((aligned(16))) double ds_t[DQK][64];  // [key][row]: dS 2^F, masked entries 0
-  __shared__ __attribute__((aligned(16))) double k_t[DQK][HD];   // [key][column]: K
-  __shared__ uint32_t red[4];
+  constexpr int KV = (DQK * HD / 8 + 255) / 256;  // 16-byte K vectors per thread per tile
   const int64_t S = a.S, W = a.window;
-  const int64_t nqb = (S + 63) / 64;
+  const int64_t nqb = (S + DQB - 1) / DQB;
   const int64_t qb = nqb - 1 - (int64_t)blockIdx.x;  // longest rows first
   const int64_t bh = blockIdx.y, b = bh / a.H, h = bh % a.H, g = h / (a.H / a.Hkv);
-  const int64_t i0 = qb * 64, i1 = (i0 + 64 < S) ? i0 + 64 : S;
+  const int64_t i0 = qb * DQB, i1 = (i0 + DQB < S) ? i0 + DQB : S;
   const uint16_t* dSh = a.dS + bh * S * S;
   const uint16_t* Kh = a.K + (b * a.Hkv + g) * S * HD;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int rg = threadIdx.x >> 4, cg = threadIdx.x & 15;
   const double two_f = ldexp(1.0, a.F);
-  uint64_t acc[4][C];
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-#pragma unroll
-    for (int c = 0; c < C; ++c) acc[r][c] = 0;
   const int64_t jlo = (W > 0 && i0 - W + 1 > 0) ? i0 - W + 1 : 0;
   const int64_t t_lo = jlo / DQK, t_hi = (i1 - 1) / DQK;
-  uint64_t n_fast = 0;  // keys added through the fast path (each added kMagicBits once per output)
-  const int sr = threadIdx.x >> 2, sk = 8 * (threadIdx.x & 3);  // dS staging: row sr, keys sk .. sk + 7
+  const int sr = threadIdx.x >> 1, sk = 8 * (threadIdx.x & 1);  // dS staging: row sr, keys sk .. sk + 7
   const int64_t si = i0 + sr;
-  for (int64_t kt = t_lo; kt <= t_hi; ++kt) {
+  bool slow = false;
+
+  auto load_ds = [&](int64_t kt, uint16_t (&v)[8]) __attribute__((always_inline)) {
     const int64_t j0 = kt * DQK;
-    uint32_t dmag = 0, kmag = 0;
-    {
-      uint16_t v[8];
-      if (a.vec && si < S && j0 + sk + 8 <= S) {
-        const uint4 u = *reinterpret_cast<const uint4*>(dSh + si * S + j0 + sk);
-        const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+    if (a.vec && si < S && j0 + sk + 8 <= S) {
+      const uint4 u = *reinterpret_cast<const uint4*>(dSh + si * S + j0 + sk);
+      const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
-        for (int e = 0; e < 4; ++e) { v[2 * e] = (uint16_t)(wv[e] & 0xFFFFu); v[2 * e + 1] = (uint16_t)(wv[e] >> 16); }
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int64_t j = j0 + sk + e;
-          v[e] = (si < S && j < S) ? dSh[si * S + j] : (uint16_t)0;
-        }
-      }
+      for (int e = 0; e < 4; ++e) { v[2 * e] = (uint16_t)(wv[e] & 0xFFFFu); v[2 * e + 1] = (uint16_t)(wv[e] >> 16); }
+    } else {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const int64_t j = j0 + sk + e;
-        const bool seen = si < S && j <= si && (W == 0 || j > si - W);
-        const uint16_t x = seen ? v[e] : (uint16_t)0;
-        dmag = max(dmag, bf16_mag(x));
-        ds_t[sk + e][sr] = (double)bf16_to_f32(x) * two_f;
+        v[e] = (si < S && j < S) ? dSh[si * S + j] : (uint16_t)0;
       }
     }
-    for (int e = threadIdx.x; e < DQK * HD; e += 256) {
-      const int kk = e / HD, col = e % HD;
-      const int64_t j = j0 + kk;
-      const uint16_t x = j < S ? Kh[j * HD + col] : (uint16_t)0;
-      kmag = max(kmag, bf16_mag(x));
-      k_t[kk][col] = (double)bf16_to_f32(x);
-    }
-    dmag = block_umax(dmag, red);  // its barriers also publish the staged tiles
-    kmag = block_umax(kmag, red);
-    const double bound = (double)__uint_as_float(dmag << 16) * two_f * (double)__uint_as_float(kmag << 16);
-    if (bound < 0x1p51) {
-      n_fast += DQK;
-#pragma unroll 4
-      for (int kk = 0; kk < DQK; ++kk) {
-        double dv[4], kv[C];
+  };
+  auto load_k = [&](int64_t kt, uint16_t (&v)[KV][8]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) dv[r] = ds_t[kk][4 * rg + r];
+    for (int q = 0; q < KV; ++q) {
+      const int e = threadIdx.x + 256 * q;  // vector e: key e / (HD / 8), columns 8 (e % (HD / 8)) ..
+      const int kk = e / (HD / 8), c0 = 8 * (e % (HD / 8));
+      const int64_t j = kt * DQK + kk;
+      if (kk < DQK && j < S) {
+        if (a.vec) {
+          const uint4 u = *reinterpret_cast<const uint4*>(Kh + j * HD + c0);
+          const uint32_t wv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int x = 0; x < 4; ++x) { v[q][2 * x] = (uint16_t)(wv[x] & 0xFFFFu); v[q][2 * x + 1] = (uint16_t)(wv[x] >> 16); }
+        } else {
+#pragma unroll
+          for (int x = 0; x < 8; ++x) v[q][x] = Kh[j * HD + c0 + x];
+        }
+      } else {
+#pragma unroll
+        for (int x = 0; x < 8; ++x) v[q][x] = 0;
+      }
+    }
+  };
+
+  uint16_t dv16[8], kv16[KV][8];
+  load_ds(t_lo, dv16);
+  load_k(t_lo, kv16);
+  int buf = 0;
+  for (int64_t kt = t_lo; kt <= t_hi; ++kt, buf ^= 1) {
+    const int64_t j0 = kt * DQK;
+    uint32_t dmag = 0, kmag = 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int64_t j = j0 + sk + e;
+      const bool seen = si < S && j <= si && (W == 0 || j > si - W);
+      const uint16_t x = seen ? dv16[e] : (uint16_t)0;
+      dmag = max(dmag, bf16_mag(x));
+      ds_t[sk + e][sr] = (double)bf16_to_f32(x) * two_f;
+    }
+#pragma unroll
+    for (int q = 0; q < KV; ++q) {
+      const int e = threadIdx.x + 256 * q;
+      const int kk = e / (HD / 8), c0 = 8 * (e % (HD / 8));
+      if (kk < DQK) {
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+          kmag = max(kmag, bf16_mag(kv16[q][x]));
+          k_t[kk][c0 + x] = (double)bf16_to_f32(kv16[q][x]);
+        }
+      }
+    }
+    if (!EXACT) {
+      dmag = wave_umax(dmag);
+      kmag = wave_umax(kmag);
+      if (lane == 0) { red[buf][0][w] = dmag; red[buf][1][w] = kmag; }
+    }
+    __syncthreads();
+    if (kt < t_hi) {  // the next tile travels while this one is multiplied
+      load_ds(kt + 1, dv16);
+      load_k(kt + 1, kv16);
+    }
+    if (!EXACT) {
+      dmag = max(max(red[buf][0][0], red[buf][0][1]), max(red[buf][0][2], red[buf][0][3]));
+      kmag = max(max(red[buf][1][0], red[buf][1][1]), max(red[buf][1][2], red[buf][1][3]));
+      const double bound = (double)__uint_as_float(dmag << 16) * two_f * (double)__uint_as_float(kmag << 16);
+      slow |= !(bound < 0x1p51);
+      n_fast += DQK;
+#pragma unroll 1
+      for (int kk = 0; kk < DQK; ++kk) {
+        double dv[8], kv[C];
+#pragma unroll
+        for (int r = 0; r < 8; ++r) dv[r] = ds_t[kk][8 * rg + r];
 #pragma unroll
         for (int c = 0; c < C; ++c) kv[c] = k_t[kk][C * cg + c];
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < 8; ++r)
 #pragma unroll
           for (int c = 0; c < C; ++c) acc[r][c] += (uint64_t)__double_as_longlong(__builtin_fma(dv[r], kv[c], kMagic));
       }
     } else {
-      for (int kk = 0; kk < DQK; ++kk)
+#pragma unroll 1
+      for (int kk = 0; kk < DQK; ++kk) {
+        double dv[8], kv[C];
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int r = 0; r < 8; ++r) dv[r] = ds_t[kk][8 * rg + r];
 #pragma unroll
-          for (int c = 0; c < C; ++c) acc[r][c] += fx_exact(ds_t[kk][4 * rg + r] * k_t[kk][C * cg + c]);
+        for (int c = 0; c < C; ++c) kv[c] = k_t[kk][C * cg + c];
+#pragma unroll
+        for (int r = 0; r < 8; ++r)
+#pragma unroll
+          for (int c = 0; c < C; ++c) acc[r][c] += fx_any(dv[r] * kv[c]);
+      }
     }
     __syncthreads();
   }
+  return slow;
+}
+
+// One workgroup per (sequence, head, query block of 128); thread t accumulates rows 8 (t / 16) .. + 7 and
+// columns C (t % 16) .. + C - 1 (hd = 16 C) in 64-bit integers.
+template <int C>
+__global__ __launch_bounds__(256) void attn_dq_fixed_kernel(DqArgs a) {
+  constexpr int HD = 16 * C;
+  __shared__ __attribute__((aligned(16))) double ds_t[DQK][DQB];  // [key][row]
+  __shared__ __attribute__((aligned(16))) double k_t[DQK][HD];    // [key][column]
+  __shared__ uint32_t red[2][2][4];
+  uint64_t acc[8][C];
+#pragma unroll
+  for (int r = 0; r < 8; ++r)
+#pragma unroll
+    for (int c = 0; c < C; ++c) acc[r][c] = 0;
+  uint64_t n_fast = 0;  // keys added through the fast form (each added kMagicBits once per output)
+  if (dq_tiles<C, false>(a, ds_t, k_t, red, acc, n_fast)) {  // uniform over the workgroup
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int c = 0; c < C; ++c) acc[r][c] = 0;
+    n_fast = 0;
+    dq_tiles<C, true>(a, ds_t, k_t, red, acc, n_fast);
+  }
+  const int64_t S = a.S;
+  const int64_t qb = (S + DQB - 1) / DQB - 1 - (int64_t)blockIdx.x;
+  const int64_t bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  const int rg = threadIdx.x >> 4, cg = threadIdx.x & 15;
   const uint64_t bias = n_fast * kMagicBits;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int64_t i = i0 + 4 * rg + r;
+  for (int r = 0; r < 8; ++r) {
+    const int64_t i = qb * DQB + 8 * rg + r;
     if (i >= S) continue;
 #pragma unroll
     for (int c = 0; c < C; ++c)
@@ -407,8 +576,8 @@ hipError_t attn_dq_fixed_launch(int64_t B, int64_t H, int64_t Hkv, int64_t S, in
   DqArgs a;
   a.dS = dS; a.K = K; a.dQ = dQ;
   a.S = S; a.H = H; a.Hkv = Hkv; a.hd = hd; a.window = window; a.ldq = ldq; a.F = F;
-  a.vec = (S % 8 == 0) && (((uintptr_t)dS & 15) == 0);
-  const dim3 grid((unsigned)((S + 63) / 64), (unsigned)(B * H));
+  a.vec = (S % 8 == 0) && (((uintptr_t)dS & 15) == 0) && (((uintptr_t)K & 15) == 0);
+  const dim3 grid((unsigned)((S + DQB - 1) / DQB), (unsigned)(B * H));
   switch (hd) {
     case 16: hipLaunchKernelGGL(attn_dq_fixed_kernel<1>, grid, dim3(256), 0, s, a); break;
     case 32: hipLaunchKernelGGL(attn_dq_fixed_kernel<2>, grid, dim3(256), 0, s, a); break;
