@@ -36,7 +36,7 @@ class ModelCfg(ctypes.Structure):
                 ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("n_kv_heads", ctypes.c_int32), ("qk_norm", ctypes.c_int32), ("embed_norm", ctypes.c_int32),
                 ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float),
-                ("pv_int8", ctypes.c_int32), ("dq_fixed_bits", ctypes.c_int32)]
+                ("pv_int8", ctypes.c_int32), ("dq_fixed_bits", ctypes.c_int32), ("int8_linear", ctypes.c_int32)]
 
 
 class Plan(ctypes.Structure):
@@ -94,6 +94,7 @@ def _load():
             "cref_attn_dq_fixed": (ctypes.c_int, [i64, i64, i64, i32, vp, vp, vp]),
             "cref_fx_product": (ctypes.c_uint64, [ctypes.c_uint16, ctypes.c_uint16, i32]),
             "cref_fx_to_f32": (f, [ctypes.c_uint64, i32]),
+            "cref_lsq_step_grad": (f, [i64, i64, vp, f, vp]),
             "cref_num_threads": (ctypes.c_int, []),
         }
         for name, (res, args) in sig.items():
@@ -401,6 +402,14 @@ def fx_product(a: int, b: int, frac_bits: int) -> int:
 def fx_to_f32(total: int, frac_bits: int) -> np.float32:
     """R18 rounding of a wrapped 64-bit sum (unsigned pattern) times 2^-F to binary32."""
     return np.float32(_load().cref_fx_to_f32(total % (1 << 64), frac_bits))
+
+
+def lsq_step_grad(x: np.ndarray, s, dx: np.ndarray) -> np.float32:
+    """R19 LSQ gradient of a per-tensor step: x bf16 [T, K] (uint16), dx fp32 [T, K]."""
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    dx = np.ascontiguousarray(dx, dtype=np.float32)
+    T, K = x.shape
+    return np.float32(_load().cref_lsq_step_grad(T, K, _p(x), np.float32(s), _p(dx)))
 
 
 def num_threads() -> int:

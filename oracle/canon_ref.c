@@ -722,6 +722,11 @@ typedef struct {
   int64_t window;                        /* 0: full causal; W: query i sees keys i - W + 1 .. i */
   int qk_norm;
   int pv_int8, dq_bits;                  /* R17 P.V, R18 dQ (0: off) */
+  int int8;                              /* R19: the four projections in int8 */
+  float sx[4];                           /* R19 activation steps (qkv, o, gate_up, down) */
+  int8_t* qx[4];                         /* R19 activation codes [T][K] */
+  int8_t* qw[4];                         /* R19 weight codes [N][K] */
+  float* sw[4];                          /* R19 re-pinned weight steps [N] */
   float eps;
   float* x;      /* [T][d] input (residual) */
   uint16_t* xn;  /* [T][d] */
@@ -750,6 +755,8 @@ static void block_saved_alloc(block_saved* s, const cref_model_cfg* c, int64_t B
   s->hd = c->head_dim; s->F = c->d_ffn; s->N = (s->H + 2 * s->Hkv) * s->hd;
   s->window = window; s->qk_norm = c->qk_norm; s->eps = c->rms_eps;
   s->pv_int8 = c->pv_int8; s->dq_bits = c->dq_fixed_bits;
+  s->int8 = c->int8_linear;
+  for (int i = 0; i < 4; ++i) { s->qx[i] = NULL; s->qw[i] = NULL; s->sw[i] = NULL; s->sx[i] = 0.0f; }
   const int64_t T = s->T, d = s->d, S = s->S, F = s->F, kvw = s->Hkv * s->hd;
   s->x = (float*)xmalloc(sizeof(float) * T * d);
   s->xn = (uint16_t*)xmalloc(2 * T * d);
@@ -769,6 +776,7 @@ static void block_saved_alloc(block_saved* s, const cref_model_cfg* c, int64_t B
 }
 
 static void block_saved_free(block_saved* s) {
+  for (int i = 0; i < 4; ++i) { free(s->qx[i]); free(s->qw[i]); free(s->sw[i]); }
   free(s->x); free(s->xn); free(s->rstd1); free(s->qkv); free(s->rq); free(s->q); free(s->k); free(s->v);
   free(s->P); free(s->O); free(s->h); free(s->hn); free(s->rstd2); free(s->gu); free(s->a);
 }
@@ -812,6 +820,31 @@ static void head_in(block_saved* s, int64_t t, int64_t col0, int64_t ridx, const
   free(xn);
 }
 
+/* R19 forward of projection li (0 qkv, 1 o, 2 gate_up, 3 down): Y [T][N] = the int8 product of X (bf16
+   [T][K]) with step s->sx[li] and W (bf16 [N][K]) with its re-pinned per-row steps; the codes and steps are
+   kept for the backward. */
+static void qlin_fwd(block_saved* s, int li, int64_t T, int64_t N, int64_t K, const uint16_t* X, const uint16_t* W,
+                     float* Y) {
+  s->sw[li] = (float*)xmalloc(sizeof(float) * N);
+  s->qw[li] = (int8_t*)xmalloc((size_t)(N * K));
+  s->qx[li] = (int8_t*)xmalloc((size_t)(T * K));
+  cref_quant_scales(N, K, W, s->sw[li]);
+  cref_quantize(N, K, 1, W, s->sw[li], 1, s->qw[li]);
+  cref_quantize(T, K, 1, X, &s->sx[li], 0, s->qx[li]);
+  cref_gemm_i8(T, N, K, s->qx[li], K, s->qw[li], K, NULL, Y, N, s->sx[li], s->sw[li]);
+}
+
+/* R19 backward of projection li: G16 is the bf16 gradient of its output [T][N] (the operand the canonical
+   path would multiply), widened; dX [T][K] and dW [N][K] by R14; *dsx the LSQ gradient of the step. */
+static void qlin_bwd(const block_saved* s, int li, int64_t T, int64_t N, int64_t K, const uint16_t* G16,
+                     const uint16_t* X, float* dX, float* dW, float* dsx) {
+  float* G = (float*)xmalloc(sizeof(float) * T * N);
+  for (int64_t i = 0; i < T * N; ++i) G[i] = widen(G16[i]);
+  cref_qlinear_bwd(T, N, K, G, s->qx[li], s->sx[li], s->qw[li], s->sw[li], dX, dW);
+  free(G);
+  *dsx = cref_lsq_step_grad(T, K, X, s->sx[li], dX);
+}
+
 /* forward of one block; w = {attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down}; y = block output.
    w_qkv rows: H query heads, then Hkv key heads, then Hkv value heads (hd rows each).  Query head h reads
    key/value head h / (H / Hkv). */
@@ -821,7 +854,9 @@ static void block_fwd(block_saved* s, const float* x, const uint16_t* const* w, 
   const int64_t G = H / Hkv;
   memcpy(s->x, x, sizeof(float) * T * d);
   cref_rownorm_fwd(T, d, x, w[0], s->eps, s->xn, s->rstd1);
-  cref_gemm(0, 1, T, N, d, s->xn, d, w[1], d, s->qkv, N);
+  if (s->int8) for (int i = 0; i < 4; ++i) s->sx[i] = widen(w[6 + i][0]);
+  if (s->int8) qlin_fwd(s, 0, T, N, d, s->xn, w[1], s->qkv);
+  else cref_gemm(0, 1, T, N, d, s->xn, d, w[1], d, s->qkv, N);
   for (int64_t t = 0; t < T; ++t) {
     const int64_t b = t / S, pos = t % S;
     for (int64_t hh = 0; hh < H; ++hh) head_in(s, t, hh * hd, hh, rope_cos, rope_sin, s->q + ((b * H + hh) * S + pos) * hd);
@@ -850,16 +885,19 @@ static void block_fwd(block_saved* s, const float* x, const uint16_t* const* w, 
   free(raw);
   free(ob);
   float* attn = (float*)xmalloc(sizeof(float) * T * d);
-  cref_gemm(0, 1, T, d, d, s->O, d, w[2], d, attn, d);
+  if (s->int8) qlin_fwd(s, 1, T, d, d, s->O, w[2], attn);
+  else cref_gemm(0, 1, T, d, d, s->O, d, w[2], d, attn, d);
   for (int64_t i = 0; i < T * d; ++i) s->h[i] = cref_add(x[i], attn[i]);
   free(attn);
   cref_rownorm_fwd(T, d, s->h, w[3], s->eps, s->hn, s->rstd2);
-  cref_gemm(0, 1, T, 2 * F, d, s->hn, d, w[4], d, s->gu, 2 * F);
+  if (s->int8) qlin_fwd(s, 2, T, 2 * F, d, s->hn, w[4], s->gu);
+  else cref_gemm(0, 1, T, 2 * F, d, s->hn, d, w[4], d, s->gu, 2 * F);
   for (int64_t t = 0; t < T; ++t)
     for (int64_t j = 0; j < F; ++j)
       s->a[t * F + j] = cref_bf16(cref_mul(cref_silu(s->gu[t * 2 * F + j]), s->gu[t * 2 * F + F + j]));
   float* ffn = (float*)xmalloc(sizeof(float) * T * d);
-  cref_gemm(0, 1, T, d, F, s->a, F, w[5], F, ffn, d);
+  if (s->int8) qlin_fwd(s, 3, T, d, F, s->a, w[5], ffn);
+  else cref_gemm(0, 1, T, d, F, s->a, F, w[5], F, ffn, d);
   for (int64_t i = 0; i < T * d; ++i) y[i] = cref_add(s->h[i], ffn[i]);
   free(ffn);
 }
@@ -897,9 +935,13 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
   const int64_t G = H / Hkv, W = s->window;
   /* MLP */
   uint16_t* dyb = to_bf16(dy, T * d);
-  cref_gemm(1, 0, d, F, T, dyb, d, s->a, F, dw[5], F);            /* dW_down = dy^T a */
   float* da = (float*)xmalloc(sizeof(float) * T * F);
-  cref_gemm(0, 0, T, F, d, dyb, d, w[5], F, da, F);               /* da = dy W_down */
+  if (s->int8) {
+    qlin_bwd(s, 3, T, d, F, dyb, s->a, da, dw[5], dw[9]);
+  } else {
+    cref_gemm(1, 0, d, F, T, dyb, d, s->a, F, dw[5], F);          /* dW_down = dy^T a */
+    cref_gemm(0, 0, T, F, d, dyb, d, w[5], F, da, F);             /* da = dy W_down */
+  }
   free(dyb);
   uint16_t* dgu = (uint16_t*)xmalloc(2 * T * 2 * F);
   for (int64_t t = 0; t < T; ++t) {
@@ -915,9 +957,13 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
     }
   }
   free(da);
-  cref_gemm(1, 0, 2 * F, d, T, dgu, 2 * F, s->hn, d, dw[4], d);   /* dW_gate_up = dgu^T hn */
   float* dhn = (float*)xmalloc(sizeof(float) * T * d);
-  cref_gemm(0, 0, T, d, 2 * F, dgu, 2 * F, w[4], d, dhn, d);      /* dhn = dgu W_gate_up */
+  if (s->int8) {
+    qlin_bwd(s, 2, T, 2 * F, d, dgu, s->hn, dhn, dw[4], dw[8]);
+  } else {
+    cref_gemm(1, 0, 2 * F, d, T, dgu, 2 * F, s->hn, d, dw[4], d); /* dW_gate_up = dgu^T hn */
+    cref_gemm(0, 0, T, d, 2 * F, dgu, 2 * F, w[4], d, dhn, d);    /* dhn = dgu W_gate_up */
+  }
   free(dgu);
   float* dhnorm = (float*)xmalloc(sizeof(float) * T * d);
   cref_rownorm_bwd(T, d, s->h, w[3], s->rstd2, dhn, dhnorm, dw[3]);
@@ -927,9 +973,13 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
   free(dhnorm);
   /* attention output projection */
   uint16_t* dhb = to_bf16(dh, T * d);
-  cref_gemm(1, 0, d, d, T, dhb, d, s->O, d, dw[2], d);            /* dW_o = dh^T O */
   float* dO = (float*)xmalloc(sizeof(float) * T * d);
-  cref_gemm(0, 0, T, d, d, dhb, d, w[2], d, dO, d);               /* dO = dh W_o */
+  if (s->int8) {
+    qlin_bwd(s, 1, T, d, d, dhb, s->O, dO, dw[2], dw[7]);
+  } else {
+    cref_gemm(1, 0, d, d, T, dhb, d, s->O, d, dw[2], d);          /* dW_o = dh^T O */
+    cref_gemm(0, 0, T, d, d, dhb, d, w[2], d, dO, d);             /* dO = dh W_o */
+  }
   free(dhb);
   /* attention core, per (batch, key/value head group) */
   const float c = attn_scale(hd);
@@ -983,9 +1033,13 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
     }
   }
   free(dOs); free(Qs); free(Ps); free(dSs); free(Ob); free(D); free(dP); free(gq); free(gk); free(gv); free(dO);
-  cref_gemm(1, 0, N, d, T, dqkv, N, s->xn, d, dw[1], d);          /* dW_qkv = dqkv^T xn */
   float* dxn = (float*)xmalloc(sizeof(float) * T * d);
-  cref_gemm(0, 0, T, d, N, dqkv, N, w[1], d, dxn, d);             /* dxn = dqkv W_qkv */
+  if (s->int8) {
+    qlin_bwd(s, 0, T, N, d, dqkv, s->xn, dxn, dw[1], dw[6]);
+  } else {
+    cref_gemm(1, 0, N, d, T, dqkv, N, s->xn, d, dw[1], d);        /* dW_qkv = dqkv^T xn */
+    cref_gemm(0, 0, T, d, N, dqkv, N, w[1], d, dxn, d);           /* dxn = dqkv W_qkv */
+  }
   free(dqkv);
   float* dxnorm = (float*)xmalloc(sizeof(float) * T * d);
   cref_rownorm_bwd(T, d, s->x, w[0], s->rstd1, dxn, dxnorm, dw[0]);
@@ -1005,6 +1059,7 @@ static int cfg_valid(const cref_model_cfg* c) {
   if (c->swa_window < 0 || c->swa_full_every < 0) return 0;
   if (!(c->z_loss >= 0.0f) || isinf(c->z_loss)) return 0;
   if ((c->pv_int8 != 0 && c->pv_int8 != 1) || c->dq_fixed_bits < 0 || c->dq_fixed_bits > 62) return 0;
+  if (c->int8_linear != 0 && c->int8_linear != 1) return 0;
   return 1;
 }
 
@@ -1032,11 +1087,14 @@ int cref_block_fwd_bwd(const cref_model_cfg* cfg, int32_t batch, const float* x,
 /* Full step: forward + backward per microbatch, Algorithm 1, AdamW          */
 /* ======================================================================== */
 
-static int64_t n_tensors_of(const cref_model_cfg* c) { return 3 + 6 * (int64_t)c->n_layers + (c->embed_norm ? 1 : 0); }
+static int64_t per_layer(const cref_model_cfg* c) { return c->int8_linear ? 10 : 6; } /* tensors per layer */
+static int64_t n_tensors_of(const cref_model_cfg* c) {
+  return 3 + per_layer(c) * (int64_t)c->n_layers + (c->embed_norm ? 1 : 0);
+}
 static int64_t layer0_of(const cref_model_cfg* c) { return 1 + (c->embed_norm ? 1 : 0); } /* first layer tensor */
 
 /* tensor sizes in the declared order: embed, [embed_norm], per layer attn_norm, w_qkv, w_o, ffn_norm,
-   w_gate_up, w_down, then final_norm, head */
+   w_gate_up, w_down [, sx_qkv, sx_o, sx_gate_up, sx_down], then final_norm, head */
 static void tensor_sizes(const cref_model_cfg* c, int64_t* sz, uint8_t* decay) {
   int64_t d = c->d_model, F = c->d_ffn, V = c->vocab;
   int64_t N = (c->n_heads + 2 * kv_heads(c)) * (int64_t)c->head_dim;
@@ -1050,6 +1108,8 @@ static void tensor_sizes(const cref_model_cfg* c, int64_t* sz, uint8_t* decay) {
     sz[i] = d; decay[i++] = 0;                       /* ffn_norm */
     sz[i] = 2 * F * d; decay[i++] = 1;               /* w_gate_up */
     sz[i] = d * F; decay[i++] = 1;                   /* w_down */
+    if (c->int8_linear)
+      for (int q = 0; q < 4; ++q) { sz[i] = 1; decay[i++] = 0; } /* R19 activation steps */
   }
   sz[i] = d; decay[i++] = 0;                         /* final_norm */
   sz[i] = V * d; decay[i++] = 1;                     /* head */
@@ -1082,15 +1142,16 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
   }
   block_saved* saved = (block_saved*)xmalloc(sizeof(block_saved) * L);
   float* y = (float*)xmalloc(sizeof(float) * T * d);
+  const int64_t PL = per_layer(c);
   for (int64_t l = 0; l < L; ++l) {
-    const uint16_t* w[6];
-    for (int i = 0; i < 6; ++i) w[i] = params[l0 + 6 * l + i];
+    const uint16_t* w[10];
+    for (int i = 0; i < PL; ++i) w[i] = params[l0 + PL * l + i];
     block_saved_alloc(&saved[l], c, B, layer_window(c, l));
     block_fwd(&saved[l], x, w, rope_cos, rope_sin, y);
     float* tmp = x; x = y; y = tmp;
   }
   /* final norm, head, loss */
-  const int64_t i_fn = l0 + 6 * L, i_head = i_fn + 1;
+  const int64_t i_fn = l0 + PL * L, i_head = i_fn + 1;
   uint16_t* xf = (uint16_t*)xmalloc(2 * T * d);
   float* rstdf = (float*)xmalloc(sizeof(float) * T);
   cref_rownorm_fwd(T, d, x, params[i_fn], c->rms_eps, xf, rstdf);
@@ -1117,11 +1178,11 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
   free(rstdf);
   float* dxp = (float*)xmalloc(sizeof(float) * T * d);
   for (int64_t l = L - 1; l >= 0; --l) {
-    const uint16_t* w[6];
-    float* dw[6];
-    for (int i = 0; i < 6; ++i) {
-      w[i] = params[l0 + 6 * l + i];
-      dw[i] = grad + off[l0 + 6 * l + i];
+    const uint16_t* w[10];
+    float* dw[10];
+    for (int i = 0; i < PL; ++i) {
+      w[i] = params[l0 + PL * l + i];
+      dw[i] = grad + off[l0 + PL * l + i];
     }
     block_bwd(&saved[l], dx, w, rope_cos, rope_sin, dxp, dw);
     block_saved_free(&saved[l]);
@@ -1488,6 +1549,36 @@ int cref_attn_dq_fixed(int64_t S, int64_t hd, int64_t window, int32_t frac_bits,
     }
   }
   return 0;
+}
+
+/* ======================================================================== */
+/* R19: int8 projections inside the block, LSQ gradient of activation steps  */
+/* ======================================================================== */
+/* The paper trains the four projections of every block with int8 weights (re-pinned per-channel steps, R13)
+   and int8 activations with a learned per-tensor step (LSQ), and runs both gradient GEMMs in int8 (R14).
+   The step's gradient is LSQ's: for each element the derivative of the dequantised value s q with respect
+   to s, round(v) - v inside the integer range and the clamp bound outside it (v = x / s), times LSQ's
+   gradient scale 1/sqrt(Q_P K) for K features. */
+static float lsq_delta(float x, float s) {
+  s = daz(s);
+  if (!(s > 0.0f)) return 0.0f;
+  const float v = cref_div(x, s);
+  if (isnan(v)) return 0.0f;
+  if (v < -128.0f) return -128.0f;
+  if (v > 127.0f) return 127.0f;
+  return cref_sub((float)rint((double)v), v); /* rint: nearest integer, ties to even */
+}
+
+float cref_lsq_step_grad(int64_t T, int64_t K, const uint16_t* x, float s, const float* dx) {
+  if (T < 0 || K < 1) return 0.0f;
+  const int64_t n = T * K;
+  float* t = (float*)xmalloc(sizeof(float) * (size_t)n);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) t[i] = cref_mul(dx[i], lsq_delta(widen(x[i]), s));
+  const float sum = cref_rsum(t, n, 1, CHUNK);
+  free(t);
+  const float gamma = (float)(1.0 / sqrt(127.0 * (double)K)); /* RN32(1/sqrt(127 K)) */
+  return cref_mul(sum, gamma);
 }
 
 int cref_num_threads(void) { return omp_get_max_threads(); }

@@ -21,13 +21,16 @@ extern "C" {
    of n_heads; qk_norm, embed_norm: 0 or 1; swa_window: 0 (full causal) or the window of the windowed
    layers, which are all but every swa_full_every-th and the last; z_loss: weight, 0 for none.
    pv_int8: 0 or 1, the attention forward's P.V by R17; dq_fixed_bits: 0 (dQ by R2) or F in [1, 62], the
-   attention backward's dQ by R18 with F fractional bits. */
+   attention backward's dQ by R18 with F fractional bits.  int8_linear: 0 or 1, the four projections of every
+   block in int8 (R19); each layer then has four more tensors after w_down, the bf16 activation steps
+   sx_qkv, sx_o, sx_gate_up, sx_down (one element each, no weight decay). */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
   float rms_eps;
   int32_t n_kv_heads, qk_norm, embed_norm, swa_window, swa_full_every;
   float z_loss;
   int32_t pv_int8, dq_fixed_bits;
+  int32_t int8_linear;
 } cref_model_cfg;
 
 typedef struct {
@@ -171,6 +174,13 @@ int cref_attn_dq_fixed(int64_t S, int64_t hd, int64_t window, int32_t frac_bits,
 /* fx of one product, and the conversion of a wrapped sum back to fp32 (exported for the pins) */
 uint64_t cref_fx_product(uint16_t a, uint16_t b, int32_t frac_bits);
 float cref_fx_to_f32(uint64_t sum, int32_t frac_bits);
+
+/* ---- R19 LSQ gradient of a per-tensor activation step ----
+   x: bf16 [T][K] (the quantised activation), s: its step, dx: fp32 [T][K] (the gradient of the dequantised
+   activation).  delta = 0 if s is not > 0 (after the input flush) or x/s is NaN; else with v = RN(x/s):
+   -128 if v < -128, 127 if v > 127, RN(rne(v) - v) otherwise.  Returns RN(R1 over the flat index of
+   RN(dx * delta) * RN32(1/sqrt(127 K))). */
+float cref_lsq_step_grad(int64_t T, int64_t K, const uint16_t* x, float s, const float* dx);
 
 int cref_num_threads(void);
 

@@ -125,10 +125,17 @@ def adamw_constants(lr=3e-4, beta1=0.9, beta2=0.95, eps=1e-8, wd=0.1, t=1):
     return tuple(float(np.float32(v)) for v in vals)
 
 
-def model_param_shapes(n_layers, d_model, d_ffn, vocab, kv_dim=None, embed_norm=False):
-    """Parameter tensors in the declared order, with (name, shape, init std, weight-decay flag).
+# Initial activation steps of the int8 projections: 2 E|x| / sqrt(127) for unit-RMS normalised inputs
+# (E|x| = sqrt(2/pi)) and for the smaller attention and SwiGLU outputs (E|x| about 0.3).
+ACT_STEPS = {"sx_qkv": 0.1416, "sx_o": 0.0532, "sx_gate_up": 0.1416, "sx_down": 0.0532}
+
+
+def model_param_shapes(n_layers, d_model, d_ffn, vocab, kv_dim=None, embed_norm=False, int8_linear=False):
+    """Parameter tensors in the declared order, with (name, shape, init, weight-decay flag); init is the
+    normal's std, None for a norm gain (1.0), or ("step", value) for an activation step.
     kv_dim: width of the key (and of the value) projection, n_kv_heads * head_dim (default d_model);
-    embed_norm: a gain tensor after the embedding."""
+    embed_norm: a gain tensor after the embedding; int8_linear: four activation steps per layer after
+    w_down (sx_qkv, sx_o, sx_gate_up, sx_down)."""
     kv = d_model if kv_dim is None else kv_dim
     out = [("embed", (vocab, d_model), 0.02, 0)]
     if embed_norm:
@@ -137,20 +144,35 @@ def model_param_shapes(n_layers, d_model, d_ffn, vocab, kv_dim=None, embed_norm=
         out += [(f"l{l}.attn_norm", (d_model,), None, 0), (f"l{l}.w_qkv", (d_model + 2 * kv, d_model), 0.02, 1),
                 (f"l{l}.w_o", (d_model, d_model), 0.02, 1), (f"l{l}.ffn_norm", (d_model,), None, 0),
                 (f"l{l}.w_gate_up", (2 * d_ffn, d_model), 0.02, 1), (f"l{l}.w_down", (d_model, d_ffn), 0.02, 1)]
+        if int8_linear:
+            out += [(f"l{l}.{k}", (1,), ("step", v), 0) for k, v in ACT_STEPS.items()]
     out += [("final_norm", (d_model,), None, 0), ("head", (vocab, d_model), 0.02, 1)]
     return out
 
 
-def model_params(n_layers, d_model, d_ffn, vocab, seed=0, std=0.02, out=None, kv_dim=None, embed_norm=False):
-    """bf16 parameters: N(0, std) for matrices, 1.0 for norm gains.  ``out`` may hold preallocated
-    uint16 buffers (e.g. pinned host tensors) to fill instead of new numpy arrays."""
+def bf16_pattern(value: float) -> int:
+    """bf16 bit pattern of a float (round to nearest even)."""
+    u = int(np.array([value], np.float32).view(np.uint32)[0])
+    return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) & 0xFFFF
+
+
+def model_params(n_layers, d_model, d_ffn, vocab, seed=0, std=0.02, out=None, kv_dim=None, embed_norm=False,
+                 int8_linear=False):
+    """bf16 parameters: N(0, std) for matrices, 1.0 for norm gains, the ACT_STEPS values for activation
+    steps.  ``out`` may hold preallocated uint16 buffers (e.g. pinned host tensors) to fill instead of new
+    numpy arrays."""
     res = []
     base = {"embed": TENSOR_IDS["embed"], "head": TENSOR_IDS["head"], "final_norm": TENSOR_IDS["final_norm"],
             "embed_norm": TENSOR_IDS["embed_norm"]}
     for idx, (name, shape, s, _) in enumerate(model_param_shapes(n_layers, d_model, d_ffn, vocab, kv_dim,
-                                                                 embed_norm)):
+                                                                 embed_norm, int8_linear)):
         buf = None if out is None else out[idx]
-        if s is None:
+        if isinstance(s, tuple):
+            pat = bf16_pattern(s[1])
+            arr = np.full(shape, pat, dtype=np.uint16) if buf is None else buf
+            if buf is not None:
+                np.asarray(arr).fill(pat) if isinstance(arr, np.ndarray) else arr.fill_(pat)
+        elif s is None:
             arr = np.full(shape, 0x3F80, dtype=np.uint16) if buf is None else buf
             if buf is not None:
                 np.asarray(arr).fill(0x3F80) if isinstance(arr, np.ndarray) else arr.fill_(0x3F80)

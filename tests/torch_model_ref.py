@@ -51,6 +51,26 @@ def linear(x, w):
     return rb(rf(x) @ w.T)
 
 
+def qlinear(x, w, s):
+    """int8 projection: y = X^ W^^T with X^ = s clamp(rne(bf16(x) / s), -128, 127) and W^ the same with the
+    per-row step 2 mean|w| / sqrt(127) (not trained).  Straight-through for x and w (no clipping mask); the
+    step s gets LSQ's gradient: round(v) - v inside the range, the bound outside (v = x / s), times
+    1/sqrt(127 K).  The gradient of y is rounded to bf16, the operand of the int8 backward."""
+    xb = rf(x)
+    K = w.shape[1]
+    sw = 2.0 * w.detach().abs().mean(dim=1, keepdim=True) / np.sqrt(127.0)
+    qw = torch.clamp(torch.round(w.detach() / sw), -128, 127)
+    w_hat = w + (qw * sw - w).detach()
+    g = 1.0 / np.sqrt(127.0 * K)
+    s_eff = s * g + (s - s * g).detach()
+    v = xb.detach() / s.detach()
+    q = torch.clamp(torch.round(v), -128, 127)
+    delta = torch.where(v < -128, torch.full_like(v, -128.0),
+                        torch.where(v > 127, torch.full_like(v, 127.0), torch.round(v) - v))
+    x_hat = xb + (q * s.detach() - xb).detach() + (s_eff - s_eff.detach()) * delta
+    return rb(x_hat @ w_hat.T)
+
+
 def rmsnorm(x, g, eps):
     return x * torch.rsqrt((x * x).mean(dim=-1, keepdim=True) + eps) * g
 
@@ -67,14 +87,21 @@ def headnorm(x, eps):
     return x * torch.rsqrt((x * x).mean(dim=-1, keepdim=True) + eps)
 
 
-def block(x, w, B, S, H, hd, F, eps, cos, sin, scale, Hkv=None, qk_norm=False, window=0):
-    """w: dict of float64 tensors attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down.  Hkv: key/value heads
-    (query head h reads head h // (H // Hkv)); qk_norm: gain-free per-head RMSNorm of q and k before the
-    rotation; window: query i sees keys i - window < j <= i (0: all j <= i)."""
+def block(x, w, B, S, H, hd, F, eps, cos, sin, scale, Hkv=None, qk_norm=False, window=0, int8=False):
+    """w: dict of float64 tensors attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down (and with int8 the
+    activation steps sx_qkv, sx_o, sx_gate_up, sx_down).  Hkv: key/value heads (query head h reads head
+    h // (H // Hkv)); qk_norm: gain-free per-head RMSNorm of q and k before the rotation; window: query i
+    sees keys i - window < j <= i (0: all j <= i); int8: the four projections by qlinear."""
     Hkv = H if Hkv is None else Hkv
+    if int8:
+        def proj(t, name):
+            return qlinear(t, w[name], w["sx" + name[1:]])
+    else:
+        def proj(t, name):
+            return linear(t, w[name])
     d, kvw = H * hd, Hkv * hd
     xn = rmsnorm(x, w["attn_norm"], eps)
-    qkv = linear(xn, w["w_qkv"])                                     # [T, d + 2 kvw]
+    qkv = proj(xn, "w_qkv")                                          # [T, d + 2 kvw]
     q, k, v = qkv[:, :d], qkv[:, d:d + kvw], qkv[:, d + kvw:]
 
     def heads(t, n):
@@ -100,12 +127,12 @@ def block(x, w, B, S, H, hd, F, eps, cos, sin, scale, Hkv=None, qk_norm=False, w
     p = rf(torch.softmax(sc, dim=-1))
     o = rb(p @ vh)                                                   # [B, H, S, hd]
     o = o.permute(0, 2, 1, 3).reshape(B * S, d)
-    h = x + linear(o, w["w_o"])
+    h = x + proj(o, "w_o")
     hn = rmsnorm(h, w["ffn_norm"], eps)
-    gu = linear(hn, w["w_gate_up"])
+    gu = proj(hn, "w_gate_up")
     g, u = gu[:, :F], gu[:, F:]
     a = g * torch.sigmoid(g) * u
-    return h + linear(a, w["w_down"])
+    return h + proj(a, "w_down")
 
 
 def layer_window(cfg, l):
@@ -128,12 +155,16 @@ def model_loss(params, tok, cfg, cos, sin, scale):
     if en:
         x = rmsnorm(x, params[1], cfg["eps"])
     names = ["attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down"]
+    q8 = bool(cfg.get("int8_linear"))
+    if q8:
+        names += ["sx_qkv", "sx_o", "sx_gate_up", "sx_down"]
+    PL = len(names)
     for l in range(L):
-        w = {n: params[1 + en + 6 * l + i] for i, n in enumerate(names)}
+        w = {n: params[1 + en + PL * l + i] for i, n in enumerate(names)}
         x = block(x, w, B, S, H, hd, F, cfg["eps"], cos, sin, scale, cfg.get("Hkv"), cfg.get("qk_norm", False),
-                  layer_window(cfg, l))
-    xf = rmsnorm(x, params[1 + en + 6 * L], cfg["eps"])
-    logits = rf(linear(xf, params[2 + en + 6 * L]))
+                  layer_window(cfg, l), int8=q8)
+    xf = rmsnorm(x, params[1 + en + PL * L], cfg["eps"])
+    logits = rf(linear(xf, params[2 + en + PL * L]))
     loss = torch.nn.functional.cross_entropy(logits, lab, reduction="mean")
     zw = cfg.get("z_loss", 0.0)
     if zw:
