@@ -78,13 +78,25 @@ typedef struct {
                      32 up to 256 and seq <= 8192, else CANON_EUNSUPPORTED.  The backward stays the bf16 one
                      (straight-through).
      dq_fixed_bits:  0: dQ by the canonical GEMM; F in [1, 62]: dQ accumulated in 64-bit fixed point with F
-                     fractional bits (R18, canon_attn_dq_fixed below); head_dim in {16, 32, 64, 128}. */
+                     fractional bits (R18, canon_attn_dq_fixed below); head_dim in {16, 32, 64, 128}.
+     int8_linear:    1: the four projections of every block (q/k/v, output, gate/up, down) in int8 (R19, the
+                     paper's W8A8 quantisation-aware training): weights quantised with their per-row steps
+                     re-pinned from the weights (canon_quant_scales), the bf16 input with a learned
+                     per-tensor activation step, the exact int8 product dequantised (canon_gemm_i8); the
+                     backward is canon_qlinear_bwd on the widened bf16 upstream gradient, and each activation
+                     step s gets LSQ's gradient RN(R1_{t,k} RN(dx * delta) * RN32(1/sqrt(127 K))) with
+                     delta = -128 / 127 outside the integer range and RN(rne(v) - v) inside (v = RN(x / s);
+                     0 for a step that is not > 0).  Each layer then has four more tensors after w_down, the
+                     bf16 activation steps sx_qkv, sx_o, sx_gate_up, sx_down (one element each, no weight
+                     decay).  Needs the tokens per call, d_model, 2 d_ffn and the q/k/v width to be multiples
+                     of 256 (whole rotation blocks), else CANON_EUNSUPPORTED. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, head_dim, d_ffn, vocab, seq, micro_seqs;
   float rms_eps; /* fp32 value, e.g. RN32(1e-5) */
   int32_t n_kv_heads, qk_norm, embed_norm, swa_window, swa_full_every;
   float z_loss;
   int32_t pv_int8, dq_fixed_bits;
+  int32_t int8_linear;
 } canon_model_cfg;
 
 /* AdamW constants, each evaluated in double and rounded once to fp32 by the caller (R9). */
@@ -199,7 +211,8 @@ size_t canon_clip_grad_norm_workspace_bytes(int64_t n_tensors, const int64_t* si
 /* One decoder block, forward then backward, for `batch` sequences of cfg->seq tokens (T = batch*seq).
    x, dy: fp32 [T, d_model] (block input, gradient of the block output).  w: HOST array of the six bf16
    block tensors in the order attn_norm [d], w_qkv [(n_heads + 2 n_kv_heads) head_dim, d], w_o [d, d],
-   ffn_norm [d], w_gate_up [2F, d] (gate rows first), w_down [d, F].  The block's attention window is
+   ffn_norm [d], w_gate_up [2F, d] (gate rows first), w_down [d, F], then with int8_linear the four bf16
+   activation steps [1] (ten tensors; dw likewise).  The block's attention window is
    cfg->swa_window (the step applies the per-layer rule); embed_norm and z_loss do not apply to a block.  rope_cos/rope_sin: fp32 [seq, head_dim/2].  Outputs: y (block
    output), dx (input gradient), dw: HOST array of six fp32 gradient buffers shaped like w. */
 canon_status canon_block_fwd_bwd(const canon_order* order, const canon_model_cfg* cfg, int32_t batch,
@@ -213,9 +226,9 @@ size_t canon_block_workspace_bytes(const canon_model_cfg* cfg, int32_t batch);
    `accum` microbatches (R12: rank r owns windows m with m mod N == r, micro_seqs consecutive ones per
    microbatch), run forward and backward of the whole model, then reduce the gradients and the
    microbatch losses through the plan and apply AdamW (R9).
-   params, m, v: HOST arrays of n = 3 + 6*n_layers (+1 with embed_norm) device pointers in the declared
-   order: embed [V, d]; [embed_norm [d]]; per layer attn_norm, w_qkv, w_o, ffn_norm, w_gate_up, w_down;
-   final_norm [d]; head [V, d].  params
+   params, m, v: HOST arrays of n = 3 + 6*n_layers (10*n_layers with int8_linear; +1 with embed_norm) device
+   pointers in the declared order: embed [V, d]; [embed_norm [d]]; per layer attn_norm, w_qkv, w_o,
+   ffn_norm, w_gate_up, w_down [, sx_qkv, sx_o, sx_gate_up, sx_down]; final_norm [d]; head [V, d].  params
    (bf16), m and v (fp32) are updated in place.  windows: device int32 [M, seq+1], M = N*accum*
    micro_seqs, each token in [0, vocab) (checked on the device: an out-of-range token makes the loss
    NaN and leaves the parameters unchanged).  loss_out: device fp32 scalar.  grads_out: NULL, or a HOST
@@ -318,6 +331,16 @@ canon_status canon_attn_pv_i8(int64_t batch, int64_t n_heads, int64_t n_kv_heads
 canon_status canon_attn_dq_fixed(int64_t batch, int64_t n_heads, int64_t n_kv_heads, int64_t seq, int64_t head_dim,
                                  int64_t window, int32_t frac_bits, const uint16_t* dS, const uint16_t* K, float* dQ,
                                  void* stream);
+
+/* LSQ gradient of a learned per-tensor activation step (R19; the int8 projections of canon_step with
+   int8_linear): x bf16 [T, K] (the quantised activation), s: device fp32 scalar (the step), dx fp32 [T, K]
+   (the gradient of the dequantised activation).  grad (device fp32 scalar) = RN(R1 over the flat index of
+   RN(dx * delta) * RN32(1/sqrt(127 K))), delta = 0 if s is not > 0 once flushed or x/s is NaN, else with
+   v = RN(x / s): -128 if v < -128, 127 if v > 127, RN(rne(v) - v) otherwise.  workspace: device memory of
+   canon_lsq_step_grad_workspace_bytes(T, K) bytes (block sums). */
+size_t canon_lsq_step_grad_workspace_bytes(int64_t T, int64_t K);
+canon_status canon_lsq_step_grad(const canon_order* order, int64_t T, int64_t K, const uint16_t* x, const float* s,
+                                 const float* dx, float* grad, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
    the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,

@@ -40,7 +40,7 @@ class ModelCfg(ctypes.Structure):
                 ("seq", ctypes.c_int32), ("micro_seqs", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("n_kv_heads", ctypes.c_int32), ("qk_norm", ctypes.c_int32), ("embed_norm", ctypes.c_int32),
                 ("swa_window", ctypes.c_int32), ("swa_full_every", ctypes.c_int32), ("z_loss", ctypes.c_float),
-                ("pv_int8", ctypes.c_int32), ("dq_fixed_bits", ctypes.c_int32)]
+                ("pv_int8", ctypes.c_int32), ("dq_fixed_bits", ctypes.c_int32), ("int8_linear", ctypes.c_int32)]
 
 
 class AdamWConsts(ctypes.Structure):
@@ -94,6 +94,8 @@ def _lib():
             "canon_attn_pv_i8": (i32, [i64, i64, i64, i64, i64, i64, vp, vp, vp, vp, vp, sz, vp]),
             "canon_attn_pv_i8_workspace_bytes": (sz, [i64, i64, i64, i64]),
             "canon_attn_dq_fixed": (i32, [i64, i64, i64, i64, i64, i64, i32, vp, vp, vp, vp]),
+            "canon_lsq_step_grad": (i32, [vp, i64, i64, vp, vp, vp, vp, vp, sz, vp]),
+            "canon_lsq_step_grad_workspace_bytes": (sz, [i64, i64]),
             "canon_status_str": (ctypes.c_char_p, [i32]),
             "canon_version": (i32, []),
         }
@@ -185,6 +187,16 @@ def attn_pv_i8(batch, n_heads, n_kv_heads, seq, head_dim, window, P, V, workspac
 def attn_dq_fixed(batch, n_heads, n_kv_heads, seq, head_dim, window, frac_bits, dS, K, dQ, stream=None):
     _check(_lib().canon_attn_dq_fixed(batch, n_heads, n_kv_heads, seq, head_dim, window, frac_bits, _ptr(dS), _ptr(K),
                                       _ptr(dQ), _stream(stream)), "canon_attn_dq_fixed")
+
+
+def lsq_step_grad_workspace_bytes(T, K) -> int:
+    return int(_lib().canon_lsq_step_grad_workspace_bytes(T, K))
+
+
+def lsq_step_grad(T, K, x, s, dx, grad, workspace, order=ORDER_V1, stream=None):
+    _check(_lib().canon_lsq_step_grad(ctypes.byref(order), T, K, _ptr(x), _ptr(s), _ptr(dx), _ptr(grad),
+                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _stream(stream)), "canon_lsq_step_grad")
 
 
 def block_workspace_bytes(cfg: ModelCfg, batch: int) -> int:

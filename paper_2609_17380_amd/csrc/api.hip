@@ -65,6 +65,7 @@ struct Dims {
   int64_t window;          // this block's attention window (0: full causal)
   int qk_norm;
   int pv_int8, dq_bits;    // R17 int8 P.V; R18 fixed-point dQ with dq_bits fractional bits (0: off)
+  int int8;                // R19: the four projections in int8
   float eps, scale, z_loss;
 };
 
@@ -94,6 +95,7 @@ Dims dims_of(const canon_model_cfg* c, int64_t B) {
   D.Hkv = kv_heads(c); D.G = D.H / D.Hkv; D.kvw = D.Hkv * D.hd; D.N = D.d + 2 * D.kvw;
   D.window = c->swa_window; D.qk_norm = c->qk_norm; D.z_loss = c->z_loss;
   D.pv_int8 = c->pv_int8; D.dq_bits = c->dq_fixed_bits;
+  D.int8 = c->int8_linear;
   return D;
 }
 
@@ -106,25 +108,52 @@ bool cfg_ok(const canon_model_cfg* c) {
   if ((c->qk_norm != 0 && c->qk_norm != 1) || (c->embed_norm != 0 && c->embed_norm != 1)) return false;
   if (c->swa_window < 0 || c->swa_full_every < 0 || !(c->z_loss >= 0.0f) || isinf(c->z_loss)) return false;
   if ((c->pv_int8 != 0 && c->pv_int8 != 1) || c->dq_fixed_bits < 0 || c->dq_fixed_bits > 62) return false;
+  if (c->int8_linear != 0 && c->int8_linear != 1) return false;
   const int64_t G = c->n_heads / kv_heads(c);
   return gemm_k_supported(c->vocab) && gemm_k_supported((int64_t)c->seq * c->micro_seqs) &&
          gemm_k_supported(2 * (int64_t)c->d_ffn) && gemm_k_supported(c->d_model + 2 * kv_heads(c) * c->head_dim) &&
          gemm_k_supported(G * (int64_t)c->seq);
 }
 
-// shapes the R17 and R18 kernels are built for
-bool attn_variants_supported(const canon_model_cfg* c) {
+// shapes the R17, R18 and R19 kernels are built for (T tokens per block call)
+bool variants_supported(const canon_model_cfg* c, int64_t T) {
   if (c->pv_int8 && (c->head_dim % 32 != 0 || c->head_dim > 256 || c->seq > 8192)) return false;
   if (c->dq_fixed_bits && c->head_dim != 16 && c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
     return false;
+  if (c->int8_linear) {  // whole rotation blocks along every contraction of the int8 backward; the GEMM's k bound
+    const int64_t d = c->d_model, F = c->d_ffn, N = d + 2 * kv_heads(c) * (int64_t)c->head_dim;
+    if (T % 256 || d % 256 || (2 * F) % 256 || N % 256) return false;
+    if (T > 65536 || N > 65536 || 2 * F > 65536 || F > 32768 || d > 32768) return false;
+  }
   return true;
 }
+
+// R19: the four projections of a block, (N, K) and the tensor index of the weight within the layer
+struct Proj {
+  int64_t N, K;
+};
+void projections(const Dims& D, Proj (&p)[4]) {
+  p[0] = {D.N, D.d};      // w_qkv
+  p[1] = {D.d, D.d};      // w_o
+  p[2] = {2 * D.F, D.d};  // w_gate_up
+  p[3] = {D.d, D.F};      // w_down
+}
+const int kProjWeight[4] = {1, 2, 4, 5};  // index of each projection's weight among the layer's tensors
+
+// LSQ's gradient scale RN32(1/sqrt(127 K)), evaluated in double and rounded once
+float lsq_gamma(int64_t K) { return (float)(1.0 / sqrt(127.0 * (double)K)); }
 
 // activations a block saves for its backward pass
 struct LayerSave {
   uint16_t *xn, *q, *k, *v, *P, *O, *hn, *a;
   float *rstd1, *h, *rstd2, *gu;
   float *qkv, *rq;  // QK-norm only: the projection output and the r of each q and k head row
+  // R19: activation codes of the four projections, their steps widened to fp32, and the weights' codes
+  // and re-pinned steps (computed once per call from the layer's weights)
+  int8_t* qx[4];
+  float* sxf;
+  int8_t* qw[4];
+  float* sw[4];
 };
 
 void carve_save(Carver& cv, const Dims& D, LayerSave& s) {
@@ -143,6 +172,14 @@ void carve_save(Carver& cv, const Dims& D, LayerSave& s) {
   s.rstd2 = cv.take<float>(T);
   s.gu = cv.take<float>(T * 2 * D.F);
   s.a = cv.take<uint16_t>(T * D.F);
+  Proj pj[4];
+  projections(D, pj);
+  for (int i = 0; i < 4; ++i) {
+    s.qx[i] = D.int8 ? cv.take<int8_t>(T * pj[i].K) : nullptr;
+    s.qw[i] = D.int8 ? cv.take<int8_t>(pj[i].N * pj[i].K) : nullptr;
+    s.sw[i] = D.int8 ? cv.take<float>(pj[i].N) : nullptr;
+  }
+  s.sxf = D.int8 ? cv.take<float>(4) : nullptr;
 }
 
 // transient buffers shared by all layers
@@ -151,6 +188,10 @@ struct Scratch {
   uint16_t *dy_b, *dgu, *dO, *dS, *dqkv, *dOh;
   int8_t* qvt;  // R17: V codes, transposed per key block
   float* sv;    // R17: V block steps
+  float* gq;    // R19: the widened upstream gradient of a projection [T][N]
+  void* qws;    // R19: workspace of the rotated int8 backward
+  float* lsq_part;  // R19: block sums of the activation-step gradients
+  float* dOf;   // R19: fp32 gradient of the attention output before its bf16 rounding
 };
 
 void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
@@ -174,6 +215,64 @@ void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
   const int64_t nb = attn_pv_blocks(D.S);
   s.qvt = D.pv_int8 ? cv.take<int8_t>(D.B * D.Hkv * D.hd * nb * 64) : nullptr;
   s.sv = D.pv_int8 ? cv.take<float>(D.B * D.Hkv * nb) : nullptr;
+  s.gq = nullptr; s.qws = nullptr; s.lsq_part = nullptr; s.dOf = nullptr;
+  if (D.int8) {
+    Proj pj[4];
+    projections(D, pj);
+    int64_t nmax = 0, parts = 1;
+    size_t wsb = 0;
+    for (int i = 0; i < 4; ++i) {
+      nmax = pj[i].N > nmax ? pj[i].N : nmax;
+      const size_t b = qlinear_bwd_workspace_bytes(T, pj[i].N, pj[i].K);
+      wsb = b > wsb ? b : wsb;
+      const int64_t np = lsq_grad_parts(T * pj[i].K);
+      parts = np > parts ? np : parts;
+    }
+    s.gq = cv.take<float>(T * nmax);
+    s.qws = cv.take<char>((int64_t)wsb);
+    s.lsq_part = cv.take<float>(parts);
+    s.dOf = cv.take<float>(T * d);
+  }
+}
+
+// R19: codes and re-pinned steps of the layer's four projection weights, and its activation steps in fp32
+// (w[6 + i]: the bf16 activation step of projection i)
+canon_status prep_int8_layer(const Dims& D, const uint16_t* const* w, LayerSave& sv, hipStream_t s) {
+  Proj pj[4];
+  projections(D, pj);
+  for (int i = 0; i < 4; ++i) {
+    const uint16_t* W = w[kProjWeight[i]];
+    TRY(quant_scales_launch(pj[i].N, pj[i].K, W, sv.sw[i], s));
+    TRY(quantize_launch(pj[i].N, pj[i].K, CANON_BF16, W, sv.sw[i], 1, sv.qw[i], s));
+    TRY(widen_bf16_launch(1, w[6 + i], sv.sxf + i, s));
+  }
+  return CANON_OK;
+}
+
+// R19 forward of projection i: Y [T][N] from the bf16 input X [T][K]
+canon_status qproj_fwd(const Dims& D, int i, const uint16_t* X, float* Y, LayerSave& sv, hipStream_t s) {
+  Proj pj[4];
+  projections(D, pj);
+  const int64_t N = pj[i].N, K = pj[i].K;
+  TRY(quantize_launch(D.T, K, CANON_BF16, X, sv.sxf + i, 0, sv.qx[i], s));
+  GemmI8Args g{};
+  g.a = sv.qx[i]; g.b = sv.qw[i]; g.y = Y; g.sa = sv.sxf + i; g.sb = sv.sw[i];
+  g.m = D.T; g.n = N; g.k = K; g.lda = K; g.ldb = K; g.ldc = N;
+  TRY(gemm_i8_launch(g, s));
+  return CANON_OK;
+}
+
+// R19 backward of projection i: G16 the bf16 gradient of its output [T][N]; dX [T][K], dW [N][K] by the rotated
+// int8 backward; dsx the activation step's gradient (X the bf16 input of the forward)
+canon_status qproj_bwd(const Dims& D, int i, const uint16_t* G16, const uint16_t* X, float* dX, float* dW, float* dsx,
+                       const LayerSave& sv, Scratch& sc, hipStream_t s) {
+  Proj pj[4];
+  projections(D, pj);
+  const int64_t N = pj[i].N, K = pj[i].K;
+  TRY(widen_bf16_launch(D.T * N, G16, sc.gq, s));
+  TRY(qlinear_bwd_launch(D.T, N, K, sc.gq, sv.qx[i], sv.sxf + i, sv.qw[i], sv.sw[i], dX, dW, sc.qws, s));
+  TRY(lsq_grad_launch(D.T * K, X, sv.sxf + i, dX, lsq_gamma(K), sc.lsq_part, dsx, s));
+  return CANON_OK;
 }
 
 hipError_t gemm(const GemmArgs& g, hipStream_t s) { return gemm_launch(g, s); }
@@ -193,7 +292,12 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
   const int64_t T = D.T, d = D.d, S = D.S, H = D.H, Hkv = D.Hkv, hd = D.hd, F = D.F, N = D.N;
   float* qkv = D.qk_norm ? sv.qkv : sc.qkv;
   TRY(rownorm_fwd_launch(T, d, x, w[0], D.eps, sv.xn, sv.rstd1, s));
-  TRY(gemm(mk(0, 1, T, N, d, sv.xn, d, w[1], d, qkv, N), s));
+  if (D.int8) {
+    canon_status st = qproj_fwd(D, 0, sv.xn, qkv, sv, s);
+    if (st != CANON_OK) return st;
+  } else {
+    TRY(gemm(mk(0, 1, T, N, d, sv.xn, d, w[1], d, qkv, N), s));
+  }
   TRY(rope_qkv_launch(D.B, S, H, Hkv, hd, qkv, cosT, sinT, D.qk_norm, D.eps, sv.q, sv.k, sv.v, sv.rq, s));
   {  // raw scores Q K^T, lower-triangle tiles only
     GemmArgs g = batched(mk(0, 1, S, S, hd, sv.q, hd, sv.k, hd, sc.scores, S), D, H * S * hd, S * hd,
@@ -214,12 +318,27 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
     g.b_group = (int32_t)D.G;
     TRY(gemm(g, s));
   }
-  TRY(gemm(mk(0, 1, T, d, d, sv.O, d, w[2], d, sc.tmp_d, d), s));
+  if (D.int8) {
+    canon_status st = qproj_fwd(D, 1, sv.O, sc.tmp_d, sv, s);
+    if (st != CANON_OK) return st;
+  } else {
+    TRY(gemm(mk(0, 1, T, d, d, sv.O, d, w[2], d, sc.tmp_d, d), s));
+  }
   TRY(add_f32_launch(T * d, x, sc.tmp_d, sv.h, s));
   TRY(rownorm_fwd_launch(T, d, sv.h, w[3], D.eps, sv.hn, sv.rstd2, s));
-  TRY(gemm(mk(0, 1, T, 2 * F, d, sv.hn, d, w[4], d, sv.gu, 2 * F), s));
+  if (D.int8) {
+    canon_status st = qproj_fwd(D, 2, sv.hn, sv.gu, sv, s);
+    if (st != CANON_OK) return st;
+  } else {
+    TRY(gemm(mk(0, 1, T, 2 * F, d, sv.hn, d, w[4], d, sv.gu, 2 * F), s));
+  }
   TRY(swiglu_fwd_launch(T, F, sv.gu, sv.a, s));
-  TRY(gemm(mk(0, 1, T, d, F, sv.a, F, w[5], F, sc.tmp_d, d), s));
+  if (D.int8) {
+    canon_status st = qproj_fwd(D, 3, sv.a, sc.tmp_d, sv, s);
+    if (st != CANON_OK) return st;
+  } else {
+    TRY(gemm(mk(0, 1, T, d, F, sv.a, F, w[5], F, sc.tmp_d, d), s));
+  }
   TRY(add_f32_launch(T * d, sv.h, sc.tmp_d, y, s));
   return CANON_OK;
 }
@@ -232,17 +351,31 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
                             float* const* dw, hipStream_t s) {
   const int64_t T = D.T, d = D.d, S = D.S, H = D.H, Hkv = D.Hkv, G = D.G, hd = D.hd, F = D.F, N = D.N;
   const int64_t kvw = D.kvw;
+  canon_status qst = CANON_OK;
   TRY(cast_bf16_launch(T * d, dy, sc.dy_b, s));
-  TRY(gemm(mk(1, 0, d, F, T, sc.dy_b, d, sv.a, F, dw[5], F), s));        // dW_down = dy^T a
-  TRY(gemm(mk(0, 0, T, F, d, sc.dy_b, d, w[5], F, sc.da, F), s));        // da = dy W_down
+  if (D.int8) {
+    if ((qst = qproj_bwd(D, 3, sc.dy_b, sv.a, sc.da, dw[5], dw[9], sv, sc, s)) != CANON_OK) return qst;
+  } else {
+    TRY(gemm(mk(1, 0, d, F, T, sc.dy_b, d, sv.a, F, dw[5], F), s));        // dW_down = dy^T a
+    TRY(gemm(mk(0, 0, T, F, d, sc.dy_b, d, w[5], F, sc.da, F), s));        // da = dy W_down
+  }
   TRY(swiglu_bwd_launch(T, F, sv.gu, sc.da, sc.dgu, s));
-  TRY(gemm(mk(1, 0, 2 * F, d, T, sc.dgu, 2 * F, sv.hn, d, dw[4], d), s)); // dW_gate_up = dgu^T hn
-  TRY(gemm(mk(0, 0, T, d, 2 * F, sc.dgu, 2 * F, w[4], d, sc.dtmp, d), s)); // dhn = dgu W_gate_up
+  if (D.int8) {
+    if ((qst = qproj_bwd(D, 2, sc.dgu, sv.hn, sc.dtmp, dw[4], dw[8], sv, sc, s)) != CANON_OK) return qst;
+  } else {
+    TRY(gemm(mk(1, 0, 2 * F, d, T, sc.dgu, 2 * F, sv.hn, d, dw[4], d), s)); // dW_gate_up = dgu^T hn
+    TRY(gemm(mk(0, 0, T, d, 2 * F, sc.dgu, 2 * F, w[4], d, sc.dtmp, d), s)); // dhn = dgu W_gate_up
+  }
   TRY(rownorm_bwd_launch(T, d, sv.h, w[3], sv.rstd2, sc.dtmp, sc.dtmp2, dw[3], s));
   TRY(add_f32_launch(T * d, dy, sc.dtmp2, sc.dh, s));                     // dh = dy + norm path
   TRY(cast_bf16_launch(T * d, sc.dh, sc.dy_b, s));
-  TRY(gemm(mk(1, 0, d, d, T, sc.dy_b, d, sv.O, d, dw[2], d), s));        // dW_o = dh^T O
-  TRY(gemm(mk(0, 0, T, d, d, sc.dy_b, d, w[2], d, sc.dO, d, 1), s));     // dO = dh W_o (bf16)
+  if (D.int8) {
+    if ((qst = qproj_bwd(D, 1, sc.dy_b, sv.O, sc.dOf, dw[2], dw[7], sv, sc, s)) != CANON_OK) return qst;
+    TRY(cast_bf16_launch(T * d, sc.dOf, sc.dO, s));
+  } else {
+    TRY(gemm(mk(1, 0, d, d, T, sc.dy_b, d, sv.O, d, dw[2], d), s));        // dW_o = dh^T O
+    TRY(gemm(mk(0, 0, T, d, d, sc.dy_b, d, w[2], d, sc.dO, d, 1), s));     // dO = dh W_o (bf16)
+  }
   TRY(attn_rowdot_launch(D.B, H, S, hd, sc.dO, sv.O, d, sc.Dv, s));      // D = rowsum(dO * O)
   {  // dP = dO V^T, turned into dS = P * (dP - D) * c in the epilogue (bf16).  Tiles with no visible entry are
      // not computed: those left of the window band get their +0 written (the windowed dQ and dK ranges may
@@ -294,8 +427,12 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
   TRY(gemm(grouped(mk(1, 0, S, hd, G * S, sv.P, S, dO_heads, dO_ld, sc.dqkv + d + kvw, N, 1), H * S * S, G * S * S,
                    dO_s1, dO_s2, S * N, hd), s));
   TRY(rope_bwd_launch(D.B, S, H, Hkv, hd, sc.dq, sc.dk, cosT, sinT, D.qk_norm, sv.qkv, sv.rq, sc.dqkv, s));
-  TRY(gemm(mk(1, 0, N, d, T, sc.dqkv, N, sv.xn, d, dw[1], d), s));       // dW_qkv = dqkv^T xn
-  TRY(gemm(mk(0, 0, T, d, N, sc.dqkv, N, w[1], d, sc.dtmp, d), s));      // dxn = dqkv W_qkv
+  if (D.int8) {
+    if ((qst = qproj_bwd(D, 0, sc.dqkv, sv.xn, sc.dtmp, dw[1], dw[6], sv, sc, s)) != CANON_OK) return qst;
+  } else {
+    TRY(gemm(mk(1, 0, N, d, T, sc.dqkv, N, sv.xn, d, dw[1], d), s));       // dW_qkv = dqkv^T xn
+    TRY(gemm(mk(0, 0, T, d, N, sc.dqkv, N, w[1], d, sc.dtmp, d), s));      // dxn = dqkv W_qkv
+  }
   TRY(rownorm_bwd_launch(T, d, x, w[0], sv.rstd1, sc.dtmp, sc.dtmp2, dw[0], s));
   TRY(add_f32_launch(T * d, sc.dh, sc.dtmp2, dx, s));
   return CANON_OK;
@@ -309,7 +446,7 @@ int bit_length(int64_t x) {
 }
 
 // tensors in the declared order: embed, [embed_norm], per layer attn_norm, w_qkv, w_o, ffn_norm, w_gate_up,
-// w_down, then final_norm, head
+// w_down [, sx_qkv, sx_o, sx_gate_up, sx_down], then final_norm, head
 void tensor_sizes(const canon_model_cfg* c, std::vector<int64_t>& sz, std::vector<uint8_t>& decay) {
   const int64_t d = c->d_model, F = c->d_ffn, V = c->vocab;
   const int64_t N = d + 2 * kv_heads(c) * c->head_dim;
@@ -320,6 +457,8 @@ void tensor_sizes(const canon_model_cfg* c, std::vector<int64_t>& sz, std::vecto
     int64_t s6[6] = {d, N * d, d * d, d, 2 * F * d, d * F};
     uint8_t d6[6] = {0, 1, 1, 0, 1, 1};
     for (int i = 0; i < 6; ++i) { sz.push_back(s6[i]); decay.push_back(d6[i]); }
+    if (c->int8_linear)  // R19 activation steps of the four projections
+      for (int i = 0; i < 4; ++i) { sz.push_back(1); decay.push_back(0); }
   }
   sz.push_back(d); decay.push_back(0);
   sz.push_back(V * d); decay.push_back(1);
@@ -801,6 +940,21 @@ canon_status canon_attn_dq_fixed(int64_t batch, int64_t n_heads, int64_t n_kv_he
                                   n_heads * head_dim, as_stream(stream)));
 }
 
+size_t canon_lsq_step_grad_workspace_bytes(int64_t T, int64_t K) {
+  if (T < 0 || K < 1) return 0;
+  return sizeof(float) * (size_t)(lsq_grad_parts(T * K) + 1) + 256;
+}
+
+canon_status canon_lsq_step_grad(const canon_order* order, int64_t T, int64_t K, const uint16_t* x, const float* s,
+                                 const float* dx, float* grad, void* workspace, size_t workspace_bytes, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (T < 0 || K < 1 || !s || !grad || (T > 0 && (!x || !dx))) return CANON_EINVAL;
+  if (T * K > (int64_t(1) << 40)) return CANON_EUNSUPPORTED;
+  if (!workspace || workspace_bytes < canon_lsq_step_grad_workspace_bytes(T, K)) return CANON_EWORKSPACE;
+  return dev(lsq_grad_launch(T * K, x, s, dx, lsq_gamma(K), (float*)workspace, grad, as_stream(stream)));
+}
+
 canon_status canon_devmath(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
                            void* stream) {
   if (op < 0 || op > 10 || n < 0) return CANON_EINVAL;
@@ -829,8 +983,9 @@ canon_status canon_block_fwd_bwd(const canon_order* order, const canon_model_cfg
   if (st != CANON_OK) return st;
   if (!cfg_ok(cfg) || batch < 1 || !x || !dy || !w || !rope_cos || !rope_sin || !y || !dx || !dw)
     return CANON_EINVAL;
-  if (!attn_variants_supported(cfg)) return CANON_EUNSUPPORTED;
-  for (int i = 0; i < 6; ++i)
+  if (!variants_supported(cfg, (int64_t)batch * cfg->seq)) return CANON_EUNSUPPORTED;
+  const int nw = cfg->int8_linear ? 10 : 6;
+  for (int i = 0; i < nw; ++i)
     if (!w[i] || !dw[i]) return CANON_EINVAL;
   if ((int64_t)batch * cfg->n_heads > 65535) return CANON_EUNSUPPORTED;
   const size_t need = canon_block_workspace_bytes(cfg, batch);
@@ -842,6 +997,7 @@ canon_status canon_block_fwd_bwd(const canon_order* order, const canon_model_cfg
   carve_save(cv, D, sv);
   carve_scratch(cv, D, sc);
   hipStream_t s = as_stream(stream);
+  if (D.int8 && (st = prep_int8_layer(D, w, sv, s)) != CANON_OK) return st;
   st = block_forward(D, w, rope_cos, rope_sin, x, sv, sc, y, s);
   if (st != CANON_OK) return st;
   return block_backward(D, w, rope_cos, rope_sin, x, sv, sc, dy, dx, dw, s);
@@ -870,7 +1026,7 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
   if (st != CANON_OK) return st;
   if (!cfg_ok(cfg) || !plan || plan->accum < 1 || plan->dp_shard < 1 || plan->dp_replicate < 1) return CANON_EINVAL;
   if (!params || !m || !v || !windows || !rope_cos || !rope_sin || !consts || !loss_out) return CANON_EINVAL;
-  if (!attn_variants_supported(cfg)) return CANON_EUNSUPPORTED;
+  if (!variants_supported(cfg, (int64_t)cfg->micro_seqs * cfg->seq)) return CANON_EUNSUPPORTED;
   if (clip && (!(clip->max_norm > 0.0f) || clip->skip_steps < 0 || (clip->skip_steps > 0 && !clip->skip_state)))
     return CANON_EINVAL;
   std::vector<int64_t> sz;
@@ -903,6 +1059,13 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
   PlanRun lplan(1, *plan, plan->accum > 1 ? L.loss_gr : nullptr, L.loss_pool);
   const int nl = cfg->n_layers;
   const int64_t l0 = cfg->embed_norm ? 2 : 1;  // first layer tensor
+  const int PL = cfg->int8_linear ? 10 : 6;    // tensors per layer
+  if (cfg->int8_linear)  // the weights' codes and re-pinned steps, once per step
+    for (int l = 0; l < nl; ++l) {
+      const uint16_t* w[10];
+      for (int i = 0; i < PL; ++i) w[i] = params[l0 + PL * l + i];
+      if ((st = prep_int8_layer(D, w, L.saves[l], s)) != CANON_OK) return st;
+    }
   for (int r = 0; r < R; ++r) {
     for (int k = 0; k < plan->accum; ++k) {
       // R12: windows r + R*(k*mb + s), s < mb
@@ -918,14 +1081,14 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
       }
       TRY(labels_launch(mb, D.S, L.win, S1, L.lab, s));
       for (int l = 0; l < nl; ++l) {
-        const uint16_t* w[6];
-        for (int i = 0; i < 6; ++i) w[i] = params[l0 + 6 * l + i];
+        const uint16_t* w[10];
+        for (int i = 0; i < PL; ++i) w[i] = params[l0 + PL * l + i];
         Dims Dl = D;
         Dl.window = layer_window(cfg, l);
         st = block_forward(Dl, w, rope_cos, rope_sin, L.xs[l], L.saves[l], L.sc, L.xs[l + 1], s);
         if (st != CANON_OK) return st;
       }
-      const int64_t i_fn = l0 + 6 * nl, i_head = i_fn + 1;
+      const int64_t i_fn = l0 + PL * nl, i_head = i_fn + 1;
       TRY(rownorm_fwd_launch(D.T, D.d, L.xs[nl], params[i_fn], D.eps, L.xf, L.rstdf, s));
       TRY(gemm(mk(0, 1, D.T, D.V, D.d, L.xf, D.d, params[i_head], D.d, L.logits, D.V, 1), s));
       TRY(xent_launch(D.T, D.V, L.logits, L.lab, invT, D.z_loss, L.dlogits, L.row_loss, L.loss_mb, s));
@@ -935,11 +1098,11 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
       float* dcur = L.dxA;
       float* dnext = L.dxB;
       for (int l = nl - 1; l >= 0; --l) {
-        const uint16_t* w[6];
-        float* dw[6];
-        for (int i = 0; i < 6; ++i) {
-          w[i] = params[l0 + 6 * l + i];
-          dw[i] = L.grad + off[l0 + 6 * l + i];
+        const uint16_t* w[10];
+        float* dw[10];
+        for (int i = 0; i < PL; ++i) {
+          w[i] = params[l0 + PL * l + i];
+          dw[i] = L.grad + off[l0 + PL * l + i];
         }
         Dims Dl = D;
         Dl.window = layer_window(cfg, l);

@@ -167,6 +167,11 @@ hipError_t attn_pv_i8_launch(int64_t B, int64_t H, int64_t Hkv, int64_t S, int64
                              float* sv, hipStream_t s);
 hipError_t attn_dq_fixed_launch(int64_t B, int64_t H, int64_t Hkv, int64_t S, int64_t hd, int64_t window, int F,
                                 const uint16_t* dS, const uint16_t* K, float* dQ, int64_t ldq, hipStream_t s);
+// lsq.hip: R19 gradient of a per-tensor activation step over n = T K terms (x bf16, dx fp32, step at s);
+// part: scratch of lsq_grad_parts(n) floats; out: one float
+int64_t lsq_grad_parts(int64_t n);
+hipError_t lsq_grad_launch(int64_t n, const uint16_t* x, const float* s, const float* dx, float gamma, float* part,
+                           float* out, hipStream_t st);
 hipError_t set_nan_if_launch(const int32_t* flag, float* x, hipStream_t s);
 
 }  // namespace canon

@@ -1,0 +1,146 @@
+"""The int8 projections of the paper's W8A8 training (R19) on the device against the oracle, bit for bit: the
+LSQ gradient of an activation step (standalone, ragged sizes, ties, clamps, degenerate steps, the 1B gate/up
+input shape), decoder blocks with int8 projections (with the other variants and the int8 attention kernels)
+and full steps with every variant on."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_17380_amd.canon as C
+import paper_2609_17380_amd.inputs as I
+from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16
+
+pytestmark = pytest.mark.gpu
+
+NAMES = ["attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down", "sx_qkv", "sx_o", "sx_gate_up", "sx_down"]
+
+
+def run_lsq(x16, s, dx):
+    T, K = x16.shape
+    ws = torch.empty(C.lsq_step_grad_workspace_bytes(T, K), dtype=torch.uint8, device=DEV)
+    g = torch.empty(1, dtype=torch.float32, device=DEV)
+    C.lsq_step_grad(T, K, dev_bf16(x16), dev_f32(np.array([s], np.float32)), dev_f32(dx), g, ws)
+    torch.cuda.synchronize()
+    return host_f32(g)
+
+
+@pytest.mark.parametrize("T,K,s", [(1, 7, 0.1), (33, 100, 0.05), (256, 2048, 0.1416), (3, 40000, 0.02),
+                                   (1024, 5632, 0.0532), (64, 96, 0.0), (64, 96, -1.0), (64, 96, 1e-39)])
+def test_lsq_step_grad_bit_exact(T, K, s):
+    print(f"lsq grad T={T} K={K} s={s}", flush=True)
+    x16 = I.normal_bf16((T, K), 1, I.TENSOR_IDS["x_in"], std=3.0 * max(s, 0.05))
+    dx = I.normal_f32((T, K), 1, I.TENSOR_IDS["dy_in"], std=1e-3)
+    want = oracle.lsq_step_grad(x16, np.float32(s), dx)
+    assert_bits(run_lsq(x16, np.float32(s), dx), np.array([want], np.float32), "lsq grad")
+
+
+def test_lsq_step_grad_ties_and_clamps():
+    s = np.float32(0.125)
+    rng = np.random.default_rng(4)
+    m = rng.integers(-255, 256, (40, 64))
+    m[0, :4] = [2000, -2000, 508, -516]
+    x16 = ((m.astype(np.float32) / 32).view(np.uint32) >> 16).astype(np.uint16)
+    dx = rng.integers(-9, 10, (40, 64)).astype(np.float32)
+    want = oracle.lsq_step_grad(x16, s, dx)
+    assert_bits(run_lsq(x16, s, dx), np.array([want], np.float32), "lsq grad")
+
+
+def test_lsq_step_grad_sampled_at_the_1b_shape():
+    """The gate/up projection's input at the 1B step (8192 tokens x 2048), whole: one value, 16.8M terms."""
+    T, K = 8192, 2048
+    x16 = I.normal_bf16((T, K), 2, I.TENSOR_IDS["x_in"])
+    dx = I.normal_f32((T, K), 2, I.TENSOR_IDS["dy_in"], std=1e-3)
+    s = np.float32(0.1416)
+    assert_bits(run_lsq(x16, s, dx), np.array([oracle.lsq_step_grad(x16, s, dx)], np.float32), "lsq grad")
+
+
+def cfgs(L, d, H, F, V, S, mb, Hkv=0, qk=0, en=0, win=0, every=0, z=0.0, pv=0, dq=0, q8=1):
+    hd = d // H
+    args = (L, d, H, hd, F, V, S, mb, np.float32(1e-5), Hkv, qk, en, win, every, np.float32(z), pv, dq, q8)
+    return oracle.ModelCfg(*args), C.ModelCfg(*args)
+
+
+@pytest.mark.parametrize("d,H,Hkv,qk,win,F,S,batch,pv,dq", [
+    (256, 2, 0, 0, 0, 256, 128, 2, 0, 0), (256, 2, 1, 1, 40, 256, 128, 2, 0, 0), (256, 4, 2, 1, 0, 384, 256, 1, 0, 0),
+    (512, 4, 2, 1, 64, 512, 256, 2, 1, 40), (256, 2, 2, 0, 0, 640, 256, 1, 1, 0)])
+def test_block_int8_projections_bit_exact(d, H, Hkv, qk, win, F, S, batch, pv, dq):
+    print(f"int8 block d={d} H={H} Hkv={Hkv} qk={qk} win={win} F={F} S={S} B={batch} pv={pv} dq={dq}", flush=True)
+    hd = d // H
+    cfg_o, cfg_c = cfgs(1, d, H, F, 100, S, batch, Hkv=Hkv, qk=qk, win=win, pv=pv, dq=dq)
+    T = batch * S
+    x = I.bf16_bits_to_f32(I.normal_bf16((T, d), 4, I.TENSOR_IDS["x_in"]))
+    dy = I.bf16_bits_to_f32(I.normal_bf16((T, d), 4, I.TENSOR_IDS["dy_in"]))
+    kvw = (Hkv or H) * hd
+    shapes = [(d,), (d + 2 * kvw, d), (d, d), (d,), (2 * F, d), (d, F)]
+    w = [I.normal_bf16(s, 4, I.TENSOR_IDS[n], std=(0.1 if len(s) == 1 else 0.05), mean=(1.0 if len(s) == 1 else 0.0))
+         for s, n in zip(shapes, NAMES)]
+    w += [np.array([I.bf16_pattern(v)], np.uint16) for v in I.ACT_STEPS.values()]
+    shapes += [(1,)] * 4
+    cos, sin = I.rope_tables(S, hd)
+    y_o, dx_o, dw_o = oracle.block_fwd_bwd(cfg_o, batch, x, dy, w, cos, sin)
+    ws = torch.empty(C.block_workspace_bytes(cfg_c, batch), dtype=torch.uint8, device=DEV)
+    y = torch.empty((T, d), dtype=torch.float32, device=DEV)
+    dx = torch.empty_like(y)
+    dw = [torch.empty(s, dtype=torch.float32, device=DEV) for s in shapes]
+    C.block_fwd_bwd(cfg_c, batch, dev_f32(x), dev_f32(dy), [dev_bf16(t) for t in w], dev_f32(cos), dev_f32(sin), y,
+                    dx, dw, ws)
+    torch.cuda.synchronize()
+    assert_bits(host_f32(y), y_o, "y")
+    assert_bits(host_f32(dx), dx_o, "dx")
+    for n, g, go in zip(NAMES, dw, dw_o):
+        assert_bits(host_f32(g), go, "d" + n)
+
+
+@pytest.mark.parametrize("variant,plan", [
+    (dict(), (1, 2, 1)),
+    (dict(Hkv=1, qk=1, en=1, win=48, every=2, z=1e-4), (2, 1, 1)),
+    (dict(Hkv=1, qk=1, en=1, win=48, every=2, z=1e-4, pv=1, dq=40), (1, 1, 2)),
+])
+def test_step_int8_projections_bit_exact(variant, plan):
+    print(f"int8 step {variant} plan {plan}", flush=True)
+    L, d, H, F, V, S, mb = 2, 256, 2, 256, 300, 128, 2
+    hd = d // H
+    cfg_o, cfg_c = cfgs(L, d, H, F, V, S, mb, **variant)
+    Hkv = variant.get("Hkv", 0) or H
+    en = bool(variant.get("en", 0))
+    params = I.model_params(L, d, F, V, seed=0, std=0.02, kv_dim=Hkv * hd, embed_norm=en, int8_linear=True)
+    R = plan[1] * plan[2]
+    windows = I.uniform_int((R * plan[0] * mb, S + 1), 0, I.TENSOR_IDS["windows"], V)
+    cos, sin = I.rope_tables(S, hd)
+    k = I.adamw_constants()
+    po = [p.copy() for p in params]
+    mo = [np.zeros(p.shape, np.float32) for p in params]
+    vo = [np.zeros(p.shape, np.float32) for p in params]
+    loss_o, g_o, info = oracle.step(cfg_o, oracle.Plan(*plan), po, mo, vo, windows, cos, sin,
+                                    oracle.AdamWConsts(*k), want_grads=True, clip=oracle.ClipCfg(1.0, 5.0, 5))
+    pg = [dev_bf16(p) for p in params]
+    mg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
+    vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
+    gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params]
+    cplan = C.DPPlan(*plan)
+    ws = torch.empty(C.step_workspace_bytes(cfg_c, cplan), dtype=torch.uint8, device=DEV)
+    loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+    norm = torch.zeros(1, dtype=torch.float32, device=DEV)
+    state = torch.zeros(1, dtype=torch.int32, device=DEV)
+    C.step(cfg_c, cplan, pg, mg, vg, dev_i32(windows), dev_f32(cos), dev_f32(sin), C.AdamWConsts(*k), ws, loss,
+           grads_out=gg, clip=C.make_clip(1.0, 5.0, 5, norm, state))
+    torch.cuda.synchronize()
+    assert_bits(host_f32(loss), np.array([loss_o], np.float32), "loss")
+    assert_bits(host_f32(norm), np.array([info["norm"]], np.float32), "pre-clip norm")
+    for i in range(len(po)):
+        assert_bits(host_f32(gg[i]), g_o[i], f"grad {i}")
+        assert_bits(host_u16(pg[i]), po[i], f"param {i}")
+        assert_bits(host_f32(mg[i]), mo[i], f"m {i}")
+        assert_bits(host_f32(vg[i]), vo[i], f"v {i}")
+
+
+def test_int8_projections_reject_unsupported_shapes():
+    # tokens per call not a multiple of 256 (no whole rotation blocks along T): refused before any launch
+    _, cfg_c = cfgs(1, 256, 2, 256, 100, 100, 1)
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device=DEV)
+    t = torch.empty(1, device=DEV)
+    with pytest.raises(C.CanonError):
+        C.block_fwd_bwd(cfg_c, 1, t, t, [t] * 10, t, t, t, t, [t] * 10, ws)
