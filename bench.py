@@ -261,6 +261,7 @@ def kernel_table(C, I, torch, np, stream, dev):
     out.update(int8_attention(C, torch, stream, dev, randn))
     out.update(open1b_step(C, I, torch, np, stream, dev))
     out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
+    out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True, int8_linear=True))
     for k_, v_ in out.items():
         print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({100 * v_['frac']:.1f}%)",
               file=sys.stderr, flush=True)
@@ -307,17 +308,21 @@ def int8_attention(C, torch, stream, dev, randn):
 O1B = dict(L=24, d=2048, H=16, Hkv=4, hd=128, F=5632, V=128256, S=4096, mb=4, window=512, full_every=5)
 
 
-def open1b_step(C, I, torch, np, stream, dev, int8_attn=False):
+def open1b_step(C, I, torch, np, stream, dev, int8_attn=False, int8_linear=False):
     """One step of the paper's architecture with every variant on (one rank, one microbatch of 4 x 4096 tokens,
     the clip at 1.0), timed after one warmup step.  int8_attn: also the int8 path's attention kernels (P.V in
-    int8 per block, dQ in 64-bit fixed point with 40 fractional bits)."""
+    int8 per block, dQ in 64-bit fixed point with 40 fractional bits); int8_linear: the four projections of
+    every block in int8 with learned activation steps (the paper's production configuration with both)."""
     o = O1B
-    print(f"bench: open-1B step (all variants{', int8 attention' if int8_attn else ''})", file=sys.stderr, flush=True)
+    tag = ("all_variants" + ("_int8_attention" if int8_attn and not int8_linear else "")
+           + ("_int8_production" if int8_linear else ""))
+    print(f"bench: open-1B step ({tag})", file=sys.stderr, flush=True)
     cfg = C.ModelCfg(o["L"], o["d"], o["H"], o["hd"], o["F"], o["V"], o["S"], o["mb"], np.float32(1e-5), o["Hkv"],
-                     1, 1, o["window"], o["full_every"], np.float32(1e-4), int(int8_attn), 40 if int8_attn else 0)
+                     1, 1, o["window"], o["full_every"], np.float32(1e-4), int(int8_attn), 40 if int8_attn else 0,
+                     int(int8_linear))
     plan = C.DPPlan(1, 1, 1)
     params = I.model_params(o["L"], o["d"], o["F"], o["V"], seed=0, std=0.02, kv_dim=o["Hkv"] * o["hd"],
-                            embed_norm=True)
+                            embed_norm=True, int8_linear=int8_linear)
     pg = [torch.from_numpy(p.view(np.int16)).to(dev) for p in params]
     del params
     mg = [torch.zeros(p.shape, dtype=torch.float32, device=dev) for p in pg]
@@ -340,7 +345,10 @@ def open1b_step(C, I, torch, np, stream, dev, int8_attn=False):
            "loss": float(loss.item()), "grad_norm_preclip": float(gnorm.item())}
     del ws, pg, mg, vg
     torch.cuda.empty_cache()
-    return {"step_open1b_4x4096_all_variants" + ("_int8_attention" if int8_attn else ""): res}
+    if int8_linear:  # int8 projections next to fp32 canonical attention and head: no single roofline
+        res.update({"bound": "mixed", "peak": None, "frac": None,
+                    "note": "algorithmic rate; the int8 projection GEMMs count 2 operations per multiply-add"})
+    return {"step_open1b_4x4096_" + tag: res}
 
 
 def main():
@@ -353,7 +361,7 @@ def main():
     ap.add_argument("--no-kernel-table", action="store_true")
     ap.add_argument("--open1b-only", action="store_true",
                     help="time only the paper-architecture step (all variants; without and with the int8 "
-                         "attention kernels) and print its entries")
+                         "attention kernels; the int8 production configuration) and print its entries")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -373,6 +381,7 @@ def main():
     if args.open1b_only:
         res = open1b_step(C, I, torch, np, stream, dev)
         res.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
+        res.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True, int8_linear=True))
         print(json.dumps(res), flush=True)
         return
     print("bench: generating inputs", file=sys.stderr, flush=True)
