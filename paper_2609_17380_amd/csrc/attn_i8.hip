@@ -39,18 +39,6 @@ __device__ __forceinline__ uint32_t bf16_mag(uint16_t h) {
   return (m & 0x7F80u) ? m : 0u;
 }
 
-// R13's quantiser clamp(rne(RN(v / s)), -128, 127) for a step s > 0 (finite, normal) and |v| <= 128 s, from
-// t = RN(v * rs) with rs = RN(1 / s): |t - v/s| <= |v/s| (2^-23 + 2^-48) < 2^-16 and |RN(v/s) - v/s| <= 2^-17, so
-// when t is farther than 2^-15 from every half-integer, no rounding boundary separates t from RN(v / s) and
-// both round to the same integer.  Closer than that, the correctly rounded quotient decides.
-__device__ __forceinline__ int8_t quant_recip(float v, float s, float rs) {
-  const float t = v * rs;
-  const float n = __builtin_rintf(t);
-  const float d = fabsf(t - n);  // exact (Sterbenz), at most 1/2
-  if (0.5f - d > 0x1p-15f) return (int8_t)(int)fminf(fmaxf(n, -128.0f), 127.0f);
-  return quant1(v, s);
-}
-
 __device__ __forceinline__ uint32_t wave_umax(uint32_t v) {
 #pragma unroll
   for (int s = 32; s >= 1; s >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, s, 64));
@@ -86,9 +74,12 @@ __global__ __launch_bounds__(256) void attn_vquant_kernel(int64_t S, int64_t hd,
   const float step = __uint_as_float(m << 16) * __uint_as_float(kInv127Bits);
   if (threadIdx.x == 0) sv[bg * nb + kb] = step;
   const float st = step_daz(step);
+  const bool recip = recip_step_ok(st);
+  const float rst = recip ? 1.0f / st : 0.0f;
   for (int64_t e = threadIdx.x; e < PVB * hd; e += 256) {
     const int64_t c = e / PVB, j = e % PVB;
-    const int8_t q = j < nk ? quant1(bf16_to_f32(src[j * hd + c]), st) : (int8_t)0;
+    const float vf = j < nk ? bf16_to_f32(src[j * hd + c]) : 0.0f;
+    const int8_t q = j < nk ? (recip ? quant_recip(vf, st, rst) : quant1(vf, st)) : (int8_t)0;
     qvt[(bg * hd + c) * Sp + k0 + j] = q;
   }
 }
@@ -222,8 +213,7 @@ __global__ __launch_bounds__(256) void attn_pv_i8_kernel(PvArgs a) {
     m = max(max(red[buf][0], red[buf][1]), max(red[buf][2], red[buf][3]));
     const float sp = __uint_as_float(m << 16) * __uint_as_float(kInv127Bits);
     const float spd = step_daz(sp);
-    // every |p| <= amax, so |p / sp| < 128 whenever the step is a positive finite number (normal after the flush)
-    const bool recip = spd > 0.0f && spd < __builtin_inff();
+    const bool recip = recip_step_ok(spd);
     const float rsp = recip ? 1.0f / spd : 0.0f;
     uint32_t word0 = 0, word1 = 0, word2 = 0, word3 = 0;
 #pragma unroll

@@ -129,6 +129,23 @@ __device__ __forceinline__ int8_t quant1(float v, float sv) {
   return out;
 }
 
+// The same quantiser through the reciprocal of a step shared by many values: for a step s in (0, 2^126]
+// (positive, normal, with a normal reciprocal) and rs = RN(1/s), t = RN(v * rs) lies within |v/s| 2^-23
+// (1 + 2^-25) of v/s.  |t| >= 129 means |v/s| > 128.9: the clamp decides.  Otherwise |t - v/s| < 1.6e-5 and
+// |RN(v/s) - v/s| <= 2^-17, so when t is farther than 2^-15 from every half-integer no rounding boundary
+// separates t from RN(v/s) and both round to the same integer; closer than that, the correctly rounded
+// quotient decides.  A NaN t falls through to it as well.
+__device__ __forceinline__ bool recip_step_ok(float s) { return s > 0.0f && s <= 0x1p126f; }
+
+__device__ __forceinline__ int8_t quant_recip(float v, float s, float rs) {
+  const float t = v * rs;
+  if (fabsf(t) >= 129.0f) return t > 0.0f ? (int8_t)127 : (int8_t)-128;
+  const float n = __builtin_rintf(t);
+  const float d = fabsf(t - n);  // exact (Sterbenz), at most 1/2
+  if (0.5f - d > 0x1p-15f) return (int8_t)(int)fminf(fmaxf(n, -128.0f), 127.0f);
+  return quant1(v, s);
+}
+
 __device__ __forceinline__ float step_daz(float s) {
   uint32_t sb = __float_as_uint(s);
   if ((sb & 0x7F800000u) == 0u) sb &= 0x80000000u;  // a subnormal step reads as zero

@@ -652,8 +652,18 @@ template <int DT>
 __global__ void quantize_kernel(int64_t rows, int64_t cols, const void* __restrict__ x,
                                 const float* __restrict__ scale, int32_t per_row, int8_t* __restrict__ q) {
   const int64_t n = rows * cols;
+  if (!per_row) {  // one step for every value: its reciprocal once per thread
+    const float sv = step_daz(scale[0]);
+    const bool recip = recip_step_ok(sv);
+    const float rs = recip ? 1.0f / sv : 0.0f;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
+      const float v = DT == 0 ? static_cast<const float*>(x)[i] : bf16_to_f32(static_cast<const uint16_t*>(x)[i]);
+      q[i] = recip ? quant_recip(v, sv, rs) : quant1(v, sv);
+    }
+    return;
+  }
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) {
-    const float sv = step_daz(scale[per_row ? i / cols : 0]);
+    const float sv = step_daz(scale[i / cols]);
     const float v = DT == 0 ? static_cast<const float*>(x)[i] : bf16_to_f32(static_cast<const uint16_t*>(x)[i]);
     q[i] = quant1(v, sv);
   }
@@ -663,15 +673,16 @@ __global__ void quantize_kernel(int64_t rows, int64_t cols, const void* __restri
 __global__ void quantize_tensor4_kernel(int64_t n, const float* __restrict__ x, const float* __restrict__ scale,
                                         int8_t* __restrict__ q) {
   const float sv = step_daz(scale[0]);
+  const bool recip = recip_step_ok(sv);
+  const float rs = recip ? 1.0f / sv : 0.0f;
+  auto qz = [&](float v) -> uint32_t { return (uint8_t)(recip ? quant_recip(v, sv, rs) : quant1(v, sv)); };
   const int64_t n4 = n >> 2;
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
     const float4 v = reinterpret_cast<const float4*>(x)[i];
-    const uint32_t b0 = (uint8_t)quant1(v.x, sv), b1 = (uint8_t)quant1(v.y, sv), b2 = (uint8_t)quant1(v.z, sv),
-                   b3 = (uint8_t)quant1(v.w, sv);
-    reinterpret_cast<uint32_t*>(q)[i] = b0 | (b1 << 8) | (b2 << 16) | (b3 << 24);
+    reinterpret_cast<uint32_t*>(q)[i] = qz(v.x) | (qz(v.y) << 8) | (qz(v.z) << 16) | (qz(v.w) << 24);
   }
   const int64_t t = n4 * 4 + (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t < n) q[t] = quant1(x[t], sv);
+  if (t < n) q[t] = (int8_t)qz(x[t]);
 }
 
 hipError_t quantize_launch(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale,

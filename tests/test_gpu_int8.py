@@ -155,3 +155,36 @@ def test_qlinear_bwd_one_output_and_mid_size():
     qlinear_bwd_case(256, 96, 40, seed=1, want_dx=False)   # dW only: N need not be a multiple of 256
     qlinear_bwd_case(80, 512, 40, seed=2, want_dw=False)   # dx only: T need not be a multiple of 256
     qlinear_bwd_case(2048, 2048, 512, seed=3)              # several tiles per operand, full rotation blocks
+
+
+@pytest.mark.parametrize("s", [0.1, 0.0173, 1.0 / 3.0, 3e-38, 2.0 ** 126, 2.0 ** 127, 1e38, 7.0])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_quantize_per_tensor_near_every_boundary(s, dtype):
+    """One step for the whole tensor takes the reciprocal path: values at, just inside and just outside every
+    half-integer multiple of the step (and of the clamp bounds), for steps whose reciprocal is inexact, tiny,
+    beyond 2^126 (no reciprocal path) or huge; the result must equal the correctly rounded quotient's."""
+    s32 = np.float32(s)
+    k = np.arange(-131, 132, dtype=np.float64)
+    base = (k + 0.5) * np.float64(s32)
+    vals = []
+    for b in base:
+        f = np.float32(b)
+        u = int(np.array([f], np.float32).view(np.uint32)[0])
+        for du in (-2, -1, 0, 1, 2):
+            vals.append(np.array([u + du], np.uint32).view(np.float32)[0] if f != 0 else np.float32(0))
+    vals += [np.float32(v) for v in (np.inf, -np.inf, np.nan, 0.0, -0.0, 1e-40, 3e38, -3e38)]
+    x = np.array(vals, np.float32)
+    x = np.concatenate([x, RNG.standard_normal(4096).astype(np.float32) * np.float32(50 * s32 if s < 1e37 else 1)])
+    n = (x.size // 4) * 4
+    x = x[:n].reshape(4, -1)
+    rows, cols = x.shape
+    if dtype == "bf16":
+        xh = (x.view(np.uint32) >> 16).astype(np.uint16)
+        want, xd = oracle.quantize(xh, np.array([s32]), False), dev_bf16(xh)
+    else:
+        want, xd = oracle.quantize(x, np.array([s32]), False), dev_f32(x)
+    q = torch.empty((rows, cols), dtype=torch.int8, device=DEV)
+    C.quantize(rows, cols, xd, dev_f32(np.array([s32])), False, q)
+    torch.cuda.synchronize()
+    got = q.cpu().numpy()
+    assert np.array_equal(got, want), np.argwhere(got != want)[:5]
