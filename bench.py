@@ -263,7 +263,8 @@ def kernel_table(C, I, torch, np, stream, dev):
     out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
     out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True, int8_linear=True))
     for k_, v_ in out.items():
-        print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({100 * v_['frac']:.1f}%)",
+        frac = f"{100 * v_['frac']:.1f}%" if v_.get("frac") is not None else "no single roofline"
+        print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({frac})",
               file=sys.stderr, flush=True)
     return out
 
