@@ -508,6 +508,215 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   }
 }
 
+// Short contractions: at most four chunks (K <= 128: the attention score and dP products), both operands
+// k-contiguous and no causal chunk ranges.  One tile is then too little work to hide a workgroup's start
+// (launch, first loads) and end (the epilogue's loads and stores), so a persistent grid of two workgroups per
+// CU walks the tiles of the batch matrices, each workgroup every G-th tile of its sequence.  The first chunk
+// of the next tile is loaded during the last chunk of the current one and its second chunk before the
+// current tile's stores (so that waiting for those loads does not wait for the stores); the dS epilogue's P
+// and D operands are fetched one chunk before the last.  Per output tile the arithmetic is that of
+// gemm_mfma_kernel: chunk chains from +0, then the fold of the at most four partials (two: p0 + p1;
+// three: (p0 + p1) + p2; four: (p0 + p1) + (p2 + p3)).
+struct ShortTile {
+  const uint16_t* A;
+  const uint16_t* B;
+  int64_t z1, z2, row0, col0;
+  bool whole;  // the whole tile inside the m x n matrix
+};
+
+// Position in a workgroup's tile sequence: batch matrix z = zl * X + x (X = kXcds when the batch splits evenly
+// over the XCDs, else 1; x = the workgroup's XCD), tile row tm, tile column tn; advanced by the number of
+// workgroups per XCD group with carries instead of divisions.
+constexpr uint32_t kXcds = 8;
+struct TileWalk {
+  uint32_t zl, tm, tn;
+};
+
+template <bool TA, bool TB, int NC>
+__global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) float As[2][A_FLOATS];
+  __shared__ __attribute__((aligned(16))) float Bs[2][B_FLOATS];
+  // the launcher keeps the tile counts below 2^31
+  const uint32_t tiles_n = (uint32_t)((g.n + BN - 1) / BN), tiles_m = (uint32_t)((g.m + BM - 1) / BM);
+  const uint32_t per = tiles_m * tiles_n, nb2 = (uint32_t)g.nb2, batch = (uint32_t)g.batch;
+  // Workgroup b runs on XCD b % 8 (the dispatcher deals workgroups to the XCDs in turn).  With the batch a
+  // multiple of 8 (and the grid too), the workgroups of one XCD take the matrices z = x, x + 8, ...: each
+  // XCD's L2 then holds the operands of its own matrices only.
+  const uint32_t X = (batch % kXcds == 0 && gridDim.x % kXcds == 0) ? kXcds : 1;
+  const uint32_t x = blockIdx.x % X, G = gridDim.x / X, nzl = batch / X;
+  const uint32_t step_n = G % tiles_n, step_m = (G / tiles_n) % tiles_m, step_z = G / per;
+  const bool ds = g.epi == EPI_DS;
+  const int lane = threadIdx.x & 63;
+  const int w = threadIdx.x >> 6;
+  const int wr = w >> 1, wc = w & 1;
+  const int ai = wr * 32 + (lane & 31), bi = wc * 64 + lane;
+  // register v, lane l -> block v/16, row (v%4) + 4*(l/32) + 8*((v%16)/4), column l%32: the tile offset of
+  // register v is a lane part plus a part common to all lanes (kept in scalar registers; the launcher keeps
+  // 64 rows of C and P within 32-bit offsets)
+  const int lrow = wr * 32 + 4 * (lane >> 5), lcol = wc * 64 + (lane & 31);
+  const uint32_t loff_c = (uint32_t)(lrow * g.ldc + lcol);
+  const uint32_t loff_p = (uint32_t)(lrow * g.ds_ldp + lcol);
+  auto urow = [](int v) { return (v & 3) + 8 * ((v & 15) >> 2); };
+  auto ucol = [](int v) { return 32 * (v >> 4); };
+  auto visible = [&](int64_t i, int64_t j) -> bool { return j <= i && (g.ds_window == 0 || j > i - g.ds_window); };
+
+  auto start = [&]() {
+    TileWalk W;
+    const uint32_t u = blockIdx.x / X, r = u % per;
+    W.zl = u / per;
+    W.tm = r / tiles_n;
+    W.tn = r - W.tm * tiles_n;
+    return W;
+  };
+  auto advance = [&](TileWalk& W) {
+    W.tn += step_n;
+    uint32_t carry = 0;
+    if (W.tn >= tiles_n) { W.tn -= tiles_n; carry = 1; }
+    W.tm += step_m + carry;
+    carry = 0;
+    if (W.tm >= tiles_m) { W.tm -= tiles_m; carry = 1; }
+    W.zl += step_z + carry;
+  };
+  auto done = [&](const TileWalk& W) { return W.zl >= nzl; };
+  auto tile_of = [&](const TileWalk& W) -> ShortTile {
+    ShortTile T;
+    const uint32_t z = W.zl * X + x;
+    T.z1 = z / nb2;
+    T.z2 = z - (uint32_t)T.z1 * nb2;
+    T.row0 = (int64_t)W.tm * BM;
+    T.col0 = (int64_t)W.tn * BN;
+    T.A = g.a + T.z1 * g.sa1 + T.z2 * g.sa2;
+    T.B = g.b + T.z1 * g.sb1 + (g.b_group > 1 ? T.z2 / g.b_group : T.z2) * g.sb2;
+    T.whole = T.row0 + BM <= g.m && T.col0 + BN <= g.n;
+    return T;
+  };
+  auto upper_dead = [&](const TileWalk& W) { return g.tri_lower && (int64_t)W.tn * BN > (int64_t)W.tm * BM + BM - 1; };
+  auto band_dead = [&](const TileWalk& W) {
+    return g.tri_lower && g.kwin > 0 && (int64_t)W.tn * BN + BN - 1 <= (int64_t)W.tm * BM - g.kwin;
+  };
+  auto in_range = [&](const ShortTile& T, int v) {
+    return T.row0 + lrow + urow(v) < g.m && T.col0 + lcol + ucol(v) < g.n;
+  };
+  // first, the tiles without a visible entry whose +0 the dS epilogue writes
+  if (ds && g.tri_lower && (g.zero_dead || g.kwin > 0)) {
+    for (TileWalk W = start(); !done(W); advance(W)) {
+      if (!((upper_dead(W) && g.zero_dead) || band_dead(W))) continue;
+      const ShortTile T = tile_of(W);
+      uint16_t* C = (uint16_t*)g.c + T.z1 * g.sc1 + T.z2 * g.sc2 + T.row0 * g.ldc + T.col0;
+#pragma unroll
+      for (int v = 0; v < 32; ++v)
+        if (in_range(T, v)) (C + urow(v) * g.ldc + ucol(v))[loff_c] = 0;
+    }
+  }
+  // move to the next tile (of this workgroup's sequence, from X on) that has a visible entry
+  auto to_live = [&](TileWalk& W) {
+    while (!done(W) && (upper_dead(W) || band_dead(W))) advance(W);
+  };
+  auto load = [&](const ShortTile& T, int c) -> Raw {
+    if (g.vec && T.whole && (int64_t)(c + 1) * KC <= g.k)
+      return load_chunk<TA, TB, true>(g, T.A, T.B, T.row0, T.col0, (int64_t)c * KC, true);
+    return load_chunk<TA, TB, false>(g, T.A, T.B, T.row0, T.col0, (int64_t)c * KC, g.vec != 0);
+  };
+
+  TileWalk cw = start();
+  to_live(cw);
+  if (done(cw)) return;
+  ShortTile cur = tile_of(cw);
+  int buf = 0;
+  store_chunk<TA, TB>(As[0], Bs[0], load(cur, 0));
+  __syncthreads();
+  Raw pre;  // chunk 1 of the current tile when its loads went ahead of the previous tile's stores
+  bool have_pre = false;
+  constexpr int PC = NC >= 2 ? NC - 2 : 0;  // the chunk during which the dS operands are fetched
+  for (;;) {
+    TileWalk nw = cw;
+    advance(nw);
+    to_live(nw);
+    const bool has_next = !done(nw);
+    const ShortTile nxt = has_next ? tile_of(nw) : cur;
+    uint16_t pv[32];
+    float dv[16];
+    v32f r, p2;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const bool last = c + 1 == NC;
+      const bool more = !last || has_next;
+      Raw nx;
+      if (more) {
+        if (last) nx = load(nxt, 0);
+        else if (c == 0 && have_pre) nx = pre;
+        else nx = load(cur, c + 1);
+      }
+      if (ds && c == PC) {  // the dS epilogue's operands of this tile (out-of-range entries: +0, not read)
+        const uint16_t* P = g.ds_p + cur.z1 * g.ds_sp1 + cur.z2 * g.ds_sp2 + cur.row0 * g.ds_ldp + cur.col0;
+        const float* Dv = g.ds_d + cur.z1 * g.ds_sd1 + cur.z2 * g.ds_sd2 + cur.row0 + lrow;
+#pragma unroll
+        for (int v = 0; v < 32; ++v)
+          pv[v] = (cur.whole || in_range(cur, v)) ? (P + urow(v) * g.ds_ldp + ucol(v))[loff_p] : (uint16_t)0;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) dv[v] = (cur.whole || cur.row0 + lrow + urow(v) < g.m) ? Dv[urow(v)] : 0.0f;
+      }
+      __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of this chunk's chain
+      const int64_t kleft = g.k - (int64_t)c * KC;
+      const v32f acc = kleft >= KC ? chain_full<TA, TB>(As[buf], Bs[buf], ai, bi)
+                                   : chain_part<TA, TB>(As[buf], Bs[buf], ai, bi, (int)kleft);
+      __builtin_amdgcn_sched_barrier(0);
+      if (more) store_chunk<TA, TB>(As[buf ^ 1], Bs[buf ^ 1], nx);
+      __syncthreads();
+      buf ^= 1;
+      if (c == 0) r = acc;
+      else if (c == 1) r = r + acc;
+      else if (c == 2) { if (NC == 3) r = r + acc; else p2 = acc; }
+      else r = r + (p2 + acc);
+    }
+    // the next tile's chunk 1 is loaded before this tile's stores, so that waiting for it does not wait for them
+    have_pre = NC > 1 && has_next;
+    if (have_pre) pre = load(nxt, 1);
+    const int64_t off = cur.z1 * g.sc1 + cur.z2 * g.sc2 + cur.row0 * g.ldc + cur.col0;
+    if (ds) {
+      uint16_t* C = (uint16_t*)g.c + off;
+      const int64_t i0 = cur.row0 + lrow, j0 = cur.col0 + lcol;
+#pragma unroll
+      for (int v = 0; v < 32; ++v) {
+        const float d = r[v] - dv[v & 15];
+        const float u = bf16_to_f32(pv[v]) * d;
+        const uint16_t val = f32_to_bf16(u * g.ds_scale);
+        const uint16_t o = visible(i0 + urow(v), j0 + ucol(v)) ? val : (uint16_t)0;
+        if (cur.whole || in_range(cur, v)) (C + urow(v) * g.ldc + ucol(v))[loff_c] = o;
+      }
+    } else if (g.out_bf16) {
+      uint16_t* C = (uint16_t*)g.c + off;
+#pragma unroll
+      for (int v = 0; v < 32; ++v)
+        if (cur.whole || in_range(cur, v)) (C + urow(v) * g.ldc + ucol(v))[loff_c] = f32_to_bf16(r[v]);
+    } else {
+      float* C = (float*)g.c + off;
+#pragma unroll
+      for (int v = 0; v < 32; ++v)
+        if (cur.whole || in_range(cur, v)) (C + urow(v) * g.ldc + ucol(v))[loff_c] = r[v];
+    }
+    if (!has_next) break;
+    cw = nw;
+    cur = nxt;
+  }
+}
+
+// g: A [m][k] and B [n][k] (both k-contiguous), 1 <= chunks <= 4
+static hipError_t launch_short(const GemmArgs& g, int64_t nc, int64_t tiles, hipStream_t s) {
+  int dev = 0, cus = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  if (e != hipSuccess) return e;
+  int64_t want = 2 * (int64_t)(cus > 0 ? cus : 1);  // two resident workgroups per CU
+  if (want >= 8) want -= want % 8;                  // whole groups of the 8 XCDs
+  const dim3 grid((unsigned)(tiles < want ? tiles : want));
+  if (nc == 1) hipLaunchKernelGGL((gemm_short_kernel<false, true, 1>), grid, dim3(256), 0, s, g);
+  else if (nc == 2) hipLaunchKernelGGL((gemm_short_kernel<false, true, 2>), grid, dim3(256), 0, s, g);
+  else if (nc == 3) hipLaunchKernelGGL((gemm_short_kernel<false, true, 3>), grid, dim3(256), 0, s, g);
+  else hipLaunchKernelGGL((gemm_short_kernel<false, true, 4>), grid, dim3(256), 0, s, g);
+  return hipGetLastError();
+}
+
 template <int MAXL>
 static hipError_t launch_maxl(const GemmArgs& g, dim3 grid, hipStream_t s) {
   if (!g.trans_a && !g.trans_b) hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false>), grid, dim3(256), 0, s, g);
@@ -531,6 +740,10 @@ hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
   int bits = 0;
   while ((int64_t(1) << bits) <= nc) ++bits;  // nc < 2^bits: a push never runs past the top level
   const int64_t tiles = ((g.m + BM - 1) / BM) * ((g.n + BN - 1) / BN);
+  if (!g.trans_a && g.trans_b && nc >= 1 && nc <= 4 && g.kmode == KMODE_FULL && g.kseg == 0 &&
+      BM * g.ldc < (int64_t(1) << 31) && BM * g.ds_ldp < (int64_t(1) << 31) && tiles * g.batch < (int64_t(1) << 31) &&
+      g.nb2 > 0 && g.batch % g.nb2 == 0)
+    return launch_short(g, nc, tiles * g.batch, s);
   dim3 grid((unsigned)tiles, 1, (unsigned)g.batch);
   if (bits <= 3) return launch_maxl<3>(g, grid, s);
   if (bits <= 5) return launch_maxl<5>(g, grid, s);

@@ -75,6 +75,23 @@ def test_strided_batched_and_determinism():
     assert torch.equal(c.view(torch.int32), c2.view(torch.int32))
 
 
+@pytest.mark.parametrize("m,n,k", [(200, 300, 128), (130, 260, 70), (64, 128, 32), (257, 129, 97)])
+def test_short_contraction_batches(m, n, k):
+    """K <= 128 with both operands k-contiguous takes the persistent short-contraction kernel: more tiles than
+    resident workgroups (each walks several tiles, ragged ones among them), every batch matrix bit-exact."""
+    tiles = -(-m // 64) * -(-n // 128)
+    bt = -(-768 // tiles)  # 768 tiles: more than the 512 resident workgroups of 256 CUs
+    print(f"gemm short {bt}x {m}x{n}x{k}", flush=True)
+    a = I.normal_bf16((bt, m, k), 6, 1)
+    b = I.normal_bf16((bt, n, k), 6, 2)
+    c = torch.empty((bt, m, n), dtype=torch.float32, device=DEV)
+    C.gemm_strided_batched(m, n, k, dev_bf16(a), k, m * k, dev_bf16(b), k, n * k, c, n, m * n, bt, trans_b=1)
+    torch.cuda.synchronize()
+    got = host_f32(c)
+    for z in range(bt):
+        assert_bits(got[z], oracle.gemm(a[z], b[z], False, True), f"batch {z}")
+
+
 def test_invalid_arguments_are_rejected():
     a = torch.zeros(16, dtype=torch.bfloat16, device=DEV)
     c = torch.zeros(16, dtype=torch.float32, device=DEV)
