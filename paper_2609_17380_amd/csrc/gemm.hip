@@ -311,11 +311,17 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   const int64_t gsize = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
   const int64_t within = tile - group * GM * tiles_n;
   int64_t tm = first_m + within % gsize, tn = within / gsize;
+  int64_t z = blockIdx.z;
   if (g.kmode != KMODE_FULL) {
-    // causally skipping GEMMs: tile cost grows with the row tile (TRAIL) or shrinks with it (LEAD); launch the
-    // longest tiles first so the short ones fill the tail
-    tm = blockIdx.x / tiles_n;
-    tn = blockIdx.x % tiles_n;
+    // causally skipping GEMMs: tile cost grows with the row tile (TRAIL) or shrinks with it (LEAD).  Over the
+    // whole launch (in dispatch order, blockIdx.x fastest), the longest tiles of every batch matrix go first
+    // so the short ones fill the tail; the batch index runs fastest, so the workgroups on one XCD (every 8th)
+    // share its matrices.
+    const int64_t l = blockIdx.x + (int64_t)gridDim.x * blockIdx.z;
+    const int64_t rank = l / g.batch;
+    z = l - rank * g.batch;
+    tm = rank / tiles_n;
+    tn = rank % tiles_n;
     if (g.kmode == KMODE_TRAIL) tm = tiles_m - 1 - tm;
   }
   const int64_t row0 = tm * BM, col0 = tn * BN;
@@ -324,7 +330,6 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   if ((upper_dead && !(g.zero_dead && g.epi == EPI_DS)) || (band_dead && g.epi != EPI_DS)) return;
   const bool dead = upper_dead || band_dead;  // the epilogue writes this tile's +0
 
-  const int64_t z = blockIdx.z;
   const int64_t z1 = z / g.nb2, z2 = z % g.nb2;
   const uint16_t* A = g.a + z1 * g.sa1 + z2 * g.sa2;
   const uint16_t* B = g.b + z1 * g.sb1 + (g.b_group > 1 ? z2 / g.b_group : z2) * g.sb2;
