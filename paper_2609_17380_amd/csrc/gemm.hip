@@ -536,6 +536,11 @@ constexpr uint32_t kXcds = 8;
 struct TileWalk {
   uint32_t zl, tm, tn;
 };
+// Position in a workgroup's sequence of computed tiles only: matrix zl as above, tile row tm, and the q-th
+// tile with a visible entry in that row.
+struct LiveWalk {
+  uint32_t zl, tm, q;
+};
 
 template <bool TA, bool TB, int NC>
 __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
@@ -613,9 +618,50 @@ __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
         if (in_range(T, v)) (C + urow(v) * g.ldc + ucol(v))[loff_c] = 0;
     }
   }
-  // move to the next tile (of this workgroup's sequence, from X on) that has a visible entry
-  auto to_live = [&](TileWalk& W) {
-    while (!done(W) && (upper_dead(W) || band_dead(W))) advance(W);
+  // The computed tiles of tile row tm are the columns [row_lo(tm), row_lo(tm) + row_cnt(tm)): below the
+  // diagonal tile (tri_lower) and right of the window band.  The workgroups of an XCD group deal out the
+  // computed tiles of their matrices (not all tiles), so each gets the same number to within one.
+  auto row_lo = [&](uint32_t tm) -> uint32_t {
+    if (!g.tri_lower || g.kwin <= 0) return 0;
+    const int64_t bound = (int64_t)tm * BM - g.kwin - BN + 1;  // a column tile is computed iff tn * BN > bound
+    return bound < 0 ? 0u : (uint32_t)(bound / BN + 1);
+  };
+  auto row_cnt = [&](uint32_t tm) -> uint32_t {
+    uint32_t hi = tiles_n;  // one past the last computed column tile
+    if (g.tri_lower) {
+      const int64_t h = ((int64_t)tm * BM + BM - 1) / BN + 1;
+      if (h < (int64_t)hi) hi = (uint32_t)h;
+    }
+    const uint32_t lo = row_lo(tm);
+    return hi > lo ? hi - lo : 0u;
+  };
+  uint32_t live = per;  // computed tiles per matrix
+  if (g.tri_lower) {
+    live = 0;
+    for (uint32_t tm = 0; tm < tiles_m; ++tm) live += row_cnt(tm);
+  }
+  // move forward by n computed tiles (any n)
+  auto lmove = [&](LiveWalk& W, uint32_t n) {
+    W.zl += n / live;
+    W.q += n % live;
+    if (!g.tri_lower) {
+      W.tm += W.q / tiles_n;
+      W.q %= tiles_n;
+      W.zl += W.tm / tiles_m;
+      W.tm %= tiles_m;
+      return;
+    }
+    for (uint32_t c = row_cnt(W.tm); W.q >= c; c = row_cnt(W.tm)) {
+      W.q -= c;
+      if (++W.tm == tiles_m) { W.tm = 0; ++W.zl; }
+    }
+  };
+  auto ltile = [&](const LiveWalk& W) {
+    TileWalk T;
+    T.zl = W.zl;
+    T.tm = W.tm;
+    T.tn = row_lo(W.tm) + W.q;
+    return tile_of(T);
   };
   auto load = [&](const ShortTile& T, int c) -> Raw {
     if (g.vec && T.whole && (int64_t)(c + 1) * KC <= g.k)
@@ -623,10 +669,11 @@ __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
     return load_chunk<TA, TB, false>(g, T.A, T.B, T.row0, T.col0, (int64_t)c * KC, g.vec != 0);
   };
 
-  TileWalk cw = start();
-  to_live(cw);
-  if (done(cw)) return;
-  ShortTile cur = tile_of(cw);
+  if (live == 0) return;
+  LiveWalk cw = {0u, 0u, 0u};
+  lmove(cw, blockIdx.x / X);
+  if (cw.zl >= nzl) return;
+  ShortTile cur = ltile(cw);
   int buf = 0;
   store_chunk<TA, TB>(As[0], Bs[0], load(cur, 0));
   __syncthreads();
@@ -634,11 +681,10 @@ __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
   bool have_pre = false;
   constexpr int PC = NC >= 2 ? NC - 2 : 0;  // the chunk during which the dS operands are fetched
   for (;;) {
-    TileWalk nw = cw;
-    advance(nw);
-    to_live(nw);
-    const bool has_next = !done(nw);
-    const ShortTile nxt = has_next ? tile_of(nw) : cur;
+    LiveWalk nw = cw;
+    lmove(nw, G);
+    const bool has_next = nw.zl < nzl;
+    const ShortTile nxt = has_next ? ltile(nw) : cur;
     uint16_t pv[32];
     float dv[16];
     v32f r, p2;
