@@ -188,7 +188,6 @@ struct Scratch {
   uint16_t *dy_b, *dgu, *dO, *dS, *dqkv, *dOh;
   int8_t* qvt;  // R17: V codes, transposed per key block
   float* sv;    // R17: V block steps
-  float* gq;    // R19: the widened upstream gradient of a projection [T][N]
   void* qws;    // R19: workspace of the rotated int8 backward
   float* lsq_part;  // R19: block sums of the activation-step gradients
   float* dOf;   // R19: fp32 gradient of the attention output before its bf16 rounding
@@ -215,20 +214,18 @@ void carve_scratch(Carver& cv, const Dims& D, Scratch& s) {
   const int64_t nb = attn_pv_blocks(D.S);
   s.qvt = D.pv_int8 ? cv.take<int8_t>(D.B * D.Hkv * D.hd * nb * 64) : nullptr;
   s.sv = D.pv_int8 ? cv.take<float>(D.B * D.Hkv * nb) : nullptr;
-  s.gq = nullptr; s.qws = nullptr; s.lsq_part = nullptr; s.dOf = nullptr;
+  s.qws = nullptr; s.lsq_part = nullptr; s.dOf = nullptr;
   if (D.int8) {
     Proj pj[4];
     projections(D, pj);
-    int64_t nmax = 0, parts = 1;
+    int64_t parts = 1;
     size_t wsb = 0;
     for (int i = 0; i < 4; ++i) {
-      nmax = pj[i].N > nmax ? pj[i].N : nmax;
       const size_t b = qlinear_bwd_workspace_bytes(T, pj[i].N, pj[i].K);
       wsb = b > wsb ? b : wsb;
       const int64_t np = lsq_grad_parts(T * pj[i].K);
       parts = np > parts ? np : parts;
     }
-    s.gq = cv.take<float>(T * nmax);
     s.qws = cv.take<char>((int64_t)wsb);
     s.lsq_part = cv.take<float>(parts);
     s.dOf = cv.take<float>(T * d);
@@ -269,8 +266,7 @@ canon_status qproj_bwd(const Dims& D, int i, const uint16_t* G16, const uint16_t
   Proj pj[4];
   projections(D, pj);
   const int64_t N = pj[i].N, K = pj[i].K;
-  TRY(widen_bf16_launch(D.T * N, G16, sc.gq, s));
-  TRY(qlinear_bwd_launch(D.T, N, K, sc.gq, sv.qx[i], sv.sxf + i, sv.qw[i], sv.sw[i], dX, dW, sc.qws, s));
+  TRY(qlinear_bwd_launch(D.T, N, K, G16, 1, sv.qx[i], sv.sxf + i, sv.qw[i], sv.sw[i], dX, dW, sc.qws, s));
   TRY(lsq_grad_launch(D.T * K, X, sv.sxf + i, dX, lsq_gamma(K), sc.lsq_part, dsx, s));
   return CANON_OK;
 }
@@ -731,7 +727,7 @@ canon_status canon_qlinear_bwd(const canon_order* order, int64_t T, int64_t N, i
   if (!dy || !qx || !sx || !qw || !sw || !workspace) return CANON_EINVAL;
   if (workspace_bytes < qlinear_bwd_workspace_bytes(T, N, K)) return CANON_EWORKSPACE;
   if (((uintptr_t)dy & 15) || ((uintptr_t)workspace & 255)) return CANON_EINVAL;
-  return dev(qlinear_bwd_launch(T, N, K, dy, qx, sx, qw, sw, dx, dw, workspace, as_stream(stream)));
+  return dev(qlinear_bwd_launch(T, N, K, dy, 0, qx, sx, qw, sw, dx, dw, workspace, as_stream(stream)));
 }
 
 size_t canon_qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K) {

@@ -63,10 +63,11 @@ hipError_t hash_launch(int64_t n_tensors, const HashTensor* tens_dev, int64_t n_
                        const int64_t* wg_first, uint32_t* leaf_a, uint32_t* leaf_b, uint32_t* tensor_digests,
                        uint8_t* out, hipStream_t s);
 
-// qlinear.hip: int8 backward (rotated straight-through gradients)
+// qlinear.hip: int8 backward (rotated straight-through gradients); dy fp32, or bf16 when dy_bf16
 size_t qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K);
-hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const float* dy, const int8_t* qx, const float* sx,
-                              const int8_t* qw, const float* sw, float* dx, float* dw, void* ws, hipStream_t s);
+hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const void* dy, int dy_bf16, const int8_t* qx,
+                              const float* sx, const int8_t* qw, const float* sw, float* dx, float* dw, void* ws,
+                              hipStream_t s);
 int gemm_max_levels();
 
 // norm.hip: global gradient norm, clip coefficient, spike decision (R15)

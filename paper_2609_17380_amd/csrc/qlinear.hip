@@ -11,9 +11,11 @@ namespace canon {
 
 constexpr uint32_t kInv127Bits = 0x3C010204u;  // RN32(1/127)
 
-// dst [C][R] = transpose of src [R][C]; SRC_I8: src int8 codes dequantised as RN(step * q) with step
-// scale[r] (per_row) or scale[0]; otherwise src fp32 copied.  64 x 64 tiles through LDS.
-template <bool SRC_I8>
+enum { SRC_F32 = 0, SRC_I8 = 1, SRC_BF16 = 2 };
+
+// dst [C][R] = transpose of src [R][C]: SRC_I8 int8 codes dequantised as RN(step * q) with step scale[r]
+// (per_row) or scale[0]; SRC_F32 fp32 copied; SRC_BF16 bf16 widened (exact).  64 x 64 tiles through LDS.
+template <int SRC>
 __global__ __launch_bounds__(256) void transpose_kernel(int64_t R, int64_t C, const void* __restrict__ src,
                                                         const float* __restrict__ scale, int32_t per_row,
                                                         float* __restrict__ dst) {
@@ -24,9 +26,11 @@ __global__ __launch_bounds__(256) void transpose_kernel(int64_t R, int64_t C, co
     const int64_t r = r0 + i, c = c0 + tx;
     float v = 0.0f;
     if (r < R && c < C) {
-      if (SRC_I8) {
+      if (SRC == SRC_I8) {
         const float s = scale[per_row ? r : 0];
         v = s * (float)static_cast<const int8_t*>(src)[r * C + c];
+      } else if (SRC == SRC_BF16) {
+        v = bf16_to_f32(static_cast<const uint16_t*>(src)[r * C + c]);
       } else {
         v = static_cast<const float*>(src)[r * C + c];
       }
@@ -40,18 +44,29 @@ __global__ __launch_bounds__(256) void transpose_kernel(int64_t R, int64_t C, co
   }
 }
 
-// dst = blockwise rotation of src (n values, blocks of 256; in place allowed), and amax = max over the
-// bit patterns of |result| (an atomic max of non-negative patterns, which is order-free).  Each wavefront
-// rotates blocks in a grid-stride loop, lane l holding values 4l .. 4l+3: butterflies of strides 1 and 2
-// inside the lane, the others across lanes by xor shuffles.  One atomic per workgroup.
-__global__ __launch_bounds__(256) void fwht_kernel(int64_t n, const float* __restrict__ src, float* dst,
+// dst = blockwise rotation of src (n values, blocks of 256; in place allowed for fp32), and amax = max over
+// the bit patterns of |result| (an atomic max of non-negative patterns, which is order-free).  Each
+// wavefront rotates blocks in a grid-stride loop, lane l holding values 4l .. 4l+3: butterflies of strides 1
+// and 2 inside the lane, the others across lanes by xor shuffles.  One atomic per workgroup.  BF16: src holds
+// bf16 values (widened exactly on load).
+template <bool BF16>
+__global__ __launch_bounds__(256) void fwht_kernel(int64_t n, const void* src, float* dst,
                                                    uint32_t* __restrict__ amax) {
   __shared__ uint32_t wmax[4];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   uint32_t m = 0;
   for (int64_t blk = (int64_t)blockIdx.x * 4 + wv; blk * 256 < n; blk += (int64_t)gridDim.x * 4) {
-    const float4 x = reinterpret_cast<const float4*>(src + blk * 256)[lane];
-    float v[4] = {x.x, x.y, x.z, x.w};
+    float v[4];
+    if (BF16) {
+      const uint2 h = reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(src) + blk * 256)[lane];
+      v[0] = __uint_as_float(h.x << 16);
+      v[1] = __uint_as_float(h.x & 0xFFFF0000u);
+      v[2] = __uint_as_float(h.y << 16);
+      v[3] = __uint_as_float(h.y & 0xFFFF0000u);
+    } else {
+      const float4 x = reinterpret_cast<const float4*>(static_cast<const float*>(src) + blk * 256)[lane];
+      v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    }
     {  // stride 1: pairs (0,1), (2,3); stride 2: pairs (0,2), (1,3)
       float a = v[0], b = v[1];
       v[0] = a + b; v[1] = a - b;
@@ -103,19 +118,21 @@ __global__ void qlin_step_kernel(const uint32_t* __restrict__ amax, float* __res
   if ((int)threadIdx.x < n) step[threadIdx.x] = __uint_as_float(amax[threadIdx.x]) * __uint_as_float(kInv127Bits);
 }
 
-static hipError_t fwht_launch(int64_t n, const float* src, float* dst, uint32_t* amax, hipStream_t s) {
+static hipError_t fwht_launch(int64_t n, const void* src, int bf16, float* dst, uint32_t* amax, hipStream_t s) {
   const int64_t blocks = n / 256;
   if (blocks == 0) return hipSuccess;
   const int64_t wgs = (blocks + 3) / 4;
-  hipLaunchKernelGGL(fwht_kernel, dim3((unsigned)(wgs < 4096 ? wgs : 4096)), dim3(256), 0, s, n, src, dst, amax);
+  const dim3 grid((unsigned)(wgs < 4096 ? wgs : 4096));
+  if (bf16) hipLaunchKernelGGL(fwht_kernel<true>, grid, dim3(256), 0, s, n, src, dst, amax);
+  else hipLaunchKernelGGL(fwht_kernel<false>, grid, dim3(256), 0, s, n, src, dst, amax);
   return hipGetLastError();
 }
 
-template <bool SRC_I8>
+template <int SRC>
 static hipError_t transpose_launch(int64_t R, int64_t C, const void* src, const float* scale, int per_row,
                                    float* dst, hipStream_t s) {
   const dim3 grid((unsigned)((C + 63) / 64), (unsigned)((R + 63) / 64));
-  hipLaunchKernelGGL(transpose_kernel<SRC_I8>, grid, dim3(256), 0, s, R, C, src, scale, per_row, dst);
+  hipLaunchKernelGGL(transpose_kernel<SRC>, grid, dim3(256), 0, s, R, C, src, scale, per_row, dst);
   return hipGetLastError();
 }
 
@@ -132,8 +149,9 @@ size_t qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K) {
     if (e_ != hipSuccess) return e_;              \
   } while (0)
 
-hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const float* dy, const int8_t* qx, const float* sx,
-                              const int8_t* qw, const float* sw, float* dx, float* dw, void* ws, hipStream_t s) {
+hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const void* dy, int dy_bf16, const int8_t* qx,
+                              const float* sx, const int8_t* qw, const float* sw, float* dx, float* dw, void* ws,
+                              hipStream_t s) {
   auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
   const size_t big = (size_t)T * (size_t)N;
   const size_t small = (size_t)K * (size_t)(N > T ? N : T);
@@ -147,9 +165,9 @@ hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const float* dy, 
   hipLaunchKernelGGL(qlin_zero_kernel, dim3(1), dim3(64), 0, s, amax, 4);
   QTRY(hipGetLastError());
   if (dx) {  // contraction over N
-    QTRY(fwht_launch(T * N, dy, fa, amax + 0, s));                        // rot(dy) [T][N]
-    QTRY(transpose_launch<true>(N, K, qw, sw, 1, fb, s));                  // W^ transposed [K][N]
-    QTRY(fwht_launch(K * N, fb, fb, amax + 1, s));
+    QTRY(fwht_launch(T * N, dy, dy_bf16, fa, amax + 0, s));               // rot(dy) [T][N]
+    QTRY(transpose_launch<SRC_I8>(N, K, qw, sw, 1, fb, s));                // W^ transposed [K][N]
+    QTRY(fwht_launch(K * N, fb, 0, fb, amax + 1, s));
     hipLaunchKernelGGL(qlin_step_kernel, dim3(1), dim3(64), 0, s, amax, step, 2);
     QTRY(hipGetLastError());
     QTRY(quantize_launch(T, N, 0, fa, step + 0, 0, qa, s));
@@ -160,10 +178,11 @@ hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const float* dy, 
     QTRY(gemm_i8_launch(g, s));
   }
   if (dw) {  // contraction over T
-    QTRY(transpose_launch<false>(T, N, dy, nullptr, 0, fa, s));            // dy transposed [N][T]
-    QTRY(fwht_launch(N * T, fa, fa, amax + 2, s));
-    QTRY(transpose_launch<true>(T, K, qx, sx, 0, fb, s));                  // X^ transposed [K][T]
-    QTRY(fwht_launch(K * T, fb, fb, amax + 3, s));
+    if (dy_bf16) QTRY(transpose_launch<SRC_BF16>(T, N, dy, nullptr, 0, fa, s));  // dy transposed [N][T]
+    else QTRY(transpose_launch<SRC_F32>(T, N, dy, nullptr, 0, fa, s));
+    QTRY(fwht_launch(N * T, fa, 0, fa, amax + 2, s));
+    QTRY(transpose_launch<SRC_I8>(T, K, qx, sx, 0, fb, s));                // X^ transposed [K][T]
+    QTRY(fwht_launch(K * T, fb, 0, fb, amax + 3, s));
     hipLaunchKernelGGL(qlin_step_kernel, dim3(1), dim3(64), 0, s, amax + 2, step + 2, 2);
     QTRY(hipGetLastError());
     QTRY(quantize_launch(N, T, 0, fa, step + 2, 0, qa, s));
