@@ -126,13 +126,17 @@ __device__ __forceinline__ void wave_segment_chunks(int64_t seg0, int64_t n, Wav
   __builtin_amdgcn_wave_barrier();
 }
 
-// nz: terms at index >= nz are known to be +0 (masked); chunks made only of them have partial +0 and are not
+// nz: terms at index >= nz are known to be +0 (masked); z0: so are the terms below z0.  Chunks made only of
+// such terms have partial +0: those at or after nz, and those of whole staging segments below z0, are not
 // staged.
 template <int W, class Term>
-__device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* parts, Term term, int64_t nz) {
+__device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* parts, Term term, int64_t nz,
+                                               int64_t z0 = 0) {
   const int lane = threadIdx.x & 63;
   const int64_t nc = (n + kChunk - 1) / kChunk;
-  for (int64_t seg0 = 0; seg0 < n && seg0 < nz; seg0 += 64 * kChunk) wave_segment_chunks<W>(seg0, n, st, parts, term);
+  const int64_t zseg = (z0 / (64 * kChunk)) * (64 * kChunk);
+  for (int64_t c = lane; c < zseg / kChunk && c < nc; c += 64) parts[c] = 0.0f;
+  for (int64_t seg0 = zseg; seg0 < n && seg0 < nz; seg0 += 64 * kChunk) wave_segment_chunks<W>(seg0, n, st, parts, term);
   for (int64_t c = (nz + kChunk - 1) / kChunk + lane; c < nc; c += 64) parts[c] = 0.0f;
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
@@ -533,7 +537,9 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
   const int64_t j0 = (window > 0 && i - window + 1 > 0) ? i - window + 1 : 0;
   const float* rr = raw + row * cols;
   float m = -__builtin_inff();
-  for (int64_t j = (int64_t)lane * W; j <= i; j += 64 * W) {
+  // keys before the window are not read: whole wavefront strides below j0 are skipped, and the loads of
+  // vectors wholly below j0 are left out (their terms are +0 either way)
+  for (int64_t j = (j0 / (64 * W)) * (64 * W) + (int64_t)lane * W; j <= i; j += 64 * W) {
     float v[W];
     ldf<W>(rr + j, v);
 #pragma unroll
@@ -544,7 +550,7 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
   // masked keys enter the chain as +0 terms
   const float S = wave_row_rsum<W>(cols, st[w], dyn + w * nc, [&](int64_t j, float (&f)[W]) {
     float v[W];
-    ldf<W>(rr + j, v);
+    if (j + W - 1 >= j0) ldf<W>(rr + j, v);
 #pragma unroll
     for (int t = 0; t < W; ++t) {
       float e = 0.0f;
@@ -554,11 +560,11 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
       }
       f[t] = e;
     }
-  }, i + 1);
+  }, i + 1, j0);
   const float rcp = 1.0f / S;
   for (int64_t j = (int64_t)lane * W; j < cols; j += 64 * W) {
     uint16_t o[W];
-    if (j <= i) {
+    if (j <= i && j + W - 1 >= j0) {
       float v[W];
       ldf<W>(rr + j, v);
 #pragma unroll
@@ -593,7 +599,7 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
   for (int q = 0; q < kRegQ; ++q) {
     const int64_t j = 256 * q + 4 * lane;
     float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    if (j < cols && j <= i) v = *reinterpret_cast<const float4*>(rr + j);
+    if (j < cols && j <= i && j + 3 >= j0) v = *reinterpret_cast<const float4*>(rr + j);
     e[q][0] = v.x; e[q][1] = v.y; e[q][2] = v.z; e[q][3] = v.w;
   }
   float m = -__builtin_inff();
