@@ -27,6 +27,7 @@ PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s
 PEAK_INT8_MFMA = 5000.0  # TOP/s, MI355X dense int8 matrix
 PEAK_VALU_OPS = 39.3     # T lane-operations/s: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (fp32 or fp64 FMA issue rate)
+SHA_BLOCK_VALU = 1698    # VALU instructions of one SHA-256 compression in hash_leaves_kernel's block loop (gfx950 ISA)
 
 L, D, H, HD, F, V, S, MB = 16, 2048, 16, 128, 8192, 50304, 2048, 4
 PLAN = (1, 8, 1)
@@ -472,9 +473,15 @@ def main():
         hd = torch.empty(32, dtype=torch.uint8, device=dev)
         hms = _timed(torch, stream, lambda: C.state_hash(state, hd, hws, stream=stream), 3)
         hbytes = sum(t.numel() * t.element_size() for t in state)
-        kernels["state_hash_params_m_v"] = _hbm(hms, hbytes)
-        print(f"bench:   state_hash_params_m_v: {hms:.3f} ms, {kernels['state_hash_params_m_v']['achieved']} GB/s",
-              file=sys.stderr, flush=True)
+        # SHA-256 is bound by integer VALU issue, not by HBM: the leaf blocks' compressions at
+        # SHA_BLOCK_VALU instructions each (the tree and digest nodes, < 0.1% more, are not counted)
+        tops = hbytes / 64 * SHA_BLOCK_VALU / (hms * 1e-3) / 1e12
+        kernels["state_hash_params_m_v"] = {
+            "bound": "alu", "ms": round(hms, 4), "bytes": int(hbytes),
+            "gb_per_s": round(hbytes / (hms * 1e-3) / 1e9, 1), "achieved": round(tops, 2), "unit": "T lane-op/s",
+            "peak": PEAK_VALU_OPS, "frac": round(tops / PEAK_VALU_OPS, 4)}
+        print(f"bench:   state_hash_params_m_v: {hms:.3f} ms, {kernels['state_hash_params_m_v']['gb_per_s']} GB/s, "
+              f"{tops:.2f} T VALU op/s", file=sys.stderr, flush=True)
         del hws
 
     cpu = None
