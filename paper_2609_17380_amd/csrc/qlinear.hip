@@ -44,17 +44,27 @@ __global__ __launch_bounds__(256) void transpose_kernel(int64_t R, int64_t C, co
   }
 }
 
-// dst = blockwise rotation of src (n values, blocks of 256; in place allowed for fp32), and amax = max over
-// the bit patterns of |result| (an atomic max of non-negative patterns, which is order-free).  Each
-// wavefront rotates blocks in a grid-stride loop, lane l holding values 4l .. 4l+3: butterflies of strides 1
-// and 2 inside the lane, the others across lanes by xor shuffles.  One atomic per workgroup.  BF16: src holds
-// bf16 values (widened exactly on load).
-template <bool BF16>
-__global__ __launch_bounds__(256) void fwht_kernel(int64_t n, const void* src, float* dst,
-                                                   uint32_t* __restrict__ amax) {
+// Blockwise rotation of src (n values, blocks of 256).  Each wavefront rotates blocks in a grid-stride loop,
+// lane l holding values 4l .. 4l+3: butterflies of strides 1 and 2 inside the lane, the others across lanes
+// by xor shuffles.  BF16: src holds bf16 values (widened exactly on load).  FWHT_AMAX: amax = max over the
+// bit patterns of |result| (an atomic max of non-negative patterns, which is order-free; one atomic per
+// workgroup); FWHT_QUANT: the rotation quantised with the per-tensor step *step (the R13 quantiser) into q.
+// The rotated values are computed twice (once per pass) and never stored.
+enum { FWHT_AMAX = 1, FWHT_QUANT = 2 };
+template <bool BF16, int MODE>
+__global__ __launch_bounds__(256) void fwht_kernel(int64_t n, const void* src, int8_t* __restrict__ q,
+                                                   const float* __restrict__ step, uint32_t* __restrict__ amax) {
   __shared__ uint32_t wmax[4];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   uint32_t m = 0;
+  float sv = 0.0f, rs = 0.0f;
+  bool recip = false;
+  if (MODE == FWHT_QUANT) {
+    sv = step_daz(step[0]);
+    recip = recip_step_ok(sv);
+    rs = recip ? 1.0f / sv : 0.0f;
+  }
+  auto qz = [&](float v) -> uint32_t { return (uint8_t)(recip ? quant_recip(v, sv, rs) : quant1(v, sv)); };
   for (int64_t blk = (int64_t)blockIdx.x * 4 + wv; blk * 256 < n; blk += (int64_t)gridDim.x * 4) {
     float v[4];
     if (BF16) {
@@ -93,8 +103,10 @@ __global__ __launch_bounds__(256) void fwht_kernel(int64_t n, const void* src, f
       const uint32_t u = __float_as_uint(v[t]) & 0x7FFFFFFFu;
       m = u > m ? u : m;
     }
-    reinterpret_cast<float4*>(dst + blk * 256)[lane] = make_float4(v[0], v[1], v[2], v[3]);
+    if (MODE == FWHT_QUANT)
+      reinterpret_cast<uint32_t*>(q + blk * 256)[lane] = qz(v[0]) | (qz(v[1]) << 8) | (qz(v[2]) << 16) | (qz(v[3]) << 24);
   }
+  if (MODE == FWHT_QUANT) return;
 #pragma unroll
   for (int s = 32; s >= 1; s >>= 1) {
     const uint32_t o = __shfl_xor(m, s, 64);
@@ -118,14 +130,23 @@ __global__ void qlin_step_kernel(const uint32_t* __restrict__ amax, float* __res
   if ((int)threadIdx.x < n) step[threadIdx.x] = __uint_as_float(amax[threadIdx.x]) * __uint_as_float(kInv127Bits);
 }
 
-static hipError_t fwht_launch(int64_t n, const void* src, int bf16, float* dst, uint32_t* amax, hipStream_t s) {
+template <int MODE>
+static hipError_t fwht_launch(int64_t n, const void* src, int bf16, int8_t* q, const float* step, uint32_t* amax,
+                              hipStream_t s) {
   const int64_t blocks = n / 256;
   if (blocks == 0) return hipSuccess;
   const int64_t wgs = (blocks + 3) / 4;
   const dim3 grid((unsigned)(wgs < 4096 ? wgs : 4096));
-  if (bf16) hipLaunchKernelGGL(fwht_kernel<true>, grid, dim3(256), 0, s, n, src, dst, amax);
-  else hipLaunchKernelGGL(fwht_kernel<false>, grid, dim3(256), 0, s, n, src, dst, amax);
+  if (bf16) hipLaunchKernelGGL((fwht_kernel<true, MODE>), grid, dim3(256), 0, s, n, src, q, step, amax);
+  else hipLaunchKernelGGL((fwht_kernel<false, MODE>), grid, dim3(256), 0, s, n, src, q, step, amax);
   return hipGetLastError();
+}
+// amax of the rotation of src, then (after the step is formed) its codes: the rotated values are never stored
+static hipError_t fwht_amax(int64_t n, const void* src, int bf16, uint32_t* amax, hipStream_t s) {
+  return fwht_launch<FWHT_AMAX>(n, src, bf16, nullptr, nullptr, amax, s);
+}
+static hipError_t fwht_quant(int64_t n, const void* src, int bf16, const float* step, int8_t* q, hipStream_t s) {
+  return fwht_launch<FWHT_QUANT>(n, src, bf16, q, step, nullptr, s);
 }
 
 template <int SRC>
@@ -165,13 +186,13 @@ hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const void* dy, i
   hipLaunchKernelGGL(qlin_zero_kernel, dim3(1), dim3(64), 0, s, amax, 4);
   QTRY(hipGetLastError());
   if (dx) {  // contraction over N
-    QTRY(fwht_launch(T * N, dy, dy_bf16, fa, amax + 0, s));               // rot(dy) [T][N]
+    QTRY(fwht_amax(T * N, dy, dy_bf16, amax + 0, s));                      // rot(dy) [T][N]
     QTRY(transpose_launch<SRC_I8>(N, K, qw, sw, 1, fb, s));                // W^ transposed [K][N]
-    QTRY(fwht_launch(K * N, fb, 0, fb, amax + 1, s));
+    QTRY(fwht_amax(K * N, fb, 0, amax + 1, s));
     hipLaunchKernelGGL(qlin_step_kernel, dim3(1), dim3(64), 0, s, amax, step, 2);
     QTRY(hipGetLastError());
-    QTRY(quantize_launch(T, N, 0, fa, step + 0, 0, qa, s));
-    QTRY(quantize_launch(K, N, 0, fb, step + 1, 0, qb, s));
+    QTRY(fwht_quant(T * N, dy, dy_bf16, step + 0, qa, s));
+    QTRY(fwht_quant(K * N, fb, 0, step + 1, qb, s));
     GemmI8Args g{};
     g.a = qa; g.b = qb; g.y = dx; g.sa = step + 0; g.sb = step + 1; g.sb_scalar = 1;
     g.m = T; g.n = K; g.k = N; g.lda = N; g.ldb = N; g.ldc = K;
@@ -180,13 +201,13 @@ hipError_t qlinear_bwd_launch(int64_t T, int64_t N, int64_t K, const void* dy, i
   if (dw) {  // contraction over T
     if (dy_bf16) QTRY(transpose_launch<SRC_BF16>(T, N, dy, nullptr, 0, fa, s));  // dy transposed [N][T]
     else QTRY(transpose_launch<SRC_F32>(T, N, dy, nullptr, 0, fa, s));
-    QTRY(fwht_launch(N * T, fa, 0, fa, amax + 2, s));
+    QTRY(fwht_amax(N * T, fa, 0, amax + 2, s));
     QTRY(transpose_launch<SRC_I8>(T, K, qx, sx, 0, fb, s));                // X^ transposed [K][T]
-    QTRY(fwht_launch(K * T, fb, 0, fb, amax + 3, s));
+    QTRY(fwht_amax(K * T, fb, 0, amax + 3, s));
     hipLaunchKernelGGL(qlin_step_kernel, dim3(1), dim3(64), 0, s, amax + 2, step + 2, 2);
     QTRY(hipGetLastError());
-    QTRY(quantize_launch(N, T, 0, fa, step + 2, 0, qa, s));
-    QTRY(quantize_launch(K, T, 0, fb, step + 3, 0, qb, s));
+    QTRY(fwht_quant(N * T, fa, 0, step + 2, qa, s));
+    QTRY(fwht_quant(K * T, fb, 0, step + 3, qb, s));
     GemmI8Args g{};
     g.a = qa; g.b = qb; g.y = dw; g.sa = step + 2; g.sb = step + 3; g.sb_scalar = 1;
     g.m = N; g.n = K; g.k = T; g.lda = T; g.ldb = T; g.ldc = K;
