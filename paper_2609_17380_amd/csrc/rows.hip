@@ -7,6 +7,8 @@
 // workgroup with the pass-through rule, which together give Algorithm 2 over the row's chunks.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "canon_dev.h"
 #include "canon_internal.h"
 
@@ -883,10 +885,58 @@ hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, cons
 
 // ------------------------------------------------------------------------------------------------
 // D[bh][i] = R1 over d of fma(dO[i,d], O[i,d]) (bf16 operands, [T, ld] layout, head h at column h*hd).
+// A row takes a group of G lanes (G = the chunk count rounded up to a power of two): lane r of the group
+// runs the chain of chunk r over its 32 columns (16-byte loads when aligned, so the lanes of a group read the
+// row's consecutive 64-byte pieces), and the group's first lane folds the chunk partials with Algorithm 2.
+template <int G>
 __global__ __launch_bounds__(256) void attn_rowdot_kernel(int64_t B, int64_t H, int64_t S, int64_t hd,
                                                           const uint16_t* __restrict__ dO,
-                                                          const uint16_t* __restrict__ O, int64_t ld,
+                                                          const uint16_t* __restrict__ O, int64_t ld, int vec,
                                                           float* __restrict__ D) {
+  const int64_t tid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t row = tid / G;
+  const int r = (int)(tid % G);
+  const int lane = threadIdx.x & 63;
+  const bool live = row < B * H * S;
+  const int nch = (int)((hd + kChunk - 1) / kChunk);
+  float p = 0.0f;
+  if (live && r < nch) {
+    const int64_t i = row % S, bh = row / S, b = bh / H, h = bh % H;
+    const int64_t off = (b * S + i) * ld + h * hd + (int64_t)r * kChunk;
+    const uint16_t* a = dO + off;
+    const uint16_t* o = O + off;
+    const int64_t n = hd - (int64_t)r * kChunk < kChunk ? hd - (int64_t)r * kChunk : kChunk;
+    if (vec && n == kChunk) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint4 av = reinterpret_cast<const uint4*>(a)[q];
+        const uint4 ov = reinterpret_cast<const uint4*>(o)[q];
+        const uint32_t aw[4] = {av.x, av.y, av.z, av.w}, ow[4] = {ov.x, ov.y, ov.z, ov.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          p = __builtin_fmaf(__uint_as_float(aw[e] << 16), __uint_as_float(ow[e] << 16), p);
+          p = __builtin_fmaf(__uint_as_float(aw[e] & 0xFFFF0000u), __uint_as_float(ow[e] & 0xFFFF0000u), p);
+        }
+      }
+    } else {
+      for (int64_t k = 0; k < n; ++k) p = __builtin_fmaf(bf16_to_f32(a[k]), bf16_to_f32(o[k]), p);
+    }
+  }
+  float parts[G];
+#pragma unroll
+  for (int q = 0; q < G; ++q) parts[q] = __shfl(p, (lane & ~(G - 1)) + q, 64);
+  if (live && r == 0) {
+    LocalFold f;
+    for (int q = 0; q < nch; ++q) f.push(parts[q]);
+    D[row] = f.result();
+  }
+}
+
+// head dims above 16 chunks: one thread per row, chunks in order
+__global__ __launch_bounds__(256) void attn_rowdot_wide_kernel(int64_t B, int64_t H, int64_t S, int64_t hd,
+                                                               const uint16_t* __restrict__ dO,
+                                                               const uint16_t* __restrict__ O, int64_t ld,
+                                                               float* __restrict__ D) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= B * H * S) return;
   const int64_t i = idx % S, bh = idx / S, b = bh / H, h = bh % H;
@@ -894,10 +944,10 @@ __global__ __launch_bounds__(256) void attn_rowdot_kernel(int64_t B, int64_t H, 
   const uint16_t* o = O + (b * S + i) * ld + h * hd;
   LocalFold f;
   for (int64_t c0 = 0; c0 < hd; c0 += kChunk) {
-    float s = 0.0f;
+    float p = 0.0f;
     const int64_t c1 = c0 + kChunk < hd ? c0 + kChunk : hd;
-    for (int64_t k = c0; k < c1; ++k) s = __builtin_fmaf(bf16_to_f32(a[k]), bf16_to_f32(o[k]), s);
-    f.push(s);
+    for (int64_t k = c0; k < c1; ++k) p = __builtin_fmaf(bf16_to_f32(a[k]), bf16_to_f32(o[k]), p);
+    f.push(p);
   }
   D[idx] = f.result();
 }
@@ -906,8 +956,24 @@ hipError_t attn_rowdot_launch(int64_t B, int64_t H, int64_t S, int64_t hd, const
                               int64_t ld, float* D, hipStream_t s) {
   const int64_t n = B * H * S;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(attn_rowdot_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, B, H, S, hd, dO, O, ld,
-                     D);
+  const int64_t nch = (hd + kChunk - 1) / kChunk;
+  if (nch > 16) {
+    hipLaunchKernelGGL(attn_rowdot_wide_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, B, H, S, hd, dO,
+                       O, ld, D);
+    return hipGetLastError();
+  }
+  const int vec = ((uintptr_t)dO & 15) == 0 && ((uintptr_t)O & 15) == 0 && ld % 8 == 0 && hd % 8 == 0;
+  auto go = [&](auto gc) {
+    constexpr int G = decltype(gc)::value;
+    const int64_t threads = n * G;
+    hipLaunchKernelGGL(attn_rowdot_kernel<G>, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, B, H, S, hd,
+                       dO, O, ld, vec, D);
+  };
+  if (nch <= 1) go(std::integral_constant<int, 1>{});
+  else if (nch <= 2) go(std::integral_constant<int, 2>{});
+  else if (nch <= 4) go(std::integral_constant<int, 4>{});
+  else if (nch <= 8) go(std::integral_constant<int, 8>{});
+  else go(std::integral_constant<int, 16>{});
   return hipGetLastError();
 }
 

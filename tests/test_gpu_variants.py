@@ -81,7 +81,9 @@ def cfgs(L, d, H, F, V, S, mb, Hkv=0, qk=0, en=0, win=0, every=0, z=0.0):
                                                      (256, 4, 2, 0, 300, 256, 256, 1),
                                                      # more score tiles than resident workgroups (1024 and 2048)
                                                      (256, 2, 2, 0, 0, 256, 1024, 4), (512, 16, 4, 1, 200, 512, 1024, 1),
-                                                     (256, 2, 1, 1, 300, 256, 1000, 4)])
+                                                     (256, 2, 1, 1, 300, 256, 1000, 4),
+                                                     # head dim 48: a ragged second chunk in every per-row reduction
+                                                     (192, 4, 4, 0, 0, 256, 96, 2)])
 def test_block_variants_bit_exact(d, H, Hkv, qk, win, F, S, batch):
     print(f"block d={d} H={H} Hkv={Hkv} qk={qk} win={win} F={F} S={S} B={batch}", flush=True)
     hd = d // H
