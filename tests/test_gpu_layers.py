@@ -37,7 +37,10 @@ def test_rownorm_fwd_bwd(rows, cols):
     assert_bits(host_f32(dgn), dg_o, "dgain")
 
 
-@pytest.mark.parametrize("bh,s", [(3, 200), (2, 64), (4, 2048), (2, 70), (1, 33), (1, 2304)])
+# rows longer than 2048 keys take the staged kernel: 2052 (a lone last chunk), 3000 (a ragged last chunk),
+# 4096 (128 full chunks, two staging segments), 4100
+@pytest.mark.parametrize("bh,s", [(3, 200), (2, 64), (4, 2048), (2, 70), (1, 33), (1, 2304), (1, 2052), (2, 3000),
+                                  (1, 4096), (1, 4100)])
 def test_softmax_causal(bh, s):
     print(f"softmax {bh}x{s}x{s}", flush=True)
     raw = I.normal_f32((bh, s, s), 0, I.TENSOR_IDS["scores"]) * np.float32(8)
