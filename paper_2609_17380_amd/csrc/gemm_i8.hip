@@ -7,10 +7,11 @@
 // reordered and spread over matrix instructions freely.  The dequantised output is
 // y[i][j] = RN(RN(RN32(acc) * sa) * sb[j]).
 //
-// Tiling: a workgroup of 4 wavefronts owns a 128 x 64 WN output tile, each wavefront a 64 x 32 WN block made
-// of 2 x WN v_mfma_i32_32x32x32_i8 blocks (WN = 2: 128 x 128 tiles, measured best at the 1B shapes).  Stages
-// of KS = 128 k bytes are staged through LDS (rows padded by 16 bytes, which keeps the 16-byte operand reads
-// of 32 consecutive rows free of bank conflicts), double buffered.
+// Tiling: a workgroup of NW wavefronts owns a 32 NW x 64 WN output tile, each wavefront a 64 x 32 WN block made
+// of 2 x WN v_mfma_i32_32x32x32_i8 blocks: 256 x 256 tiles of 8 wavefronts with 64-byte stages for large
+// products, else 128 x 128 tiles of 4 wavefronts with 128-byte stages.  Stages of KS k bytes are staged
+// through LDS (rows padded by 16 bytes, which keeps the 16-byte operand reads of 32 consecutive rows free of
+// bank conflicts), double buffered.
 // Each lane of a 32x32x32 instruction supplies 16 consecutive k bytes of one row of A and of B; the two
 // half-wavefronts cover k 0..15 and 16..31 of the instruction's 32.
 #include <hip/hip_runtime.h>
@@ -22,19 +23,22 @@ namespace canon {
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int QBM = 128;
-
-template <int WN, int KS>
+// Workgroup configuration: NW wavefronts in (NW / 2) x 2, wavefront (wr, wc) owning rows [64 wr, 64 wr + 64)
+// and columns [32 WN wc, 32 WN (wc + 1)) of a BM x (64 WN) tile; stages of KS k bytes.
+template <int BM_, int WN, int KS, int NW>
 struct I8Cfg {
+  static constexpr int BM = BM_;
+  static constexpr int NT = 64 * NW;          // threads
   static constexpr int BN = 64 * WN;          // workgroup tile columns
   static constexpr int LD = KS + 16;          // padded LDS row (bytes)
-  static constexpr int AV = QBM * KS / 16 / 256;  // 16-byte vectors of A per thread per stage
-  static constexpr int BV = BN * KS / 16 / 256;   // ... of B
+  static constexpr int AV = BM * KS / 16 / NT;  // 16-byte vectors of A per thread per stage
+  static constexpr int BV = BN * KS / 16 / NT;  // ... of B
+  static_assert(BM == 32 * NW, "wavefront rows");
 };
 
-template <int WN, int KS>
+template <class Cf>
 struct I8Raw {
-  uint4 a[I8Cfg<WN, KS>::AV], b[I8Cfg<WN, KS>::BV];
+  uint4 a[Cf::AV], b[Cf::BV];
 };
 
 // 16 consecutive bytes of which the first `valid` exist (zero fill beyond)
@@ -47,57 +51,55 @@ __device__ __forceinline__ uint4 ld16(const int8_t* p, int64_t valid, bool vec) 
   return make_uint4(w[0], w[1], w[2], w[3]);
 }
 
-// Global -> registers for the stage starting at k0: vector idx = t + 256 it covers row idx / (KS/16),
+// Global -> registers for the stage starting at k0: vector idx = t + NT it covers row idx / (KS/16),
 // 16-byte segment idx % (KS/16) of the row's KS bytes.
-template <int WN, int KS, bool FAST>
-__device__ __forceinline__ I8Raw<WN, KS> load_stage(const GemmI8Args& g, int64_t row0, int64_t col0, int64_t k0) {
-  using Cf = I8Cfg<WN, KS>;
+template <class Cf, int KS, bool FAST>
+__device__ __forceinline__ I8Raw<Cf> load_stage(const GemmI8Args& g, int64_t row0, int64_t col0, int64_t k0) {
   constexpr int SEG = KS / 16;
   const int t = threadIdx.x;
-  I8Raw<WN, KS> r;
+  I8Raw<Cf> r;
 #pragma unroll
   for (int it = 0; it < Cf::AV; ++it) {
-    const int idx = t + 256 * it;
+    const int idx = t + Cf::NT * it;
     const int64_t k = k0 + 16 * (idx % SEG), row = row0 + idx / SEG;
     r.a[it] = ld16<FAST>(g.a + row * g.lda + k, (row < g.m) ? g.k - k : 0, g.vec);
   }
 #pragma unroll
   for (int it = 0; it < Cf::BV; ++it) {
-    const int idx = t + 256 * it;
+    const int idx = t + Cf::NT * it;
     const int64_t k = k0 + 16 * (idx % SEG), col = col0 + idx / SEG;
     r.b[it] = ld16<FAST>(g.b + col * g.ldb + k, (col < g.n) ? g.k - k : 0, g.vec);
   }
   return r;
 }
 
-template <int WN, int KS>
-__device__ __forceinline__ void store_stage(int8_t* As, int8_t* Bs, const I8Raw<WN, KS>& r) {
-  using Cf = I8Cfg<WN, KS>;
+template <class Cf, int KS>
+__device__ __forceinline__ void store_stage(int8_t* As, int8_t* Bs, const I8Raw<Cf>& r) {
   constexpr int SEG = KS / 16;
   const int t = threadIdx.x;
 #pragma unroll
   for (int it = 0; it < Cf::AV; ++it) {
-    const int idx = t + 256 * it;
+    const int idx = t + Cf::NT * it;
     *reinterpret_cast<uint4*>(As + (idx / SEG) * Cf::LD + 16 * (idx % SEG)) = r.a[it];
   }
 #pragma unroll
   for (int it = 0; it < Cf::BV; ++it) {
-    const int idx = t + 256 * it;
+    const int idx = t + Cf::NT * it;
     *reinterpret_cast<uint4*>(Bs + (idx / SEG) * Cf::LD + 16 * (idx % SEG)) = r.b[it];
   }
 }
 
-template <int WN, int KS>
-__global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
-  using Cf = I8Cfg<WN, KS>;
-  constexpr int BN = Cf::BN, LD = Cf::LD;
-  __shared__ __attribute__((aligned(16))) int8_t As[2][QBM * LD];
+template <int BM_, int WN, int KS, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_i8_kernel(GemmI8Args g) {
+  using Cf = I8Cfg<BM_, WN, KS, NW>;
+  constexpr int BM = Cf::BM, BN = Cf::BN, LD = Cf::LD;
+  __shared__ __attribute__((aligned(16))) int8_t As[2][BM * LD];
   __shared__ __attribute__((aligned(16))) int8_t Bs[2][BN * LD];
 
   // tile order: a contiguous run of tiles per XCD, walked in groups of 8 tile rows
   constexpr int64_t GM = 8;
   const int64_t tiles_n = (g.n + BN - 1) / BN;
-  const int64_t tiles_m = (g.m + QBM - 1) / QBM;
+  const int64_t tiles_m = (g.m + BM - 1) / BM;
   const int64_t tiles = tiles_m * tiles_n;
   int64_t tile = blockIdx.x;
   if ((tiles & 7) == 0) tile = (blockIdx.x & 7) * (tiles >> 3) + (blockIdx.x >> 3);
@@ -105,8 +107,8 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
   const int64_t first_m = group * GM;
   const int64_t gsize = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
   const int64_t within = tile - group * GM * tiles_n;
-  const int64_t row0 = (first_m + within % gsize) * QBM, col0 = (within / gsize) * BN;
-  const bool tile_in = g.vec && row0 + QBM <= g.m && col0 + BN <= g.n;
+  const int64_t row0 = (first_m + within % gsize) * BM, col0 = (within / gsize) * BN;
+  const bool tile_in = g.vec && row0 + BM <= g.m && col0 + BN <= g.n;
 
   // wavefront (wr, wc) owns rows [64 wr, 64 wr + 64) and columns [32 WN wc, 32 WN (wc + 1)) of the tile
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -124,14 +126,14 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
 
   const int64_t ns = (g.k + KS - 1) / KS;
   int buf = 0;
-  if (ns > 0) store_stage<WN, KS>(As[0], Bs[0], load_stage<WN, KS, false>(g, row0, col0, 0));
+  if (ns > 0) store_stage<Cf, KS>(As[0], Bs[0], load_stage<Cf, KS, false>(g, row0, col0, 0));
   __syncthreads();
   for (int64_t s = 0; s < ns; ++s) {
     const bool more = s + 1 < ns;
-    I8Raw<WN, KS> nxt;
+    I8Raw<Cf> nxt;
     if (more) {
-      if (tile_in && (s + 2) * KS <= g.k) nxt = load_stage<WN, KS, true>(g, row0, col0, (s + 1) * KS);
-      else nxt = load_stage<WN, KS, false>(g, row0, col0, (s + 1) * KS);
+      if (tile_in && (s + 2) * KS <= g.k) nxt = load_stage<Cf, KS, true>(g, row0, col0, (s + 1) * KS);
+      else nxt = load_stage<Cf, KS, false>(g, row0, col0, (s + 1) * KS);
     }
     __builtin_amdgcn_sched_barrier(0);
     const int8_t* as = As[buf];
@@ -151,7 +153,7 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
           acc[h][v2] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[h], b[v2], acc[h][v2], 0, 0, 0);
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (more) store_stage<WN, KS>(As[buf ^ 1], Bs[buf ^ 1], nxt);
+    if (more) store_stage<Cf, KS>(As[buf ^ 1], Bs[buf ^ 1], nxt);
     __syncthreads();
     buf ^= 1;
   }
@@ -178,16 +180,31 @@ __global__ __launch_bounds__(256) void gemm_i8_kernel(GemmI8Args g) {
       }
 }
 
-constexpr int I8_WN = 2, I8_KS = 128;
+template <int BM, int WN, int KS, int NW>
+static hipError_t launch_i8(const GemmI8Args& g, hipStream_t s) {
+  using Cf = I8Cfg<BM, WN, KS, NW>;
+  const int64_t tiles = ((g.m + BM - 1) / BM) * ((g.n + Cf::BN - 1) / Cf::BN);
+  hipLaunchKernelGGL((gemm_i8_kernel<BM, WN, KS, NW>), dim3((unsigned)tiles), dim3(Cf::NT), 0, s, g);
+  return hipGetLastError();
+}
 
 hipError_t gemm_i8_launch(const GemmI8Args& gin, hipStream_t s) {
   if (gin.m == 0 || gin.n == 0) return hipSuccess;
   GemmI8Args g = gin;
   g.vec = ((uintptr_t)g.a & 15) == 0 && ((uintptr_t)g.b & 15) == 0 && g.lda % 16 == 0 && g.ldb % 16 == 0;
-  constexpr int BN = I8Cfg<I8_WN, I8_KS>::BN;
-  const int64_t tiles = ((g.m + QBM - 1) / QBM) * ((g.n + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_i8_kernel<I8_WN, I8_KS>), dim3((unsigned)tiles), dim3(256), 0, s, g);
-  return hipGetLastError();
+  // 256 x 256 tiles of 8 wavefronts (one workgroup per CU, 64-byte stages) halve the operand bytes staged per
+  // multiply-add and run a tile's work about 1.12x faster than four 128 x 128 tiles of 4 wavefronts (two
+  // workgroups per CU); they are taken unless their coarser rounds of workgroups over the CUs cost more
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                                              hipSuccess || cus <= 0)
+    cus = 256;
+  const int64_t small_tiles = ((g.m + 127) / 128) * ((g.n + 127) / 128);
+  const int64_t big_tiles = ((g.m + 255) / 256) * ((g.n + 255) / 256);
+  const double small_time = (double)((small_tiles + 2 * cus - 1) / (2 * cus));        // rounds of one tile time
+  const double big_time = (double)((big_tiles + cus - 1) / cus) * (2.0 / 1.12);
+  if (big_time < small_time) return launch_i8<256, 4, 64, 8>(g, s);
+  return launch_i8<128, 2, 128, 4>(g, s);
 }
 
 }  // namespace canon

@@ -123,6 +123,28 @@ def test_quantised_linear_1b_shapes_sampled():
     assert_bits(host_f32(y)[rows], y_o, "y rows")
 
 
+@pytest.mark.parametrize("m,n,k", [(8000, 8100, 320), (4352, 16200, 96)])
+def test_gemm_i8_large_ragged_tiles_sampled(m, n, k):
+    """Products large enough for the 256 x 256 tiles, with ragged last tile rows, columns and stages: the
+    int32 accumulators and the dequantised outputs of sampled rows (the first and last tile rows among them)
+    against the oracle."""
+    print(f"gemm_i8 {m}x{n}x{k}", flush=True)
+    rng = np.random.default_rng(m + n + k)
+    a = rng.integers(-128, 128, (m, k)).astype(np.int8)
+    b = rng.integers(-128, 128, (n, k)).astype(np.int8)
+    sa = np.array([0.013], np.float32)
+    sb = (np.abs(rng.standard_normal(n)) * 0.01 + 1e-3).astype(np.float32)
+    acc = torch.empty((m, n), dtype=torch.int32, device=DEV)
+    y = torch.empty((m, n), dtype=torch.float32, device=DEV)
+    C.gemm_i8(m, n, k, torch.from_numpy(a).to(DEV), k, torch.from_numpy(b).to(DEV), k, acc=acc, y=y,
+              sa=dev_f32(sa), sb=dev_f32(sb))
+    torch.cuda.synchronize()
+    rows = np.concatenate([np.arange(0, 8), np.arange(m - 8, m), rng.choice(m, 48, replace=False)])
+    acc_o, y_o = oracle.gemm_i8(a[rows], b, sa[0], sb)
+    assert np.array_equal(acc.cpu().numpy()[rows], acc_o)
+    assert_bits(host_f32(y)[rows], y_o, "y rows")
+
+
 def qlinear_bwd_case(T, N, K, seed, want_dx=True, want_dw=True, outlier=True):
     rng = np.random.default_rng(seed)
     dy = (rng.standard_normal((T, N)) * 1e-3).astype(np.float32)
