@@ -707,6 +707,32 @@ __global__ void quantize_tensor_bf16x8_kernel(int64_t n, const uint16_t* __restr
   if (t < n) q[t] = (int8_t)qz(bf16_to_f32(x[t]));
 }
 
+// one step per row, bf16 input with 16-byte aligned rows (cols a multiple of 8) and 8-byte aligned q: a
+// workgroup per row (grid-stride over rows), 8 values per thread per pass over the row
+__global__ __launch_bounds__(256) void quantize_rows_bf16x8_kernel(int64_t rows, int64_t cols,
+                                                                   const uint16_t* __restrict__ x,
+                                                                   const float* __restrict__ scale,
+                                                                   int8_t* __restrict__ q) {
+  const int64_t g8 = cols >> 3;
+  for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+    const float sv = step_daz(scale[r]);
+    const uint4* xr = reinterpret_cast<const uint4*>(x + r * cols);
+    uint2* qr = reinterpret_cast<uint2*>(q + r * cols);
+    for (int64_t i = threadIdx.x; i < g8; i += 256) {
+      const uint4 h = xr[i];
+      const uint32_t w[4] = {h.x, h.y, h.z, h.w};
+      uint32_t o[2];
+#pragma unroll
+      for (int k = 0; k < 2; ++k)
+        o[k] = (uint32_t)(uint8_t)quant1(__uint_as_float(w[2 * k] << 16), sv) |
+               ((uint32_t)(uint8_t)quant1(__uint_as_float(w[2 * k] & 0xFFFF0000u), sv) << 8) |
+               ((uint32_t)(uint8_t)quant1(__uint_as_float(w[2 * k + 1] << 16), sv) << 16) |
+               ((uint32_t)(uint8_t)quant1(__uint_as_float(w[2 * k + 1] & 0xFFFF0000u), sv) << 24);
+      qr[i] = make_uint2(o[0], o[1]);
+    }
+  }
+}
+
 hipError_t quantize_launch(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale,
                            int32_t per_row, int8_t* q, hipStream_t s) {
   const int64_t n = rows * cols;
@@ -716,6 +742,12 @@ hipError_t quantize_launch(int64_t rows, int64_t cols, int32_t dtype, const void
     if (b < 1) b = 1;
     const unsigned grid = (unsigned)(b < (1 << 20) ? b : (1 << 20));
     hipLaunchKernelGGL(quantize_tensor4_kernel, dim3(grid), dim3(256), 0, s, n, (const float*)x, scale, q);
+    return hipGetLastError();
+  }
+  if (dtype == 1 && per_row && cols % 8 == 0 && ((uintptr_t)x & 15) == 0 && ((uintptr_t)q & 7) == 0) {
+    const unsigned grid = (unsigned)(rows < 8192 ? rows : 8192);
+    hipLaunchKernelGGL(quantize_rows_bf16x8_kernel, dim3(grid), dim3(256), 0, s, rows, cols, (const uint16_t*)x, scale,
+                       q);
     return hipGetLastError();
   }
   if (dtype == 1 && !per_row && ((uintptr_t)x & 15) == 0 && ((uintptr_t)q & 7) == 0) {

@@ -42,8 +42,9 @@ def special_values(shape):
 
 @pytest.mark.parametrize("per_row", [True, False])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_quantize(per_row, dtype):
-    rows, cols = 37, 301
+@pytest.mark.parametrize("cols", [301, 304])  # 304: whole 16-byte vectors per row (the vector kernels)
+def test_quantize(per_row, dtype, cols):
+    rows = 37
     x = special_values((rows, cols))
     s = (np.abs(RNG.standard_normal(rows)) * 0.1 + 0.01).astype(np.float32)
     s[1], s[2], s[3], s[4] = 0.0, -1.0, np.nan, 1e-40  # steps that quantise to 0
