@@ -83,7 +83,9 @@ def cfgs(L, d, H, F, V, S, mb, Hkv=0, qk=0, en=0, win=0, every=0, z=0.0):
                                                      (256, 2, 2, 0, 0, 256, 1024, 4), (512, 16, 4, 1, 200, 512, 1024, 1),
                                                      (256, 2, 1, 1, 300, 256, 1000, 4),
                                                      # head dim 48: a ragged second chunk in every per-row reduction
-                                                     (192, 4, 4, 0, 0, 256, 96, 2)])
+                                                     (192, 4, 4, 0, 0, 256, 96, 2),
+                                                     # head dim 544: 17 chunks per attention row dot (the wide path)
+                                                     (544, 1, 1, 0, 0, 256, 64, 1)])
 def test_block_variants_bit_exact(d, H, Hkv, qk, win, F, S, batch):
     print(f"block d={d} H={H} Hkv={Hkv} qk={qk} win={win} F={F} S={S} B={batch}", flush=True)
     hd = d // H
