@@ -510,12 +510,43 @@ __global__ __launch_bounds__(256) void quant_scales_kernel(int64_t rows, int64_t
   if (lane == 0) scale[row] = two * __uint_as_float(kInvSqrtQmaxBits);
 }
 
+// The same for rows held in registers (cols <= 2048, a multiple of 4, 8-byte aligned rows): one read of the row
+__global__ __launch_bounds__(256) void quant_scales_reg_kernel(int64_t rows, int64_t cols,
+                                                               const uint16_t* __restrict__ w, float inv_k,
+                                                               float* __restrict__ scale) {
+  __shared__ WaveStage st[4];
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + wv;
+  if (row >= rows) return;
+  const uint16_t* wr = w + row * cols;
+  float e[kRegQ][4];
+#pragma unroll
+  for (int q = 0; q < kRegQ; ++q) {
+    const int64_t j = 256 * q + 4 * lane;
+    if (j < cols) {
+      float f[4];
+      ldb<4>(wr + j, f);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) e[q][t] = __builtin_fabsf(f[t]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) e[q][t] = 0.0f;
+    }
+  }
+  const float a = reg_row_sum(st[wv], e, cols);
+  const float mean = a * inv_k;
+  const float two = 2.0f * mean;
+  if (lane == 0) scale[row] = two * __uint_as_float(kInvSqrtQmaxBits);
+}
+
 hipError_t quant_scales_launch(int64_t rows, int64_t cols, const uint16_t* w, float* scale, hipStream_t s) {
   if (rows == 0) return hipSuccess;
   const float inv_k = (float)(1.0 / (double)cols);  // RN32(1/cols)
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
-  if (cols % 4 == 0 && al(w, 8))
+  if (cols % 4 == 0 && cols <= kRegCols && al(w, 8))
+    hipLaunchKernelGGL(quant_scales_reg_kernel, grid, dim3(256), 0, s, rows, cols, w, inv_k, scale);
+  else if (cols % 4 == 0 && al(w, 8))
     hipLaunchKernelGGL(quant_scales_kernel<4>, grid, dim3(256), lds, s, rows, cols, w, inv_k, scale);
   else
     hipLaunchKernelGGL(quant_scales_kernel<1>, grid, dim3(256), lds, s, rows, cols, w, inv_k, scale);

@@ -19,7 +19,7 @@ def dev_i8(a):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.int8)).to(DEV)
 
 
-@pytest.mark.parametrize("rows,cols", [(5, 2048), (130, 97), (3, 1), (64, 8192), (2, 32768)])
+@pytest.mark.parametrize("rows,cols", [(5, 2048), (130, 97), (3, 1), (64, 8192), (2, 32768), (7, 1000), (9, 36)])
 def test_quant_scales(rows, cols):
     print(f"quant_scales {rows}x{cols}", flush=True)
     w = I.normal_bf16((rows, cols), 0, I.TENSOR_IDS["gemm_b"], std=0.02)
