@@ -26,7 +26,9 @@ CFLAGS = ["-O2", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off", "-fno-fast
 
 
 def build() -> str:
-    subprocess.run(["gcc", *CFLAGS, "-o", _LIB, _SRC, "-lm"], check=True)
+    tmp = _LIB + ".tmp"
+    subprocess.run(["gcc", *CFLAGS, "-o", tmp, _SRC, "-lm"], check=True)
+    os.replace(tmp, _LIB)  # a process that has the old library loaded keeps its copy
     return _LIB
 
 
@@ -95,7 +97,11 @@ def _load():
             "cref_fx_product": (ctypes.c_uint64, [ctypes.c_uint16, ctypes.c_uint16, i32]),
             "cref_fx_to_f32": (f, [ctypes.c_uint64, i32]),
             "cref_lsq_step_grad": (f, [i64, i64, vp, f, vp]),
+            "cref_embed_bwd": (ctypes.c_int, [i64, i64, i64, vp, vp, vp]),
+            "cref_inv_sqrt_int": (f, [i64]),
+            "cref_swiglu": (ctypes.c_int, [i64, vp, vp, vp, vp, vp, vp]),
             "cref_num_threads": (ctypes.c_int, []),
+            "cref_set_threads": (None, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(lib, name)
@@ -410,6 +416,37 @@ def lsq_step_grad(x: np.ndarray, s, dx: np.ndarray) -> np.float32:
     dx = np.ascontiguousarray(dx, dtype=np.float32)
     T, K = x.shape
     return np.float32(_load().cref_lsq_step_grad(T, K, _p(x), np.float32(s), _p(dx)))
+
+
+def embed_bwd(tokens: np.ndarray, dx: np.ndarray, vocab: int) -> np.ndarray:
+    """R11: dE [vocab, d] from dx [T, d] (fp32) and the int32 tokens [T] of the microbatch."""
+    tokens = np.ascontiguousarray(tokens, dtype=np.int32).reshape(-1)
+    dx = np.ascontiguousarray(dx, dtype=np.float32)
+    T, d = dx.shape
+    assert tokens.size == T
+    dE = np.empty((vocab, d), dtype=np.float32)
+    _check(_load().cref_embed_bwd(T, vocab, d, _p(tokens), _p(dx), _p(dE)))
+    return dE
+
+
+def swiglu(g: np.ndarray, u: np.ndarray, da: np.ndarray):
+    """SwiGLU per element: (a, dg, du) as bf16 bit patterns (uint16) from fp32 g, u and da."""
+    g = np.ascontiguousarray(g, dtype=np.float32).reshape(-1)
+    u = np.ascontiguousarray(u, dtype=np.float32).reshape(-1)
+    da = np.ascontiguousarray(da, dtype=np.float32).reshape(-1)
+    a, dg, du = (np.empty(g.size, np.uint16) for _ in range(3))
+    _check(_load().cref_swiglu(g.size, _p(g), _p(u), _p(da), _p(a), _p(dg), _p(du)))
+    return a, dg, du
+
+
+def inv_sqrt_int(n: int) -> np.float32:
+    """RN32(1/sqrt(n)) for an integer n >= 1, as the oracle evaluates the attention and LSQ scales."""
+    return np.float32(_load().cref_inv_sqrt_int(int(n)))
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (independent outputs only; the arithmetic is the same)."""
+    _load().cref_set_threads(int(n))
 
 
 def num_threads() -> int:

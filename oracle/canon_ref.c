@@ -26,6 +26,7 @@
 #include "canon_ref.h"
 
 #include <math.h>
+#include <stdio.h>
 #include <omp.h>
 #include <stdlib.h>
 #include <string.h>
@@ -783,9 +784,63 @@ static void block_saved_free(block_saved* s) {
 
 static const uint32_t ATTN_SCALE_128 = 0x3DB504F3u; /* RN32(1/sqrt(128)) */
 
+/* Sign of (P 2^Q - 1/sqrt(n)) for an odd P < 2^27 and 1 <= n < 2^60: the sign of P^2 n - 2^(-2Q), exact in
+   128-bit integers (every boundary used below has Q <= -24 and -2Q < 120). */
+static int cmp_inv_sqrt(uint64_t P, int Q, uint64_t n) {
+  unsigned __int128 lhs = (unsigned __int128)P * P * n;
+  unsigned __int128 rhs = (unsigned __int128)1 << (-2 * Q);
+  return lhs < rhs ? -1 : (lhs > rhs ? 1 : 0);
+}
+
+/* RN32(1/sqrt(n)) for an integer 1 <= n < 2^60, decided exactly.  A binary64 estimate gives a candidate y;
+   y is the correctly rounded value iff 1/sqrt(n) lies strictly between the midpoints to its neighbours
+   (1/sqrt(n) is never a midpoint: that would make n the square of a power of two over an odd square).
+   Used for the attention scale RN32(1/sqrt(head_dim)) and LSQ's gradient scale RN32(1/sqrt(127 K)). */
+float cref_inv_sqrt_int(int64_t n) {
+  if (n < 1 || n >= ((int64_t)1 << 60)) return NAN;
+  float y = (float)(1.0 / sqrt((double)n));
+  for (int it = 0; it < 8; ++it) {
+    int e;
+    const float fr = frexpf(y, &e); /* y = fr 2^e, fr in [1/2, 1) */
+    const uint64_t m = (uint64_t)ldexpf(fr, 24);
+    e -= 24; /* y = m 2^e with 2^23 <= m < 2^24 */
+    if (cmp_inv_sqrt(2 * m + 1, e - 1, (uint64_t)n) < 0) { y = nextafterf(y, INFINITY); continue; }
+    const int pow2 = (m == ((uint64_t)1 << 23));
+    if (cmp_inv_sqrt(pow2 ? 4 * m - 1 : 2 * m - 1, pow2 ? e - 2 : e - 1, (uint64_t)n) > 0) {
+      y = nextafterf(y, 0.0f);
+      continue;
+    }
+    return y;
+  }
+  return NAN; /* not reached: the binary64 estimate is within one unit of the answer */
+}
+
 static float attn_scale(int64_t hd) {
   if (hd == 128) return f_from_bits(ATTN_SCALE_128);
-  return (float)(1.0 / sqrt((double)hd)); /* RN32(1/sqrt(hd)) for other head sizes used in tests */
+  return cref_inv_sqrt_int(hd);
+}
+
+/* SwiGLU forward of one element: a = bf16(RN(silu(g) u)) */
+static uint16_t swiglu_fwd1(float g, float u) { return cref_bf16(cref_mul(cref_silu(g), u)); }
+
+/* SwiGLU backward of one element from the fp32 gradient da of a: du = RN(da silu(g)) and
+   dg = RN(RN(da u) dsg) with dsg = RN(sig RN(1 + RN(g RN(1 - sig)))), sig = sigmoid(g); both to bf16 */
+static void swiglu_bwd1(float g, float u, float da, uint16_t* dg, uint16_t* du) {
+  const float sig = cref_sigmoid(g);
+  const float silu = cref_mul(g, sig);
+  const float dsg = cref_mul(sig, cref_add(1.0f, cref_mul(g, cref_sub(1.0f, sig))));
+  *du = cref_bf16(cref_mul(da, silu));
+  *dg = cref_bf16(cref_mul(cref_mul(da, u), dsg));
+}
+
+int cref_swiglu(int64_t n, const float* g, const float* u, const float* da, uint16_t* a, uint16_t* dg,
+                uint16_t* du) {
+  if (n < 0 || (n > 0 && (!g || !u))) return -1;
+  for (int64_t i = 0; i < n; ++i) {
+    if (a) a[i] = swiglu_fwd1(g[i], u[i]);
+    if (da && dg && du) swiglu_bwd1(g[i], u[i], da[i], &dg[i], &du[i]);
+  }
+  return 0;
 }
 
 /* R16 gain-free QK-norm of one head row (the architecture section: RMSNorm per head before RoPE, no
@@ -893,8 +948,7 @@ static void block_fwd(block_saved* s, const float* x, const uint16_t* const* w, 
   if (s->int8) qlin_fwd(s, 2, T, 2 * F, d, s->hn, w[4], s->gu);
   else cref_gemm(0, 1, T, 2 * F, d, s->hn, d, w[4], d, s->gu, 2 * F);
   for (int64_t t = 0; t < T; ++t)
-    for (int64_t j = 0; j < F; ++j)
-      s->a[t * F + j] = cref_bf16(cref_mul(cref_silu(s->gu[t * 2 * F + j]), s->gu[t * 2 * F + F + j]));
+    for (int64_t j = 0; j < F; ++j) s->a[t * F + j] = swiglu_fwd1(s->gu[t * 2 * F + j], s->gu[t * 2 * F + F + j]);
   float* ffn = (float*)xmalloc(sizeof(float) * T * d);
   if (s->int8) qlin_fwd(s, 3, T, d, F, s->a, w[5], ffn);
   else cref_gemm(0, 1, T, d, F, s->a, F, w[5], F, ffn, d);
@@ -946,14 +1000,8 @@ static void block_bwd(const block_saved* s, const float* dy, const uint16_t* con
   uint16_t* dgu = (uint16_t*)xmalloc(2 * T * 2 * F);
   for (int64_t t = 0; t < T; ++t) {
     for (int64_t j = 0; j < F; ++j) {
-      float g = s->gu[t * 2 * F + j], u = s->gu[t * 2 * F + F + j], dav = da[t * F + j];
-      float sig = cref_sigmoid(g);
-      float silu = cref_mul(g, sig);
-      float dup = cref_mul(dav, silu);
-      float dsg = cref_mul(sig, cref_add(1.0f, cref_mul(g, cref_sub(1.0f, sig))));
-      float dgate = cref_mul(cref_mul(dav, u), dsg);
-      dgu[t * 2 * F + j] = cref_bf16(dgate);
-      dgu[t * 2 * F + F + j] = cref_bf16(dup);
+      swiglu_bwd1(s->gu[t * 2 * F + j], s->gu[t * 2 * F + F + j], da[t * F + j], &dgu[t * 2 * F + j],
+                  &dgu[t * 2 * F + F + j]);
     }
   }
   free(da);
@@ -1115,6 +1163,52 @@ static void tensor_sizes(const cref_model_cfg* c, int64_t* sz, uint8_t* decay) {
   sz[i] = V * d; decay[i++] = 1;                     /* head */
 }
 
+/* R11 (the model section's list of bitwise-reproducible operators names the embedding backward):
+   dE[v] = R1 sum over the ascending positions t with tok[t] == v of dx[t] (plain terms: chains of 32 from +0,
+   then Algorithm 2 over the chain partials).  A vocabulary row that never occurs is +0; a token outside
+   [0, V) contributes nothing. */
+int cref_embed_bwd(int64_t T, int64_t V, int64_t d, const int32_t* tok, const float* dx, float* dE) {
+  if (T < 0 || V <= 0 || d <= 0 || (T > 0 && (!tok || !dx)) || !dE) return -1;
+  int64_t* cnt = (int64_t*)calloc((size_t)V + 1, sizeof(int64_t));
+  for (int64_t t = 0; t < T; ++t)
+    if (tok[t] >= 0 && tok[t] < V) cnt[tok[t] + 1]++;
+  for (int64_t v = 0; v < V; ++v) cnt[v + 1] += cnt[v];
+  int64_t* pos = (int64_t*)xmalloc(sizeof(int64_t) * (T > 0 ? T : 1));
+  int64_t* fill = (int64_t*)xmalloc(sizeof(int64_t) * V);
+  memcpy(fill, cnt, sizeof(int64_t) * V);
+  for (int64_t t = 0; t < T; ++t) /* ascending t within each vocabulary row */
+    if (tok[t] >= 0 && tok[t] < V) pos[fill[tok[t]]++] = t;
+#pragma omp parallel for schedule(dynamic, 16)
+  for (int64_t v = 0; v < V; ++v) {
+    int64_t n = cnt[v + 1] - cnt[v];
+    for (int64_t j = 0; j < d; ++j) {
+      sfold f = {0};
+      for (int64_t c0 = 0; c0 < n; c0 += CHUNK) {
+        int64_t c1 = c0 + CHUNK < n ? c0 + CHUNK : n;
+        float s = 0.0f;
+        for (int64_t q = c0; q < c1; ++q) s = cref_add(s, dx[pos[cnt[v] + q] * d + j]);
+        sfold_push(&f, s);
+      }
+      dE[v * d + j] = sfold_result(&f);
+    }
+  }
+  free(cnt); free(pos); free(fill);
+  return 0;
+}
+
+/* Progress lines on stderr for long oracle runs (set CANON_REF_PROGRESS=1); no effect on any result. */
+static void progress(const char* what, int64_t a, int64_t b) {
+  static int on = -1;
+  if (on < 0) {
+    const char* e = getenv("CANON_REF_PROGRESS");
+    on = (e && e[0] == '1') ? 1 : 0;
+  }
+  if (on) {
+    fprintf(stderr, "oracle: %s %lld %lld\n", what, (long long)a, (long long)b);
+    fflush(stderr);
+  }
+}
+
 /* gradient of the mean loss of one microbatch; grad = flat fp32 buffer in tensor order */
 static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params, const int32_t* tok, int64_t B,
                                 const float* rope_cos, const float* rope_sin, float* grad, const int64_t* off) {
@@ -1148,6 +1242,7 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
     for (int i = 0; i < PL; ++i) w[i] = params[l0 + PL * l + i];
     block_saved_alloc(&saved[l], c, B, layer_window(c, l));
     block_fwd(&saved[l], x, w, rope_cos, rope_sin, y);
+    progress("block forward done: layer, tokens", l, T);
     float* tmp = x; x = y; y = tmp;
   }
   /* final norm, head, loss */
@@ -1164,12 +1259,14 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
   float loss = 0.0f;
   const float invT = inv_of(T);
   cref_xent_z(T, V, logits, lab, invT, c->z_loss, dlogits, row_loss, &loss);
+  progress("head forward and cross-entropy done: tokens, vocab", T, V);
   free(logits);
   free(row_loss);
   /* backward */
   cref_gemm(1, 0, V, d, T, dlogits, V, xf, d, grad + off[i_head], d);     /* dHead = dlogits^T xf */
   float* dxf = (float*)xmalloc(sizeof(float) * T * d);
   cref_gemm(0, 0, T, d, V, dlogits, V, params[i_head], d, dxf, d);       /* dxf = dlogits Head */
+  progress("head backward done: tokens, vocab", T, V);
   free(dlogits);
   free(xf);
   float* dx = (float*)xmalloc(sizeof(float) * T * d);
@@ -1185,6 +1282,7 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
       dw[i] = grad + off[l0 + PL * l + i];
     }
     block_bwd(&saved[l], dx, w, rope_cos, rope_sin, dxp, dw);
+    progress("block backward done: layer, tokens", l, T);
     block_saved_free(&saved[l]);
     float* tmp = dx; dx = dxp; dxp = tmp;
   }
@@ -1196,30 +1294,7 @@ static float microbatch_fwd_bwd(const cref_model_cfg* c, uint16_t* const* params
     free(x_emb);
     free(rstd_emb);
   }
-  /* R11: dE[v] = rsum over ascending positions t with inp[t] == v of dx[t] */
-  float* dE = grad + off[0];
-  int64_t* cnt = (int64_t*)calloc((size_t)V + 1, sizeof(int64_t));
-  for (int64_t t = 0; t < T; ++t) cnt[inp[t] + 1]++;
-  for (int64_t v = 0; v < V; ++v) cnt[v + 1] += cnt[v];
-  int64_t* pos = (int64_t*)xmalloc(sizeof(int64_t) * T);
-  int64_t* fill = (int64_t*)xmalloc(sizeof(int64_t) * V);
-  memcpy(fill, cnt, sizeof(int64_t) * V);
-  for (int64_t t = 0; t < T; ++t) pos[fill[inp[t]]++] = t; /* ascending t within each vocab row */
-#pragma omp parallel for schedule(dynamic, 16)
-  for (int64_t v = 0; v < V; ++v) {
-    int64_t n = cnt[v + 1] - cnt[v];
-    for (int64_t j = 0; j < d; ++j) {
-      sfold f = {0};
-      for (int64_t c0 = 0; c0 < n; c0 += CHUNK) {
-        int64_t c1 = c0 + CHUNK < n ? c0 + CHUNK : n;
-        float s = 0.0f;
-        for (int64_t q = c0; q < c1; ++q) s = cref_add(s, dx[pos[cnt[v] + q] * d + j]);
-        sfold_push(&f, s);
-      }
-      dE[v * d + j] = sfold_result(&f);
-    }
-  }
-  free(cnt); free(pos); free(fill);
+  cref_embed_bwd(T, V, d, inp, dx, grad + off[0]);
   free(dx); free(dxp); free(x); free(y); free(inp); free(lab);
   return loss;
 }
@@ -1577,8 +1652,12 @@ float cref_lsq_step_grad(int64_t T, int64_t K, const uint16_t* x, float s, const
   for (int64_t i = 0; i < n; ++i) t[i] = cref_mul(dx[i], lsq_delta(widen(x[i]), s));
   const float sum = cref_rsum(t, n, 1, CHUNK);
   free(t);
-  const float gamma = (float)(1.0 / sqrt(127.0 * (double)K)); /* RN32(1/sqrt(127 K)) */
+  const float gamma = cref_inv_sqrt_int(127 * K); /* RN32(1/sqrt(127 K)) */
   return cref_mul(sum, gamma);
 }
 
 int cref_num_threads(void) { return omp_get_max_threads(); }
+
+void cref_set_threads(int n) {
+  if (n > 0) omp_set_num_threads(n);
+}

@@ -182,7 +182,17 @@ float cref_fx_to_f32(uint64_t sum, int32_t frac_bits);
    RN(dx * delta) * RN32(1/sqrt(127 K))). */
 float cref_lsq_step_grad(int64_t T, int64_t K, const uint16_t* x, float s, const float* dx);
 
+/* R11 embedding backward: dE [V][d] from dx [T][d] and the tokens [T] of the microbatch (position t's token) */
+int cref_embed_bwd(int64_t T, int64_t V, int64_t d, const int32_t* tok, const float* dx, float* dE);
+/* SwiGLU per element (R4): a = bf16 forward output (if a), dg, du = bf16 gradients of g and u from the fp32
+   gradient da of a (if da, dg and du) */
+int cref_swiglu(int64_t n, const float* g, const float* u, const float* da, uint16_t* a, uint16_t* dg,
+                uint16_t* du);
+/* RN32(1/sqrt(n)) for 1 <= n < 2^60 (NaN otherwise), decided exactly */
+float cref_inv_sqrt_int(int64_t n);
 int cref_num_threads(void);
+/* threads of the parallel loops (each parallel loop runs over independent outputs) */
+void cref_set_threads(int n);
 
 #ifdef __cplusplus
 }
