@@ -235,9 +235,10 @@ size_t canon_block_workspace_bytes(const canon_model_cfg* cfg, int32_t batch);
    array of n device fp32 buffers that receive the reduced gradient (before any clip).  clip: NULL, or the
    R15 settings (canon_clip above) applied to the reduced gradient of all n tensors in the declared order
    between the plan and AdamW; a skipped step leaves params, m and v unchanged.  An out-of-range token
-   also makes *norm_out NaN and sets *skipped_out, and leaves *skip_state unchanged.  step_t is
-   informational (the bias corrections come in consts; a caller that skips an update does not advance
-   them). */
+   also makes *norm_out NaN and sets *skipped_out, and leaves *skip_state unchanged.  step_t: AdamW's step
+   index t >= 1 (else CANON_EINVAL) that consts was computed for; the bias corrections RN32(1/(1 - beta^t))
+   come in consts (evaluated by the caller in binary64 and rounded once), so the library uses t only for this
+   check; a caller that skips an update does not advance t. */
 canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, const canon_dp_plan* plan,
                         uint16_t* const* params, float* const* m, float* const* v, int32_t step_t,
                         const int32_t* windows, const float* rope_cos, const float* rope_sin,
@@ -341,6 +342,16 @@ canon_status canon_attn_dq_fixed(int64_t batch, int64_t n_heads, int64_t n_kv_he
 size_t canon_lsq_step_grad_workspace_bytes(int64_t T, int64_t K);
 canon_status canon_lsq_step_grad(const canon_order* order, int64_t T, int64_t K, const uint16_t* x, const float* s,
                                  const float* dx, float* grad, void* workspace, size_t workspace_bytes, void* stream);
+
+/* R11 embedding backward (the model section lists the embedding backward among the operators made bitwise
+   reproducible): dE[v][:] = R1 over the ascending positions t with tokens[t] == v of dx[t][:] (plain terms:
+   chains of 32 from +0, Algorithm 2 over the chain partials), for every v < V.  A row that never occurs is +0;
+   a token outside [0, V) contributes nothing.  tokens: device int32 [T]; dx: device fp32 [T][d]; dE: device
+   fp32 [V][d], fully written.  T < 2^25 (else CANON_EUNSUPPORTED).  workspace: device memory of
+   canon_embed_bwd_workspace_bytes(T, d) bytes (sort keys, segment starts, chunk partials). */
+size_t canon_embed_bwd_workspace_bytes(int64_t T, int64_t d);
+canon_status canon_embed_bwd(const canon_order* order, int64_t T, int64_t V, int64_t d, const int32_t* tokens,
+                             const float* dx, float* dE, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
    the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,

@@ -96,6 +96,8 @@ def _lib():
             "canon_attn_dq_fixed": (i32, [i64, i64, i64, i64, i64, i64, i32, vp, vp, vp, vp]),
             "canon_lsq_step_grad": (i32, [vp, i64, i64, vp, vp, vp, vp, vp, sz, vp]),
             "canon_lsq_step_grad_workspace_bytes": (sz, [i64, i64]),
+            "canon_embed_bwd": (i32, [vp, i64, i64, i64, vp, vp, vp, vp, sz, vp]),
+            "canon_embed_bwd_workspace_bytes": (sz, [i64, i64]),
             "canon_status_str": (ctypes.c_char_p, [i32]),
             "canon_version": (i32, []),
         }
@@ -197,6 +199,16 @@ def lsq_step_grad(T, K, x, s, dx, grad, workspace, order=ORDER_V1, stream=None):
     _check(_lib().canon_lsq_step_grad(ctypes.byref(order), T, K, _ptr(x), _ptr(s), _ptr(dx), _ptr(grad),
                                       _ptr(workspace), workspace.numel() * workspace.element_size(),
                                       _stream(stream)), "canon_lsq_step_grad")
+
+
+def embed_bwd_workspace_bytes(T, d) -> int:
+    return int(_lib().canon_embed_bwd_workspace_bytes(T, d))
+
+
+def embed_bwd(T, V, d, tokens, dx, dE, workspace, order=ORDER_V1, stream=None):
+    """R11: dE [V, d] from the int32 tokens [T] and dx [T, d] (device tensors)."""
+    _check(_lib().canon_embed_bwd(ctypes.byref(order), T, V, d, _ptr(tokens), _ptr(dx), _ptr(dE), _ptr(workspace),
+                                  workspace.numel() * workspace.element_size(), _stream(stream)), "canon_embed_bwd")
 
 
 def block_workspace_bytes(cfg: ModelCfg, batch: int) -> int:

@@ -69,15 +69,36 @@ struct Dims {
   float eps, scale, z_loss;
 };
 
-float attn_scale(int64_t hd) {
-  if (hd == 128) {
-    uint32_t u = 0x3DB504F3u;  // RN32(1/sqrt(128))
-    float f;
-    memcpy(&f, &u, 4);
-    return f;
-  }
-  return (float)(1.0 / sqrt((double)hd));
+// floor(sqrt(x)) for x < 2^62: a binary64 estimate corrected in integers
+uint64_t isqrt_u64(uint64_t x) {
+  uint64_t r = (uint64_t)sqrt((double)x);
+  while (r > 0 && r * r > x) --r;
+  while ((r + 1) * (r + 1) <= x) ++r;
+  return r;
 }
+
+// RN32(1/sqrt(n)) for 1 <= n < 2^40, in integers: with s such that 2^23 <= m = 2^s / sqrt(n) < 2^24, the
+// significand is m rounded to an integer.  t = floor(2m) = floor(sqrt(floor(4^(s+1) / n))), and m rounds to
+// (t + 1) / 2: 2m is never an odd integer (4^(s+1) / n would be an odd square), so no tie arises.
+float rn32_inv_sqrt(int64_t n) {
+  if (n < 1 || n >= ((int64_t)1 << 40)) return NAN;
+  int bits = 0;
+  while ((n >> bits) > 0) ++bits;
+  int s = 23 + (bits + 1) / 2;
+  uint64_t t = 0;
+  for (;;) {
+    const unsigned __int128 num = (unsigned __int128)1 << (2 * s + 2);
+    t = isqrt_u64((uint64_t)(num / (unsigned __int128)n));
+    if (t < ((uint64_t)1 << 24)) { ++s; continue; }   // m < 2^23
+    if (t >= ((uint64_t)1 << 25)) { --s; continue; }  // m >= 2^24
+    break;
+  }
+  uint64_t m = (t + 1) >> 1;
+  if (m == ((uint64_t)1 << 24)) { m >>= 1; --s; }
+  return ldexpf((float)m, -s);
+}
+
+float attn_scale(int64_t hd) { return rn32_inv_sqrt(hd); }  // 0x3DB504F3 for head_dim 128
 
 int64_t kv_heads(const canon_model_cfg* c) { return c->n_kv_heads > 0 ? c->n_kv_heads : c->n_heads; }
 
@@ -140,8 +161,8 @@ void projections(const Dims& D, Proj (&p)[4]) {
 }
 const int kProjWeight[4] = {1, 2, 4, 5};  // index of each projection's weight among the layer's tensors
 
-// LSQ's gradient scale RN32(1/sqrt(127 K)), evaluated in double and rounded once
-float lsq_gamma(int64_t K) { return (float)(1.0 / sqrt(127.0 * (double)K)); }
+// LSQ's gradient scale RN32(1/sqrt(127 K)), correctly rounded
+float lsq_gamma(int64_t K) { return rn32_inv_sqrt(127 * K); }
 
 // activations a block saves for its backward pass
 struct LayerSave {
@@ -499,7 +520,7 @@ void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, in
   L.win = cv.take<int32_t>((int64_t)c->micro_seqs * (c->seq + 1));
   L.lab = cv.take<int32_t>(D.T);
   L.bad = cv.take<int32_t>(1);
-  L.embed_scratch = cv.take<char>((int64_t)embed_bwd_scratch_bytes(D.T));
+  L.embed_scratch = cv.take<char>((int64_t)embed_bwd_scratch_bytes(D.T, D.d));
   L.grad = cv.take<float>(P);
   L.g_r = p->accum > 1 ? cv.take<float>(P) : nullptr;
   const int nbuf = bit_length(p->dp_replicate) + 1;
@@ -951,6 +972,23 @@ canon_status canon_lsq_step_grad(const canon_order* order, int64_t T, int64_t K,
   return dev(lsq_grad_launch(T * K, x, s, dx, lsq_gamma(K), (float*)workspace, grad, as_stream(stream)));
 }
 
+size_t canon_embed_bwd_workspace_bytes(int64_t T, int64_t d) {
+  if (T < 0 || d < 1 || T >= (int64_t(1) << 25)) return 0;
+  return embed_bwd_scratch_bytes(T, d) + 256;
+}
+
+canon_status canon_embed_bwd(const canon_order* order, int64_t T, int64_t V, int64_t d, const int32_t* tokens,
+                             const float* dx, float* dE, void* workspace, size_t workspace_bytes, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (T < 0 || V < 1 || d < 1 || !dE || (T > 0 && (!tokens || !dx))) return CANON_EINVAL;
+  if (T >= (int64_t(1) << 25) || V > (int64_t(1) << 31) - 1) return CANON_EUNSUPPORTED;
+  const size_t need = canon_embed_bwd_workspace_bytes(T, d);
+  if (!workspace || workspace_bytes < need) return CANON_EWORKSPACE;
+  void* ws = (void*)(((uintptr_t)workspace + 255) & ~(uintptr_t)255);
+  return dev(embed_bwd_launch(1, T, d, tokens, T, V, dx, dE, ws, as_stream(stream)));
+}
+
 canon_status canon_devmath(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
                            void* stream) {
   if (op < 0 || op > 10 || n < 0) return CANON_EINVAL;
@@ -1017,9 +1055,9 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
                         const int32_t* windows, const float* rope_cos, const float* rope_sin,
                         const canon_adamw_consts* consts, const canon_clip* clip, void* workspace,
                         size_t workspace_bytes, float* loss_out, float* const* grads_out, void* stream) {
-  (void)step_t;
   canon_status st = check_order(order);
   if (st != CANON_OK) return st;
+  if (step_t < 1) return CANON_EINVAL;  // AdamW's step index starts at 1
   if (!cfg_ok(cfg) || !plan || plan->accum < 1 || plan->dp_shard < 1 || plan->dp_replicate < 1) return CANON_EINVAL;
   if (!params || !m || !v || !windows || !rope_cos || !rope_sin || !consts || !loss_out) return CANON_EINVAL;
   if (!variants_supported(cfg, (int64_t)cfg->micro_seqs * cfg->seq)) return CANON_EUNSUPPORTED;

@@ -133,7 +133,9 @@ hipError_t token_check_launch(int64_t n, const int32_t* tok, int32_t bound, int3
 hipError_t embed_gather_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld,
                                const uint16_t* E, int64_t V, float* x, hipStream_t s);
 hipError_t labels_launch(int64_t B, int64_t S, const int32_t* win, int64_t win_ld, int32_t* lab, hipStream_t s);
-size_t embed_bwd_scratch_bytes(int64_t T);
+// R11 embedding backward over T = B S positions (T < 2^25): dE [V][d] fully written; scratch of
+// embed_bwd_scratch_bytes(T, d) bytes, 256-byte aligned
+size_t embed_bwd_scratch_bytes(int64_t T, int64_t d);
 hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld, int64_t V,
                             const float* dx, float* dE, void* scratch, hipStream_t s);
 hipError_t quantize_launch(int64_t rows, int64_t cols, int32_t dtype, const void* x, const float* scale,

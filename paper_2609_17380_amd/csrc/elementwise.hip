@@ -565,27 +565,154 @@ hipError_t labels_launch(int64_t B, int64_t S, const int32_t* win, int64_t win_l
   return hipGetLastError();
 }
 
-// ---- embedding backward (R11) --------------------------------------------------------------------
-// A stable counting sort of the positions by token: position t goes to slot
-//   #{t' : tok[t'] < tok[t]} + #{t' < t : tok[t'] == tok[t]},
-// so each token's positions sit together in ascending t.  Then one workgroup per token segment reduces
-// dx over the segment's positions in that order (chunks of 32, binary-carry fold), per column.
+// ---- embedding backward (R11) ----------------------------------------------------------------------
+// dE[v] = R1 over the ascending positions t with tok[t] = v of dx[t].
+//  1. Keys key[t] = (uint32 token) << 32 | t, padded with ~0 to a power of two.  Every key is distinct, so
+//     the sorted order is unique: tokens ascending, positions ascending within a token (no atomics, no
+//     tie order to fix).
+//  2. Bitonic sort of the keys: blocks of kSortBlk keys sorted in LDS, then for each larger merge size the
+//     steps with a partner distance of kSortBlk or more in global memory and the rest in LDS.
+//  3. Segment starts: one workgroup max-scans the head flags of the sorted slots.
+//  4. Chunk chains: one workgroup per sorted slot that starts a chunk (its distance from the segment start
+//     a multiple of 32) runs the chain of its <= 32 positions for every column; a segment of one chunk writes
+//     dE directly, longer segments write the chain partial to part[slot].
+//  5. Fold: one workgroup per segment of more than one chunk folds its chunk partials by Algorithm 2.
+// Tokens outside [0, V) sort after every valid token and contribute nothing.
+constexpr int kSortBlk = 2048;  // keys per LDS sort block (16 KB), one compare-exchange per thread per step
+
 __device__ __forceinline__ int32_t tok_at(const int32_t* win, int64_t win_ld, int64_t S, int64_t t) {
   return win[(t / S) * win_ld + (t % S)];
 }
 
-__global__ void embed_sort_kernel(int64_t T, int64_t S, const int32_t* __restrict__ win, int64_t win_ld,
-                                  int32_t* __restrict__ perm) {
+static int64_t sort_len(int64_t T) {
+  int64_t P = 2;
+  while (P < T) P <<= 1;
+  return P;
+}
+
+__global__ void embed_keys_kernel(int64_t T, int64_t P, int64_t S, const int32_t* __restrict__ win, int64_t win_ld,
+                                  uint64_t* __restrict__ keys) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= T) return;
-  const int32_t v = tok_at(win, win_ld, S, t);
-  int64_t before = 0, rank = 0;
-  for (int64_t u = 0; u < T; ++u) {
-    int32_t w = tok_at(win, win_ld, S, u);
-    before += (w < v);
-    rank += (w == v && u < t);
+  if (t >= P) return;
+  keys[t] = t < T ? ((uint64_t)(uint32_t)tok_at(win, win_ld, S, t) << 32) | (uint64_t)t : ~uint64_t(0);
+}
+
+// one compare-exchange of the bitonic network at merge size k, partner distance j, for pair q
+__device__ __forceinline__ void bitonic_pair(uint64_t* a, int64_t base, int64_t q, int64_t k, int64_t j) {
+  const int64_t i = 2 * j * (q / j) + (q % j), l = i + j;
+  const bool up = ((base + i) & k) == 0;
+  const uint64_t x = a[i], y = a[l];
+  if (up ? (x > y) : (x < y)) {
+    a[i] = y;
+    a[l] = x;
   }
-  perm[before + rank] = (int32_t)t;
+}
+
+// blk = min(P, kSortBlk) keys per workgroup.  k == 0: sort each block completely (merge sizes 2 .. blk);
+// otherwise the steps j = blk/2 .. 1 of merge size k.
+__global__ __launch_bounds__(1024) void bitonic_local_kernel(uint64_t* __restrict__ keys, int64_t blk, int64_t k) {
+  __shared__ uint64_t a[kSortBlk];
+  const int64_t base = (int64_t)blockIdx.x * blk;
+  for (int64_t i = threadIdx.x; i < blk; i += 1024) a[i] = keys[base + i];
+  __syncthreads();
+  const int64_t k0 = k == 0 ? 2 : k, k1 = k == 0 ? blk : k;
+  for (int64_t kk = k0; kk <= k1; kk <<= 1) {
+    for (int64_t j = (k == 0 ? kk : blk) >> 1; j > 0; j >>= 1) {
+      for (int64_t q = threadIdx.x; q < blk / 2; q += 1024) bitonic_pair(a, base, q, kk, j);
+      __syncthreads();
+    }
+  }
+  for (int64_t i = threadIdx.x; i < blk; i += 1024) keys[base + i] = a[i];
+}
+
+__global__ void bitonic_global_kernel(uint64_t* __restrict__ keys, int64_t P, int64_t k, int64_t j) {
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= P / 2) return;
+  bitonic_pair(keys, 0, q, k, j);
+}
+
+// seg[p] = the first sorted slot of p's token, for p < T (one workgroup of 1024 threads)
+__global__ __launch_bounds__(1024) void embed_segstart_kernel(int64_t T, const uint64_t* __restrict__ keys,
+                                                              int32_t* __restrict__ seg) {
+  __shared__ int64_t pre[1024];
+  const int64_t per = (T + 1023) / 1024, p0 = (int64_t)threadIdx.x * per;
+  int64_t run = 0;
+  for (int64_t p = p0; p < p0 + per && p < T; ++p)
+    if (p == 0 || (keys[p] >> 32) != (keys[p - 1] >> 32)) run = p;
+  pre[threadIdx.x] = run;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {  // inclusive max-scan of the thread maxima
+    const int64_t o = threadIdx.x >= (unsigned)off ? pre[threadIdx.x - off] : 0;
+    __syncthreads();
+    if (o > pre[threadIdx.x]) pre[threadIdx.x] = o;
+    __syncthreads();
+  }
+  run = threadIdx.x > 0 ? pre[threadIdx.x - 1] : 0;
+  for (int64_t p = p0; p < p0 + per && p < T; ++p) {
+    if (p == 0 || (keys[p] >> 32) != (keys[p - 1] >> 32)) run = p;
+    seg[p] = (int32_t)run;
+  }
+}
+
+// VEC: four columns per thread with 16-byte loads (d % 4 == 0, dx, dE and part 16-byte aligned)
+template <bool VEC>
+__global__ __launch_bounds__(256) void embed_chunk_kernel(int64_t T, int64_t d, int64_t V,
+                                                          const uint64_t* __restrict__ keys,
+                                                          const int32_t* __restrict__ seg,
+                                                          const float* __restrict__ dx, float* __restrict__ dE,
+                                                          float* __restrict__ part) {
+  const int64_t p = blockIdx.x;
+  const int64_t ss = seg[p];
+  if ((p - ss) % kChunk != 0) return;  // not the first slot of a chunk
+  const uint64_t v = keys[p] >> 32;
+  if (v >= (uint64_t)V) return;
+  __shared__ int32_t pos[kChunk];
+  if (threadIdx.x < kChunk) {
+    const int64_t q = p + threadIdx.x;
+    pos[threadIdx.x] = (q < T && (keys[q] >> 32) == v) ? (int32_t)(uint32_t)keys[q] : -1;
+  }
+  __syncthreads();
+  int len = 0;
+  while (len < kChunk && pos[len] >= 0) ++len;
+  const bool more = p + kChunk < T && (keys[p + kChunk] >> 32) == v;
+  float* out = (p == ss && !more) ? dE + (int64_t)v * d : part + p * d;  // one chunk: the result itself
+  if (VEC) {
+    for (int64_t k = 4 * (int64_t)threadIdx.x; k < d; k += 1024) {
+      float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      for (int i = 0; i < len; ++i) {
+        const float4 g = *reinterpret_cast<const float4*>(dx + (int64_t)pos[i] * d + k);
+        acc.x = acc.x + g.x;
+        acc.y = acc.y + g.y;
+        acc.z = acc.z + g.z;
+        acc.w = acc.w + g.w;
+      }
+      *reinterpret_cast<float4*>(out + k) = acc;
+    }
+  } else {
+    for (int64_t k = threadIdx.x; k < d; k += 256) {
+      float acc = 0.0f;
+      for (int i = 0; i < len; ++i) acc = acc + dx[(int64_t)pos[i] * d + k];
+      out[k] = acc;
+    }
+  }
+}
+
+// one workgroup per segment of more than one chunk: Algorithm 2 over its chunk partials, per column
+__global__ __launch_bounds__(256) void embed_fold_kernel(int64_t T, int64_t d, int64_t V,
+                                                         const uint64_t* __restrict__ keys,
+                                                         const int32_t* __restrict__ seg,
+                                                         const float* __restrict__ part, float* __restrict__ dE) {
+  const int64_t p = blockIdx.x;
+  if (seg[p] != p) return;
+  const uint64_t v = keys[p] >> 32;
+  if (v >= (uint64_t)V || !(p + kChunk < T && (keys[p + kChunk] >> 32) == v)) return;
+  int64_t nc = 2;
+  while (p + nc * kChunk < T && (keys[p + nc * kChunk] >> 32) == v) ++nc;
+  for (int64_t k = threadIdx.x; k < d; k += 256) {
+    LocalFoldN<20> f;  // up to 2^20 - 1 chunks: T < 2^25
+    for (int64_t c = 0; c < nc; ++c) f.push(part[(p + c * kChunk) * d + k]);
+    dE[(int64_t)v * d + k] = f.result();
+  }
 }
 
 __global__ void fill_zero_kernel(int64_t n, float* __restrict__ x) {
@@ -593,58 +720,40 @@ __global__ void fill_zero_kernel(int64_t n, float* __restrict__ x) {
   if (i < n) x[i] = 0.0f;
 }
 
-__global__ __launch_bounds__(256) void embed_segment_kernel(int64_t T, int64_t S, int64_t d,
-                                                            const int32_t* __restrict__ win, int64_t win_ld,
-                                                            int64_t V, const int32_t* __restrict__ perm,
-                                                            const float* __restrict__ dx, float* __restrict__ dE) {
-  const int64_t p = blockIdx.x;
-  const int32_t v = tok_at(win, win_ld, S, perm[p]);
-  if (p > 0 && tok_at(win, win_ld, S, perm[p - 1]) == v) return;  // not the first slot of its segment
-  if (v < 0 || v >= V) return;
-  int64_t n = 1;
-  while (p + n < T && tok_at(win, win_ld, S, perm[p + n]) == v) ++n;
-  for (int64_t k = threadIdx.x; k < d; k += 256) {
-    float st[16];
-    int64_t count = 0;
-    for (int64_t c0 = 0; c0 < n; c0 += kChunk) {
-      float s = 0.0f;
-      const int64_t c1 = c0 + kChunk < n ? c0 + kChunk : n;
-      for (int64_t q = c0; q < c1; ++q) s = s + dx[(int64_t)perm[p + q] * d + k];
-      // binary-carry push
-#pragma unroll
-      for (int L = 0; L < 16; ++L) {
-        if ((count >> L) & 1) {
-          s = st[L] + s;
-        } else {
-          st[L] = s;
-          break;
-        }
-      }
-      ++count;
-    }
-    float r = 0.0f;
-    bool have = false;
-#pragma unroll
-    for (int L = 0; L < 16; ++L) {
-      if ((count >> L) & 1) {
-        if (!have) { r = st[L]; have = true; }
-        else r = st[L] + r;
-      }
-    }
-    dE[(int64_t)v * d + k] = r;
-  }
+// scratch: keys (sort_len(T) uint64), seg (T int32), part (T d floats), each 256-byte aligned
+size_t embed_bwd_scratch_bytes(int64_t T, int64_t d) {
+  const int64_t P = sort_len(T > 0 ? T : 1);
+  auto up = [](size_t b) { return (b + 255) & ~size_t(255); };
+  return up(sizeof(uint64_t) * (size_t)P) + up(sizeof(int32_t) * (size_t)(T > 0 ? T : 1)) +
+         up(sizeof(float) * (size_t)(T > 0 ? T : 1) * (size_t)(d > 0 ? d : 1));
 }
-
-size_t embed_bwd_scratch_bytes(int64_t T) { return sizeof(int32_t) * (size_t)(T > 0 ? T : 1); }
 
 hipError_t embed_bwd_launch(int64_t B, int64_t S, int64_t d, const int32_t* win, int64_t win_ld, int64_t V,
                             const float* dx, float* dE, void* scratch, hipStream_t s) {
   const int64_t T = B * S;
   hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks_for(V * d)), dim3(256), 0, s, V * d, dE);
   if (T == 0) return hipGetLastError();
-  int32_t* perm = (int32_t*)scratch;
-  hipLaunchKernelGGL(embed_sort_kernel, dim3(blocks_for(T)), dim3(256), 0, s, T, S, win, win_ld, perm);
-  hipLaunchKernelGGL(embed_segment_kernel, dim3((unsigned)T), dim3(256), 0, s, T, S, d, win, win_ld, V, perm, dx, dE);
+  const int64_t P = sort_len(T);
+  auto up = [](size_t b) { return (b + 255) & ~size_t(255); };
+  char* base = static_cast<char*>(scratch);
+  uint64_t* keys = reinterpret_cast<uint64_t*>(base);
+  int32_t* seg = reinterpret_cast<int32_t*>(base + up(sizeof(uint64_t) * (size_t)P));
+  float* part = reinterpret_cast<float*>(base + up(sizeof(uint64_t) * (size_t)P) + up(sizeof(int32_t) * (size_t)T));
+  hipLaunchKernelGGL(embed_keys_kernel, dim3(blocks_for(P)), dim3(256), 0, s, T, P, S, win, win_ld, keys);
+  const int64_t blk = P < kSortBlk ? P : kSortBlk;
+  hipLaunchKernelGGL(bitonic_local_kernel, dim3((unsigned)(P / blk)), dim3(1024), 0, s, keys, blk, (int64_t)0);
+  for (int64_t k = 2 * blk; k <= P; k <<= 1) {
+    for (int64_t j = k / 2; j >= blk; j >>= 1)
+      hipLaunchKernelGGL(bitonic_global_kernel, dim3(blocks_for(P / 2)), dim3(256), 0, s, keys, P, k, j);
+    hipLaunchKernelGGL(bitonic_local_kernel, dim3((unsigned)(P / blk)), dim3(1024), 0, s, keys, blk, k);
+  }
+  hipLaunchKernelGGL(embed_segstart_kernel, dim3(1), dim3(1024), 0, s, T, keys, seg);
+  const bool vec = d % 4 == 0 && ((uintptr_t)dx & 15) == 0 && ((uintptr_t)dE & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(embed_chunk_kernel<true>, dim3((unsigned)T), dim3(256), 0, s, T, d, V, keys, seg, dx, dE, part);
+  else
+    hipLaunchKernelGGL(embed_chunk_kernel<false>, dim3((unsigned)T), dim3(256), 0, s, T, d, V, keys, seg, dx, dE, part);
+  hipLaunchKernelGGL(embed_fold_kernel, dim3((unsigned)T), dim3(256), 0, s, T, d, V, keys, seg, part, dE);
   return hipGetLastError();
 }
 

@@ -1,0 +1,57 @@
+"""Seeded inputs of the full-shape parity cases (inputs only: no arithmetic of the method).
+
+Two cases at the shapes the workloads name:
+* ``block``: one decoder block forward and backward at d_model 2048, 16 heads of 128, FFN 8192, RMSNorm eps
+  RN32(1e-5), causal attention, seq 2048, batch 1; x and the upstream gradient bf16 N(0, 1) widened, weights
+  bf16 N(0, 0.02), gains 1.
+* ``step``: a full-width training step: 2 layers, d_model 2048, 16 heads of 128, FFN 8192, vocab 50304,
+  seq 2048, one sequence per microbatch, plan (accum 1, dp_shard 2, dp_replicate 1), tokens uniform over the
+  vocabulary, weights N(0, 0.02), AdamW at t = 1, global-norm clip at 1.0 with the spike rule (5.0, 5).
+
+Both the golden-digest script (oracle side) and the GPU parity test build their inputs here.
+"""
+import hashlib
+
+import numpy as np
+
+import paper_2609_17380_amd.inputs as I
+
+BLOCK = dict(d=2048, H=16, hd=128, F=8192, S=2048, batch=1, eps=1e-5, seed=0, std=0.02)
+STEP = dict(L=2, d=2048, H=16, hd=128, F=8192, V=50304, S=2048, mb=1, plan=(1, 2, 1), eps=1e-5, seed=0,
+            std=0.02, clip=(1.0, 5.0, 5))
+BLOCK_NAMES = ["attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down"]
+
+
+def block_inputs(c=BLOCK):
+    d, F, T = c["d"], c["F"], c["batch"] * c["S"]
+    x = I.bf16_bits_to_f32(I.normal_bf16((T, d), c["seed"], I.TENSOR_IDS["x_in"]))
+    dy = I.bf16_bits_to_f32(I.normal_bf16((T, d), c["seed"], I.TENSOR_IDS["dy_in"]))
+    shapes = [(d,), (3 * d, d), (d, d), (d,), (2 * F, d), (d, F)]
+    w = []
+    for s, n in zip(shapes, BLOCK_NAMES):
+        if len(s) == 1:
+            w.append(np.full(s, 0x3F80, np.uint16))  # gain 1.0
+        else:
+            w.append(I.normal_bf16(s, c["seed"], I.TENSOR_IDS[n], std=c["std"]))
+    cos, sin = I.rope_tables(c["S"], c["hd"])
+    return x, dy, w, cos, sin
+
+
+def step_inputs(c=STEP):
+    params = I.model_params(c["L"], c["d"], c["F"], c["V"], seed=c["seed"], std=c["std"])
+    accum, shard, rep = c["plan"]
+    windows = I.uniform_int((shard * rep * accum * c["mb"], c["S"] + 1), c["seed"], I.TENSOR_IDS["windows"], c["V"])
+    cos, sin = I.rope_tables(c["S"], c["hd"])
+    return params, windows, cos, sin, I.adamw_constants()
+
+
+def digest(a: np.ndarray) -> str:
+    """SHA-256 of a tensor's bytes (little-endian bit patterns, row-major)."""
+    return hashlib.sha256(np.ascontiguousarray(a).tobytes()).hexdigest()
+
+
+def head_bits(a: np.ndarray, n: int = 4) -> list:
+    """The bit patterns of a tensor's first n elements, for a readable first difference."""
+    flat = np.ascontiguousarray(a).reshape(-1)
+    view = flat.view(np.uint32) if flat.dtype == np.float32 else flat.view(np.uint16)
+    return [int(v) for v in view[:n]]

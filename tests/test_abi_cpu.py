@@ -74,6 +74,19 @@ def test_host_validation_rejects_before_any_launch():
         for k_, v_ in fields.items():
             setattr(cfg, k_, v_)
         assert lib.canon_block_workspace_bytes(ctypes.byref(cfg), 1) == 0, fields
+    # a step index below 1
+    cfg = C.ModelCfg(1, 64, 4, 16, 96, 97, 48, 1, 1e-5)
+    plan = C.DPPlan(1, 1, 1)
+    ptrs = (ctypes.c_void_p * 9)(*([base] * 9))
+    consts = C.AdamWConsts(*([0.1] * 9))
+    for t in (0, -3):
+        assert lib.canon_step(order, ctypes.byref(cfg), ctypes.byref(plan), ptrs, ptrs, ptrs, t, x, x, x,
+                              ctypes.byref(consts), None, x, 1 << 30, x, None, None) == C.EINVAL
+    # embedding backward: negative sizes, a missing pointer, too many positions, a small workspace
+    assert lib.canon_embed_bwd(order, -1, 10, 4, x, dx, dy, x, 1 << 20, None) == C.EINVAL
+    assert lib.canon_embed_bwd(order, 8, 10, 4, None, dx, dy, x, 1 << 20, None) == C.EINVAL
+    assert lib.canon_embed_bwd(order, 1 << 25, 10, 4, x, dx, dy, x, 1 << 40, None) == C.EUNSUPPORTED
+    assert lib.canon_embed_bwd(order, 8, 10, 4, x, dx, dy, x, 16, None) == C.EWORKSPACE
 
 
 def test_sha256_constants_in_the_device_source():

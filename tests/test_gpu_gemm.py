@@ -42,13 +42,15 @@ def test_layouts_and_ragged_shapes(m, n, k, ta, tb):
     assert_bits(gpu_gemm(a, b, ta, tb, m, n, k), oracle.gemm(a, b, bool(ta), bool(tb)), f"{m}x{n}x{k}")
 
 
-@pytest.mark.parametrize("k", [2048, 6144 + 32, 8192, 16384 + 96, 50304])
-def test_deep_folds(k):
-    # chunk counts 64, 193, 256, 515, 1572: every register-stack depth the 1B step uses
-    print(f"gemm fold depth k={k}", flush=True)
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+@pytest.mark.parametrize("k", [2048, 6144, 6144 + 32, 8192, 16384, 16384 + 96, 50304, 128256])
+def test_deep_folds(k, ta, tb):
+    # chunk counts 64, 192, 193, 256, 512, 515, 1572, 4008: every fold depth the steps use (stack depths 7, 9,
+    # 11 and 12), in every operand layout
+    print(f"gemm fold depth k={k} ta={ta} tb={tb}", flush=True)
     m, n = 70, 130
-    a, b = operands(m, n, k, 0, 1, 4)
-    assert_bits(gpu_gemm(a, b, 0, 1, m, n, k), oracle.gemm(a, b, False, True), f"k={k}")
+    a, b = operands(m, n, k, ta, tb, 4)
+    assert_bits(gpu_gemm(a, b, ta, tb, m, n, k), oracle.gemm(a, b, bool(ta), bool(tb)), f"k={k}")
 
 
 def test_k_zero_and_empty():
@@ -106,11 +108,17 @@ def test_invalid_arguments_are_rejected():
     assert e.value.status == C.EUNSUPPORTED
 
 
-# full 1B shapes (8192-token microbatch): forward, weight-gradient and input-gradient GEMMs
+# full 1B shapes (8192-token microbatch): all fourteen forward, weight-gradient and input-gradient GEMMs of the
+# sweep, and the head's input gradient at the paper architecture's vocabulary (contraction 128256)
 FULL = [
-    ("qkv", 8192, 6144, 2048, 0, 1), ("down", 8192, 2048, 8192, 0, 1), ("head", 8192, 50304, 2048, 0, 1),
-    ("wgrad_gate_up", 16384, 2048, 8192, 1, 0), ("wgrad_head", 50304, 2048, 8192, 1, 0),
-    ("dgrad_head", 8192, 2048, 50304, 0, 0),
+    ("qkv", 8192, 6144, 2048, 0, 1), ("out", 8192, 2048, 2048, 0, 1), ("gate_up", 8192, 16384, 2048, 0, 1),
+    ("down", 8192, 2048, 8192, 0, 1), ("head", 8192, 50304, 2048, 0, 1),
+    ("wgrad_qkv", 6144, 2048, 8192, 1, 0), ("wgrad_out", 2048, 2048, 8192, 1, 0),
+    ("wgrad_gate_up", 16384, 2048, 8192, 1, 0), ("wgrad_down", 2048, 8192, 8192, 1, 0),
+    ("wgrad_head", 50304, 2048, 8192, 1, 0),
+    ("dgrad_qkv", 8192, 2048, 6144, 0, 0), ("dgrad_gate_up", 8192, 2048, 16384, 0, 0),
+    ("dgrad_down", 8192, 8192, 2048, 0, 0), ("dgrad_head", 8192, 2048, 50304, 0, 0),
+    ("dgrad_head_v128256", 4096, 2048, 128256, 0, 0),
 ]
 
 

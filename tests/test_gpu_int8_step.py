@@ -37,6 +37,18 @@ def test_lsq_step_grad_bit_exact(T, K, s):
     assert_bits(run_lsq(x16, np.float32(s), dx), np.array([want], np.float32), "lsq grad")
 
 
+def test_lsq_gradient_scale_over_many_widths():
+    """The host constant RN32(1/sqrt(127 K)) of the device path against the oracle's (pinned to exact
+    arithmetic) for every K up to 64 and a spread of widths beyond, on a constant gradient sum."""
+    ks = list(range(1, 65)) + [127, 128, 1000, 2047, 2048, 4096, 5632, 8192, 11264, 16384, 28672, 65536, 131071]
+    for K in ks:
+        T = 2
+        x16 = I.normal_bf16((T, K), 5, I.TENSOR_IDS["x_in"], std=0.3)
+        dx = I.normal_f32((T, K), 5, I.TENSOR_IDS["dy_in"], std=1e-3)
+        s = np.float32(0.05)
+        assert_bits(run_lsq(x16, s, dx), np.array([oracle.lsq_step_grad(x16, s, dx)], np.float32), f"K={K}")
+
+
 def test_lsq_step_grad_ties_and_clamps():
     s = np.float32(0.125)
     rng = np.random.default_rng(4)

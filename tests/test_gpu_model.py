@@ -46,11 +46,12 @@ def test_block_bit_exact(d, H, F, S, batch, std):
     block_case(d, H, F, S, batch, std)
 
 
-def run_step(L, d, H, F, V, S, mb, plan, seed=0, grads=True):
+def run_step(L, d, H, F, V, S, mb, plan, seed=0, grads=True, windows=None):
     hd = d // H
     params = I.model_params(L, d, F, V, seed=seed, std=0.02)
     R = plan[1] * plan[2]
-    windows = I.uniform_int((R * plan[0] * mb, S + 1), seed, I.TENSOR_IDS["windows"], V)
+    if windows is None:
+        windows = I.uniform_int((R * plan[0] * mb, S + 1), seed, I.TENSOR_IDS["windows"], V)
     cos, sin = I.rope_tables(S, hd)
     k = I.adamw_constants()
     po = [p.copy() for p in params]
@@ -83,6 +84,29 @@ def test_step_bit_exact(plan):
         assert_bits(pg[i], po[i], f"param {i}")
         assert_bits(mg[i], mo[i], f"m {i}")
         assert_bits(vg[i], vo[i], f"v {i}")
+
+
+def test_step_with_heavily_repeated_tokens():
+    """Token draws skewed like text: one token takes ~60% of each 2048-token microbatch (more than 1024
+    occurrences: the embedding backward's chunk chain runs over 39 chunks and the fold over them), others
+    ~10% and ~2% (several chunks), the rest uniform."""
+    L, d, H, F, V, S, mb, plan = 1, 128, 1, 128, 300, 2048, 1, (1, 2, 1)
+    rng = np.random.default_rng(17)
+    n = plan[1] * mb
+    win = rng.integers(0, V, size=(n, S + 1)).astype(np.int32)
+    u = rng.random((n, S + 1))
+    win[u < 0.60] = 7
+    win[(u >= 0.60) & (u < 0.70)] = 11
+    win[(u >= 0.70) & (u < 0.72)] = 13
+    counts = [(win[i, :S] == 7).sum() for i in range(n)]
+    print(f"step skewed tokens: token 7 occurs {counts} times per microbatch", flush=True)
+    assert min(counts) > 1024
+    (lo, go, po, mo, vo), (lg, gg, pg, mg, vg) = run_step(L, d, H, F, V, S, mb, plan, windows=win)
+    assert_bits(lg, np.array([lo], np.float32), "loss")
+    assert_bits(gg[0], go[0], "embedding gradient")
+    for i in range(len(po)):
+        assert_bits(gg[i], go[i], f"grad {i}")
+        assert_bits(pg[i], po[i], f"param {i}")
 
 
 def test_step_rejects_bad_tokens_without_update():
