@@ -353,6 +353,17 @@ size_t canon_embed_bwd_workspace_bytes(int64_t T, int64_t d);
 canon_status canon_embed_bwd(const canon_order* order, int64_t T, int64_t V, int64_t d, const int32_t* tokens,
                              const float* dx, float* dE, void* workspace, size_t workspace_bytes, void* stream);
 
+/* canon_lsq_step_grad without a workspace argument, for callers that cannot allocate device memory (code under
+   HIP graph capture, serving loops, harnesses that forbid hipMalloc).  Same arguments, result and errors as
+   canon_lsq_step_grad.  The block sums live in a 256 KiB device array inside the library, one copy per GPU,
+   taken on the first call on that GPU and held until the process ends; no call allocates or frees memory.
+   T * K may be at most canon_lsq_step_grad_noalloc_max_terms() (2^31); larger calls return
+   CANON_EUNSUPPORTED and enqueue nothing.  Every call on one GPU shares its array: calls that overlap on one
+   GPU (different streams, or host threads without ordering) race and give undefined results. */
+canon_status canon_lsq_step_grad_noalloc(const canon_order* order, int64_t T, int64_t K, const uint16_t* x,
+                                         const float* s, const float* dx, float* grad, void* stream);
+int64_t canon_lsq_step_grad_noalloc_max_terms(void);
+
 /* Device evaluation of the R0/R4 primitives, element by element, for testing the device math against
    the oracle: op 0 add, 1 sub, 2 mul, 3 fma(a,b,c), 4 div, 5 sqrt, 6 cexp, 7 clog, 8 sigmoid, 9 silu,
    10 bf16 round trip.  a, b, c, out: device fp32 [n] (b, c may be NULL when unused). */

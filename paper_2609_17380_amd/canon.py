@@ -96,8 +96,10 @@ def _lib():
             "canon_attn_dq_fixed": (i32, [i64, i64, i64, i64, i64, i64, i32, vp, vp, vp, vp]),
             "canon_lsq_step_grad": (i32, [vp, i64, i64, vp, vp, vp, vp, vp, sz, vp]),
             "canon_lsq_step_grad_workspace_bytes": (sz, [i64, i64]),
+            "canon_lsq_step_grad_noalloc": (i32, [vp, i64, i64, vp, vp, vp, vp, vp]),
             "canon_embed_bwd": (i32, [vp, i64, i64, i64, vp, vp, vp, vp, sz, vp]),
             "canon_embed_bwd_workspace_bytes": (sz, [i64, i64]),
+            "canon_lsq_step_grad_noalloc_max_terms": (i64, []),
             "canon_status_str": (ctypes.c_char_p, [i32]),
             "canon_version": (i32, []),
         }
@@ -209,6 +211,16 @@ def embed_bwd(T, V, d, tokens, dx, dE, workspace, order=ORDER_V1, stream=None):
     """R11: dE [V, d] from the int32 tokens [T] and dx [T, d] (device tensors)."""
     _check(_lib().canon_embed_bwd(ctypes.byref(order), T, V, d, _ptr(tokens), _ptr(dx), _ptr(dE), _ptr(workspace),
                                   workspace.numel() * workspace.element_size(), _stream(stream)), "canon_embed_bwd")
+
+
+def lsq_step_grad_noalloc(T, K, x, s, dx, grad, order=ORDER_V1, stream=None):
+    """canon_lsq_step_grad with the block sums in the library's own device array (no workspace)."""
+    _check(_lib().canon_lsq_step_grad_noalloc(ctypes.byref(order), T, K, _ptr(x), _ptr(s), _ptr(dx), _ptr(grad),
+                                              _stream(stream)), "canon_lsq_step_grad_noalloc")
+
+
+def lsq_step_grad_noalloc_max_terms() -> int:
+    return int(_lib().canon_lsq_step_grad_noalloc_max_terms())
 
 
 def block_workspace_bytes(cfg: ModelCfg, batch: int) -> int:

@@ -989,6 +989,19 @@ canon_status canon_embed_bwd(const canon_order* order, int64_t T, int64_t V, int
   return dev(embed_bwd_launch(1, T, d, tokens, T, V, dx, dE, ws, as_stream(stream)));
 }
 
+canon_status canon_lsq_step_grad_noalloc(const canon_order* order, int64_t T, int64_t K, const uint16_t* x,
+                                         const float* s, const float* dx, float* grad, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (T < 0 || K < 1 || !s || !grad || (T > 0 && (!x || !dx))) return CANON_EINVAL;
+  if (T > lsq_noalloc_max_terms() / K) return CANON_EUNSUPPORTED;  // T K beyond the library's array
+  float* part = nullptr;
+  TRY(lsq_scratch(&part));
+  return dev(lsq_grad_launch(T * K, x, s, dx, lsq_gamma(K), part, grad, as_stream(stream)));
+}
+
+int64_t canon_lsq_step_grad_noalloc_max_terms(void) { return lsq_noalloc_max_terms(); }
+
 canon_status canon_devmath(int32_t op, int64_t n, const float* a, const float* b, const float* c, float* out,
                            void* stream) {
   if (op < 0 || op > 10 || n < 0) return CANON_EINVAL;

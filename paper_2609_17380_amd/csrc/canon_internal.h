@@ -175,6 +175,10 @@ hipError_t attn_dq_fixed_launch(int64_t B, int64_t H, int64_t Hkv, int64_t S, in
 int64_t lsq_grad_parts(int64_t n);
 hipError_t lsq_grad_launch(int64_t n, const uint16_t* x, const float* s, const float* dx, float gamma, float* part,
                            float* out, hipStream_t st);
+// the allocation-free variant: the calling GPU's copy of lsq.hip's device array of block sums (its address
+// taken once per device), and the largest n it holds
+hipError_t lsq_scratch(float** out);
+int64_t lsq_noalloc_max_terms();
 hipError_t set_nan_if_launch(const int32_t* flag, float* x, hipStream_t s);
 
 }  // namespace canon

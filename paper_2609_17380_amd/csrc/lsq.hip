@@ -10,6 +10,8 @@
 // the block sums (each thread a complete subtree of consecutive sums, then across threads) and scales.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "canon_dev.h"
 #include "canon_internal.h"
 
@@ -125,6 +127,34 @@ __global__ __launch_bounds__(256) void lsq_final_kernel(int64_t nparts, const fl
 }  // namespace
 
 int64_t lsq_grad_parts(int64_t n) { return (n + (int64_t)kBlockChunks * kChunk - 1) / ((int64_t)kBlockChunks * kChunk); }
+
+// ---- the allocation-free variant: the block sums live in a file-scope device array ----
+// One copy per GPU, held until the process ends.  Host code never uses the array's name as an address:
+// the device address of each GPU's copy comes from hipGetSymbolAddress with that GPU current.
+constexpr int64_t kScratchParts = 65536;  // 256 KiB: block sums of up to 2^31 terms
+static __device__ __align__(256) float scratch[kScratchParts];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static float* g_scratch_dev[kMaxDevices];  // device address of the current GPU's copy, set on first use
+
+int64_t lsq_noalloc_max_terms() { return kScratchParts * (int64_t)kBlockChunks * kChunk; }
+
+hipError_t lsq_scratch(float** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return e != hipSuccess ? e : hipErrorInvalidSymbol;
+    g_scratch_dev[dev] = static_cast<float*>(ptr);
+  }
+  *out = g_scratch_dev[dev];
+  return hipSuccess;
+}
 
 hipError_t lsq_grad_launch(int64_t n, const uint16_t* x, const float* s, const float* dx, float gamma, float* part,
                            float* out, hipStream_t st) {

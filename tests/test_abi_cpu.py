@@ -87,6 +87,9 @@ def test_host_validation_rejects_before_any_launch():
     assert lib.canon_embed_bwd(order, 8, 10, 4, None, dx, dy, x, 1 << 20, None) == C.EINVAL
     assert lib.canon_embed_bwd(order, 1 << 25, 10, 4, x, dx, dy, x, 1 << 40, None) == C.EUNSUPPORTED
     assert lib.canon_embed_bwd(order, 8, 10, 4, x, dx, dy, x, 16, None) == C.EWORKSPACE
+    # the allocation-free LSQ gradient beyond its array
+    big = lib.canon_lsq_step_grad_noalloc_max_terms() // 8 + 1
+    assert lib.canon_lsq_step_grad_noalloc(order, big, 8, x, dx, dy, rstd, None) == C.EUNSUPPORTED
 
 
 def test_sha256_constants_in_the_device_source():
