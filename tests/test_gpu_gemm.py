@@ -53,6 +53,17 @@ def test_deep_folds(k, ta, tb):
     assert_bits(gpu_gemm(a, b, ta, tb, m, n, k), oracle.gemm(a, b, bool(ta), bool(tb)), f"k={k}")
 
 
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+@pytest.mark.parametrize("k", [64, 96, 2048, 2080, 6144, 8192, 16384 + 32, 50304, 128256])
+def test_whole_tiles_every_depth(k, ta, tb):
+    # whole 64 x 128 tiles (the unchecked 16-byte load path of every chunk), even and odd chunk counts, every
+    # stack depth, every layout
+    print(f"gemm whole tiles 128x256x{k} ta={ta} tb={tb}", flush=True)
+    m, n = 128, 256
+    a, b = operands(m, n, k, ta, tb, 8)
+    assert_bits(gpu_gemm(a, b, ta, tb, m, n, k), oracle.gemm(a, b, bool(ta), bool(tb)), f"k={k}")
+
+
 def test_k_zero_and_empty():
     c = torch.full((4, 5), float("nan"), dtype=torch.float32, device=DEV)
     a = torch.zeros(4, 1, dtype=torch.bfloat16, device=DEV)
@@ -138,7 +149,7 @@ def test_full_size_sampled(name, m, n, k, ta, tb):
 
 @pytest.mark.parametrize("kind", ["wide", "tiny", "ties", "cancel", "huge"])
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
-@pytest.mark.parametrize("m,n,k", [(130, 260, 192), (70, 130, 167)])
+@pytest.mark.parametrize("m,n,k", [(130, 260, 192), (70, 130, 167), (128, 256, 224)])
 def test_adversarial_operands(kind, ta, tb, m, n, k):
     # the matrix-core chains against the oracle where rounding decides: subnormal products and partial sums
     # (flush), bf16 subnormal operands (read as zero), round-half-even ties, exact cancellation with signed
