@@ -85,7 +85,9 @@ def gemm_case(m, n, k, a_off=0, seed=0, extreme=False):
 
 
 @pytest.mark.parametrize("m,n,k", [(130, 260, 192), (128, 128, 64), (1, 1, 1), (200, 3, 1000), (64, 300, 48),
-                                   (129, 129, 4096), (7, 5, 0)])
+                                   (129, 129, 4096), (7, 5, 0),
+                                   # whole 256 x 256 tiles: 128-byte stages, 64-byte stages, one stage
+                                   (256, 256, 128), (512, 768, 192), (768, 512, 2048), (256, 256, 64)])
 def test_gemm_i8(m, n, k):
     print(f"gemm_i8 {m}x{n}x{k}", flush=True)
     gemm_case(m, n, k)
@@ -94,6 +96,7 @@ def test_gemm_i8(m, n, k):
 def test_gemm_i8_misaligned_and_extreme():
     gemm_case(70, 90, 160, a_off=3)           # operand off 16-byte alignment: byte loads
     gemm_case(64, 64, 65536, extreme=True)    # |acc| up to 2^30
+    gemm_case(256, 256, 65536, extreme=True)  # the same through the whole-tile kernel
 
 
 def test_quantised_linear_1b_shapes_sampled():
