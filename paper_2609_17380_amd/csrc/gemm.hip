@@ -143,40 +143,11 @@ __device__ __forceinline__ v4f fetch4(const float* base, int idx, int g4) {
 }
 
 // One full chunk's chain: 32 dependent rank-1 updates from +0, operand reads one group ahead.
-#ifndef CHAIN_VARIANT
-#define CHAIN_VARIANT 0
-#endif
 template <bool TA, bool TB>
 __device__ __forceinline__ v32f chain_full(const float* As, const float* Bs, int ai, int bi) {
   v32f acc;
 #pragma unroll
   for (int v = 0; v < 32; ++v) acc[v] = 0.0f;
-#if CHAIN_VARIANT == 2
-  v4f a4[KC / 4], b4[KC / 4];
-#pragma unroll
-  for (int g4 = 0; g4 < KC / 4; ++g4) {
-    a4[g4] = fetch4<TA, LDMA>(As, ai, g4);
-    b4[g4] = fetch4<!TB, LDMB>(Bs, bi, g4);
-  }
-#pragma unroll
-  for (int g4 = 0; g4 < KC / 4; ++g4)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x1f32(a4[g4][j], b4[g4][j], acc, 0, 0, 0);
-#elif CHAIN_VARIANT == 1
-  v4f a0 = fetch4<TA, LDMA>(As, ai, 0), b0 = fetch4<!TB, LDMB>(Bs, bi, 0);
-  v4f a1 = fetch4<TA, LDMA>(As, ai, 1), b1 = fetch4<!TB, LDMB>(Bs, bi, 1);
-#pragma unroll
-  for (int g4 = 0; g4 < KC / 4; ++g4) {
-    v4f a2 = a1, b2 = b1;
-    if (g4 + 2 < KC / 4) {
-      a2 = fetch4<TA, LDMA>(As, ai, g4 + 2);
-      b2 = fetch4<!TB, LDMB>(Bs, bi, g4 + 2);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x1f32(a0[j], b0[j], acc, 0, 0, 0);
-    a0 = a1; b0 = b1; a1 = a2; b1 = b2;
-  }
-#else
   v4f a4 = fetch4<TA, LDMA>(As, ai, 0), b4 = fetch4<!TB, LDMB>(Bs, bi, 0);
 #pragma unroll
   for (int g4 = 0; g4 < KC / 4; ++g4) {
@@ -190,7 +161,6 @@ __device__ __forceinline__ v32f chain_full(const float* As, const float* Bs, int
     a4 = an;
     b4 = bn;
   }
-#endif
   return acc;
 }
 
