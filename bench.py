@@ -110,7 +110,10 @@ def _hbm(ms, nbytes):
             "peak": PEAK_HBM, "frac": round(gbs / PEAK_HBM, 4)}
 
 
-def kernel_table(C, I, torch, np, stream, dev):
+KERNEL_GROUPS = ("gemm", "int8", "rows", "embed", "plan", "block", "attn_i8", "open1b")
+
+
+def kernel_table(C, I, torch, np, stream, dev, groups=KERNEL_GROUPS):
     """Each entry point at the shapes of the single-kernel workloads: the GEMM sweep over the 1B shapes, RMSNorm
     over a microbatch, causal softmax at 16 heads x 2048 x 2048, cross-entropy 8192 x 50304, the ordered sum of 8
     gradient buffers of 1.2e9 fp32, AdamW over 1.2e9 parameters, the global gradient norm (and clip) over the
@@ -125,145 +128,168 @@ def kernel_table(C, I, torch, np, stream, dev):
 
     out = {}
     print("bench: kernel table", file=sys.stderr, flush=True)
-    for name, m, n, k, ta, tb in GEMM_SWEEP:
-        a = randn((k, m) if ta else (m, k), dtype=torch.bfloat16)
-        b = randn((n, k) if tb else (k, n), dtype=torch.bfloat16)
-        c = torch.empty((m, n), dtype=torch.float32, device=dev)
-        lda, ldb = a.shape[1], b.shape[1]
-        # two warm launches: the first shape of the sweep otherwise carries the clock ramp after the step replays
-        ms = _timed(torch, stream, lambda: C.gemm(m, n, k, a, lda, b, ldb, c, n, ta, tb, stream=stream), 5, warm=2)
-        tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
-        out[f"gemm_{name}_{m}x{n}x{k}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tf, 2),
-                                           "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
-                                           "frac": round(tf / PEAK_FP32_MFMA, 4),
-                                           "pct_bf16_peak": round(100 * tf / PEAK_BF16_MFMA, 3)}
-        del a, b, c
 
-    # the int8 quantised linear (the paper's W8A8 path): exact int8 GEMM with dequantisation at the
-    # projection shapes of the 1B decoder, and the quantisers
-    for name, m, n, k in [("qkv", 8192, 6144, 2048), ("gate_up", 8192, 16384, 2048), ("down", 8192, 2048, 8192),
-                          ("out", 8192, 2048, 2048)]:
-        qa = torch.randint(-128, 128, (m, k), generator=g, device=dev, dtype=torch.int8)
-        qb = torch.randint(-128, 128, (n, k), generator=g, device=dev, dtype=torch.int8)
-        sa = torch.full((1,), 0.01, device=dev)
-        sb = torch.full((n,), 0.001, device=dev)
-        yq = torch.empty((m, n), dtype=torch.float32, device=dev)
-        ms = _timed(torch, stream, lambda: C.gemm_i8(m, n, k, qa, k, qb, k, y=yq, sa=sa, sb=sb, stream=stream), 5)
-        tops = 2.0 * m * n * k / (ms * 1e-3) / 1e12
-        out[f"gemm_i8_{name}_{m}x{n}x{k}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tops, 1),
-                                              "unit": "TOP/s", "peak": PEAK_INT8_MFMA,
-                                              "frac": round(tops / PEAK_INT8_MFMA, 4)}
-        del qa, qb, yq
-    # int8 backward of the gate/up projection: rotated straight-through dx and dW (2 GEMMs of 2*T*N*K each)
-    Tq, Nq, Kq = 8192, 16384, 2048
-    dyq = randn((Tq, Nq), 1e-3)
-    qxq = torch.randint(-128, 128, (Tq, Kq), generator=g, device=dev, dtype=torch.int8)
-    qwq = torch.randint(-128, 128, (Nq, Kq), generator=g, device=dev, dtype=torch.int8)
-    sxq = torch.full((1,), 0.02, device=dev)
-    swq = torch.full((Nq,), 0.001, device=dev)
-    dxq = torch.empty((Tq, Kq), device=dev)
-    dwq = torch.empty((Nq, Kq), device=dev)
-    wsq = torch.empty(C.qlinear_bwd_workspace_bytes(Tq, Nq, Kq), dtype=torch.uint8, device=dev)
-    ms = _timed(torch, stream, lambda: C.qlinear_bwd(Tq, Nq, Kq, dyq, qxq, sxq, qwq, swq, dxq, dwq, wsq,
-                                                    stream=stream), 3)
-    tops = 2 * 2.0 * Tq * Nq * Kq / (ms * 1e-3) / 1e12
-    out[f"qlinear_bwd_gate_up_{Tq}x{Nq}x{Kq}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tops, 1),
-                                                 "unit": "TOP/s", "peak": PEAK_INT8_MFMA,
-                                                 "frac": round(tops / PEAK_INT8_MFMA, 4)}
-    del dyq, qxq, qwq, dxq, dwq, wsq
-    wq = randn((16384, 2048), 0.02, torch.bfloat16)
-    swq = torch.empty(16384, dtype=torch.float32, device=dev)
-    ms = _timed(torch, stream, lambda: C.quant_scales(16384, 2048, wq, swq, stream=stream), 10)
-    out["quant_scales_16384x2048"] = _hbm(ms, 16384 * 2048 * 2 + 16384 * 4)
-    qq = torch.empty((16384, 2048), dtype=torch.int8, device=dev)
-    ms = _timed(torch, stream, lambda: C.quantize(16384, 2048, wq, swq, True, qq, stream=stream), 10)
-    out["quantize_16384x2048_bf16"] = _hbm(ms, 16384 * 2048 * 3 + 16384 * 4)
-    del wq, swq, qq
+    def want(group):
+        return group in groups
 
-    T, d = MB * S, D
-    x = randn((T, d))
-    gain = torch.full((d,), 0x3F80, dtype=torch.int16, device=dev)
-    y = torch.empty((T, d), dtype=torch.int16, device=dev)
-    rstd = torch.empty(T, dtype=torch.float32, device=dev)
-    ms = _timed(torch, stream, lambda: C.rownorm(C.FWD, T, d, x, gain, 1e-5, y=y, rstd=rstd, stream=stream), 20)
-    out[f"rownorm_fwd_{T}x{d}"] = _hbm(ms, T * d * (4 + 2) + T * 4 + d * 2)
-    dy, dx = randn((T, d)), torch.empty((T, d), dtype=torch.float32, device=dev)
-    dgain = torch.empty(d, dtype=torch.float32, device=dev)
-    ms = _timed(torch, stream, lambda: C.rownorm(C.BWD, T, d, x, gain, 1e-5, rstd=rstd, dy=dy, dx=dx, dgain=dgain,
-                                                stream=stream), 20)
-    out[f"rownorm_bwd_{T}x{d}"] = _hbm(ms, T * d * 12 + T * 4 + d * 6)
-    del x, y, rstd, dy, dx, dgain
+    if want("gemm"):
+        for name, m, n, k, ta, tb in GEMM_SWEEP:
+            a = randn((k, m) if ta else (m, k), dtype=torch.bfloat16)
+            b = randn((n, k) if tb else (k, n), dtype=torch.bfloat16)
+            c = torch.empty((m, n), dtype=torch.float32, device=dev)
+            lda, ldb = a.shape[1], b.shape[1]
+            # two warm launches: the first shape of the sweep otherwise carries the clock ramp after the step replays
+            ms = _timed(torch, stream, lambda: C.gemm(m, n, k, a, lda, b, ldb, c, n, ta, tb, stream=stream), 5, warm=2)
+            tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+            out[f"gemm_{name}_{m}x{n}x{k}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tf, 2),
+                                               "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
+                                               "frac": round(tf / PEAK_FP32_MFMA, 4),
+                                               "pct_bf16_peak": round(100 * tf / PEAK_BF16_MFMA, 3)}
+            del a, b, c
 
-    bh = 16
-    raw = randn((bh, S, S))
-    probs = torch.empty((bh, S, S), dtype=torch.int16, device=dev)
-    scale = float(np.float32(1 / np.sqrt(128)))
-    ms = _timed(torch, stream, lambda: C.softmax_xent(C.SOFTMAX_CAUSAL, bh * S, S, raw, probs, scale=scale,
-                                                     stream=stream), 10)
-    out[f"softmax_causal_{bh}x{S}x{S}"] = _hbm(ms, bh * (S * (S + 1) // 2) * 4 + bh * S * S * 2)
-    del raw, probs
+    if want("int8"):
+        # the int8 quantised linear (the paper's W8A8 path): exact int8 GEMM with dequantisation at the
+        # projection shapes of the 1B decoder, and the quantisers
+        for name, m, n, k in [("qkv", 8192, 6144, 2048), ("gate_up", 8192, 16384, 2048), ("down", 8192, 2048, 8192),
+                              ("out", 8192, 2048, 2048)]:
+            qa = torch.randint(-128, 128, (m, k), generator=g, device=dev, dtype=torch.int8)
+            qb = torch.randint(-128, 128, (n, k), generator=g, device=dev, dtype=torch.int8)
+            sa = torch.full((1,), 0.01, device=dev)
+            sb = torch.full((n,), 0.001, device=dev)
+            yq = torch.empty((m, n), dtype=torch.float32, device=dev)
+            ms = _timed(torch, stream, lambda: C.gemm_i8(m, n, k, qa, k, qb, k, y=yq, sa=sa, sb=sb, stream=stream), 5)
+            tops = 2.0 * m * n * k / (ms * 1e-3) / 1e12
+            out[f"gemm_i8_{name}_{m}x{n}x{k}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tops, 1),
+                                                  "unit": "TOP/s", "peak": PEAK_INT8_MFMA,
+                                                  "frac": round(tops / PEAK_INT8_MFMA, 4)}
+            del qa, qb, yq
+        # int8 backward of the gate/up projection: rotated straight-through dx and dW (2 GEMMs of 2*T*N*K each)
+        Tq, Nq, Kq = 8192, 16384, 2048
+        dyq = randn((Tq, Nq), 1e-3)
+        qxq = torch.randint(-128, 128, (Tq, Kq), generator=g, device=dev, dtype=torch.int8)
+        qwq = torch.randint(-128, 128, (Nq, Kq), generator=g, device=dev, dtype=torch.int8)
+        sxq = torch.full((1,), 0.02, device=dev)
+        swq = torch.full((Nq,), 0.001, device=dev)
+        dxq = torch.empty((Tq, Kq), device=dev)
+        dwq = torch.empty((Nq, Kq), device=dev)
+        wsq = torch.empty(C.qlinear_bwd_workspace_bytes(Tq, Nq, Kq), dtype=torch.uint8, device=dev)
+        ms = _timed(torch, stream, lambda: C.qlinear_bwd(Tq, Nq, Kq, dyq, qxq, sxq, qwq, swq, dxq, dwq, wsq,
+                                                        stream=stream), 3)
+        tops = 2 * 2.0 * Tq * Nq * Kq / (ms * 1e-3) / 1e12
+        out[f"qlinear_bwd_gate_up_{Tq}x{Nq}x{Kq}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tops, 1),
+                                                     "unit": "TOP/s", "peak": PEAK_INT8_MFMA,
+                                                     "frac": round(tops / PEAK_INT8_MFMA, 4)}
+        del dyq, qxq, qwq, dxq, dwq, wsq
+        wq = randn((16384, 2048), 0.02, torch.bfloat16)
+        swq = torch.empty(16384, dtype=torch.float32, device=dev)
+        ms = _timed(torch, stream, lambda: C.quant_scales(16384, 2048, wq, swq, stream=stream), 10)
+        out["quant_scales_16384x2048"] = _hbm(ms, 16384 * 2048 * 2 + 16384 * 4)
+        qq = torch.empty((16384, 2048), dtype=torch.int8, device=dev)
+        ms = _timed(torch, stream, lambda: C.quantize(16384, 2048, wq, swq, True, qq, stream=stream), 10)
+        out["quantize_16384x2048_bf16"] = _hbm(ms, 16384 * 2048 * 3 + 16384 * 4)
+        del wq, swq, qq
 
-    logits = randn((T, V), std=2.0, dtype=torch.bfloat16)
-    tgt = torch.randint(0, V, (T,), generator=g, device=dev, dtype=torch.int32)
-    dl = torch.empty((T, V), dtype=torch.bfloat16, device=dev)
-    rl = torch.empty(T, dtype=torch.float32, device=dev)
-    ml = torch.empty(1, dtype=torch.float32, device=dev)
-    ms = _timed(torch, stream, lambda: C.softmax_xent(C.XENT, T, V, logits, dl, targets=tgt, inv_tokens=1.0 / T,
-                                                     row_loss=rl, mean_loss=ml, stream=stream), 10)
-    out[f"xent_{T}x{V}"] = _hbm(ms, T * V * 4 + T * 8)
-    del logits, tgt, dl, rl, ml
+    if want("rows"):
+        T, d = MB * S, D
+        x = randn((T, d))
+        gain = torch.full((d,), 0x3F80, dtype=torch.int16, device=dev)
+        y = torch.empty((T, d), dtype=torch.int16, device=dev)
+        rstd = torch.empty(T, dtype=torch.float32, device=dev)
+        ms = _timed(torch, stream, lambda: C.rownorm(C.FWD, T, d, x, gain, 1e-5, y=y, rstd=rstd, stream=stream), 20)
+        out[f"rownorm_fwd_{T}x{d}"] = _hbm(ms, T * d * (4 + 2) + T * 4 + d * 2)
+        dy, dx = randn((T, d)), torch.empty((T, d), dtype=torch.float32, device=dev)
+        dgain = torch.empty(d, dtype=torch.float32, device=dev)
+        ms = _timed(torch, stream, lambda: C.rownorm(C.BWD, T, d, x, gain, 1e-5, rstd=rstd, dy=dy, dx=dx, dgain=dgain,
+                                                    stream=stream), 20)
+        out[f"rownorm_bwd_{T}x{d}"] = _hbm(ms, T * d * 12 + T * 4 + d * 6)
+        del x, y, rstd, dy, dx, dgain
 
-    n = 1_200_000_000
-    grads = [randn((n,), std=1e-3) for _ in range(8)]
-    gsum = torch.empty(n, dtype=torch.float32, device=dev)
-    ms = _timed(torch, stream, lambda: C.grad_accum(C.DPPlan(1, 8, 1), n, grads, gsum, stream=stream), 3)
-    out["grad_accum_8x1.2e9"] = _hbm(ms, 9 * n * 4)
-    del grads
-    torch.cuda.empty_cache()
-    p = randn((n,), std=0.02, dtype=torch.bfloat16)
-    m1 = torch.zeros(n, dtype=torch.float32, device=dev)
-    v1 = torch.zeros(n, dtype=torch.float32, device=dev)
-    consts = C.AdamWConsts(*I.adamw_constants())
-    ms = _timed(torch, stream, lambda: C.adamw([p], [m1], [v1], [gsum], [1], consts, stream=stream), 3)
-    out["adamw_1.2e9"] = _hbm(ms, n * 24)
-    del p, m1, v1
-    # R15 over the whole 1B gradient in one flat buffer (the step's launch): the norm alone (clip not
-    # engaged: 4 bytes read per element), then norm + in-place clip (engaged: 12 bytes per element)
-    P = sum(int(np.prod(sh)) for _, sh, _, _ in I.model_param_shapes(L, D, F, V))
-    gflat = randn((P,), std=1e-3)
-    nrm = torch.empty(1, dtype=torch.float32, device=dev)
-    cws = torch.empty(C.clip_grad_norm_workspace_bytes([gflat]), dtype=torch.uint8, device=dev)
-    off = C.make_clip(float(np.float32(1e30)), float("inf"), 0, nrm)
-    ms = _timed(torch, stream, lambda: C.clip_grad_norm([gflat], off, cws, stream=stream), 5)
-    out[f"global_norm_{P}"] = _hbm(ms, 4 * P)
-    on = C.make_clip(1e-30, float("inf"), 0, nrm)  # coef < 1 every call: the clip pass runs each time
-    ms = _timed(torch, stream, lambda: C.clip_grad_norm([gflat], on, cws, stream=stream), 3)
-    out[f"global_norm_and_clip_{P}"] = _hbm(ms, 12 * P)
-    del gflat, gsum, cws
-    torch.cuda.empty_cache()
+        bh = 16
+        raw = randn((bh, S, S))
+        probs = torch.empty((bh, S, S), dtype=torch.int16, device=dev)
+        scale = float(np.float32(1 / np.sqrt(128)))
+        ms = _timed(torch, stream, lambda: C.softmax_xent(C.SOFTMAX_CAUSAL, bh * S, S, raw, probs, scale=scale,
+                                                         stream=stream), 10)
+        out[f"softmax_causal_{bh}x{S}x{S}"] = _hbm(ms, bh * (S * (S + 1) // 2) * 4 + bh * S * S * 2)
+        del raw, probs
 
-    cfg = C.ModelCfg(1, D, H, HD, F, V, S, 1, np.float32(1e-5))
-    xb, dyb = randn((S, D)), randn((S, D)).to(torch.bfloat16).float()
-    w = [torch.full((D,), 0x3F80, dtype=torch.int16, device=dev), randn((3 * D, D), 0.02, torch.bfloat16),
-         randn((D, D), 0.02, torch.bfloat16), torch.full((D,), 0x3F80, dtype=torch.int16, device=dev),
-         randn((2 * F, D), 0.02, torch.bfloat16), randn((D, F), 0.02, torch.bfloat16)]
-    dw = [torch.empty(t.shape, dtype=torch.float32, device=dev) for t in w]
-    cos, sin = I.rope_tables(S, HD)
-    cos, sin = torch.from_numpy(cos).to(dev), torch.from_numpy(sin).to(dev)
-    yb, dxb = torch.empty_like(xb), torch.empty_like(xb)
-    wsb = torch.empty(C.block_workspace_bytes(cfg, 1), dtype=torch.uint8, device=dev)
-    ms = _timed(torch, stream, lambda: C.block_fwd_bwd(cfg, 1, xb, dyb, w, cos, sin, yb, dxb, dw, wsb,
-                                                      stream=stream), 3)
-    fl = step_flops(L=1, mb=1, ranks=1) - 3 * 2 * S * D * V  # one block, no head
-    out[f"block_fwd_bwd_seq{S}"] = {"bound": "mfma", "ms": round(ms, 3), "achieved": round(fl / (ms * 1e-3) / 1e12, 2),
-                                    "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
-                                    "frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA, 4)}
-    del xb, dyb, w, dw, yb, dxb, wsb
-    torch.cuda.empty_cache()
-    out.update(int8_attention(C, torch, stream, dev, randn))
-    out.update(open1b_step(C, I, torch, np, stream, dev))
-    out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
-    out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True, int8_linear=True))
+        logits = randn((T, V), std=2.0, dtype=torch.bfloat16)
+        tgt = torch.randint(0, V, (T,), generator=g, device=dev, dtype=torch.int32)
+        dl = torch.empty((T, V), dtype=torch.bfloat16, device=dev)
+        rl = torch.empty(T, dtype=torch.float32, device=dev)
+        ml = torch.empty(1, dtype=torch.float32, device=dev)
+        ms = _timed(torch, stream, lambda: C.softmax_xent(C.XENT, T, V, logits, dl, targets=tgt, inv_tokens=1.0 / T,
+                                                         row_loss=rl, mean_loss=ml, stream=stream), 10)
+        out[f"xent_{T}x{V}"] = _hbm(ms, T * V * 4 + T * 8)
+        del logits, tgt, dl, rl, ml
+
+    if want("embed"):
+        # R11 embedding backward of one 1B microbatch (8192 tokens, d 2048, vocabulary 50304): bound by writing
+        # the +0 rows of dE and reading dx once
+        Te, Ve = MB * S, V
+        tok = torch.randint(0, Ve, (Te,), generator=g, device=dev, dtype=torch.int32)
+        dxe = randn((Te, D), 1e-3)
+        dE = torch.empty((Ve, D), dtype=torch.float32, device=dev)
+        wse = torch.empty(C.embed_bwd_workspace_bytes(Te, D), dtype=torch.uint8, device=dev)
+        ms = _timed(torch, stream, lambda: C.embed_bwd(Te, Ve, D, tok, dxe, dE, wse, stream=stream), 10)
+        out[f"embed_bwd_{Te}x{D}_v{Ve}"] = _hbm(ms, Te * D * 4 + Ve * D * 4 + Te * 4)
+        del tok, dxe, dE, wse
+
+    if want("plan"):
+        n = 1_200_000_000
+        grads = [randn((n,), std=1e-3) for _ in range(8)]
+        gsum = torch.empty(n, dtype=torch.float32, device=dev)
+        ms = _timed(torch, stream, lambda: C.grad_accum(C.DPPlan(1, 8, 1), n, grads, gsum, stream=stream), 3)
+        out["grad_accum_8x1.2e9"] = _hbm(ms, 9 * n * 4)
+        del grads
+        torch.cuda.empty_cache()
+        p = randn((n,), std=0.02, dtype=torch.bfloat16)
+        m1 = torch.zeros(n, dtype=torch.float32, device=dev)
+        v1 = torch.zeros(n, dtype=torch.float32, device=dev)
+        consts = C.AdamWConsts(*I.adamw_constants())
+        ms = _timed(torch, stream, lambda: C.adamw([p], [m1], [v1], [gsum], [1], consts, stream=stream), 3)
+        out["adamw_1.2e9"] = _hbm(ms, n * 24)
+        del p, m1, v1
+        # R15 over the whole 1B gradient in one flat buffer (the step's launch): the norm alone (clip not
+        # engaged: 4 bytes read per element), then norm + in-place clip (engaged: 12 bytes per element)
+        P = sum(int(np.prod(sh)) for _, sh, _, _ in I.model_param_shapes(L, D, F, V))
+        gflat = randn((P,), std=1e-3)
+        nrm = torch.empty(1, dtype=torch.float32, device=dev)
+        cws = torch.empty(C.clip_grad_norm_workspace_bytes([gflat]), dtype=torch.uint8, device=dev)
+        off = C.make_clip(float(np.float32(1e30)), float("inf"), 0, nrm)
+        ms = _timed(torch, stream, lambda: C.clip_grad_norm([gflat], off, cws, stream=stream), 5)
+        out[f"global_norm_{P}"] = _hbm(ms, 4 * P)
+        on = C.make_clip(1e-30, float("inf"), 0, nrm)  # coef < 1 every call: the clip pass runs each time
+        ms = _timed(torch, stream, lambda: C.clip_grad_norm([gflat], on, cws, stream=stream), 3)
+        out[f"global_norm_and_clip_{P}"] = _hbm(ms, 12 * P)
+        del gflat, gsum, cws
+        torch.cuda.empty_cache()
+
+    if want("block"):
+        cfg = C.ModelCfg(1, D, H, HD, F, V, S, 1, np.float32(1e-5))
+        xb, dyb = randn((S, D)), randn((S, D)).to(torch.bfloat16).float()
+        w = [torch.full((D,), 0x3F80, dtype=torch.int16, device=dev), randn((3 * D, D), 0.02, torch.bfloat16),
+             randn((D, D), 0.02, torch.bfloat16), torch.full((D,), 0x3F80, dtype=torch.int16, device=dev),
+             randn((2 * F, D), 0.02, torch.bfloat16), randn((D, F), 0.02, torch.bfloat16)]
+        dw = [torch.empty(t.shape, dtype=torch.float32, device=dev) for t in w]
+        cos, sin = I.rope_tables(S, HD)
+        cos, sin = torch.from_numpy(cos).to(dev), torch.from_numpy(sin).to(dev)
+        yb, dxb = torch.empty_like(xb), torch.empty_like(xb)
+        wsb = torch.empty(C.block_workspace_bytes(cfg, 1), dtype=torch.uint8, device=dev)
+        ms = _timed(torch, stream, lambda: C.block_fwd_bwd(cfg, 1, xb, dyb, w, cos, sin, yb, dxb, dw, wsb,
+                                                          stream=stream), 3)
+        fl = step_flops(L=1, mb=1, ranks=1) - 3 * 2 * S * D * V  # one block, no head
+        out[f"block_fwd_bwd_seq{S}"] = {"bound": "mfma", "ms": round(ms, 3), "achieved": round(fl / (ms * 1e-3) / 1e12, 2),
+                                        "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
+                                        "frac": round(fl / (ms * 1e-3) / 1e12 / PEAK_FP32_MFMA, 4)}
+        del xb, dyb, w, dw, yb, dxb, wsb
+        torch.cuda.empty_cache()
+    if want("attn_i8"):
+        out.update(int8_attention(C, torch, stream, dev, randn))
+    if want("open1b"):
+        out.update(open1b_step(C, I, torch, np, stream, dev))
+        out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
+        out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True, int8_linear=True))
     for k_, v_ in out.items():
         frac = f"{100 * v_['frac']:.1f}%" if v_.get("frac") is not None else "no single roofline"
         print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({frac})",
@@ -404,6 +430,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gemm-reps", type=int, default=10)
     ap.add_argument("--no-kernel-table", action="store_true")
+    ap.add_argument("--kernels", default=",".join(KERNEL_GROUPS),
+                    help="comma-separated groups of the kernel table: " + ",".join(KERNEL_GROUPS))
+    ap.add_argument("--no-step", action="store_true",
+                    help="time only the kernel table (no step replays, no dominant-GEMM launches); prints its JSON")
     ap.add_argument("--open1b-only", action="store_true",
                     help="time only the paper-architecture step (all variants; without and with the int8 "
                          "attention kernels; the int8 production configuration) and print its entries")
@@ -423,6 +453,10 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
+    groups = tuple(x for x in args.kernels.split(",") if x)
+    if args.no_step:
+        print(json.dumps({"kernels": kernel_table(C, I, torch, np, stream, dev, groups)}), flush=True)
+        return
     if args.open1b_only:
         res = open1b_step(C, I, torch, np, stream, dev)
         res.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
@@ -533,7 +567,7 @@ def main():
 
     del ws, p0, hws
     torch.cuda.empty_cache()
-    kernels = {} if args.no_kernel_table else kernel_table(C, I, torch, np, stream, dev)
+    kernels = {} if args.no_kernel_table else kernel_table(C, I, torch, np, stream, dev, groups)
     if not args.no_kernel_table:
         # the canonical state hash of the post-step state (parameters, both moments): 1,279,854,592 x 10 bytes
         hws = torch.empty(C.state_hash_workspace_bytes(state), dtype=torch.uint8, device=dev)

@@ -110,10 +110,20 @@ typedef struct {
    are combined by Algorithm 2 (binary carry, leftover blocks smallest first).  A(i,k) = a[i*lda + k]
    (trans_a = 0) or a[k*lda + i] (trans_a = 1); B(k,j) = b[k*ldb + j] (trans_b = 0) or b[j*ldb + k]
    (trans_b = 1); C row-major with leading dimension ldc >= n.  k = 0 writes +0; m = 0 or n = 0 is a
-   no-op.  Operands must not alias C. */
+   no-op.  Operands must not alias C.
+   epilogue: NULL or kind CANON_EPI_NONE writes C = d (the canonical sum d above).  kind CANON_EPI_ACCUM_PLAN
+   (Algorithm 1's microbatch accumulation, with every average a multiply by a reciprocal as the appendix on
+   deterministic gradient reduction states it): C = RN(C + RN(d * scale)), C read and written in place; with
+   C cleared to +0 before the first microbatch and scale = RN32(1/accum), accum calls leave C = g_r of the
+   plan (R7).  Another kind returns CANON_EINVAL. */
+enum { CANON_EPI_NONE = 0, CANON_EPI_ACCUM_PLAN = 1 };
+typedef struct {
+  int32_t kind;
+  float scale;
+} canon_gemm_epilogue;
 canon_status canon_gemm(const canon_order* order, int32_t trans_a, int32_t trans_b, int64_t m, int64_t n,
                         int64_t k, const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, float* c,
-                        int64_t ldc, void* stream);
+                        int64_t ldc, const canon_gemm_epilogue* epilogue, void* stream);
 
 /* Strided batched form: matrix z of the batch uses a + z*stride_a, b + z*stride_b, c + z*stride_c
    (strides in elements). */

@@ -70,7 +70,7 @@ def _lib():
         lib = ctypes.CDLL(LIB_PATH)
         vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
         sigs = {
-            "canon_gemm": (i32, [vp, i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp]),
+            "canon_gemm": (i32, [vp, i32, i32, i64, i64, i64, vp, i64, vp, i64, vp, i64, vp, vp]),
             "canon_gemm_strided_batched": (i32, [vp, i32, i32, i64, i64, i64, vp, i64, i64, vp, i64, i64, vp, i64,
                                                  i64, i64, vp]),
             "canon_rownorm": (i32, [vp, i32, i64, i64, vp, vp, f32, vp, vp, vp, vp, vp, vp]),
@@ -139,9 +139,18 @@ def _stream(stream=None) -> int:
 
 # ---- entry points (same names as the C ABI, without the prefix) -------------------------------------
 
-def gemm(m, n, k, a, lda, b, ldb, c, ldc, trans_a=0, trans_b=0, order=ORDER_V1, stream=None):
+EPI_NONE, EPI_ACCUM_PLAN = 0, 1
+
+
+class GemmEpilogue(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+def gemm(m, n, k, a, lda, b, ldb, c, ldc, trans_a=0, trans_b=0, order=ORDER_V1, stream=None, accum_scale=None):
+    """C = A B, or with accum_scale the plan's accumulation C = RN(C + RN(A B * accum_scale))."""
+    epi = None if accum_scale is None else ctypes.byref(GemmEpilogue(EPI_ACCUM_PLAN, accum_scale))
     _check(_lib().canon_gemm(ctypes.byref(order), int(trans_a), int(trans_b), m, n, k, _ptr(a), lda, _ptr(b), ldb,
-                             _ptr(c), ldc, _stream(stream)), "canon_gemm")
+                             _ptr(c), ldc, epi, _stream(stream)), "canon_gemm")
 
 
 def gemm_strided_batched(m, n, k, a, lda, stride_a, b, ldb, stride_b, c, ldc, stride_c, batch, trans_a=0, trans_b=0,

@@ -560,14 +560,20 @@ struct PlanRun {
   }
   // microbatch k of rank r produced `grad` (may be overwritten when accum == 1)
   hipError_t microbatch(int r, int k, float* grad, hipStream_t s) {
-    float* gr = g_r ? g_r : grad;
-    hipError_t e = plan_accum_launch(n, grad, inv_accum, g_r ? (k == 0) : 1, gr, s);
-    if (e != hipSuccess || k != p.accum - 1) return e;
     const int shard = r % p.dp_shard;
-    if (shard == 0) inner = take();
-    e = plan_shard_launch(n, gr, shard == 0, inner, s);
-    if (e != hipSuccess || shard != p.dp_shard - 1) return e;
-    e = plan_scale_launch(n, inner, inv_shard, inner, s);
+    hipError_t e = hipSuccess;
+    if (!g_r) {  // one microbatch per rank: its sum, the shard sum and the last shard's scale in one pass
+      if (shard == 0) inner = take();
+      e = plan_rank_launch(n, grad, inv_accum, shard == 0, shard == p.dp_shard - 1, inv_shard, inner, s);
+      if (e != hipSuccess || shard != p.dp_shard - 1) return e;
+    } else {
+      e = plan_accum_launch(n, grad, inv_accum, k == 0, g_r, s);
+      if (e != hipSuccess || k != p.accum - 1) return e;
+      if (shard == 0) inner = take();
+      e = plan_shard_launch(n, g_r, shard == 0, inner, s);
+      if (e != hipSuccess || shard != p.dp_shard - 1) return e;
+      e = plan_scale_launch(n, inner, inv_shard, inner, s);
+    }
     int level = 0;
     float* part = inner;
     while (e == hipSuccess && !stack.empty() && stack.back().first == level) {
@@ -630,8 +636,22 @@ canon_status canon_gemm_strided_batched(const canon_order* order, int32_t trans_
 
 canon_status canon_gemm(const canon_order* order, int32_t trans_a, int32_t trans_b, int64_t m, int64_t n, int64_t k,
                         const uint16_t* a, int64_t lda, const uint16_t* b, int64_t ldb, float* c, int64_t ldc,
-                        void* stream) {
-  return canon_gemm_strided_batched(order, trans_a, trans_b, m, n, k, a, lda, 0, b, ldb, 0, c, ldc, 0, 1, stream);
+                        const canon_gemm_epilogue* epilogue, void* stream) {
+  if (!epilogue || epilogue->kind == CANON_EPI_NONE)
+    return canon_gemm_strided_batched(order, trans_a, trans_b, m, n, k, a, lda, 0, b, ldb, 0, c, ldc, 0, 1, stream);
+  if (epilogue->kind != CANON_EPI_ACCUM_PLAN) return CANON_EINVAL;
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (m < 0 || n < 0 || k < 0) return CANON_EINVAL;
+  if (m == 0 || n == 0) return CANON_OK;
+  if (!c || (k > 0 && (!a || !b))) return CANON_EINVAL;
+  if (lda < (trans_a ? m : k) || ldb < (trans_b ? k : n) || ldc < n || lda < 1 || ldb < 1) return CANON_EINVAL;
+  if (!gemm_k_supported(k)) return CANON_EUNSUPPORTED;
+  if (((m + 63) / 64) * ((n + 127) / 128) > 0x7FFFFFFF) return CANON_EUNSUPPORTED;
+  GemmArgs g = mk(trans_a ? 1 : 0, trans_b ? 1 : 0, m, n, k, a, lda, b, ldb, c, ldc);
+  g.epi = EPI_ACCUM;
+  g.epi_scale = epilogue->scale;
+  return dev(gemm_launch(g, as_stream(stream)));
 }
 
 canon_status canon_rownorm(const canon_order* order, int32_t dir, int64_t rows, int64_t cols, const float* x,

@@ -33,8 +33,9 @@ struct GemmArgs {
   float ds_scale;
   int64_t ds_ldp, ds_sp1, ds_sp2, ds_sd1, ds_sd2;
   int64_t ds_window;
+  float epi_scale;  // EPI_ACCUM
 };
-enum { EPI_NONE = 0, EPI_DS = 1 };
+enum { EPI_NONE = 0, EPI_DS = 1, EPI_ACCUM = 2 };  // EPI_ACCUM: C = RN(C + RN(d * epi_scale)) (fp32 C)
 
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);
 
@@ -152,6 +153,10 @@ hipError_t grad_accum_fused_launch(int accum, int dp_shard, int dp_replicate, in
                                    float* out, hipStream_t s);
 // out = (first ? +0 : out) + RN(grad * inv)        (Algorithm 1, microbatch accumulation)
 hipError_t plan_accum_launch(int64_t n, const float* grad, float inv, int first, float* out, hipStream_t s);
+// accum = 1: a rank's gradient into the ascending shard sum inner (first: shard 0), scaled by inv_shard on the
+// last shard, in one pass
+hipError_t plan_rank_launch(int64_t n, const float* grad, float inv_accum, int first, int last, float inv_shard,
+                            float* inner, hipStream_t s);
 // out = first ? a : RN(out + a)                      (ascending shard sum)
 hipError_t plan_shard_launch(int64_t n, const float* a, int first, float* out, hipStream_t s);
 // out = RN(lower + out)                              (fold merge, lower block on the left)

@@ -466,6 +466,20 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     }
     return;
   }
+  if (g.epi == EPI_ACCUM) {  // the plan's microbatch accumulation g = RN(g + RN(d * s)) into the fp32 C
+    float* C = (float*)g.c + z1 * g.sc1 + z2 * g.sc2;
+#pragma unroll
+    for (int v = 0; v < 32; ++v) {
+      const int vv = v & 15, blk = v >> 4;
+      const int64_t i = crow0 + (vv & 3) + 4 * (lane >> 5) + 8 * (vv >> 2);
+      const int64_t j = ccol0 + blk * 32 + (lane & 31);
+      if (i < g.m && j < g.n) {
+        const float t = r[v] * g.epi_scale;
+        C[i * g.ldc + j] = C[i * g.ldc + j] + t;
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int v = 0; v < 32; ++v) {
     const int vv = v & 15, blk = v >> 4;
@@ -761,7 +775,7 @@ hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
   int bits = 0;
   while ((int64_t(1) << bits) <= nc) ++bits;  // nc < 2^bits: a push never runs past the top level
   const int64_t tiles = ((g.m + BM - 1) / BM) * ((g.n + BN - 1) / BN);
-  if (!g.trans_a && g.trans_b && nc >= 1 && nc <= 4 && g.kmode == KMODE_FULL && g.kseg == 0 &&
+  if (!g.trans_a && g.trans_b && nc >= 1 && nc <= 4 && g.kmode == KMODE_FULL && g.kseg == 0 && g.epi != EPI_ACCUM &&
       BM * g.ldc < (int64_t(1) << 31) && BM * g.ds_ldp < (int64_t(1) << 31) && tiles * g.batch < (int64_t(1) << 31) &&
       g.nb2 > 0 && g.batch % g.nb2 == 0)
     return launch_short(g, nc, tiles * g.batch, s);

@@ -204,6 +204,52 @@ __global__ void plan_scale_kernel(int64_t n, const float* x, float inv, float* o
     out[i] = x[i] * inv;
 }
 
+// With one microbatch per rank (accum = 1) the rank's sum g_r = RN(+0 + RN(grad * inv_accum)) goes straight
+// into the ascending shard sum: inner = g_r on shard 0, RN(inner + g_r) after; on the last shard the result is
+// also scaled, RN(inner * inv_shard).  The same operations as plan_accum, plan_shard and plan_scale in turn,
+// in one pass over the gradient (16-byte accesses when n % 4 == 0 and both buffers are aligned).
+template <bool VEC>
+__global__ __launch_bounds__(256) void plan_rank_kernel(int64_t n, const float* __restrict__ grad, float inv_accum,
+                                                        int first, int last, float inv_shard, float* __restrict__ inner) {
+  auto one = [&](float gv, float iv) -> float {
+    const float t = gv * inv_accum;
+    const float gr = 0.0f + t;
+    float v = first ? gr : iv + gr;
+    if (last) v = v * inv_shard;
+    return v;
+  };
+  if (VEC) {
+    const int64_t n4 = n >> 2;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4; i += (int64_t)gridDim.x * 256) {
+      const float4 gv = reinterpret_cast<const float4*>(grad)[i];
+      float4 iv = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (!first) iv = reinterpret_cast<const float4*>(inner)[i];
+      float4 o;
+      o.x = one(gv.x, iv.x);
+      o.y = one(gv.y, iv.y);
+      o.z = one(gv.z, iv.z);
+      o.w = one(gv.w, iv.w);
+      reinterpret_cast<float4*>(inner)[i] = o;
+    }
+  } else {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256)
+      inner[i] = one(grad[i], first ? 0.0f : inner[i]);
+  }
+}
+
+hipError_t plan_rank_launch(int64_t n, const float* grad, float inv_accum, int first, int last, float inv_shard,
+                            float* inner, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const bool vec = n % 4 == 0 && ((uintptr_t)grad & 15) == 0 && ((uintptr_t)inner & 15) == 0;
+  if (vec)
+    hipLaunchKernelGGL(plan_rank_kernel<true>, dim3(grid_for(n / 4)), dim3(256), 0, s, n, grad, inv_accum, first, last,
+                       inv_shard, inner);
+  else
+    hipLaunchKernelGGL(plan_rank_kernel<false>, dim3(grid_for(n)), dim3(256), 0, s, n, grad, inv_accum, first, last,
+                       inv_shard, inner);
+  return hipGetLastError();
+}
+
 hipError_t plan_accum_launch(int64_t n, const float* grad, float inv, int first, float* out, hipStream_t s) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(plan_accum_kernel, dim3(grid_for(n)), dim3(256), 0, s, n, grad, inv, first, out);

@@ -61,7 +61,10 @@ def test_host_validation_rejects_before_any_launch():
                              None) != C.OK
     assert lib.canon_rownorm(order, 7, rows, cols, x, gain, 1e-5, dx, rstd, None, None, None, None) == C.EINVAL
     # GEMM with negative sizes, softmax with rows not a multiple of cols
-    assert lib.canon_gemm(order, 0, 0, -1, 4, 4, x, 4, dy, 4, dx, 4, None) == C.EINVAL
+    assert lib.canon_gemm(order, 0, 0, -1, 4, 4, x, 4, dy, 4, dx, 4, None, None) == C.EINVAL
+    # an unknown GEMM epilogue kind
+    bad_epi = C.GemmEpilogue(7, 1.0)
+    assert lib.canon_gemm(order, 0, 0, 4, 4, 4, x, 4, dy, 4, dx, 4, ctypes.byref(bad_epi), None) == C.EINVAL
     assert lib.canon_softmax_xent(order, C.SOFTMAX_CAUSAL, 10, 4, x, 1.0, 0, None, 1.0, 0.0, dx, None, None,
                                   None) == C.EINVAL
     # a negative window or z-loss weight

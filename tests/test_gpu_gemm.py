@@ -64,6 +64,25 @@ def test_whole_tiles_every_depth(k, ta, tb):
     assert_bits(gpu_gemm(a, b, ta, tb, m, n, k), oracle.gemm(a, b, bool(ta), bool(tb)), f"k={k}")
 
 
+@pytest.mark.parametrize("ta,tb", [(0, 1), (1, 0)])
+@pytest.mark.parametrize("m,n,k,accum", [(130, 260, 192, 3), (128, 256, 2048, 2), (64, 128, 32, 4), (70, 90, 8192, 1)])
+def test_accum_plan_epilogue(m, n, k, accum, ta, tb):
+    """canon_gemm's ACCUM_PLAN epilogue over `accum` microbatches, C cleared to +0 first, against the oracle's
+    plan on the oracle's GEMMs: g_r = R7's ascending sum of RN(grad * RN(1/accum)) (one rank: the plan's
+    result is g_r itself)."""
+    print(f"gemm accum-plan {m}x{n}x{k} accum={accum} ta={ta} tb={tb}", flush=True)
+    c = torch.zeros((m, n), dtype=torch.float32, device=DEV)
+    inv = float(np.float32(1.0 / accum))
+    grads = []
+    for j in range(accum):
+        a, b = operands(m, n, k, ta, tb, 20 + j)
+        C.gemm(m, n, k, dev_bf16(a), a.shape[1], dev_bf16(b), b.shape[1], c, n, ta, tb, accum_scale=inv)
+        grads.append(oracle.gemm(a, b, bool(ta), bool(tb)))
+    torch.cuda.synchronize()
+    want = oracle.grad_accum([g.reshape(-1) for g in grads], accum, 1, 1).reshape(m, n)
+    assert_bits(host_f32(c), want, f"accum {m}x{n}x{k}")
+
+
 def test_k_zero_and_empty():
     c = torch.full((4, 5), float("nan"), dtype=torch.float32, device=DEV)
     a = torch.zeros(4, 1, dtype=torch.bfloat16, device=DEV)
