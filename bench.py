@@ -26,7 +26,8 @@ PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s
 PEAK_INT8_MFMA = 5000.0  # TOP/s, MI355X dense int8 matrix
-PEAK_VALU_OPS = 39.3     # T lane-operations/s: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (fp32 or fp64 FMA issue rate)
+PEAK_VALU_OPS = 78.6     # T lane-operations/s: 256 CUs x 4 SIMDs x 32 lanes x 2.4 GHz (the fp32 vector rate, 157.3
+                         # TFLOP/s counting an FMA as 2; counters show kernels issuing above a 16-lane rate)
 SHA_BLOCK_VALU = 1698    # VALU instructions of one SHA-256 compression in hash_leaves_kernel's block loop (gfx950 ISA)
 
 L, D, H, HD, F, V, S, MB = 16, 2048, 16, 128, 8192, 50304, 2048, 4
@@ -126,7 +127,17 @@ def kernel_table(C, I, torch, np, stream, dev, groups=KERNEL_GROUPS):
     def randn(shape, std=1.0, dtype=torch.float32):
         return (torch.randn(shape, generator=g, device=dev, dtype=torch.float32) * std).to(dtype)
 
-    out = {}
+    class Entries(dict):  # each entry is printed when it is measured (a long table shows its progress)
+        def __setitem__(self, k_, v_):
+            super().__setitem__(k_, v_)
+            frac = f"{100 * v_['frac']:.1f}%" if v_.get("frac") is not None else "no single roofline"
+            print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({frac})", file=sys.stderr, flush=True)
+
+        def update(self, other):
+            for k_, v_ in other.items():
+                self[k_] = v_
+
+    out = Entries()
     print("bench: kernel table", file=sys.stderr, flush=True)
 
     def want(group):
@@ -290,11 +301,7 @@ def kernel_table(C, I, torch, np, stream, dev, groups=KERNEL_GROUPS):
         out.update(open1b_step(C, I, torch, np, stream, dev))
         out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True))
         out.update(open1b_step(C, I, torch, np, stream, dev, int8_attn=True, int8_linear=True))
-    for k_, v_ in out.items():
-        frac = f"{100 * v_['frac']:.1f}%" if v_.get("frac") is not None else "no single roofline"
-        print(f"bench:   {k_}: {v_['ms']} ms, {v_['achieved']} {v_['unit']} ({frac})",
-              file=sys.stderr, flush=True)
-    return out
+    return dict(out)
 
 
 def int8_attention(C, torch, stream, dev, randn):

@@ -592,7 +592,8 @@ struct PlanRun {
     float* acc = stack.back().second;
     hipError_t e = hipSuccess;
     for (int i = (int)stack.size() - 2; i >= 0 && e == hipSuccess; --i) e = plan_merge_launch(n, stack[i].second, acc, s);
-    if (e == hipSuccess) e = plan_scale_launch(n, acc, inv_rep, acc, s);
+    // RN(x * 1) = x for every x the sums can hold (never subnormal): one replica needs no pass
+    if (e == hipSuccess && inv_rep != 1.0f) e = plan_scale_launch(n, acc, inv_rep, acc, s);
     *err = e;
     return acc;
   }
