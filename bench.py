@@ -433,6 +433,8 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--hash-steps", type=int, default=1,
+                    help="steps timed again with the per-step audit hash inside canon_step (0: skip)")
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--gemm-reps", type=int, default=10)
@@ -539,6 +541,31 @@ def main():
     flops = step_flops()
     value = flops / (ms * 1e-3) / 1e12
 
+    # the paper's hash-on / hash-off comparison: the same step with the per-step audit hash (H1 of the
+    # windows, parameters, m, v and reduced gradient, 17.9 GB) computed inside canon_step
+    audit = None
+    if args.hash_steps > 0:
+        sdig = torch.zeros(32, dtype=torch.uint8, device=dev)
+
+        def one_step_hashed():
+            restore()
+            C.step(cfg, plan, pg, mg, vg, windows, cos, sin, consts, ws, loss, stream=stream, clip=clip,
+                   state_digest=sdig)
+        one_step_hashed()
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        for i in range(args.hash_steps):
+            one_step_hashed()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        ms_h = ev0.elapsed_time(ev1) / args.hash_steps
+        audit = {"steps": args.hash_steps, "ms_per_step_hash_on": round(ms_h, 2), "ms_per_step_hash_off": round(ms, 2),
+                 "overhead_pct": round(100 * (ms_h - ms) / ms, 3),
+                 "step_state_digest": bytes(sdig.cpu().numpy().tobytes()).hex(),
+                 "params_m_v_digest_unchanged": state_digest() == first_digest}
+        print(f"bench: hash on {ms_h / 1000:.3f} s/step ({audit['overhead_pct']:.2f}% over hash off); step digest "
+              f"{audit['step_state_digest'][:16]}..", file=sys.stderr, flush=True)
+
     # dominant kernel: the canonical GEMM at the fused gate/up shape (8192 x 16384 x 2048), timed per launch
     gm, gn, gk = MB * S, 2 * F, D
     a = torch.from_numpy(I.normal_bf16((gm, gk), 0, I.TENSOR_IDS["gemm_a"]).view(np.int16)).to(dev)
@@ -632,6 +659,7 @@ def main():
                    "note": "each replay restores the initial parameters and zero moments (inside the timed "
                            "region) and recomputes step t = 1; the digest is the canonical state hash (H1) of "
                            "the post-AdamW parameters and both moments"},
+        "audit_hash": audit,
         "kernels": kernels,
     }
     print(json.dumps(out), flush=True)

@@ -175,6 +175,40 @@ canon_status canon_softmax_xent(const canon_order* order, int32_t mode, int64_t 
 canon_status canon_grad_accum(const canon_order* order, const canon_dp_plan* plan, int64_t n,
                               const float* const* grads, float* out, void* stream);
 
+/* The same plan fed one microbatch gradient at a time (Algorithm 1's loop, with Algorithm 2's stack over the
+   replicas), so that it can stop after any microbatch and resume later, in another process or in other
+   memory: the analogue of restarting a run from its last checkpoint and comparing the repeated steps'
+   hashes (the paper's training-run account).  canon_step runs its plan through this same code.
+   The whole state is a plain host record (canon_plan_cursor: the plan, n, the count of microbatches in,
+   the stack's levels and slot numbers; no pointers) plus a caller-owned device buffer of
+   canon_plan_state_bytes(plan, n) bytes (256-byte aligned) holding the partial sums in slots of n floats.
+   To persist: copy the record and the buffer's bytes; to resume: copy both back, into any buffer of that
+   size.  canon_plan_begin initialises the record (host only).  canon_plan_push takes the gradient of the
+   next microbatch in Algorithm 1's order, rank-major and microbatch-minor (rank r = next / accum,
+   microbatch k = next % accum): grad, n fp32 device values, read only.  canon_plan_finish, after all
+   N*accum pushes, writes the reduced gradient to out (n fp32, device); it leaves the buffer's contents
+   unspecified.  Both return CANON_EINVAL for a record that the calls above cannot produce (position out
+   of range, a stack shape or a shard sum that does not match the position, slots repeated or out of
+   range), a push after the last microbatch or a finish before it, and leave the record unchanged on any
+   error.  The result is bit-identical to canon_grad_accum over the same buffers, wherever the plan was
+   stopped and resumed.  dp_replicate below 2^31. */
+#define CANON_PLAN_MAX_DEPTH 31
+typedef struct {
+  canon_dp_plan plan;
+  int32_t next;                          /* microbatches pushed */
+  int64_t n;                             /* floats per gradient */
+  int32_t inner;                         /* slot of the current replica's shard sum, -1 when none */
+  int32_t depth;                         /* entries on Algorithm 2's stack */
+  int32_t level[CANON_PLAN_MAX_DEPTH];   /* level of entry i, bottom first (strictly decreasing) */
+  int32_t slot[CANON_PLAN_MAX_DEPTH];    /* slot holding entry i */
+} canon_plan_cursor;
+size_t canon_plan_state_bytes(const canon_dp_plan* plan, int64_t n);
+canon_status canon_plan_begin(const canon_dp_plan* plan, int64_t n, canon_plan_cursor* cursor);
+canon_status canon_plan_push(const canon_order* order, canon_plan_cursor* cursor, const float* grad, void* state,
+                             size_t state_bytes, void* stream);
+canon_status canon_plan_finish(const canon_order* order, canon_plan_cursor* cursor, void* state, size_t state_bytes,
+                               float* out, void* stream);
+
 /* ------------------------------------------------------------------------------------------------ */
 /* AdamW (R9): per tensor t of n_tensors (HOST arrays of device pointers and host sizes), widen the bf16
    parameter, apply decoupled decay if decay_mask[t] (host) != 0, update fp32 m and v, bias-correct by
@@ -248,12 +282,20 @@ size_t canon_block_workspace_bytes(const canon_model_cfg* cfg, int32_t batch);
    also makes *norm_out NaN and sets *skipped_out, and leaves *skip_state unchanged.  step_t: AdamW's step
    index t >= 1 (else CANON_EINVAL) that consts was computed for; the bias corrections RN32(1/(1 - beta^t))
    come in consts (evaluated by the caller in binary64 and rounded once), so the library uses t only for this
-   check; a caller that skips an update does not advance t. */
+   check; a caller that skips an update does not advance t.
+   state_digest: NULL, or device memory of 32 bytes that receives the per-step audit hash (the paper's
+   state-hash appendix: every step digests its data batch, parameters, optimizer state and gradients):
+   H1 (canon_state_hash below) over, in this order, windows (M*(seq+1) int32), the n parameters (bf16) and
+   the n tensors of m and of v (fp32) as this step leaves them, and the n tensors of the reduced gradient
+   (fp32, before any clip), each in the declared order.  The digest names the tensors, not the plan's
+   shards, so it is the same for every plan that gives the same bits.  The workspace must then be 256-byte
+   aligned (CANON_EINVAL otherwise); canon_step_workspace_bytes includes the hash's tables. */
 canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, const canon_dp_plan* plan,
                         uint16_t* const* params, float* const* m, float* const* v, int32_t step_t,
                         const int32_t* windows, const float* rope_cos, const float* rope_sin,
                         const canon_adamw_consts* consts, const canon_clip* clip, void* workspace,
-                        size_t workspace_bytes, float* loss_out, float* const* grads_out, void* stream);
+                        size_t workspace_bytes, float* loss_out, float* const* grads_out, uint8_t* state_digest,
+                        void* stream);
 size_t canon_step_workspace_bytes(const canon_model_cfg* cfg, const canon_dp_plan* plan);
 
 /* ------------------------------------------------------------------------------------------------ */

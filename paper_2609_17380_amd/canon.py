@@ -34,6 +34,16 @@ class DPPlan(ctypes.Structure):
     _fields_ = [("accum", ctypes.c_int32), ("dp_shard", ctypes.c_int32), ("dp_replicate", ctypes.c_int32)]
 
 
+PLAN_MAX_DEPTH = 31
+
+
+class PlanCursor(ctypes.Structure):
+    """The gradient plan's position and Algorithm 2 stack (plain data: bytes(cursor) persists it)."""
+    _fields_ = [("plan", DPPlan), ("next", ctypes.c_int32), ("n", ctypes.c_int64), ("inner", ctypes.c_int32),
+                ("depth", ctypes.c_int32), ("level", ctypes.c_int32 * PLAN_MAX_DEPTH),
+                ("slot", ctypes.c_int32 * PLAN_MAX_DEPTH)]
+
+
 class ModelCfg(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("d_ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
@@ -76,10 +86,14 @@ def _lib():
             "canon_rownorm": (i32, [vp, i32, i64, i64, vp, vp, f32, vp, vp, vp, vp, vp, vp]),
             "canon_softmax_xent": (i32, [vp, i32, i64, i64, vp, f32, i64, vp, f32, f32, vp, vp, vp, vp]),
             "canon_grad_accum": (i32, [vp, vp, i64, vp, vp, vp]),
+            "canon_plan_state_bytes": (sz, [vp, i64]),
+            "canon_plan_begin": (i32, [vp, i64, vp]),
+            "canon_plan_push": (i32, [vp, vp, vp, vp, sz, vp]),
+            "canon_plan_finish": (i32, [vp, vp, vp, sz, vp, vp]),
             "canon_adamw": (i32, [i64, vp, vp, vp, vp, vp, vp, vp, vp]),
             "canon_block_fwd_bwd": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
             "canon_block_workspace_bytes": (sz, [vp, i32]),
-            "canon_step": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp]),
+            "canon_step": (i32, [vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp, vp, sz, vp, vp, vp, vp]),
             "canon_clip_grad_norm": (i32, [vp, i64, vp, vp, vp, vp, sz, vp]),
             "canon_clip_grad_norm_workspace_bytes": (sz, [i64, vp]),
             "canon_step_workspace_bytes": (sz, [vp, vp]),
@@ -133,6 +147,8 @@ def _ptrs(ts):
 
 
 def _stream(stream=None) -> int:
+    if isinstance(stream, int):  # a raw hipStream_t (0: the null stream)
+        return stream
     s = stream if stream is not None else torch.cuda.current_stream()
     return s.cuda_stream
 
@@ -176,6 +192,34 @@ def softmax_xent(mode, rows, cols, x, out, scale=1.0, targets=None, inv_tokens=1
 def grad_accum(plan: DPPlan, n, grads, out, order=ORDER_V1, stream=None):
     _check(_lib().canon_grad_accum(ctypes.byref(order), ctypes.byref(plan), n, _ptrs(grads), _ptr(out),
                                    _stream(stream)), "canon_grad_accum")
+
+
+def plan_state_bytes(plan: DPPlan, n: int) -> int:
+    return int(_lib().canon_plan_state_bytes(ctypes.byref(plan), n))
+
+
+def plan_begin(plan: DPPlan, n: int) -> PlanCursor:
+    cur = PlanCursor()
+    _check(_lib().canon_plan_begin(ctypes.byref(plan), n, ctypes.byref(cur)), "canon_plan_begin")
+    return cur
+
+
+def _state_bytes(state, state_bytes):
+    if state_bytes is not None:
+        return state_bytes
+    return 0 if state is None or isinstance(state, int) else state.numel() * state.element_size()
+
+
+def plan_push(cursor: PlanCursor, grad, state, order=ORDER_V1, stream=None, state_bytes=None):
+    """Feed the next microbatch's gradient (Algorithm 1's order); updates cursor in place."""
+    _check(_lib().canon_plan_push(ctypes.byref(order), ctypes.byref(cursor), _ptr(grad), _ptr(state),
+                                  _state_bytes(state, state_bytes), _stream(stream)), "canon_plan_push")
+
+
+def plan_finish(cursor: PlanCursor, state, out, order=ORDER_V1, stream=None, state_bytes=None):
+    _check(_lib().canon_plan_finish(ctypes.byref(order), ctypes.byref(cursor), _ptr(state),
+                                    _state_bytes(state, state_bytes), _ptr(out), _stream(stream)),
+           "canon_plan_finish")
 
 
 def adamw(params, m, v, grads, decay_mask, consts: AdamWConsts, stream=None):
@@ -249,12 +293,16 @@ def step_workspace_bytes(cfg: ModelCfg, plan: DPPlan) -> int:
 
 
 def step(cfg: ModelCfg, plan: DPPlan, params, m, v, windows, rope_cos, rope_sin, consts: AdamWConsts, workspace,
-         loss_out, grads_out=None, step_t=1, order=ORDER_V1, stream=None, clip: Clip | None = None):
+         loss_out, grads_out=None, step_t=1, order=ORDER_V1, stream=None, clip: Clip | None = None,
+         state_digest=None):
+    """state_digest: None, or a 32-byte device tensor for the per-step audit hash (H1 of the windows, the
+    parameters, m and v after the step, and the reduced gradient)."""
     _check(_lib().canon_step(ctypes.byref(order), ctypes.byref(cfg), ctypes.byref(plan), _ptrs(params), _ptrs(m),
                              _ptrs(v), step_t, _ptr(windows), _ptr(rope_cos), _ptr(rope_sin), ctypes.byref(consts),
                              ctypes.byref(clip) if clip is not None else None,
                              _ptr(workspace), workspace.numel() * workspace.element_size(), _ptr(loss_out),
-                             _ptrs(grads_out) if grads_out is not None else None, _stream(stream)), "canon_step")
+                             _ptrs(grads_out) if grads_out is not None else None, _ptr(state_digest),
+                             _stream(stream)), "canon_step")
 
 
 def _sizes(tensors):

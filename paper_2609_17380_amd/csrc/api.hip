@@ -481,6 +481,15 @@ void tensor_sizes(const canon_model_cfg* c, std::vector<int64_t>& sz, std::vecto
   sz.push_back(V * d); decay.push_back(1);
 }
 
+// slots of the gradient plan (see the plan cursor below): 256-byte aligned, n floats each
+int64_t plan_slot_stride(int64_t n) { return (n + 63) & ~int64_t(63); }  // 256-byte aligned slots
+int plan_slot_count(const canon_dp_plan& p) { return (p.accum > 1 ? 1 : 0) + bit_length(p.dp_replicate) + 1; }
+bool plan_ok(const canon_dp_plan* p) {
+  return p && p->accum >= 1 && p->dp_shard >= 1 && p->dp_replicate >= 1 &&
+         (int64_t)p->accum * p->dp_shard * p->dp_replicate <= INT32_MAX;
+}
+int64_t plan_total(const canon_dp_plan& p) { return (int64_t)p.accum * p.dp_shard * p.dp_replicate; }
+
 struct StepLayout {
   std::vector<LayerSave> saves;
   std::vector<float*> xs;  // residual stream: xs[0] = embedding output, xs[l+1] = block l output
@@ -490,17 +499,31 @@ struct StepLayout {
   int32_t *win, *lab, *bad;
   void* embed_scratch;
   float* grad;            // one microbatch's gradient, all tensors
-  float* g_r;             // rank accumulator (accum > 1)
-  std::vector<float*> pool;  // inner + fold stack buffers
+  float* plan_slots;      // the gradient plan's slots (rank accumulator, shard sum, Algorithm 2 stack)
   float* loss_mb;         // [1]
-  float* loss_gr;         // [1]
-  std::vector<float*> loss_pool;
+  float* loss_slots;      // the same plan over the microbatch losses
   float* norm_part;       // R15 block sums
   float* clip_coef;       // [1]
   int32_t* skip;          // [1]: no update this step (bad token or spike window)
   float* x_emb;           // embedding norm: the gathered rows [T][d]
   float* rstd_emb;        // embedding norm: r per row [T]
+  char* hash_ws;          // the per-step state hash's tables and leaf digests
 };
+
+// the tensors of the per-step state hash: the step's windows, then the parameters, m, v and the reduced
+// gradient, each in the declared order
+void step_hash_sizes(const canon_model_cfg* c, const canon_dp_plan* p, std::vector<int64_t>& nb) {
+  std::vector<int64_t> sz;
+  std::vector<uint8_t> decay;
+  tensor_sizes(c, sz, decay);
+  const int64_t M = (int64_t)p->accum * p->dp_shard * p->dp_replicate * c->micro_seqs;
+  nb.clear();
+  nb.push_back(M * (c->seq + 1) * (int64_t)sizeof(int32_t));
+  for (int64_t x : sz) nb.push_back(2 * x);
+  for (int rep = 0; rep < 3; ++rep)
+    for (int64_t x : sz) nb.push_back(4 * x);
+}
+size_t step_hash_bytes(const canon_model_cfg* c, const canon_dp_plan* p);
 
 void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, int64_t P, StepLayout& L) {
   Dims D = dims_of(c, c->micro_seqs);
@@ -522,82 +545,200 @@ void carve_step(Carver& cv, const canon_model_cfg* c, const canon_dp_plan* p, in
   L.bad = cv.take<int32_t>(1);
   L.embed_scratch = cv.take<char>((int64_t)embed_bwd_scratch_bytes(D.T, D.d));
   L.grad = cv.take<float>(P);
-  L.g_r = p->accum > 1 ? cv.take<float>(P) : nullptr;
-  const int nbuf = bit_length(p->dp_replicate) + 1;
-  L.pool.resize(nbuf);
-  for (auto& b : L.pool) b = cv.take<float>(P);
+  L.plan_slots = cv.take<float>(plan_slot_stride(P) * plan_slot_count(*p));
   L.loss_mb = cv.take<float>(1);
-  L.loss_gr = cv.take<float>(1);
-  L.loss_pool.resize(nbuf);
-  for (auto& b : L.loss_pool) b = cv.take<float>(1);
+  L.loss_slots = cv.take<float>(plan_slot_stride(1) * plan_slot_count(*p));
   L.norm_part = cv.take<float>(gnorm_blocks(P));
   L.clip_coef = cv.take<float>(1);
   L.skip = cv.take<int32_t>(1);
   L.x_emb = c->embed_norm ? cv.take<float>(D.T * D.d) : nullptr;
   L.rstd_emb = c->embed_norm ? cv.take<float>(D.T) : nullptr;
+  L.hash_ws = cv.take<char>((int64_t)step_hash_bytes(c, p));
 }
 
-// Algorithm 1 driven from the host over device buffers of n floats (the gradient, or the loss with n = 1).
-struct PlanRun {
-  int64_t n;
-  canon_dp_plan p;
-  float inv_accum, inv_shard, inv_rep;
-  float* g_r;                   // nullptr when accum == 1 (the microbatch buffer is reused in place)
-  std::vector<float*> free_bufs;
-  std::vector<std::pair<int, float*>> stack;  // (level, buffer) of Algorithm 2
-  float* inner = nullptr;
+// Algorithm 1 driven from the host, one microbatch at a time, over device slots of n floats each (the
+// gradient, or the loss with n = 1).  The position and the Algorithm 2 stack live in a plain host record
+// (canon_plan_cursor) and the partial sums in the caller's slots, so the plan can stop after any microbatch,
+// be persisted (record + slot bytes) and resume in other memory.  Slot 0 is the rank accumulator when
+// accum > 1; the others hold the shard sum being built and the stack entries.
+void plan_cursor_init(const canon_dp_plan& p, int64_t n, canon_plan_cursor* c) {
+  memset(c, 0, sizeof(*c));
+  c->plan = p;
+  c->n = n;
+  c->next = 0;
+  c->inner = -1;
+  c->depth = 0;
+}
 
-  PlanRun(int64_t n_, const canon_dp_plan& p_, float* gr, const std::vector<float*>& pool) : n(n_), p(p_), g_r(gr) {
-    inv_accum = (float)(1.0 / p.accum);
-    inv_shard = (float)(1.0 / p.dp_shard);
-    inv_rep = (float)(1.0 / p.dp_replicate);
-    free_bufs = pool;
+// The record must be one that plan_cursor_init and plan_cursor_push can produce: its stack shape and the
+// presence of a shard sum follow from `next`, and the slots are distinct and in range.
+bool plan_cursor_valid(const canon_plan_cursor* c) {
+  if (!c || !plan_ok(&c->plan) || c->n < 0) return false;
+  const canon_dp_plan& p = c->plan;
+  const int64_t total = plan_total(p);
+  if (c->next < 0 || c->next > total) return false;
+  const int64_t r = c->next / p.accum;               // ranks whose microbatches are all in (== N at the end)
+  const int64_t groups = r / p.dp_shard;             // replica groups complete
+  const bool partial_group = (r % p.dp_shard) != 0;  // some shards of the current replica are in
+  if (partial_group != (c->inner >= 0)) return false;
+  int64_t bits = groups;
+  int depth = 0;
+  for (int L = 30; L >= 0; --L) {
+    if (!((bits >> L) & 1)) continue;
+    if (depth >= CANON_PLAN_MAX_DEPTH || c->level[depth] != L) return false;
+    ++depth;
   }
-  float* take() {
-    float* b = free_bufs.back();
-    free_bufs.pop_back();
-    return b;
+  if (depth != c->depth) return false;
+  const int first = p.accum > 1 ? 1 : 0, nslots = plan_slot_count(p);
+  uint64_t used = 0;
+  for (int i = 0; i <= depth; ++i) {
+    const int sl = i < depth ? c->slot[i] : c->inner;
+    if (i == depth && sl < 0) continue;
+    if (sl < first || sl >= nslots || ((used >> sl) & 1)) return false;
+    used |= uint64_t(1) << sl;
   }
-  // microbatch k of rank r produced `grad` (may be overwritten when accum == 1)
-  hipError_t microbatch(int r, int k, float* grad, hipStream_t s) {
-    const int shard = r % p.dp_shard;
-    hipError_t e = hipSuccess;
-    if (!g_r) {  // one microbatch per rank: its sum, the shard sum and the last shard's scale in one pass
-      if (shard == 0) inner = take();
-      e = plan_rank_launch(n, grad, inv_accum, shard == 0, shard == p.dp_shard - 1, inv_shard, inner, s);
-      if (e != hipSuccess || shard != p.dp_shard - 1) return e;
-    } else {
-      e = plan_accum_launch(n, grad, inv_accum, k == 0, g_r, s);
-      if (e != hipSuccess || k != p.accum - 1) return e;
-      if (shard == 0) inner = take();
-      e = plan_shard_launch(n, g_r, shard == 0, inner, s);
-      if (e != hipSuccess || shard != p.dp_shard - 1) return e;
-      e = plan_scale_launch(n, inner, inv_shard, inner, s);
-    }
-    int level = 0;
-    float* part = inner;
-    while (e == hipSuccess && !stack.empty() && stack.back().first == level) {
-      float* lower = stack.back().second;
-      e = plan_merge_launch(n, lower, part, s);  // part = lower + part
-      free_bufs.push_back(lower);
-      stack.pop_back();
-      ++level;
-    }
-    stack.push_back({level, part});
-    inner = nullptr;
-    return e;
+  return true;
+}
+
+int plan_take_slot(const canon_plan_cursor* c) {
+  const int first = c->plan.accum > 1 ? 1 : 0, nslots = plan_slot_count(c->plan);
+  for (int sl = first; sl < nslots; ++sl) {
+    bool busy = sl == c->inner;
+    for (int i = 0; i < c->depth; ++i) busy = busy || c->slot[i] == sl;
+    if (!busy) return sl;
   }
-  // Result of Algorithm 2 times 1/dp_replicate; returns the buffer holding g
-  float* finish(hipStream_t s, hipError_t* err) {
-    float* acc = stack.back().second;
-    hipError_t e = hipSuccess;
-    for (int i = (int)stack.size() - 2; i >= 0 && e == hipSuccess; --i) e = plan_merge_launch(n, stack[i].second, acc, s);
-    // RN(x * 1) = x for every x the sums can hold (never subnormal): one replica needs no pass
-    if (e == hipSuccess && inv_rep != 1.0f) e = plan_scale_launch(n, acc, inv_rep, acc, s);
-    *err = e;
-    return acc;
+  return -1;  // cannot happen for a valid cursor
+}
+
+// microbatch k of rank r (r = next / accum, k = next % accum) produced `grad`
+hipError_t plan_cursor_push(canon_plan_cursor* c, float* base, const float* grad, hipStream_t s) {
+  const canon_dp_plan& p = c->plan;
+  const int64_t n = c->n, st = plan_slot_stride(n);
+  const int r = (int)(c->next / p.accum), k = (int)(c->next % p.accum);
+  const int shard = r % p.dp_shard;
+  const float inv_accum = (float)(1.0 / p.accum), inv_shard = (float)(1.0 / p.dp_shard);
+  auto slot = [&](int i) { return base + st * i; };
+  hipError_t e = hipSuccess;
+  ++c->next;
+  if (p.accum == 1) {  // one microbatch per rank: its sum, the shard sum and the last shard's scale in one pass
+    if (shard == 0) c->inner = plan_take_slot(c);
+    if (n > 0) e = plan_rank_launch(n, grad, inv_accum, shard == 0, shard == p.dp_shard - 1, inv_shard, slot(c->inner), s);
+    if (e != hipSuccess || shard != p.dp_shard - 1) return e;
+  } else {
+    float* g_r = slot(0);
+    if (n > 0) e = plan_accum_launch(n, grad, inv_accum, k == 0, g_r, s);
+    if (e != hipSuccess || k != p.accum - 1) return e;
+    if (shard == 0) c->inner = plan_take_slot(c);
+    if (n > 0) e = plan_shard_launch(n, g_r, shard == 0, slot(c->inner), s);
+    if (e != hipSuccess || shard != p.dp_shard - 1) return e;
+    if (n > 0) e = plan_scale_launch(n, slot(c->inner), inv_shard, slot(c->inner), s);
   }
+  // Algorithm 2: push the replica's average at level 0 and carry
+  int level = 0, part = c->inner;
+  while (e == hipSuccess && c->depth > 0 && c->level[c->depth - 1] == level) {
+    const int lower = c->slot[c->depth - 1];
+    if (n > 0) e = plan_merge_launch(n, slot(lower), slot(part), s);  // part = lower + part
+    --c->depth;
+    ++level;
+  }
+  c->level[c->depth] = level;
+  c->slot[c->depth] = part;
+  ++c->depth;
+  c->inner = -1;
+  return e;
+}
+
+// Result of Algorithm 2 (the entries from the top of the stack down, each added on the left) times
+// 1/dp_replicate, left in a slot whose address is returned (the caller's `out` when given).
+float* plan_cursor_finish(canon_plan_cursor* c, float* base, float* out, hipStream_t s, hipError_t* err) {
+  const int64_t n = c->n, st = plan_slot_stride(n);
+  float* acc = base + st * c->slot[c->depth - 1];
+  hipError_t e = hipSuccess;
+  for (int i = c->depth - 2; i >= 0 && e == hipSuccess; --i)
+    if (n > 0) e = plan_merge_launch(n, base + st * c->slot[i], acc, s);
+  const float inv_rep = (float)(1.0 / c->plan.dp_replicate);
+  float* dst = out ? out : acc;
+  // RN(x * 1) = x for every x the sums can hold (never subnormal): one replica needs no pass
+  if (e == hipSuccess && n > 0) {
+    if (inv_rep != 1.0f) e = plan_scale_launch(n, acc, inv_rep, dst, s);
+    else if (dst != acc) e = hipMemcpyAsync(dst, acc, sizeof(float) * n, hipMemcpyDeviceToDevice, s);
+  }
+  *err = e;
+  return dst;
+}
+
+struct HashPlan {
+  int64_t total_leaves = 0, n_wg = 0;
+  size_t off_tens = 0, off_wgt = 0, off_wgf = 0, off_la = 0, off_lb = 0, off_td = 0, bytes = 0;
 };
+
+HashPlan hash_plan(int64_t n, const int64_t* nbytes) {
+  HashPlan hp;
+  for (int64_t t = 0; t < n; ++t) {
+    const int64_t w = hash_leaf_count(nbytes[t]);
+    hp.total_leaves += w;
+    hp.n_wg += (w + 255) / 256;
+  }
+  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  size_t o = 0;
+  hp.off_tens = o; o += up(sizeof(HashTensor) * (size_t)n);
+  hp.off_wgt = o; o += up(sizeof(int32_t) * (size_t)hp.n_wg);
+  hp.off_wgf = o; o += up(sizeof(int64_t) * (size_t)hp.n_wg);
+  hp.off_la = o; o += up(32 * (size_t)hp.total_leaves);
+  hp.off_lb = o; o += up(32 * (size_t)hp.total_leaves);
+  hp.off_td = o; o += up(32 * (size_t)n);
+  hp.bytes = o;
+  return hp;
+}
+
+size_t step_hash_bytes(const canon_model_cfg* c, const canon_dp_plan* p) {
+  std::vector<int64_t> nb;
+  step_hash_sizes(c, p, nb);
+  return hash_plan((int64_t)nb.size(), nb.data()).bytes;
+}
+
+// H1 of the tensors (ptrs, nbytes: host arrays) into the device digest, enqueued on s; the workspace is
+// device memory of hash_plan(...).bytes bytes, 256-byte aligned.
+canon_status state_hash_enqueue(int64_t n_tensors, const void* const* ptrs, const int64_t* nbytes, uint8_t* digest,
+                                void* workspace, size_t workspace_bytes, hipStream_t s) {
+  if (n_tensors < 0 || !digest || !workspace || (n_tensors > 0 && (!ptrs || !nbytes))) return CANON_EINVAL;
+  if (n_tensors > (int64_t(1) << 24)) return CANON_EUNSUPPORTED;
+  for (int64_t t = 0; t < n_tensors; ++t)
+    if (nbytes[t] < 0 || (nbytes[t] > 0 && !ptrs[t])) return CANON_EINVAL;
+  if ((uintptr_t)workspace & 255) return CANON_EINVAL;
+  const HashPlan hp = hash_plan(n_tensors, nbytes);
+  if (workspace_bytes < hp.bytes) return CANON_EWORKSPACE;
+  if (hp.n_wg > INT32_MAX) return CANON_EUNSUPPORTED;
+  // host tables: per tensor, and per workgroup (tensor, first leaf)
+  std::vector<char> host(hp.off_la);
+  HashTensor* tens = (HashTensor*)(host.data() + hp.off_tens);
+  int32_t* wgt = (int32_t*)(host.data() + hp.off_wgt);
+  int64_t* wgf = (int64_t*)(host.data() + hp.off_wgf);
+  int64_t leaf = 0, wg = 0;
+  for (int64_t t = 0; t < n_tensors; ++t) {
+    const int64_t w = hash_leaf_count(nbytes[t]);
+    tens[t].ptr = ptrs[t];
+    tens[t].nbytes = nbytes[t];
+    tens[t].leaves = w;
+    tens[t].leaf_offset = leaf;
+    tens[t].aligned = (((uintptr_t)ptrs[t]) & 15) == 0;
+    for (int64_t f = 0; f < w; f += 256) {
+      wgt[wg] = (int32_t)t;
+      wgf[wg] = f;
+      ++wg;
+    }
+    leaf += w;
+  }
+  char* ws = (char*)workspace;
+  if (hp.off_la > 0) {
+    hipError_t e = hipMemcpyAsync(ws, host.data(), hp.off_la, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return CANON_EDEVICE;
+  }
+  return dev(hash_launch(n_tensors, (const HashTensor*)(ws + hp.off_tens), hp.n_wg,
+                         (const int32_t*)(ws + hp.off_wgt), (const int64_t*)(ws + hp.off_wgf),
+                         (uint32_t*)(ws + hp.off_la), (uint32_t*)(ws + hp.off_lb), (uint32_t*)(ws + hp.off_td),
+                         digest, s));
+}
 
 }  // namespace
 
@@ -728,6 +869,44 @@ canon_status canon_grad_accum(const canon_order* order, const canon_dp_plan* pla
   return dev(grad_accum_fused_launch(plan->accum, plan->dp_shard, plan->dp_replicate, n, pp, out, as_stream(stream)));
 }
 
+size_t canon_plan_state_bytes(const canon_dp_plan* plan, int64_t n) {
+  if (!plan_ok(plan) || n < 0) return 0;
+  return sizeof(float) * (size_t)(plan_slot_stride(n) * plan_slot_count(*plan));
+}
+
+canon_status canon_plan_begin(const canon_dp_plan* plan, int64_t n, canon_plan_cursor* cursor) {
+  if (!plan_ok(plan) || n < 0 || !cursor) return CANON_EINVAL;
+  if (bit_length(plan->dp_replicate) > CANON_PLAN_MAX_DEPTH) return CANON_EUNSUPPORTED;
+  plan_cursor_init(*plan, n, cursor);
+  return CANON_OK;
+}
+
+canon_status canon_plan_push(const canon_order* order, canon_plan_cursor* cursor, const float* grad, void* state,
+                             size_t state_bytes, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (!plan_cursor_valid(cursor) || cursor->next >= plan_total(cursor->plan)) return CANON_EINVAL;
+  if (cursor->n > 0 && (!grad || !state || ((uintptr_t)state & 255))) return CANON_EINVAL;
+  if (state_bytes < canon_plan_state_bytes(&cursor->plan, cursor->n)) return CANON_EWORKSPACE;
+  canon_plan_cursor c = *cursor;  // the caller's record changes only when every launch was enqueued
+  if (plan_cursor_push(&c, (float*)state, grad, as_stream(stream)) != hipSuccess) return CANON_EDEVICE;
+  *cursor = c;
+  return CANON_OK;
+}
+
+canon_status canon_plan_finish(const canon_order* order, canon_plan_cursor* cursor, void* state, size_t state_bytes,
+                               float* out, void* stream) {
+  canon_status st = check_order(order);
+  if (st != CANON_OK) return st;
+  if (!plan_cursor_valid(cursor) || cursor->next != plan_total(cursor->plan)) return CANON_EINVAL;
+  if (cursor->n > 0 && (!out || !state || ((uintptr_t)state & 255))) return CANON_EINVAL;
+  if (state_bytes < canon_plan_state_bytes(&cursor->plan, cursor->n)) return CANON_EWORKSPACE;
+  canon_plan_cursor c = *cursor;
+  hipError_t e = hipSuccess;
+  plan_cursor_finish(&c, (float*)state, out, as_stream(stream), &e);
+  return dev(e);
+}
+
 canon_status canon_quant_scales(const canon_order* order, int64_t rows, int64_t cols, const uint16_t* w,
                                 float* scale, void* stream) {
   canon_status st = check_order(order);
@@ -777,31 +956,6 @@ size_t canon_qlinear_bwd_workspace_bytes(int64_t T, int64_t N, int64_t K) {
   return qlinear_bwd_workspace_bytes(T, N, K);
 }
 
-namespace {
-struct HashPlan {
-  int64_t total_leaves = 0, n_wg = 0;
-  size_t off_tens = 0, off_wgt = 0, off_wgf = 0, off_la = 0, off_lb = 0, off_td = 0, bytes = 0;
-};
-
-HashPlan hash_plan(int64_t n, const int64_t* nbytes) {
-  HashPlan hp;
-  for (int64_t t = 0; t < n; ++t) {
-    const int64_t w = hash_leaf_count(nbytes[t]);
-    hp.total_leaves += w;
-    hp.n_wg += (w + 255) / 256;
-  }
-  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
-  size_t o = 0;
-  hp.off_tens = o; o += up(sizeof(HashTensor) * (size_t)n);
-  hp.off_wgt = o; o += up(sizeof(int32_t) * (size_t)hp.n_wg);
-  hp.off_wgf = o; o += up(sizeof(int64_t) * (size_t)hp.n_wg);
-  hp.off_la = o; o += up(32 * (size_t)hp.total_leaves);
-  hp.off_lb = o; o += up(32 * (size_t)hp.total_leaves);
-  hp.off_td = o; o += up(32 * (size_t)n);
-  hp.bytes = o;
-  return hp;
-}
-}  // namespace
 
 size_t canon_state_hash_workspace_bytes(int64_t n_tensors, const int64_t* nbytes) {
   if (n_tensors < 0 || (n_tensors > 0 && !nbytes)) return 0;
@@ -812,44 +966,7 @@ size_t canon_state_hash_workspace_bytes(int64_t n_tensors, const int64_t* nbytes
 
 canon_status canon_state_hash(int64_t n_tensors, const void* const* ptrs, const int64_t* nbytes, uint8_t* digest,
                               void* workspace, size_t workspace_bytes, void* stream) {
-  if (n_tensors < 0 || !digest || !workspace || (n_tensors > 0 && (!ptrs || !nbytes))) return CANON_EINVAL;
-  if (n_tensors > (int64_t(1) << 24)) return CANON_EUNSUPPORTED;
-  for (int64_t t = 0; t < n_tensors; ++t)
-    if (nbytes[t] < 0 || (nbytes[t] > 0 && !ptrs[t])) return CANON_EINVAL;
-  if ((uintptr_t)workspace & 255) return CANON_EINVAL;
-  const HashPlan hp = hash_plan(n_tensors, nbytes);
-  if (workspace_bytes < hp.bytes) return CANON_EWORKSPACE;
-  if (hp.n_wg > INT32_MAX) return CANON_EUNSUPPORTED;
-  // host tables: per tensor, and per workgroup (tensor, first leaf)
-  std::vector<char> host(hp.off_la);
-  HashTensor* tens = (HashTensor*)(host.data() + hp.off_tens);
-  int32_t* wgt = (int32_t*)(host.data() + hp.off_wgt);
-  int64_t* wgf = (int64_t*)(host.data() + hp.off_wgf);
-  int64_t leaf = 0, wg = 0;
-  for (int64_t t = 0; t < n_tensors; ++t) {
-    const int64_t w = hash_leaf_count(nbytes[t]);
-    tens[t].ptr = ptrs[t];
-    tens[t].nbytes = nbytes[t];
-    tens[t].leaves = w;
-    tens[t].leaf_offset = leaf;
-    tens[t].aligned = (((uintptr_t)ptrs[t]) & 15) == 0;
-    for (int64_t f = 0; f < w; f += 256) {
-      wgt[wg] = (int32_t)t;
-      wgf[wg] = f;
-      ++wg;
-    }
-    leaf += w;
-  }
-  hipStream_t s = as_stream(stream);
-  char* ws = (char*)workspace;
-  if (hp.off_la > 0) {
-    hipError_t e = hipMemcpyAsync(ws, host.data(), hp.off_la, hipMemcpyHostToDevice, s);
-    if (e != hipSuccess) return CANON_EDEVICE;
-  }
-  return dev(hash_launch(n_tensors, (const HashTensor*)(ws + hp.off_tens), hp.n_wg,
-                         (const int32_t*)(ws + hp.off_wgt), (const int64_t*)(ws + hp.off_wgf),
-                         (uint32_t*)(ws + hp.off_la), (uint32_t*)(ws + hp.off_lb), (uint32_t*)(ws + hp.off_td),
-                         digest, s));
+  return state_hash_enqueue(n_tensors, ptrs, nbytes, digest, workspace, workspace_bytes, as_stream(stream));
 }
 
 canon_status canon_adamw(int64_t n_tensors, const int64_t* sizes, uint16_t* const* params, float* const* m,
@@ -1088,7 +1205,8 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
                         uint16_t* const* params, float* const* m, float* const* v, int32_t step_t,
                         const int32_t* windows, const float* rope_cos, const float* rope_sin,
                         const canon_adamw_consts* consts, const canon_clip* clip, void* workspace,
-                        size_t workspace_bytes, float* loss_out, float* const* grads_out, void* stream) {
+                        size_t workspace_bytes, float* loss_out, float* const* grads_out, uint8_t* state_digest,
+                        void* stream) {
   canon_status st = check_order(order);
   if (st != CANON_OK) return st;
   if (step_t < 1) return CANON_EINVAL;  // AdamW's step index starts at 1
@@ -1109,6 +1227,7 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
   const int64_t P = off[nt];
   const size_t need = canon_step_workspace_bytes(cfg, plan);
   if (!workspace || workspace_bytes < need) return CANON_EWORKSPACE;
+  if (state_digest && ((uintptr_t)workspace & 255)) return CANON_EINVAL;  // the hash's tables are aligned
 
   hipStream_t s = as_stream(stream);
   Carver cv(workspace);
@@ -1123,8 +1242,9 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
   TRY(hipMemsetAsync(L.bad, 0, sizeof(int32_t), s));
   TRY(token_check_launch(M * S1, windows, cfg->vocab, L.bad, s));
 
-  PlanRun gplan(P, *plan, L.g_r, L.pool);
-  PlanRun lplan(1, *plan, plan->accum > 1 ? L.loss_gr : nullptr, L.loss_pool);
+  canon_plan_cursor gplan, lplan;
+  plan_cursor_init(*plan, P, &gplan);
+  plan_cursor_init(*plan, 1, &lplan);
   const int nl = cfg->n_layers;
   const int64_t l0 = cfg->embed_norm ? 2 : 1;  // first layer tensor
   const int PL = cfg->int8_linear ? 10 : 6;    // tensors per layer
@@ -1183,16 +1303,15 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
         float* t = dcur; dcur = dnext; dnext = t;
       }
       TRY(embed_bwd_launch(mb, D.S, D.d, L.win, S1, D.V, dcur, L.grad + off[0], L.embed_scratch, s));
-      TRY(gplan.microbatch(r, k, L.grad, s));
-      TRY(lplan.microbatch(r, k, L.loss_mb, s));
+      TRY(plan_cursor_push(&gplan, L.plan_slots, L.grad, s));
+      TRY(plan_cursor_push(&lplan, L.loss_slots, L.loss_mb, s));
     }
   }
   hipError_t e = hipSuccess;
-  float* g = gplan.finish(s, &e);
+  float* g = plan_cursor_finish(&gplan, L.plan_slots, nullptr, s, &e);
   TRY(e);
-  float* lossv = lplan.finish(s, &e);
+  plan_cursor_finish(&lplan, L.loss_slots, loss_out, s, &e);
   TRY(e);
-  TRY(hipMemcpyAsync(loss_out, lossv, sizeof(float), hipMemcpyDeviceToDevice, s));
   TRY(set_nan_if_launch(L.bad, loss_out, s));
   if (grads_out)
     for (int64_t t = 0; t < nt; ++t)
@@ -1223,6 +1342,19 @@ canon_status canon_step(const canon_order* order, const canon_model_cfg* cfg, co
   }
   for (int64_t t = 0; t < nt; ++t)
     TRY(adamw_launch(sz[t], params[t], m[t], v[t], g + off[t], decay[t], c9, gscale, skip, s));
+  if (state_digest) {  // the per-step audit hash of the state this step leaves
+    std::vector<int64_t> nb;
+    step_hash_sizes(cfg, plan, nb);
+    std::vector<const void*> ptrs;
+    ptrs.push_back(windows);
+    for (int64_t t = 0; t < nt; ++t) ptrs.push_back(params[t]);
+    for (int64_t t = 0; t < nt; ++t) ptrs.push_back(m[t]);
+    for (int64_t t = 0; t < nt; ++t) ptrs.push_back(v[t]);
+    for (int64_t t = 0; t < nt; ++t) ptrs.push_back(g + off[t]);
+    st = state_hash_enqueue((int64_t)nb.size(), ptrs.data(), nb.data(), state_digest, L.hash_ws,
+                            step_hash_bytes(cfg, plan), s);
+    if (st != CANON_OK) return st;
+  }
   return CANON_OK;
 }
 

@@ -84,7 +84,10 @@ def test_host_validation_rejects_before_any_launch():
     consts = C.AdamWConsts(*([0.1] * 9))
     for t in (0, -3):
         assert lib.canon_step(order, ctypes.byref(cfg), ctypes.byref(plan), ptrs, ptrs, ptrs, t, x, x, x,
-                              ctypes.byref(consts), None, x, 1 << 30, x, None, None) == C.EINVAL
+                              ctypes.byref(consts), None, x, 1 << 30, x, None, None, None) == C.EINVAL
+    # a per-step digest with a workspace off 256-byte alignment
+    assert lib.canon_step(order, ctypes.byref(cfg), ctypes.byref(plan), ptrs, ptrs, ptrs, 1, x, x, x,
+                          ctypes.byref(consts), None, x + 16, 1 << 40, x, None, x, None) == C.EINVAL
     # embedding backward: negative sizes, a missing pointer, too many positions, a small workspace
     assert lib.canon_embed_bwd(order, -1, 10, 4, x, dx, dy, x, 1 << 20, None) == C.EINVAL
     assert lib.canon_embed_bwd(order, 8, 10, 4, None, dx, dy, x, 1 << 20, None) == C.EINVAL
@@ -114,3 +117,95 @@ def test_sha256_constants_in_the_device_source():
 
     assert k == [iroot(p << 96, 3) & 0xFFFFFFFF for p in primes]
     assert h0 == [iroot(p << 64, 2) & 0xFFFFFFFF for p in primes[:8]]
+
+
+def _plan_record_shape(plan, next_):
+    """What the plan record must hold after next_ pushes: the shard sum's presence and the stack levels."""
+    accum, shard, rep = plan
+    r = next_ // accum
+    groups = r // shard
+    return (r % shard) != 0, [L for L in range(30, -1, -1) if (groups >> L) & 1]
+
+
+def test_plan_cursor_walk_without_gpu():
+    """With n = 0 the plan calls launch nothing, so the host record's whole walk (position, shard sum, the
+    binary-carry stack of Algorithm 2, slot use) can be followed on the CPU, including persisting the record
+    and resuming from its bytes after every push."""
+    import paper_2609_17380_amd.canon as C
+    STATE = 1 << 20  # a stand-in address: with n = 0 nothing reads or writes it
+    for plan in [(1, 8, 1), (2, 4, 1), (1, 2, 4), (3, 1, 5), (2, 3, 3), (1, 1, 13), (1, 1, 64), (2, 1, 100)]:
+        p = C.DPPlan(*plan)
+        nslots = (1 if plan[0] > 1 else 0) + int(plan[2]).bit_length() + 1
+        assert C.plan_state_bytes(p, 0) == 0
+        assert C.plan_state_bytes(p, 100) == 4 * 128 * nslots  # slots of 64-float multiples
+        total = plan[0] * plan[1] * plan[2]
+        cur = C.plan_begin(p, 0)
+        for i in range(total):
+            C.plan_push(cur, None, STATE, state_bytes=0, stream=0)
+            cur = C.PlanCursor.from_buffer_copy(bytes(cur))  # persisted and resumed
+            has_inner, levels = _plan_record_shape(plan, i + 1)
+            assert cur.next == i + 1
+            assert (cur.inner >= 0) == has_inner
+            assert list(cur.level[:cur.depth]) == levels
+            used = list(cur.slot[:cur.depth]) + ([cur.inner] if has_inner else [])
+            assert len(set(used)) == len(used) and all(0 <= s < nslots for s in used)
+        assert cur.depth == bin(plan[2]).count("1")
+        C.plan_finish(cur, STATE, None, state_bytes=0, stream=0)
+
+
+def test_plan_cursor_validation_without_gpu():
+    """Records the calls cannot produce are rejected before any launch, and the record is left unchanged."""
+    import paper_2609_17380_amd.canon as C
+    p = C.DPPlan(1, 1, 6)
+    n = 1000
+    need = C.plan_state_bytes(p, n)
+    STATE, GRAD = 1 << 20, 1 << 21  # never dereferenced: every case below fails validation first
+    cur = C.plan_begin(p, 0)
+    for _ in range(3):  # three replicas in: levels 1 and 0
+        C.plan_push(cur, None, STATE, state_bytes=0, stream=0)
+    good = bytes(cur)
+    good_n = C.PlanCursor.from_buffer_copy(good)
+    good_n.n = n
+
+    def mutated(fn):
+        c = C.PlanCursor.from_buffer_copy(bytes(good_n))
+        fn(c)
+        return c
+
+    bad = [
+        mutated(lambda c: setattr(c, "next", 7)),                        # beyond the plan's 6 microbatches
+        mutated(lambda c: setattr(c, "next", -1)),
+        mutated(lambda c: setattr(c, "depth", 1)),                       # stack shape not that of 3 replicas
+        mutated(lambda c: c.level.__setitem__(0, 0)),
+        mutated(lambda c: c.slot.__setitem__(1, c.slot[0])),             # one slot twice
+        mutated(lambda c: c.slot.__setitem__(0, 9)),                     # slot out of range
+        mutated(lambda c: setattr(c, "inner", 2)),                       # a shard sum with dp_shard = 1
+        mutated(lambda c: setattr(c, "plan", C.DPPlan(0, 1, 6))),
+        mutated(lambda c: setattr(c, "n", -5)),
+    ]
+    for c in bad:
+        before = bytes(c)
+        for call in (lambda: C.plan_push(c, GRAD, STATE, state_bytes=need, stream=0),
+                     lambda: C.plan_finish(c, STATE, GRAD, state_bytes=need, stream=0)):
+            try:
+                call()
+                raise AssertionError("accepted a record the calls cannot produce")
+            except C.CanonError as e:
+                assert e.status == C.EINVAL, e
+            assert bytes(c) == before
+    # a valid record: a misaligned or too small state, a missing gradient
+    for kw, args in [(dict(state_bytes=need), (GRAD, STATE + 4)), (dict(state_bytes=need - 4), (GRAD, STATE)),
+                     (dict(state_bytes=need), (None, STATE))]:
+        c = C.PlanCursor.from_buffer_copy(bytes(good_n))
+        try:
+            C.plan_push(c, *args, stream=0, **kw)
+            raise AssertionError("accepted")
+        except C.CanonError as e:
+            assert e.status in (C.EINVAL, C.EWORKSPACE)
+        assert bytes(c) == bytes(good_n)
+    # finish before the last push
+    try:
+        C.plan_finish(C.PlanCursor.from_buffer_copy(bytes(good_n)), STATE, GRAD, state_bytes=need, stream=0)
+        raise AssertionError("accepted")
+    except C.CanonError as e:
+        assert e.status == C.EINVAL

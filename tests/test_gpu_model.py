@@ -128,3 +128,49 @@ def test_step_rejects_bad_tokens_without_update():
     assert np.isnan(host_f32(loss)[0])
     for a, b in zip(pg, params):
         assert np.array_equal(host_u16(a), b)
+
+
+@pytest.mark.parametrize("plan", [(1, 2, 2), (2, 1, 3)])
+def test_step_state_digest_matches_oracle_state(plan):
+    """The per-step audit hash computed inside canon_step equals H1 of the oracle's own step outputs (windows,
+    parameters, m, v, reduced gradient), written by the oracle's hash code, and canon_state_hash of the
+    device outputs; a second run of the same step gives the same digest."""
+    from oracle import state_hash as H
+    L, d, H_, F, V, S, mb = 2, 128, 1, 128, 200, 64, 1
+    hd = d // H_
+    params = I.model_params(L, d, F, V, seed=3, std=0.02)
+    R = plan[1] * plan[2]
+    windows = I.uniform_int((R * plan[0] * mb, S + 1), 3, I.TENSOR_IDS["windows"], V)
+    cos, sin = I.rope_tables(S, hd)
+    k = I.adamw_constants()
+    po = [p.copy() for p in params]
+    mo = [np.zeros(p.shape, np.float32) for p in params]
+    vo = [np.zeros(p.shape, np.float32) for p in params]
+    _, g_o = oracle.step(oracle.ModelCfg(L, d, H_, hd, F, V, S, mb, np.float32(1e-5)), oracle.Plan(*plan), po, mo, vo,
+                         windows, cos, sin, oracle.AdamWConsts(*k), want_grads=True)
+    want = H.state_digest([windows.astype(np.int32).tobytes()] + [p.astype(np.uint16).tobytes() for p in po] +
+                          [m.tobytes() for m in mo] + [v.tobytes() for v in vo] + [g.tobytes() for g in g_o])
+    cfg = C.ModelCfg(L, d, H_, hd, F, V, S, mb, np.float32(1e-5))
+    cplan = C.DPPlan(*plan)
+    ws = torch.empty(C.step_workspace_bytes(cfg, cplan), dtype=torch.uint8, device=DEV)
+    digests = []
+    for run in range(2):
+        pg = [dev_bf16(p) for p in params]
+        mg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
+        vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
+        gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params]
+        win = dev_i32(windows)
+        loss = torch.zeros(1, dtype=torch.float32, device=DEV)
+        dig = torch.zeros(32, dtype=torch.uint8, device=DEV)
+        C.step(cfg, cplan, pg, mg, vg, win, dev_f32(cos), dev_f32(sin), C.AdamWConsts(*k), ws, loss, grads_out=gg,
+               state_digest=dig)
+        torch.cuda.synchronize()
+        digests.append(bytes(dig.cpu().numpy()))
+        state = [win] + pg + mg + vg + gg
+        hws = torch.empty(C.state_hash_workspace_bytes(state), dtype=torch.uint8, device=DEV)
+        d2 = torch.zeros(32, dtype=torch.uint8, device=DEV)
+        C.state_hash(state, d2, hws)
+        torch.cuda.synchronize()
+        assert bytes(d2.cpu().numpy()) == digests[-1]
+    print(f"step digest {digests[0].hex()[:16]}.. oracle {want.hex()[:16]}..", flush=True)
+    assert digests[0] == want and digests[1] == want
