@@ -7,15 +7,18 @@
 // reordered and spread over matrix instructions freely.  The dequantised output is
 // y[i][j] = RN(RN(RN32(acc) * sa) * sb[j]).
 //
-// Tiling: whole 256 x 256 tiles (m, n multiples of 256) run on 4 wavefronts, each a 128 x 128 block of
-// 4 x 4 v_mfma_i32_32x32x32_i8 instructions (gemm_i8_tile_kernel).  Other shapes: a workgroup of NW wavefronts
-// owns a 16 NW HB x 64 WN output tile, each wavefront a 32 HB x 32 WN block: 256 x 256 tiles of 8 wavefronts
-// with 64-byte stages for large products, else 128 x 128 tiles of 4 wavefronts with 128-byte stages.  Stages of KS k bytes are staged
-// through LDS (rows padded by 16 bytes, which keeps the 16-byte operand reads of 32 consecutive rows free of
-// bank conflicts), double buffered.
+// Tiling: whole 256 x 256 tiles (m, n multiples of 256, k of 64) run on 4 wavefronts, each a 128 x 128 block of
+// 4 x 4 v_mfma_i32_32x32x32_i8 instructions, with direct-to-LDS loads three stages ahead (gemm_i8_tile_kernel).
+// Other shapes: a workgroup of NW wavefronts owns a 16 NW HB x 64 WN output tile, each wavefront a 32 HB x 32 WN
+// block: 256 x 256 tiles of 8 wavefronts with 64-byte stages for large products, else 128 x 128 tiles of 4
+// wavefronts with 128-byte stages; their stages of KS k bytes are staged through registers into LDS (rows
+// padded by 16 bytes, which keeps the 16-byte operand reads of 32 consecutive rows free of bank conflicts),
+// double buffered.
 // Each lane of a 32x32x32 instruction supplies 16 consecutive k bytes of one row of A and of B; the two
 // half-wavefronts cover k 0..15 and 16..31 of the instruction's 32.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "canon_internal.h"
 
@@ -23,6 +26,7 @@ namespace canon {
 
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 typedef int32_t i32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // Workgroup configuration: NW wavefronts in (NW / 2) x 2, wavefront (wr, wc) owning rows [32 HB wr, 32 HB (wr + 1))
 // and columns [32 WN wc, 32 WN (wc + 1)) of a BM x (64 WN) tile (HB x WN instruction blocks); stages of KS k bytes.
@@ -181,16 +185,46 @@ __global__ __launch_bounds__(64 * NW) void gemm_i8_kernel(GemmI8Args g) {
       }
 }
 
-// Whole 256 x 256 tiles (m, n multiples of 256, k of KS, 16-byte aligned rows): 4 wavefronts, each a 128 x 128
-// block of 4 x 4 instructions, so every 16-byte operand read from LDS feeds four instructions (twice the reuse
-// of the 64 x 128 wavefront blocks).  The 256 int32 accumulators per lane live in the accumulation registers;
-// one workgroup per CU.
-template <int KS>
+// 16 bytes per lane from global memory straight into LDS: lane l of the wavefront writes lds_addr + 16 l
+// (lds_addr wavefront-uniform, in m0).  Written as assembly so that the compiler does not track these loads:
+// it would otherwise wait for all of them before every LDS read, which defeats loading stages ahead; the
+// kernel waits for them itself (vm_wait).  The kernel issues no other instruction that uses m0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const int8_t* g, unsigned lds_addr) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds_addr), "v"(g)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+// wait until at most N vector-memory loads of this wavefront are outstanding (they complete in order)
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);  // expcnt, lgkmcnt left at max
+}
+
+// Whole 256 x 256 tiles (m, n multiples of 256, k of 64, 16-byte aligned rows): 4 wavefronts, each a 128 x 128
+// block of 4 x 4 instructions, so every 16-byte operand read from LDS feeds four instructions.  The 256 int32
+// accumulators per lane live in the accumulation registers; one workgroup per CU, so the pipeline hides every
+// latency inside the wavefront:
+//  * stages of 64 k bytes go from global memory straight into LDS (16-byte direct-to-LDS loads, no register
+//    staging), NBUF = 4 stages deep: stage s + 3 is requested while stage s is multiplied;
+//  * LDS rows are 64 bytes with their four 16-byte segments permuted by the row (segment c of row r at
+//    position c ^ sw(r), sw(r) = ((r >> 2) ^ (r & 2)) & 3), so the operand reads of 8 (or 16) consecutive
+//    rows at one k offset cover distinct banks; each direct load of a wavefront fills 16 rows, lane l the
+//    position l of that kilobyte, fetching the global segment that belongs there;
+//  * operand fragments run one k step ahead (two sets), and the stage's barrier sits before the last k
+//    step's instructions, whose fragments are already in registers.
+// Buffer safety: buffer (s + 3) % NBUF = (s - 1) % NBUF is refilled during stage s, after the barrier inside
+// stage s - 1, which every wavefront passes only once its reads of stage s - 1 have completed; stage s + 1 is
+// read after the barrier inside stage s, which every wavefront passes only once its own loads of stage s + 1
+// have landed.
+template <int NBUF>
 __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
-  constexpr int BM = 256, BN = 256, LD = KS + 16, SEG = KS / 16;
-  constexpr int V = BM * KS / 16 / 256;  // 16-byte vectors of A (and of B) per thread per stage
-  __shared__ __attribute__((aligned(16))) int8_t As[2][BM * LD];
-  __shared__ __attribute__((aligned(16))) int8_t Bs[2][BN * LD];
+  constexpr int BM = 256, BN = 256, KS = 64, ROWB = 64;
+  constexpr int STAGE = (BM + BN) * KS;  // bytes per stage: A rows, then B rows
+  static_assert(NBUF == 4, "three stages ahead: the waits below count three");
+  __shared__ __attribute__((aligned(1024))) int8_t lds[NBUF * STAGE];
 
   constexpr int64_t GM = 8;
   const int64_t tiles_n = g.n / BN, tiles_m = g.m / BM, tiles = tiles_m * tiles_n;
@@ -202,21 +236,21 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
   const int64_t within = tile - group * GM * tiles_n;
   const int64_t row0 = (first_m + within % gsize) * BM, col0 = (within / gsize) * BN;
 
-  const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+  const int t = threadIdx.x, lane = t & 63;
+  const int w = __builtin_amdgcn_readfirstlane(t >> 6);
   const int wr = w >> 1, wc = w & 1;
-  const int ar = 128 * wr + (lane & 31), bc = 128 * wc + (lane & 31);
-  const int kh = 16 * (lane >> 5);
-  // this thread's global sources and LDS slots: vector idx = t + 256 it is row idx / SEG, segment idx % SEG
-  const int8_t* ga[V];
-  const int8_t* gb[V];
-  int so[V];
-#pragma unroll
-  for (int it = 0; it < V; ++it) {
-    const int idx = t + 256 * it, r = idx / SEG, sg = idx % SEG;
-    ga[it] = g.a + (row0 + r) * g.lda + 16 * sg;
-    gb[it] = g.b + (col0 + r) * g.ldb + 16 * sg;
-    so[it] = r * LD + 16 * sg;
-  }
+  // fragment reads: lane (rl, hi) reads row rl of a 32-row block at k segment 2 ks + hi
+  const int rl = lane & 31, hi = lane >> 5;
+  const int cs = hi ^ (((rl >> 2) ^ (rl & 2)) & 3);
+  const int seg0 = 16 * cs, seg1 = 16 * (cs ^ 2);  // positions of segments hi and 2 + hi
+  const int a_off = (128 * wr + rl) * ROWB, b_off = BM * KS + (128 * wc + rl) * ROWB;
+  // direct loads: wavefront w fills row blocks 4 w .. 4 w + 3 (16 rows each) of A and of B; lane l writes
+  // position l of a block: row l / 4, segment position l % 4, holding global segment (l % 4) ^ sw(row)
+  const int dr = lane >> 2;
+  const int dseg = (lane & 3) ^ (((dr >> 2) ^ (dr & 2)) & 3);
+  const int8_t* ga = g.a + (row0 + 64 * w + dr) * g.lda + 16 * dseg;
+  const int8_t* gb = g.b + (col0 + 64 * w + dr) * g.ldb + 16 * dseg;
+  const int64_t sta = 16 * g.lda, stb = 16 * g.ldb;
 
   i32x16 acc[4][4];
 #pragma unroll
@@ -227,100 +261,110 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
       for (int v = 0; v < 16; ++v) acc[h][v2][v] = 0;
 
   const int64_t ns = g.k / KS;
-  {
-    i32x4 ra[V], rb[V];
+  i32x4 fa[2][4], fb[2][4];  // two fragment sets
+  // wavefront-uniform LDS byte address of this wavefront's first row block in stage buffer 0
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) int8_t*)lds + 64 * w * ROWB;
+  auto issue = [&](int64_t st) {
+    const unsigned base = lds0 + (unsigned)(st & (NBUF - 1)) * STAGE;
+    const int64_t k0 = st * KS;
 #pragma unroll
-    for (int it = 0; it < V; ++it) {
-      ra[it] = *reinterpret_cast<const i32x4*>(ga[it]);
-      rb[it] = *reinterpret_cast<const i32x4*>(gb[it]);
-    }
-#pragma unroll
-    for (int it = 0; it < V; ++it) {
-      *reinterpret_cast<i32x4*>(As[0] + so[it]) = ra[it];
-      *reinterpret_cast<i32x4*>(Bs[0] + so[it]) = rb[it];
-    }
-  }
-  __syncthreads();
-  // stage s's multiply-adds from LDS buffer s & 1
-  auto compute = [&](int buf) {
-    const int8_t* as = As[buf];
-    const int8_t* bs = Bs[buf];
-#pragma unroll
-    for (int ks = 0; ks < KS / 32; ++ks) {
-      const int kk = 32 * ks + kh;
-      i32x4 a[4], b[4];
-#pragma unroll
-      for (int h = 0; h < 4; ++h) a[h] = *reinterpret_cast<const i32x4*>(as + (ar + 32 * h) * LD + kk);
-#pragma unroll
-      for (int v2 = 0; v2 < 4; ++v2) b[v2] = *reinterpret_cast<const i32x4*>(bs + (bc + 32 * v2) * LD + kk);
-#pragma unroll
-      for (int h = 0; h < 4; ++h)
-#pragma unroll
-        for (int v2 = 0; v2 < 4; ++v2)
-          acc[h][v2] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a[h], b[v2], acc[h][v2], 0, 0, 0);
+    for (int i = 0; i < 4; ++i) {
+      dma16(ga + i * sta + k0, base + 16 * i * ROWB);
+      dma16(gb + i * stb + k0, base + BM * KS + 16 * i * ROWB);
     }
   };
-  for (int64_t s = 0; s + 1 < ns; ++s) {
-    const int buf = (int)(s & 1);
-    const int64_t off = (s + 1) * KS;
-    i32x4 ra[V], rb[V];
+  auto frags = [&](int f, int64_t st, int ks) {
+    const int8_t* base = lds + (int)(st & (NBUF - 1)) * STAGE;
+    const int so = ks ? seg1 : seg0;
 #pragma unroll
-    for (int it = 0; it < V; ++it) {
-      ra[it] = *reinterpret_cast<const i32x4*>(ga[it] + off);
-      rb[it] = *reinterpret_cast<const i32x4*>(gb[it] + off);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    compute(buf);
-    __builtin_amdgcn_sched_barrier(0);
+    for (int h = 0; h < 4; ++h) fa[f][h] = *reinterpret_cast<const i32x4*>(base + a_off + 32 * h * ROWB + so);
 #pragma unroll
-    for (int it = 0; it < V; ++it) {
-      *reinterpret_cast<i32x4*>(As[buf ^ 1] + so[it]) = ra[it];
-      *reinterpret_cast<i32x4*>(Bs[buf ^ 1] + so[it]) = rb[it];
-    }
-    __syncthreads();
-  }
-  compute((int)((ns - 1) & 1));
+    for (int v2 = 0; v2 < 4; ++v2) fb[f][v2] = *reinterpret_cast<const i32x4*>(base + b_off + 32 * v2 * ROWB + so);
+  };
+  auto mma = [&](int f) {
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+#pragma unroll
+      for (int v2 = 0; v2 < 4; ++v2)
+        acc[h][v2] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[f][h], fb[f][v2], acc[h][v2], 0, 0, 0);
+  };
 
-  // result layout: register v, lane l -> row (v % 4) + 4 (l / 32) + 8 (v / 4), column l % 32 of the block.
-  // The wavefront-uniform part of each address (block, row within the lane group) is kept apart from the
-  // lane's offset, so the stores take a scalar base and a 32-bit lane offset.
-  const int64_t wrow = row0 + 128 * wr, wcol = col0 + 128 * wc;
-  const int lo = 4 * (lane >> 5) * (int)g.ldc + (lane & 31);  // the launcher keeps 260 ldc below 2^31
-  if (g.y) {
-    const float sa = *g.sa;
-#pragma unroll
-    for (int v2 = 0; v2 < 4; ++v2) {
-      const float sbj = g.sb[g.sb_scalar ? 0 : wcol + 32 * v2 + (lane & 31)];
-#pragma unroll
-      for (int h = 0; h < 4; ++h)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          float* Yr = g.y + (wrow + 32 * h + (v & 3) + 8 * (v >> 2)) * g.ldc + wcol + 32 * v2;
-          const float af = (float)acc[h][v2][v];  // round to nearest even
-          const float tq = af * sa;
-          Yr[lo] = tq * sbj;
-          if ((v & 3) == 3) __builtin_amdgcn_sched_barrier(0);  // a few accumulators at a time
-        }
-    }
+  issue(0);
+  if (ns > 1) issue(1);
+  if (ns > 2) issue(2);
+  // stage 0 landed (this wavefront's loads of stages 1 and 2 may still be in flight), then everyone's
+  if (ns > 2) vm_wait<16>();
+  else if (ns > 1) vm_wait<8>();
+  else vm_wait<0>();
+  __syncthreads();
+  frags(0, 0, 0);
+  // Every stage but the last: no branch around LDS operations inside the loop, so the compiler's wait counts
+  // stay exact (the last k step's instructions wait only for their own fragments, not for the next stage's
+  // reads issued after the barrier).
+  for (int64_t st = 0; st + 1 < ns; ++st) {
+    if (st + 3 < ns) issue(st + 3);
+    frags(1, st, 1);
+    mma(0);
+    __builtin_amdgcn_sched_barrier(0);
+    // this wavefront's loads of stage st + 1 landed (those of later stages may stay in flight), then everyone's
+    if (st + 3 < ns) vm_wait<16>();
+    else if (st + 2 < ns) vm_wait<8>();
+    else vm_wait<0>();
+    __syncthreads();
+    frags(0, st + 1, 0);
+    mma(1);
+    // the next stage's reads first, under this step's 16 instructions
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
-  if (g.acc) {
+  frags(1, ns - 1, 1);
+  mma(0);
+  mma(1);
+
+  // Epilogue through LDS, 32 rows of the wavefront's 128 x 128 block at a time, so that every lane stores 16
+  // contiguous bytes (4 columns) and a store instruction covers two 512-byte row segments.  Result layout of
+  // the instruction: register v, lane (rl, hi) -> row (v % 4) + 4 hi + 8 (v / 4), column rl of the 32 x 32
+  // block.  Each wavefront writes and reads back only its own LDS region (LDS operations of a wavefront complete
+  // in order); the barrier first lets every wavefront finish reading the last stage.
+  constexpr int ELD = 136;  // padded row (ints): the two half-wavefronts' rows 4 apart fall on other banks
+  __syncthreads();
+  int32_t* eb = reinterpret_cast<int32_t*>(lds) + w * (32 * ELD);
+  const int64_t wrow = row0 + 128 * wr, wcol = col0 + 128 * wc;
+  const int c4 = 4 * rl;  // this lane's 4 columns in the read-back
+  float sa = 0.0f, sb4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (g.y) {
+    sa = *g.sa;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sb4[e] = g.sb[g.sb_scalar ? 0 : wcol + c4 + e];
+  }
+#pragma unroll
+  for (int h = 0; h < 4; ++h) {
 #pragma unroll
     for (int v2 = 0; v2 < 4; ++v2)
 #pragma unroll
-      for (int h = 0; h < 4; ++h)
+      for (int v = 0; v < 16; ++v) eb[((v & 3) + 4 * hi + 8 * (v >> 2)) * ELD + 32 * v2 + rl] = acc[h][v2][v];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          int32_t* Ar = g.acc + (wrow + 32 * h + (v & 3) + 8 * (v >> 2)) * g.ldc + wcol + 32 * v2;
-          Ar[lo] = acc[h][v2][v];
-          if ((v & 3) == 3) __builtin_amdgcn_sched_barrier(0);
-        }
+    for (int q = 0; q < 16; ++q) {
+      const int r = 2 * q + hi;
+      const i32x4 x = *reinterpret_cast<const i32x4*>(eb + r * ELD + c4);
+      const int64_t o = (wrow + 32 * h + r) * g.ldc + wcol + c4;
+      if (g.y) {  // streamed out: nontemporal
+        f32x4 y;
+        y[0] = ((float)x[0] * sa) * sb4[0];  // RN(RN(RN32(acc) sa) sb), one rounding per operation
+        y[1] = ((float)x[1] * sa) * sb4[1];
+        y[2] = ((float)x[2] * sa) * sb4[2];
+        y[3] = ((float)x[3] * sa) * sb4[3];
+        __builtin_nontemporal_store(y, reinterpret_cast<f32x4*>(g.y + o));
+      }
+      if (g.acc) __builtin_nontemporal_store(x, reinterpret_cast<i32x4*>(g.acc + o));
+    }
   }
 }
 
-template <int KS>
 static hipError_t launch_i8_tile(const GemmI8Args& g, hipStream_t s) {
   const int64_t tiles = (g.m / 256) * (g.n / 256);
-  hipLaunchKernelGGL((gemm_i8_tile_kernel<KS>), dim3((unsigned)tiles), dim3(256), 0, s, g);
+  hipLaunchKernelGGL((gemm_i8_tile_kernel<4>), dim3((unsigned)tiles), dim3(256), 0, s, g);
   return hipGetLastError();
 }
 
@@ -347,11 +391,11 @@ hipError_t gemm_i8_launch(const GemmI8Args& gin, hipStream_t s) {
   const int64_t big_tiles = ((g.m + 255) / 256) * ((g.n + 255) / 256);
   const double small_time = (double)((small_tiles + 2 * cus - 1) / (2 * cus));        // rounds of one tile time
   const double big_time = (double)((big_tiles + cus - 1) / cus) * (2.0 / 1.12);
-  // whole 256 x 256 tiles: the 128 x 128 wavefront blocks (1.06-1.16x the rate of the 64 x 128 blocks at the
-  // 1B projection shapes), with 128-byte stages when k allows
-  const bool whole = g.vec && g.m % 256 == 0 && g.n % 256 == 0 && g.ldc * 260 < (int64_t(1) << 31);
-  if (whole && g.k % 128 == 0) return launch_i8_tile<128>(g, s);
-  if (whole && g.k % 64 == 0) return launch_i8_tile<64>(g, s);
+  // whole 256 x 256 tiles (and 16-byte output stores: y, acc and ldc aligned to 4 elements): the pipelined
+  // kernel with 128 x 128 wavefront blocks
+  const bool whole = g.vec && g.m % 256 == 0 && g.n % 256 == 0 && g.ldc % 4 == 0 && ((uintptr_t)g.y & 15) == 0 &&
+                     ((uintptr_t)g.acc & 15) == 0;
+  if (whole && g.k % 64 == 0 && g.k > 0) return launch_i8_tile(g, s);
   if (big_time < small_time) return launch_i8<2, 4, 64, 8>(g, s);
   return launch_i8<2, 2, 128, 4>(g, s);
 }
