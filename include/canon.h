@@ -334,8 +334,8 @@ canon_status canon_gemm_i8(int64_t m, int64_t n, int64_t k, const int8_t* a, int
    asked for) in blocks of 256 by the Sylvester matrix scaled by 1/16 (fast transform, strides 1..128),
    quantised with the per-tensor step RN(amax * RN(1/127)) (amax: the largest |value| by bit pattern),
    multiplied exactly on the int8 matrix cores and dequantised as RN(RN(RN32(acc) * s_left) * s_right).
-   workspace: device memory of canon_qlinear_bwd_workspace_bytes(T, N, K) bytes (rotated operands and
-   their codes); T*N and K*max(N, T) at most 2^34. */
+   workspace: device memory of canon_qlinear_bwd_workspace_bytes(T, N, K) bytes (the rotated operands'
+   codes; the rotated values themselves are recomputed, never stored); T*N and K*max(N, T) at most 2^34. */
 canon_status canon_qlinear_bwd(const canon_order* order, int64_t T, int64_t N, int64_t K, const float* dy,
                                const int8_t* qx, const float* sx, const int8_t* qw, const float* sw, float* dx,
                                float* dw, void* workspace, size_t workspace_bytes, void* stream);
