@@ -301,10 +301,29 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
   // Every stage but the last: no branch around LDS operations inside the loop, so the compiler's wait counts
   // stay exact (the last k step's instructions wait only for their own fragments, not for the next stage's
   // reads issued after the barrier).
+  // k step 0 of a stage with the 8 loads of stage st + 3 spread over its 16 instructions (one load after every
+  // two): issued in one burst they stall the wavefront, the only one on its SIMD, while the matrix core idles
+  auto mma0_loads = [&](int64_t st3, bool more) {  // more: stage st3 exists (wavefront-uniform)
+    const unsigned base = lds0 + (unsigned)(st3 & (NBUF - 1)) * STAGE;
+    const int64_t k0 = st3 * KS;
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+#pragma unroll
+      for (int v2 = 0; v2 < 4; ++v2) {
+        acc[h][v2] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[0][h], fb[0][v2], acc[h][v2], 0, 0, 0);
+        if (v2 & 1) {
+          const int i = h, ab = v2 >> 1;  // pieces in order A0, B0, A1, B1, ...
+          if (more) {
+            if (ab == 0) dma16(ga + i * sta + k0, base + 16 * i * ROWB);
+            else dma16(gb + i * stb + k0, base + BM * KS + 16 * i * ROWB);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+  };
   for (int64_t st = 0; st + 1 < ns; ++st) {
-    if (st + 3 < ns) issue(st + 3);
     frags(1, st, 1);
-    mma(0);
+    mma0_loads(st + 3, st + 3 < ns);
     __builtin_amdgcn_sched_barrier(0);
     // this wavefront's loads of stage st + 1 landed (those of later stages may stay in flight), then everyone's
     if (st + 3 < ns) vm_wait<16>();
