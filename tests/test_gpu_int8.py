@@ -86,11 +86,39 @@ def gemm_case(m, n, k, a_off=0, seed=0, extreme=False):
 
 @pytest.mark.parametrize("m,n,k", [(130, 260, 192), (128, 128, 64), (1, 1, 1), (200, 3, 1000), (64, 300, 48),
                                    (129, 129, 4096), (7, 5, 0),
-                                   # whole 256 x 256 tiles: 128-byte stages, 64-byte stages, one stage
-                                   (256, 256, 128), (512, 768, 192), (768, 512, 2048), (256, 256, 64)])
+                                   # whole 256 x 256 tiles (64-byte stages loaded three ahead): 1 .. 5 stages
+                                   # (the pipeline's start and end cases), many stages
+                                   (256, 256, 64), (256, 256, 128), (512, 768, 192), (256, 512, 256),
+                                   (512, 256, 320), (768, 512, 2048)])
 def test_gemm_i8(m, n, k):
     print(f"gemm_i8 {m}x{n}x{k}", flush=True)
     gemm_case(m, n, k)
+
+
+@pytest.mark.parametrize("outputs", ["y", "acc"])
+def test_gemm_i8_whole_tiles_one_output(outputs):
+    """The whole-tile kernel with only the dequantised output (as the quantised linear asks) or only the
+    int32 accumulators; the other buffer stays untouched."""
+    m, n, k = 512, 512, 320
+    rng = np.random.default_rng(11)
+    a = rng.integers(-128, 128, (m, k)).astype(np.int8)
+    b = rng.integers(-128, 128, (n, k)).astype(np.int8)
+    sa = np.float32(0.021)
+    sb = (np.abs(rng.standard_normal(n)) * 0.01).astype(np.float32)
+    acc_o, y_o = oracle.gemm_i8(a, b, sa, sb)
+    acc = torch.full((m, n), -1, dtype=torch.int32, device=DEV)
+    y = torch.full((m, n), float("nan"), dtype=torch.float32, device=DEV)
+    if outputs == "y":
+        C.gemm_i8(m, n, k, dev_i8(a), k, dev_i8(b), k, y=y, sa=dev_f32(np.array([sa])), sb=dev_f32(sb))
+    else:
+        C.gemm_i8(m, n, k, dev_i8(a), k, dev_i8(b), k, acc=acc)
+    torch.cuda.synchronize()
+    if outputs == "y":
+        assert_bits(host_f32(y), y_o, "y")
+        assert np.all(acc.cpu().numpy() == -1)
+    else:
+        assert np.array_equal(acc.cpu().numpy(), acc_o)
+        assert np.all(np.isnan(host_f32(y)))
 
 
 def test_gemm_i8_misaligned_and_extreme():
@@ -181,6 +209,13 @@ def test_qlinear_bwd_one_output_and_mid_size():
     qlinear_bwd_case(256, 96, 40, seed=1, want_dx=False)   # dW only: N need not be a multiple of 256
     qlinear_bwd_case(80, 512, 40, seed=2, want_dw=False)   # dx only: T need not be a multiple of 256
     qlinear_bwd_case(2048, 2048, 512, seed=3)              # several tiles per operand, full rotation blocks
+
+
+def test_qlinear_bwd_many_blocks():
+    """T N = 2^25 rotation blocks' worth of the upstream gradient: the contiguous-direction rotation runs more
+    than one grid-stride round per wavefront, the strided-direction one 4096 tiles."""
+    print("qlinear_bwd 4096x8192x256", flush=True)
+    qlinear_bwd_case(4096, 8192, 256, seed=4)
 
 
 @pytest.mark.parametrize("s", [0.1, 0.0173, 1.0 / 3.0, 3e-38, 2.0 ** 126, 2.0 ** 127, 1e38, 7.0])
