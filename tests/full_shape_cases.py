@@ -8,7 +8,11 @@ Two cases at the shapes the workloads name:
   seq 2048, one sequence per microbatch, plan (accum 1, dp_shard 2, dp_replicate 1), tokens uniform over the
   vocabulary, weights N(0, 0.02), AdamW at t = 1, global-norm clip at 1.0 with the spike rule (5.0, 5).
 
-Both the golden-digest script (oracle side) and the GPU parity test build their inputs here.
+* ``qlinear``: the int8 quantised linear's backward at the 1B decoder's gate/up projection: upstream gradient
+  fp32 N(0, 1e-3) [8192, 16384], int8 codes uniform over [-128, 127] for the input [8192, 2048] and the
+  weight [16384, 2048], input step 0.0173, per-row weight steps |N(0, 1e-3)| + 1e-4.
+
+The golden-digest script (oracle side) and the GPU parity test build their inputs here.
 """
 import hashlib
 
@@ -19,6 +23,7 @@ import paper_2609_17380_amd.inputs as I
 BLOCK = dict(d=2048, H=16, hd=128, F=8192, S=2048, batch=1, eps=1e-5, seed=0, std=0.02)
 STEP = dict(L=2, d=2048, H=16, hd=128, F=8192, V=50304, S=2048, mb=1, plan=(1, 2, 1), eps=1e-5, seed=0,
             std=0.02, clip=(1.0, 5.0, 5))
+QLIN = dict(T=8192, N=16384, K=2048, seed=0, dy_std=1e-3, sx=0.0173)
 BLOCK_NAMES = ["attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down"]
 
 
@@ -43,6 +48,16 @@ def step_inputs(c=STEP):
     windows = I.uniform_int((shard * rep * accum * c["mb"], c["S"] + 1), c["seed"], I.TENSOR_IDS["windows"], c["V"])
     cos, sin = I.rope_tables(c["S"], c["hd"])
     return params, windows, cos, sin, I.adamw_constants()
+
+
+def qlin_inputs(c=QLIN):
+    T, N, K, seed = c["T"], c["N"], c["K"], c["seed"]
+    dy = I.normal_f32((T, N), seed, I.TENSOR_IDS["dy_in"], std=c["dy_std"])
+    qx = (I.uniform_int((T, K), seed, I.TENSOR_IDS["x_in"], 256) - 128).astype(np.int8)
+    qw = (I.uniform_int((N, K), seed, I.TENSOR_IDS["w_gate_up"], 256) - 128).astype(np.int8)
+    sx = np.array([c["sx"]], np.float32)
+    sw = (np.abs(I.normal_f32((N,), seed, I.TENSOR_IDS["gemm_b"], std=1e-3)) + np.float32(1e-4)).astype(np.float32)
+    return dy, qx, sx, qw, sw
 
 
 def digest(a: np.ndarray) -> str:

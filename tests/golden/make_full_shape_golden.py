@@ -1,7 +1,8 @@
 """Writes the oracle's results of the full-shape parity cases as per-tensor SHA-256 digests.
 
-Runs the CPU oracle only (no GPU code is imported): ``python tests/golden/make_full_shape_golden.py [block|step]``
-writes ``full_shape_block.json`` and/or ``full_shape_step.json`` beside this script (or into ``--out-dir``).
+Runs the CPU oracle only (no GPU code is imported):
+``python tests/golden/make_full_shape_golden.py [block|step|qlinear]`` writes ``full_shape_<case>.json`` beside this
+script (or into ``--out-dir``).
 With CANON_REF_PROGRESS=1 the oracle prints a line after each block and head pass.  The GPU parity test
 (`tests/test_gpu_full_shape.py`) regenerates the same seeded inputs, runs the HIP path and compares digests.
 The oracle needs about 1 TFLOP for the block and 6 TFLOP for the step (minutes to tens of minutes on a few
@@ -63,8 +64,18 @@ def make_step():
             "loss": float(loss), "skip_state": info["skip_state"], "skipped": info["skipped"], "tensors": out}
 
 
+def make_qlinear():
+    c = FC.QLIN
+    dy, qx, sx, qw, sw = FC.qlin_inputs(c)
+    t0 = time.time()
+    dx, dw = oracle.qlinear_bwd(dy, qx, sx[0], qw, sw)
+    secs = time.time() - t0
+    return {"case": "qlinear", "config": c, "oracle_seconds": round(secs, 1), "threads": oracle.num_threads(),
+            "tensors": [entry("dx", dx), entry("dw", dw)]}
+
+
 def main(which, out_dir=HERE):
-    for case, fn in (("block", make_block), ("step", make_step)):
+    for case, fn in (("block", make_block), ("step", make_step), ("qlinear", make_qlinear)):
         if which in (case, "all"):
             print(f"{case}: running the oracle on {oracle.num_threads()} threads", flush=True)
             res = fn()
@@ -77,7 +88,7 @@ def main(which, out_dir=HERE):
 if __name__ == "__main__":
     import argparse
     ap = argparse.ArgumentParser()
-    ap.add_argument("case", nargs="?", default="all", choices=["block", "step", "all"])
+    ap.add_argument("case", nargs="?", default="all", choices=["block", "step", "qlinear", "all"])
     ap.add_argument("--out-dir", default=HERE, help="where the JSON files go (default: beside this script)")
     args = ap.parse_args()
     os.makedirs(args.out_dir, exist_ok=True)

@@ -3,6 +3,7 @@
 * One decoder block forward and backward at d_model 2048, 16 heads of 128, FFN 8192, seq 2048, batch 1.
 * A full-width training step: 2 layers, d_model 2048, FFN 8192, vocab 50304, seq 2048, plan (1, 2, 1), with
   the global-norm clip: loss, pre-clip norm, every reduced gradient, and the post-AdamW parameters and moments.
+* The int8 quantised linear's backward at the gate/up projection (T 8192, N 16384, K 2048): dx and dW.
 
 The expected values are SHA-256 digests of every output tensor, written by
 ``tests/golden/make_full_shape_golden.py`` from the CPU oracle on the same seeded inputs (``full_shape_cases``).
@@ -91,3 +92,19 @@ def test_step_full_width_matches_oracle():
         got["v." + n] = host_f32(t)
     print(f"loss gpu {float(got['loss'][0]):.6f} oracle {g['loss']:.6f}", flush=True)
     check(g, got)
+
+
+def test_qlinear_bwd_gate_up_shape_matches_oracle():
+    g = load("qlinear")
+    c = FC.QLIN
+    assert (g["config"]["T"], g["config"]["N"], g["config"]["K"]) == (c["T"], c["N"], c["K"])
+    print(f"qlinear_bwd T={c['T']} N={c['N']} K={c['K']}", flush=True)
+    dy, qx, sx, qw, sw = FC.qlin_inputs(c)
+    T, N, K = c["T"], c["N"], c["K"]
+    ws = torch.empty(C.qlinear_bwd_workspace_bytes(T, N, K), dtype=torch.uint8, device=DEV)
+    dx = torch.empty((T, K), dtype=torch.float32, device=DEV)
+    dw = torch.empty((N, K), dtype=torch.float32, device=DEV)
+    C.qlinear_bwd(T, N, K, dev_f32(dy), torch.from_numpy(qx).to(DEV), dev_f32(sx), torch.from_numpy(qw).to(DEV),
+                  dev_f32(sw), dx, dw, ws)
+    torch.cuda.synchronize()
+    check(g, {"dx": host_f32(dx), "dw": host_f32(dw)})
