@@ -4,24 +4,26 @@
 // fused multiply-adds from +0 in ascending k; the chunk partials are combined by the binary-carry fold of
 // Algorithm 2 (pushed in ascending chunk order, leftover blocks combined smallest first).
 //
-// Matrix-core mapping.  v_mfma_f32_32x32x1_2b_f32 performs, for two independent 32x32 blocks, the
-// rank-1 update D = C + a*b with ONE product per output element.  On gfx950 it returns RN(c + a*b) with
-// the flush rule of R0, bit for bit (checked against a sequential fma chain, including ties, signed zeros
-// and 32-step dependent chains).  A bf16 x bf16 product is exact in fp32, so a chain of these updates,
-// one per k, is exactly the canonical fma chain.  The bf16 MFMA shapes that sum several products inside
-// one instruction do not give the chain's roundings and are not used.
+// Matrix-core mapping.  v_mfma_f32_32x32x1_2b_f32 (two independent 32x32 blocks) and
+// v_mfma_f32_16x16x1_4b_f32 (four 16x16 blocks) perform the rank-1 update D = C + a*b with ONE product per
+// output element.  On gfx950 they return RN(c + a*b) with the flush rule of R0, bit for bit (checked against
+// a sequential fma chain, including ties, signed zeros and 32-step dependent chains).  A bf16 x bf16 product
+// is exact in fp32, so a chain of these updates, one per k, is exactly the canonical fma chain.  The bf16
+// MFMA shapes that sum several products inside one instruction do not give the chain's roundings and are
+// not used.
 //
-// Tiling: a workgroup of 4 waves computes a 64 x 128 tile of C; wave (wr, wc) owns rows 32*wr..+32 and
-// columns 64*wc..+64 as the instruction's two 32x32 blocks (block 0: columns +0..31, block 1: +32..63).
-// Two workgroups share a CU (two waves per SIMD) so one hides the other's LDS and barrier waits.
-// Per chunk the 64x32 A tile and 32x128 B tile are staged through LDS as fp32, widened once and double
-// buffered, with the next chunk's 16-byte global loads in flight during the current chunk's MFMA chain.
-// An operand whose source is k-contiguous is stored as rows [row][k] (one 16-byte LDS read gives a lane
-// four k values); one whose source is row-contiguous is stored k-major [k][row] (one 4-byte read per k),
-// so neither layout needs a transposing scatter.
+// Tiling (GemmCfg): a workgroup computes a 64-row tile of C, 128 columns with four wavefronts of the 32x32
+// instruction (wave (wr, wc) owns rows 32*wr..+32 and columns 64*wc..+64 as two 32x32 blocks), or 64 columns
+// with four wavefronts of the 16x16 instruction (wave w owns rows 16*w..+16 as four 16x16 blocks).  Two or
+// three workgroups share a CU so one hides the others' LDS and barrier waits.  Per chunk the 64x32 A tile and
+// the 32-deep B tile are staged through LDS as fp32, widened once and double buffered, with the next chunk's
+// 16-byte global loads in flight during the current chunk's MFMA chain.  An operand whose source is
+// k-contiguous is stored as rows [row][k] (one 16-byte LDS read gives a lane four k values); one whose source
+// is row-contiguous is stored k-major [k][row] (one 4-byte read per k), so neither layout needs a transposing
+// scatter.
 // Fold: inside an aligned group of four chunks the two lowest levels of Algorithm 2 are fixed and merged
-// in place; the group partial is pushed at level 2.  Levels 2 and 3 stay in registers; levels 4 and up,
-// touched once per 16 chunks, live in per-lane private memory.
+// in place; the group partial is pushed at level 2.  The next levels (2 to 4 of them, by shape) stay in
+// registers; the levels above, touched once per 16 chunks or less often, live in per-lane private memory.
 //
 // Causal modes (attention): KMODE_TRAIL skips key chunks that are masked for every row of the tile and
 // KMODE_LEAD skips query chunks below the tile; the skipped chunks' partials are exactly +0 in the
@@ -39,12 +41,55 @@ namespace canon {
 
 typedef float v32f __attribute__((ext_vector_type(32)));
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+
+// The rank-1 matrix instructions; both add exactly one product into every output.  V = 32:
+// v_mfma_f32_32x32x1_2b_f32, a wavefront owns 32 x 64 outputs (two 32x32 blocks sharing the A column), 32
+// accumulators per lane.  V = 16: v_mfma_f32_16x16x1_4b_f32, a wavefront owns 16 x 64 (four 16x16 blocks sharing
+// the A column), 16 accumulators per lane: half the registers per chain and per fold level.
+template <int V>
+struct Mfma;
+template <>
+struct Mfma<32> {
+  typedef v32f T;
+  static constexpr int WR = 32;  // rows per wavefront
+  static __device__ __forceinline__ T step(float a, float b, const T& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x1f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ int arow(int lane) { return lane & 31; }  // A row of this lane
+  // output register v of a lane -> row and column inside the wavefront's block
+  static __device__ __forceinline__ int orow(int v, int lane) {
+    return (v & 3) + 4 * (lane >> 5) + 8 * ((v & 15) >> 2);
+  }
+  static __device__ __forceinline__ int ocol(int v, int lane) { return (v >> 4) * 32 + (lane & 31); }
+};
+template <>
+struct Mfma<16> {
+  typedef v16f T;
+  static constexpr int WR = 16;
+  static __device__ __forceinline__ T step(float a, float b, const T& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x1f32(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ int arow(int lane) { return lane & 15; }
+  static __device__ __forceinline__ int orow(int v, int lane) { return (v & 3) + 4 * (lane >> 4); }
+  static __device__ __forceinline__ int ocol(int v, int lane) { return (v >> 2) * 16 + (lane & 15); }
+};
 
 constexpr int BM = 64, BN = 128, KC = 32;
 constexpr int LDK = KC + 4;               // row-layout stride (floats): [row][k]
 constexpr int LDMA = BM + 4, LDMB = BN + 4;  // k-major stride (floats): [k][row]
 constexpr int A_FLOATS = (BM * LDK > KC * LDMA) ? BM * LDK : KC * LDMA;
 constexpr int B_FLOATS = (BN * LDK > KC * LDMB) ? BN * LDK : KC * LDMB;
+
+// Workgroup shape of the general kernel: instruction V, WC wavefront columns of 64 (the tile is 64 x 64*WC, the
+// wavefronts (64 / WR) x WC), OCC workgroups per CU, and the number of fold levels kept in registers for the
+// row/row layout (RLR) and the layouts with k-major staging (RLK).
+template <int V_, int WC_, int OCC_, int RLR_, int RLK_>
+struct GemmCfg {
+  static constexpr int V = V_, WC = WC_, OCC = OCC_, RLR = RLR_, RLK = RLK_;
+  static constexpr int NW = (BM / Mfma<V>::WR) * WC, NT = 64 * NW, TBN = 64 * WC, LDMB = TBN + 4;
+  static constexpr int BFL = (TBN * LDK > KC * LDMB) ? TBN * LDK : KC * LDMB;
+};
 
 // Raw bf16 data of one chunk for one thread: 8 A elements and 16 B elements, as 16-byte vectors.
 struct Raw {
@@ -83,27 +128,29 @@ __device__ __forceinline__ uint4 load8(const uint16_t* p, int64_t valid, bool ve
 // Global -> registers for the chunk starting at k0.  Per operand, a thread takes 8 consecutive elements
 // along the source's contiguous dimension: (row, 8 k) for a k-contiguous source, (k, 8 rows) otherwise.
 // FAST: the whole chunk is in range and 16-byte aligned (no checks).
-template <bool TA, bool TB, bool FAST>
+template <bool TA, bool TB, bool FAST, int NT, int TBN>
 __device__ __forceinline__ Raw load_chunk(const GemmArgs& g, const uint16_t* A, const uint16_t* B, int64_t row0,
                                           int64_t col0, int64_t k0, bool vec) {
   const int t = threadIdx.x;
   Raw r;
-  if (!TA) {
-    const int64_t row = row0 + (t >> 2), k = k0 + (t & 3) * 8;
-    r.a = load8<FAST>(A + row * g.lda + k, (row < g.m) ? (g.k - k) : 0, vec);
-  } else {
-    const int64_t k = k0 + (t >> 3), row = row0 + (t & 7) * 8;
-    r.a = load8<FAST>(A + k * g.lda + row, (k < g.k) ? (g.m - row) : 0, vec);
+  if (NT == 256 || t < 256) {  // 256 A pieces
+    if (!TA) {
+      const int64_t row = row0 + (t >> 2), k = k0 + (t & 3) * 8;
+      r.a = load8<FAST>(A + row * g.lda + k, (row < g.m) ? (g.k - k) : 0, vec);
+    } else {
+      const int64_t k = k0 + (t >> 3), row = row0 + (t & 7) * 8;
+      r.a = load8<FAST>(A + k * g.lda + row, (k < g.k) ? (g.m - row) : 0, vec);
+    }
   }
 #pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    const int idx = t + 256 * it;
+  for (int it = 0; it < 4 * TBN / NT; ++it) {  // 4 * TBN B pieces
+    const int idx = t + NT * it;
     uint4 v;
     if (TB) {
       const int64_t col = col0 + (idx >> 2), k = k0 + (idx & 3) * 8;
       v = load8<FAST>(B + col * g.ldb + k, (col < g.n) ? (g.k - k) : 0, vec);
     } else {
-      const int64_t k = k0 + (idx >> 4), col = col0 + (idx & 15) * 8;
+      const int64_t k = k0 + idx / (TBN / 8), col = col0 + (idx % (TBN / 8)) * 8;
       v = load8<FAST>(B + k * g.ldb + col, (k < g.k) ? (g.n - col) : 0, vec);
     }
     if (it == 0) r.b0 = v; else r.b1 = v;
@@ -118,19 +165,21 @@ __device__ __forceinline__ void st8(float* d, const float (&f)[8]) {
 
 // Registers -> LDS: rows [row][k] for k-contiguous sources, k-major [k][row] otherwise; both are
 // 8 contiguous floats per thread.
-template <bool TA, bool TB>
+template <bool TA, bool TB, int NT, int TBN>
 __device__ __forceinline__ void store_chunk(float* As, float* Bs, const Raw& r) {
   const int t = threadIdx.x;
   float f[8];
-  widen8(r.a, f);
-  if (!TA) st8(As + (t >> 2) * LDK + (t & 3) * 8, f);
-  else st8(As + (t >> 3) * LDMA + (t & 7) * 8, f);
+  if (NT == 256 || t < 256) {
+    widen8(r.a, f);
+    if (!TA) st8(As + (t >> 2) * LDK + (t & 3) * 8, f);
+    else st8(As + (t >> 3) * LDMA + (t & 7) * 8, f);
+  }
 #pragma unroll
-  for (int it = 0; it < 2; ++it) {
-    const int idx = t + 256 * it;
+  for (int it = 0; it < 4 * TBN / NT; ++it) {
+    const int idx = t + NT * it;
     widen8(it == 0 ? r.b0 : r.b1, f);
     if (TB) st8(Bs + (idx >> 2) * LDK + (idx & 3) * 8, f);
-    else st8(Bs + (idx >> 4) * LDMB + (idx & 15) * 8, f);
+    else st8(Bs + (idx / (TBN / 8)) * (TBN + 4) + (idx % (TBN / 8)) * 8, f);
   }
 }
 
@@ -143,21 +192,21 @@ __device__ __forceinline__ v4f fetch4(const float* base, int idx, int g4) {
 }
 
 // One full chunk's chain: 32 dependent rank-1 updates from +0, operand reads one group ahead.
-template <bool TA, bool TB>
-__device__ __forceinline__ v32f chain_full(const float* As, const float* Bs, int ai, int bi) {
-  v32f acc;
+template <bool TA, bool TB, int V, int LDB>
+__device__ __forceinline__ typename Mfma<V>::T chain_full(const float* As, const float* Bs, int ai, int bi) {
+  typename Mfma<V>::T acc;
 #pragma unroll
-  for (int v = 0; v < 32; ++v) acc[v] = 0.0f;
-  v4f a4 = fetch4<TA, LDMA>(As, ai, 0), b4 = fetch4<!TB, LDMB>(Bs, bi, 0);
+  for (int v = 0; v < V; ++v) acc[v] = 0.0f;
+  v4f a4 = fetch4<TA, LDMA>(As, ai, 0), b4 = fetch4<!TB, LDB>(Bs, bi, 0);
 #pragma unroll
   for (int g4 = 0; g4 < KC / 4; ++g4) {
     v4f an = a4, bn = b4;
     if (g4 + 1 < KC / 4) {
       an = fetch4<TA, LDMA>(As, ai, g4 + 1);
-      bn = fetch4<!TB, LDMB>(Bs, bi, g4 + 1);
+      bn = fetch4<!TB, LDB>(Bs, bi, g4 + 1);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc = __builtin_amdgcn_mfma_f32_32x32x1f32(a4[j], b4[j], acc, 0, 0, 0);
+    for (int j = 0; j < 4; ++j) acc = Mfma<V>::step(a4[j], b4[j], acc);
     a4 = an;
     b4 = bn;
   }
@@ -165,48 +214,50 @@ __device__ __forceinline__ v32f chain_full(const float* As, const float* Bs, int
 }
 
 // A ragged last chunk: only its kleft < 32 real terms enter the chain.
-template <bool TA, bool TB>
-__device__ __forceinline__ v32f chain_part(const float* As, const float* Bs, int ai, int bi, int kleft) {
-  v32f acc;
+template <bool TA, bool TB, int V, int LDB>
+__device__ __forceinline__ typename Mfma<V>::T chain_part(const float* As, const float* Bs, int ai, int bi,
+                                                          int kleft) {
+  typename Mfma<V>::T acc;
 #pragma unroll
-  for (int v = 0; v < 32; ++v) acc[v] = 0.0f;
+  for (int v = 0; v < V; ++v) acc[v] = 0.0f;
   for (int kk = 0; kk < kleft; ++kk) {
     float av = TA ? As[kk * LDMA + ai] : As[ai * LDK + kk];
-    float bv = TB ? Bs[bi * LDK + kk] : Bs[kk * LDMB + bi];
-    acc = __builtin_amdgcn_mfma_f32_32x32x1f32(av, bv, acc, 0, 0, 0);
+    float bv = TB ? Bs[bi * LDK + kk] : Bs[kk * LDB + bi];
+    acc = Mfma<V>::step(av, bv, acc);
   }
   return acc;
 }
 
 // Fold levels kept in private memory (levels >= the register levels); rarely touched.
-template <int N>
+template <int N, class T>
 struct FoldMem {
-  float s[N > 0 ? N : 1][32];
+  static constexpr int V = sizeof(T) / sizeof(float);
+  float s[N > 0 ? N : 1][V];
   // levels whose bit is set in c0 hold +0 (skipped leading blocks); the others are written before read
   __device__ __forceinline__ void clear(int64_t c0) {
     for (int L = 0; L < N; ++L, c0 >>= 1)
       if (c0 & 1)
-        for (int v = 0; v < 32; ++v) s[L][v] = 0.0f;
+        for (int v = 0; v < V; ++v) s[L][v] = 0.0f;
   }
-  __device__ __forceinline__ void push(v32f p, int64_t c) {
+  __device__ __forceinline__ void push(T p, int64_t c) {
     int L = 0;
     while (c & 1) {
-      v32f lower;
+      T lower;
 #pragma unroll
-      for (int v = 0; v < 32; ++v) lower[v] = s[L][v];
+      for (int v = 0; v < V; ++v) lower[v] = s[L][v];
       p = lower + p;
       c >>= 1;
       ++L;
     }
 #pragma unroll
-    for (int v = 0; v < 32; ++v) s[L][v] = p[v];
+    for (int v = 0; v < V; ++v) s[L][v] = p[v];
   }
-  __device__ __forceinline__ void result(v32f& r, bool& have, int64_t n) const {
+  __device__ __forceinline__ void result(T& r, bool& have, int64_t n) const {
     for (int L = 0; L < N; ++L, n >>= 1) {
       if (n & 1) {
-        v32f x;
+        T x;
 #pragma unroll
-        for (int v = 0; v < 32; ++v) x[v] = s[L][v];
+        for (int v = 0; v < V; ++v) x[v] = s[L][v];
         if (!have) { r = x; have = true; }
         else r = x + r;
       }
@@ -219,24 +270,24 @@ struct FoldMem {
 // push(p, c, mem) pushes the partial with index c at this level: at each level whose bit of c is set the
 // stored block is merged (earlier block on the left) and the carry moves up.  The caller keeps the chunk
 // count below 2^MAXL.
-template <int R>
+template <int R, class T>
 struct FoldRegs {
-  v32f s;
-  FoldRegs<R - 1> up;
+  T s;
+  FoldRegs<R - 1, T> up;
   // the stack after c0 pushes of +0: +0 at the set bits of c0
   template <class M>
-  __device__ __forceinline__ void clear(const v32f& z, int64_t c0, M& mem) {
+  __device__ __forceinline__ void clear(const T& z, int64_t c0, M& mem) {
     s = z;
     up.clear(z, c0 >> 1, mem);
   }
   template <class M>
-  __device__ __forceinline__ void push(v32f p, int64_t c, M& mem) {
+  __device__ __forceinline__ void push(T p, int64_t c, M& mem) {
     if (c & 1) up.push(s + p, c >> 1, mem);
     else s = p;
   }
   // Result: lowest occupied level first, then the others in ascending level order
   template <class M>
-  __device__ __forceinline__ void result(v32f& r, bool& have, int64_t n, const M& mem) const {
+  __device__ __forceinline__ void result(T& r, bool& have, int64_t n, const M& mem) const {
     if (n & 1) {
       if (!have) { r = s; have = true; }
       else r = s + r;
@@ -244,26 +295,28 @@ struct FoldRegs {
     up.result(r, have, n >> 1, mem);
   }
 };
-template <>
-struct FoldRegs<0> {
+template <class T>
+struct FoldRegs<0, T> {
   template <class M>
-  __device__ __forceinline__ void clear(const v32f&, int64_t c0, M& mem) { mem.clear(c0); }
+  __device__ __forceinline__ void clear(const T&, int64_t c0, M& mem) { mem.clear(c0); }
   template <class M>
-  __device__ __forceinline__ void push(v32f p, int64_t c, M& mem) { mem.push(p, c); }
+  __device__ __forceinline__ void push(T p, int64_t c, M& mem) { mem.push(p, c); }
   template <class M>
-  __device__ __forceinline__ void result(v32f& r, bool& have, int64_t n, const M& mem) const {
+  __device__ __forceinline__ void result(T& r, bool& have, int64_t n, const M& mem) const {
     mem.result(r, have, n);
   }
 };
 
-template <int MAXL, bool TA, bool TB>
-__global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
+template <int MAXL, bool TA, bool TB, class CF>
+__global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel(GemmArgs g) {
+  typedef typename Mfma<CF::V>::T vec;
+  constexpr int NT = CF::NT, TBN = CF::TBN, V = CF::V, WR = Mfma<V>::WR;
   __shared__ __attribute__((aligned(16))) float As[2][A_FLOATS];
-  __shared__ __attribute__((aligned(16))) float Bs[2][B_FLOATS];
+  __shared__ __attribute__((aligned(16))) float Bs[2][CF::BFL];
   // the stack holds levels >= 2 (levels 0 and 1 live inside the group code): register levels (three for
   // the row/row layout, two for layouts with k-major staging, which need more address registers), the
   // rest in private memory
-  constexpr int RLMAX = (!TA && TB) ? 3 : 2;
+  constexpr int RLMAX = (!TA && TB) ? CF::RLR : CF::RLK;
   constexpr int RL = (MAXL - 2) < RLMAX ? (MAXL - 2) : RLMAX;
   constexpr int NMEM = MAXL - 2 - RL;
 
@@ -271,7 +324,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   // tiles; then walk that run in groups of GM tile rows (column of GM tiles, then the next column), so the
   // workgroups resident on one XCD share a few A and B tiles in its L2
   constexpr int64_t GM = 8;
-  const int64_t tiles_n = (g.n + BN - 1) / BN;
+  const int64_t tiles_n = (g.n + TBN - 1) / TBN;
   const int64_t tiles_m = (g.m + BM - 1) / BM;
   const int64_t tiles = tiles_m * tiles_n;
   int64_t tile = blockIdx.x;
@@ -294,22 +347,22 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     tn = rank % tiles_n;
     if (g.kmode == KMODE_TRAIL) tm = tiles_m - 1 - tm;
   }
-  const int64_t row0 = tm * BM, col0 = tn * BN;
+  const int64_t row0 = tm * BM, col0 = tn * TBN;
   const bool upper_dead = g.tri_lower && col0 > row0 + BM - 1;                           // above the diagonal
-  const bool band_dead = g.tri_lower && g.kwin > 0 && col0 + BN - 1 <= row0 - g.kwin;   // left of the window
+  const bool band_dead = g.tri_lower && g.kwin > 0 && col0 + TBN - 1 <= row0 - g.kwin;   // left of the window
   if ((upper_dead && !(g.zero_dead && g.epi == EPI_DS)) || (band_dead && g.epi != EPI_DS)) return;
   const bool dead = upper_dead || band_dead;  // the epilogue writes this tile's +0
 
   const int64_t z1 = z / g.nb2, z2 = z % g.nb2;
   const uint16_t* A = g.a + z1 * g.sa1 + z2 * g.sa2;
   const uint16_t* B = g.b + z1 * g.sb1 + (g.b_group > 1 ? z2 / g.b_group : z2) * g.sb2;
-  const bool vec = g.vec != 0;
-  const bool tile_in = vec && row0 + BM <= g.m && col0 + BN <= g.n;
+  const bool vload = g.vec != 0;
+  const bool tile_in = vload && row0 + BM <= g.m && col0 + TBN <= g.n;
 
   const int lane = threadIdx.x & 63;
   const int w = threadIdx.x >> 6;
-  const int wr = w >> 1, wc = w & 1;
-  const int ai = wr * 32 + (lane & 31);  // this lane's A row within the tile
+  const int wr = w / CF::WC, wc = w % CF::WC;
+  const int ai = wr * WR + Mfma<V>::arow(lane);  // this lane's A row within the tile
   const int bi = wc * 64 + lane;         // this lane's B column within the tile
 
   const int64_t nc = (g.k + KC - 1) / KC;
@@ -339,43 +392,43 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   }
   if (dead) lb = le = 0;
 
-  v32f zero;
+  vec zero;
 #pragma unroll
-  for (int v = 0; v < 32; ++v) zero[v] = 0.0f;
+  for (int v = 0; v < V; ++v) zero[v] = 0.0f;
   // Level-2 stack (one entry per aligned group of four chunks).  Groups entirely before lb (in the first
   // segment) are skipped chunks: pushing them as +0 partials leaves +0 at the set bits of their count,
   // i.e. clear().
-  FoldRegs<RL> S;
-  FoldMem<NMEM> Smem;
+  FoldRegs<RL, vec> S;
+  FoldMem<NMEM, vec> Smem;
   S.clear(zero, lb >> 2, Smem);
 
   int buf = 0;
   if (lb < le)
-    store_chunk<TA, TB>(As[0], Bs[0], load_chunk<TA, TB, false>(g, A, B, row0, col0, lb * KC, vec));
+    store_chunk<TA, TB, NT, TBN>(As[0], Bs[0], load_chunk<TA, TB, false, NT, TBN>(g, A, B, row0, col0, lb * KC, vload));
   __syncthreads();
 
   // generic pipelined chunk (checked loads, ragged chunk allowed): real chunks run in ascending order;
   // nextc is the next real chunk (its loads go ahead of this chunk's chain), or -1
-  auto run_chunk = [&](int64_t c, int64_t nextc) -> v32f {
+  auto run_chunk = [&](int64_t c, int64_t nextc) -> vec {
     const bool more = nextc >= 0;
     Raw nxt;
-    if (more) nxt = load_chunk<TA, TB, false>(g, A, B, row0, col0, nextc * KC, vec);
+    if (more) nxt = load_chunk<TA, TB, false, NT, TBN>(g, A, B, row0, col0, nextc * KC, vload);
     __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
     const int64_t kleft = g.k - c * KC;
-    v32f acc = (kleft >= KC) ? chain_full<TA, TB>(As[buf], Bs[buf], ai, bi)
-                             : chain_part<TA, TB>(As[buf], Bs[buf], ai, bi, (int)kleft);
-    if (more) store_chunk<TA, TB>(As[buf ^ 1], Bs[buf ^ 1], nxt);
+    vec acc = (kleft >= KC) ? chain_full<TA, TB, V, CF::LDMB>(As[buf], Bs[buf], ai, bi)
+                             : chain_part<TA, TB, V, CF::LDMB>(As[buf], Bs[buf], ai, bi, (int)kleft);
+    if (more) store_chunk<TA, TB, NT, TBN>(As[buf ^ 1], Bs[buf ^ 1], nxt);
     __syncthreads();
     buf ^= 1;
     return acc;
   };
   // fast chunk: this and the next chunk full and real (unchecked 16-byte loads)
-  auto run_fast = [&](int64_t c) -> v32f {
-    Raw nxt = load_chunk<TA, TB, true>(g, A, B, row0, col0, (c + 1) * KC, vec);
+  auto run_fast = [&](int64_t c) -> vec {
+    Raw nxt = load_chunk<TA, TB, true, NT, TBN>(g, A, B, row0, col0, (c + 1) * KC, vload);
     __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
-    v32f acc = chain_full<TA, TB>(As[buf], Bs[buf], ai, bi);
+    vec acc = chain_full<TA, TB, V, CF::LDMB>(As[buf], Bs[buf], ai, bi);
     __builtin_amdgcn_sched_barrier(0);
-    store_chunk<TA, TB>(As[buf ^ 1], Bs[buf ^ 1], nxt);
+    store_chunk<TA, TB, NT, TBN>(As[buf ^ 1], Bs[buf ^ 1], nxt);
     __syncthreads();
     buf ^= 1;
     return acc;
@@ -386,7 +439,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     return (base + spc < nc && lb < le) ? base + spc + lb : -1;
   };
   // a chunk of a group in the segment at base: real chunks run, skipped ones are +0 partials
-  auto part = [&](int64_t c, int64_t base) -> v32f {
+  auto part = [&](int64_t c, int64_t base) -> vec {
     return (c - base >= lb && c - base < le) ? run_chunk(c, next_real(c, base)) : zero;
   };
 
@@ -403,22 +456,22 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     const int64_t base = sgi * spc;
     const int64_t c = gj * 4, cl = c - base;
     if (nseg == 1 && cl >= le) break;  // the rest are skipped chunks
-    v32f q;
+    vec q;
     if (cl + 4 <= lb || cl >= le) {
       q = zero + zero;  // a group of skipped chunks
     } else if (tile_in && cl >= lb && cl + 5 <= le && c + 5 <= kfull) {
-      v32f p0 = run_fast(c);
-      v32f p1 = run_fast(c + 1);
-      v32f s01 = p0 + p1;
-      v32f p2 = run_fast(c + 2);
-      v32f p3 = run_fast(c + 3);
+      vec p0 = run_fast(c);
+      vec p1 = run_fast(c + 1);
+      vec s01 = p0 + p1;
+      vec p2 = run_fast(c + 2);
+      vec p3 = run_fast(c + 3);
       q = s01 + (p2 + p3);
     } else {
-      v32f p0 = part(c, base);
-      v32f p1 = part(c + 1, base);
-      v32f s01 = p0 + p1;
-      v32f p2 = part(c + 2, base);
-      v32f p3 = part(c + 3, base);
+      vec p0 = part(c, base);
+      vec p1 = part(c + 1, base);
+      vec s01 = p0 + p1;
+      vec p2 = part(c + 2, base);
+      vec p3 = part(c + 3, base);
       q = s01 + (p2 + p3);
     }
     S.push(q, gj, Smem);
@@ -426,16 +479,16 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   // complete groups made only of skipped trailing chunks: their partial is +0
   for (; gj < ng_full; ++gj) S.push(zero + zero, gj, Smem);
 
-  v32f r = zero;
+  vec r = zero;
   bool have = false;
   const int rem = (int)(nc & 3);
   if (rem) {
     const int64_t c = ng_full * 4;
-    v32f p0 = part(c, 0);
+    vec p0 = part(c, 0);
     if (rem == 1) {
       r = p0;
     } else {
-      v32f p1 = part(c + 1, 0);
+      vec p1 = part(c + 1, 0);
       r = p0 + p1;
       if (rem == 3) r = r + part(c + 2, 0);
     }
@@ -443,17 +496,16 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   }
   S.result(r, have, ng_full, Smem);
 
-  // store: register v, lane l -> block v/16, row (v%4) + 4*(l/32) + 8*((v%16)/4), column l%32
-  const int64_t crow0 = row0 + wr * 32, ccol0 = col0 + wc * 64;
+  // store: register v of lane l -> row Mfma::orow, column Mfma::ocol of the wavefront's block
+  const int64_t crow0 = row0 + wr * WR, ccol0 = col0 + wc * 64;
   if (g.epi == EPI_DS) {
     uint16_t* C = (uint16_t*)g.c + z1 * g.sc1 + z2 * g.sc2;
     const uint16_t* P = g.ds_p + z1 * g.ds_sp1 + z2 * g.ds_sp2;
     const float* Dv = g.ds_d + z1 * g.ds_sd1 + z2 * g.ds_sd2;
 #pragma unroll
-    for (int v = 0; v < 32; ++v) {
-      const int vv = v & 15, blk = v >> 4;
-      const int64_t i = crow0 + (vv & 3) + 4 * (lane >> 5) + 8 * (vv >> 2);
-      const int64_t j = ccol0 + blk * 32 + (lane & 31);
+    for (int v = 0; v < V; ++v) {
+      const int64_t i = crow0 + Mfma<V>::orow(v, lane);
+      const int64_t j = ccol0 + Mfma<V>::ocol(v, lane);
       if (i < g.m && j < g.n) {
         uint16_t o = 0;
         if (j <= i && (g.ds_window == 0 || j > i - g.ds_window)) {
@@ -469,10 +521,9 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
   if (g.epi == EPI_ACCUM) {  // the plan's microbatch accumulation g = RN(g + RN(d * s)) into the fp32 C
     float* C = (float*)g.c + z1 * g.sc1 + z2 * g.sc2;
 #pragma unroll
-    for (int v = 0; v < 32; ++v) {
-      const int vv = v & 15, blk = v >> 4;
-      const int64_t i = crow0 + (vv & 3) + 4 * (lane >> 5) + 8 * (vv >> 2);
-      const int64_t j = ccol0 + blk * 32 + (lane & 31);
+    for (int v = 0; v < V; ++v) {
+      const int64_t i = crow0 + Mfma<V>::orow(v, lane);
+      const int64_t j = ccol0 + Mfma<V>::ocol(v, lane);
       if (i < g.m && j < g.n) {
         const float t = r[v] * g.epi_scale;
         C[i * g.ldc + j] = C[i * g.ldc + j] + t;
@@ -481,10 +532,9 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_kernel(GemmArgs g) {
     return;
   }
 #pragma unroll
-  for (int v = 0; v < 32; ++v) {
-    const int vv = v & 15, blk = v >> 4;
-    const int64_t i = crow0 + (vv & 3) + 4 * (lane >> 5) + 8 * (vv >> 2);
-    const int64_t j = ccol0 + blk * 32 + (lane & 31);
+  for (int v = 0; v < V; ++v) {
+    const int64_t i = crow0 + Mfma<V>::orow(v, lane);
+    const int64_t j = ccol0 + Mfma<V>::ocol(v, lane);
     if (i < g.m && j < g.n) {
       if (g.out_bf16) {
         uint16_t* C = (uint16_t*)g.c + z1 * g.sc1 + z2 * g.sc2;
@@ -649,8 +699,8 @@ __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
   };
   auto load = [&](const ShortTile& T, int c) -> Raw {
     if (g.vec && T.whole && (int64_t)(c + 1) * KC <= g.k)
-      return load_chunk<TA, TB, true>(g, T.A, T.B, T.row0, T.col0, (int64_t)c * KC, true);
-    return load_chunk<TA, TB, false>(g, T.A, T.B, T.row0, T.col0, (int64_t)c * KC, g.vec != 0);
+      return load_chunk<TA, TB, true, 256, BN>(g, T.A, T.B, T.row0, T.col0, (int64_t)c * KC, true);
+    return load_chunk<TA, TB, false, 256, BN>(g, T.A, T.B, T.row0, T.col0, (int64_t)c * KC, g.vec != 0);
   };
 
   if (live == 0) return;
@@ -659,7 +709,7 @@ __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
   if (cw.zl >= nzl) return;
   ShortTile cur = ltile(cw);
   int buf = 0;
-  store_chunk<TA, TB>(As[0], Bs[0], load(cur, 0));
+  store_chunk<TA, TB, 256, BN>(As[0], Bs[0], load(cur, 0));
   __syncthreads();
   Raw pre;  // chunk 1 of the current tile when its loads went ahead of the previous tile's stores
   bool have_pre = false;
@@ -693,10 +743,10 @@ __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
       }
       __builtin_amdgcn_sched_barrier(0);  // keep the loads ahead of this chunk's chain
       const int64_t kleft = g.k - (int64_t)c * KC;
-      const v32f acc = kleft >= KC ? chain_full<TA, TB>(As[buf], Bs[buf], ai, bi)
-                                   : chain_part<TA, TB>(As[buf], Bs[buf], ai, bi, (int)kleft);
+      const v32f acc = kleft >= KC ? chain_full<TA, TB, 32, LDMB>(As[buf], Bs[buf], ai, bi)
+                                   : chain_part<TA, TB, 32, LDMB>(As[buf], Bs[buf], ai, bi, (int)kleft);
       __builtin_amdgcn_sched_barrier(0);
-      if (more) store_chunk<TA, TB>(As[buf ^ 1], Bs[buf ^ 1], nx);
+      if (more) store_chunk<TA, TB, 256, BN>(As[buf ^ 1], Bs[buf ^ 1], nx);
       __syncthreads();
       buf ^= 1;
       if (c == 0) r = acc;
@@ -752,12 +802,31 @@ static hipError_t launch_short(const GemmArgs& g, int64_t nc, int64_t tiles, hip
   return hipGetLastError();
 }
 
+// Workgroup shapes of the general kernel (measured at the 1B shapes; bit-identical results either way).  Both
+// operands k-contiguous (every forward projection, the head): 64 x 64 tiles with the 16x16 instruction, three
+// workgroups per CU (three wavefronts per SIMD in 168 registers, four fold levels in registers), 3-7% faster than
+// the 32x32 shape.  A k-major operand (weight and input gradients): 64 x 128 tiles with the 32x32 instruction,
+// two per CU; there the 16x16 shape lost 2-18% (twice the 4-byte LDS reads per product).
+typedef GemmCfg<16, 1, 3, 4, 4> CfgRowRow;
+typedef GemmCfg<32, 2, 2, 3, 2> CfgKMajor;
+
+template <class CF>
+static dim3 general_grid(const GemmArgs& g) {
+  return dim3((unsigned)(((g.m + BM - 1) / BM) * ((g.n + CF::TBN - 1) / CF::TBN)), 1, (unsigned)g.batch);
+}
+
 template <int MAXL>
-static hipError_t launch_maxl(const GemmArgs& g, dim3 grid, hipStream_t s) {
-  if (!g.trans_a && !g.trans_b) hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false>), grid, dim3(256), 0, s, g);
-  else if (!g.trans_a && g.trans_b) hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, true>), grid, dim3(256), 0, s, g);
-  else if (g.trans_a && !g.trans_b) hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, false>), grid, dim3(256), 0, s, g);
-  else hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, true>), grid, dim3(256), 0, s, g);
+static hipError_t launch_maxl(const GemmArgs& g, hipStream_t s) {
+  typedef CfgRowRow R;
+  typedef CfgKMajor K;
+  if (!g.trans_a && g.trans_b)
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, true, R>), general_grid<R>(g), dim3(R::NT), 0, s, g);
+  else if (!g.trans_a && !g.trans_b)
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false, K>), general_grid<K>(g), dim3(K::NT), 0, s, g);
+  else if (g.trans_a && !g.trans_b)
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, false, K>), general_grid<K>(g), dim3(K::NT), 0, s, g);
+  else
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, true, K>), general_grid<K>(g), dim3(K::NT), 0, s, g);
   return hipGetLastError();
 }
 
@@ -774,18 +843,17 @@ hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
   const int64_t nc = (g.k + KC - 1) / KC;
   int bits = 0;
   while ((int64_t(1) << bits) <= nc) ++bits;  // nc < 2^bits: a push never runs past the top level
-  const int64_t tiles = ((g.m + BM - 1) / BM) * ((g.n + BN - 1) / BN);
+  const int64_t tiles = ((g.m + BM - 1) / BM) * ((g.n + BN - 1) / BN);  // short kernel's tiles
   if (!g.trans_a && g.trans_b && nc >= 1 && nc <= 4 && g.kmode == KMODE_FULL && g.kseg == 0 && g.epi != EPI_ACCUM &&
       BM * g.ldc < (int64_t(1) << 31) && BM * g.ds_ldp < (int64_t(1) << 31) && tiles * g.batch < (int64_t(1) << 31) &&
       g.nb2 > 0 && g.batch % g.nb2 == 0)
     return launch_short(g, nc, tiles * g.batch, s);
-  dim3 grid((unsigned)tiles, 1, (unsigned)g.batch);
-  if (bits <= 3) return launch_maxl<3>(g, grid, s);
-  if (bits <= 5) return launch_maxl<5>(g, grid, s);
-  if (bits <= 7) return launch_maxl<7>(g, grid, s);
-  if (bits <= 9) return launch_maxl<9>(g, grid, s);
-  if (bits <= 11) return launch_maxl<11>(g, grid, s);
-  if (bits <= 12) return launch_maxl<12>(g, grid, s);
+  if (bits <= 3) return launch_maxl<3>(g, s);
+  if (bits <= 5) return launch_maxl<5>(g, s);
+  if (bits <= 7) return launch_maxl<7>(g, s);
+  if (bits <= 9) return launch_maxl<9>(g, s);
+  if (bits <= 11) return launch_maxl<11>(g, s);
+  if (bits <= 12) return launch_maxl<12>(g, s);
   return hipErrorInvalidValue;
 }
 
