@@ -19,8 +19,8 @@
 // the 32-deep B tile are staged through LDS as fp32, widened once and double buffered, with the next chunk's
 // 16-byte global loads in flight during the current chunk's MFMA chain.  An operand whose source is
 // k-contiguous is stored as rows [row][k] (one 16-byte LDS read gives a lane four k values); one whose source
-// is row-contiguous is stored k-major [k][row] (one 4-byte read per k), so neither layout needs a transposing
-// scatter.
+// is row-contiguous is either stored k-major [k][row] (one 4-byte read per k, no transposing scatter) or, in
+// the shapes that read twice as often, scattered into rows with a bank-spreading permutation (LROWX).
 // Fold: inside an aligned group of four chunks the two lowest levels of Algorithm 2 are fixed and merged
 // in place; the group partial is pushed at level 2.  The next levels (2 to 4 of them, by shape) stay in
 // registers; the levels above, touched once per 16 chunks or less often, live in per-lane private memory.
@@ -82,14 +82,23 @@ constexpr int A_FLOATS = (BM * LDK > KC * LDMA) ? BM * LDK : KC * LDMA;
 constexpr int B_FLOATS = (BN * LDK > KC * LDMB) ? BN * LDK : KC * LDMB;
 
 // Workgroup shape of the general kernel: instruction V, WC wavefront columns of 64 (the tile is 64 x 64*WC, the
-// wavefronts (64 / WR) x WC), OCC workgroups per CU, and the number of fold levels kept in registers for the
-// row/row layout (RLR) and the layouts with k-major staging (RLK).
-template <int V_, int WC_, int OCC_, int RLR_, int RLK_>
+// wavefronts (64 / WR) x WC), OCC workgroups per CU, the number of fold levels kept in registers for the
+// row/row layout (RLR) and the layouts with a k-major operand (RLK), and TR: a k-major operand is transposed
+// while it is staged, so that every chain read is a 16-byte row read.
+template <int V_, int WC_, int OCC_, int RLR_, int RLK_, bool TR_ = false>
 struct GemmCfg {
   static constexpr int V = V_, WC = WC_, OCC = OCC_, RLR = RLR_, RLK = RLK_;
+  static constexpr bool TR = TR_;
   static constexpr int NW = (BM / Mfma<V>::WR) * WC, NT = 64 * NW, TBN = 64 * WC, LDMB = TBN + 4;
   static constexpr int BFL = (TBN * LDK > KC * LDMB) ? TBN * LDK : KC * LDMB;
 };
+
+// Layout of an operand tile in LDS: LROW [row][k] (stride LDK); LKM k-major [k][row] (stride LDM); LROWX
+// [row][k] with the 16-byte k segments of row r permuted by r: element (r, k) at r * LDK + (k ^ swz(r)).  LROWX
+// holds transposed k-major sources: the staging thread writes one k of eight consecutive rows, and the permutation
+// (constant over those rows) spreads the eight rows of a wavefront's writes over distinct banks.
+enum { LROW = 0, LKM = 1, LROWX = 2 };
+__device__ __forceinline__ int swz(int r) { return 4 * ((r >> 4) & 7); }
 
 // Raw bf16 data of one chunk for one thread: 8 A elements and 16 B elements, as 16-byte vectors.
 struct Raw {
@@ -165,13 +174,21 @@ __device__ __forceinline__ void st8(float* d, const float (&f)[8]) {
 
 // Registers -> LDS: rows [row][k] for k-contiguous sources, k-major [k][row] otherwise; both are
 // 8 contiguous floats per thread.
-template <bool TA, bool TB, int NT, int TBN>
+// one k of eight consecutive rows r0.. into an LROWX tile
+__device__ __forceinline__ void st8x(float* d, int r0, int k, const float (&f)[8]) {
+  const int kx = k ^ swz(r0);  // r0 is a multiple of 8: the eight rows share swz
+#pragma unroll
+  for (int e = 0; e < 8; ++e) d[(r0 + e) * LDK + kx] = f[e];
+}
+
+template <bool TA, bool TB, int NT, int TBN, bool TR = false>
 __device__ __forceinline__ void store_chunk(float* As, float* Bs, const Raw& r) {
   const int t = threadIdx.x;
   float f[8];
   if (NT == 256 || t < 256) {
     widen8(r.a, f);
     if (!TA) st8(As + (t >> 2) * LDK + (t & 3) * 8, f);
+    else if (TR) st8x(As, (t & 7) * 8, t >> 3, f);
     else st8(As + (t >> 3) * LDMA + (t & 7) * 8, f);
   }
 #pragma unroll
@@ -179,31 +196,46 @@ __device__ __forceinline__ void store_chunk(float* As, float* Bs, const Raw& r) 
     const int idx = t + NT * it;
     widen8(it == 0 ? r.b0 : r.b1, f);
     if (TB) st8(Bs + (idx >> 2) * LDK + (idx & 3) * 8, f);
+    else if (TR) st8x(Bs, (idx % (TBN / 8)) * 8, idx / (TBN / 8), f);
     else st8(Bs + (idx / (TBN / 8)) * (TBN + 4) + (idx % (TBN / 8)) * 8, f);
   }
 }
 
 // four consecutive k values (4*g4 .. 4*g4+3) of this lane's row / column
-template <bool KMAJOR, int LDM>
+template <int L, int LDM>
 __device__ __forceinline__ v4f fetch4(const float* base, int idx, int g4) {
-  if (!KMAJOR) return *reinterpret_cast<const v4f*>(base + idx * LDK + 4 * g4);
+  if (L == LROW) return *reinterpret_cast<const v4f*>(base + idx * LDK + 4 * g4);
+  if (L == LROWX) return *reinterpret_cast<const v4f*>(base + idx * LDK + ((4 * g4) ^ swz(idx)));
   const float* p = base + (4 * g4) * LDM + idx;
   return v4f{p[0], p[LDM], p[2 * LDM], p[3 * LDM]};
 }
+// the single value (idx, kk)
+template <int L, int LDM>
+__device__ __forceinline__ float elem(const float* base, int idx, int kk) {
+  if (L == LROW) return base[idx * LDK + kk];
+  if (L == LROWX) return base[idx * LDK + (kk ^ swz(idx))];
+  return base[kk * LDM + idx];
+}
+// the LDS layout of an operand: transposed (TA for A, !TB for B) sources are k-major unless TR
+template <bool TRANSPOSED, bool TR>
+struct Lay {
+  static constexpr int L = !TRANSPOSED ? LROW : (TR ? LROWX : LKM);
+};
 
 // One full chunk's chain: 32 dependent rank-1 updates from +0, operand reads one group ahead.
-template <bool TA, bool TB, int V, int LDB>
+template <bool TA, bool TB, int V, int LDB, bool TR = false>
 __device__ __forceinline__ typename Mfma<V>::T chain_full(const float* As, const float* Bs, int ai, int bi) {
+  constexpr int LA = Lay<TA, TR>::L, LB = Lay<!TB, TR>::L;
   typename Mfma<V>::T acc;
 #pragma unroll
   for (int v = 0; v < V; ++v) acc[v] = 0.0f;
-  v4f a4 = fetch4<TA, LDMA>(As, ai, 0), b4 = fetch4<!TB, LDB>(Bs, bi, 0);
+  v4f a4 = fetch4<LA, LDMA>(As, ai, 0), b4 = fetch4<LB, LDB>(Bs, bi, 0);
 #pragma unroll
   for (int g4 = 0; g4 < KC / 4; ++g4) {
     v4f an = a4, bn = b4;
     if (g4 + 1 < KC / 4) {
-      an = fetch4<TA, LDMA>(As, ai, g4 + 1);
-      bn = fetch4<!TB, LDB>(Bs, bi, g4 + 1);
+      an = fetch4<LA, LDMA>(As, ai, g4 + 1);
+      bn = fetch4<LB, LDB>(Bs, bi, g4 + 1);
     }
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc = Mfma<V>::step(a4[j], b4[j], acc);
@@ -214,15 +246,16 @@ __device__ __forceinline__ typename Mfma<V>::T chain_full(const float* As, const
 }
 
 // A ragged last chunk: only its kleft < 32 real terms enter the chain.
-template <bool TA, bool TB, int V, int LDB>
+template <bool TA, bool TB, int V, int LDB, bool TR = false>
 __device__ __forceinline__ typename Mfma<V>::T chain_part(const float* As, const float* Bs, int ai, int bi,
                                                           int kleft) {
+  constexpr int LA = Lay<TA, TR>::L, LB = Lay<!TB, TR>::L;
   typename Mfma<V>::T acc;
 #pragma unroll
   for (int v = 0; v < V; ++v) acc[v] = 0.0f;
   for (int kk = 0; kk < kleft; ++kk) {
-    float av = TA ? As[kk * LDMA + ai] : As[ai * LDK + kk];
-    float bv = TB ? Bs[bi * LDK + kk] : Bs[kk * LDB + bi];
+    const float av = elem<LA, LDMA>(As, ai, kk);
+    const float bv = elem<LB, LDB>(Bs, bi, kk);
     acc = Mfma<V>::step(av, bv, acc);
   }
   return acc;
@@ -404,7 +437,7 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
 
   int buf = 0;
   if (lb < le)
-    store_chunk<TA, TB, NT, TBN>(As[0], Bs[0], load_chunk<TA, TB, false, NT, TBN>(g, A, B, row0, col0, lb * KC, vload));
+    store_chunk<TA, TB, NT, TBN, CF::TR>(As[0], Bs[0], load_chunk<TA, TB, false, NT, TBN>(g, A, B, row0, col0, lb * KC, vload));
   __syncthreads();
 
   // generic pipelined chunk (checked loads, ragged chunk allowed): real chunks run in ascending order;
@@ -415,9 +448,9 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
     if (more) nxt = load_chunk<TA, TB, false, NT, TBN>(g, A, B, row0, col0, nextc * KC, vload);
     __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
     const int64_t kleft = g.k - c * KC;
-    vec acc = (kleft >= KC) ? chain_full<TA, TB, V, CF::LDMB>(As[buf], Bs[buf], ai, bi)
-                             : chain_part<TA, TB, V, CF::LDMB>(As[buf], Bs[buf], ai, bi, (int)kleft);
-    if (more) store_chunk<TA, TB, NT, TBN>(As[buf ^ 1], Bs[buf ^ 1], nxt);
+    vec acc = (kleft >= KC) ? chain_full<TA, TB, V, CF::LDMB, CF::TR>(As[buf], Bs[buf], ai, bi)
+                             : chain_part<TA, TB, V, CF::LDMB, CF::TR>(As[buf], Bs[buf], ai, bi, (int)kleft);
+    if (more) store_chunk<TA, TB, NT, TBN, CF::TR>(As[buf ^ 1], Bs[buf ^ 1], nxt);
     __syncthreads();
     buf ^= 1;
     return acc;
@@ -426,9 +459,9 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
   auto run_fast = [&](int64_t c) -> vec {
     Raw nxt = load_chunk<TA, TB, true, NT, TBN>(g, A, B, row0, col0, (c + 1) * KC, vload);
     __builtin_amdgcn_sched_barrier(0);  // keep the next chunk's loads ahead of this chunk's chain
-    vec acc = chain_full<TA, TB, V, CF::LDMB>(As[buf], Bs[buf], ai, bi);
+    vec acc = chain_full<TA, TB, V, CF::LDMB, CF::TR>(As[buf], Bs[buf], ai, bi);
     __builtin_amdgcn_sched_barrier(0);
-    store_chunk<TA, TB, NT, TBN>(As[buf ^ 1], Bs[buf ^ 1], nxt);
+    store_chunk<TA, TB, NT, TBN, CF::TR>(As[buf ^ 1], Bs[buf ^ 1], nxt);
     __syncthreads();
     buf ^= 1;
     return acc;
@@ -802,13 +835,18 @@ static hipError_t launch_short(const GemmArgs& g, int64_t nc, int64_t tiles, hip
   return hipGetLastError();
 }
 
-// Workgroup shapes of the general kernel (measured at the 1B shapes; bit-identical results either way).  Both
-// operands k-contiguous (every forward projection, the head): 64 x 64 tiles with the 16x16 instruction, three
-// workgroups per CU (three wavefronts per SIMD in 168 registers, four fold levels in registers), 3-7% faster than
-// the 32x32 shape.  A k-major operand (weight and input gradients): 64 x 128 tiles with the 32x32 instruction,
-// two per CU; there the 16x16 shape lost 2-18% (twice the 4-byte LDS reads per product).
+// Workgroup shapes of the general kernel (timed at the 1B shapes; bit-identical results with any of them).
+// * Both operands k-contiguous (every forward projection, the head): 64 x 64 tiles with the 16x16 instruction,
+//   three workgroups per CU (three wavefronts per SIMD in 168 registers), four fold levels in registers; 3-7%
+//   faster than 64 x 128 tiles of the 32x32 instruction with two workgroups per CU.
+// * A k-major (weight-gradient layouts): the same 64 x 64 shape with A transposed while staged (LROWX) and
+//   three register fold levels, 0-3% faster than the 32x32 shape; left k-major, its 4-byte LDS reads per
+//   product (twice as many as with the 32x32 instruction) made it 2-18% slower.
+// * Only B k-major (input gradients): 64 x 128 tiles of the 32x32 instruction, two per CU; the transposed
+//   16x16 shape was 0-6% slower there.
 typedef GemmCfg<16, 1, 3, 4, 4> CfgRowRow;
-typedef GemmCfg<32, 2, 2, 3, 2> CfgKMajor;
+typedef GemmCfg<16, 1, 3, 4, 3, true> CfgAKMajor;
+typedef GemmCfg<32, 2, 2, 3, 2> CfgBKMajor;
 
 template <class CF>
 static dim3 general_grid(const GemmArgs& g) {
@@ -818,15 +856,16 @@ static dim3 general_grid(const GemmArgs& g) {
 template <int MAXL>
 static hipError_t launch_maxl(const GemmArgs& g, hipStream_t s) {
   typedef CfgRowRow R;
-  typedef CfgKMajor K;
+  typedef CfgAKMajor A;
+  typedef CfgBKMajor B;
   if (!g.trans_a && g.trans_b)
     hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, true, R>), general_grid<R>(g), dim3(R::NT), 0, s, g);
   else if (!g.trans_a && !g.trans_b)
-    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false, K>), general_grid<K>(g), dim3(K::NT), 0, s, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false, B>), general_grid<B>(g), dim3(B::NT), 0, s, g);
   else if (g.trans_a && !g.trans_b)
-    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, false, K>), general_grid<K>(g), dim3(K::NT), 0, s, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, false, A>), general_grid<A>(g), dim3(A::NT), 0, s, g);
   else
-    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, true, K>), general_grid<K>(g), dim3(K::NT), 0, s, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, true, A>), general_grid<A>(g), dim3(A::NT), 0, s, g);
   return hipGetLastError();
 }
 
