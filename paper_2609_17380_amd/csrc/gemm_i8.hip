@@ -203,10 +203,11 @@ __device__ __forceinline__ void vm_wait() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);  // expcnt, lgkmcnt left at max
 }
 
-// Whole 256 x 256 tiles (m, n multiples of 256, k of 64, 16-byte aligned rows): 4 wavefronts, each a 128 x 128
-// block of 4 x 4 instructions, so every 16-byte operand read from LDS feeds four instructions.  The 256 int32
-// accumulators per lane live in the accumulation registers; one workgroup per CU, so the pipeline hides every
-// latency inside the wavefront:
+// Whole 256 x 256 tiles (m, n multiples of 256, k of 64, 16-byte aligned rows), one workgroup per CU.  NW = 4:
+// 4 wavefronts, each a 128 x 128 block of 4 x 4 instructions (256 int32 accumulators per lane), one per SIMD.
+// NW = 8 (used): 8 wavefronts, each 128 x 64 as 4 x 2 instructions (128 accumulators), two per SIMD, so one
+// wavefront's direct loads, barrier and LDS waits overlap the other's products (15% faster at k = 2048; LDS
+// reads, 50% more per product, stay well under the CU's LDS bandwidth).  The pipeline:
 //  * stages of 64 k bytes go from global memory straight into LDS (16-byte direct-to-LDS loads, no register
 //    staging), NBUF = 4 stages deep: stage s + 3 is requested while stage s is multiplied;
 //  * LDS rows are 64 bytes with their four 16-byte segments permuted by the row (segment c of row r at
@@ -219,11 +220,17 @@ __device__ __forceinline__ void vm_wait() {
 // stage s - 1, which every wavefront passes only once its reads of stage s - 1 have completed; stage s + 1 is
 // read after the barrier inside stage s, which every wavefront passes only once its own loads of stage s + 1
 // have landed.
-template <int NBUF>
-__global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
+// NW = 8: eight wavefronts (two per SIMD), each a 128 x 64 block of 4 x 2 instructions (128 accumulators), four
+// direct loads per wavefront and stage.
+template <int NBUF, int NW>
+__global__ __launch_bounds__(64 * NW, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
   constexpr int BM = 256, BN = 256, KS = 64, ROWB = 64;
   constexpr int STAGE = (BM + BN) * KS;  // bytes per stage: A rows, then B rows
   static_assert(NBUF == 4, "three stages ahead: the waits below count three");
+  static_assert(NW == 4 || NW == 8, "four or eight wavefronts");
+  constexpr int WC = NW / 2, WCOLS = BN / WC, V2N = WCOLS / 32;  // wavefront columns, its width, its 32-col blocks
+  constexpr int RB = 16 / NW;   // 16-row blocks of A (and of B) each wavefront loads per stage
+  constexpr int LPW = 2 * RB;   // direct loads per wavefront and stage
   __shared__ __attribute__((aligned(1024))) int8_t lds[NBUF * STAGE];
 
   constexpr int64_t GM = 8;
@@ -238,37 +245,37 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
 
   const int t = threadIdx.x, lane = t & 63;
   const int w = __builtin_amdgcn_readfirstlane(t >> 6);
-  const int wr = w >> 1, wc = w & 1;
+  const int wr = w / WC, wc = w % WC;
   // fragment reads: lane (rl, hi) reads row rl of a 32-row block at k segment 2 ks + hi
   const int rl = lane & 31, hi = lane >> 5;
   const int cs = hi ^ (((rl >> 2) ^ (rl & 2)) & 3);
   const int seg0 = 16 * cs, seg1 = 16 * (cs ^ 2);  // positions of segments hi and 2 + hi
-  const int a_off = (128 * wr + rl) * ROWB, b_off = BM * KS + (128 * wc + rl) * ROWB;
-  // direct loads: wavefront w fills row blocks 4 w .. 4 w + 3 (16 rows each) of A and of B; lane l writes
+  const int a_off = (128 * wr + rl) * ROWB, b_off = BM * KS + (WCOLS * wc + rl) * ROWB;
+  // direct loads: wavefront w fills row blocks RB w .. RB w + RB - 1 (16 rows each) of A and of B; lane l writes
   // position l of a block: row l / 4, segment position l % 4, holding global segment (l % 4) ^ sw(row)
   const int dr = lane >> 2;
   const int dseg = (lane & 3) ^ (((dr >> 2) ^ (dr & 2)) & 3);
-  const int8_t* ga = g.a + (row0 + 64 * w + dr) * g.lda + 16 * dseg;
-  const int8_t* gb = g.b + (col0 + 64 * w + dr) * g.ldb + 16 * dseg;
+  const int8_t* ga = g.a + (row0 + 16 * RB * w + dr) * g.lda + 16 * dseg;
+  const int8_t* gb = g.b + (col0 + 16 * RB * w + dr) * g.ldb + 16 * dseg;
   const int64_t sta = 16 * g.lda, stb = 16 * g.ldb;
 
-  i32x16 acc[4][4];
+  i32x16 acc[4][V2N];
 #pragma unroll
   for (int h = 0; h < 4; ++h)
 #pragma unroll
-    for (int v2 = 0; v2 < 4; ++v2)
+    for (int v2 = 0; v2 < V2N; ++v2)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[h][v2][v] = 0;
 
   const int64_t ns = g.k / KS;
-  i32x4 fa[2][4], fb[2][4];  // two fragment sets
+  i32x4 fa[2][4], fb[2][V2N];  // two fragment sets
   // wavefront-uniform LDS byte address of this wavefront's first row block in stage buffer 0
-  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) int8_t*)lds + 64 * w * ROWB;
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) int8_t*)lds + 16 * RB * w * ROWB;
   auto issue = [&](int64_t st) {
     const unsigned base = lds0 + (unsigned)(st & (NBUF - 1)) * STAGE;
     const int64_t k0 = st * KS;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < RB; ++i) {
       dma16(ga + i * sta + k0, base + 16 * i * ROWB);
       dma16(gb + i * stb + k0, base + BM * KS + 16 * i * ROWB);
     }
@@ -279,13 +286,13 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
 #pragma unroll
     for (int h = 0; h < 4; ++h) fa[f][h] = *reinterpret_cast<const i32x4*>(base + a_off + 32 * h * ROWB + so);
 #pragma unroll
-    for (int v2 = 0; v2 < 4; ++v2) fb[f][v2] = *reinterpret_cast<const i32x4*>(base + b_off + 32 * v2 * ROWB + so);
+    for (int v2 = 0; v2 < V2N; ++v2) fb[f][v2] = *reinterpret_cast<const i32x4*>(base + b_off + 32 * v2 * ROWB + so);
   };
   auto mma = [&](int f) {
 #pragma unroll
     for (int h = 0; h < 4; ++h)
 #pragma unroll
-      for (int v2 = 0; v2 < 4; ++v2)
+      for (int v2 = 0; v2 < V2N; ++v2)
         acc[h][v2] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[f][h], fb[f][v2], acc[h][v2], 0, 0, 0);
   };
 
@@ -293,26 +300,26 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
   if (ns > 1) issue(1);
   if (ns > 2) issue(2);
   // stage 0 landed (this wavefront's loads of stages 1 and 2 may still be in flight), then everyone's
-  if (ns > 2) vm_wait<16>();
-  else if (ns > 1) vm_wait<8>();
+  if (ns > 2) vm_wait<2 * LPW>();
+  else if (ns > 1) vm_wait<LPW>();
   else vm_wait<0>();
   __syncthreads();
   frags(0, 0, 0);
   // Every stage but the last: no branch around LDS operations inside the loop, so the compiler's wait counts
   // stay exact (the last k step's instructions wait only for their own fragments, not for the next stage's
   // reads issued after the barrier).
-  // k step 0 of a stage with the 8 loads of stage st + 3 spread over its 16 instructions (one load after every
-  // two): issued in one burst they stall the wavefront, the only one on its SIMD, while the matrix core idles
+  // k step 0 of a stage with the LPW loads of stage st + 3 spread over its 4 V2N instructions (one load after
+  // every two): issued in one burst they stall the wavefront while the matrix core idles
   auto mma0_loads = [&](int64_t st3, bool more) {  // more: stage st3 exists (wavefront-uniform)
     const unsigned base = lds0 + (unsigned)(st3 & (NBUF - 1)) * STAGE;
     const int64_t k0 = st3 * KS;
 #pragma unroll
     for (int h = 0; h < 4; ++h)
 #pragma unroll
-      for (int v2 = 0; v2 < 4; ++v2) {
+      for (int v2 = 0; v2 < V2N; ++v2) {
         acc[h][v2] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[0][h], fb[0][v2], acc[h][v2], 0, 0, 0);
         if (v2 & 1) {
-          const int i = h, ab = v2 >> 1;  // pieces in order A0, B0, A1, B1, ...
+          const int j = (h * V2N + v2) >> 1, i = j >> 1, ab = j & 1;  // pieces in order A0, B0, A1, B1, ...
           if (more) {
             if (ab == 0) dma16(ga + i * sta + k0, base + 16 * i * ROWB);
             else dma16(gb + i * stb + k0, base + BM * KS + 16 * i * ROWB);
@@ -326,31 +333,33 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
     mma0_loads(st + 3, st + 3 < ns);
     __builtin_amdgcn_sched_barrier(0);
     // this wavefront's loads of stage st + 1 landed (those of later stages may stay in flight), then everyone's
-    if (st + 3 < ns) vm_wait<16>();
-    else if (st + 2 < ns) vm_wait<8>();
+    if (st + 3 < ns) vm_wait<2 * LPW>();
+    else if (st + 2 < ns) vm_wait<LPW>();
     else vm_wait<0>();
     __syncthreads();
     frags(0, st + 1, 0);
     mma(1);
     // the next stage's reads first, under this step's 16 instructions
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4 + V2N, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * V2N, 0);
     __builtin_amdgcn_sched_barrier(0);
   }
   frags(1, ns - 1, 1);
   mma(0);
   mma(1);
 
-  // Epilogue through LDS, 32 rows of the wavefront's 128 x 128 block at a time, so that every lane stores 16
-  // contiguous bytes (4 columns) and a store instruction covers two 512-byte row segments.  Result layout of
+  // Epilogue through LDS, 32 rows of the wavefront's 128 x WCOLS block at a time, so that every lane stores 16
+  // contiguous bytes (4 columns) and a store instruction covers 64 / (WCOLS / 4) row segments of 4 WCOLS bytes.  Result layout of
   // the instruction: register v, lane (rl, hi) -> row (v % 4) + 4 hi + 8 (v / 4), column rl of the 32 x 32
   // block.  Each wavefront writes and reads back only its own LDS region (LDS operations of a wavefront complete
   // in order); the barrier first lets every wavefront finish reading the last stage.
-  constexpr int ELD = 136;  // padded row (ints): the two half-wavefronts' rows 4 apart fall on other banks
+  constexpr int ELD = WCOLS + 8;  // padded row (ints): the two half-wavefronts' rows 4 apart fall on other banks
+  constexpr int LPR = WCOLS / 4, RPI = 64 / LPR;  // read-back lanes per row, rows per instruction
+  static_assert(NW * 32 * ELD * 4 <= NBUF * STAGE, "epilogue rows fit in the stage buffers");
   __syncthreads();
   int32_t* eb = reinterpret_cast<int32_t*>(lds) + w * (32 * ELD);
-  const int64_t wrow = row0 + 128 * wr, wcol = col0 + 128 * wc;
-  const int c4 = 4 * rl;  // this lane's 4 columns in the read-back
+  const int64_t wrow = row0 + 128 * wr, wcol = col0 + WCOLS * wc;
+  const int c4 = 4 * (lane % LPR), rq = lane / LPR;  // this lane's 4 columns and row offset in the read-back
   float sa = 0.0f, sb4[4] = {0.0f, 0.0f, 0.0f, 0.0f};
   if (g.y) {
     sa = *g.sa;
@@ -360,12 +369,12 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
 #pragma unroll
-    for (int v2 = 0; v2 < 4; ++v2)
+    for (int v2 = 0; v2 < V2N; ++v2)
 #pragma unroll
       for (int v = 0; v < 16; ++v) eb[((v & 3) + 4 * hi + 8 * (v >> 2)) * ELD + 32 * v2 + rl] = acc[h][v2][v];
 #pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const int r = 2 * q + hi;
+    for (int q = 0; q < 32 / RPI; ++q) {
+      const int r = RPI * q + rq;
       const i32x4 x = *reinterpret_cast<const i32x4*>(eb + r * ELD + c4);
       const int64_t o = (wrow + 32 * h + r) * g.ldc + wcol + c4;
       if (g.y) {  // streamed out: nontemporal
@@ -381,9 +390,11 @@ __global__ __launch_bounds__(256, 1) void gemm_i8_tile_kernel(GemmI8Args g) {
   }
 }
 
+constexpr int kI8TileWaves = 8;
+
 static hipError_t launch_i8_tile(const GemmI8Args& g, hipStream_t s) {
   const int64_t tiles = (g.m / 256) * (g.n / 256);
-  hipLaunchKernelGGL((gemm_i8_tile_kernel<4>), dim3((unsigned)tiles), dim3(256), 0, s, g);
+  hipLaunchKernelGGL((gemm_i8_tile_kernel<4, kI8TileWaves>), dim3((unsigned)tiles), dim3(64 * kI8TileWaves), 0, s, g);
   return hipGetLastError();
 }
 
