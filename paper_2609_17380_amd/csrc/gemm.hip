@@ -318,6 +318,13 @@ struct FoldRegs {
     if (c & 1) up.push(s + p, c >> 1, mem);
     else s = p;
   }
+  // push(a + b, c), with the sum formed at the level where the carry stops, so that it is computed straight
+  // into that level's registers (no copy)
+  template <class M>
+  __device__ __forceinline__ void push_sum(const T& a, const T& b, int64_t c, M& mem) {
+    if (c & 1) up.push_sum(s, a + b, c >> 1, mem);
+    else s = a + b;
+  }
   // Result: lowest occupied level first, then the others in ascending level order
   template <class M>
   __device__ __forceinline__ void result(T& r, bool& have, int64_t n, const M& mem) const {
@@ -334,6 +341,8 @@ struct FoldRegs<0, T> {
   __device__ __forceinline__ void clear(const T&, int64_t c0, M& mem) { mem.clear(c0); }
   template <class M>
   __device__ __forceinline__ void push(T p, int64_t c, M& mem) { mem.push(p, c); }
+  template <class M>
+  __device__ __forceinline__ void push_sum(const T& a, const T& b, int64_t c, M& mem) { mem.push(a + b, c); }
   template <class M>
   __device__ __forceinline__ void result(T& r, bool& have, int64_t n, const M& mem) const {
     mem.result(r, have, n);
@@ -489,25 +498,29 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
     const int64_t base = sgi * spc;
     const int64_t c = gj * 4, cl = c - base;
     if (nseg == 1 && cl >= le) break;  // the rest are skipped chunks
-    vec q;
+    vec qa, qb;  // the group's partial is qa + qb
     if (cl + 4 <= lb || cl >= le) {
-      q = zero + zero;  // a group of skipped chunks
+      qa = zero;  // a group of skipped chunks: +0 + +0
+      qb = zero;
     } else if (tile_in && cl >= lb && cl + 5 <= le && c + 5 <= kfull) {
       vec p0 = run_fast(c);
       vec p1 = run_fast(c + 1);
-      vec s01 = p0 + p1;
+      qa = p0 + p1;
       vec p2 = run_fast(c + 2);
       vec p3 = run_fast(c + 3);
-      q = s01 + (p2 + p3);
+      qb = p2 + p3;
     } else {
       vec p0 = part(c, base);
       vec p1 = part(c + 1, base);
-      vec s01 = p0 + p1;
+      qa = p0 + p1;
       vec p2 = part(c + 2, base);
       vec p3 = part(c + 3, base);
-      q = s01 + (p2 + p3);
+      qb = p2 + p3;
     }
-    S.push(q, gj, Smem);
+    // the 16x16 shapes form the pushed sum at its level (1-5% faster on the weight gradients); the 32x32 shape
+    // was 0-1% faster pushing the formed sum
+    if (V == 16) S.push_sum(qa, qb, gj, Smem);
+    else S.push(qa + qb, gj, Smem);
   }
   // complete groups made only of skipped trailing chunks: their partial is +0
   for (; gj < ng_full; ++gj) S.push(zero + zero, gj, Smem);
