@@ -144,13 +144,15 @@ def kernel_table(C, I, torch, np, stream, dev, groups=KERNEL_GROUPS):
         return group in groups
 
     if want("gemm"):
-        for name, m, n, k, ta, tb in GEMM_SWEEP:
+        for si, (name, m, n, k, ta, tb) in enumerate(GEMM_SWEEP):
             a = randn((k, m) if ta else (m, k), dtype=torch.bfloat16)
             b = randn((n, k) if tb else (k, n), dtype=torch.bfloat16)
             c = torch.empty((m, n), dtype=torch.float32, device=dev)
             lda, ldb = a.shape[1], b.shape[1]
-            # two warm launches: the first shape of the sweep otherwise carries the clock ramp after the step replays
-            ms = _timed(torch, stream, lambda: C.gemm(m, n, k, a, lda, b, ldb, c, n, ta, tb, stream=stream), 5, warm=2)
+            # warm launches (ten before the first shape of the sweep, which otherwise carries the clock ramp after
+            # the step replays and the state hash)
+            ms = _timed(torch, stream, lambda: C.gemm(m, n, k, a, lda, b, ldb, c, n, ta, tb, stream=stream), 5,
+                        warm=10 if si == 0 else 2)
             tf = 2.0 * m * n * k / (ms * 1e-3) / 1e12
             out[f"gemm_{name}_{m}x{n}x{k}"] = {"bound": "mfma", "ms": round(ms, 4), "achieved": round(tf, 2),
                                                "unit": "TFLOP/s", "peak": PEAK_FP32_MFMA,
