@@ -338,10 +338,12 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
   if (D.int8) {
     canon_status st = qproj_fwd(D, 1, sv.O, sc.tmp_d, sv, s);
     if (st != CANON_OK) return st;
-  } else {
-    TRY(gemm(mk(0, 1, T, d, d, sv.O, d, w[2], d, sc.tmp_d, d), s));
+    TRY(add_f32_launch(T * d, x, sc.tmp_d, sv.h, s));
+  } else {  // h = x + O W_o^T, the residual addition in the GEMM's epilogue
+    GemmArgs g = mk(0, 1, T, d, d, sv.O, d, w[2], d, sv.h, d);
+    g.epi = EPI_RES; g.res = x; g.ldres = d;
+    TRY(gemm(g, s));
   }
-  TRY(add_f32_launch(T * d, x, sc.tmp_d, sv.h, s));
   TRY(rownorm_fwd_launch(T, d, sv.h, w[3], D.eps, sv.hn, sv.rstd2, s));
   if (D.int8) {
     canon_status st = qproj_fwd(D, 2, sv.hn, sv.gu, sv, s);
@@ -353,10 +355,12 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
   if (D.int8) {
     canon_status st = qproj_fwd(D, 3, sv.a, sc.tmp_d, sv, s);
     if (st != CANON_OK) return st;
-  } else {
-    TRY(gemm(mk(0, 1, T, d, F, sv.a, F, w[5], F, sc.tmp_d, d), s));
+    TRY(add_f32_launch(T * d, sv.h, sc.tmp_d, y, s));
+  } else {  // y = h + a W_down^T
+    GemmArgs g = mk(0, 1, T, d, F, sv.a, F, w[5], F, y, d);
+    g.epi = EPI_RES; g.res = sv.h; g.ldres = d;
+    TRY(gemm(g, s));
   }
-  TRY(add_f32_launch(T * d, sv.h, sc.tmp_d, y, s));
   return CANON_OK;
 }
 
@@ -383,9 +387,8 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
     TRY(gemm(mk(1, 0, 2 * F, d, T, sc.dgu, 2 * F, sv.hn, d, dw[4], d), s)); // dW_gate_up = dgu^T hn
     TRY(gemm(mk(0, 0, T, d, 2 * F, sc.dgu, 2 * F, w[4], d, sc.dtmp, d), s)); // dhn = dgu W_gate_up
   }
-  TRY(rownorm_bwd_launch(T, d, sv.h, w[3], sv.rstd2, sc.dtmp, sc.dtmp2, dw[3], s));
-  TRY(add_f32_launch(T * d, dy, sc.dtmp2, sc.dh, s));                     // dh = dy + norm path
-  TRY(cast_bf16_launch(T * d, sc.dh, sc.dy_b, s));
+  // dh = dy + norm path (the residual addition inside the norm's backward), and its bf16 copy
+  TRY(rownorm_bwd_launch(T, d, sv.h, w[3], sv.rstd2, sc.dtmp, sc.dh, dw[3], s, dy, sc.dy_b));
   if (D.int8) {
     if ((qst = qproj_bwd(D, 1, sc.dy_b, sv.O, sc.dOf, dw[2], dw[7], sv, sc, s)) != CANON_OK) return qst;
     TRY(cast_bf16_launch(T * d, sc.dOf, sc.dO, s));
@@ -450,8 +453,7 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
     TRY(gemm(mk(1, 0, N, d, T, sc.dqkv, N, sv.xn, d, dw[1], d), s));       // dW_qkv = dqkv^T xn
     TRY(gemm(mk(0, 0, T, d, N, sc.dqkv, N, w[1], d, sc.dtmp, d), s));      // dxn = dqkv W_qkv
   }
-  TRY(rownorm_bwd_launch(T, d, x, w[0], sv.rstd1, sc.dtmp, sc.dtmp2, dw[0], s));
-  TRY(add_f32_launch(T * d, sc.dh, sc.dtmp2, dx, s));
+  TRY(rownorm_bwd_launch(T, d, x, w[0], sv.rstd1, sc.dtmp, dx, dw[0], s, sc.dh));  // dx = dh + norm path
   return CANON_OK;
 }
 

@@ -34,8 +34,11 @@ struct GemmArgs {
   int64_t ds_ldp, ds_sp1, ds_sp2, ds_sd1, ds_sd2;
   int64_t ds_window;
   float epi_scale;  // EPI_ACCUM
+  const float* res;  // EPI_RES: fp32 [m][ldres] with C's batch offsets
+  int64_t ldres;
 };
-enum { EPI_NONE = 0, EPI_DS = 1, EPI_ACCUM = 2 };  // EPI_ACCUM: C = RN(C + RN(d * epi_scale)) (fp32 C)
+// EPI_ACCUM: C = RN(C + RN(d * epi_scale)) (fp32 C); EPI_RES: C = RN(res + d) (fp32 C, the residual addition)
+enum { EPI_NONE = 0, EPI_DS = 1, EPI_ACCUM = 2, EPI_RES = 3 };
 
 hipError_t gemm_launch(const GemmArgs& g, hipStream_t s);
 
@@ -99,8 +102,10 @@ hipError_t rownorm_fwd_launch(int64_t rows, int64_t cols, const float* x, const 
 // the same with y kept fp32 (the embedding norm)
 hipError_t rownorm_fwd_f32_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, float eps,
                                   float* y, float* rstd, hipStream_t s);
+// res (optional): dx = RN(res + the norm's gradient), the residual addition fused; dxb (optional): bf16 copy of dx
 hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
-                              const float* dy, float* dx, float* dgain, hipStream_t s);
+                              const float* dy, float* dx, float* dgain, hipStream_t s, const float* res = nullptr,
+                              uint16_t* dxb = nullptr);
 // window > 0: query i sees keys i - window < j <= i
 hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, int64_t window,
                                  uint16_t* probs, hipStream_t s);

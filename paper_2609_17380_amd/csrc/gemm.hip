@@ -564,6 +564,17 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
     }
     return;
   }
+  if (g.epi == EPI_RES) {  // the residual addition RN(res + d) into the fp32 C
+    float* C = (float*)g.c + z1 * g.sc1 + z2 * g.sc2;
+    const float* R = g.res + z1 * g.sc1 + z2 * g.sc2;
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      const int64_t i = crow0 + Mfma<V>::orow(v, lane);
+      const int64_t j = ccol0 + Mfma<V>::ocol(v, lane);
+      if (i < g.m && j < g.n) C[i * g.ldc + j] = R[i * g.ldres + j] + r[v];
+    }
+    return;
+  }
   if (g.epi == EPI_ACCUM) {  // the plan's microbatch accumulation g = RN(g + RN(d * s)) into the fp32 C
     float* C = (float*)g.c + z1 * g.sc1 + z2 * g.sc2;
 #pragma unroll
@@ -897,6 +908,7 @@ hipError_t gemm_launch(const GemmArgs& gin, hipStream_t s) {
   while ((int64_t(1) << bits) <= nc) ++bits;  // nc < 2^bits: a push never runs past the top level
   const int64_t tiles = ((g.m + BM - 1) / BM) * ((g.n + BN - 1) / BN);  // short kernel's tiles
   if (!g.trans_a && g.trans_b && nc >= 1 && nc <= 4 && g.kmode == KMODE_FULL && g.kseg == 0 && g.epi != EPI_ACCUM &&
+      g.epi != EPI_RES &&
       BM * g.ldc < (int64_t(1) << 31) && BM * g.ds_ldp < (int64_t(1) << 31) && tiles * g.batch < (int64_t(1) << 31) &&
       g.nb2 > 0 && g.batch % g.nb2 == 0)
     return launch_short(g, nc, tiles * g.batch, s);

@@ -225,12 +225,14 @@ __global__ __launch_bounds__(256) void rownorm_fwd_kernel(int64_t rows, int64_t 
 }
 
 // RMSNorm backward (dx): one wavefront per row.
+// res (optional): dx = RN(res + the norm's gradient), the residual addition; dxb (optional): bf16 copy of dx.
 template <int W>
 __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t cols, const float* __restrict__ x,
                                                           const uint16_t* __restrict__ gain,
                                                           const float* __restrict__ rstd,
                                                           const float* __restrict__ dy, float inv_d,
-                                                          float* __restrict__ dx) {
+                                                          float* __restrict__ dx, const float* __restrict__ res,
+                                                          uint16_t* __restrict__ dxb) {
   __shared__ WaveStage st[4];
   extern __shared__ float dyn[];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -267,7 +269,19 @@ __global__ __launch_bounds__(256) void rownorm_bwd_kernel(int64_t rows, int64_t 
       float b = xv[i] * q;
       o[i] = a - b;
     }
+    if (res) {
+      float rv[W];
+      ldf<W>(res + row * cols + k, rv);
+#pragma unroll
+      for (int i = 0; i < W; ++i) o[i] = rv[i] + o[i];
+    }
     stf<W>(dx + row * cols + k, o);
+    if (dxb) {
+      uint16_t h[W];
+#pragma unroll
+      for (int i = 0; i < W; ++i) h[i] = f32_to_bf16(o[i]);
+      stb<W>(dxb + row * cols + k, h);
+    }
   }
 }
 
@@ -322,7 +336,8 @@ __global__ __launch_bounds__(256) void rownorm_bwd_reg_kernel(int64_t rows, int6
                                                               const uint16_t* __restrict__ gain,
                                                               const float* __restrict__ rstd,
                                                               const float* __restrict__ dy, float inv_d,
-                                                              float* __restrict__ dx) {
+                                                              float* __restrict__ dx, const float* __restrict__ res,
+                                                              uint16_t* __restrict__ dxb) {
   __shared__ WaveStage st[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
@@ -363,7 +378,19 @@ __global__ __launch_bounds__(256) void rownorm_bwd_reg_kernel(int64_t rows, int6
         float b = xv[q][t] * qq;
         o[t] = a - b;
       }
+      if (res) {
+        float rv[4];
+        ldf<4>(res + row * cols + j, rv);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) o[t] = rv[t] + o[t];
+      }
       stf<4>(dx + row * cols + j, o);
+      if (dxb) {
+        uint16_t h[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) h[t] = f32_to_bf16(o[t]);
+        stb<4>(dxb + row * cols + j, h);
+      }
     }
   }
 }
@@ -461,7 +488,9 @@ hipError_t rownorm_fwd_f32_launch(int64_t rows, int64_t cols, const float* x, co
 // dx doubles as the scratch of the dgain chunk partials (ceil(rows/32) x cols floats <= rows x cols), so
 // the dgain launches run before the dx kernel overwrites it.
 hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
-                              const float* dy, float* dx, float* dgain, hipStream_t s) {
+                              const float* dy, float* dx, float* dgain, hipStream_t s, const float* res,
+                              uint16_t* dxb) {
+  if (dgain && res && res == dx) return hipErrorInvalidValue;  // dx holds the dgain partials before res is read
   if (rows == 0) {
     if (dgain) return hipMemsetAsync(dgain, 0, sizeof(float) * cols, s);
     return hipSuccess;
@@ -476,12 +505,17 @@ hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const 
   }
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
-  if (cols % 4 == 0 && cols <= kRegCols && al(x, 16) && al(gain, 8) && al(dy, 16) && al(dx, 16))
-    hipLaunchKernelGGL(rownorm_bwd_reg_kernel, grid, dim3(256), 0, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
-  else if (cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(dy, 16) && al(dx, 16))
-    hipLaunchKernelGGL(rownorm_bwd_kernel<4>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
+  const bool v4 = cols % 4 == 0 && al(x, 16) && al(gain, 8) && al(dy, 16) && al(dx, 16) && (!res || al(res, 16)) &&
+                  (!dxb || al(dxb, 8));
+  if (v4 && cols <= kRegCols)
+    hipLaunchKernelGGL(rownorm_bwd_reg_kernel, grid, dim3(256), 0, s, rows, cols, x, gain, rstd, dy, inv_d, dx, res,
+                       dxb);
+  else if (v4)
+    hipLaunchKernelGGL(rownorm_bwd_kernel<4>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx, res,
+                       dxb);
   else
-    hipLaunchKernelGGL(rownorm_bwd_kernel<1>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx);
+    hipLaunchKernelGGL(rownorm_bwd_kernel<1>, grid, dim3(256), lds, s, rows, cols, x, gain, rstd, dy, inv_d, dx, res,
+                       dxb);
   return hipGetLastError();
 }
 
