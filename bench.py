@@ -310,7 +310,7 @@ def int8_attention(C, torch, stream, dev, randn):
     """The int8 path's attention kernels at the paper's shape (4 sequences x 16 heads (4 key/value heads) x 4096
     tokens, head_dim 128), full causal and 512-token window: P.V in int8 per block (bound by reading P once:
     2 bytes per visible entry, plus V and O) and dQ in 64-bit fixed point (bound by the VALU: one binary64 fma
-    and a 64-bit add, 3 lane-operations, per product)."""
+    and one 64-bit integer add per product, each issuing at half the 32-lane rate, so 4 lane-operations)."""
     o = O1B
     B, Hh, Hkv, Ss, hd = o["mb"], o["H"], o["Hkv"], o["S"], o["hd"]
     out = {}
@@ -330,7 +330,7 @@ def int8_attention(C, torch, stream, dev, randn):
         ms = _timed(torch, stream, lambda: C.attn_dq_fixed(B, Hh, Hkv, Ss, hd, window, 40, P, Vt, dQ,
                                                           stream=stream), 3)
         prods = B * Hh * pairs * hd
-        ops = 3.0 * prods / (ms * 1e-3) / 1e12
+        ops = 4.0 * prods / (ms * 1e-3) / 1e12
         out[f"attn_dq_fixed_{B}x{Hh}x{Ss}x{hd}_w{window}"] = {
             "bound": "alu", "ms": round(ms, 4), "achieved": round(ops, 2), "unit": "T lane-op/s",
             "peak": PEAK_VALU_OPS, "frac": round(ops / PEAK_VALU_OPS, 4),

@@ -356,12 +356,21 @@ struct DqArgs {
   const uint16_t* dS;  // [B][H][S][S]
   const uint16_t* K;   // [B][Hkv][S][hd]
   float* dQ;           // [B][S][ldq], head h at columns h hd ..
-  int64_t S, H, Hkv, hd, window, ldq;
+  int64_t B, S, H, Hkv, hd, window, ldq;
   int F;
   int vec;  // 16-byte loads of dS and K rows allowed
 };
 
 constexpr int DQB = 128;  // R18 query rows per workgroup
+
+// Workgroup -> (query block, sequence x head): the query block index is the slow one and descends, so the
+// whole launch runs its longest rows first (with heads as the fast index, the long blocks of the last heads
+// would start late and leave a tail).
+__device__ __forceinline__ void dq_block(const DqArgs& a, int64_t& qb, int64_t& bh) {
+  const int64_t nbh = a.B * a.H, nqb = (a.S + DQB - 1) / DQB;
+  qb = nqb - 1 - (int64_t)blockIdx.x / nbh;
+  bh = (int64_t)blockIdx.x % nbh;
+}
 
 // The key tiles of one query block, summed into acc.  EXACT = false: the magic-number form (fast); a tile
 // whose bound |dS| 2^F |K| reaches 2^51 makes the call return true, and the caller runs the tiles again with
@@ -374,9 +383,9 @@ __device__ __forceinline__ bool dq_tiles(const DqArgs& a, double (*ds_t)[DQB], d
   constexpr int HD = 16 * C;
   constexpr int KV = (DQK * HD / 8 + 255) / 256;  // 16-byte K vectors per thread per tile
   const int64_t S = a.S, W = a.window;
-  const int64_t nqb = (S + DQB - 1) / DQB;
-  const int64_t qb = nqb - 1 - (int64_t)blockIdx.x;  // longest rows first
-  const int64_t bh = blockIdx.y, b = bh / a.H, h = bh % a.H, g = h / (a.H / a.Hkv);
+  int64_t qb, bh;
+  dq_block(a, qb, bh);
+  const int64_t b = bh / a.H, h = bh % a.H, g = h / (a.H / a.Hkv);
   const int64_t i0 = qb * DQB, i1 = (i0 + DQB < S) ? i0 + DQB : S;
   const uint16_t* dSh = a.dS + bh * S * S;
   const uint16_t* Kh = a.K + (b * a.Hkv + g) * S * HD;
@@ -524,8 +533,9 @@ __global__ __launch_bounds__(256) void attn_dq_fixed_kernel(DqArgs a) {
     dq_tiles<C, true>(a, ds_t, k_t, red, acc, n_fast);
   }
   const int64_t S = a.S;
-  const int64_t qb = (S + DQB - 1) / DQB - 1 - (int64_t)blockIdx.x;
-  const int64_t bh = blockIdx.y, b = bh / a.H, h = bh % a.H;
+  int64_t qb, bh;
+  dq_block(a, qb, bh);
+  const int64_t b = bh / a.H, h = bh % a.H;
   const int rg = threadIdx.x >> 4, cg = threadIdx.x & 15;
   const uint64_t bias = n_fast * kMagicBits;
 #pragma unroll
@@ -565,9 +575,12 @@ hipError_t attn_dq_fixed_launch(int64_t B, int64_t H, int64_t Hkv, int64_t S, in
   if (B == 0) return hipSuccess;
   DqArgs a;
   a.dS = dS; a.K = K; a.dQ = dQ;
-  a.S = S; a.H = H; a.Hkv = Hkv; a.hd = hd; a.window = window; a.ldq = ldq; a.F = F;
+  a.B = B; a.S = S; a.H = H; a.Hkv = Hkv; a.hd = hd; a.window = window; a.ldq = ldq; a.F = F;
   a.vec = (S % 8 == 0) && (((uintptr_t)dS & 15) == 0) && (((uintptr_t)K & 15) == 0);
-  const dim3 grid((unsigned)((S + DQB - 1) / DQB), (unsigned)(B * H));
+  const int64_t nwg = (S + DQB - 1) / DQB * B * H;
+  if (nwg == 0) return hipSuccess;
+  if (nwg > 0xFFFFFFFFll) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)nwg);
   switch (hd) {
     case 16: hipLaunchKernelGGL(attn_dq_fixed_kernel<1>, grid, dim3(256), 0, s, a); break;
     case 32: hipLaunchKernelGGL(attn_dq_fixed_kernel<2>, grid, dim3(256), 0, s, a); break;
