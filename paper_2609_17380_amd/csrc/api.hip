@@ -324,7 +324,10 @@ canon_status block_forward(const Dims& D, const uint16_t* const* w, const float*
     g.b_group = (int32_t)D.G;
     TRY(gemm(g, s));
   }
-  TRY(softmax_causal_launch(D.B * H * S, S, sc.scores, D.scale, D.window, sv.P, s));
+  // P is written only where the P.V and dV products read it, unless dV reads every query (grouped heads
+  // with S not a multiple of 128: one contraction without per-head ranges)
+  const int band = (D.G == 1 || S % 128 == 0) ? 1 : 0;
+  TRY(softmax_causal_launch(D.B * H * S, S, sc.scores, D.scale, D.window, sv.P, s, band));
   if (D.pv_int8) {  // R17: O = P V on the int8 matrix cores, per block of 64 queries x 64 keys
     TRY(attn_pv_i8_launch(D.B, H, Hkv, S, hd, D.window, sv.P, sv.v, nullptr, sv.O, d, sc.qvt, sc.sv, s));
   } else {  // O = P V (keys beyond the tile's last query are masked chunks), bf16 into [T, d]
@@ -398,14 +401,14 @@ canon_status block_backward(const Dims& D, const uint16_t* const* w, const float
   }
   TRY(attn_rowdot_launch(D.B, H, S, hd, sc.dO, sv.O, d, sc.Dv, s));      // D = rowsum(dO * O)
   {  // dP = dO V^T, turned into dS = P * (dP - D) * c in the epilogue (bf16).  Tiles with no visible entry are
-     // not computed: those left of the window band get their +0 written (the windowed dQ and dK ranges may
-     // read them); those above the diagonal stay unwritten with one head per key/value head (the dQ and dK
-     // ranges never reach them), and get their +0 with grouped heads (dK then reads each head's dS whole).
+     // not computed: those left of the window band that the windowed dQ and dK ranges reach get their +0
+     // written, the rest stay unwritten; with grouped heads and S not a multiple of 128, dK reads each
+     // head's dS whole, and every such tile gets its +0.
     GemmArgs g = batched(mk(0, 1, S, S, hd, sc.dO, d, sv.v, hd, sc.dS, S), D, S * d, hd, Hkv * S * hd, S * hd,
                          H * S * S, S * S);
     g.tri_lower = 1;
     g.kwin = D.window;
-    g.zero_dead = G > 1 ? 1 : 0;
+    g.zero_dead = (G > 1 && S % 128 != 0) ? 1 : 0;
     g.b_group = (int32_t)G;
     g.epi = EPI_DS;
     g.ds_p = sv.P; g.ds_d = sc.Dv; g.ds_scale = D.scale; g.ds_window = D.window;

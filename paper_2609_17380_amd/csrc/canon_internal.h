@@ -7,6 +7,12 @@ namespace canon {
 
 enum { KMODE_FULL = 0, KMODE_TRAIL = 1, KMODE_LEAD = 2 };
 
+// Reach of the causally skipping attention products (KMODE_TRAIL with the window kwin, KMODE_LEAD with kwin
+// per K segment): with output tiles of at most 128 rows and chunks of 32, they read row i of a square
+// per-head matrix (P, dS) only at columns i - kwin - kAttnLead <= j < floor(i / 128) * 128 + 128 (from j = 0
+// without a window).  Writers of P and dS may leave everything outside that band unwritten.
+constexpr int64_t kAttnLead = 157;
+
 // One (possibly batched) GEMM.  Matrix z of the batch is (z1, z2) = (z / nb2, z % nb2), with operand
 // offsets z1*s?1 + z2*s?2 (elements).
 struct GemmArgs {
@@ -20,7 +26,8 @@ struct GemmArgs {
   int32_t vec;      // set by the launcher: 16-byte operand loads allowed
   int32_t b_group;  // > 1: B's inner batch offset is (z2 / b_group) * sb2 (grouped key/value heads)
   int64_t kwin;     // > 0: sliding attention window for the KMODE ranges and the tri_lower band
-  int32_t zero_dead;  // EPI_DS with tri_lower: write the +0 of the tiles above the diagonal too
+  int32_t zero_dead;  // EPI_DS with tri_lower: write the +0 of every tile without a visible entry (0: only
+                      // of those left of the window band that the band's readers reach, see kAttnLead)
   int64_t kseg;       // > 0 (a multiple of 128 dividing k): the KMODE ranges repeat in every K segment of kseg
                       // (grouped heads stacked along K); 0: one segment
   // EPI_DS epilogue (attention backward, R5): the finished value d = dP[i][j] of a square per-head matrix
@@ -106,9 +113,10 @@ hipError_t rownorm_fwd_f32_launch(int64_t rows, int64_t cols, const float* x, co
 hipError_t rownorm_bwd_launch(int64_t rows, int64_t cols, const float* x, const uint16_t* gain, const float* rstd,
                               const float* dy, float* dx, float* dgain, hipStream_t s, const float* res = nullptr,
                               uint16_t* dxb = nullptr);
-// window > 0: query i sees keys i - window < j <= i
+// window > 0: query i sees keys i - window < j <= i.  band = 0: every column of probs is written (+0 where
+// masked); band = 1: only the columns the causally skipping products read (kAttnLead), the rest unwritten.
 hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, int64_t window,
-                                 uint16_t* probs, hipStream_t s);
+                                 uint16_t* probs, hipStream_t s, int band = 0);
 hipError_t xent_launch(int64_t rows, int64_t vocab, const uint16_t* logits, const int32_t* targets,
                        float inv_tokens, float z_loss, uint16_t* dlogits, float* row_loss, float* mean_loss,
                        hipStream_t s);

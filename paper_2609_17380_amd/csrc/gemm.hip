@@ -31,7 +31,8 @@
 // sliding window kwin, TRAIL also skips the key chunks before the window of the tile's first query and
 // LEAD the query chunks after the window of the tile's last key.  Output tiles with no visible entry
 // (tri_lower: above the diagonal, or left of the window band) are not computed: the dS epilogue writes
-// their +0 (band tiles always, diagonal tiles when zero_dead), other outputs leave them unwritten.
+// their +0 (every such tile when zero_dead, else the band tiles within the readers' reach, kAttnLead),
+// other outputs leave them unwritten.
 #include <hip/hip_runtime.h>
 
 #include "canon_dev.h"
@@ -76,6 +77,7 @@ struct Mfma<16> {
 };
 
 constexpr int BM = 64, BN = 128, KC = 32;
+static_assert(BM <= 128 && 128 % BM == 0 && KC == 32, "the attention read reach (kAttnLead) assumes these tiles");
 constexpr int LDK = KC + 4;               // row-layout stride (floats): [row][k]
 constexpr int LDMA = BM + 4, LDMB = BN + 4;  // k-major stride (floats): [k][row]
 constexpr int A_FLOATS = (BM * LDK > KC * LDMA) ? BM * LDK : KC * LDMA;
@@ -392,7 +394,9 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
   const int64_t row0 = tm * BM, col0 = tn * TBN;
   const bool upper_dead = g.tri_lower && col0 > row0 + BM - 1;                           // above the diagonal
   const bool band_dead = g.tri_lower && g.kwin > 0 && col0 + TBN - 1 <= row0 - g.kwin;   // left of the window
-  if ((upper_dead && !(g.zero_dead && g.epi == EPI_DS)) || (band_dead && g.epi != EPI_DS)) return;
+  // out of every reader's reach (the dS epilogue writes the +0 of the dead tiles the readers reach)
+  const bool band_far = band_dead && !g.zero_dead && col0 + TBN - 1 < row0 - g.kwin - kAttnLead;
+  if ((upper_dead && !(g.zero_dead && g.epi == EPI_DS)) || (band_dead && (g.epi != EPI_DS || band_far))) return;
   const bool dead = upper_dead || band_dead;  // the epilogue writes this tile's +0
 
   const int64_t z1 = z / g.nb2, z2 = z % g.nb2;
@@ -695,13 +699,17 @@ __global__ __launch_bounds__(256, 2) void gemm_short_kernel(GemmArgs g) {
   auto band_dead = [&](const TileWalk& W) {
     return g.tri_lower && g.kwin > 0 && (int64_t)W.tn * BN + BN - 1 <= (int64_t)W.tm * BM - g.kwin;
   };
+  auto band_far = [&](const TileWalk& W) {  // left of the window band and out of every reader's reach
+    return band_dead(W) && !g.zero_dead &&
+           (int64_t)W.tn * BN + BN - 1 < (int64_t)W.tm * BM - g.kwin - kAttnLead;
+  };
   auto in_range = [&](const ShortTile& T, int v) {
     return T.row0 + lrow + urow(v) < g.m && T.col0 + lcol + ucol(v) < g.n;
   };
   // first, the tiles without a visible entry whose +0 the dS epilogue writes
   if (ds && g.tri_lower && (g.zero_dead || g.kwin > 0)) {
     for (TileWalk W = start(); !done(W); advance(W)) {
-      if (!((upper_dead(W) && g.zero_dead) || band_dead(W))) continue;
+      if (!((upper_dead(W) && g.zero_dead) || (band_dead(W) && !band_far(W)))) continue;
       const ShortTile T = tile_of(W);
       uint16_t* C = (uint16_t*)g.c + T.z1 * g.sc1 + T.z2 * g.sc2 + T.row0 * g.ldc + T.col0;
 #pragma unroll

@@ -590,10 +590,18 @@ hipError_t quant_scales_launch(int64_t rows, int64_t cols, const uint16_t* w, fl
 // ------------------------------------------------------------------------------------------------
 // Causal softmax of raw scores: row r is query i = r mod cols; one wavefront per row, coalesced.  With
 // window > 0 query i sees keys j0 = max(0, i - window + 1) .. i (the hybrid attention's windowed layers).
+// band = 1 writes only the columns [wlo, whi) that the causally skipping products read (kAttnLead).
+__device__ __forceinline__ void band_cols(int band, int64_t i, int64_t window, int64_t cols, int64_t& wlo,
+                                          int64_t& whi) {
+  if (!band) return;
+  const int64_t lo = i - window - kAttnLead, hi = (i / 128) * 128 + 128;
+  wlo = (window > 0 && lo > 0) ? lo : 0;
+  whi = hi < cols ? hi : cols;
+}
 template <int W>
 __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64_t cols, const float* __restrict__ raw,
                                                              float scale, int64_t window,
-                                                             uint16_t* __restrict__ probs) {
+                                                             uint16_t* __restrict__ probs, int band) {
   __shared__ WaveStage st[4];
   extern __shared__ float dyn[];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -629,7 +637,9 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
     }
   }, i + 1, j0);
   const float rcp = 1.0f / S;
-  for (int64_t j = (int64_t)lane * W; j < cols; j += 64 * W) {
+  int64_t wlo = 0, whi = cols;  // columns written
+  band_cols(band, i, window, cols, wlo, whi);
+  for (int64_t j = (wlo / (64 * W)) * (64 * W) + (int64_t)lane * W; j < whi; j += 64 * W) {
     uint16_t o[W];
     if (j <= i && j + W - 1 >= j0) {
       float v[W];
@@ -653,7 +663,8 @@ __global__ __launch_bounds__(256) void softmax_causal_kernel(int64_t rows, int64
 
 __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, int64_t cols,
                                                                  const float* __restrict__ raw, float scale,
-                                                                 int64_t window, uint16_t* __restrict__ probs) {
+                                                                 int64_t window, uint16_t* __restrict__ probs,
+                                                                 int band) {
   __shared__ WaveStage st[4];
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + w;
@@ -693,10 +704,12 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
     }
   const float S = reg_row_sum(st[w], e, cols);
   const float rcp = 1.0f / S;
+  int64_t wlo = 0, whi = cols;  // columns written
+  band_cols(band, i, window, cols, wlo, whi);
 #pragma unroll
   for (int q = 0; q < kRegQ; ++q) {
     const int64_t j = 256 * q + 4 * lane;
-    if (j < cols) {
+    if (j < whi && j + 3 >= wlo) {
       uint16_t o[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) o[t] = ((j + t <= i && j + t >= j0)) ? f32_to_bf16(e[q][t] * rcp) : (uint16_t)0;
@@ -706,16 +719,19 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
 }
 
 hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, int64_t window,
-                                 uint16_t* probs, hipStream_t s) {
+                                 uint16_t* probs, hipStream_t s, int band) {
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
   if (cols % 4 == 0 && cols <= kRegCols && al(raw, 16) && al(probs, 8))
-    hipLaunchKernelGGL(softmax_causal_reg_kernel, grid, dim3(256), 0, s, rows, cols, raw, scale, window, probs);
+    hipLaunchKernelGGL(softmax_causal_reg_kernel, grid, dim3(256), 0, s, rows, cols, raw, scale, window, probs,
+                       band);
   else if (cols % 4 == 0 && al(raw, 16) && al(probs, 8))
-    hipLaunchKernelGGL(softmax_causal_kernel<4>, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs);
+    hipLaunchKernelGGL(softmax_causal_kernel<4>, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs,
+                       band);
   else
-    hipLaunchKernelGGL(softmax_causal_kernel<1>, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs);
+    hipLaunchKernelGGL(softmax_causal_kernel<1>, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs,
+                       band);
   return hipGetLastError();
 }
 

@@ -35,3 +35,9 @@ def assert_bits(got: np.ndarray, want: np.ndarray, what: str):
         raise AssertionError(f"{what}: {bad.size}/{g.size} elements differ; first at {i}: "
                              f"gpu {got.ravel()[i]!r} (0x{int(g.ravel()[i]):x}) oracle {want.ravel()[i]!r} "
                              f"(0x{int(w.ravel()[i]):x})")
+
+
+def poisoned_workspace(nbytes: int) -> torch.Tensor:
+    """A workspace of all-ones bytes (NaN as bf16 and as fp32): a read of any part the library did not write
+    first (outside the ranges its kernels mask) turns into NaN in the results, which the bit comparison sees."""
+    return torch.full((max(int(nbytes), 1),), 255, dtype=torch.uint8, device=DEV)

@@ -11,7 +11,8 @@ import torch
 import oracle
 import paper_2609_17380_amd.canon as C
 import paper_2609_17380_amd.inputs as I
-from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16
+from gpu_util import (DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16,
+                      poisoned_workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -130,7 +131,8 @@ def cfgs(L, d, H, F, V, S, mb, Hkv=0, qk=0, en=0, win=0, every=0, z=0.0, pv=0, d
 
 @pytest.mark.parametrize("d,H,Hkv,qk,win,F,S,batch,pv,dq", [
     (64, 2, 0, 0, 0, 96, 96, 2, 1, 0), (64, 2, 0, 0, 0, 96, 96, 2, 0, 40), (64, 2, 1, 1, 20, 96, 130, 1, 1, 40),
-    (256, 2, 1, 1, 0, 256, 192, 1, 1, 40), (256, 4, 2, 1, 40, 384, 128, 2, 1, 40), (128, 2, 2, 0, 0, 128, 64, 1, 1, 12)])
+    (256, 2, 1, 1, 0, 256, 192, 1, 1, 40), (256, 4, 2, 1, 40, 384, 128, 2, 1, 40), (128, 2, 2, 0, 0, 128, 64, 1, 1, 12),
+    (256, 4, 1, 1, 64, 256, 512, 1, 1, 40)])
 def test_block_int8_attention_bit_exact(d, H, Hkv, qk, win, F, S, batch, pv, dq):
     print(f"block pv={pv} dq={dq} d={d} H={H} Hkv={Hkv} qk={qk} win={win} S={S} B={batch}", flush=True)
     hd = d // H
@@ -144,7 +146,7 @@ def test_block_int8_attention_bit_exact(d, H, Hkv, qk, win, F, S, batch, pv, dq)
          for s, n in zip(shapes, NAMES)]
     cos, sin = I.rope_tables(S, hd)
     y_o, dx_o, dw_o = oracle.block_fwd_bwd(cfg_o, batch, x, dy, w, cos, sin)
-    ws = torch.empty(C.block_workspace_bytes(cfg_c, batch), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.block_workspace_bytes(cfg_c, batch))
     y = torch.empty((T, d), dtype=torch.float32, device=DEV)
     dx = torch.empty_like(y)
     dw = [torch.empty(s, dtype=torch.float32, device=DEV) for s in shapes]
@@ -179,7 +181,7 @@ def test_step_paper_attention_bit_exact():
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params]
     cplan = C.DPPlan(*plan)
-    ws = torch.empty(C.step_workspace_bytes(cfg_c, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg_c, cplan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     norm = torch.zeros(1, dtype=torch.float32, device=DEV)
     state = torch.zeros(1, dtype=torch.int32, device=DEV)

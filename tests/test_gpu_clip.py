@@ -8,7 +8,8 @@ import torch
 import oracle
 import paper_2609_17380_amd.canon as C
 import paper_2609_17380_amd.inputs as I
-from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16
+from gpu_util import (DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16,
+                      poisoned_workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -180,7 +181,7 @@ def run_step(clip, skip_state=0, L=2, d=256, H=2, F=256, V=300, S=64, mb=2, plan
     mg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params]
-    ws = torch.empty(C.step_workspace_bytes(cfg, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg, cplan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     norm = torch.full((1,), -1.0, dtype=torch.float32, device=DEV)
     state = torch.full((1,), skip_state, dtype=torch.int32, device=DEV)
@@ -230,7 +231,7 @@ def test_step_bad_token_with_clip():
     pg = [dev_bf16(p) for p in params]
     mg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
-    ws = torch.empty(C.step_workspace_bytes(cfg, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg, cplan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     norm = torch.zeros(1, dtype=torch.float32, device=DEV)
     state = torch.full((1,), 2, dtype=torch.int32, device=DEV)

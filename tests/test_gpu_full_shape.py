@@ -17,7 +17,7 @@ import torch
 
 import full_shape_cases as FC
 import paper_2609_17380_amd.canon as C
-from gpu_util import DEV, dev_bf16, dev_f32, dev_i32, host_f32, host_u16
+from gpu_util import DEV, dev_bf16, dev_f32, dev_i32, host_f32, host_u16, poisoned_workspace
 
 pytestmark = pytest.mark.gpu
 
@@ -47,7 +47,7 @@ def test_block_d2048_seq2048_matches_oracle():
     x, dy, w, cos, sin = FC.block_inputs(c)
     cfg = C.ModelCfg(1, c["d"], c["H"], c["hd"], c["F"], 100, c["S"], c["batch"], np.float32(c["eps"]))
     T = c["batch"] * c["S"]
-    ws = torch.empty(C.block_workspace_bytes(cfg, c["batch"]), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.block_workspace_bytes(cfg, c["batch"]))
     y = torch.empty((T, c["d"]), dtype=torch.float32, device=DEV)
     dx = torch.empty_like(y)
     dw = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in w]
@@ -72,7 +72,7 @@ def test_step_full_width_matches_oracle():
     mg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params]
-    ws = torch.empty(C.step_workspace_bytes(cfg, plan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg, plan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     norm = torch.zeros(1, dtype=torch.float32, device=DEV)
     state = torch.zeros(1, dtype=torch.int32, device=DEV)

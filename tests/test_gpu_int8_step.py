@@ -11,7 +11,8 @@ import torch
 import oracle
 import paper_2609_17380_amd.canon as C
 import paper_2609_17380_amd.inputs as I
-from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16
+from gpu_util import (DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16,
+                      poisoned_workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -93,7 +94,7 @@ def test_block_int8_projections_bit_exact(d, H, Hkv, qk, win, F, S, batch, pv, d
     shapes += [(1,)] * 4
     cos, sin = I.rope_tables(S, hd)
     y_o, dx_o, dw_o = oracle.block_fwd_bwd(cfg_o, batch, x, dy, w, cos, sin)
-    ws = torch.empty(C.block_workspace_bytes(cfg_c, batch), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.block_workspace_bytes(cfg_c, batch))
     y = torch.empty((T, d), dtype=torch.float32, device=DEV)
     dx = torch.empty_like(y)
     dw = [torch.empty(s, dtype=torch.float32, device=DEV) for s in shapes]
@@ -133,7 +134,7 @@ def test_step_int8_projections_bit_exact(variant, plan):
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params]
     cplan = C.DPPlan(*plan)
-    ws = torch.empty(C.step_workspace_bytes(cfg_c, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg_c, cplan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     norm = torch.zeros(1, dtype=torch.float32, device=DEV)
     state = torch.zeros(1, dtype=torch.int32, device=DEV)

@@ -7,7 +7,8 @@ import torch
 import oracle
 import paper_2609_17380_amd.canon as C
 import paper_2609_17380_amd.inputs as I
-from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16
+from gpu_util import (DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16,
+                      poisoned_workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -26,7 +27,7 @@ def block_case(d, H, F, S, batch, std):
          for s, n in zip(shapes, NAMES)]
     cos, sin = I.rope_tables(S, hd)
     y_o, dx_o, dw_o = oracle.block_fwd_bwd(cfg_o, batch, x, dy, w, cos, sin)
-    ws = torch.empty(C.block_workspace_bytes(cfg_c, batch), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.block_workspace_bytes(cfg_c, batch))
     y = torch.empty((T, d), dtype=torch.float32, device=DEV)
     dx = torch.empty_like(y)
     dw = [torch.empty(s, dtype=torch.float32, device=DEV) for s in shapes]
@@ -65,7 +66,7 @@ def run_step(L, d, H, F, V, S, mb, plan, seed=0, grads=True, windows=None):
     mg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params] if grads else None
-    ws = torch.empty(C.step_workspace_bytes(cfg, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg, cplan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     C.step(cfg, cplan, pg, mg, vg, dev_i32(windows), dev_f32(cos), dev_f32(sin), C.AdamWConsts(*k), ws, loss,
            grads_out=gg)
@@ -120,7 +121,7 @@ def test_step_rejects_bad_tokens_without_update():
     pg = [dev_bf16(p) for p in params]
     mg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
-    ws = torch.empty(C.step_workspace_bytes(cfg, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg, cplan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     C.step(cfg, cplan, pg, mg, vg, dev_i32(windows), dev_f32(cos), dev_f32(sin), C.AdamWConsts(*I.adamw_constants()),
            ws, loss)
@@ -152,7 +153,7 @@ def test_step_state_digest_matches_oracle_state(plan):
                           [m.tobytes() for m in mo] + [v.tobytes() for v in vo] + [g.tobytes() for g in g_o])
     cfg = C.ModelCfg(L, d, H_, hd, F, V, S, mb, np.float32(1e-5))
     cplan = C.DPPlan(*plan)
-    ws = torch.empty(C.step_workspace_bytes(cfg, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg, cplan))
     digests = []
     for run in range(2):
         pg = [dev_bf16(p) for p in params]

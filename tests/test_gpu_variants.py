@@ -10,7 +10,8 @@ import torch
 import oracle
 import paper_2609_17380_amd.canon as C
 import paper_2609_17380_amd.inputs as I
-from gpu_util import DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16
+from gpu_util import (DEV, assert_bits, dev_bf16, dev_f32, dev_i32, host_f32, host_u16,
+                      poisoned_workspace)
 
 pytestmark = pytest.mark.gpu
 
@@ -82,6 +83,9 @@ def cfgs(L, d, H, F, V, S, mb, Hkv=0, qk=0, en=0, win=0, every=0, z=0.0):
                                                      # more score tiles than resident workgroups (1024 and 2048)
                                                      (256, 2, 2, 0, 0, 256, 1024, 4), (512, 16, 4, 1, 200, 512, 1024, 1),
                                                      (256, 2, 1, 1, 300, 256, 1000, 4),
+                                                     # windows far shorter than the sequence: P and dS stay
+                                                     # unwritten beyond the products' reach (poisoned workspace)
+                                                     (256, 2, 2, 1, 50, 256, 512, 1), (256, 4, 1, 0, 64, 256, 640, 1),
                                                      # head dim 48: a ragged second chunk in every per-row reduction
                                                      (192, 4, 4, 0, 0, 256, 96, 2),
                                                      # head dim 544: 17 chunks per attention row dot (the wide path)
@@ -99,7 +103,7 @@ def test_block_variants_bit_exact(d, H, Hkv, qk, win, F, S, batch):
          for s, n in zip(shapes, NAMES)]
     cos, sin = I.rope_tables(S, hd)
     y_o, dx_o, dw_o = oracle.block_fwd_bwd(cfg_o, batch, x, dy, w, cos, sin)
-    ws = torch.empty(C.block_workspace_bytes(cfg_c, batch), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.block_workspace_bytes(cfg_c, batch))
     y = torch.empty((T, d), dtype=torch.float32, device=DEV)
     dx = torch.empty_like(y)
     dw = [torch.empty(s, dtype=torch.float32, device=DEV) for s in shapes]
@@ -132,7 +136,7 @@ def run_step(L, d, H, F, V, S, mb, plan, variant, seed=0, clip=None):
     vg = [torch.zeros(p.shape, dtype=torch.float32, device=DEV) for p in params]
     gg = [torch.empty(p.shape, dtype=torch.float32, device=DEV) for p in params]
     cplan = C.DPPlan(*plan)
-    ws = torch.empty(C.step_workspace_bytes(cfg_c, cplan), dtype=torch.uint8, device=DEV)
+    ws = poisoned_workspace(C.step_workspace_bytes(cfg_c, cplan))
     loss = torch.zeros(1, dtype=torch.float32, device=DEV)
     norm = torch.zeros(1, dtype=torch.float32, device=DEV)
     state = torch.zeros(1, dtype=torch.int32, device=DEV)
