@@ -131,6 +131,19 @@ __device__ __forceinline__ void wave_segment_chunks(int64_t seg0, int64_t n, Wav
 // nz: terms at index >= nz are known to be +0 (masked); z0: so are the terms below z0.  Chunks made only of
 // such terms have partial +0: those at or after nz, and those of whole staging segments below z0, are not
 // staged.
+// Algorithm 2 over the nc chunk partials of one row in parts[] (written and made visible by the caller):
+// lane l folds the block of G consecutive partials it owns, then the lane results are folded across the
+// wavefront.  Returns the row sum in every lane.
+__device__ __forceinline__ float fold_parts(const float* parts, int64_t nc) {
+  const int lane = threadIdx.x & 63;
+  const int64_t G = block_chunks(nc, 64);
+  const int64_t c0 = lane * G, c1 = (c0 + G < nc) ? c0 + G : nc;
+  LocalFold f;
+  for (int64_t c = c0; c < c1; ++c) f.push(parts[c]);
+  float tot = wave_fold(f.result(), (int)((nc + G - 1) / G));
+  return __shfl(tot, 0, 64);
+}
+
 template <int W, class Term>
 __device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* parts, Term term, int64_t nz,
                                                int64_t z0 = 0) {
@@ -142,12 +155,7 @@ __device__ __forceinline__ float wave_row_rsum(int64_t n, WaveStage& st, float* 
   for (int64_t c = (nz + kChunk - 1) / kChunk + lane; c < nc; c += 64) parts[c] = 0.0f;
   __builtin_amdgcn_s_waitcnt(0);
   __builtin_amdgcn_wave_barrier();
-  const int64_t G = block_chunks(nc, 64);
-  const int64_t c0 = lane * G, c1 = (c0 + G < nc) ? c0 + G : nc;
-  LocalFold f;
-  for (int64_t c = c0; c < c1; ++c) f.push(parts[c]);
-  float tot = wave_fold(f.result(), (int)((nc + G - 1) / G));
-  return __shfl(tot, 0, 64);
+  return fold_parts(parts, nc);
 }
 
 constexpr int kMaxRowChunks = 64 * 16;  // rows up to 32768 terms in the wave kernels
@@ -718,12 +726,102 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
   }
 }
 
+// Windowed rows (0 < window <= kBandWin): the visible keys j0 .. i lie in the 768 columns [base, base + 768),
+// base = j0 rounded down to 256, which lane l holds as float4 vectors at base + 256 q + 4 l (q < 3): the row
+// is read from memory once.  The band's 24 chunks are staged in LDS and chained by lanes 0 .. 23 (every
+// other chunk of the row is a +0 partial), and the nc partials are folded as in wave_row_rsum.
+constexpr int64_t kBandWin = 512;
+struct BandStage {
+  float t[24][33];
+};
+__global__ __launch_bounds__(256) void softmax_band_kernel(int64_t rows, int64_t cols, const float* __restrict__ raw,
+                                                           float scale, int64_t window, uint16_t* __restrict__ probs,
+                                                           int band) {
+  __shared__ BandStage st[4];
+  extern __shared__ float dyn[];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= rows) return;
+  const int64_t nc = (cols + kChunk - 1) / kChunk;
+  float* parts = dyn + w * nc;
+  const int64_t i = row % cols;
+  const int64_t j0 = (i - window + 1 > 0) ? i - window + 1 : 0;
+  const int64_t base = (j0 / 256) * 256;
+  const float* rr = raw + row * cols;
+  auto seen = [&](int64_t j) { return j <= i && j >= j0; };
+  float e[3][4];
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const int64_t j = base + 256 * q + 4 * lane;
+    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (j < cols && j <= i && j + 3 >= j0) v = *reinterpret_cast<const float4*>(rr + j);
+    e[q][0] = v.x; e[q][1] = v.y; e[q][2] = v.z; e[q][3] = v.w;
+  }
+  float m = -__builtin_inff();
+#pragma unroll
+  for (int q = 0; q < 3; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      if (seen(base + 256 * q + 4 * lane + t)) m = fmaxf(m, e[q][t] * scale);
+  m = wave_max(m);
+  // masked keys enter the chain as +0 terms
+#pragma unroll
+  for (int q = 0; q < 3; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      float x = 0.0f;
+      if (seen(base + 256 * q + 4 * lane + t)) {
+        float sc = e[q][t] * scale;
+        x = cexp(sc - m);
+      }
+      e[q][t] = x;
+    }
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    const int local = 256 * q + 4 * lane;
+    float* dst = &st[w].t[local >> 5][local & 31];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) dst[t] = e[q][t];
+  }
+  for (int64_t c = lane; c < nc; c += 64) parts[c] = 0.0f;
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  const int64_t cb = base / kChunk + lane;  // this lane's band chunk
+  if (lane < 24 && cb < nc) {
+    const int64_t k1 = cols - cb * kChunk < kChunk ? cols - cb * kChunk : kChunk;
+    float p = 0.0f;
+    for (int k = 0; k < (int)k1; ++k) p = p + st[w].t[lane][k];
+    parts[cb] = p;
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __builtin_amdgcn_wave_barrier();
+  const float S = fold_parts(parts, nc);
+  const float rcp = 1.0f / S;
+  int64_t wlo = 0, whi = cols;  // columns written
+  band_cols(band, i, window, cols, wlo, whi);
+  for (int64_t j = (wlo / 256) * 256 + 4 * lane; j < whi; j += 256) {
+    uint16_t o[4] = {0, 0, 0, 0};
+    const int64_t d = j - base;
+    if (d >= 0 && d < 768) {
+      const int q = (int)(d >> 8);
+      float x[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) x[t] = q == 0 ? e[0][t] : (q == 1 ? e[1][t] : e[2][t]);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) o[t] = seen(j + t) ? f32_to_bf16(x[t] * rcp) : (uint16_t)0;
+    }
+    stb<4>(probs + row * cols + j, o);
+  }
+}
+
 hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, float scale, int64_t window,
                                  uint16_t* probs, hipStream_t s, int band) {
   if (rows == 0) return hipSuccess;
   const dim3 grid((unsigned)((rows + 3) / 4));
   const size_t lds = wave_kernel_lds(cols);
-  if (cols % 4 == 0 && cols <= kRegCols && al(raw, 16) && al(probs, 8))
+  if (window > 0 && window <= kBandWin && cols % 4 == 0 && al(raw, 16) && al(probs, 8))
+    hipLaunchKernelGGL(softmax_band_kernel, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs, band);
+  else if (cols % 4 == 0 && cols <= kRegCols && al(raw, 16) && al(probs, 8))
     hipLaunchKernelGGL(softmax_causal_reg_kernel, grid, dim3(256), 0, s, rows, cols, raw, scale, window, probs,
                        band);
   else if (cols % 4 == 0 && al(raw, 16) && al(probs, 8))
