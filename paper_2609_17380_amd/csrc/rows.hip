@@ -726,6 +726,96 @@ __global__ __launch_bounds__(256) void softmax_causal_reg_kernel(int64_t rows, i
   }
 }
 
+// Rows of 2048 < cols <= 4096 terms held in registers (lane l: terms 4l + 256q .. +3 for q < 16), read from
+// memory once.  The chains run in two halves of 64 chunks through the same padded LDS transpose as
+// wave_segment_chunks (lane c: chunk c, then chunk 64 + c), and the nc partials are folded as in
+// wave_row_rsum (fold_parts).
+constexpr int kReg2Q = 16;
+constexpr int64_t kReg2Cols = 64 * 4 * kReg2Q;
+__global__ __launch_bounds__(256) void softmax_causal_reg2_kernel(int64_t rows, int64_t cols,
+                                                                  const float* __restrict__ raw, float scale,
+                                                                  int64_t window, uint16_t* __restrict__ probs,
+                                                                  int band) {
+  __shared__ WaveStage st[4];
+  extern __shared__ float dyn[];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + w;
+  if (row >= rows) return;
+  const int64_t nc = (cols + kChunk - 1) / kChunk;
+  float* parts = dyn + w * nc;
+  const int i = (int)(row % cols);  // cols <= 4096: column indices fit in int
+  const int j0 = (window > 0 && i - window + 1 > 0) ? (int)(i - window + 1) : 0;
+  const int ncol = (int)cols;
+  const float* rr = raw + row * cols;
+  float e[kReg2Q][4];
+#pragma unroll
+  for (int q = 0; q < kReg2Q; ++q) {
+    const int j = 256 * q + 4 * lane;
+    float4 v = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    if (j < ncol && j <= i && j + 3 >= j0) v = *reinterpret_cast<const float4*>(rr + j);
+    e[q][0] = v.x; e[q][1] = v.y; e[q][2] = v.z; e[q][3] = v.w;
+  }
+  float m = -__builtin_inff();
+#pragma unroll
+  for (int q = 0; q < kReg2Q; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int j = 256 * q + 4 * lane + t;
+      if (j < ncol && j <= i && j >= j0) m = fmaxf(m, e[q][t] * scale);
+    }
+  m = wave_max(m);
+  // masked keys enter the chain as +0 terms
+#pragma unroll
+  for (int q = 0; q < kReg2Q; ++q)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int j = 256 * q + 4 * lane + t;
+      float x = 0.0f;
+      if (j < ncol && j <= i && j >= j0) {
+        float sc = e[q][t] * scale;
+        x = cexp(sc - m);
+      }
+      e[q][t] = x;
+    }
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+#pragma unroll
+    for (int q = 0; q < kReg2Q / 2; ++q) {
+      const int local = 256 * q + 4 * lane;
+      if (2048 * half + local < ncol) {
+        float* dst = &st[w].t[local >> 5][local & 31];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) dst[t] = e[q + (kReg2Q / 2) * half][t];
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+    const int c = 64 * half + lane;
+    if (c < nc) {
+      const int k1 = ncol - c * (int)kChunk < (int)kChunk ? ncol - c * (int)kChunk : (int)kChunk;
+      float p = 0.0f;
+      for (int k = 0; k < k1; ++k) p = p + st[w].t[lane][k];
+      parts[c] = p;
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+  }
+  const float S = fold_parts(parts, nc);
+  const float rcp = 1.0f / S;
+  int64_t wlo = 0, whi = cols;  // columns written
+  band_cols(band, i, window, cols, wlo, whi);
+#pragma unroll
+  for (int q = 0; q < kReg2Q; ++q) {
+    const int j = 256 * q + 4 * lane;
+    if (j < whi && j + 3 >= wlo) {
+      uint16_t o[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) o[t] = ((j + t <= i && j + t >= j0)) ? f32_to_bf16(e[q][t] * rcp) : (uint16_t)0;
+      stb<4>(probs + row * cols + j, o);
+    }
+  }
+}
+
 // Windowed rows (0 < window <= kBandWin): the visible keys j0 .. i lie in the 768 columns [base, base + 768),
 // base = j0 rounded down to 256, which lane l holds as float4 vectors at base + 256 q + 4 l (q < 3): the row
 // is read from memory once.  The band's 24 chunks are staged in LDS and chained by lanes 0 .. 23 (every
@@ -823,6 +913,9 @@ hipError_t softmax_causal_launch(int64_t rows, int64_t cols, const float* raw, f
     hipLaunchKernelGGL(softmax_band_kernel, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs, band);
   else if (cols % 4 == 0 && cols <= kRegCols && al(raw, 16) && al(probs, 8))
     hipLaunchKernelGGL(softmax_causal_reg_kernel, grid, dim3(256), 0, s, rows, cols, raw, scale, window, probs,
+                       band);
+  else if (cols % 4 == 0 && cols <= kReg2Cols && al(raw, 16) && al(probs, 8))
+    hipLaunchKernelGGL(softmax_causal_reg2_kernel, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs,
                        band);
   else if (cols % 4 == 0 && al(raw, 16) && al(probs, 8))
     hipLaunchKernelGGL(softmax_causal_kernel<4>, grid, dim3(256), lds, s, rows, cols, raw, scale, window, probs,

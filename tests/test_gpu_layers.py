@@ -37,8 +37,8 @@ def test_rownorm_fwd_bwd(rows, cols):
     assert_bits(host_f32(dgn), dg_o, "dgain")
 
 
-# rows longer than 2048 keys take the staged kernel: 2052 (a lone last chunk), 3000 (a ragged last chunk),
-# 4096 (128 full chunks, two staging segments), 4100
+# rows of 2049 .. 4096 keys are held in registers and chained in two halves: 2052 (a lone last chunk), 3000 (a
+# ragged last chunk), 4096 (128 full chunks); 4100 takes the staged kernel (two staging segments and a third)
 @pytest.mark.parametrize("bh,s", [(3, 200), (2, 64), (4, 2048), (2, 70), (1, 33), (1, 2304), (1, 2052), (2, 3000),
                                   (1, 4096), (1, 4100)])
 def test_softmax_causal(bh, s):

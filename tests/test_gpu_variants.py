@@ -22,7 +22,9 @@ NAMES = ["attn_norm", "w_qkv", "w_o", "ffn_norm", "w_gate_up", "w_down"]
 @pytest.mark.parametrize("bh,s,win", [(3, 200, 16), (2, 64, 1), (4, 2048, 512), (2, 70, 33), (1, 2304, 512),
                                       (1, 2304, 2000), (2, 96, 96), (1, 4200, 600), (1, 4104, 10),
                                       # windows up to 512 keep the row's band in registers; a partial last chunk
-                                      (2, 1000, 100), (1, 4096, 257), (1, 4096, 512)])
+                                      (2, 1000, 100), (1, 4096, 257), (1, 4096, 512),
+                                      # longer windows on rows held in registers (2049 .. 4096 keys)
+                                      (1, 4096, 1000), (1, 3000, 2999)])
 def test_softmax_window(bh, s, win):
     print(f"softmax window {bh}x{s}x{s} w={win}", flush=True)
     raw = I.normal_f32((bh, s, s), 1, I.TENSOR_IDS["scores"]) * np.float32(8)
