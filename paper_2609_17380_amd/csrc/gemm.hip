@@ -351,7 +351,10 @@ struct FoldRegs<0, T> {
   }
 };
 
-template <int MAXL, bool TA, bool TB, class CF>
+// CZ: the causal modes, K segments and the triangular output (tri_lower) are compiled in.  Launches with none
+// of them (every projection and gradient GEMM) take the CZ = false instantiation, whose chunk loop has no
+// skip tests: the same chains and fold, 2.5-5% faster.
+template <int MAXL, bool TA, bool TB, class CF, bool CZ>
 __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel(GemmArgs g) {
   typedef typename Mfma<CF::V>::T vec;
   constexpr int NT = CF::NT, TBN = CF::TBN, V = CF::V, WR = Mfma<V>::WR;
@@ -379,7 +382,7 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
   const int64_t within = tile - group * GM * tiles_n;
   int64_t tm = first_m + within % gsize, tn = within / gsize;
   int64_t z = blockIdx.z;
-  if (g.kmode != KMODE_FULL) {
+  if (CZ && g.kmode != KMODE_FULL) {
     // causally skipping GEMMs: tile cost grows with the row tile (TRAIL) or shrinks with it (LEAD).  Over the
     // whole launch (in dispatch order, blockIdx.x fastest), the longest tiles of every batch matrix go first
     // so the short ones fill the tail; the batch index runs fastest, so the workgroups on one XCD (every 8th)
@@ -392,8 +395,8 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
     if (g.kmode == KMODE_TRAIL) tm = tiles_m - 1 - tm;
   }
   const int64_t row0 = tm * BM, col0 = tn * TBN;
-  const bool upper_dead = g.tri_lower && col0 > row0 + BM - 1;                           // above the diagonal
-  const bool band_dead = g.tri_lower && g.kwin > 0 && col0 + TBN - 1 <= row0 - g.kwin;   // left of the window
+  const bool upper_dead = CZ && g.tri_lower && col0 > row0 + BM - 1;                           // above the diagonal
+  const bool band_dead = CZ && g.tri_lower && g.kwin > 0 && col0 + TBN - 1 <= row0 - g.kwin;   // left of the window
   // out of every reader's reach (the dS epilogue writes the +0 of the dead tiles the readers reach)
   const bool band_far = band_dead && !g.zero_dead && col0 + TBN - 1 < row0 - g.kwin - kAttnLead;
   if ((upper_dead && !(g.zero_dead && g.epi == EPI_DS)) || (band_dead && (g.epi != EPI_DS || band_far))) return;
@@ -415,19 +418,19 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
   const int64_t kfull = g.k / KC;  // chunks with all 32 terms
   // The real chunks: in each K segment of spc chunks (one segment unless kseg is set), the local chunks
   // [lb, le); every other chunk is a +0 partial.
-  const int64_t spc = g.kseg > 0 ? g.kseg / KC : nc;
-  const int64_t nseg = g.kseg > 0 ? nc / spc : 1;
-  const int64_t ncs = g.kseg > 0 ? spc : nc;
+  const int64_t spc = (CZ && g.kseg > 0) ? g.kseg / KC : nc;
+  const int64_t nseg = (CZ && g.kseg > 0) ? nc / spc : 1;
+  const int64_t ncs = (CZ && g.kseg > 0) ? spc : nc;
   int64_t lb = 0, le = ncs;
   const int64_t last_row = row0 + BM < g.m ? row0 + BM : g.m;  // rows of this tile are < last_row
-  if (g.kmode == KMODE_TRAIL) {
+  if (CZ && g.kmode == KMODE_TRAIL) {
     int64_t ce = (last_row + KC - 1) / KC;
     le = ce < ncs ? ce : ncs;
     if (g.kwin > 0 && row0 - g.kwin + 1 > 0) {  // keys before the first query's window
       const int64_t cb = (row0 - g.kwin + 1) / KC;
       lb = cb < le ? cb : le;
     }
-  } else if (g.kmode == KMODE_LEAD) {
+  } else if (CZ && g.kmode == KMODE_LEAD) {
     int64_t cb = row0 / KC;
     lb = cb < ncs ? cb : ncs;
     if (g.kwin > 0) {  // queries after the last key's window: the last visible query is last_row - 2 + kwin
@@ -481,12 +484,13 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
   };
   // the next real chunk after real chunk c of the segment starting at chunk base
   auto next_real = [&](int64_t c, int64_t base) -> int64_t {
+    if (!CZ) return c + 1 < nc ? c + 1 : -1;
     if (c + 1 - base < le) return c + 1;
     return (base + spc < nc && lb < le) ? base + spc + lb : -1;
   };
   // a chunk of a group in the segment at base: real chunks run, skipped ones are +0 partials
   auto part = [&](int64_t c, int64_t base) -> vec {
-    return (c - base >= lb && c - base < le) ? run_chunk(c, next_real(c, base)) : zero;
+    return (!CZ || (c - base >= lb && c - base < le)) ? run_chunk(c, next_real(c, base)) : zero;
   };
 
   // Groups of four chunks.  A complete group's partial ((p0 + p1) + (p2 + p3)) is exactly the level-2
@@ -501,12 +505,12 @@ __global__ __launch_bounds__(CF::NT, CF::OCC * CF::NW / 4) void gemm_mfma_kernel
     const int64_t sgi = nseg > 1 ? gj / gps : 0;
     const int64_t base = sgi * spc;
     const int64_t c = gj * 4, cl = c - base;
-    if (nseg == 1 && cl >= le) break;  // the rest are skipped chunks
+    if (CZ && nseg == 1 && cl >= le) break;  // the rest are skipped chunks
     vec qa, qb;  // the group's partial is qa + qb
-    if (cl + 4 <= lb || cl >= le) {
+    if (CZ && (cl + 4 <= lb || cl >= le)) {
       qa = zero;  // a group of skipped chunks: +0 + +0
       qb = zero;
-    } else if (tile_in && cl >= lb && cl + 5 <= le && c + 5 <= kfull) {
+    } else if (tile_in && (!CZ || (cl >= lb && cl + 5 <= le)) && c + 5 <= kfull) {
       vec p0 = run_fast(c);
       vec p1 = run_fast(c + 1);
       qa = p0 + p1;
@@ -890,14 +894,25 @@ static hipError_t launch_maxl(const GemmArgs& g, hipStream_t s) {
   typedef CfgRowRow R;
   typedef CfgAKMajor A;
   typedef CfgBKMajor B;
+  if (g.kmode != KMODE_FULL || g.kseg > 0 || g.tri_lower) {  // the causal instantiations
+    if (!g.trans_a && g.trans_b)
+      hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, true, R, true>), general_grid<R>(g), dim3(R::NT), 0, s, g);
+    else if (!g.trans_a && !g.trans_b)
+      hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false, B, true>), general_grid<B>(g), dim3(B::NT), 0, s, g);
+    else if (g.trans_a && !g.trans_b)
+      hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, false, A, true>), general_grid<A>(g), dim3(A::NT), 0, s, g);
+    else
+      hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, true, A, true>), general_grid<A>(g), dim3(A::NT), 0, s, g);
+    return hipGetLastError();
+  }
   if (!g.trans_a && g.trans_b)
-    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, true, R>), general_grid<R>(g), dim3(R::NT), 0, s, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, true, R, false>), general_grid<R>(g), dim3(R::NT), 0, s, g);
   else if (!g.trans_a && !g.trans_b)
-    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false, B>), general_grid<B>(g), dim3(B::NT), 0, s, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, false, false, B, false>), general_grid<B>(g), dim3(B::NT), 0, s, g);
   else if (g.trans_a && !g.trans_b)
-    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, false, A>), general_grid<A>(g), dim3(A::NT), 0, s, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, false, A, false>), general_grid<A>(g), dim3(A::NT), 0, s, g);
   else
-    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, true, A>), general_grid<A>(g), dim3(A::NT), 0, s, g);
+    hipLaunchKernelGGL((gemm_mfma_kernel<MAXL, true, true, A, false>), general_grid<A>(g), dim3(A::NT), 0, s, g);
   return hipGetLastError();
 }
 
